@@ -1,0 +1,192 @@
+"""FAVOR attention in fp64, step by step as the paper states it.
+
+Test infrastructure only (see ``oracle/__init__``).
+
+Shapes: Q, K, V are [..., L, d] (leading axes are batch and head); W is
+[H, M, d] and b is [H, M], one draw per head shared across the batch. When the
+inputs carry a head axis (axis -3) W and b broadcast over it.
+
+Readings of points the paper leaves open (each is restated in the design doc):
+  * Gaussian-kernel features use omega ~ N(0, I_d) acting on the scaled input
+    x~ = s x (s = input_scale; s = d^-1/4 gives the paper's exp(QK^T / sqrt d)).
+    With s = d^-1/4 this is the same as omega ~ N(0, sigma^-2 I) on raw x with
+    sigma = d^1/4; the printed "N(0, sigma^2 I)" contradicts Bochner's theorem
+    and the paper's own Theorem 1, which uses N(0, I_d) on d^-1/4-scaled inputs.
+  * "ortho_scaling = 0.0" (App. B) is read as chi_d-distributed row norms, which
+    keeps each row's Gaussian marginal (Sec. 2.4) and so stays unbiased.
+  * The stabiliser is added to the denominator D-hat; 0 reproduces Algorithm 1.
+  * Algorithm 1's "Result in R^{L x L}" is read as R^{L x d}; the prefix-sum
+    row is (G^PS_i)^T Q'_i in R^{d+1}; the cumsum index runs over j.
+"""
+import numpy as np
+
+from . import philox
+
+RF_ORTHO_CHI = 0     # R-ORF blocks, rows scaled by independent chi_d norms
+RF_ORTHO_FIXED = 1   # R-ORF blocks, rows scaled to sqrt(d)
+RF_IID = 2           # unstructured Gaussian rows
+
+
+def gram_schmidt_rows(G):
+    """Orthonormalise the rows of a square matrix in order (Sec. 2.4, R-ORFs).
+
+    Modified Gram-Schmidt in fp64: row i loses its components along rows
+    0..i-1 already orthonormalised, then is normalised. The result is the
+    unique orthogonal factor whose triangular factor has a positive diagonal.
+    """
+    G = np.array(G, dtype=np.float64)
+    n = G.shape[0]
+    Qr = np.zeros_like(G)
+    for i in range(n):
+        r = G[i].copy()
+        for j in range(i):
+            r -= np.dot(Qr[j], r) * Qr[j]
+        Qr[i] = r / np.linalg.norm(r)
+    return Qr
+
+
+def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI):
+    """Random-feature matrix W [H, M, d] and phases b [H, M] (Secs. 2.3-2.4).
+
+    For each head and each d x d block k < ceil(M/d): a Gaussian block (Philox
+    stream, purpose ORF, row-major element index (k d + r) d + c) has its rows
+    orthonormalised by Gram-Schmidt; row m = k d + r is then scaled by rho_m,
+    the norm of an independent N(0, I_d) vector (purpose CHI, elements
+    m d .. m d + d - 1). The blocks are stacked and the first M rows kept.
+    b_m = 2 pi u_m with u_m uniform (purpose PHASE, element m).
+    FIXED kind uses rho = sqrt(d); IID kind keeps the raw Gaussian rows.
+    """
+    nblk = -(-M // d)
+    W = np.zeros((n_heads, M, d), dtype=np.float64)
+    b = np.zeros((n_heads, M), dtype=np.float64)
+    for h in range(n_heads):
+        g = philox.gaussians(seed, h, philox.PURPOSE_ORF, nblk * d * d).reshape(nblk, d, d)
+        rows = []
+        for k in range(nblk):
+            if kind == RF_IID:
+                rows.append(g[k])
+            else:
+                rows.append(gram_schmidt_rows(g[k]))
+        Wh = np.concatenate(rows, axis=0)[:M]
+        if kind == RF_ORTHO_CHI:
+            chi = philox.gaussians(seed, h, philox.PURPOSE_CHI, M * d).reshape(M, d)
+            rho = np.sqrt(np.sum(chi * chi, axis=1))
+            Wh = Wh * rho[:, None]
+        elif kind == RF_ORTHO_FIXED:
+            Wh = Wh * np.sqrt(d)
+        W[h] = Wh
+        b[h] = 2.0 * np.pi * philox.uniforms(seed, h, philox.PURPOSE_PHASE, M)
+    return W, b
+
+
+def _per_head(W, b, X):
+    """Broadcast W [H,M,d], b [H,M] against X [..., H, L, d]."""
+    W = np.asarray(W, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    if X.ndim >= 3:
+        return W, b[..., None, :]          # W [H,M,d], b [H,1,M]
+    return W[0], b[0][None, :]             # single head, X [L, d]
+
+
+def feature_map(X, W, b, input_scale):
+    """X' = D_X X-hat (Sec. 2.3, Eqs. dqdk and qkprime), X [..., L, d] -> [..., L, M].
+
+    x~ = s x; X-hat = sqrt(2/M) cos(W x~ + b) (Gaussian-kernel features, c = sqrt 2,
+    f = cos); D_X = diag(exp(||x~||^2 / 2)), which is the paper's exp(||x||^2 / r)
+    with r = 2 sqrt(d) when s = d^-1/4.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    W, bb = _per_head(W, b, X)
+    M = W.shape[-2]
+    Xs = input_scale * X
+    proj = np.matmul(Xs, np.swapaxes(W, -1, -2))                # [..., L, M]
+    Xhat = np.sqrt(2.0 / M) * np.cos(proj + bb)
+    D = np.exp(0.5 * np.sum(Xs * Xs, axis=-1))                  # [..., L]
+    return D[..., None] * Xhat
+
+
+def _with_ones(V):
+    """C = [V 1_L] (Algorithm 1)."""
+    V = np.asarray(V, dtype=np.float64)
+    ones = np.ones(V.shape[:-1] + (1,), dtype=np.float64)
+    return np.concatenate([V, ones], axis=-1)
+
+
+def attn_bidir_features(Qp, Kp, V, denom_eps=0.0):
+    """Algorithm 1, bidirectional branch, given Q' and K'.
+
+    Buf1 = K'^T C, Buf2 = Q' Buf1, [Buf3 buf4] = Buf2, return diag(buf4)^-1 Buf3.
+    """
+    C = _with_ones(V)
+    d = C.shape[-1] - 1
+    Buf1 = np.matmul(np.swapaxes(Kp, -1, -2), C)                # [..., M, d+1]
+    Buf2 = np.matmul(Qp, Buf1)                                  # [..., L, d+1]
+    Buf3, buf4 = Buf2[..., :d], Buf2[..., d]
+    return Buf3 / (buf4 + denom_eps)[..., None]
+
+
+def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0):
+    """Bidirectional FAVOR (Sec. 2.5, Algorithm 1)."""
+    Qp = feature_map(Q, W, b, input_scale)
+    Kp = feature_map(K, W, b, input_scale)
+    return attn_bidir_features(Qp, Kp, V, denom_eps)
+
+
+def attn_causal_features(Qp, Kp, V, denom_eps=0.0, state_in=None):
+    """Unidirectional FAVOR by sequential prefix aggregation (Sec. 2.5.1, Eq. cumsum;
+    the O(Md + Ld + ML)-space variant of Sec. 2.6).
+
+    For i = 1..L: G^PS_i = G^PS_{i-1} + K'_i C_i^T, Buf2_i = (G^PS_i)^T Q'_i;
+    then normalise as in Algorithm 1. Vectorised over the leading axes only.
+    Returns (out [..., L, d], G^PS_L [..., M, d+1]); state_in, if given, is the
+    aggregate carried in from earlier tokens (G^PS_0).
+    """
+    C = _with_ones(V)
+    L = C.shape[-2]
+    d = C.shape[-1] - 1
+    M = Kp.shape[-1]
+    S = np.zeros(Kp.shape[:-2] + (M, d + 1), dtype=np.float64)
+    if state_in is not None:
+        S = S + np.asarray(state_in, dtype=np.float64)
+    Buf2 = np.zeros(C.shape, dtype=np.float64)
+    for i in range(L):
+        S += Kp[..., i, :, None] * C[..., i, None, :]
+        Buf2[..., i, :] = np.einsum("...m,...mp->...p", Qp[..., i, :], S)
+    Buf3, buf4 = Buf2[..., :d], Buf2[..., d]
+    return Buf3 / (buf4 + denom_eps)[..., None], S
+
+
+def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None):
+    """Unidirectional FAVOR (Algorithm 1, prefix-sum branch). Returns (out, state)."""
+    Qp = feature_map(Q, W, b, input_scale)
+    Kp = feature_map(K, W, b, input_scale)
+    return attn_causal_features(Qp, Kp, V, denom_eps, state_in)
+
+
+def attn_explicit(Q, K, V, W, b, input_scale, causal, denom_eps=0.0):
+    """The L x L estimator itself: A-hat = Q' K'^T (Eq. unbiased_attention_estimation),
+    masked by tril (diagonal included) when causal, then D-hat^-1 A-hat V with
+    D-hat = diag(A-hat 1_L). Only for small L."""
+    Qp = feature_map(Q, W, b, input_scale)
+    Kp = feature_map(K, W, b, input_scale)
+    Ahat = np.matmul(Qp, np.swapaxes(Kp, -1, -2))
+    if causal:
+        Ahat = np.tril(Ahat)
+    Dhat = np.sum(Ahat, axis=-1)
+    return np.matmul(Ahat, np.asarray(V, dtype=np.float64)) / (Dhat + denom_eps)[..., None]
+
+
+def softmax_attn(Q, K, V, input_scale, causal):
+    """Exact attention (Sec. 2.1, Eqs. attnorm and uattnorm) on x~ = s x:
+    A = exp(Q~ K~^T), tril(A) when causal (diagonal included), D^-1 A V.
+    Evaluated as a row-max-shifted softmax, which leaves D^-1 A unchanged."""
+    Qs = input_scale * np.asarray(Q, dtype=np.float64)
+    Ks = input_scale * np.asarray(K, dtype=np.float64)
+    logits = np.matmul(Qs, np.swapaxes(Ks, -1, -2))
+    if causal:
+        L = logits.shape[-1]
+        mask = np.tril(np.ones((L, L), dtype=bool))
+        logits = np.where(mask, logits, -np.inf)
+    logits = logits - np.max(logits, axis=-1, keepdims=True)
+    A = np.exp(logits)
+    return np.matmul(A, np.asarray(V, dtype=np.float64)) / np.sum(A, axis=-1)[..., None]
