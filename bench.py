@@ -1,0 +1,193 @@
+"""Benchmark of the FAVOR hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step is one pass of the whole path over the protein-shaped workload
+(B4 H8 L8192, d 64, M 256, bf16): draw the orthogonal random features for the
+8 heads (favor_orf_draw, a fresh seed per step), then bidirectional FAVOR and
+unidirectional FAVOR over the same Q, K, V. Inputs are synthetic and already
+resident in HBM; nothing is skipped inside the timed region.
+
+value = B*H*L / (seconds per step): token-heads per second through the whole
+step (each token-head goes through the draw, both directions). The JSON line
+also carries the per-kernel times measured with HIP events inside the timed
+region, a roofline entry for the dominant kernel and the fp64 CPU oracle timed
+on this host (cpu_baseline).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads as wl  # noqa: E402
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+# v_cos_f32 is a quarter-rate transcendental: 256 CUs x 4 SIMD x 16 lanes x
+# 2.4 GHz / 4 = 9.83e12 cosines per second.
+PEAK_COS_PER_S = 256 * 4 * 16 * 2.4e9 / 4
+
+
+def per_token_head(kernel, d, M, elt):
+    """Algorithmic (flops, bytes, cosines) per token-head of one launch of `kernel`.
+
+    flops: the feature projections (2 d M each side computed) and the
+    contractions of Algorithm 1 / Eq. cumsum (2 M (d+1) each); bytes: the
+    minimal HBM traffic of the kernel's inputs and outputs; cosines: M per
+    feature row computed."""
+    proj = 2 * d * M
+    contr = 2 * M * (d + 1)
+    row = d * elt
+    if kernel == "k_causal":      # Q and K features, Q S + intra, S update; reads Q K V, writes out
+        return 2 * proj + 2 * contr, 4 * row, 2 * M
+    if kernel == "k_qside":       # Q features, Q' Buf1; reads Q, writes out
+        return proj + contr, 2 * row, M
+    if kernel == "k_kside":       # K features, K'^T [V 1]; reads K, V
+        return proj + contr, 2 * row, M
+    return None
+
+
+def cpu_baseline(w, Q, K, V):
+    """The fp64 oracle on this host's cores over the whole workload (or a head
+    subset), timed like one GPU step: ORF draw + bidirectional + causal."""
+    from oracle import favor
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        cores = max((p["num_threads"] for p in blas), default=1)
+    except Exception:
+        cores = 1
+    heads = w.B * w.H
+    t0 = time.perf_counter()
+    Wr, br = favor.orf_draw(12345, w.H, w.M, w.d)
+    Qp = favor.feature_map(Q, Wr, br, w.input_scale)
+    Kp = favor.feature_map(K, Wr, br, w.input_scale)
+    favor.attn_bidir_features(Qp, Kp, V)
+    favor.attn_causal_features(Qp, Kp, V)
+    t = time.perf_counter() - t0
+    return {"value": heads * w.L / t, "unit": "token-heads/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"whole workload ({w.B}x{w.H} heads x L={w.L}): ORF draw + bidirectional "
+                      f"+ causal in fp64 NumPy, {t:.2f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FAVOR path "
+              "shards over heads with no communication, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2006_03555_amd as fv
+
+    w = wl.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    Q, K, V = wl.make_qkv(w)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    up = lambda x: torch.from_numpy(x).to(device=dev, dtype=tdt).contiguous()
+    Qd, Kd, Vd = up(Q), up(K), up(V)
+    s = w.input_scale
+    H, M = w.H, w.M
+    Wd = torch.empty((H, M, w.d), dtype=torch.float32, device=dev)
+    bd = torch.empty((H, M), dtype=torch.float32, device=dev)
+    out_b = torch.empty_like(Qd)
+    out_c = torch.empty_like(Qd)
+    g = fv.make_desc(w.B, H, w.L, w.d, M, fv.BF16 if w.dtype == "bf16" else fv.F32,
+                     fv.BF16 if w.dtype == "bf16" else fv.F32, s)
+    ws_b = torch.empty(fv.workspace_size(g, 0), dtype=torch.uint8, device=dev)
+    ws_c = torch.empty(fv.workspace_size(g, 1), dtype=torch.uint8, device=dev)
+    do_bidir = w.direction in ("bidir", "both")
+    do_causal = w.direction in ("causal", "both")
+
+    def step(i):
+        fv.orf_draw(1000 + i, H, M, w.d, W=Wd, b=bd)
+        if do_bidir:
+            fv.attn_bidir(Qd, Kd, Vd, Wd, bd, s, out=out_b, workspace=ws_b)
+        if do_causal:
+            fv.attn_causal(Qd, Kd, Vd, Wd, bd, s, out=out_c, workspace=ws_c)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    fv.timing_reset()
+    fv.timing_enable(True)
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    fv.timing_enable(False)
+    ms_step = e0.elapsed_time(e1) / args.steps
+    kt = fv.timing_read()
+    kernels = {k: {"ms_per_launch": v[0] / v[1], "launches_per_step": v[1] / args.steps}
+               for k, v in kt.items() if v[1] > 0}
+
+    token_heads = w.B * w.H * w.L
+    value = token_heads / (ms_step / 1e3)
+
+    # roofline of the kernel with the largest share of the step
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_launch"] * kernels[k]["launches_per_step"])
+    roof = None
+    elt = 2 if w.dtype == "bf16" else 4
+    costs = per_token_head(dom, w.d, M, elt)
+    if costs is not None:
+        fl, by, cs = costs
+        t = kernels[dom]["ms_per_launch"] / 1e3
+        cand = {
+            "mfma": (fl * token_heads / t / 1e12, PEAK_MFMA_TFLOPS[w.dtype], "TFLOP/s"),
+            "hbm": (by * token_heads / t / 1e9, PEAK_HBM_GBS, "GB/s"),
+            "alu": (cs * token_heads / t / 1e12, PEAK_COS_PER_S / 1e12, "Tcos/s"),
+        }
+        bound = max(cand, key=lambda k: cand[k][0] / cand[k][1])
+        a, p, u = cand[bound]
+        roof = {"kernel": dom, "bound": bound, "achieved": a, "peak": p, "unit": u,
+                "frac": a / p, "traffic": None,
+                "others": {k: {"achieved": v[0], "peak": v[1], "unit": v[2],
+                               "frac": v[0] / v[1]} for k, v in cand.items() if k != bound}}
+
+    res = {
+        "metric": "FAVOR attention tokens/sec (B*H*L/s) + % of MFMA/HBM peak at L=8192, M=256",
+        "value": value,
+        "unit": "token-heads/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": M,
+                   "direction": w.direction, "orf_draw_per_step": True,
+                   "parallelism": "single GPU"},
+        "kernels": kernels,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, Q, K, V)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,175 @@
+/*
+ * favor.h - C ABI of libfavor, FAVOR attention (Fast Attention Via Orthogonal
+ * Random features, arXiv 2006.03555) for AMD MI355X (gfx950).
+ *
+ * Every tensor argument is a DEVICE pointer owned by the caller; the library
+ * never allocates, frees or retains device memory (scratch is the caller's
+ * workspace). Every call is asynchronous: work is enqueued on `stream` (a
+ * hipStream_t passed as void*, NULL = the default stream) and nothing waits.
+ *
+ * Errors: arguments are validated completely before anything is launched. On
+ * failure a call returns a non-zero favor_status, writes no output and records
+ * a message retrievable with favor_last_error() (per thread). A failed launch
+ * returns FAVOR_ERR_DEVICE. Numerical outcomes are not errors: a denominator
+ * D-hat that is zero gives IEEE Inf/NaN rows exactly as the formulas do.
+ *
+ * Layouts (row-major, contiguous, 16-byte aligned):
+ *   Q, K, V, out   [B][H][L][d]      in_dtype (out: out_dtype)
+ *   W              [H][M][d]  float  rows omega_m of the random-feature matrix
+ *   b              [H][M]     float  phases b_m
+ *   X' (features)  [B][H][L][M]      out_dtype
+ *   state          [B][H][M][d+1] float, column d holds sum_j K'_j (the "1" column)
+ * One draw (W, b) per head is shared by every batch entry.
+ *
+ * Supported: d = 64; M in {64, 128, 256}; L >= 0 (any length, ragged tails
+ * handled; L = 0 is a no-op); B, H >= 0; in_dtype F32 or BF16; out_dtype F32
+ * or BF16. F32 inputs use fp32 matrix cores and an accurate cosine; BF16
+ * inputs use bf16 matrix cores with fp32 accumulation, the hardware cosine
+ * and bf16 features.
+ */
+#ifndef FAVOR_H
+#define FAVOR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define FAVOR_API __attribute__((visibility("default")))
+#else
+#define FAVOR_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FAVOR_OK = 0,
+  FAVOR_ERR_INVALID_ARGUMENT = 1,  /* null/misaligned pointer, negative size, bad enum */
+  FAVOR_ERR_UNSUPPORTED = 2,       /* valid but not implemented (d, M, dtype combo)    */
+  FAVOR_ERR_WORKSPACE_TOO_SMALL = 3,
+  FAVOR_ERR_DEVICE = 4             /* a HIP launch or runtime call failed               */
+} favor_status;
+
+typedef enum { FAVOR_F32 = 0, FAVOR_BF16 = 1 } favor_dtype;
+
+typedef enum {
+  FAVOR_RF_ORTHO_CHI = 0,   /* R-ORF blocks, rows scaled by independent chi_d norms (default) */
+  FAVOR_RF_ORTHO_FIXED = 1, /* R-ORF blocks, every row scaled to norm sqrt(d)                  */
+  FAVOR_RF_IID = 2          /* unstructured i.i.d. N(0, I_d) rows                              */
+} favor_rf_kind;
+
+typedef struct {
+  int32_t B, H, L, d, M;
+  favor_dtype in_dtype;     /* Q, K, V (and X for the feature map) */
+  favor_dtype out_dtype;    /* out, X'                             */
+  float input_scale;        /* x~ = input_scale * x. d^-1/4 evaluates the paper's
+                               exp(Q K^T / sqrt d) (Sec. 2.1) on the given Q, K.  */
+  float denom_eps;          /* added to D-hat before dividing; 0 = Algorithm 1      */
+  int32_t chunk;            /* causal: tokens per segment handled by one workgroup
+                               (multiple of 64); 0 = library default                */
+} favor_desc;
+
+/*
+ * favor_orf_draw - draw the random-feature matrix W [n_heads][M][d] and phases
+ * b [n_heads][M] (Sec. 2.3 for the Gaussian-kernel features, Sec. 2.4 for the
+ * orthogonal R-ORF construction).
+ *
+ * For each head h and block k < ceil(M/d): a d x d matrix of N(0,1) entries has
+ * its rows orthonormalised in order by Gram-Schmidt (the orthogonal factor
+ * with positive triangular diagonal); row m = k d + r is scaled by rho_m (kind
+ * CHI: the norm of an independent N(0, I_d) vector; FIXED: sqrt(d)); the first
+ * M stacked rows are kept. IID kind keeps the raw Gaussian rows. b_m = 2 pi u_m.
+ *
+ * Random numbers: Philox4x64-10 (Salmon et al., SC'11), key (seed, 0), counter
+ * (i, h, purpose, 0) with purpose 0 = Gaussian blocks, 1 = chi-norm Gaussians,
+ * 2 = phases. Call i yields four 64-bit words w0..w3, i.e. eight 32-bit words
+ * x[2j] = low(wj), x[2j+1] = high(wj); stream element n is word n % 8 of call
+ * n / 8; u = (x + 0.5) 2^-32; Gaussians by Box-Muller from uniform pairs
+ * (u[2p], u[2p+1]): sqrt(-2 ln u[2p]) * (cos, sin)(2 pi u[2p+1]). Gaussian
+ * element of block k, row r, column c: n = (k d + r) d + c; chi vector of row
+ * m: n = m d + c; phase of row m: n = m. Arithmetic is fp32.
+ *
+ * Requires n_heads >= 0, d = 64, 1 <= M <= 4096. W, b: device, fp32.
+ */
+FAVOR_API favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d,
+                            favor_rf_kind kind, float *W, float *b, void *stream);
+
+/*
+ * favor_feature_map - X' = D_X X-hat, the paper's Q' = D_Q Q-hat (Sec. 2.3,
+ * Eqs. dqdk and qkprime) with Gaussian-kernel features (c = sqrt 2, f = cos):
+ *   X'[l][m] = exp(||x~_l||^2 / 2) * sqrt(2/M) * cos(omega_m . x~_l + b_m),
+ *   x~_l = input_scale * X[l].
+ * X [B][H][L][d] in g->in_dtype -> Xprime [B][H][L][M] in g->out_dtype.
+ * g->denom_eps and g->chunk are ignored.
+ */
+FAVOR_API favor_status favor_feature_map(const favor_desc *g, const void *X, const float *W,
+                               const float *b, void *Xprime, void *stream);
+
+/*
+ * favor_workspace_size - bytes of device workspace favor_attn_bidir (causal = 0)
+ * or favor_attn_causal (causal != 0) needs for descriptor g; 0 if g is invalid.
+ * The workspace must be 256-byte aligned; its contents on entry do not matter.
+ */
+FAVOR_API size_t favor_workspace_size(const favor_desc *g, int causal);
+
+/*
+ * favor_attn_bidir - bidirectional FAVOR (Sec. 2.5, Algorithm 1):
+ *   C = [V 1_L], Buf1 = K'^T C (M x (d+1)), Buf2 = Q' Buf1,
+ *   out = diag(buf4 + denom_eps)^-1 Buf3 with [Buf3 buf4] = Buf2,
+ * where Q', K' are the feature maps of favor_feature_map. The L x L matrix
+ * Q' K'^T and the L x M features are never stored. Deterministic (no atomics).
+ */
+FAVOR_API favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
+                              const void *V, const float *W, const float *b, void *out,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * favor_attn_causal - unidirectional FAVOR by prefix sums (Sec. 2.5.1, Eq.
+ * cumsum): row i of the result is (G^PS_i)^T Q'_i normalised as in Algorithm 1,
+ * G^PS_i = S_0 + sum_{j <= i} K'_j C_j^T (keys up to and including i). The
+ * prefix tensor is never stored: workgroups scan chunks of tokens carrying an
+ * M x (d+1) fp32 state.
+ * state_in  (nullable) [B][H][M][d+1] fp32: S_0, the aggregate of earlier tokens.
+ * state_out (nullable) [B][H][M][d+1] fp32: receives S_0 + sum over all L tokens,
+ * so a long sequence can be processed in pieces. Deterministic (no atomics).
+ */
+FAVOR_API favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K,
+                               const void *V, const float *W, const float *b, void *out,
+                               const float *state_in, float *state_out,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/* Host-only validation of a descriptor for an operation (0 feature map,
+ * 1 bidirectional, 2 causal); launches nothing and touches no device. */
+FAVOR_API favor_status favor_validate_desc(const favor_desc *g, int op);
+
+FAVOR_API const char *favor_status_string(favor_status s);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+FAVOR_API const char *favor_last_error(void);
+
+/*
+ * Per-kernel timing for benchmarks. While enabled, every kernel the library
+ * launches is bracketed by two HIP events recorded on the launch stream (the
+ * events come from a pool; nothing is allocated on the device). Reading
+ * waits for the recorded events and returns, for kernel id k, the summed
+ * milliseconds and launch count since the last reset. Ids run from 0 to
+ * favor_timing_num_kernels() - 1; favor_timing_kernel_name(k) names them.
+ * Not thread-safe with respect to concurrent launches from several threads.
+ */
+FAVOR_API favor_status favor_timing_enable(int on);
+FAVOR_API favor_status favor_timing_reset(void);
+FAVOR_API int32_t favor_timing_num_kernels(void);
+FAVOR_API const char *favor_timing_kernel_name(int32_t k);
+FAVOR_API favor_status favor_timing_read(int32_t k, double *ms, int64_t *count);
+
+/* ABI version of this header; bumped on any incompatible change. */
+FAVOR_API int32_t favor_abi_version(void);
+
+#define FAVOR_ABI_VERSION 1
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FAVOR_H */

@@ -1,0 +1,146 @@
+"""FAVOR attention (arXiv 2006.03555) on AMD MI355X: Python binding of libfavor.
+
+Every function here only marshals arguments for the C ABI declared in
+``include/favor.h`` (device pointers, sizes, the current HIP stream); all
+arithmetic runs in the library's HIP kernels. PyTorch provides device memory
+and streams. If ``libfavor.so`` has not been built the calls raise
+``FavorLibraryMissing``; there is no fallback.
+
+Tensors: Q, K, V [B, H, L, d] (bfloat16 or float32, contiguous, on the GPU);
+W [H, M, d] float32 and b [H, M] float32 from ``orf_draw``.
+"""
+import ctypes
+import os
+
+from ._lib import (  # noqa: F401
+    BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, OP_BIDIR, OP_CAUSAL, OP_FEATURE_MAP,
+    FavorDesc, FavorError, FavorLibraryMissing, lib, lib_path, make_desc, status_string,
+    validate_desc, workspace_size, last_error, timing_enable, timing_reset, timing_read,
+)
+
+__all__ = [
+    "orf_draw", "feature_map", "attn_bidir", "attn_causal", "workspace_size", "make_desc",
+    "validate_desc", "FavorError", "FavorLibraryMissing", "lib", "lib_path",
+]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t == torch.bfloat16:
+        return BF16
+    if t == torch.float32:
+        return F32
+    raise FavorError(1, f"unsupported tensor dtype {t}; use bfloat16 or float32")
+
+
+def _torch_dtype(code):
+    torch = _torch()
+    return torch.bfloat16 if code == BF16 else torch.float32
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _check(status):
+    if status != 0:
+        raise FavorError(status, last_error())
+
+
+def _require_cuda(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise FavorError(1, "tensors must be contiguous GPU tensors")
+
+
+def orf_draw(seed, n_heads, M, d=64, kind=RF_ORTHO_CHI, W=None, b=None, stream=None):
+    """Draw W [n_heads, M, d] and b [n_heads, M] on the GPU (favor_orf_draw)."""
+    torch = _torch()
+    dev = torch.device("cuda", torch.cuda.current_device())
+    if W is None:
+        W = torch.empty((n_heads, M, d), dtype=torch.float32, device=dev)
+    if b is None:
+        b = torch.empty((n_heads, M), dtype=torch.float32, device=dev)
+    _require_cuda(W, b)
+    _check(lib().favor_orf_draw(ctypes.c_uint64(seed), n_heads, M, d, kind, _ptr(W), _ptr(b),
+                                _stream(stream)))
+    return W, b
+
+
+def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0):
+    B, H, L, d = X.shape
+    M = W.shape[1]
+    in_code = _dtype_code(X.dtype)
+    out_code = in_code if out_dtype is None else _dtype_code(out_dtype)
+    return make_desc(B, H, L, d, M, in_code, out_code, input_scale, denom_eps, chunk)
+
+
+def feature_map(X, W, b, input_scale, out_dtype=None, out=None, stream=None):
+    """X' = D_X X-hat [B, H, L, M] (favor_feature_map)."""
+    torch = _torch()
+    g = _desc_for(X, W, input_scale, out_dtype)
+    if out is None:
+        out = torch.empty((g.B, g.H, g.L, g.M), dtype=_torch_dtype(g.out_dtype), device=X.device)
+    _require_cuda(X, W, b, out)
+    _check(lib().favor_feature_map(ctypes.byref(g), _ptr(X), _ptr(W), _ptr(b), _ptr(out),
+                                   _stream(stream)))
+    return out
+
+
+def _workspace(g, causal, workspace):
+    torch = _torch()
+    n = workspace_size(g, causal)
+    if workspace is None:
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8,
+                                device=torch.device("cuda", torch.cuda.current_device()))
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=None,
+               workspace=None, stream=None):
+    """Bidirectional FAVOR, Algorithm 1 (favor_attn_bidir). Returns out [B, H, L, d]."""
+    torch = _torch()
+    g = _desc_for(Q, W, input_scale, out_dtype, denom_eps)
+    if out is None:
+        out = torch.empty(Q.shape, dtype=_torch_dtype(g.out_dtype), device=Q.device)
+    _require_cuda(Q, K, V, W, b, out)
+    ws, nbytes = _workspace(g, 0, workspace)
+    _check(lib().favor_attn_bidir(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
+                                  _ptr(out), _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
+    return out
+
+
+def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
+                chunk=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None):
+    """Unidirectional FAVOR by prefix sums (favor_attn_causal).
+
+    Returns out, or (out, state_out [B, H, M, d+1]) when return_state is true.
+    """
+    torch = _torch()
+    g = _desc_for(Q, W, input_scale, out_dtype, denom_eps, chunk)
+    if out is None:
+        out = torch.empty(Q.shape, dtype=_torch_dtype(g.out_dtype), device=Q.device)
+    if return_state and state_out is None:
+        state_out = torch.empty((g.B, g.H, g.M, g.d + 1), dtype=torch.float32, device=Q.device)
+    _require_cuda(Q, K, V, W, b, out, state_in, state_out)
+    ws, nbytes = _workspace(g, 1, workspace)
+    _check(lib().favor_attn_causal(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
+                                   _ptr(out), _ptr(state_in), _ptr(state_out), _ptr(ws),
+                                   ctypes.c_size_t(nbytes), _stream(stream)))
+    return (out, state_out) if return_state else out
+
+
+def library_loaded_from():
+    """Absolute path of the libfavor.so this process uses."""
+    return os.path.realpath(lib_path())

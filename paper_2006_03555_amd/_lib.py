@@ -1,0 +1,123 @@
+"""ctypes declarations of libfavor's C ABI (include/favor.h)."""
+import ctypes
+import os
+
+F32 = 0
+BF16 = 1
+RF_ORTHO_CHI = 0
+RF_ORTHO_FIXED = 1
+RF_IID = 2
+OP_FEATURE_MAP = 0
+OP_BIDIR = 1
+OP_CAUSAL = 2
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+
+class FavorLibraryMissing(ImportError):
+    pass
+
+
+class FavorError(RuntimeError):
+    def __init__(self, status, message):
+        self.status = status
+        super().__init__(f"{status_string(status) if _LIB else status}: {message}")
+
+
+class FavorDesc(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("L", ctypes.c_int32),
+        ("d", ctypes.c_int32), ("M", ctypes.c_int32),
+        ("in_dtype", ctypes.c_int), ("out_dtype", ctypes.c_int),
+        ("input_scale", ctypes.c_float), ("denom_eps", ctypes.c_float),
+        ("chunk", ctypes.c_int32),
+    ]
+
+
+def lib_path():
+    return os.environ.get("FAVOR_LIBRARY", os.path.join(_HERE, "libfavor.so"))
+
+
+def lib():
+    """Load libfavor.so once; raise FavorLibraryMissing if it has not been built."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = lib_path()
+    if not os.path.exists(path):
+        raise FavorLibraryMissing(
+            f"{path} not found: build it with `python -m paper_2006_03555_amd.build`")
+    L = ctypes.CDLL(path)
+    vp, i32, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+    dp = ctypes.POINTER(FavorDesc)
+    sig = {
+        "favor_orf_draw": (ctypes.c_int, [u64, i32, i32, i32, ctypes.c_int, vp, vp, vp]),
+        "favor_feature_map": (ctypes.c_int, [dp, vp, vp, vp, vp, vp]),
+        "favor_workspace_size": (sz, [dp, ctypes.c_int]),
+        "favor_attn_bidir": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_causal": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_validate_desc": (ctypes.c_int, [dp, ctypes.c_int]),
+        "favor_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "favor_last_error": (ctypes.c_char_p, []),
+        "favor_abi_version": (i32, []),
+        "favor_timing_enable": (ctypes.c_int, [ctypes.c_int]),
+        "favor_timing_reset": (ctypes.c_int, []),
+        "favor_timing_num_kernels": (i32, []),
+        "favor_timing_kernel_name": (ctypes.c_char_p, [i32]),
+        "favor_timing_read": (ctypes.c_int, [i32, ctypes.POINTER(ctypes.c_double),
+                                             ctypes.POINTER(ctypes.c_int64)]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    if L.favor_abi_version() != 1:
+        raise FavorLibraryMissing(f"{path}: ABI version {L.favor_abi_version()} != 1")
+    _LIB = L
+    return L
+
+
+def status_string(s):
+    return lib().favor_status_string(int(s)).decode()
+
+
+def last_error():
+    return lib().favor_last_error().decode()
+
+
+def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, chunk=0):
+    return FavorDesc(B, H, L, d, M, in_dtype, out_dtype, float(input_scale), float(denom_eps),
+                     chunk)
+
+
+def validate_desc(g, op):
+    return lib().favor_validate_desc(ctypes.byref(g), op)
+
+
+def workspace_size(g, causal):
+    return lib().favor_workspace_size(ctypes.byref(g), 1 if causal else 0)
+
+
+def timing_enable(on=True):
+    lib().favor_timing_enable(1 if on else 0)
+
+
+def timing_reset():
+    st = lib().favor_timing_reset()
+    if st != 0:
+        raise FavorError(st, "timing reset failed")
+
+
+def timing_read():
+    """{kernel name: (total ms, launches)} since the last reset (waits for the events)."""
+    L = lib()
+    out = {}
+    for k in range(L.favor_timing_num_kernels()):
+        ms = ctypes.c_double()
+        n = ctypes.c_int64()
+        st = L.favor_timing_read(k, ctypes.byref(ms), ctypes.byref(n))
+        if st != 0:
+            raise FavorError(st, "timing read failed")
+        out[L.favor_timing_kernel_name(k).decode()] = (ms.value, n.value)
+    return out

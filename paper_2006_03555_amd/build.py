@@ -1,0 +1,69 @@
+"""Build libfavor.so (HIP kernels for gfx950 + the C ABI) in place.
+
+    python -m paper_2006_03555_amd.build        # or: from ... import build; build.build()
+
+Every call recompiles all sources (objects go to ``_build/`` next to this file,
+the library to ``paper_2006_03555_amd/libfavor.so``). hipcc cross-compiles, so
+this runs on a machine without a GPU.
+"""
+import concurrent.futures
+import os
+import shutil
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+BUILD = os.path.join(HERE, "_build")
+LIB = os.path.join(HERE, "libfavor.so")
+ARCH = "gfx950"
+
+SOURCES = ["orf_draw.hip", "feature_map.hip", "bidir.hip", "causal.hip", "favor_api.cpp",
+           "timing.cpp"]
+
+# Packed fp32 arithmetic is disabled for all device code (no v_pk_*_f32).
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
+                "-Wno-unused-function", "-I", os.path.join(ROOT, "include")]
+
+
+def hipcc():
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    path = os.path.join(rocm, "bin", "hipcc")
+    return path if os.path.exists(path) else shutil.which("hipcc")
+
+
+def _compile(src):
+    out = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+    cmd = [hipcc(), f"--offload-arch={ARCH}", *COMMON_FLAGS, *DEVICE_FLAGS, "-x", "hip",
+           "-c", os.path.join(CSRC, src), "-o", out]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    noise = ("unknown target feature", "packed-fp32-ops", "warning generated")
+    msg = "\n".join(ln for ln in (r.stdout + r.stderr).splitlines()
+                    if ln.strip() and not any(n in ln for n in noise))
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {src}:\n{msg}")
+    return out, msg
+
+
+def build(verbose=False):
+    os.makedirs(BUILD, exist_ok=True)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(len(SOURCES), 8)) as ex:
+        results = list(ex.map(_compile, SOURCES))
+    for _, msg in results:
+        if msg and verbose:
+            print(msg, file=sys.stderr)
+    tmp = LIB + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp,
+           *[o for o, _ in results], "-Wl,-rpath," + os.path.join(
+               os.environ.get("ROCM_PATH", "/opt/rocm"), "lib")]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link of libfavor.so failed:\n" + r.stdout + r.stderr)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,304 @@
+// favor_api.cpp - the C ABI of libfavor: argument validation, workspace
+// sizing, launch planning and dispatch to the kernels. Validation is plain
+// host code that touches no device, so a bad call never launches anything.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/favor.h"
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+favor_status fail(favor_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+favor_status ok() {
+  g_last_error.clear();
+  return FAVOR_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
+constexpr int kMinRowsPerSplit = 256;
+
+enum Op { kOpFeatureMap = 0, kOpBidir = 1, kOpCausal = 2 };
+
+favor_status validate(const favor_desc *g, int op) {
+  if (!g) return fail(FAVOR_ERR_INVALID_ARGUMENT, "descriptor is NULL");
+  if (op < kOpFeatureMap || op > kOpCausal)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown operation %d", op);
+  if (g->B < 0 || g->H < 0 || g->L < 0)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "negative size B=%d H=%d L=%d", g->B, g->H, g->L);
+  if (g->d <= 0 || g->M <= 0)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "d=%d and M=%d must be positive", g->d, g->M);
+  if (g->in_dtype != FAVOR_F32 && g->in_dtype != FAVOR_BF16)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown in_dtype %d", (int)g->in_dtype);
+  if (g->out_dtype != FAVOR_F32 && g->out_dtype != FAVOR_BF16)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown out_dtype %d", (int)g->out_dtype);
+  if (!std::isfinite(g->input_scale))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "input_scale must be finite");
+  if (!std::isfinite(g->denom_eps) || g->denom_eps < 0.f)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "denom_eps must be finite and >= 0");
+  if (g->chunk < 0 || g->chunk % 64 != 0)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "chunk=%d must be a non-negative multiple of 64",
+                g->chunk);
+  if (g->d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", g->d);
+  if (g->M != 64 && g->M != 128 && g->M != 256)
+    return fail(FAVOR_ERR_UNSUPPORTED, "M=%d not supported (64, 128, 256)", g->M);
+  const long long bh = (long long)g->B * g->H;
+  if (bh > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "B*H=%lld exceeds 65535", bh);
+  if (op == kOpCausal && g->in_dtype == FAVOR_F32 && g->M > 128)
+    return fail(FAVOR_ERR_UNSUPPORTED, "causal with fp32 inputs supports M <= 128");
+  return FAVOR_OK;
+}
+
+struct Plan {
+  int BH = 0;
+  int nsplit = 0;         // bidir: K-side splits; causal: segments
+  int rows_per_split = 0;
+  size_t part_bytes = 0;
+  size_t frag_bytes = 0;  // bidir only
+  size_t total = 0;
+};
+
+Plan make_plan(const favor_desc *g, bool causal) {
+  Plan p;
+  p.BH = g->B * g->H;
+  if (p.BH == 0 || g->L == 0) return p;
+  const int tiles = (g->L + 63) / 64;
+  int rows;
+  if (causal && g->chunk > 0) {
+    rows = g->chunk;
+  } else {
+    int want = (kTargetWorkgroups + p.BH - 1) / p.BH;
+    int max_split = tiles / (kMinRowsPerSplit / 64);
+    if (max_split < 1) max_split = 1;
+    if (want > max_split) want = max_split;
+    if (want < 1) want = 1;
+    rows = 64 * ((tiles + want - 1) / want);
+  }
+  p.rows_per_split = rows;
+  p.nsplit = (g->L + rows - 1) / rows;
+  p.part_bytes = round_up((size_t)p.BH * p.nsplit * g->M * 65 * sizeof(float), 256);
+  if (!causal) {
+    const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
+    p.frag_bytes = round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
+  }
+  p.total = p.part_bytes + p.frag_bytes;
+  return p;
+}
+
+favor::Shape shape_of(const favor_desc *g) {
+  favor::Shape sh;
+  sh.BH = g->B * g->H;
+  sh.H = g->H;
+  sh.L = g->L;
+  sh.M = g->M;
+  sh.s = g->input_scale;
+  sh.eps = g->denom_eps;
+  return sh;
+}
+
+favor::Dt dt_of(favor_dtype d) { return d == FAVOR_BF16 ? favor::Dt::BF16 : favor::Dt::F32; }
+
+favor_status check_ptr(const void *p, const char *name, bool needed) {
+  if (!needed) return FAVOR_OK;
+  if (!p) return fail(FAVOR_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+  if (!aligned(p, 16)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+  return FAVOR_OK;
+}
+
+favor_status device_result(hipError_t e, const char *what) {
+  if (e != hipSuccess)
+    return fail(FAVOR_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+#define FAVOR_TRY(expr)                   \
+  do {                                    \
+    favor_status st__ = (expr);           \
+    if (st__ != FAVOR_OK) return st__;    \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int32_t favor_abi_version(void) { return FAVOR_ABI_VERSION; }
+
+const char *favor_last_error(void) { return g_last_error.c_str(); }
+
+const char *favor_status_string(favor_status s) {
+  switch (s) {
+    case FAVOR_OK: return "FAVOR_OK";
+    case FAVOR_ERR_INVALID_ARGUMENT: return "FAVOR_ERR_INVALID_ARGUMENT";
+    case FAVOR_ERR_UNSUPPORTED: return "FAVOR_ERR_UNSUPPORTED";
+    case FAVOR_ERR_WORKSPACE_TOO_SMALL: return "FAVOR_ERR_WORKSPACE_TOO_SMALL";
+    case FAVOR_ERR_DEVICE: return "FAVOR_ERR_DEVICE";
+  }
+  return "FAVOR_ERR_UNKNOWN";
+}
+
+favor_status favor_validate_desc(const favor_desc *g, int op) {
+  FAVOR_TRY(validate(g, op));
+  return ok();
+}
+
+size_t favor_workspace_size(const favor_desc *g, int causal) {
+  if (validate(g, causal ? kOpCausal : kOpBidir) != FAVOR_OK) return 0;
+  return make_plan(g, causal != 0).total;
+}
+
+favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d,
+                            favor_rf_kind kind, float *W, float *b, void *stream) {
+  if (n_heads < 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "n_heads=%d is negative", n_heads);
+  if (M <= 0 || d <= 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "M=%d d=%d must be positive", M, d);
+  if (kind != FAVOR_RF_ORTHO_CHI && kind != FAVOR_RF_ORTHO_FIXED && kind != FAVOR_RF_IID)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown random-feature kind %d", (int)kind);
+  if (d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", d);
+  if (M > 4096) return fail(FAVOR_ERR_UNSUPPORTED, "M=%d exceeds 4096", M);
+  if (n_heads > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "n_heads=%d exceeds 65535", n_heads);
+  if (n_heads == 0) return ok();
+  if (!W || !b) return fail(FAVOR_ERR_INVALID_ARGUMENT, "W and b must be non-NULL");
+  if (!aligned(W, 4) || !aligned(b, 4))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "W and b must be 4-byte aligned");
+  hipError_t e;
+  {
+    favor::LaunchTimer t(favor::kKerOrfDraw, (hipStream_t)stream);
+    e = favor::launch_orf_draw(seed, n_heads, M, (int)kind, W, b, (hipStream_t)stream);
+  }
+  return device_result(e, "favor_orf_draw launch");
+}
+
+favor_status favor_feature_map(const favor_desc *g, const void *X, const float *W,
+                               const float *b, void *Xprime, void *stream) {
+  FAVOR_TRY(validate(g, kOpFeatureMap));
+  const bool work = (long long)g->B * g->H * g->L > 0;
+  FAVOR_TRY(check_ptr(X, "X", work));
+  FAVOR_TRY(check_ptr(W, "W", work));
+  FAVOR_TRY(check_ptr(b, "b", work));
+  FAVOR_TRY(check_ptr(Xprime, "Xprime", work));
+  if (!work) return ok();
+  hipError_t e;
+  {
+    favor::LaunchTimer t(favor::kKerFeatureMap, (hipStream_t)stream);
+    e = favor::launch_feature_map(shape_of(g), dt_of(g->in_dtype), dt_of(g->out_dtype), X, W, b,
+                                  Xprime, (hipStream_t)stream);
+  }
+  return device_result(e, "favor_feature_map launch");
+}
+
+favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
+                              const void *V, const float *W, const float *b, void *out,
+                              void *ws, size_t ws_bytes, void *stream) {
+  FAVOR_TRY(validate(g, kOpBidir));
+  const Plan p = make_plan(g, false);
+  const bool work = p.total > 0;
+  FAVOR_TRY(check_ptr(Q, "Q", work));
+  FAVOR_TRY(check_ptr(K, "K", work));
+  FAVOR_TRY(check_ptr(V, "V", work));
+  FAVOR_TRY(check_ptr(W, "W", work));
+  FAVOR_TRY(check_ptr(b, "b", work));
+  FAVOR_TRY(check_ptr(out, "out", work));
+  if (!work) return ok();
+  if (!ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is not 256-byte aligned");
+  if (ws_bytes < p.total)
+    return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, p.total);
+  const favor::Shape sh = shape_of(g);
+  const favor::Dt in = dt_of(g->in_dtype);
+  hipStream_t st = (hipStream_t)stream;
+  float *part = static_cast<float *>(ws);
+  void *frags = static_cast<char *>(ws) + p.part_bytes;
+  hipError_t e;
+  {
+    favor::LaunchTimer t(favor::kKerKside, st);
+    e = favor::launch_kside(sh, in, K, V, W, b, part, p.rows_per_split, p.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir key pass");
+  {
+    favor::LaunchTimer t(favor::kKerFinalize, st);
+    e = favor::launch_finalize(sh, in, part, p.nsplit, frags, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir reduction");
+  {
+    favor::LaunchTimer t(favor::kKerQside, st);
+    e = favor::launch_qside(sh, in, dt_of(g->out_dtype), Q, W, b, frags, out, st);
+  }
+  return device_result(e, "favor_attn_bidir query pass");
+}
+
+favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K,
+                               const void *V, const float *W, const float *b, void *out,
+                               const float *state_in, float *state_out, void *ws,
+                               size_t ws_bytes, void *stream) {
+  FAVOR_TRY(validate(g, kOpCausal));
+  const Plan p = make_plan(g, true);
+  const bool work = p.total > 0;
+  const bool heads = (long long)g->B * g->H > 0;
+  FAVOR_TRY(check_ptr(Q, "Q", work));
+  FAVOR_TRY(check_ptr(K, "K", work));
+  FAVOR_TRY(check_ptr(V, "V", work));
+  FAVOR_TRY(check_ptr(W, "W", work));
+  FAVOR_TRY(check_ptr(b, "b", work));
+  FAVOR_TRY(check_ptr(out, "out", work));
+  if (state_in && !aligned(state_in, 16))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "state_in is not 16-byte aligned");
+  if (state_out && !aligned(state_out, 16))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "state_out is not 16-byte aligned");
+  const favor::Shape sh = shape_of(g);
+  hipStream_t st = (hipStream_t)stream;
+  if (!work) {
+    // no tokens: the carried state passes through unchanged
+    if (heads && state_out) {
+      hipError_t e;
+      {
+        favor::LaunchTimer t(favor::kKerSegScan, st);
+        e = favor::launch_seg_scan(sh, nullptr, 0, state_in, state_out, st);
+      }
+      return device_result(e, "favor_attn_causal state copy");
+    }
+    return ok();
+  }
+  if (!ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is not 256-byte aligned");
+  if (ws_bytes < p.total)
+    return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, p.total);
+  const favor::Dt in = dt_of(g->in_dtype);
+  float *part = static_cast<float *>(ws);
+  hipError_t e;
+  {
+    favor::LaunchTimer t(favor::kKerKside, st);
+    e = favor::launch_kside(sh, in, K, V, W, b, part, p.rows_per_split, p.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal segment aggregates");
+  {
+    favor::LaunchTimer t(favor::kKerSegScan, st);
+    e = favor::launch_seg_scan(sh, part, p.nsplit, state_in, state_out, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal segment scan");
+  {
+    favor::LaunchTimer t(favor::kKerCausal, st);
+    e = favor::launch_causal(sh, in, dt_of(g->out_dtype), Q, K, V, W, b, part, out,
+                             p.rows_per_split, p.nsplit, st);
+  }
+  return device_result(e, "favor_attn_causal chunk scan");
+}
+
+}  // extern "C"

@@ -1,0 +1,144 @@
+// favor_common.hpp - device building blocks shared by the FAVOR kernels.
+//
+// Matrix-core conventions (CDNA3/CDNA4 16x16 MFMA tiles, wave64):
+//   A operand [16 rows x K]:  lane l holds row (l % 16)
+//   B operand [K x 16 cols]:  lane l holds col (l % 16)
+//   C/D       [16 x 16] fp32: lane l holds col (l % 16), rows 4*(l/16) + j, j = 0..3
+// A "k32 fragment" is one lane's share of a 32-deep slice of K: 8 values. The
+// eight k positions a lane holds are paired with the same eight positions of
+// the other operand, so any bijection between (lane group g = l/16, slot i)
+// and the 32 logical k indices is valid as long as both operands use it.
+//
+// Two bijections are used:
+//   loaded   slot i of group g  <->  k = 8 g + i          (16 contiguous bytes)
+//   chained  slot i of group g  <->  k = 16 (i / 4) + 4 g + (i % 4)
+// "Chained" is the k order in which two vertically adjacent 16x16 accumulator
+// tiles already sit in a lane (rows 4g+j of tile 0, then of tile 1), so an MFMA
+// result can feed the next MFMA as its k operand without moving data across
+// lanes. Tables written for an operand that meets a chained one (the value
+// tile C~, the state, Buf1) are stored in chained order.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace favor {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kWave = 64;
+constexpr float kInv2Pi = 0.15915494309189535f;
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// Policy for the matrix-core element type T (the type of Q, K, V).
+template <typename T> struct Mma;
+
+// bf16 inputs: v_mfma_f32_16x16x32_bf16, bf16 features, hardware cosine.
+template <> struct Mma<bf16> {
+  using frag = bf16x8;
+  static constexpr int kFragBytes = 16;
+  __device__ __forceinline__ static f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static frag pack(f32x4 lo, f32x4 hi) {
+    frag r;
+    r[0] = (bf16)lo[0]; r[1] = (bf16)lo[1]; r[2] = (bf16)lo[2]; r[3] = (bf16)lo[3];
+    r[4] = (bf16)hi[0]; r[5] = (bf16)hi[1]; r[6] = (bf16)hi[2]; r[7] = (bf16)hi[3];
+    return r;
+  }
+  __device__ __forceinline__ static frag from_f32(const float *v, float s) {
+    frag r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = (bf16)(v[i] * s);
+    return r;
+  }
+  __device__ __forceinline__ static frag splat(float v) {
+    frag r;
+    bf16 h = (bf16)v;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = h;
+    return r;
+  }
+  // cos(2 pi x): v_cos_f32 takes its argument in revolutions.
+  __device__ __forceinline__ static float cos_rev(float x) { return __builtin_amdgcn_cosf(x); }
+};
+
+// fp32 inputs: eight v_mfma_f32_16x16x4_f32 per k32 fragment (slot i = k-step i),
+// fp32 features, accurately rounded cosine.
+template <> struct Mma<float> {
+  using frag = f32x8;
+  static constexpr int kFragBytes = 32;
+  __device__ __forceinline__ static f32x4 mma(frag a, frag b, f32x4 c) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[i], c, 0, 0, 0);
+    return c;
+  }
+  __device__ __forceinline__ static frag pack(f32x4 lo, f32x4 hi) {
+    frag r;
+    r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+    r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+    return r;
+  }
+  __device__ __forceinline__ static frag from_f32(const float *v, float s) {
+    frag r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = v[i] * s;
+    return r;
+  }
+  __device__ __forceinline__ static frag splat(float v) {
+    frag r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = v;
+    return r;
+  }
+  __device__ __forceinline__ static float cos_rev(float x) { return cospif(2.0f * x); }
+};
+
+// ---- element conversions ---------------------------------------------------
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+__device__ __forceinline__ float to_f32(float v) { return v; }
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+
+// Load 8 consecutive elements starting at p as a fragment (16 B bf16, 32 B fp32).
+template <typename T>
+__device__ __forceinline__ typename Mma<T>::frag load_frag(const T *p) {
+  return *reinterpret_cast<const typename Mma<T>::frag *>(p);
+}
+template <typename T>
+__device__ __forceinline__ void store_frag(T *p, typename Mma<T>::frag v) {
+  *reinterpret_cast<typename Mma<T>::frag *>(p) = v;
+}
+
+// Load 8 consecutive elements and widen to fp32.
+__device__ __forceinline__ void load8_f32(const bf16 *p, float *v) {
+  bf16x8 x = *reinterpret_cast<const bf16x8 *>(p);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (float)x[i];
+}
+__device__ __forceinline__ void load8_f32(const float *p, float *v) {
+  f32x4 a = *reinterpret_cast<const f32x4 *>(p);
+  f32x4 b = *reinterpret_cast<const f32x4 *>(p + 4);
+  v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+  v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+}
+
+// Store 4 consecutive output elements from fp32 values.
+__device__ __forceinline__ void store4(bf16 *p, f32x4 v) {
+  bf16x4 r;
+  r[0] = (bf16)v[0]; r[1] = (bf16)v[1]; r[2] = (bf16)v[2]; r[3] = (bf16)v[3];
+  *reinterpret_cast<bf16x4 *>(p) = r;
+}
+__device__ __forceinline__ void store4(float *p, f32x4 v) { *reinterpret_cast<f32x4 *>(p) = v; }
+
+// Chained slot of logical k index r in [0, 32): k = 16 h + 4 g + i'  ->  (g, slot 4h + i').
+__device__ __forceinline__ int chained_group(int r) { return (r & 15) >> 2; }
+__device__ __forceinline__ int chained_slot(int r) { return ((r >> 4) << 2) | (r & 3); }
+
+}  // namespace favor

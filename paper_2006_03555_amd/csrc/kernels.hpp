@@ -1,0 +1,84 @@
+// kernels.hpp - host-side launchers of the FAVOR kernels (internal to libfavor).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace favor {
+
+enum class Dt { F32 = 0, BF16 = 1 };
+
+// Bytes of one k32 operand fragment for element type dt (8 elements).
+inline int frag_bytes(Dt dt) { return dt == Dt::BF16 ? 16 : 32; }
+
+// Shape and scalars of one call; pointers are device pointers.
+struct Shape {
+  int BH;        // B * H
+  int H;         // heads (W and b are per head)
+  int L;
+  int M;
+  float s;       // input scale
+  float eps;     // denominator stabiliser
+};
+
+hipError_t launch_orf_draw(uint64_t seed, int n_heads, int M, int kind, float *W, float *b,
+                           hipStream_t st);
+
+hipError_t launch_feature_map(const Shape &sh, Dt in, Dt out, const void *X, const float *W,
+                              const float *b, void *Xp, hipStream_t st);
+
+// K side: per (head, row range) partial Buf1 = K'^T [V 1] -> part [BH][nsplit][M][65].
+hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const float *W,
+                        const float *b, float *part, int rows_per_split, int nsplit,
+                        hipStream_t st);
+
+// Sum the partials of each head and write Buf1^T as Q-side operand fragments.
+hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit, void *frags,
+                           hipStream_t st);
+
+// Q side: out = (Q' Buf1)[:, :d] / ((Q' Buf1)[:, d] + eps), Q' rebuilt on the fly.
+hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const float *W,
+                        const float *b, const void *frags, void *o, hipStream_t st);
+
+// In-place exclusive scan of segment partials (plus state_in); writes state_out.
+hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
+                           float *state_out, hipStream_t st);
+
+// Causal chunk scan of each segment starting from its prefix state.
+hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,
+                         const void *V, const float *W, const float *b, const float *prefix,
+                         void *o, int seg_len, int nseg, hipStream_t st);
+
+}  // namespace favor
+
+namespace favor {
+
+// Kernel ids for the per-launch timing facility (favor_timing_*).
+enum KernelId {
+  kKerOrfDraw = 0,
+  kKerFeatureMap,
+  kKerKside,
+  kKerFinalize,
+  kKerQside,
+  kKerSegScan,
+  kKerCausal,
+  kNumKernels
+};
+const char *kernel_name(int k);
+
+// Brackets one launch with pooled HIP events on `st` while timing is enabled.
+class LaunchTimer {
+ public:
+  LaunchTimer(int kernel, hipStream_t st);
+  ~LaunchTimer();
+  LaunchTimer(const LaunchTimer &) = delete;
+  LaunchTimer &operator=(const LaunchTimer &) = delete;
+
+ private:
+  int kernel_;
+  hipStream_t st_;
+  hipEvent_t begin_ = nullptr;
+};
+
+}  // namespace favor

@@ -1,0 +1,59 @@
+"""Shared test helpers: move seeded host arrays to the GPU and gate parity."""
+import numpy as np
+
+from oracle import favor, metrics
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def torch_dtype(name):
+    import torch
+    return torch.bfloat16 if name == "bf16" else torch.float32
+
+
+def to_dev(x, dtype="f32"):
+    """float32 host array (values exact in dtype) -> contiguous GPU tensor."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(device="cuda", dtype=torch_dtype(dtype)).contiguous()
+
+
+def to_host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def oracle_features(Q, K, W, b, s):
+    return favor.feature_map(Q, W, b, s), favor.feature_map(K, W, b, s)
+
+
+def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=None,
+           heads=None):
+    """Compare a GPU output with the oracle on the same inputs and features.
+
+    heads: optional list of (batch, head) pairs to check (large inputs).
+    Returns (E_row, E_cond); asserts both are within the tolerance."""
+    tol = TOL[dtype] if tol is None else tol
+    Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
+    out = np.asarray(out, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    if heads is not None:
+        sel = lambda a: np.stack([a[bi, hi] for bi, hi in heads])[:, None]
+        Q, K, V, out = sel(Q), sel(K), sel(V), sel(out)
+        W = np.stack([W[hi] for _, hi in heads])[:, None]
+        b = np.stack([b[hi] for _, hi in heads])[:, None]
+        if state_in is not None:
+            state_in = sel(np.asarray(state_in, dtype=np.float64))
+    Qp, Kp = oracle_features(Q, K, W, b, s)
+    if causal:
+        ref, _ = favor.attn_causal_features(Qp, Kp, V, eps, state_in)
+    else:
+        ref = favor.attn_bidir_features(Qp, Kp, V, eps)
+    e_row = metrics.err_row(out, ref)
+    S, den = metrics.error_scale(Qp, Kp, V, causal, state_in_abs=state_in)
+    if eps:
+        den = np.abs(den + eps)
+    e_cond = metrics.err_cond(out, ref, S, den)
+    assert e_row <= tol, f"E_row {e_row:.3e} > {tol}"
+    assert e_cond <= tol, f"E_cond {e_cond:.3e} > {tol}"
+    return e_row, e_cond

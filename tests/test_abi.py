@@ -1,0 +1,134 @@
+"""C-ABI tests that need no GPU: the library loads, exports every function the
+header declares, and rejects bad arguments before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2006_03555_amd as fv
+from paper_2006_03555_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for fn in os.listdir(inc):
+        if fn.endswith(".h"):
+            text = open(os.path.join(inc, fn)).read()
+            names |= set(re.findall(r"FAVOR_API\s+[\w\s\*]+?\b(favor_\w+)\s*\(", text))
+    return sorted(names)
+
+
+@pytest.fixture(scope="module")
+def L():
+    return fv.lib()
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for required in ("favor_orf_draw", "favor_feature_map", "favor_attn_bidir",
+                     "favor_attn_causal", "favor_workspace_size", "favor_last_error"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in _declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_abi_version_and_strings(L):
+    assert L.favor_abi_version() == 1
+    assert fv.status_string(0) == "FAVOR_OK"
+    assert fv.status_string(3) == "FAVOR_ERR_WORKSPACE_TOO_SMALL"
+
+
+def _desc(**kw):
+    base = dict(B=2, H=4, L=1000, d=64, M=256, in_dtype=fv.BF16, out_dtype=fv.BF16,
+                input_scale=64 ** -0.25, denom_eps=0.0, chunk=0)
+    base.update(kw)
+    return fv.make_desc(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(), 0),
+    (dict(L=0), 0),
+    (dict(B=0), 0),
+    (dict(L=-1), 1),
+    (dict(d=0), 1),
+    (dict(d=32), 2),
+    (dict(M=100), 2),
+    (dict(M=0), 1),
+    (dict(in_dtype=7), 1),
+    (dict(out_dtype=-1), 1),
+    (dict(input_scale=float("nan")), 1),
+    (dict(denom_eps=-1.0), 1),
+    (dict(chunk=100), 1),
+    (dict(B=300, H=300), 2),
+])
+def test_validate_desc(kw, status):
+    for op in (fv.OP_FEATURE_MAP, fv.OP_BIDIR, fv.OP_CAUSAL):
+        assert fv.validate_desc(_desc(**kw), op) == status
+        if status:
+            assert fv.last_error() != ""
+
+
+def test_fp32_causal_limits_m():
+    g = _desc(in_dtype=fv.F32, out_dtype=fv.F32, M=256)
+    assert fv.validate_desc(g, fv.OP_CAUSAL) == 2
+    assert fv.validate_desc(g, fv.OP_BIDIR) == 0
+    assert fv.validate_desc(_desc(in_dtype=fv.F32, M=128), fv.OP_CAUSAL) == 0
+
+
+def test_workspace_size():
+    g = _desc()
+    nb = fv.workspace_size(g, 0)
+    nc = fv.workspace_size(g, 1)
+    assert nb > 0 and nc > 0 and nb % 256 == 0 and nc % 256 == 0
+    assert fv.workspace_size(_desc(L=0), 0) == 0
+    assert fv.workspace_size(_desc(M=100), 0) == 0
+    # causal segment length is honoured: more segments need more workspace
+    assert fv.workspace_size(_desc(chunk=128), 1) > fv.workspace_size(_desc(chunk=512), 1)
+
+
+def test_calls_fail_before_launch(L):
+    g = _desc()
+    null = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    # NULL tensors
+    st = L.favor_attn_bidir(ctypes.byref(g), null, null, null, null, null, null, null, 0, null)
+    assert st == 1 and "NULL" in fv.last_error()
+    # misaligned tensor
+    odd = ctypes.c_void_p((1 << 20) + 2)
+    st = L.favor_attn_bidir(ctypes.byref(g), odd, fake, fake, fake, fake, fake, fake, 1 << 30, null)
+    assert st == 1 and "aligned" in fv.last_error()
+    # workspace too small
+    st = L.favor_attn_bidir(ctypes.byref(g), fake, fake, fake, fake, fake, fake, fake, 16, null)
+    assert st == 3
+    st = L.favor_attn_causal(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, null,
+                             fake, 16, null)
+    assert st == 3
+    # bad descriptor
+    bad = _desc(M=100)
+    assert L.favor_feature_map(ctypes.byref(bad), fake, fake, fake, fake, null) == 2
+    assert L.favor_feature_map(None, fake, fake, fake, fake, null) == 1
+
+
+def test_orf_draw_argument_errors(L):
+    null = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    assert L.favor_orf_draw(1, -1, 256, 64, 0, fake, fake, null) == 1
+    assert L.favor_orf_draw(1, 4, 256, 32, 0, fake, fake, null) == 2
+    assert L.favor_orf_draw(1, 4, 256, 64, 9, fake, fake, null) == 1
+    assert L.favor_orf_draw(1, 4, 256, 64, 0, null, fake, null) == 1
+    assert L.favor_orf_draw(1, 4, 8192, 64, 0, fake, fake, null) == 2
+    assert L.favor_orf_draw(1, 0, 256, 64, 0, null, null, null) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "_LIB", None)
+    monkeypatch.setenv("FAVOR_LIBRARY", str(tmp_path / "nope.so"))
+    with pytest.raises(fv.FavorLibraryMissing):
+        fv.lib()
