@@ -19,11 +19,18 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfavor.so")
 ARCH = "gfx950"
 
-SOURCES = ["orf_draw.hip", "feature_map.hip", "bidir.hip", "causal.hip", "favor_api.cpp",
+SOURCES = ["orf_draw.hip", "prep.hip", "feature_map.hip", "bidir.hip", "causal.hip", "favor_api.cpp",
            "timing.cpp"]
 
 # Packed fp32 arithmetic is disabled for all device code (no v_pk_*_f32).
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# MFMA results stay in VGPRs (no AGPR copies before the fused cosine epilogues);
+# not for the causal kernel, whose carried fp32 state is better kept in AGPRs.
+PER_SOURCE_FLAGS = {
+    "feature_map.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "bidir.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "causal.hip": os.environ.get("FAVOR_CAUSAL_FLAGS", "").split(),
+}
 COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
                 "-Wno-unused-function", "-I", os.path.join(ROOT, "include")]
 
@@ -36,8 +43,8 @@ def hipcc():
 
 def _compile(src):
     out = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), f"--offload-arch={ARCH}", *COMMON_FLAGS, *DEVICE_FLAGS, "-x", "hip",
-           "-c", os.path.join(CSRC, src), "-o", out]
+    cmd = [hipcc(), f"--offload-arch={ARCH}", *COMMON_FLAGS, *DEVICE_FLAGS,
+           *PER_SOURCE_FLAGS.get(src, []), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = ("unknown target feature", "packed-fp32-ops", "warning generated")
     msg = "\n".join(ln for ln in (r.stdout + r.stderr).splitlines()

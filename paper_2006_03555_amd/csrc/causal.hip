@@ -16,10 +16,13 @@
 // Work split inside a workgroup of 4 waves for one chunk:
 //   wave w owns features [w M/4, (w+1) M/4) of the state (fp32 accumulators)
 //   and of the key projection; it publishes S (bf16/fp32 A-operand fragments)
-//   and its key features (row-major fragments) through LDS; then wave w owns
-//   queries 16 w .. 16 w + 15 of the chunk: it rebuilds their features over all
-//   M, forms Q-hat S, the masked 16 x (16 w + 16) block of Q-hat K-hat^T and
-//   its product with C~, and writes normalised rows.
+//   and its key features, transposed on the matrix cores to token-major
+//   fragments, through LDS; then wave w owns queries 16 w .. 16 w + 15 of the
+//   chunk: it rebuilds their features over all M, forms Q-hat S and the masked
+//   16 x 64 block of Q-hat K-hat^T with its product with C~ (all waves do the
+//   same work, keys after the query are zeroed), and writes normalised rows.
+// Keys, values and queries of the next chunk are loaded while this one is
+// computed.
 #include "favor_common.hpp"
 #include "kernels.hpp"
 #include "tile_common.hpp"
@@ -34,7 +37,18 @@ __global__ __launch_bounds__(256) void k_seg_scan(float *__restrict__ part, int 
   if (idx >= n) return;
   float run = state_in ? state_in[(size_t)bh * n + idx] : 0.f;
   float *p = part + (size_t)bh * nseg * n + idx;
-  for (int sg = 0; sg < nseg; ++sg) {
+  int sg = 0;
+  for (; sg + 8 <= nseg; sg += 8) {   // eight loads in flight
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = p[(size_t)(sg + k) * n];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      p[(size_t)(sg + k) * n] = run;
+      run += v[k];
+    }
+  }
+  for (; sg < nseg; ++sg) {
     const float v = p[(size_t)sg * n];
     p[(size_t)sg * n] = run;
     run += v;
@@ -47,16 +61,18 @@ struct CausalSmem {
   using frag = typename Mma<T>::frag;
   KVTile<T> tl;
   frag KA[4][M / 32][64];   // key features K-hat as A fragments: lane row t', chained m order
-  frag SA[5][M / 32][64];   // S^T as A fragments: lane row n, chained m order
-  frag WA[M / 16][2][64];   // W'' as A fragments for the query projection
+  frag SA[4][M / 32][64];   // S^T (value columns) as A fragments: lane row n, chained m order
+  frag SZ[M / 32][4];       // the ones column of S^T: one fragment per lane group
+  frag WA[M / 16][2][64];   // W'' fragments (A operand of the query projection, B of the key one)
+  frag SEL[4][64];          // selection matrices for the matrix-core transposes
   float bq[M];
 };
 
 template <typename T, typename To, int M>
 __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T *__restrict__ K,
                                                 const T *__restrict__ V,
-                                                const float *__restrict__ W,
-                                                const float *__restrict__ bph,
+                                                const typename Mma<T>::frag *__restrict__ wfr,
+                                                const float *__restrict__ bqg,
                                                 const float *__restrict__ prefix,
                                                 To *__restrict__ out, int H, int L, int seg_len,
                                                 int nseg, float s, float eps) {
@@ -67,8 +83,9 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
   using frag = typename P::frag;
   __shared__ CausalSmem<T, M> sm;
 
-  const int seg = blockIdx.x;
-  const int bh = blockIdx.y;
+  const int item = xcd_item(blockIdx.x, gridDim.x);
+  const int bh = item / nseg;
+  const int seg = item - bh * nseg;
   const int h = bh % H;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
@@ -76,12 +93,15 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
   const int g = l >> 4;
   const int c16 = l & 15;
 
-  const float *Wh = W + (size_t)h * M * kD;
-  const float *bhh = bph + (size_t)h * M;
-  fill_w_afrags<T, M>(sm.WA, sm.bq, Wh, bhh, s * kInv2Pi);
-  frag Wf[MB][2];
-  f32x4 bC[MB];
-  load_w_bfrags<T, MB>(Wh, bhh, w * MW, s * kInv2Pi, Wf, bC);
+  const frag *wh = wfr + (size_t)h * (M / 16) * 2 * 64;
+  copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wh);
+  if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
+  if (w == 0) {
+    sm.SEL[0][l] = select_frag<T>(0);
+    sm.SEL[1][l] = select_frag<T>(1);
+    sm.SEL[2][l] = chained_select_frag<T>(0);
+    sm.SEL[3][l] = chained_select_frag<T>(1);
+  }
 
   // state rows m = w MW + 16 mb + 4 g + j, columns 16 nb + c16 (the fifth block
   // holds the ones column replicated over its 16 columns)
@@ -108,75 +128,87 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
   const int r0 = seg * seg_len;
   const int r1 = min(L, r0 + seg_len);
 
+  __syncthreads();
+  TileRegs<T> rg;
+  load_tile_regs<T>(rg, Kh, Vh, r0, r1);
+  frag qn[2];
+  load_query_frags<T>(qn, Qh, r0 + 16 * w + c16, r1);
+  KVTile<T> &tl = sm.tl;
   for (int t0 = r0; t0 < r1; t0 += 64) {
-    __syncthreads();
-    stage_kv_tile<T>(sm.tl, Kh, Vh, t0, r1, s2half, cM);
-    // publish S before this chunk's update
+    const bool next = t0 + 64 < r1;
+    // the previous chunk's readers are done: stage this chunk's prefetched keys
+    // and values and publish S (the state before this chunk)
+    {
+      const frag sel[2] = {sm.SEL[0][l], sm.SEL[1][l]};
+      stage_tile<T>(tl, rg, sel, t0, r1, s2half, cM);
+    }
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       const int mbg = w * MB + mb;
 #pragma unroll
-      for (int nb = 0; nb < 5; ++nb) {
+      for (int nb = 0; nb < 4; ++nb) {
         T *p = reinterpret_cast<T *>(&sm.SA[nb][mbg >> 1][l]) + 4 * (mbg & 1);
 #pragma unroll
         for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(accS[mb][nb][j]);
       }
+      if (c16 == 0) {   // ones column: identical in every lane of the group
+        T *p = reinterpret_cast<T *>(&sm.SZ[mbg >> 1][g]) + 4 * (mbg & 1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(accS[mb][4][j]);
+      }
     }
+    const frag qf[2] = {qn[0], qn[1]};
     __syncthreads();
+    if (next) {
+      load_tile_regs<T>(rg, Kh, Vh, t0 + 64, r1);
+      load_query_frags<T>(qn, Qh, t0 + 64 + 16 * w + c16, r1);
+    }
 
-    // key features for this wave's features: publish and fold into S
+    // key features of this wave's feature range: fold into S, and publish them
+    // transposed (row = token) for the intra-chunk products
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
       f32x4 kf[MB][2];
-      key_features<T, MB>(sm.tl, Wf, bC, sidx, kf);
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const int mg = w * MW + mb * 16 + c16;
-        const int sm_ = mg >> 5;
-        const int lane_hi = 16 * chained_group(mg & 31);
-        const int sl = chained_slot(mg & 31);
-#pragma unroll
-        for (int tbl = 0; tbl < 2; ++tbl)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            reinterpret_cast<T *>(&sm.KA[2 * sidx + tbl][sm_][4 * g + j + lane_hi])[sl] =
-                from_f32<T>(kf[mb][tbl][j]);
-      }
+      key_features_lds<T, MB>(tl, sm.WA, sm.bq, w * MB, sidx, kf);
       frag vb[4];
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) vb[nb] = sm.tl.VtF[nb][sidx][l];
-      const frag db = sm.tl.DF[sidx][g];
+      for (int nb = 0; nb < 4; ++nb) vb[nb] = tl.VtF[nb][sidx][l];
+      const frag db = tl.DF[sidx][g];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const frag a = P::pack(kf[mb][0], kf[mb][1]);
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb) accS[mb][nb] = P::mma(a, vb[nb], accS[mb][nb]);
         accS[mb][4] = P::mma(a, db, accS[mb][4]);
+        const int mbg = w * MB + mb;
+#pragma unroll
+        for (int tbl = 0; tbl < 2; ++tbl) {
+          // exact transpose on the matrix cores: lane = token, rows = 4 features
+          const f32x4 c = P::mma(a, sm.SEL[2 + tbl][l], f32x4{0.f, 0.f, 0.f, 0.f});
+          T *p = reinterpret_cast<T *>(&sm.KA[2 * sidx + tbl][mbg >> 1][l]) + 4 * (mbg & 1);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(c[j]);
+        }
       }
     }
     __syncthreads();
 
-    // queries 16 w .. 16 w + 15 of the chunk
+    // queries 16 w .. 16 w + 15 of the chunk (every wave does the same work)
     const int qt = t0 + 16 * w + c16;
-    frag qf[2];
-    float nrm = 0.f;
-    if (qt < r1) {
+    float epsq = 0.f;
+    if (eps != 0.f) {
+      float nrm = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        qf[ks] = load_frag<T>(Qh + (size_t)qt * kD + ks * 32 + 8 * g);
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const float x = to_f32(qf[ks][i]);
           nrm = fmaf(x, x, nrm);
         }
-      }
-    } else {
-      qf[0] = P::splat(0.f);
-      qf[1] = P::splat(0.f);
+      nrm += __shfl_xor(nrm, 16);
+      nrm += __shfl_xor(nrm, 32);
+      epsq = eps / (cM * expf(s2half * nrm));
     }
-    nrm += __shfl_xor(nrm, 16);
-    nrm += __shfl_xor(nrm, 32);
-    const float epsq = (eps != 0.f) ? eps / (cM * expf(s2half * nrm)) : 0.f;
 
     f32x4 o[5];
     f32x4 pt[4];
@@ -185,46 +217,71 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) pt[tb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // operands of one feature step (32 features): W'' for the query projection,
+    // S^T (value columns and ones column) and the key features; loaded one step
+    // ahead so their LDS latency overlaps the current step's matrix work
+    struct StepOps {
+      frag wa[2][2];
+      frag sa[4];
+      frag sz;
+      frag ka[4];
+      f32x4 bc[2];
+    };
+    auto load_ops = [&](StepOps &op, int sidx) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        op.wa[hh][0] = sm.WA[2 * sidx + hh][0][l];
+        op.wa[hh][1] = sm.WA[2 * sidx + hh][1][l];
+        op.bc[hh] = *reinterpret_cast<const f32x4 *>(&sm.bq[(2 * sidx + hh) * 16 + 4 * g]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) op.sa[nb] = sm.SA[nb][sidx][l];
+      op.sz = sm.SZ[sidx][g];
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb) op.ka[tb] = sm.KA[tb][sidx][l];
+    };
+    StepOps cur, nxt;
+    load_ops(nxt, 0);
+#pragma unroll
     for (int sidx = 0; sidx < NS; ++sidx) {
+      cur = nxt;
+      if (sidx + 1 < NS) load_ops(nxt, sidx + 1);
+      __builtin_amdgcn_sched_barrier(0);
       f32x4 pf[2];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        const int mb = 2 * sidx + hh;
-        const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&sm.bq[mb * 16 + 4 * g]);
-        f32x4 p = P::mma(sm.WA[mb][0][l], qf[0], bcv);
-        p = P::mma(sm.WA[mb][1][l], qf[1], p);
+        f32x4 p = P::mma(cur.wa[hh][0], qf[0], cur.bc[hh]);
+        p = P::mma(cur.wa[hh][1], qf[1], p);
 #pragma unroll
         for (int j = 0; j < 4; ++j) pf[hh][j] = P::cos_rev(p[j]);
       }
       const frag qb = P::pack(pf[0], pf[1]);
 #pragma unroll
-      for (int nb = 0; nb < 5; ++nb) o[nb] = P::mma(sm.SA[nb][sidx][l], qb, o[nb]);
+      for (int nb = 0; nb < 4; ++nb) o[nb] = P::mma(cur.sa[nb], qb, o[nb]);
+      o[4] = P::mma(cur.sz, qb, o[4]);
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-        if (tb <= w) pt[tb] = P::mma(sm.KA[tb][sidx][l], qb, pt[tb]);
+      for (int tb = 0; tb < 4; ++tb) pt[tb] = P::mma(cur.ka[tb], qb, pt[tb]);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // keys after the query inside the diagonal block: t' = 16 w + 4 g + j > t = 16 w + c16
+    // keep keys t' = 16 tb + 4 g + j up to the query t = 16 w + c16
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb)
-      if (tb == w) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (4 * g + j > c16) pt[tb][j] = 0.f;
-      }
+      for (int j = 0; j < 4; ++j)
+        pt[tb][j] = (16 * tb + 4 * g + j <= 16 * w + c16) ? pt[tb][j] : 0.f;
 #pragma unroll
     for (int sp = 0; sp < 2; ++sp) {
-      if (2 * sp <= w) {
-        const frag pb = P::pack(pt[2 * sp], pt[2 * sp + 1]);
+      const frag pb = P::pack(pt[2 * sp], pt[2 * sp + 1]);
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) o[nb] = P::mma(sm.tl.VtF[nb][sp][l], pb, o[nb]);
-        o[4] = P::mma(sm.tl.DF[sp][g], pb, o[4]);
-      }
+      for (int nb = 0; nb < 4; ++nb) o[nb] = P::mma(tl.VtF[nb][sp][l], pb, o[nb]);
+      o[4] = P::mma(tl.DF[sp][g], pb, o[4]);
     }
     if (qt < r1) {
       const float inv = 1.0f / (o[4][0] + epsq);
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) store4(Oh + (size_t)qt * kD + nb * 16 + 4 * g, o[nb] * inv);
     }
+    __syncthreads();
   }
 }
 
@@ -238,12 +295,13 @@ hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *
 
 template <typename T, typename To>
 static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, const void *V,
-                               const float *W, const float *b, const float *prefix, void *o,
+                               const void *wfr, const float *bq, const float *prefix, void *o,
                                int seg_len, int nseg, hipStream_t st) {
-  dim3 grid(nseg, sh.BH);
+  dim3 grid(nseg * sh.BH);
 #define FAVOR_CAUSAL_LAUNCH(MM)                                                             \
   hipLaunchKernelGGL((k_causal<T, To, MM>), grid, dim3(256), 0, st, (const T *)Q,             \
-                     (const T *)K, (const T *)V, W, b, prefix, (To *)o, sh.H, sh.L, seg_len,  \
+                     (const T *)K, (const T *)V, (const typename Mma<T>::frag *)wfr, bq, prefix,  \
+                     (To *)o, sh.H, sh.L, seg_len,                                           \
                      nseg, sh.s, sh.eps)
   switch (sh.M) {
     case 64: FAVOR_CAUSAL_LAUNCH(64); break;
@@ -261,15 +319,15 @@ static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, co
 }
 
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,
-                         const void *V, const float *W, const float *b, const float *prefix,
+                         const void *V, const void *wfr, const float *bq, const float *prefix,
                          void *o, int seg_len, int nseg, hipStream_t st) {
   if (in == Dt::BF16)
     return out == Dt::BF16
-               ? causal_typed<bf16, bf16>(sh, Q, K, V, W, b, prefix, o, seg_len, nseg, st)
-               : causal_typed<bf16, float>(sh, Q, K, V, W, b, prefix, o, seg_len, nseg, st);
+               ? causal_typed<bf16, bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st)
+               : causal_typed<bf16, float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st);
   return out == Dt::BF16
-             ? causal_typed<float, bf16>(sh, Q, K, V, W, b, prefix, o, seg_len, nseg, st)
-             : causal_typed<float, float>(sh, Q, K, V, W, b, prefix, o, seg_len, nseg, st);
+             ? causal_typed<float, bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st)
+             : causal_typed<float, float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st);
 }
 
 }  // namespace favor

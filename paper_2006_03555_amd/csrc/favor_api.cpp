@@ -68,12 +68,15 @@ favor_status validate(const favor_desc *g, int op) {
   return FAVOR_OK;
 }
 
+// Workspace: [ split partials | Buf1^T fragments (bidir) | W'' fragments | b'' ]
 struct Plan {
   int BH = 0;
   int nsplit = 0;         // bidir: K-side splits; causal: segments
   int rows_per_split = 0;
   size_t part_bytes = 0;
   size_t frag_bytes = 0;  // bidir only
+  size_t wfr_bytes = 0;
+  size_t bq_bytes = 0;
   size_t total = 0;
 };
 
@@ -96,11 +99,11 @@ Plan make_plan(const favor_desc *g, bool causal) {
   p.rows_per_split = rows;
   p.nsplit = (g->L + rows - 1) / rows;
   p.part_bytes = round_up((size_t)p.BH * p.nsplit * g->M * 65 * sizeof(float), 256);
-  if (!causal) {
-    const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
-    p.frag_bytes = round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
-  }
-  p.total = p.part_bytes + p.frag_bytes;
+  const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
+  if (!causal) p.frag_bytes = round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
+  p.wfr_bytes = round_up((size_t)g->H * (g->M / 16) * 2 * 64 * fb, 256);
+  p.bq_bytes = round_up((size_t)g->H * g->M * sizeof(float), 256);
+  p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
   return p;
 }
 
@@ -226,10 +229,17 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
   hipStream_t st = (hipStream_t)stream;
   float *part = static_cast<float *>(ws);
   void *frags = static_cast<char *>(ws) + p.part_bytes;
+  void *wfr = static_cast<char *>(frags) + p.frag_bytes;
+  float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
   hipError_t e;
   {
+    favor::LaunchTimer t(favor::kKerPrepW, st);
+    e = favor::launch_prep_w(sh, in, W, b, wfr, bq, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir feature preparation");
+  {
     favor::LaunchTimer t(favor::kKerKside, st);
-    e = favor::launch_kside(sh, in, K, V, W, b, part, p.rows_per_split, p.nsplit, st);
+    e = favor::launch_kside(sh, in, K, V, wfr, bq, part, p.rows_per_split, p.nsplit, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_bidir key pass");
   {
@@ -239,7 +249,7 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
   if (e != hipSuccess) return device_result(e, "favor_attn_bidir reduction");
   {
     favor::LaunchTimer t(favor::kKerQside, st);
-    e = favor::launch_qside(sh, in, dt_of(g->out_dtype), Q, W, b, frags, out, st);
+    e = favor::launch_qside(sh, in, dt_of(g->out_dtype), Q, wfr, bq, frags, out, st);
   }
   return device_result(e, "favor_attn_bidir query pass");
 }
@@ -282,10 +292,17 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
     return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, p.total);
   const favor::Dt in = dt_of(g->in_dtype);
   float *part = static_cast<float *>(ws);
+  void *wfr = static_cast<char *>(ws) + p.part_bytes;
+  float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
   hipError_t e;
   {
+    favor::LaunchTimer t(favor::kKerPrepW, st);
+    e = favor::launch_prep_w(sh, in, W, b, wfr, bq, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal feature preparation");
+  {
     favor::LaunchTimer t(favor::kKerKside, st);
-    e = favor::launch_kside(sh, in, K, V, W, b, part, p.rows_per_split, p.nsplit, st);
+    e = favor::launch_kside(sh, in, K, V, wfr, bq, part, p.rows_per_split, p.nsplit, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal segment aggregates");
   {
@@ -295,7 +312,7 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
   if (e != hipSuccess) return device_result(e, "favor_attn_causal segment scan");
   {
     favor::LaunchTimer t(favor::kKerCausal, st);
-    e = favor::launch_causal(sh, in, dt_of(g->out_dtype), Q, K, V, W, b, part, out,
+    e = favor::launch_causal(sh, in, dt_of(g->out_dtype), Q, K, V, wfr, bq, part, out,
                              p.rows_per_split, p.nsplit, st);
   }
   return device_result(e, "favor_attn_causal chunk scan");

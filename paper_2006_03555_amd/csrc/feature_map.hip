@@ -19,14 +19,17 @@ template <typename T, typename To, int M>
 __global__ __launch_bounds__(256) void k_feature_map(const T *__restrict__ X,
                                                      const float *__restrict__ W,
                                                      const float *__restrict__ bph,
-                                                     To *__restrict__ Xp, int H, int L, float s) {
+                                                     To *__restrict__ Xp, int H, int L, float s,
+                                                     int ntiles) {
   constexpr int TBW = FmapCfg<T>::TBW;
   using P = Mma<T>;
   using frag = typename P::frag;
   __shared__ frag WA[M / 16][2][64];
   __shared__ float bq[M];
 
-  const int bh = blockIdx.y;
+  const int item = xcd_item(blockIdx.x, gridDim.x);
+  const int bh = item / ntiles;
+  const int tile = item - bh * ntiles;
   const int h = bh % H;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
@@ -36,7 +39,7 @@ __global__ __launch_bounds__(256) void k_feature_map(const T *__restrict__ X,
 
   fill_w_afrags<T, M>(WA, bq, W + (size_t)h * M * kD, bph + (size_t)h * M, s * kInv2Pi);
 
-  const int rbase = blockIdx.x * (64 * TBW) + w * (16 * TBW);
+  const int rbase = tile * (64 * TBW) + w * (16 * TBW);
   const T *Xh = X + (size_t)bh * L * kD;
   frag xf[TBW][2];
   float dfac[TBW];
@@ -87,19 +90,20 @@ template <typename T, typename To>
 static hipError_t fmap_typed(const Shape &sh, const void *X, const float *W, const float *b,
                              void *Xp, hipStream_t st) {
   const int rows = 64 * FmapCfg<T>::TBW;
-  dim3 grid((sh.L + rows - 1) / rows, sh.BH);
+  const int ntiles = (sh.L + rows - 1) / rows;
+  dim3 grid(ntiles * sh.BH);
   switch (sh.M) {
     case 64:
       hipLaunchKernelGGL((k_feature_map<T, To, 64>), grid, dim3(256), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s);
+                         (To *)Xp, sh.H, sh.L, sh.s, ntiles);
       break;
     case 128:
       hipLaunchKernelGGL((k_feature_map<T, To, 128>), grid, dim3(256), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s);
+                         (To *)Xp, sh.H, sh.L, sh.s, ntiles);
       break;
     case 256:
       hipLaunchKernelGGL((k_feature_map<T, To, 256>), grid, dim3(256), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s);
+                         (To *)Xp, sh.H, sh.L, sh.s, ntiles);
       break;
     default:
       return hipErrorInvalidValue;

@@ -28,9 +28,14 @@ hipError_t launch_orf_draw(uint64_t seed, int n_heads, int M, int kind, float *W
 hipError_t launch_feature_map(const Shape &sh, Dt in, Dt out, const void *X, const float *W,
                               const float *b, void *Xp, hipStream_t st);
 
+// W'' = (s / 2 pi) W as matrix-core fragments [H][M/16][2][64] (element type of
+// `in`) and b'' = b / 2 pi [H][M] fp32, once per call into the workspace.
+hipError_t launch_prep_w(const Shape &sh, Dt in, const float *W, const float *b, void *wfr,
+                         float *bq, hipStream_t st);
+
 // K side: per (head, row range) partial Buf1 = K'^T [V 1] -> part [BH][nsplit][M][65].
-hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const float *W,
-                        const float *b, float *part, int rows_per_split, int nsplit,
+hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const void *wfr,
+                        const float *bq, float *part, int rows_per_split, int nsplit,
                         hipStream_t st);
 
 // Sum the partials of each head and write Buf1^T as Q-side operand fragments.
@@ -38,8 +43,8 @@ hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit
                            hipStream_t st);
 
 // Q side: out = (Q' Buf1)[:, :d] / ((Q' Buf1)[:, d] + eps), Q' rebuilt on the fly.
-hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const float *W,
-                        const float *b, const void *frags, void *o, hipStream_t st);
+hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const void *wfr,
+                        const float *bq, const void *frags, void *o, hipStream_t st);
 
 // In-place exclusive scan of segment partials (plus state_in); writes state_out.
 hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
@@ -47,7 +52,7 @@ hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *
 
 // Causal chunk scan of each segment starting from its prefix state.
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,
-                         const void *V, const float *W, const float *b, const float *prefix,
+                         const void *V, const void *wfr, const float *bq, const float *prefix,
                          void *o, int seg_len, int nseg, hipStream_t st);
 
 }  // namespace favor
@@ -63,6 +68,7 @@ enum KernelId {
   kKerQside,
   kKerSegScan,
   kKerCausal,
+  kKerPrepW,
   kNumKernels
 };
 const char *kernel_name(int k);

@@ -5,11 +5,17 @@
 // (index, head, purpose, 0); each call gives eight 32-bit words (low then high
 // half of each 64-bit output), u = (x + 0.5) 2^-32, and Gaussians by the
 // Box-Muller transform of consecutive uniform pairs. The Gaussian block is
-// orthonormalised row by row with classical Gram-Schmidt applied twice per row
-// ("twice is enough", which keeps fp32 rows orthogonal to rounding level);
-// the triangular factor of row Gram-Schmidt has a positive diagonal, so the
-// result is the unique orthogonal factor. Rows are then scaled by chi_d norms
-// (independent Gaussian vectors) or sqrt(d).
+// orthogonalised row by row with classical Gram-Schmidt in fp64: one pass per
+// row suffices there (the loss of orthogonality grows like cond^2 * 1e-16),
+// and rows are kept unnormalised during the sweep (coefficients divide by the
+// squared norms, each formed by the threads that project onto that row next),
+// so that each row costs two barrier-separated phases with quad-local sums;
+// all rows are normalised at the end. The triangular factor of row
+// Gram-Schmidt has a positive diagonal, so the result is the unique orthogonal
+// factor. Rows are then scaled by chi_d norms (independent Gaussian vectors) or
+// sqrt(d) and rounded to fp32.
+#include <type_traits>
+
 #include "favor_common.hpp"
 #include "kernels.hpp"
 
@@ -71,20 +77,28 @@ __device__ __forceinline__ void gaussians8(uint64_t seed, uint32_t head, uint32_
   }
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+// Sum over the four lanes of an aligned quad (DPP quad permutes, no LDS traffic).
+__device__ __forceinline__ double quad_sum(double v) {
+  auto perm = [](double x, auto ctrl_tag) {
+    constexpr int ctrl = decltype(ctrl_tag)::value;
+    const long long b = __double_as_longlong(x);
+    const int lo = __builtin_amdgcn_mov_dpp((int)b, ctrl, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), ctrl, 0xF, 0xF, false);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+  };
+  v += perm(v, std::integral_constant<int, 0xB1>{});   // quad_perm(1,0,3,2): lane ^ 1
+  v += perm(v, std::integral_constant<int, 0x4E>{});   // quad_perm(2,3,0,1): lane ^ 2
   return v;
 }
 
 __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind,
                                                   float *__restrict__ W, float *__restrict__ b) {
   constexpr int D = kOrfD;
-  __shared__ float G[D][D + 1];
-  __shared__ float Qm[D][D + 1];
+  constexpr int RS = D + 2;            // fp64 row stride (16-byte aligned rows)
+  __shared__ double R[D][RS];          // rows: Gaussian block, orthogonalised in place
+  __shared__ double dots[D];           // <R_j, R_i> / ||R_j||^2 for the current row i
+  __shared__ double nrm2[D];           // ||R_j||^2 of finished rows
   __shared__ float rho[D];
-  __shared__ float r[D];
-  __shared__ float coef[D];
 
   const int blk = blockIdx.x;
   const int h = blockIdx.y;
@@ -96,7 +110,7 @@ __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind
     gaussians8(seed, h, 0, (uint64_t)blk * (D * D / 8) + ci, z);
     const int n0 = ci * 8;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) G[n0 / D][n0 % D + i] = z[i];
+    for (int i = 0; i < 8; ++i) R[n0 / D][n0 % D + i] = (double)z[i];
   }
   // chi_d norms: row m = blk D + rr uses elements m D .. m D + D - 1 (8 calls)
   for (int ci = tid; ci < D * D / 8; ci += 256) {
@@ -129,43 +143,53 @@ __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind
     for (int idx = tid; idx < D * D; idx += 256) {
       const int rr = idx / D;
       const int m = blk * D + rr;
-      if (m < M) W[((size_t)h * M + m) * D + idx % D] = G[rr][idx % D];
+      if (m < M) W[((size_t)h * M + m) * D + idx % D] = (float)R[rr][idx % D];
     }
     return;
   }
 
-  for (int i = 0; i < D; ++i) {
-    if (tid < D) r[tid] = G[i][tid];
-    __syncthreads();
-    for (int pass = 0; pass < 2; ++pass) {
-      {  // coef_j = q_j . r, four threads per j
-        const int j = tid >> 2;
-        const int part = tid & 3;
-        float acc = 0.f;
-        if (j < i) {
+  const int q4 = tid >> 2;    // row (phase 1) or column (phase 2) owned by 4 threads
+  const int part = tid & 3;   // quarter of the 64-long sum
+  for (int i = 0; i <= D; ++i) {
+    // phase 1: coefficients <R_j, R_i> / ||R_j||^2 for the finished rows j < i. The four
+    // threads of row i - 1 also form ||R_{i-1}||^2 (its last use of the previous step).
+    // Loads are unconditional and in bounds so that they issue together.
+    if (q4 < i) {
+      const int ic = min(i, D - 1);
+      double a0 = 0.0, a1 = 0.0, n0 = 0.0, n1 = 0.0;
 #pragma unroll
-          for (int cc = 0; cc < 16; ++cc) acc = fmaf(Qm[j][part * 16 + cc], r[part * 16 + cc], acc);
-        }
-        acc += __shfl_xor(acc, 1);
-        acc += __shfl_xor(acc, 2);
-        if (part == 0) coef[j] = acc;
+      for (int cc = 0; cc < 16; cc += 2) {
+        const double x0 = R[q4][part * 16 + cc];
+        const double x1 = R[q4][part * 16 + cc + 1];
+        a0 = fma(x0, R[ic][part * 16 + cc], a0);
+        a1 = fma(x1, R[ic][part * 16 + cc + 1], a1);
+        n0 = fma(x0, x0, n0);
+        n1 = fma(x1, x1, n1);
       }
-      __syncthreads();
-      {  // r_c -= sum_{j < i} coef_j q_j[c], four threads per c
-        const int c = tid >> 2;
-        const int part = tid & 3;
-        float acc = 0.f;
-        for (int j = part; j < i; j += 4) acc = fmaf(coef[j], Qm[j][c], acc);
-        acc += __shfl_xor(acc, 1);
-        acc += __shfl_xor(acc, 2);
-        if (part == 0) r[c] -= acc;
+      const double a = quad_sum(a0 + a1);
+      const double nn = quad_sum(n0 + n1);
+      if (part == 0) {
+        if (q4 == i - 1) nrm2[q4] = nn;
+        dots[q4] = a / nn;
       }
-      __syncthreads();
     }
-    if (tid < D) {
-      const float v = r[tid];
-      const float n2 = wave_sum(v * v);
-      Qm[i][tid] = v / sqrtf(n2);
+    __syncthreads();
+    if (i == D) break;
+    // phase 2: R_i[c] -= sum_{j < i} coef_j * R_j[c] for column c = q4;
+    // thread part p sums j in [16 p, 16 p + 16) (coefficients of rows j >= i masked)
+    {
+      double a0 = 0.0, a1 = 0.0;
+      const int j0 = part * 16;
+#pragma unroll
+      for (int jj = 0; jj < 16; jj += 2) {
+        const int j = j0 + jj;
+        const double c0 = (j < i) ? dots[j] : 0.0;
+        const double c1 = (j + 1 < i) ? dots[j + 1] : 0.0;
+        a0 = fma(c0, R[j][q4], a0);
+        a1 = fma(c1, R[j + 1][q4], a1);
+      }
+      const double a = quad_sum(a0 + a1);
+      if (part == 0) R[i][q4] -= a;
     }
     __syncthreads();
   }
@@ -174,8 +198,8 @@ __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind
     const int rr = idx / D;
     const int m = blk * D + rr;
     if (m < M) {
-      const float sc = (kind == 0) ? rho[rr] : 8.0f;  // sqrt(64)
-      W[((size_t)h * M + m) * D + idx % D] = Qm[rr][idx % D] * sc;
+      const double sc = (kind == 0 ? (double)rho[rr] : 8.0) / sqrt(nrm2[rr]);  // 8 = sqrt(64)
+      W[((size_t)h * M + m) * D + idx % D] = (float)(R[rr][idx % D] * sc);
     }
   }
 }

@@ -22,8 +22,9 @@ std::vector<Pending> g_pending;
 double g_ms[kNumKernels] = {};
 int64_t g_count[kNumKernels] = {};
 
-const char *const kNames[kNumKernels] = {"k_orf_draw", "k_feature_map", "k_kside", "k_finalize",
-                                         "k_qside",    "k_seg_scan",    "k_causal"};
+const char *const kNames[kNumKernels] = {"k_orf_draw", "k_feature_map", "k_kside",
+                                         "k_finalize", "k_qside",       "k_seg_scan",
+                                         "k_causal",   "k_prep_w"};
 
 hipEvent_t take_event() {
   if (!g_pool.empty()) {
