@@ -31,9 +31,38 @@ import workloads as wl  # noqa: E402
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
-# v_cos_f32 is a quarter-rate transcendental: 256 CUs x 4 SIMD x 16 lanes x
-# 2.4 GHz / 4 = 9.83e12 cosines per second.
-PEAK_COS_PER_S = 256 * 4 * 16 * 2.4e9 / 4
+# v_cos_f32 issues at half the fp32 rate on CDNA4: 256 CUs x 4 SIMD x 16 lanes x
+# 2.4 GHz / 2 = 19.66e12 cosines per second (a microbenchmark of independent
+# v_cos_f32 chains reaches 18.1e12/s, 92 %).
+PEAK_COS_PER_S = 256 * 4 * 16 * 2.4e9 / 2
+# Measured HBM traffic per launch (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by a
+# plain copy of known size), valid only for the kernel sources it was taken on.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = os.path.join(ROOT, "paper_2006_03555_amd", "csrc")
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for fn in sorted(os.listdir(KERNEL_SOURCES)):
+        if fn.endswith((".hip", ".hpp", ".cpp")):
+            with open(os.path.join(KERNEL_SOURCES, fn), "rb") as f:
+                h.update(fn.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the committed counter
+    summary, or None if there is none or the kernel sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    k = t.get("kernels", {}).get(kernel)
+    return None if k is None else k["bytes_per_launch"]
 
 
 def per_token_head(kernel, d, M, elt):
@@ -79,6 +108,28 @@ def cpu_baseline(w, Q, K, V):
                       f"+ causal in fp64 NumPy, {t:.2f} s wall"}
 
 
+def copy_reference(nbytes, steps, warmup):
+    """Time dst.copy_(src) on the device: nbytes read + nbytes written per launch."""
+    import torch
+    torch.cuda.set_device(0)
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(json.dumps({"copy_bytes": n * 4, "ms_per_copy": ms,
+                      "GB_per_s_read_plus_write": 2 * n * 4 / (ms / 1e3) / 1e9}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,6 +137,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="instead of the workload, time a plain device-to-device copy of this "
+                         "many bytes (reference for HBM bandwidth and for scaling the "
+                         "FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FAVOR path "
@@ -94,6 +149,10 @@ def main():
 
     import torch
     import paper_2006_03555_amd as fv
+
+    if args.copy_bytes:
+        copy_reference(args.copy_bytes, args.steps, args.warmup)
+        return
 
     w = wl.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
@@ -161,7 +220,8 @@ def main():
         bound = max(cand, key=lambda k: cand[k][0] / cand[k][1])
         a, p, u = cand[bound]
         roof = {"kernel": dom, "bound": bound, "achieved": a, "peak": p, "unit": u,
-                "frac": a / p, "traffic": None,
+                "frac": a / p, "traffic": measured_traffic(dom, w.name),
+                "algorithmic_bytes_per_launch": by * token_heads,
                 "others": {k: {"achieved": v[0], "peak": v[1], "unit": v[2],
                                "frac": v[0] / v[1]} for k, v in cand.items() if k != bound}}
 

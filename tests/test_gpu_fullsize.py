@@ -1,0 +1,82 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark uses (library defaults: segment length, workgroup counts).
+
+The whole output is computed on the GPU; the fp64 oracle recomputes sampled
+(batch, head) pairs exactly, and properties that hold at any size are checked
+on the whole output (finite values, equal token ids giving equal rows for the
+protein-shaped workload, the last causal row equal to the bidirectional one).
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from helpers import parity, to_dev, to_host
+from oracle import favor
+
+pytestmark = pytest.mark.gpu
+
+
+def _fv():
+    import paper_2006_03555_amd as fv
+    return fv
+
+
+def _run(w, seed_w, heads, gpu_draw=False):
+    import torch
+    fv = _fv()
+    Q, K, V = wl.make_qkv(w)
+    dt = w.dtype
+    dQ, dK, dV = (to_dev(x, dt) for x in (Q, K, V))
+    if gpu_draw:
+        Wd, bd = fv.orf_draw(seed_w, w.H, w.M)
+        Wr, br = favor.orf_draw(seed_w, w.H, w.M, w.d)
+    else:
+        Wr, br = favor.orf_draw(seed_w, w.H, w.M, w.d)
+        Wr, br = Wr.astype(np.float32), br.astype(np.float32)
+        Wd, bd = to_dev(Wr), to_dev(br)
+    out = {}
+    if w.direction in ("bidir", "both"):
+        out["bidir"] = fv.attn_bidir(dQ, dK, dV, Wd, bd, w.input_scale)
+    if w.direction in ("causal", "both"):
+        out["causal"] = fv.attn_causal(dQ, dK, dV, Wd, bd, w.input_scale)
+    torch.cuda.synchronize()
+    out = {k: to_host(v) for k, v in out.items()}
+    for k, v in out.items():
+        assert np.all(np.isfinite(v)), k
+        parity(v, Q, K, V, Wr, br, w.input_scale, k == "causal", dt, heads=heads)
+    return Q, out
+
+
+def test_bidir_b8h8_full():
+    w = wl.WORKLOADS["bidir_b8h8"]
+    _run(w, 2, heads=[(0, 0), (7, 5)])
+
+
+def test_causal_b8h8_full():
+    w = wl.WORKLOADS["causal_b8h8"]
+    _run(w, 3, heads=[(0, 3), (6, 7)])
+
+
+def test_protein_b4h8_full_both_directions():
+    w = wl.WORKLOADS["protein_b4h8"]
+    Q, out = _run(w, 4, heads=[(1, 2)], gpu_draw=True)
+    ids = wl.protein_ids(w)
+    # bidirectional rows depend only on the query row: equal token ids (so equal
+    # Q rows within a head) give bitwise equal outputs
+    bi = out["bidir"]
+    for b in range(w.B):
+        first = {}
+        for l, tok in enumerate(ids[b]):
+            first.setdefault(int(tok), l)
+        for h in range(w.H):
+            ref_rows = {tok: bi[b, h, l] for tok, l in first.items()}
+            for l in range(0, w.L, 97):
+                assert np.array_equal(bi[b, h, l], ref_rows[int(ids[b, l])])
+    # the causal output's last row attends to every key, like the bidirectional one
+    ca = out["causal"]
+    np.testing.assert_allclose(ca[:, :, -1, :], bi[:, :, -1, :], rtol=0, atol=2e-2 * np.max(np.abs(bi)))
+
+
+def test_causal_long_full_with_gpu_draw():
+    w = wl.WORKLOADS["causal_long"]
+    _run(w, 5, heads=[(0, 11)], gpu_draw=True)
