@@ -107,8 +107,9 @@ FAVOR_API favor_status favor_feature_map(const favor_desc *g, const void *X, con
                                const float *b, void *Xprime, void *stream);
 
 /*
- * favor_workspace_size - bytes of device workspace favor_attn_bidir (causal = 0)
- * or favor_attn_causal (causal != 0) needs for descriptor g; 0 if g is invalid.
+ * favor_workspace_size - bytes of device workspace favor_attn_bidir (causal = 0),
+ * favor_attn_causal (causal = 1, or any value other than 0 and 2) or
+ * favor_attn_both (causal = 2) needs for descriptor g; 0 if g is invalid.
  * The workspace must be 256-byte aligned; its contents on entry do not matter.
  */
 FAVOR_API size_t favor_workspace_size(const favor_desc *g, int causal);
@@ -139,8 +140,23 @@ FAVOR_API favor_status favor_attn_causal(const favor_desc *g, const void *Q, con
                                const float *state_in, float *state_out,
                                void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * favor_attn_both - both directions over the same Q, K, V in one call: the
+ * results of favor_attn_bidir (out_bidir) and favor_attn_causal (out_causal,
+ * with state_in / state_out as there; state_in affects the causal output only).
+ * The bidirectional Buf1 = K'^T [V 1] is the causal aggregate over the whole
+ * sequence (G^PS_L of Eq. cumsum), so one pass over the keys serves both:
+ * the key features are built once per segment and the segment scan also
+ * returns the total. Workspace: favor_workspace_size(g, 2). Deterministic.
+ */
+FAVOR_API favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K,
+                                       const void *V, const float *W, const float *b,
+                                       void *out_bidir, void *out_causal,
+                                       const float *state_in, float *state_out,
+                                       void *ws, size_t ws_bytes, void *stream);
+
 /* Host-only validation of a descriptor for an operation (0 feature map,
- * 1 bidirectional, 2 causal); launches nothing and touches no device. */
+ * 1 bidirectional, 2 causal, 3 both); launches nothing and touches no device. */
 FAVOR_API favor_status favor_validate_desc(const favor_desc *g, int op);
 
 FAVOR_API const char *favor_status_string(favor_status s);

@@ -13,13 +13,14 @@ import ctypes
 import os
 
 from ._lib import (  # noqa: F401
-    BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, OP_BIDIR, OP_CAUSAL, OP_FEATURE_MAP,
+    BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, OP_BIDIR, OP_BOTH, OP_CAUSAL, OP_FEATURE_MAP,
     FavorDesc, FavorError, FavorLibraryMissing, lib, lib_path, make_desc, status_string,
     validate_desc, workspace_size, last_error, timing_enable, timing_reset, timing_read,
 )
 
 __all__ = [
-    "orf_draw", "feature_map", "attn_bidir", "attn_causal", "workspace_size", "make_desc",
+    "orf_draw", "feature_map", "attn_bidir", "attn_causal", "attn_both", "workspace_size",
+    "make_desc",
     "validate_desc", "FavorError", "FavorLibraryMissing", "lib", "lib_path",
 ]
 
@@ -139,6 +140,33 @@ def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return
                                    _ptr(out), _ptr(state_in), _ptr(state_out), _ptr(ws),
                                    ctypes.c_size_t(nbytes), _stream(stream)))
     return (out, state_out) if return_state else out
+
+
+def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
+              chunk=0, out_dtype=None, out_bidir=None, out_causal=None, state_out=None,
+              workspace=None, stream=None):
+    """Both directions over the same inputs with one key pass (favor_attn_both).
+
+    Returns (out_bidir, out_causal) or (out_bidir, out_causal, state_out).
+    """
+    torch = _torch()
+    g = _desc_for(Q, W, input_scale, out_dtype, denom_eps, chunk)
+    odt = _torch_dtype(g.out_dtype)
+    if out_bidir is None:
+        out_bidir = torch.empty(Q.shape, dtype=odt, device=Q.device)
+    if out_causal is None:
+        out_causal = torch.empty(Q.shape, dtype=odt, device=Q.device)
+    if return_state and state_out is None:
+        state_out = torch.empty((g.B, g.H, g.M, g.d + 1), dtype=torch.float32, device=Q.device)
+    _require_cuda(Q, K, V, W, b, out_bidir, out_causal, state_in, state_out)
+    ws, nbytes = _workspace(g, 2, workspace)
+    _check(lib().favor_attn_both(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
+                                 _ptr(out_bidir), _ptr(out_causal), _ptr(state_in),
+                                 _ptr(state_out), _ptr(ws), ctypes.c_size_t(nbytes),
+                                 _stream(stream)))
+    if return_state:
+        return out_bidir, out_causal, state_out
+    return out_bidir, out_causal
 
 
 def library_loaded_from():

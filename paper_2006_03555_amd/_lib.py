@@ -10,6 +10,7 @@ RF_IID = 2
 OP_FEATURE_MAP = 0
 OP_BIDIR = 1
 OP_CAUSAL = 2
+OP_BOTH = 3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
@@ -57,6 +58,7 @@ def lib():
         "favor_workspace_size": (sz, [dp, ctypes.c_int]),
         "favor_attn_bidir": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_attn_causal": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_both": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_validate_desc": (ctypes.c_int, [dp, ctypes.c_int]),
         "favor_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "favor_last_error": (ctypes.c_char_p, []),
@@ -96,7 +98,8 @@ def validate_desc(g, op):
 
 
 def workspace_size(g, causal):
-    return lib().favor_workspace_size(ctypes.byref(g), 1 if causal else 0)
+    """causal: False/0 bidirectional, True/1 causal, 2 both directions."""
+    return lib().favor_workspace_size(ctypes.byref(g), 2 if causal == 2 else (1 if causal else 0))
 
 
 def timing_enable(on=True):

@@ -5,7 +5,9 @@
 // parallel and hand each other M x (d+1) fp32 aggregates:
 //   k_kside (bidir.hip)  segment aggregates sum_{j in seg} K'_j C_j^T
 //   k_seg_scan           exclusive prefix over segments, plus state_in;
-//                        the total goes to state_out
+//                        state_in + total goes to state_out and, when both
+//                        directions are requested, the total alone (the
+//                        bidirectional Buf1 = K'^T [V 1]) to its own buffer
 //   k_causal             per segment, 64-token chunks in order. With S the
 //                        state before the chunk (Q-hat, K-hat the features of
 //                        the chunk's queries and keys, C~ = D_K [V 1]):
@@ -31,11 +33,13 @@ namespace favor {
 
 __global__ __launch_bounds__(256) void k_seg_scan(float *__restrict__ part, int nseg, int n,
                                                   const float *__restrict__ state_in,
-                                                  float *__restrict__ state_out) {
+                                                  float *__restrict__ state_out,
+                                                  float *__restrict__ total) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   const int bh = blockIdx.y;
   if (idx >= n) return;
-  float run = state_in ? state_in[(size_t)bh * n + idx] : 0.f;
+  const float s0 = state_in ? state_in[(size_t)bh * n + idx] : 0.f;
+  float run = 0.f;   // aggregate of the segments before sg (tokens of this call only)
   float *p = part + (size_t)bh * nseg * n + idx;
   int sg = 0;
   for (; sg + 8 <= nseg; sg += 8) {   // eight loads in flight
@@ -44,16 +48,17 @@ __global__ __launch_bounds__(256) void k_seg_scan(float *__restrict__ part, int 
     for (int k = 0; k < 8; ++k) v[k] = p[(size_t)(sg + k) * n];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      p[(size_t)(sg + k) * n] = run;
+      p[(size_t)(sg + k) * n] = s0 + run;
       run += v[k];
     }
   }
   for (; sg < nseg; ++sg) {
     const float v = p[(size_t)sg * n];
-    p[(size_t)sg * n] = run;
+    p[(size_t)sg * n] = s0 + run;
     run += v;
   }
-  if (state_out) state_out[(size_t)bh * n + idx] = run;
+  if (state_out) state_out[(size_t)bh * n + idx] = s0 + run;
+  if (total) total[(size_t)bh * n + idx] = run;
 }
 
 template <typename T, int M>
@@ -240,27 +245,42 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 #pragma unroll
       for (int tb = 0; tb < 4; ++tb) op.ka[tb] = sm.KA[tb][sidx][l];
     };
+    // software pipeline: the projection of step sidx + 1 is issued to the matrix
+    // cores before the cosines of step sidx run on the vector unit
+    auto project = [&](const StepOps &op, f32x4 (&pr)[2]) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        pr[hh] = P::mma(op.wa[hh][0], qf[0], op.bc[hh]);
+        pr[hh] = P::mma(op.wa[hh][1], qf[1], pr[hh]);
+      }
+    };
     StepOps cur, nxt;
-    load_ops(nxt, 0);
+    load_ops(cur, 0);
+    f32x4 pc[2];
+    project(cur, pc);
+    if (NS > 1) load_ops(nxt, 1);
 #pragma unroll
     for (int sidx = 0; sidx < NS; ++sidx) {
-      cur = nxt;
-      if (sidx + 1 < NS) load_ops(nxt, sidx + 1);
+      f32x4 pn[2];
+      if (sidx + 1 < NS) project(nxt, pn);
       __builtin_amdgcn_sched_barrier(0);
       f32x4 pf[2];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        f32x4 p = P::mma(cur.wa[hh][0], qf[0], cur.bc[hh]);
-        p = P::mma(cur.wa[hh][1], qf[1], p);
+      for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) pf[hh][j] = P::cos_rev(p[j]);
-      }
+        for (int j = 0; j < 4; ++j) pf[hh][j] = P::cos_rev(pc[hh][j]);
       const frag qb = P::pack(pf[0], pf[1]);
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) o[nb] = P::mma(cur.sa[nb], qb, o[nb]);
       o[4] = P::mma(cur.sz, qb, o[4]);
 #pragma unroll
       for (int tb = 0; tb < 4; ++tb) pt[tb] = P::mma(cur.ka[tb], qb, pt[tb]);
+      if (sidx + 1 < NS) {
+        cur = nxt;
+        pc[0] = pn[0];
+        pc[1] = pn[1];
+        if (sidx + 2 < NS) load_ops(nxt, sidx + 2);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
     // keep keys t' = 16 tb + 4 g + j up to the query t = 16 w + c16
@@ -286,10 +306,11 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 }
 
 hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
-                           float *state_out, hipStream_t st) {
+                           float *state_out, float *total, hipStream_t st) {
   const int n = sh.M * 65;
   dim3 grid((n + 255) / 256, sh.BH);
-  hipLaunchKernelGGL(k_seg_scan, grid, dim3(256), 0, st, part, nseg, n, state_in, state_out);
+  hipLaunchKernelGGL(k_seg_scan, grid, dim3(256), 0, st, part, nseg, n, state_in, state_out,
+                     total);
   return hipGetLastError();
 }
 

@@ -37,11 +37,11 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
 constexpr int kMinRowsPerSplit = 256;
 
-enum Op { kOpFeatureMap = 0, kOpBidir = 1, kOpCausal = 2 };
+enum Op { kOpFeatureMap = 0, kOpBidir = 1, kOpCausal = 2, kOpBoth = 3 };
 
 favor_status validate(const favor_desc *g, int op) {
   if (!g) return fail(FAVOR_ERR_INVALID_ARGUMENT, "descriptor is NULL");
-  if (op < kOpFeatureMap || op > kOpCausal)
+  if (op < kOpFeatureMap || op > kOpBoth)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown operation %d", op);
   if (g->B < 0 || g->H < 0 || g->L < 0)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "negative size B=%d H=%d L=%d", g->B, g->H, g->L);
@@ -63,24 +63,27 @@ favor_status validate(const favor_desc *g, int op) {
     return fail(FAVOR_ERR_UNSUPPORTED, "M=%d not supported (64, 128, 256)", g->M);
   const long long bh = (long long)g->B * g->H;
   if (bh > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "B*H=%lld exceeds 65535", bh);
-  if (op == kOpCausal && g->in_dtype == FAVOR_F32 && g->M > 128)
+  if ((op == kOpCausal || op == kOpBoth) && g->in_dtype == FAVOR_F32 && g->M > 128)
     return fail(FAVOR_ERR_UNSUPPORTED, "causal with fp32 inputs supports M <= 128");
   return FAVOR_OK;
 }
 
-// Workspace: [ split partials | Buf1^T fragments (bidir) | W'' fragments | b'' ]
+// Workspace: [ split partials | total (both) | Buf1^T fragments (bidir, both) |
+//              W'' fragments | b'' ]
 struct Plan {
   int BH = 0;
-  int nsplit = 0;         // bidir: K-side splits; causal: segments
+  int nsplit = 0;         // bidir: K-side splits; causal and both: segments
   int rows_per_split = 0;
   size_t part_bytes = 0;
-  size_t frag_bytes = 0;  // bidir only
+  size_t tot_bytes = 0;   // both only
+  size_t frag_bytes = 0;  // bidir and both
   size_t wfr_bytes = 0;
   size_t bq_bytes = 0;
   size_t total = 0;
 };
 
-Plan make_plan(const favor_desc *g, bool causal) {
+Plan make_plan(const favor_desc *g, int op) {
+  const bool causal = (op != kOpBidir);
   Plan p;
   p.BH = g->B * g->H;
   if (p.BH == 0 || g->L == 0) return p;
@@ -100,10 +103,11 @@ Plan make_plan(const favor_desc *g, bool causal) {
   p.nsplit = (g->L + rows - 1) / rows;
   p.part_bytes = round_up((size_t)p.BH * p.nsplit * g->M * 65 * sizeof(float), 256);
   const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
-  if (!causal) p.frag_bytes = round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
+  if (op != kOpCausal) p.frag_bytes = round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
+  if (op == kOpBoth) p.tot_bytes = round_up((size_t)p.BH * g->M * 65 * sizeof(float), 256);
   p.wfr_bytes = round_up((size_t)g->H * (g->M / 16) * 2 * 64 * fb, 256);
   p.bq_bytes = round_up((size_t)g->H * g->M * sizeof(float), 256);
-  p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
+  p.total = p.part_bytes + p.tot_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
   return p;
 }
 
@@ -164,8 +168,9 @@ favor_status favor_validate_desc(const favor_desc *g, int op) {
 }
 
 size_t favor_workspace_size(const favor_desc *g, int causal) {
-  if (validate(g, causal ? kOpCausal : kOpBidir) != FAVOR_OK) return 0;
-  return make_plan(g, causal != 0).total;
+  const int op = causal == 2 ? kOpBoth : (causal ? kOpCausal : kOpBidir);
+  if (validate(g, op) != FAVOR_OK) return 0;
+  return make_plan(g, op).total;
 }
 
 favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d,
@@ -211,7 +216,7 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
                               const void *V, const float *W, const float *b, void *out,
                               void *ws, size_t ws_bytes, void *stream) {
   FAVOR_TRY(validate(g, kOpBidir));
-  const Plan p = make_plan(g, false);
+  const Plan p = make_plan(g, kOpBidir);
   const bool work = p.total > 0;
   FAVOR_TRY(check_ptr(Q, "Q", work));
   FAVOR_TRY(check_ptr(K, "K", work));
@@ -228,7 +233,7 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
   const favor::Dt in = dt_of(g->in_dtype);
   hipStream_t st = (hipStream_t)stream;
   float *part = static_cast<float *>(ws);
-  void *frags = static_cast<char *>(ws) + p.part_bytes;
+  void *frags = static_cast<char *>(ws) + p.part_bytes + p.tot_bytes;
   void *wfr = static_cast<char *>(frags) + p.frag_bytes;
   float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
   hipError_t e;
@@ -259,7 +264,7 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
                                const float *state_in, float *state_out, void *ws,
                                size_t ws_bytes, void *stream) {
   FAVOR_TRY(validate(g, kOpCausal));
-  const Plan p = make_plan(g, true);
+  const Plan p = make_plan(g, kOpCausal);
   const bool work = p.total > 0;
   const bool heads = (long long)g->B * g->H > 0;
   FAVOR_TRY(check_ptr(Q, "Q", work));
@@ -280,7 +285,7 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
       hipError_t e;
       {
         favor::LaunchTimer t(favor::kKerSegScan, st);
-        e = favor::launch_seg_scan(sh, nullptr, 0, state_in, state_out, st);
+        e = favor::launch_seg_scan(sh, nullptr, 0, state_in, state_out, nullptr, st);
       }
       return device_result(e, "favor_attn_causal state copy");
     }
@@ -307,7 +312,7 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
   if (e != hipSuccess) return device_result(e, "favor_attn_causal segment aggregates");
   {
     favor::LaunchTimer t(favor::kKerSegScan, st);
-    e = favor::launch_seg_scan(sh, part, p.nsplit, state_in, state_out, st);
+    e = favor::launch_seg_scan(sh, part, p.nsplit, state_in, state_out, nullptr, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal segment scan");
   {
@@ -316,6 +321,83 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
                              p.rows_per_split, p.nsplit, st);
   }
   return device_result(e, "favor_attn_causal chunk scan");
+}
+
+favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, const void *V,
+                             const float *W, const float *b, void *out_bidir, void *out_causal,
+                             const float *state_in, float *state_out, void *ws,
+                             size_t ws_bytes, void *stream) {
+  FAVOR_TRY(validate(g, kOpBoth));
+  const Plan p = make_plan(g, kOpBoth);
+  const bool work = p.total > 0;
+  const bool heads = (long long)g->B * g->H > 0;
+  FAVOR_TRY(check_ptr(Q, "Q", work));
+  FAVOR_TRY(check_ptr(K, "K", work));
+  FAVOR_TRY(check_ptr(V, "V", work));
+  FAVOR_TRY(check_ptr(W, "W", work));
+  FAVOR_TRY(check_ptr(b, "b", work));
+  FAVOR_TRY(check_ptr(out_bidir, "out_bidir", work));
+  FAVOR_TRY(check_ptr(out_causal, "out_causal", work));
+  if (state_in && !aligned(state_in, 16))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "state_in is not 16-byte aligned");
+  if (state_out && !aligned(state_out, 16))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "state_out is not 16-byte aligned");
+  const favor::Shape sh = shape_of(g);
+  hipStream_t st = (hipStream_t)stream;
+  if (!work) {
+    if (heads && state_out) {
+      hipError_t e;
+      {
+        favor::LaunchTimer t(favor::kKerSegScan, st);
+        e = favor::launch_seg_scan(sh, nullptr, 0, state_in, state_out, nullptr, st);
+      }
+      return device_result(e, "favor_attn_both state copy");
+    }
+    return ok();
+  }
+  if (!ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is not 256-byte aligned");
+  if (ws_bytes < p.total)
+    return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, p.total);
+  const favor::Dt in = dt_of(g->in_dtype);
+  const favor::Dt out = dt_of(g->out_dtype);
+  float *part = static_cast<float *>(ws);
+  float *tot = reinterpret_cast<float *>(static_cast<char *>(ws) + p.part_bytes);
+  void *frags = static_cast<char *>(ws) + p.part_bytes + p.tot_bytes;
+  void *wfr = static_cast<char *>(frags) + p.frag_bytes;
+  float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
+  hipError_t e;
+  {
+    favor::LaunchTimer t(favor::kKerPrepW, st);
+    e = favor::launch_prep_w(sh, in, W, b, wfr, bq, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both feature preparation");
+  {
+    favor::LaunchTimer t(favor::kKerKside, st);
+    e = favor::launch_kside(sh, in, K, V, wfr, bq, part, p.rows_per_split, p.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both segment aggregates");
+  {
+    favor::LaunchTimer t(favor::kKerSegScan, st);
+    e = favor::launch_seg_scan(sh, part, p.nsplit, state_in, state_out, tot, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both segment scan");
+  {
+    favor::LaunchTimer t(favor::kKerFinalize, st);
+    e = favor::launch_finalize(sh, in, tot, 1, frags, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both Buf1 fragments");
+  {
+    favor::LaunchTimer t(favor::kKerQside, st);
+    e = favor::launch_qside(sh, in, out, Q, wfr, bq, frags, out_bidir, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both bidirectional query pass");
+  {
+    favor::LaunchTimer t(favor::kKerCausal, st);
+    e = favor::launch_causal(sh, in, out, Q, K, V, wfr, bq, part, out_causal, p.rows_per_split,
+                             p.nsplit, st);
+  }
+  return device_result(e, "favor_attn_both chunk scan");
 }
 
 }  // extern "C"

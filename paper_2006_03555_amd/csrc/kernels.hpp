@@ -46,9 +46,10 @@ hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit
 hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const void *wfr,
                         const float *bq, const void *frags, void *o, hipStream_t st);
 
-// In-place exclusive scan of segment partials (plus state_in); writes state_out.
+// In-place exclusive scan of segment partials (plus state_in); writes state_out
+// (state_in + total) and, if non-null, the total of this call's tokens.
 hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
-                           float *state_out, hipStream_t st);
+                           float *state_out, float *total, hipStream_t st);
 
 // Causal chunk scan of each segment starting from its prefix state.
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,

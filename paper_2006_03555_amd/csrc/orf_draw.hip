@@ -94,8 +94,9 @@ __device__ __forceinline__ double quad_sum(double v) {
 __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind,
                                                   float *__restrict__ W, float *__restrict__ b) {
   constexpr int D = kOrfD;
-  constexpr int RS = D + 2;            // fp64 row stride (16-byte aligned rows)
+  constexpr int RS = D + 2;            // fp64 row stride (16-byte aligned rows; 2-way banks)
   __shared__ double R[D][RS];          // rows: Gaussian block, orthogonalised in place
+  __shared__ double RT[D][RS];         // the same block column-major, for column sums
   __shared__ double dots[D];           // <R_j, R_i> / ||R_j||^2 for the current row i
   __shared__ double nrm2[D];           // ||R_j||^2 of finished rows
   __shared__ float rho[D];
@@ -110,7 +111,10 @@ __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind
     gaussians8(seed, h, 0, (uint64_t)blk * (D * D / 8) + ci, z);
     const int n0 = ci * 8;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) R[n0 / D][n0 % D + i] = (double)z[i];
+    for (int i = 0; i < 8; ++i) {
+      R[n0 / D][n0 % D + i] = (double)z[i];
+      RT[n0 % D + i][n0 / D] = (double)z[i];
+    }
   }
   // chi_d norms: row m = blk D + rr uses elements m D .. m D + D - 1 (8 calls)
   for (int ci = tid; ci < D * D / 8; ci += 256) {
@@ -169,8 +173,12 @@ __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind
       const double a = quad_sum(a0 + a1);
       const double nn = quad_sum(n0 + n1);
       if (part == 0) {
+        // 1 / ||R_j||^2: hardware reciprocal refined by two Newton steps
+        double r = __builtin_amdgcn_rcp(nn);
+        r = r * fma(-nn, r, 2.0);
+        r = r * fma(-nn, r, 2.0);
         if (q4 == i - 1) nrm2[q4] = nn;
-        dots[q4] = a / nn;
+        dots[q4] = a * r;
       }
     }
     __syncthreads();
@@ -185,11 +193,15 @@ __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind
         const int j = j0 + jj;
         const double c0 = (j < i) ? dots[j] : 0.0;
         const double c1 = (j + 1 < i) ? dots[j + 1] : 0.0;
-        a0 = fma(c0, R[j][q4], a0);
-        a1 = fma(c1, R[j + 1][q4], a1);
+        a0 = fma(c0, RT[q4][j], a0);
+        a1 = fma(c1, RT[q4][j + 1], a1);
       }
       const double a = quad_sum(a0 + a1);
-      if (part == 0) R[i][q4] -= a;
+      if (part == 0) {
+        const double v = R[i][q4] - a;
+        R[i][q4] = v;
+        RT[q4][i] = v;
+      }
     }
     __syncthreads();
   }

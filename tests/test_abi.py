@@ -69,7 +69,7 @@ def _desc(**kw):
     (dict(B=300, H=300), 2),
 ])
 def test_validate_desc(kw, status):
-    for op in (fv.OP_FEATURE_MAP, fv.OP_BIDIR, fv.OP_CAUSAL):
+    for op in (fv.OP_FEATURE_MAP, fv.OP_BIDIR, fv.OP_CAUSAL, fv.OP_BOTH):
         assert fv.validate_desc(_desc(**kw), op) == status
         if status:
             assert fv.last_error() != ""
@@ -78,7 +78,9 @@ def test_validate_desc(kw, status):
 def test_fp32_causal_limits_m():
     g = _desc(in_dtype=fv.F32, out_dtype=fv.F32, M=256)
     assert fv.validate_desc(g, fv.OP_CAUSAL) == 2
+    assert fv.validate_desc(g, fv.OP_BOTH) == 2
     assert fv.validate_desc(g, fv.OP_BIDIR) == 0
+    assert fv.validate_desc(g, 4) == 1
     assert fv.validate_desc(_desc(in_dtype=fv.F32, M=128), fv.OP_CAUSAL) == 0
 
 
@@ -87,6 +89,8 @@ def test_workspace_size():
     nb = fv.workspace_size(g, 0)
     nc = fv.workspace_size(g, 1)
     assert nb > 0 and nc > 0 and nb % 256 == 0 and nc % 256 == 0
+    nboth = fv.workspace_size(g, 2)
+    assert nboth > nc and nboth % 256 == 0
     assert fv.workspace_size(_desc(L=0), 0) == 0
     assert fv.workspace_size(_desc(M=100), 0) == 0
     # causal segment length is honoured: more segments need more workspace
@@ -109,6 +113,12 @@ def test_calls_fail_before_launch(L):
     assert st == 3
     st = L.favor_attn_causal(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, null,
                              fake, 16, null)
+    assert st == 3
+    st = L.favor_attn_both(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, null, null,
+                           fake, 1 << 30, null)
+    assert st == 1 and "out_causal" in fv.last_error()
+    st = L.favor_attn_both(ctypes.byref(g), fake, fake, fake, fake, fake, fake, fake, null, null,
+                           fake, 16, null)
     assert st == 3
     # bad descriptor
     bad = _desc(M=100)

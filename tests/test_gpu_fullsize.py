@@ -35,9 +35,11 @@ def _run(w, seed_w, heads, gpu_draw=False):
         Wr, br = Wr.astype(np.float32), br.astype(np.float32)
         Wd, bd = to_dev(Wr), to_dev(br)
     out = {}
-    if w.direction in ("bidir", "both"):
+    if w.direction == "both":      # one key pass for both directions, as the benchmark runs it
+        out["bidir"], out["causal"] = fv.attn_both(dQ, dK, dV, Wd, bd, w.input_scale)
+    elif w.direction == "bidir":
         out["bidir"] = fv.attn_bidir(dQ, dK, dV, Wd, bd, w.input_scale)
-    if w.direction in ("causal", "both"):
+    else:
         out["causal"] = fv.attn_causal(dQ, dK, dV, Wd, bd, w.input_scale)
     torch.cuda.synchronize()
     out = {k: to_host(v) for k, v in out.items()}

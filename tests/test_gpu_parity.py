@@ -263,3 +263,41 @@ def test_end_to_end_gpu_draw():
     torch.cuda.synchronize()
     parity(to_host(ob), Q, K, V, Wr, br, S64, False, "bf16")
     parity(to_host(oc), Q, K, V, Wr, br, S64, True, "bf16")
+
+
+# ---------------------------------------------------------------- both directions
+@pytest.mark.parametrize("B,H,L,M,dtype,chunk", [
+    (2, 2, 1000, 256, "bf16", 0),
+    (1, 3, 65, 64, "bf16", 64),
+    (1, 2, 300, 128, "f32", 0),
+])
+def test_both_directions_one_pass(B, H, L, M, dtype, chunk):
+    import torch
+    fv = _fv()
+    Q, K, V = _qkv(B, H, L, dtype, seed=81 + L)
+    W, b = _features(81 + L, H, M)
+    args = [to_dev(x, dtype) for x in (Q, K, V)] + [to_dev(W), to_dev(b)]
+    ob, oc = fv.attn_both(*args, S64, chunk=chunk)
+    torch.cuda.synchronize()
+    parity(to_host(ob), Q, K, V, W, b, S64, False, dtype)
+    parity(to_host(oc), Q, K, V, W, b, S64, True, dtype)
+    # the causal output is the one favor_attn_causal gives (same kernels, same order)
+    oc2 = fv.attn_causal(*args, S64, chunk=chunk)
+    torch.cuda.synchronize()
+    assert torch.equal(oc, oc2)
+
+
+def test_both_state_in_affects_causal_only():
+    import torch
+    fv = _fv()
+    B, H, L, M = 1, 2, 200, 128
+    Q, K, V = _qkv(B, H, L, "f32", seed=91)
+    W, b = _features(91, H, M)
+    S0 = np.abs(np.random.default_rng(2).standard_normal((B, H, M, 65))).astype(np.float32) * 3
+    args = [to_dev(x) for x in (Q, K, V)] + [to_dev(W), to_dev(b)]
+    ob, oc, st = fv.attn_both(*args, S64, state_in=to_dev(S0), return_state=True)
+    oc2, st2 = fv.attn_causal(*args, S64, state_in=to_dev(S0), return_state=True)
+    torch.cuda.synchronize()
+    parity(to_host(ob), Q, K, V, W, b, S64, False, "f32")
+    parity(to_host(oc), Q, K, V, W, b, S64, True, "f32", state_in=S0)
+    assert torch.equal(oc, oc2) and torch.equal(st, st2)
