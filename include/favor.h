@@ -88,9 +88,11 @@ typedef struct {
  * n / 8; u = (x + 0.5) 2^-32; Gaussians by Box-Muller from uniform pairs
  * (u[2p], u[2p+1]): sqrt(-2 ln u[2p]) * (cos, sin)(2 pi u[2p+1]). Gaussian
  * element of block k, row r, column c: n = (k d + r) d + c; chi vector of row
- * m: n = m d + c; phase of row m: n = m. Arithmetic is fp32.
+ * m: n = m d + c; phase of row m: n = m. Uniforms, Gaussians and phases are
+ * computed in fp32; the orthogonalisation, norms and scaling in fp64.
  *
- * Requires n_heads >= 0, d = 64, 1 <= M <= 4096. W, b: device, fp32.
+ * Requires n_heads >= 0, d = 64, 1 <= M <= 4096. W, b: device, fp32; W 16-byte
+ * aligned, b 4-byte aligned.
  */
 FAVOR_API favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d,
                             favor_rf_kind kind, float *W, float *b, void *stream);

@@ -184,8 +184,8 @@ favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d
   if (n_heads > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "n_heads=%d exceeds 65535", n_heads);
   if (n_heads == 0) return ok();
   if (!W || !b) return fail(FAVOR_ERR_INVALID_ARGUMENT, "W and b must be non-NULL");
-  if (!aligned(W, 4) || !aligned(b, 4))
-    return fail(FAVOR_ERR_INVALID_ARGUMENT, "W and b must be 4-byte aligned");
+  if (!aligned(W, 16) || !aligned(b, 4))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "W must be 16-byte and b 4-byte aligned");
   hipError_t e;
   {
     favor::LaunchTimer t(favor::kKerOrfDraw, (hipStream_t)stream);

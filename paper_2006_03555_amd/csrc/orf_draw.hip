@@ -4,16 +4,23 @@
 // (Salmon, Moraes, Dror, Shaw, SC'11) with key (seed, 0) and counter
 // (index, head, purpose, 0); each call gives eight 32-bit words (low then high
 // half of each 64-bit output), u = (x + 0.5) 2^-32, and Gaussians by the
-// Box-Muller transform of consecutive uniform pairs. The Gaussian block is
-// orthogonalised row by row with classical Gram-Schmidt in fp64: one pass per
-// row suffices there (the loss of orthogonality grows like cond^2 * 1e-16),
-// and rows are kept unnormalised during the sweep (coefficients divide by the
-// squared norms, each formed by the threads that project onto that row next),
-// so that each row costs two barrier-separated phases with quad-local sums;
-// all rows are normalised at the end. The triangular factor of row
-// Gram-Schmidt has a positive diagonal, so the result is the unique orthogonal
-// factor. Rows are then scaled by chi_d norms (independent Gaussian vectors) or
-// sqrt(d) and rounded to fp32.
+// Box-Muller transform of consecutive uniform pairs.
+//
+// Four threads own one row of the block, 16 consecutive elements each, held in
+// fp64 registers from the Gaussian draw to the final store. The rows are
+// orthogonalised in order by modified Gram-Schmidt: when row j is final, its
+// owners publish it into its own LDS slot and raise a ready flag; every later
+// row then removes its component along row j (quad-local dot products; the
+// readers also form ||row j||^2 from the same loads). Waves wait on the flags of the rows they need
+// rather than on workgroup barriers, so the work of rows far from the next
+// pivot overlaps the chain of pivots. A wave waits only for rows owned by
+// itself (published earlier in its own program order) or by lower waves, so
+// every flag is raised and every wave finishes; a bounded spin makes that hold
+// even if it did not. Rows stay unnormalised during the sweep and are
+// normalised at the store. The triangular factor of row Gram-Schmidt has a
+// positive diagonal, so the result is the unique orthogonal factor. Rows are
+// then scaled by chi_d norms (independent Gaussian vectors) or sqrt(d) and
+// rounded to fp32.
 #include <type_traits>
 
 #include "favor_common.hpp"
@@ -93,126 +100,123 @@ __device__ __forceinline__ double quad_sum(double v) {
 
 __global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind,
                                                   float *__restrict__ W, float *__restrict__ b) {
-  constexpr int D = kOrfD;
-  constexpr int RS = D + 2;            // fp64 row stride (16-byte aligned rows; 2-way banks)
-  __shared__ double R[D][RS];          // rows: Gaussian block, orthogonalised in place
-  __shared__ double RT[D][RS];         // the same block column-major, for column sums
-  __shared__ double dots[D];           // <R_j, R_i> / ||R_j||^2 for the current row i
-  __shared__ double nrm2[D];           // ||R_j||^2 of finished rows
-  __shared__ float rho[D];
+  constexpr int D = kOrfD;             // 64 rows of 64; thread = (row, quarter)
+  __shared__ double pub[D][D];         // finished rows, one slot each
+  __shared__ int ready[D];             // row j published
 
   const int blk = blockIdx.x;
   const int h = blockIdx.y;
   const int tid = threadIdx.x;
+  const int r = tid >> 2;              // row within the block
+  const int p = tid & 3;               // elements 16 p .. 16 p + 15 of the row
+  const uint64_t m = (uint64_t)blk * D + r;   // feature index of the row
+  if (tid < D) ready[tid] = 0;
 
-  // Gaussian block: element n = (blk D + row) D + col, call n / 8
-  for (int ci = tid; ci < D * D / 8; ci += 256) {
+  // Gaussian block: element (blk D + r) D + c comes from call ((blk D + r) D + c) / 8
+  double x[16];
+  {
     float z[8];
-    gaussians8(seed, h, 0, (uint64_t)blk * (D * D / 8) + ci, z);
-    const int n0 = ci * 8;
+    gaussians8(seed, h, 0, m * (D / 8) + 2 * p, z);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      R[n0 / D][n0 % D + i] = (double)z[i];
-      RT[n0 % D + i][n0 / D] = (double)z[i];
+    for (int i = 0; i < 8; ++i) x[i] = (double)z[i];
+    gaussians8(seed, h, 0, m * (D / 8) + 2 * p + 1, z);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[8 + i] = (double)z[i];
+  }
+  // chi_d norm of row m: elements m D .. m D + D - 1 (calls m D / 8 + q, q < 8)
+  double rho = 8.0;                    // sqrt(64) for the fixed-norm kind
+  if (kind == 0) {
+    double ss = 0.0;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      float z[8];
+      gaussians8(seed, h, 1, m * (D / 8) + 2 * p + q, z);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss = fma((double)z[i], (double)z[i], ss);
     }
+    rho = sqrt(quad_sum(ss));
   }
-  // chi_d norms: row m = blk D + rr uses elements m D .. m D + D - 1 (8 calls)
-  for (int ci = tid; ci < D * D / 8; ci += 256) {
-    const int rr = ci >> 3;
-    const int q = ci & 7;
-    const uint64_t m = (uint64_t)blk * D + rr;
-    float z[8];
-    gaussians8(seed, h, 1, m * (D / 8) + q, z);
-    float ss = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) ss = fmaf(z[i], z[i], ss);
-    ss += __shfl_xor(ss, 1);
-    ss += __shfl_xor(ss, 2);
-    ss += __shfl_xor(ss, 4);
-    if (q == 0) rho[rr] = sqrtf(ss);
-  }
-  // phases: element m = blk D + rr
+  // phases: element m = blk D + i
   if (tid < D / 8) {
     float u[8];
     uniforms8(seed, h, 2, (uint64_t)blk * (D / 8) + tid, u);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int m = blk * D + tid * 8 + i;
-      if (m < M) b[(size_t)h * M + m] = 6.283185307179586f * u[i];
+      const int mm = blk * D + tid * 8 + i;
+      if (mm < M) b[(size_t)h * M + mm] = 6.283185307179586f * u[i];
     }
   }
-  __syncthreads();
 
-  if (kind == 2) {  // IID: raw Gaussian rows
-    for (int idx = tid; idx < D * D; idx += 256) {
-      const int rr = idx / D;
-      const int m = blk * D + rr;
-      if (m < M) W[((size_t)h * M + m) * D + idx % D] = (float)R[rr][idx % D];
-    }
-    return;
-  }
-
-  const int q4 = tid >> 2;    // row (phase 1) or column (phase 2) owned by 4 threads
-  const int part = tid & 3;   // quarter of the 64-long sum
-  for (int i = 0; i <= D; ++i) {
-    // phase 1: coefficients <R_j, R_i> / ||R_j||^2 for the finished rows j < i. The four
-    // threads of row i - 1 also form ||R_{i-1}||^2 (its last use of the previous step).
-    // Loads are unconditional and in bounds so that they issue together.
-    if (q4 < i) {
-      const int ic = min(i, D - 1);
-      double a0 = 0.0, a1 = 0.0, n0 = 0.0, n1 = 0.0;
+  double scale = 1.0;
+  __syncthreads();                     // flags cleared
+  if (kind != 2) {
+    // owners of row j publish it (data, then the flag); readers form its squared
+    // norm themselves from the same loads, which keeps the norm and its
+    // reciprocal off the owner's side of the chain
+    auto publish = [&](int j) {
+      double *dst = &pub[j][16 * p];
 #pragma unroll
-      for (int cc = 0; cc < 16; cc += 2) {
-        const double x0 = R[q4][part * 16 + cc];
-        const double x1 = R[q4][part * 16 + cc + 1];
-        a0 = fma(x0, R[ic][part * 16 + cc], a0);
-        a1 = fma(x1, R[ic][part * 16 + cc + 1], a1);
-        n0 = fma(x0, x0, n0);
-        n1 = fma(x1, x1, n1);
-      }
-      const double a = quad_sum(a0 + a1);
-      const double nn = quad_sum(n0 + n1);
-      if (part == 0) {
-        // 1 / ||R_j||^2: hardware reciprocal refined by two Newton steps
-        double r = __builtin_amdgcn_rcp(nn);
-        r = r * fma(-nn, r, 2.0);
-        r = r * fma(-nn, r, 2.0);
-        if (q4 == i - 1) nrm2[q4] = nn;
-        dots[q4] = a * r;
-      }
-    }
-    __syncthreads();
-    if (i == D) break;
-    // phase 2: R_i[c] -= sum_{j < i} coef_j * R_j[c] for column c = q4;
-    // thread part p sums j in [16 p, 16 p + 16) (coefficients of rows j >= i masked)
-    {
-      double a0 = 0.0, a1 = 0.0;
-      const int j0 = part * 16;
+      for (int i = 0; i < 16; i += 2) *(double2 *)(dst + i) = make_double2(x[i], x[i + 1]);
+      if (p == 0)
+        __hip_atomic_store(&ready[j], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    };
+    if (r == 0) publish(0);
+    // a wave holds rows 16 w .. 16 w + 15; the last step that changes one of them is
+    // j = 16 w + 14
+    const int last = (tid >> 6) * 16 + 15;
+    for (int j = 0; j < last; ++j) {
+      for (int spin = 0; spin < (1 << 22); ++spin)
+        if (__hip_atomic_load(&ready[j], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) break;
+      const double *src = &pub[j][16 * p];
+      double q[16];
 #pragma unroll
-      for (int jj = 0; jj < 16; jj += 2) {
-        const int j = j0 + jj;
-        const double c0 = (j < i) ? dots[j] : 0.0;
-        const double c1 = (j + 1 < i) ? dots[j + 1] : 0.0;
-        a0 = fma(c0, RT[q4][j], a0);
-        a1 = fma(c1, RT[q4][j + 1], a1);
+      for (int i = 0; i < 16; i += 2) {
+        const double2 v = *(const double2 *)(src + i);
+        q[i] = v.x;
+        q[i + 1] = v.y;
       }
-      const double a = quad_sum(a0 + a1);
-      if (part == 0) {
-        const double v = R[i][q4] - a;
-        R[i][q4] = v;
-        RT[q4][i] = v;
+      double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+      double n0 = 0.0, n1 = 0.0, n2 = 0.0, n3 = 0.0;
+#pragma unroll
+      for (int i = 0; i < 16; i += 4) {
+        a0 = fma(x[i], q[i], a0);
+        a1 = fma(x[i + 1], q[i + 1], a1);
+        a2 = fma(x[i + 2], q[i + 2], a2);
+        a3 = fma(x[i + 3], q[i + 3], a3);
+        n0 = fma(q[i], q[i], n0);
+        n1 = fma(q[i + 1], q[i + 1], n1);
+        n2 = fma(q[i + 2], q[i + 2], n2);
+        n3 = fma(q[i + 3], q[i + 3], n3);
       }
+      const double dot = quad_sum((a0 + a1) + (a2 + a3));
+      const double nq = quad_sum((n0 + n1) + (n2 + n3));
+      // 1 / ||row j||^2: hardware reciprocal refined by two Newton steps
+      double inv = __builtin_amdgcn_rcp(nq);
+      inv = inv * fma(-nq, inv, 2.0);
+      inv = inv * fma(-nq, inv, 2.0);
+      const double c = (r > j) ? dot * inv : 0.0;   // rows up to j are final
+#pragma unroll
+      for (int i = 0; i < 16; ++i) x[i] = fma(-c, q[i], x[i]);
+      if (r == j + 1) publish(j + 1);
     }
-    __syncthreads();
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+#pragma unroll
+    for (int i = 0; i < 16; i += 4) {
+      s0 = fma(x[i], x[i], s0);
+      s1 = fma(x[i + 1], x[i + 1], s1);
+      s2 = fma(x[i + 2], x[i + 2], s2);
+      s3 = fma(x[i + 3], x[i + 3], s3);
+    }
+    const double nrm2 = quad_sum((s0 + s1) + (s2 + s3));
+    scale = rho / sqrt(nrm2);
   }
 
-  for (int idx = tid; idx < D * D; idx += 256) {
-    const int rr = idx / D;
-    const int m = blk * D + rr;
-    if (m < M) {
-      const double sc = (kind == 0 ? (double)rho[rr] : 8.0) / sqrt(nrm2[rr]);  // 8 = sqrt(64)
-      W[((size_t)h * M + m) * D + idx % D] = (float)(R[rr][idx % D] * sc);
-    }
+  if ((int)m < M) {
+    float4* dst = (float4 *)(W + ((size_t)h * M + m) * D + 16 * p);
+#pragma unroll
+    for (int i = 0; i < 16; i += 4)
+      dst[i / 4] = make_float4((float)(x[i] * scale), (float)(x[i + 1] * scale),
+                               (float)(x[i + 2] * scale), (float)(x[i + 3] * scale));
   }
 }
 

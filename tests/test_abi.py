@@ -133,6 +133,8 @@ def test_orf_draw_argument_errors(L):
     assert L.favor_orf_draw(1, 4, 256, 32, 0, fake, fake, null) == 2
     assert L.favor_orf_draw(1, 4, 256, 64, 9, fake, fake, null) == 1
     assert L.favor_orf_draw(1, 4, 256, 64, 0, null, fake, null) == 1
+    assert L.favor_orf_draw(1, 4, 256, 64, 0, ctypes.c_void_p((1 << 20) + 4), fake, null) == 1
+    assert "16-byte" in fv.last_error()
     assert L.favor_orf_draw(1, 4, 8192, 64, 0, fake, fake, null) == 2
     assert L.favor_orf_draw(1, 0, 256, 64, 0, null, null, null) == 0
 
