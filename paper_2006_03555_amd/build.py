@@ -29,7 +29,7 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 PER_SOURCE_FLAGS = {
     "feature_map.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "bidir.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-    "causal.hip": os.environ.get("FAVOR_CAUSAL_FLAGS", "").split(),
+    "causal.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
                 "-Wno-unused-function", "-I", os.path.join(ROOT, "include")]

@@ -305,12 +305,435 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
   }
 }
 
+// ---------------------------------------------------------------------------
+// Feature-split form for bf16 inputs. Wave w owns features [w MW, (w + 1) MW),
+// MW = M / 4, for the keys and for the queries of every 64-token chunk: its
+// slice of the state S (fp32 accumulators, rows m of its slice, 65 columns
+// padded to 80 with the ones column replicated over the last 16) never leaves
+// its registers, its W'' fragments are loaded once, and its key features are
+// transposed on the matrix cores without LDS. Since
+//   Buf2 = Q-hat S + tril(Q-hat K-hat^T) C~ = sum over feature slices,
+// each wave forms partial numerators and denominators for all 64 tokens of
+// the chunk; wave w then finalises tokens 16 w .. 16 w + 15 from its own
+// partial and the three others, handed over through LDS. Tiles of K, Q and
+// C~ and the hand-over area are double-buffered, so one barrier per chunk
+// separates producers from consumers.
+//
+// Value columns are held in a permuted order: row r of value block nb (the
+// lane row of C~ as an A operand, the row of an output tile) is column
+//   pi(nb, r) = 32 (nb / 2) + 8 (r / 4) + 4 (nb % 2) + r % 4,
+// so that the lane holding rows 4 g .. 4 g + 3 of blocks 2 p and 2 p + 1 holds
+// the eight consecutive output columns 32 p + 8 g .. 32 p + 8 g + 7.
+struct CausalFsTile {
+  KVTile<bf16> kv;               // keys row-major, C~ (permuted columns) and D_K fragments
+  bf16 Qs[64][kD + kKsPad];      // queries row-major (B operand of the query projection)
+  float epsq[64];                // denominator stabiliser per query (eps / (sqrt(2/M) D_Q))
+};
+struct CausalFsSmem {
+  CausalFsTile tile[2];
+  f32x4 num[2][4][3][4][64];     // [buffer][source wave][slot][value block][lane]
+  float den[2][4][3][16];        // [buffer][source wave][slot][token]
+};
+
+__device__ __forceinline__ int perm_col(int nb, int r) {
+  return 32 * (nb >> 1) + 8 * (r >> 2) + 4 * (nb & 1) + (r & 3);
+}
+
+// Selection matrix in loaded k order with B[k][c] = (k == 8 (c / 4) + 4 half + c % 4):
+// the MFMA of value rows (A operand, k = 32 value columns of step kh) with it
+// moves value column 32 kh + 8 (c / 4) + 4 half + c % 4 = pi(2 kh + half, c) to lane c.
+__device__ __forceinline__ bf16x8 select_perm_frag(int half) {
+  const int l = lane_id();
+  const int c = l & 15;
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (8 * (l >> 4) + i == 8 * (c >> 2) + 4 * half + (c & 3)) ? 1.f : 0.f;
+  return Mma<bf16>::from_f32(v, 1.f);
+}
+
+// Sum over the four lanes of an aligned quad (DPP quad permutes).
+__device__ __forceinline__ float quad_sum_f32(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));
+  return v;
+}
+
+// Query rows of a 64-token tile, loaded like the keys (row tid / 4, 16 columns).
+__device__ __forceinline__ void load_q_rows(bf16x8 (&q)[2], const bf16 *__restrict__ Qh, int t0,
+                                            int r1) {
+  const int tid = threadIdx.x;
+  const int rq = t0 + (tid >> 2);
+  if (rq < r1) {
+    const bf16 *qp = Qh + (size_t)rq * kD + (tid & 3) * 16;
+    q[0] = load_frag<bf16>(qp);
+    q[1] = load_frag<bf16>(qp + 8);
+  } else {
+    q[0] = Mma<bf16>::splat(0.f);
+    q[1] = Mma<bf16>::splat(0.f);
+  }
+}
+
+// Stage a prefetched tile: keys and queries row-major, D_K(t) = sqrt(2/M)
+// exp(||s k_t||^2 / 2) (0 past r1), C~ = D_K [V 1] as chained-order B fragments
+// in permuted column order (wave w transposes the values of tokens 16 w ..),
+// and the per-query stabiliser when eps != 0.
+__device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRegs<bf16> &r,
+                                                  const bf16x8 (&q)[2], int t0, int r1,
+                                                  float s2half, float cM, float eps) {
+  using P = Mma<bf16>;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int l = tid & 63;
+  const int g = l >> 4;
+  const int c16 = l & 15;
+  const int tr = tid >> 2;
+  const int cq = (tid & 3) * 16;
+  store_frag<bf16>(&tl.kv.Ks[tr][cq], r.k[0]);
+  store_frag<bf16>(&tl.kv.Ks[tr][cq + 8], r.k[1]);
+  store_frag<bf16>(&tl.Qs[tr][cq], q[0]);
+  store_frag<bf16>(&tl.Qs[tr][cq + 8], q[1]);
+  float nrm = 0.f;
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float x = to_f32(r.k[hh][i]);
+      nrm = fmaf(x, x, nrm);
+    }
+  nrm = quad_sum_f32(nrm);
+  const float Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
+  float Dj[4];   // D of tokens 16 w + 4 g + j, held by the quad of lanes 16 g + 4 j
+#pragma unroll
+  for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Dt, 16 * g + 4 * j);
+  const bf16x8 sel[2] = {select_perm_frag(0), select_perm_frag(1)};
+  const int sidx = w >> 1;
+  const int hw = w & 1;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const f32x4 c = P::mma(r.v[kh], sel[half], zero4);
+      bf16 *p = reinterpret_cast<bf16 *>(&tl.kv.VtF[2 * kh + half][sidx][l]) + 4 * hw;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) p[j] = (bf16)(c[j] * Dj[j]);
+    }
+  if (c16 == 0) {
+    bf16 *p = reinterpret_cast<bf16 *>(&tl.kv.DF[sidx][g]) + 4 * hw;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) p[j] = (bf16)Dj[j];
+  }
+  if (eps != 0.f) {
+    float qn = 0.f;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float x = to_f32(q[hh][i]);
+        qn = fmaf(x, x, qn);
+      }
+    qn = quad_sum_f32(qn);
+    if ((tid & 3) == 0) tl.epsq[tr] = (t0 + tr < r1) ? eps / (cM * expf(s2half * qn)) : 0.f;
+  }
+}
+
+// Eight consecutive output elements from two fp32 quadruples.
+__device__ __forceinline__ void store8(bf16 *p, f32x4 a, f32x4 b) {
+  bf16x8 r;
+  r[0] = (bf16)a[0]; r[1] = (bf16)a[1]; r[2] = (bf16)a[2]; r[3] = (bf16)a[3];
+  r[4] = (bf16)b[0]; r[5] = (bf16)b[1]; r[6] = (bf16)b[2]; r[7] = (bf16)b[3];
+  *reinterpret_cast<bf16x8 *>(p) = r;
+}
+__device__ __forceinline__ void store8(float *p, f32x4 a, f32x4 b) {
+  *reinterpret_cast<f32x4 *>(p) = a;
+  *reinterpret_cast<f32x4 *>(p + 4) = b;
+}
+
+template <typename To, int M>
+__global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
+                                                   const bf16 *__restrict__ K,
+                                                   const bf16 *__restrict__ V,
+                                                   const bf16x8 *__restrict__ wfr,
+                                                   const float *__restrict__ bqg,
+                                                   const float *__restrict__ prefix,
+                                                   To *__restrict__ out, int H, int L,
+                                                   int seg_len, int nseg, float s, float eps) {
+  constexpr int MW = M / 4;          // features per wave
+  constexpr int MB = MW / 16;        // 16-feature blocks per wave
+  constexpr int KS = (MB + 1) / 2;   // 32-feature k-steps per wave (a lone block is zero-padded)
+  using P = Mma<bf16>;
+  using frag = bf16x8;
+  __shared__ CausalFsSmem sm;
+
+  const int item = xcd_item(blockIdx.x, gridDim.x);
+  const int bh = item / nseg;
+  const int seg = item - bh * nseg;
+  const int h = bh % H;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int l = tid & 63;
+  const int g = l >> 4;
+  const int c16 = l & 15;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+
+  const bf16 *Qh = Q + (size_t)bh * L * kD;
+  const bf16 *Kh = K + (size_t)bh * L * kD;
+  const bf16 *Vh = V + (size_t)bh * L * kD;
+  To *Oh = out + (size_t)bh * L * kD;
+  const float s2half = 0.5f * s * s;
+  const float cM = sqrtf(2.0f / M);
+  const int r0 = seg * seg_len;
+  const int r1 = min(L, r0 + seg_len);
+
+  // the first tile's loads go out first: staging waits for them alone
+  TileRegs<bf16> rg;
+  frag rq[2];
+  load_tile_regs<bf16>(rg, Kh, Vh, r0, r1);
+  load_q_rows(rq, Qh, r0, r1);
+
+  // W'' fragments of this wave's features: A operand of the query projection
+  // (lane row m), B operand of the key one (lane col m); b'' per row and column
+  frag wf[MB][2];
+  float bk[MB];
+  f32x4 bqv[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int mbg = w * MB + mb;
+    const frag *wh = wfr + ((size_t)h * (M / 16) + mbg) * 2 * 64;
+    wf[mb][0] = wh[l];
+    wf[mb][1] = wh[64 + l];
+    const float *bb = bqg + (size_t)h * M + 16 * mbg;
+    bk[mb] = bb[c16];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bqv[mb][j] = bb[4 * g + j];
+  }
+
+  // state rows m = w MW + 16 mb + 4 g + j, lane column c16 of block nb holding
+  // value column pi(nb, c16) (block 4: the ones column in all 16 columns)
+  f32x4 accS[MB][5];
+  {
+    const float *pre = prefix + ((size_t)bh * nseg + seg) * M * 65;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = w * MW + mb * 16 + 4 * g + j;
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) accS[mb][nb][j] = pre[m * 65 + perm_col(nb, c16)];
+        accS[mb][4][j] = pre[m * 65 + 64];
+      }
+  }
+
+  stage_causal_tile(sm.tile[0], rg, rq, r0, r1, s2half, cM, eps);
+  if (r0 + 64 < r1) {
+    load_tile_regs<bf16>(rg, Kh, Vh, r0 + 64, r1);
+    load_q_rows(rq, Qh, r0 + 64, r1);
+  }
+  __syncthreads();
+
+  int buf = 0;
+  for (int t0 = r0; t0 < r1; t0 += 64, buf ^= 1) {
+    const CausalFsTile &tl = sm.tile[buf];
+    const float my_epsq = (eps != 0.f) ? tl.epsq[16 * w + c16] : 0.f;
+
+    // query features of this wave's slice, transposed: qB[tb][ks] is the B operand
+    // (col = token 16 tb + c16, k = 32 features of step ks, chained order)
+    frag qB[4][KS];
+    frag qa[4][2];   // all query fragments of the tile, loaded together
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      qa[tb][0] = load_frag<bf16>(&tl.Qs[16 * tb + c16][8 * g]);
+      qa[tb][1] = load_frag<bf16>(&tl.Qs[16 * tb + c16][32 + 8 * g]);
+    }
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      f32x4 pr[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        pr[mb] = P::mma(wf[mb][0], qa[tb][0], bqv[mb]);
+        pr[mb] = P::mma(wf[mb][1], qa[tb][1], pr[mb]);
+      }
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pr[mb][j] = P::cos_rev(pr[mb][j]);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qB[tb][ks] = P::pack(pr[2 * ks], (2 * ks + 1 < MB) ? pr[2 * ks + 1] : zero4);
+    }
+
+    // partial Buf2 (value columns and the denominator) over this slice: o[nb][tb]
+    // holds rows pi(nb, 4 g + j), column = token 16 tb + c16; first Q-hat S with
+    // the state before the chunk
+    f32x4 o[5][4];
+    {
+      frag sA[5][KS];   // lane row = value column, k = m
+#pragma unroll
+      for (int nb = 0; nb < 5; ++nb)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          sA[nb][ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+        for (int nb = 0; nb < 5; ++nb) {
+          o[nb][tb] = P::mma(sA[nb][0], qB[tb][0], zero4);
+#pragma unroll
+          for (int ks = 1; ks < KS; ++ks) o[nb][tb] = P::mma(sA[nb][ks], qB[tb][ks], o[nb][tb]);
+        }
+    }
+
+    // keys, one 32-token half at a time: features of the slice, folded into S
+    // (after the queries above used it), transposed to token rows on the matrix
+    // cores, then the intra-chunk part of that half: P^T[t'][t] = K-hat_t' .
+    // Q-hat_t over the slice for key blocks tb' <= tb (keys after the query
+    // zeroed) and C~^T P^T into o
+#pragma unroll
+    for (int sidx = 0; sidx < 2; ++sidx) {
+      // C~ of the half: B operand of the state update and A operand of the
+      // intra-chunk product (lane = value column, k = token in chained order)
+      frag vt[4];
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) vt[nb] = tl.kv.VtF[nb][sidx][l];
+      const frag df = tl.kv.DF[sidx][g];
+      const frag a0[2] = {load_frag<bf16>(&tl.kv.Ks[32 * sidx + c16][8 * g]),
+                          load_frag<bf16>(&tl.kv.Ks[32 * sidx + 16 + c16][8 * g])};
+      const frag a1[2] = {load_frag<bf16>(&tl.kv.Ks[32 * sidx + c16][32 + 8 * g]),
+                          load_frag<bf16>(&tl.kv.Ks[32 * sidx + 16 + c16][32 + 8 * g])};
+      frag kT[2][KS];   // A operand: lane row = token 32 sidx + 16 tbl + c16, k = 32 features
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        f32x4 ct[2][2];
+#pragma unroll
+        for (int hm = 0; hm < 2; ++hm) {
+          const int mb = 2 * ks + hm;
+          if (mb >= MB) {
+            ct[0][hm] = zero4;
+            ct[1][hm] = zero4;
+            continue;
+          }
+          f32x4 kf[2];
+#pragma unroll
+          for (int tbl = 0; tbl < 2; ++tbl) {
+            const float bb = bk[mb];
+            f32x4 p = P::mma(a0[tbl], wf[mb][0], f32x4{bb, bb, bb, bb});
+            p = P::mma(a1[tbl], wf[mb][1], p);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) kf[tbl][j] = P::cos_rev(p[j]);
+          }
+          const frag a = P::pack(kf[0], kf[1]);   // lane row m, k = 32 tokens
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) accS[mb][nb] = P::mma(a, vt[nb], accS[mb][nb]);
+          accS[mb][4] = P::mma(a, df, accS[mb][4]);
+#pragma unroll
+          for (int tbl = 0; tbl < 2; ++tbl)
+            ct[tbl][hm] = P::mma(a, chained_select_frag<bf16>(tbl), zero4);
+        }
+#pragma unroll
+        for (int tbl = 0; tbl < 2; ++tbl) kT[tbl][ks] = P::pack(ct[tbl][0], ct[tbl][1]);
+      }
+#pragma unroll
+      for (int tb = 2 * sidx; tb < 4; ++tb) {
+        f32x4 pt[2];
+#pragma unroll
+        for (int tbl = 0; tbl < 2; ++tbl) {
+          const int tp = 2 * sidx + tbl;
+          if (tp > tb) {
+            pt[tbl] = zero4;
+            continue;
+          }
+          pt[tbl] = P::mma(kT[tbl][0], qB[tb][0], zero4);
+#pragma unroll
+          for (int ks = 1; ks < KS; ++ks) pt[tbl] = P::mma(kT[tbl][ks], qB[tb][ks], pt[tbl]);
+          if (tp == tb) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) pt[tbl][j] = (4 * g + j <= c16) ? pt[tbl][j] : 0.f;
+          }
+        }
+        const frag pb = P::pack(pt[0], pt[1]);
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) o[nb][tb] = P::mma(vt[nb], pb, o[nb][tb]);
+        o[4][tb] = P::mma(df, pb, o[4][tb]);
+      }
+    }
+
+    // hand the partials of the other waves' tokens over; keep this wave's own
+    f32x4 own[5];
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      if (tb == w) {
+#pragma unroll
+        for (int nb = 0; nb < 5; ++nb) own[nb] = o[nb][tb];
+      } else {
+        const int slot = (tb - w - 1) & 3;
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) sm.num[buf][w][slot][nb][l] = o[nb][tb];
+        if (g == 0) sm.den[buf][w][slot][c16] = o[4][tb][0];
+      }
+    }
+
+    // stage the next tile into the other buffer and start loading the one after
+    if (t0 + 64 < r1) {
+      stage_causal_tile(sm.tile[buf ^ 1], rg, rq, t0 + 64, r1, s2half, cM, eps);
+      if (t0 + 128 < r1) {
+        load_tile_regs<bf16>(rg, Kh, Vh, t0 + 128, r1);
+        load_q_rows(rq, Qh, t0 + 128, r1);
+      }
+    }
+    __syncthreads();
+
+    // tokens 16 w .. 16 w + 15: sum the four partials, normalise, store
+    {
+      f32x4 part[3][4];   // the other waves' partials, all loads issued together
+      float pden[3];
+#pragma unroll
+      for (int k = 1; k < 4; ++k) {
+        const int src = (w + k) & 3;         // source wave
+        const int slot = (w - src - 1) & 3;  // its slot for this wave's tokens
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) part[k - 1][nb] = sm.num[buf][src][slot][nb][l];
+        pden[k - 1] = sm.den[buf][src][slot][c16];
+      }
+      f32x4 num[4];
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) num[nb] = own[nb] + (part[0][nb] + part[1][nb] + part[2][nb]);
+      const float den = own[4][0] + (pden[0] + pden[1] + pden[2]);
+      const int qt = t0 + 16 * w + c16;
+      if (qt < r1) {
+        const float inv = 1.0f / (den + my_epsq);
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp)
+          store8(Oh + (size_t)qt * kD + 32 * pp + 8 * g, num[2 * pp] * inv, num[2 * pp + 1] * inv);
+      }
+    }
+  }
+}
+
 hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
                            float *state_out, float *total, hipStream_t st) {
   const int n = sh.M * 65;
   dim3 grid((n + 255) / 256, sh.BH);
   hipLaunchKernelGGL(k_seg_scan, grid, dim3(256), 0, st, part, nseg, n, state_in, state_out,
                      total);
+  return hipGetLastError();
+}
+
+template <typename To>
+static hipError_t causal_fs_typed(const Shape &sh, const void *Q, const void *K, const void *V,
+                                  const void *wfr, const float *bq, const float *prefix, void *o,
+                                  int seg_len, int nseg, hipStream_t st) {
+  dim3 grid(nseg * sh.BH);
+#define FAVOR_CAUSAL_FS_LAUNCH(MM)                                                          \
+  hipLaunchKernelGGL((k_causal_fs<To, MM>), grid, dim3(256), 0, st, (const bf16 *)Q,          \
+                     (const bf16 *)K, (const bf16 *)V, (const bf16x8 *)wfr, bq, prefix,        \
+                     (To *)o, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps)
+  switch (sh.M) {
+    case 64: FAVOR_CAUSAL_FS_LAUNCH(64); break;
+    case 128: FAVOR_CAUSAL_FS_LAUNCH(128); break;
+    case 256: FAVOR_CAUSAL_FS_LAUNCH(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef FAVOR_CAUSAL_FS_LAUNCH
   return hipGetLastError();
 }
 
@@ -344,8 +767,8 @@ hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const vo
                          void *o, int seg_len, int nseg, hipStream_t st) {
   if (in == Dt::BF16)
     return out == Dt::BF16
-               ? causal_typed<bf16, bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st)
-               : causal_typed<bf16, float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st);
+               ? causal_fs_typed<bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st)
+               : causal_fs_typed<float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st);
   return out == Dt::BF16
              ? causal_typed<float, bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st)
              : causal_typed<float, float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st);

@@ -35,6 +35,9 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
+// the causal pass holds a whole compute unit per workgroup (LDS and registers),
+// so its segments are sized for one workgroup per CU
+constexpr int kCausalWorkgroups = 256;
 constexpr int kMinRowsPerSplit = 256;
 
 enum Op { kOpFeatureMap = 0, kOpBidir = 1, kOpCausal = 2, kOpBoth = 3 };
@@ -92,7 +95,8 @@ Plan make_plan(const favor_desc *g, int op) {
   if (causal && g->chunk > 0) {
     rows = g->chunk;
   } else {
-    int want = (kTargetWorkgroups + p.BH - 1) / p.BH;
+    const int target = causal ? kCausalWorkgroups : kTargetWorkgroups;
+    int want = (target + p.BH - 1) / p.BH;
     int max_split = tiles / (kMinRowsPerSplit / 64);
     if (max_split < 1) max_split = 1;
     if (want > max_split) want = max_split;

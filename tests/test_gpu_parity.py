@@ -137,6 +137,8 @@ CAUSAL_CASES = [
     (1, 1, 1, 128, "f32", 0),
     (2, 1, 200, 64, "f32", 128),
     (1, 1, 4096, 256, "bf16", 0),
+    (1, 2, 777, 128, "bf16", 0),
+    (2, 1, 300, 128, "bf16", 128),
 ]
 
 
@@ -150,6 +152,18 @@ def test_causal_parity(B, H, L, M, dtype, chunk):
                          to_dev(b), S64, chunk=chunk)
     torch.cuda.synchronize()
     parity(to_host(out), Q, K, V, W, b, S64, True, dtype)
+
+
+@pytest.mark.parametrize("M", [256, 64])
+def test_causal_denominator_stabiliser_bf16(M):
+    import torch
+    fv = _fv()
+    Q, K, V = _qkv(1, 2, 300, "bf16", seed=7)
+    W, b = _features(7, 2, M)
+    out = fv.attn_causal(to_dev(Q, "bf16"), to_dev(K, "bf16"), to_dev(V, "bf16"), to_dev(W),
+                         to_dev(b), S64, denom_eps=0.5)
+    torch.cuda.synchronize()
+    parity(to_host(out), Q, K, V, W, b, S64, True, "bf16", eps=0.5)
 
 
 def test_causal_state_carry_over():
