@@ -11,10 +11,15 @@ nothing is skipped inside the timed region.
 
 value = B*H*L / (seconds per step): token-heads per second through the whole
 step (each token-head goes through the draw, both directions), from a timed
-region without per-launch instrumentation. An identical region follows in which
-the library brackets every launch with HIP events on its stream; it gives the
-per-kernel durations and the roofline entry for the dominant kernel. The line
-also carries the fp64 CPU oracle timed on this host (cpu_baseline).
+region without per-launch instrumentation. In that region the features of step
+i + 1 are drawn on a second stream while step i attends with its own (two
+feature buffers, ordered by events), as a training loop that redraws features
+every step would run; the region holds exactly one draw and one attention pass
+per step. ms_per_step_serial times the same steps with the draw in line on one
+stream. A third region, serial, with every launch bracketed by HIP events on its
+stream, gives the per-kernel durations and the roofline entry for the dominant
+kernel. The line also carries the fp64 CPU oracle timed on this host
+(cpu_baseline).
 """
 import argparse
 import json
@@ -146,7 +151,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FAVOR path "
-              "shards over heads with no communication, see DESIGN.md", file=sys.stderr)
+              "shards over heads with no communication between GPUs", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -165,50 +170,94 @@ def main():
     Qd, Kd, Vd = up(Q), up(K), up(V)
     s = w.input_scale
     H, M = w.H, w.M
-    Wd = torch.empty((H, M, w.d), dtype=torch.float32, device=dev)
-    bd = torch.empty((H, M), dtype=torch.float32, device=dev)
+    # two random-feature buffers: a step reads slot i % 2 while the next step's
+    # features are drawn into the other one
+    Wd = [torch.empty((H, M, w.d), dtype=torch.float32, device=dev) for _ in range(2)]
+    bd = [torch.empty((H, M), dtype=torch.float32, device=dev) for _ in range(2)]
     out_b = torch.empty_like(Qd)
     out_c = torch.empty_like(Qd)
     g = fv.make_desc(w.B, H, w.L, w.d, M, fv.BF16 if w.dtype == "bf16" else fv.F32,
                      fv.BF16 if w.dtype == "bf16" else fv.F32, s)
     op = {"bidir": 0, "causal": 1, "both": 2}[w.direction]
     ws = torch.empty(fv.workspace_size(g, op), dtype=torch.uint8, device=dev)
+    s_main = torch.cuda.current_stream()
+    s_draw = torch.cuda.Stream()   # default priority, like every stream here
+    ev_draw = [torch.cuda.Event(), torch.cuda.Event()]   # slot k drawn
+    ev_attn = [torch.cuda.Event(), torch.cuda.Event()]   # attention done reading slot k
 
-    def step(i):
-        fv.orf_draw(1000 + i, H, M, w.d, W=Wd, b=bd)
+    def attention(slot):
         if op == 2:     # one key pass serves both directions
-            fv.attn_both(Qd, Kd, Vd, Wd, bd, s, out_bidir=out_b, out_causal=out_c, workspace=ws)
+            fv.attn_both(Qd, Kd, Vd, Wd[slot], bd[slot], s, out_bidir=out_b, out_causal=out_c,
+                         workspace=ws, stream=s_main)
         elif op == 0:
-            fv.attn_bidir(Qd, Kd, Vd, Wd, bd, s, out=out_b, workspace=ws)
+            fv.attn_bidir(Qd, Kd, Vd, Wd[slot], bd[slot], s, out=out_b, workspace=ws, stream=s_main)
         else:
-            fv.attn_causal(Qd, Kd, Vd, Wd, bd, s, out=out_c, workspace=ws)
+            fv.attn_causal(Qd, Kd, Vd, Wd[slot], bd[slot], s, out=out_c, workspace=ws,
+                           stream=s_main)
 
-    def timed_region(instrumented, first):
-        """Time args.steps steps with events on the launch stream (torch's current
-        stream, which the library launches on)."""
+    def step_serial(i):
+        """Draw this step's features, then attend with them (one stream)."""
+        fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
+        attention(0)
+
+    def prime(i):
+        """Draw the features of step i ahead of the pipelined steps."""
+        for e in ev_attn:
+            e.record(s_main)
+        s_draw.wait_stream(s_main)
+        fv.orf_draw(1000 + i, H, M, w.d, W=Wd[i & 1], b=bd[i & 1], stream=s_draw)
+        ev_draw[i & 1].record(s_draw)
+
+    def step_pipelined(i):
+        """Attend with the features drawn during step i - 1 while the second stream
+        draws those of step i + 1 into the other slot."""
+        slot, nxt = i & 1, (i & 1) ^ 1
+        s_draw.wait_event(ev_attn[nxt])       # step i - 1 no longer reads slot nxt
+        fv.orf_draw(1000 + i + 1, H, M, w.d, W=Wd[nxt], b=bd[nxt], stream=s_draw)
+        ev_draw[nxt].record(s_draw)
+        s_main.wait_event(ev_draw[slot])      # this step's features are ready
+        attention(slot)
+        ev_attn[slot].record(s_main)
+
+    def timed_region(step, first, instrumented=False, last_draw=None):
+        """Time args.steps steps with events on the main stream (the library launches
+        on the stream it is given). A pipelined region also waits for the draw it
+        issued in its last step, so it holds exactly args.steps draws."""
         torch.cuda.synchronize()
         if instrumented:
             fv.timing_reset()
             fv.timing_enable(True)
-        stream = torch.cuda.current_stream()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+        e0.record(s_main)
         for i in range(args.steps):
             step(first + i)
-        e1.record(stream)
+        if last_draw is not None:
+            s_main.wait_event(last_draw((first + args.steps) & 1))
+        e1.record(s_main)
         torch.cuda.synchronize()
         if instrumented:
             fv.timing_enable(False)
         return e0.elapsed_time(e1) / args.steps
 
     for i in range(args.warmup):
-        step(i)
-    # headline: no per-launch instrumentation (each event record adds a gap of a few
-    # microseconds between launches)
-    ms_step = timed_region(False, args.warmup)
-    # per-kernel durations: an identical region with every launch bracketed by events
-    ms_step_instrumented = timed_region(True, args.warmup + args.steps)
+        step_serial(i)
+    first = args.warmup
+    prime(first)
+    for i in range(args.warmup):
+        step_pipelined(first + i)
+    first += args.warmup
+    torch.cuda.synchronize()
+    prime(first)
+    # headline: the pipelined loop, no per-launch instrumentation (each event record
+    # adds a gap of a few microseconds between launches)
+    ms_step = timed_region(step_pipelined, first, last_draw=lambda k: ev_draw[k])
+    first += args.steps
+    # the same steps with the draw in line, on one stream
+    ms_step_serial = timed_region(step_serial, first)
+    first += args.steps
+    # per-kernel durations: serial steps with every launch bracketed by events
+    ms_step_instrumented = timed_region(step_serial, first, instrumented=True)
     kt = fv.timing_read()
     kernels = {k: {"ms_per_launch": v[0] / v[1], "launches_per_step": v[1] / args.steps}
                for k, v in kt.items() if v[1] > 0}
@@ -252,8 +301,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": M,
                    "direction": w.direction, "orf_draw_per_step": True,
+                   "orf_draw": "drawn one step ahead on a second stream",
                    "parallelism": "single GPU"},
         "kernels": kernels,
+        "ms_per_step_serial": ms_step_serial,
         "ms_per_step_instrumented": ms_step_instrumented,
         "roofline": roof,
     }

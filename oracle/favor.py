@@ -6,7 +6,7 @@ Shapes: Q, K, V are [..., L, d] (leading axes are batch and head); W is
 [H, M, d] and b is [H, M], one draw per head shared across the batch. When the
 inputs carry a head axis (axis -3) W and b broadcast over it.
 
-Readings of points the paper leaves open (each is restated in the design doc):
+Readings of points the paper leaves open:
   * Gaussian-kernel features use omega ~ N(0, I_d) acting on the scaled input
     x~ = s x (s = input_scale; s = d^-1/4 gives the paper's exp(QK^T / sqrt d)).
     With s = d^-1/4 this is the same as omega ~ N(0, sigma^-2 I) on raw x with

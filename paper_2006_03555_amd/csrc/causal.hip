@@ -25,6 +25,8 @@
 //   same work, keys after the query are zeroed), and writes normalised rows.
 // Keys, values and queries of the next chunk are loaded while this one is
 // computed.
+#include <type_traits>
+
 #include "favor_common.hpp"
 #include "kernels.hpp"
 #include "tile_common.hpp"
@@ -324,6 +326,15 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 //   pi(nb, r) = 32 (nb / 2) + 8 (r / 4) + 4 (nb % 2) + r % 4,
 // so that the lane holding rows 4 g .. 4 g + 3 of blocks 2 p and 2 p + 1 holds
 // the eight consecutive output columns 32 p + 8 g .. 32 p + 8 g + 7.
+// Calls f(integral_constant<int, I>) for I = B .. E - 1 in order.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 struct CausalFsTile {
   KVTile<bf16> kv;               // keys row-major, C~ (permuted columns) and D_K fragments
   bf16 Qs[64][kD + kKsPad];      // queries row-major (B operand of the query projection)
@@ -531,63 +542,144 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   }
   __syncthreads();
 
+  // tokens 16 w .. 16 w + 15 of the previous chunk: sum the four partials (this
+  // wave's own and three handed over in buffer xb), normalise, store
+  f32x4 own[5];
+  float own_epsq = 0.f;
+  auto finalize = [&](int tp, int xb) __attribute__((always_inline)) {
+    f32x4 part[3][4];   // the other waves' partials, all loads issued together
+    float pden[3];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      const int src = (w + k) & 3;         // source wave
+      const int slot = (w - src - 1) & 3;  // its slot for this wave's tokens
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) part[k - 1][nb] = sm.num[xb][src][slot][nb][l];
+      pden[k - 1] = sm.den[xb][src][slot][c16];
+    }
+    f32x4 num[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) num[nb] = own[nb] + (part[0][nb] + part[1][nb] + part[2][nb]);
+    const float den = own[4][0] + (pden[0] + pden[1] + pden[2]);
+    const int qt = tp + 16 * w + c16;
+    if (qt < r1) {
+      const float inv = 1.0f / (den + own_epsq);
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp)
+        store8(Oh + (size_t)qt * kD + 32 * pp + 8 * g, num[2 * pp] * inv, num[2 * pp + 1] * inv);
+    }
+  };
+
+  // Chunk c: stage tile c + 1 (its loads were issued during chunk c - 1) and
+  // load tile c + 2; form the features of chunk c; finalise chunk c - 1 (its
+  // partials were handed over before the last barrier); the contractions of
+  // chunk c; hand its partials over; barrier. The vector and LDS work of
+  // staging and finalising overlaps the matrix work of the chunk.
   int buf = 0;
   for (int t0 = r0; t0 < r1; t0 += 64, buf ^= 1) {
     const CausalFsTile &tl = sm.tile[buf];
     const float my_epsq = (eps != 0.f) ? tl.epsq[16 * w + c16] : 0.f;
-
-    // query features of this wave's slice, transposed: qB[tb][ks] is the B operand
-    // (col = token 16 tb + c16, k = 32 features of step ks, chained order)
-    frag qB[4][KS];
-    frag qa[4][2];   // all query fragments of the tile, loaded together
-#pragma unroll
-    for (int tb = 0; tb < 4; ++tb) {
-      qa[tb][0] = load_frag<bf16>(&tl.Qs[16 * tb + c16][8 * g]);
-      qa[tb][1] = load_frag<bf16>(&tl.Qs[16 * tb + c16][32 + 8 * g]);
-    }
-#pragma unroll
-    for (int tb = 0; tb < 4; ++tb) {
-      f32x4 pr[MB];
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        pr[mb] = P::mma(wf[mb][0], qa[tb][0], bqv[mb]);
-        pr[mb] = P::mma(wf[mb][1], qa[tb][1], pr[mb]);
+    if (t0 + 64 < r1) {
+      stage_causal_tile(sm.tile[buf ^ 1], rg, rq, t0 + 64, r1, s2half, cM, eps);
+      if (t0 + 128 < r1) {
+        load_tile_regs<bf16>(rg, Kh, Vh, t0 + 128, r1);
+        load_q_rows(rq, Qh, t0 + 128, r1);
       }
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) pr[mb][j] = P::cos_rev(pr[mb][j]);
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        qB[tb][ks] = P::pack(pr[2 * ks], (2 * ks + 1 < MB) ? pr[2 * ks + 1] : zero4);
     }
+
+    // features of this wave's slice for the chunk's queries and keys: eight
+    // projection groups (query blocks tb, then key blocks tb), software-pipelined so
+    // that the matrix cores project group i + 1 while the vector unit takes the
+    // cosines of group i.
+    //   qB[tb][ks]  B operand: col = query 16 tb + c16, k = 32 features (chained)
+    //   kA[mb][s]   A operand: lane row = feature 16 mb + c16, k = keys 32 s .. (chained)
+    frag qB[4][KS];
+    frag kA[MB][2];
+    {
+      auto load_rows = [&](auto ic, frag (&r)[2]) __attribute__((always_inline)) {
+        constexpr int i = decltype(ic)::value;
+        const auto &src = (i < 4) ? tl.Qs : tl.kv.Ks;
+        r[0] = load_frag<bf16>(&src[16 * (i & 3) + c16][8 * g]);
+        r[1] = load_frag<bf16>(&src[16 * (i & 3) + c16][32 + 8 * g]);
+      };
+      auto project = [&](auto ic, const frag (&r)[2], f32x4 (&pr)[MB]) __attribute__((always_inline)) {
+        constexpr int i = decltype(ic)::value;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          if constexpr (i < 4) {   // C[m][t] = W'' q_t + b''
+            pr[mb] = P::mma(wf[mb][0], r[0], bqv[mb]);
+            pr[mb] = P::mma(wf[mb][1], r[1], pr[mb]);
+          } else {                 // C[t][m] = W'' k_t + b''
+            const float bb = bk[mb];
+            pr[mb] = P::mma(r[0], wf[mb][0], f32x4{bb, bb, bb, bb});
+            pr[mb] = P::mma(r[1], wf[mb][1], pr[mb]);
+          }
+        }
+      };
+      f32x4 kfh[MB];   // cosines of the first key block of a pair
+      auto finish = [&](auto ic, f32x4 (&pr)[MB]) __attribute__((always_inline)) {
+        constexpr int i = decltype(ic)::value;
+        constexpr int tb = i & 3;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pr[mb][j] = P::cos_rev(pr[mb][j]);
+        if constexpr (i < 4) {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            qB[tb][ks] = P::pack(pr[2 * ks], (2 * ks + 1 < MB) ? pr[2 * ks + 1] : zero4);
+        } else if constexpr ((tb & 1) == 0) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) kfh[mb] = pr[mb];
+        } else {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) kA[mb][tb >> 1] = P::pack(kfh[mb], pr[mb]);
+        }
+      };
+      frag rows0[2], rows1[2];
+      f32x4 pr0[MB], pr1[MB];
+      load_rows(std::integral_constant<int, 0>{}, rows0);
+      load_rows(std::integral_constant<int, 1>{}, rows1);
+      project(std::integral_constant<int, 0>{}, rows0, pr0);
+      static_for<1, 8>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int i = decltype(ic)::value;
+        auto &rn = (i & 1) ? rows0 : rows1;   // the buffer of group i + 1
+        auto &rc = (i & 1) ? rows1 : rows0;
+        auto &pc = (i & 1) ? pr1 : pr0;
+        auto &pp = (i & 1) ? pr0 : pr1;
+        if constexpr (i + 1 < 8) load_rows(std::integral_constant<int, i + 1>{}, rn);
+        project(ic, rc, pc);
+        finish(std::integral_constant<int, i - 1>{}, pp);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      finish(std::integral_constant<int, 7>{}, pr1);
+    }
+
+    if (t0 > r0) finalize(t0 - 64, buf ^ 1);
 
     // partial Buf2 (value columns and the denominator) over this slice: o[nb][tb]
     // holds rows pi(nb, 4 g + j), column = token 16 tb + c16; first Q-hat S with
     // the state before the chunk
     f32x4 o[5][4];
-    {
-      frag sA[5][KS];   // lane row = value column, k = m
 #pragma unroll
-      for (int nb = 0; nb < 5; ++nb)
+    for (int nb = 0; nb < 5; ++nb) {
+      frag sA[KS];   // lane row = value column, k = m
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          sA[nb][ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
+      for (int ks = 0; ks < KS; ++ks)
+        sA[ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
+      for (int tb = 0; tb < 4; ++tb) {
+        o[nb][tb] = P::mma(sA[0], qB[tb][0], zero4);
 #pragma unroll
-        for (int nb = 0; nb < 5; ++nb) {
-          o[nb][tb] = P::mma(sA[nb][0], qB[tb][0], zero4);
-#pragma unroll
-          for (int ks = 1; ks < KS; ++ks) o[nb][tb] = P::mma(sA[nb][ks], qB[tb][ks], o[nb][tb]);
-        }
+        for (int ks = 1; ks < KS; ++ks) o[nb][tb] = P::mma(sA[ks], qB[tb][ks], o[nb][tb]);
+      }
     }
 
-    // keys, one 32-token half at a time: features of the slice, folded into S
-    // (after the queries above used it), transposed to token rows on the matrix
-    // cores, then the intra-chunk part of that half: P^T[t'][t] = K-hat_t' .
-    // Q-hat_t over the slice for key blocks tb' <= tb (keys after the query
-    // zeroed) and C~^T P^T into o
+    // keys, one 32-token half at a time: fold into S (after the queries above
+    // used it), transpose to token rows on the matrix cores, then the
+    // intra-chunk part of that half: P^T[t'][t] = K-hat_t' . Q-hat_t over the
+    // slice for key blocks tb' <= tb (keys after the query zeroed) and C~^T P^T
+    // into o
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
       // C~ of the half: B operand of the state update and A operand of the
@@ -596,10 +688,6 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) vt[nb] = tl.kv.VtF[nb][sidx][l];
       const frag df = tl.kv.DF[sidx][g];
-      const frag a0[2] = {load_frag<bf16>(&tl.kv.Ks[32 * sidx + c16][8 * g]),
-                          load_frag<bf16>(&tl.kv.Ks[32 * sidx + 16 + c16][8 * g])};
-      const frag a1[2] = {load_frag<bf16>(&tl.kv.Ks[32 * sidx + c16][32 + 8 * g]),
-                          load_frag<bf16>(&tl.kv.Ks[32 * sidx + 16 + c16][32 + 8 * g])};
       frag kT[2][KS];   // A operand: lane row = token 32 sidx + 16 tbl + c16, k = 32 features
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -612,16 +700,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
             ct[1][hm] = zero4;
             continue;
           }
-          f32x4 kf[2];
-#pragma unroll
-          for (int tbl = 0; tbl < 2; ++tbl) {
-            const float bb = bk[mb];
-            f32x4 p = P::mma(a0[tbl], wf[mb][0], f32x4{bb, bb, bb, bb});
-            p = P::mma(a1[tbl], wf[mb][1], p);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) kf[tbl][j] = P::cos_rev(p[j]);
-          }
-          const frag a = P::pack(kf[0], kf[1]);   // lane row m, k = 32 tokens
+          const frag a = kA[mb][sidx];
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) accS[mb][nb] = P::mma(a, vt[nb], accS[mb][nb]);
           accS[mb][4] = P::mma(a, df, accS[mb][4]);
@@ -658,55 +737,23 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
     }
 
     // hand the partials of the other waves' tokens over; keep this wave's own
-    f32x4 own[5];
+#pragma unroll
+    for (int nb = 0; nb < 5; ++nb)
+      own[nb] = (w == 0) ? o[nb][0] : (w == 1) ? o[nb][1] : (w == 2) ? o[nb][2] : o[nb][3];
+    own_epsq = my_epsq;
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) {
-      if (tb == w) {
-#pragma unroll
-        for (int nb = 0; nb < 5; ++nb) own[nb] = o[nb][tb];
-      } else {
+      if (tb != w) {
         const int slot = (tb - w - 1) & 3;
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb) sm.num[buf][w][slot][nb][l] = o[nb][tb];
         if (g == 0) sm.den[buf][w][slot][c16] = o[4][tb][0];
       }
     }
-
-    // stage the next tile into the other buffer and start loading the one after
-    if (t0 + 64 < r1) {
-      stage_causal_tile(sm.tile[buf ^ 1], rg, rq, t0 + 64, r1, s2half, cM, eps);
-      if (t0 + 128 < r1) {
-        load_tile_regs<bf16>(rg, Kh, Vh, t0 + 128, r1);
-        load_q_rows(rq, Qh, t0 + 128, r1);
-      }
-    }
     __syncthreads();
-
-    // tokens 16 w .. 16 w + 15: sum the four partials, normalise, store
-    {
-      f32x4 part[3][4];   // the other waves' partials, all loads issued together
-      float pden[3];
-#pragma unroll
-      for (int k = 1; k < 4; ++k) {
-        const int src = (w + k) & 3;         // source wave
-        const int slot = (w - src - 1) & 3;  // its slot for this wave's tokens
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) part[k - 1][nb] = sm.num[buf][src][slot][nb][l];
-        pden[k - 1] = sm.den[buf][src][slot][c16];
-      }
-      f32x4 num[4];
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) num[nb] = own[nb] + (part[0][nb] + part[1][nb] + part[2][nb]);
-      const float den = own[4][0] + (pden[0] + pden[1] + pden[2]);
-      const int qt = t0 + 16 * w + c16;
-      if (qt < r1) {
-        const float inv = 1.0f / (den + my_epsq);
-#pragma unroll
-        for (int pp = 0; pp < 2; ++pp)
-          store8(Oh + (size_t)qt * kD + 32 * pp + 8 * g, num[2 * pp] * inv, num[2 * pp + 1] * inv);
-      }
-    }
   }
+  // the last chunk
+  if (r1 > r0) finalize(r0 + 64 * ((r1 - r0 - 1) / 64), buf ^ 1);
 }
 
 hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
