@@ -68,31 +68,67 @@ def _require_cuda(*ts):
 def orf_draw(seed, n_heads, M, d=64, kind=RF_ORTHO_CHI, W=None, b=None, stream=None):
     """Draw W [n_heads, M, d] and b [n_heads, M] on the GPU (favor_orf_draw)."""
     torch = _torch()
-    dev = torch.device("cuda", torch.cuda.current_device())
+    if W is None or b is None:
+        dev = torch.device("cuda", torch.cuda.current_device())
     if W is None:
         W = torch.empty((n_heads, M, d), dtype=torch.float32, device=dev)
     if b is None:
         b = torch.empty((n_heads, M), dtype=torch.float32, device=dev)
+    _require_features(W, b, n_heads, M, d)
     _require_cuda(W, b)
     _check(lib().favor_orf_draw(ctypes.c_uint64(seed), n_heads, M, d, kind, _ptr(W), _ptr(b),
                                 _stream(stream)))
     return W, b
 
 
-def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0):
+def _require_like(t, shape, dtype, name):
+    """A caller-supplied tensor must have exactly the shape and dtype the call
+    writes or reads (the kernels trust the descriptor, not the tensor)."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise FavorError(1, f"{name} must be {tuple(shape)} {dtype}, got {tuple(t.shape)} "
+                            f"{t.dtype}")
+
+
+def _require_features(W, b, H, M, d):
+    torch = _torch()
+    _require_like(W, (H, M, d), torch.float32, "W")
+    _require_like(b, (H, M), torch.float32, "b")
+
+
+def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0, others=()):
+    """Descriptor for inputs X [B, H, L, d] (and tensors `others` of the same shape
+    and dtype) with features W [H, M, d], b [H, M]."""
+    if X.dim() != 4:
+        raise FavorError(1, f"inputs must be [B, H, L, d], got {tuple(X.shape)}")
     B, H, L, d = X.shape
+    for name, t in others:
+        _require_like(t, X.shape, X.dtype, name)
+    if W.dim() != 3:
+        raise FavorError(1, f"W must be [H, M, d], got {tuple(W.shape)}")
     M = W.shape[1]
     in_code = _dtype_code(X.dtype)
     out_code = in_code if out_dtype is None else _dtype_code(out_dtype)
     return make_desc(B, H, L, d, M, in_code, out_code, input_scale, denom_eps, chunk)
 
 
+def _out_dtype(out_dtype, out, X):
+    """Output dtype: as given, else that of a supplied output tensor, else X's."""
+    if out_dtype is not None:
+        return out_dtype
+    return out.dtype if out is not None else X.dtype
+
+
 def feature_map(X, W, b, input_scale, out_dtype=None, out=None, stream=None):
     """X' = D_X X-hat [B, H, L, M] (favor_feature_map)."""
     torch = _torch()
-    g = _desc_for(X, W, input_scale, out_dtype)
+    g = _desc_for(X, W, input_scale, _out_dtype(out_dtype, out, X))
+    _require_features(W, b, g.H, g.M, g.d)
+    shape = (g.B, g.H, g.L, g.M)
     if out is None:
-        out = torch.empty((g.B, g.H, g.L, g.M), dtype=_torch_dtype(g.out_dtype), device=X.device)
+        out = torch.empty(shape, dtype=_torch_dtype(g.out_dtype), device=X.device)
+    _require_like(out, shape, _torch_dtype(g.out_dtype), "out")
     _require_cuda(X, W, b, out)
     _check(lib().favor_feature_map(ctypes.byref(g), _ptr(X), _ptr(W), _ptr(b), _ptr(out),
                                    _stream(stream)))
@@ -112,9 +148,12 @@ def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=No
                workspace=None, stream=None):
     """Bidirectional FAVOR, Algorithm 1 (favor_attn_bidir). Returns out [B, H, L, d]."""
     torch = _torch()
-    g = _desc_for(Q, W, input_scale, out_dtype, denom_eps)
+    g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps,
+                  others=(("K", K), ("V", V)))
+    _require_features(W, b, g.H, g.M, g.d)
     if out is None:
         out = torch.empty(Q.shape, dtype=_torch_dtype(g.out_dtype), device=Q.device)
+    _require_like(out, Q.shape, _torch_dtype(g.out_dtype), "out")
     _require_cuda(Q, K, V, W, b, out)
     ws, nbytes = _workspace(g, 0, workspace)
     _check(lib().favor_attn_bidir(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
@@ -129,11 +168,17 @@ def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return
     Returns out, or (out, state_out [B, H, M, d+1]) when return_state is true.
     """
     torch = _torch()
-    g = _desc_for(Q, W, input_scale, out_dtype, denom_eps, chunk)
+    g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps, chunk,
+                  others=(("K", K), ("V", V)))
+    _require_features(W, b, g.H, g.M, g.d)
+    sshape = (g.B, g.H, g.M, g.d + 1)
     if out is None:
         out = torch.empty(Q.shape, dtype=_torch_dtype(g.out_dtype), device=Q.device)
     if return_state and state_out is None:
-        state_out = torch.empty((g.B, g.H, g.M, g.d + 1), dtype=torch.float32, device=Q.device)
+        state_out = torch.empty(sshape, dtype=torch.float32, device=Q.device)
+    _require_like(out, Q.shape, _torch_dtype(g.out_dtype), "out")
+    _require_like(state_in, sshape, torch.float32, "state_in")
+    _require_like(state_out, sshape, torch.float32, "state_out")
     _require_cuda(Q, K, V, W, b, out, state_in, state_out)
     ws, nbytes = _workspace(g, 1, workspace)
     _check(lib().favor_attn_causal(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
@@ -150,14 +195,21 @@ def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_s
     Returns (out_bidir, out_causal) or (out_bidir, out_causal, state_out).
     """
     torch = _torch()
-    g = _desc_for(Q, W, input_scale, out_dtype, denom_eps, chunk)
+    g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out_bidir, Q), denom_eps, chunk,
+                  others=(("K", K), ("V", V)))
+    _require_features(W, b, g.H, g.M, g.d)
     odt = _torch_dtype(g.out_dtype)
+    sshape = (g.B, g.H, g.M, g.d + 1)
     if out_bidir is None:
         out_bidir = torch.empty(Q.shape, dtype=odt, device=Q.device)
     if out_causal is None:
         out_causal = torch.empty(Q.shape, dtype=odt, device=Q.device)
     if return_state and state_out is None:
-        state_out = torch.empty((g.B, g.H, g.M, g.d + 1), dtype=torch.float32, device=Q.device)
+        state_out = torch.empty(sshape, dtype=torch.float32, device=Q.device)
+    _require_like(out_bidir, Q.shape, odt, "out_bidir")
+    _require_like(out_causal, Q.shape, odt, "out_causal")
+    _require_like(state_in, sshape, torch.float32, "state_in")
+    _require_like(state_out, sshape, torch.float32, "state_out")
     _require_cuda(Q, K, V, W, b, out_bidir, out_causal, state_in, state_out)
     ws, nbytes = _workspace(g, 2, workspace)
     _check(lib().favor_attn_both(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),

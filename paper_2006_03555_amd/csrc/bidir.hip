@@ -119,7 +119,7 @@ __global__ __launch_bounds__(256) void k_finalize(const float *__restrict__ part
   const int nb = fi / NS;
   const int sidx = fi - nb * NS;
   const int g = l >> 4;
-  const int n = nb < 4 ? nb * 16 + (l & 15) : 64;
+  const int n = nb < 4 ? perm_col(nb, l & 15) : 64;   // lane row = value column (permuted)
   const float *src = part + (size_t)bh * nsplit * M * 65;
   float v[8];
 #pragma unroll
@@ -140,20 +140,6 @@ __global__ __launch_bounds__(256) void k_finalize(const float *__restrict__ part
 // Rows per workgroup: 4 waves x TBW blocks of 16 rows.
 template <typename T> struct QsideCfg { static constexpr int TBW = 4; };
 template <> struct QsideCfg<float> { static constexpr int TBW = 2; };
-
-// Contiguous range of work items for workgroup `id` of `nwg`: the items of
-// XCD x (ids congruent to x mod 8) form one contiguous block (xcd_item), split
-// evenly over that XCD's workgroups, so a workgroup's items are consecutive
-// tiles of mostly one head.
-__device__ __forceinline__ void xcd_range(int id, int nwg, int n, int &begin, int &end) {
-  const int x = id & 7;
-  const int k = id >> 3;
-  const int nw = (nwg >> 3) + (x < (nwg & 7) ? 1 : 0);
-  const int cnt = (n >> 3) + (x < (n & 7) ? 1 : 0);
-  const int base = x * (n >> 3) + min(x, n & 7);
-  begin = base + (int)((long long)k * cnt / nw);
-  end = base + (int)((long long)(k + 1) * cnt / nw);
-}
 
 // Query fragments of one tile for this wave: rows rbase + 16 tb + lane % 16.
 template <typename T, int TBW>
@@ -289,9 +275,11 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
       const int t = rbase + tb * 16 + c16;
       if (t < L) {
         const float inv = 1.0f / (acc[4][tb][0] + epsq[tb]);
+        // blocks 2 p, 2 p + 1 hold value columns 32 p + 8 g .. + 7 in this lane
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-          store4(Oh + (size_t)t * kD + nb * 16 + 4 * g, acc[nb][tb] * inv);
+        for (int pp = 0; pp < 2; ++pp)
+          store8(Oh + (size_t)t * kD + 32 * pp + 8 * g, acc[2 * pp][tb] * inv,
+                 acc[2 * pp + 1][tb] * inv);
       }
     }
   }

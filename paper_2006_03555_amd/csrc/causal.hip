@@ -346,10 +346,6 @@ struct CausalFsSmem {
   float den[2][4][3][16];        // [buffer][source wave][slot][token]
 };
 
-__device__ __forceinline__ int perm_col(int nb, int r) {
-  return 32 * (nb >> 1) + 8 * (r >> 2) + 4 * (nb & 1) + (r & 3);
-}
-
 // Selection matrix in loaded k order with B[k][c] = (k == 8 (c / 4) + 4 half + c % 4):
 // the MFMA of value rows (A operand, k = 32 value columns of step kh) with it
 // moves value column 32 kh + 8 (c / 4) + 4 half + c % 4 = pi(2 kh + half, c) to lane c.
@@ -446,18 +442,6 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
     qn = quad_sum_f32(qn);
     if ((tid & 3) == 0) tl.epsq[tr] = (t0 + tr < r1) ? eps / (cM * expf(s2half * qn)) : 0.f;
   }
-}
-
-// Eight consecutive output elements from two fp32 quadruples.
-__device__ __forceinline__ void store8(bf16 *p, f32x4 a, f32x4 b) {
-  bf16x8 r;
-  r[0] = (bf16)a[0]; r[1] = (bf16)a[1]; r[2] = (bf16)a[2]; r[3] = (bf16)a[3];
-  r[4] = (bf16)b[0]; r[5] = (bf16)b[1]; r[6] = (bf16)b[2]; r[7] = (bf16)b[3];
-  *reinterpret_cast<bf16x8 *>(p) = r;
-}
-__device__ __forceinline__ void store8(float *p, f32x4 a, f32x4 b) {
-  *reinterpret_cast<f32x4 *>(p) = a;
-  *reinterpret_cast<f32x4 *>(p + 4) = b;
 }
 
 template <typename To, int M>

@@ -137,6 +137,28 @@ __device__ __forceinline__ void store4(bf16 *p, f32x4 v) {
 }
 __device__ __forceinline__ void store4(float *p, f32x4 v) { *reinterpret_cast<f32x4 *>(p) = v; }
 
+// Eight consecutive output elements from two fp32 quadruples.
+__device__ __forceinline__ void store8(bf16 *p, f32x4 a, f32x4 b) {
+  bf16x8 r;
+  r[0] = (bf16)a[0]; r[1] = (bf16)a[1]; r[2] = (bf16)a[2]; r[3] = (bf16)a[3];
+  r[4] = (bf16)b[0]; r[5] = (bf16)b[1]; r[6] = (bf16)b[2]; r[7] = (bf16)b[3];
+  *reinterpret_cast<bf16x8 *>(p) = r;
+}
+__device__ __forceinline__ void store8(float *p, f32x4 a, f32x4 b) {
+  *reinterpret_cast<f32x4 *>(p) = a;
+  *reinterpret_cast<f32x4 *>(p + 4) = b;
+}
+
+// Value-column order of the output-side operands (Buf1^T fragments, the causal
+// value tiles and state): row r of 16-column block nb is value column
+//   pi(nb, r) = 32 (nb / 2) + 8 (r / 4) + 4 (nb % 2) + r % 4,
+// so that a lane holding rows 4 g .. 4 g + 3 of output blocks 2 p and 2 p + 1
+// holds the eight consecutive columns 32 p + 8 g .. 32 p + 8 g + 7 (one 16-byte
+// store in bf16).
+__device__ __forceinline__ int perm_col(int nb, int r) {
+  return 32 * (nb >> 1) + 8 * (r >> 2) + 4 * (nb & 1) + (r & 3);
+}
+
 // Chained slot of logical k index r in [0, 32): k = 16 h + 4 g + i'  ->  (g, slot 4h + i').
 __device__ __forceinline__ int chained_group(int r) { return (r & 15) >> 2; }
 __device__ __forceinline__ int chained_slot(int r) { return ((r >> 4) << 2) | (r & 3); }

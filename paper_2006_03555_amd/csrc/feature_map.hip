@@ -1,87 +1,181 @@
 // feature_map.hip - the random-feature map X' = D_X X-hat (Sec. 2.3, Eqs. dqdk
 // and qkprime) materialised in HBM.
 //
-// One workgroup handles 64 * TBW rows of one head; the projection W'' x is a
-// matrix-core product in transposed orientation (result lane = row, 4
-// consecutive features per lane), seeded with b'' so the epilogue is
-// cos(2 pi acc) * D_X(row) * sqrt(2/M) followed by a 4-element store. The
-// kernel is bound by writing X' (M elements per row against d read).
+// The projection W'' x is a matrix-core product in transposed orientation
+// (result lane = row), seeded with b'' so the epilogue is cos(2 pi acc) *
+// D_X(row) * sqrt(2/M). The kernel is bound by writing X' (M elements per row
+// against d read), so the W'' rows are ordered for whole-line stores: with bf16
+// output row r of 16-feature block mb is feature perm_col(mb, r) (each lane
+// then holds two runs of 8 consecutive features of its row and every 16-byte
+// store instruction writes 64 contiguous bytes per row); with fp32 output the
+// natural order already gives 16 contiguous bytes per lane and 64 per row.
 #include "favor_common.hpp"
 #include "kernels.hpp"
 #include "tile_common.hpp"
 
 namespace favor {
 
-template <typename T> struct FmapCfg { static constexpr int TBW = 4; };
+// Rows per work item: 4 waves x TBW blocks of 16 rows.
+template <typename T> struct FmapCfg { static constexpr int TBW = 2; };
 template <> struct FmapCfg<float> { static constexpr int TBW = 2; };
+// workgroups launched (measured best on 256 CUs: one per CU when writing bf16,
+// two when writing fp32)
+template <typename To> struct FmapGrid { static constexpr int kWorkgroups = 256; };
+template <> struct FmapGrid<float> { static constexpr int kWorkgroups = 512; };
 
+template <typename To>
+__device__ __forceinline__ int fmap_row(int mb, int r) {
+  if constexpr (sizeof(To) == 2) return perm_col(mb, r);
+  return 16 * mb + r;
+}
+
+// W'' A-operand fragments in the store order above and b'' (natural order)
+// into LDS, cooperatively (256 threads, all global loads in flight).
 template <typename T, typename To, int M>
-__global__ __launch_bounds__(256) void k_feature_map(const T *__restrict__ X,
+__device__ __forceinline__ void fill_w_afrags_perm(typename Mma<T>::frag (*WA)[2][64], float *bq,
+                                                   const float *__restrict__ Wh,
+                                                   const float *__restrict__ bh, float ws) {
+  constexpr int N = (M / 16) * 2 * 64;
+  constexpr int NB = (N / 256) < 4 ? (N / 256) : 4;   // loads in flight per batch
+  static_assert(N % (256 * NB) == 0, "256 threads");
+#pragma unroll
+  for (int it0 = 0; it0 < N / 256; it0 += NB) {
+    float v[NB][8];
+#pragma unroll
+    for (int it = 0; it < NB; ++it) {
+      const int idx = (it0 + it) * 256 + threadIdx.x;
+      const int m = fmap_row<To>(idx >> 7, idx & 15);
+      load8_f32(Wh + (size_t)m * kD + ((idx >> 6) & 1) * 32 + 8 * ((idx & 63) >> 4), v[it]);
+    }
+#pragma unroll
+    for (int it = 0; it < NB; ++it) {
+      const int idx = (it0 + it) * 256 + threadIdx.x;
+      WA[idx >> 7][(idx >> 6) & 1][idx & 63] = Mma<T>::from_f32(v[it], ws);
+    }
+  }
+  if (threadIdx.x < M) bq[threadIdx.x] = bh[threadIdx.x] * kInv2Pi;
+}
+
+// The four result tiles of 64 features for one row: bf16 lanes hold features
+// 8 g .. 8 g + 7 (tiles 0, 1) and 32 + 8 g .. (tiles 2, 3) of the 64; fp32 lanes
+// hold 16 k + 4 g .. 16 k + 4 g + 3 in tile k.
+__device__ __forceinline__ void store_row64(bf16 *p, int g, const f32x4 (&v)[4]) {
+  store8(p + 8 * g, v[0], v[1]);
+  store8(p + 32 + 8 * g, v[2], v[3]);
+}
+__device__ __forceinline__ void store_row64(float *p, int g, const f32x4 (&v)[4]) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) *reinterpret_cast<f32x4 *>(p + 16 * k + 4 * g) = v[k];
+}
+
+// Persistent: workgroup i takes an XCD-local range of (head, row tile) items,
+// loads the head's W'' when the head changes, and prefetches the next tile's
+// rows while the current one is projected and written.
+template <typename T, typename To, int M>
+__global__ __launch_bounds__(256, sizeof(T) == 2 ? 4 : 2) void k_feature_map(const T *__restrict__ X,
                                                      const float *__restrict__ W,
                                                      const float *__restrict__ bph,
                                                      To *__restrict__ Xp, int H, int L, float s,
-                                                     int ntiles) {
+                                                     int ntiles, int nitems) {
   constexpr int TBW = FmapCfg<T>::TBW;
   using P = Mma<T>;
   using frag = typename P::frag;
   __shared__ frag WA[M / 16][2][64];
   __shared__ float bq[M];
 
-  const int item = xcd_item(blockIdx.x, gridDim.x);
-  const int bh = item / ntiles;
-  const int tile = item - bh * ntiles;
-  const int h = bh % H;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
-
-  fill_w_afrags<T, M>(WA, bq, W + (size_t)h * M * kD, bph + (size_t)h * M, s * kInv2Pi);
-
-  const int rbase = tile * (64 * TBW) + w * (16 * TBW);
-  const T *Xh = X + (size_t)bh * L * kD;
-  frag xf[TBW][2];
-  float dfac[TBW];
   const float cM = sqrtf(2.0f / M);
+  const float s2half = 0.5f * s * s;
+
+  int begin, end;
+  xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
+  if (begin >= end) return;
+
+  // rows rbase + 16 tb + c16 of an item, columns 8 g .. and 32 + 8 g ..
+  auto load_rows = [&](int item, frag (&xf)[TBW][2]) {
+    const int bh = item / ntiles;
+    const int rbase = (item - bh * ntiles) * (64 * TBW) + w * (16 * TBW);
+    const T *Xh = X + (size_t)bh * L * kD;
 #pragma unroll
-  for (int tb = 0; tb < TBW; ++tb) {
-    const int t = rbase + tb * 16 + c16;
-    float nrm = 0.f;
-    if (t < L) {
+    for (int tb = 0; tb < TBW; ++tb) {
+      const int t = rbase + tb * 16 + c16;
+      if (t < L) {
+        xf[tb][0] = load_frag<T>(Xh + (size_t)t * kD + 8 * g);
+        xf[tb][1] = load_frag<T>(Xh + (size_t)t * kD + 32 + 8 * g);
+      } else {
+        xf[tb][0] = P::splat(0.f);
+        xf[tb][1] = P::splat(0.f);
+      }
+    }
+  };
+
+  frag xn[TBW][2];
+  load_rows(begin, xn);
+  int cur = -1;
+  for (int item = begin; item < end; ++item) {
+    const int bh = item / ntiles;
+    if (bh != cur) {   // the head's W'' fragments and b''
+      const int h = bh % H;
+      __syncthreads();
+      fill_w_afrags_perm<T, To, M>(WA, bq, W + (size_t)h * M * kD, bph + (size_t)h * M,
+                                   s * kInv2Pi);
+      __syncthreads();
+      cur = bh;
+    }
+    frag xf[TBW][2];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        xf[tb][ks] = load_frag<T>(Xh + (size_t)t * kD + ks * 32 + 8 * g);
+    for (int tb = 0; tb < TBW; ++tb) {
+      xf[tb][0] = xn[tb][0];
+      xf[tb][1] = xn[tb][1];
+    }
+    if (item + 1 < end) load_rows(item + 1, xn);
+
+    // D_X(row) sqrt(2/M) = sqrt(2/M) exp(||s x||^2 / 2)
+    float dfac[TBW];
+#pragma unroll
+    for (int tb = 0; tb < TBW; ++tb) {
+      float nrm = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const float x = to_f32(xf[tb][ks][i]);
           nrm = fmaf(x, x, nrm);
         }
-      }
-    } else {
-      xf[tb][0] = P::splat(0.f);
-      xf[tb][1] = P::splat(0.f);
+      nrm += __shfl_xor(nrm, 16);
+      nrm += __shfl_xor(nrm, 32);
+      dfac[tb] = cM * expf(s2half * nrm);
     }
-    nrm += __shfl_xor(nrm, 16);
-    nrm += __shfl_xor(nrm, 32);
-    dfac[tb] = cM * expf(0.5f * s * s * nrm);
-  }
-  __syncthreads();
 
-  To *Oh = Xp + (size_t)bh * L * M;
-  for (int mb = 0; mb < M / 16; ++mb) {
-    const frag a0 = WA[mb][0][l];
-    const frag a1 = WA[mb][1][l];
-    const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&bq[mb * 16 + 4 * g]);
+    const int rbase = (item - bh * ntiles) * (64 * TBW) + w * (16 * TBW);
+    To *Oh = Xp + (size_t)bh * L * M;
+    for (int q = 0; q < M / 64; ++q) {   // features 64 q .. 64 q + 63
+      frag a[4][2];
+      f32x4 bcv[4];   // b'' of result rows 4 g + j of tile k (in store order)
 #pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-      f32x4 p = P::mma(a0, xf[tb][0], bcv);
-      p = P::mma(a1, xf[tb][1], p);
-      f32x4 v;
+      for (int k = 0; k < 4; ++k) {
+        a[k][0] = WA[4 * q + k][0][l];
+        a[k][1] = WA[4 * q + k][1][l];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = P::cos_rev(p[j]) * dfac[tb];
-      const int t = rbase + tb * 16 + c16;
-      if (t < L) store4(Oh + (size_t)t * M + mb * 16 + 4 * g, v);
+        for (int j = 0; j < 4; ++j) bcv[k][j] = bq[fmap_row<To>(4 * q + k, 4 * g + j)];
+      }
+#pragma unroll
+      for (int tb = 0; tb < TBW; ++tb) {
+        f32x4 v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          f32x4 p = P::mma(a[k][0], xf[tb][0], bcv[k]);
+          p = P::mma(a[k][1], xf[tb][1], p);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[k][j] = P::cos_rev(p[j]) * dfac[tb];
+        }
+        const int t = rbase + tb * 16 + c16;
+        if (t < L) store_row64(Oh + (size_t)t * M + 64 * q, g, v);
+      }
     }
   }
 }
@@ -91,19 +185,21 @@ static hipError_t fmap_typed(const Shape &sh, const void *X, const float *W, con
                              void *Xp, hipStream_t st) {
   const int rows = 64 * FmapCfg<T>::TBW;
   const int ntiles = (sh.L + rows - 1) / rows;
-  dim3 grid(ntiles * sh.BH);
+  const int nitems = ntiles * sh.BH;
+  const int cap = FmapGrid<To>::kWorkgroups;
+  dim3 grid(nitems < cap ? nitems : cap);
   switch (sh.M) {
     case 64:
       hipLaunchKernelGGL((k_feature_map<T, To, 64>), grid, dim3(256), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s, ntiles);
+                         (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
       break;
     case 128:
       hipLaunchKernelGGL((k_feature_map<T, To, 128>), grid, dim3(256), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s, ntiles);
+                         (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
       break;
     case 256:
       hipLaunchKernelGGL((k_feature_map<T, To, 256>), grid, dim3(256), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s, ntiles);
+                         (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
       break;
     default:
       return hipErrorInvalidValue;

@@ -289,4 +289,18 @@ __device__ __forceinline__ int xcd_item(int id, int n) {
   return x * per + min(x, rem) + k;
 }
 
+// Contiguous range of work items for workgroup `id` of `nwg`: the items of
+// XCD x (ids congruent to x mod 8) form one contiguous block (xcd_item), split
+// evenly over that XCD's workgroups, so a workgroup's items are consecutive
+// tiles of mostly one head.
+__device__ __forceinline__ void xcd_range(int id, int nwg, int n, int &begin, int &end) {
+  const int x = id & 7;
+  const int k = id >> 3;
+  const int nw = (nwg >> 3) + (x < (nwg & 7) ? 1 : 0);
+  const int cnt = (n >> 3) + (x < (n & 7) ? 1 : 0);
+  const int base = x * (n >> 3) + min(x, n & 7);
+  begin = base + (int)((long long)k * cnt / nw);
+  end = base + (int)((long long)(k + 1) * cnt / nw);
+}
+
 }  // namespace favor

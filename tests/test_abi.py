@@ -144,3 +144,30 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setenv("FAVOR_LIBRARY", str(tmp_path / "nope.so"))
     with pytest.raises(fv.FavorLibraryMissing):
         fv.lib()
+
+
+def test_binding_checks_tensor_shapes_and_dtypes():
+    """A caller-supplied tensor of the wrong shape or dtype is refused before any
+    launch (the kernels size their writes from the descriptor)."""
+    import torch
+    bf = torch.bfloat16
+    Q = torch.zeros((1, 2, 64, 64), dtype=bf)
+    W = torch.zeros((2, 128, 64))
+    b = torch.zeros((2, 128))
+    cases = [
+        (lambda: fv.feature_map(Q, W, b, 0.35, out_dtype=bf, out=torch.zeros((1, 2, 64, 128))),
+         "out"),
+        (lambda: fv.feature_map(Q, W, b, 0.35, out=torch.zeros((1, 2, 64, 64), dtype=bf)), "out"),
+        (lambda: fv.attn_bidir(Q, Q[:, :, :32], Q, W, b, 0.35), "K"),
+        (lambda: fv.attn_bidir(Q, Q, Q.float(), W, b, 0.35), "V"),
+        (lambda: fv.attn_bidir(Q, Q, Q, W, b[:1], 0.35), "b"),
+        (lambda: fv.attn_causal(Q, Q, Q, W, b, 0.35, state_in=torch.zeros((1, 2, 128, 64))),
+         "state_in"),
+        (lambda: fv.attn_both(Q, Q, Q, W, b, 0.35, out_causal=torch.zeros((1, 2, 64, 64))),
+         "out_causal"),
+        (lambda: fv.orf_draw(1, 2, 128, 64, W=torch.zeros((2, 128, 32)), b=b), "W"),
+    ]
+    for call, name in cases:
+        with pytest.raises(fv.FavorError) as e:
+            call()
+        assert name in str(e.value), (name, str(e.value))
