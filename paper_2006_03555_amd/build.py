@@ -19,7 +19,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfavor.so")
 ARCH = "gfx950"
 
-SOURCES = ["orf_draw.hip", "prep.hip", "feature_map.hip", "bidir.hip", "causal.hip", "favor_api.cpp",
+SOURCES = ["orf_draw.hip", "feature_map.hip", "bidir.hip", "causal.hip", "favor_api.cpp",
            "timing.cpp"]
 
 # Packed fp32 arithmetic is disabled for all device code (no v_pk_*_f32).

@@ -1,7 +1,9 @@
 // bidir.hip - bidirectional FAVOR (Sec. 2.5, Algorithm 1) on CDNA4 matrix cores.
 //
 // Three launches, none of which stores a feature matrix:
-//   k_kside     grid (splits * B*H). Each workgroup streams 64-token tiles of
+//   k_kside     grid (splits * B*H). Each wave converts its slice of W to
+//               W'' = (s / 2 pi) W fragments (one workgroup per head also stores
+//               them for the Q side). Each workgroup streams 64-token tiles of
 //               one head's K and V, rebuilds the key features K-hat on the
 //               matrix cores (projection + fused cosine), and accumulates its
 //               share of Buf1 = K'^T [V 1] in fp32 accumulators. D_K and the
@@ -24,11 +26,39 @@
 
 namespace favor {
 
+// W'' = (s / 2 pi) W fragments of this wave's feature blocks (B operand of the
+// key projection, lane col m) and b'' = b / 2 pi as accumulator seeds, built
+// from the fp32 draw; the workgroup of (batch 0, split 0) of each head also
+// stores the head's fragments and b'' for the launches that follow.
+template <typename T, int MB>
+__device__ __forceinline__ void build_w_bfrags(const float *__restrict__ Wh,
+                                               const float *__restrict__ bh, int mb0, float ws,
+                                               typename Mma<T>::frag (&Wf)[MB][2], f32x4 (&bC)[MB],
+                                               typename Mma<T>::frag *__restrict__ wfr_out,
+                                               float *__restrict__ bq_out) {
+  const int l = lane_id();
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = 16 * (mb0 + mb) + (l & 15);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      float v[8];
+      load8_f32(Wh + (size_t)m * kD + 32 * ks + 8 * (l >> 4), v);
+      Wf[mb][ks] = Mma<T>::from_f32(v, ws);
+      if (wfr_out) wfr_out[((mb0 + mb) * 2 + ks) * 64 + l] = Wf[mb][ks];
+    }
+    const float bb = bh[m] * kInv2Pi;
+    bC[mb] = f32x4{bb, bb, bb, bb};
+    if (bq_out && l < 16) bq_out[m] = bb;
+  }
+}
+
 template <typename T, int M>
 __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_kside(
-    const T *__restrict__ K, const T *__restrict__ V,
-    const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
-    float *__restrict__ part, int H, int L, int rows_per_split, int nsplit, float s) {
+    const T *__restrict__ K, const T *__restrict__ V, const float *__restrict__ W,
+    const float *__restrict__ b, typename Mma<T>::frag *__restrict__ wfr,
+    float *__restrict__ bqg, float *__restrict__ part, int H, int L, int rows_per_split,
+    int nsplit, float s) {
   const int item = xcd_item(blockIdx.x, gridDim.x);
   const int bh = item / nsplit;
   const int split = item - bh * nsplit;
@@ -49,7 +79,12 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_kside(
 
   frag Wf[MB][2];
   f32x4 bC[MB];
-  load_w_bfrags<T, MB>(wfr + (size_t)h * (M / 16) * 2 * 64, bqg + (size_t)h * M, w * MW, Wf, bC);
+  {
+    const bool writer = bh < H && split == 0;   // one workgroup per head
+    build_w_bfrags<T, MB>(W + (size_t)h * M * kD, b + (size_t)h * M, w * MB, s * kInv2Pi, Wf, bC,
+                          writer ? wfr + (size_t)h * (M / 16) * 2 * 64 : nullptr,
+                          writer ? bqg + (size_t)h * M : nullptr);
+  }
   frag sel[2] = {select_frag<T>(0), select_frag<T>(1)};
 
   f32x4 acc[MB][5];
@@ -294,20 +329,20 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
     default: return hipErrorInvalidValue;                           \
   }
 
-hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const void *wfr,
-                        const float *bq, float *part, int rows_per_split, int nsplit,
-                        hipStream_t st) {
+hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const float *W,
+                        const float *b, void *wfr, float *bq, float *part, int rows_per_split,
+                        int nsplit, hipStream_t st) {
   dim3 grid(nsplit * sh.BH);
   if (in == Dt::BF16) {
     FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<bf16, MM>), grid, dim3(256), 0, st,
-                                               (const bf16 *)K, (const bf16 *)V,
-                                               (const Mma<bf16>::frag *)wfr, bq, part, sh.H,
-                                               sh.L, rows_per_split, nsplit, sh.s));
+                                               (const bf16 *)K, (const bf16 *)V, W, b,
+                                               (Mma<bf16>::frag *)wfr, bq, part, sh.H, sh.L,
+                                               rows_per_split, nsplit, sh.s));
   } else {
     FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM>), grid, dim3(256), 0, st,
-                                               (const float *)K, (const float *)V,
-                                               (const Mma<float>::frag *)wfr, bq, part, sh.H,
-                                               sh.L, rows_per_split, nsplit, sh.s));
+                                               (const float *)K, (const float *)V, W, b,
+                                               (Mma<float>::frag *)wfr, bq, part, sh.H, sh.L,
+                                               rows_per_split, nsplit, sh.s));
   }
   return hipGetLastError();
 }

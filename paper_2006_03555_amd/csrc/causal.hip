@@ -33,34 +33,59 @@
 
 namespace favor {
 
-__global__ __launch_bounds__(256) void k_seg_scan(float *__restrict__ part, int nseg, int n,
+// Thread idx = m * 65 + n of head bh. With frags non-null the total of this
+// call's tokens is scattered into the Buf1^T fragments: value column n < 64 is
+// lane row c of block nb with pi(nb, c) = n; column 64 (the denominator) is
+// replicated over the 16 lane rows of block 4. Feature m is slot
+// 4 ((m % 32) / 16) + m % 4 of lane group (m % 16) / 4 in k-step m / 32.
+template <typename E>
+__global__ __launch_bounds__(256) void k_seg_scan(float *__restrict__ part, int nseg, int M,
                                                   const float *__restrict__ state_in,
                                                   float *__restrict__ state_out,
-                                                  float *__restrict__ total) {
+                                                  E *__restrict__ frags) {
+  const int n65 = M * 65;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   const int bh = blockIdx.y;
-  if (idx >= n) return;
-  const float s0 = state_in ? state_in[(size_t)bh * n + idx] : 0.f;
+  if (idx >= n65) return;
+  const float s0 = state_in ? state_in[(size_t)bh * n65 + idx] : 0.f;
   float run = 0.f;   // aggregate of the segments before sg (tokens of this call only)
-  float *p = part + (size_t)bh * nseg * n + idx;
+  float *p = part + (size_t)bh * nseg * n65 + idx;
   int sg = 0;
   for (; sg + 8 <= nseg; sg += 8) {   // eight loads in flight
     float v[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = p[(size_t)(sg + k) * n];
+    for (int k = 0; k < 8; ++k) v[k] = p[(size_t)(sg + k) * n65];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      p[(size_t)(sg + k) * n] = s0 + run;
+      p[(size_t)(sg + k) * n65] = s0 + run;
       run += v[k];
     }
   }
   for (; sg < nseg; ++sg) {
-    const float v = p[(size_t)sg * n];
-    p[(size_t)sg * n] = s0 + run;
+    const float v = p[(size_t)sg * n65];
+    p[(size_t)sg * n65] = s0 + run;
     run += v;
   }
-  if (state_out) state_out[(size_t)bh * n + idx] = s0 + run;
-  if (total) total[(size_t)bh * n + idx] = run;
+  if (state_out) state_out[(size_t)bh * n65 + idx] = s0 + run;
+  if (frags) {
+    const int m = idx / 65;
+    const int n = idx - m * 65;
+    const int ns = M / 32;
+    const int sidx = m >> 5;
+    const int q = m & 31;
+    const int gq = (q >> 2) & 3;
+    const int slot = 4 * (q >> 4) + (q & 3);
+    E *fb = frags + (size_t)bh * 5 * ns * 64 * 8;
+    const E v = (E)run;
+    if (n < 64) {
+      const int nb = 2 * (n >> 5) + ((n >> 2) & 1);
+      const int c = 4 * ((n & 31) >> 3) + (n & 3);        // lane row with pi(nb, c) = n
+      fb[((size_t)(nb * ns + sidx) * 64 + 16 * gq + c) * 8 + slot] = v;
+    } else {
+#pragma unroll 4
+      for (int c = 0; c < 16; ++c) fb[((size_t)(4 * ns + sidx) * 64 + 16 * gq + c) * 8 + slot] = v;
+    }
+  }
 }
 
 template <typename T, int M>
@@ -740,12 +765,16 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   if (r1 > r0) finalize(r0 + 64 * ((r1 - r0 - 1) / 64), buf ^ 1);
 }
 
-hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
-                           float *state_out, float *total, hipStream_t st) {
+hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const float *state_in,
+                           float *state_out, void *total_frags, hipStream_t st) {
   const int n = sh.M * 65;
   dim3 grid((n + 255) / 256, sh.BH);
-  hipLaunchKernelGGL(k_seg_scan, grid, dim3(256), 0, st, part, nseg, n, state_in, state_out,
-                     total);
+  if (in == Dt::BF16)
+    hipLaunchKernelGGL(k_seg_scan<bf16>, grid, dim3(256), 0, st, part, nseg, sh.M, state_in,
+                       state_out, (bf16 *)total_frags);
+  else
+    hipLaunchKernelGGL(k_seg_scan<float>, grid, dim3(256), 0, st, part, nseg, sh.M, state_in,
+                       state_out, (float *)total_frags);
   return hipGetLastError();
 }
 

@@ -71,14 +71,12 @@ favor_status validate(const favor_desc *g, int op) {
   return FAVOR_OK;
 }
 
-// Workspace: [ split partials | total (both) | Buf1^T fragments (bidir, both) |
-//              W'' fragments | b'' ]
+// Workspace: [ split partials | Buf1^T fragments (bidir, both) | W'' fragments | b'' ]
 struct Plan {
   int BH = 0;
   int nsplit = 0;         // bidir: K-side splits; causal and both: segments
   int rows_per_split = 0;
   size_t part_bytes = 0;
-  size_t tot_bytes = 0;   // both only
   size_t frag_bytes = 0;  // bidir and both
   size_t wfr_bytes = 0;
   size_t bq_bytes = 0;
@@ -108,10 +106,9 @@ Plan make_plan(const favor_desc *g, int op) {
   p.part_bytes = round_up((size_t)p.BH * p.nsplit * g->M * 65 * sizeof(float), 256);
   const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
   if (op != kOpCausal) p.frag_bytes = round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
-  if (op == kOpBoth) p.tot_bytes = round_up((size_t)p.BH * g->M * 65 * sizeof(float), 256);
   p.wfr_bytes = round_up((size_t)g->H * (g->M / 16) * 2 * 64 * fb, 256);
   p.bq_bytes = round_up((size_t)g->H * g->M * sizeof(float), 256);
-  p.total = p.part_bytes + p.tot_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
+  p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
   return p;
 }
 
@@ -237,18 +234,13 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
   const favor::Dt in = dt_of(g->in_dtype);
   hipStream_t st = (hipStream_t)stream;
   float *part = static_cast<float *>(ws);
-  void *frags = static_cast<char *>(ws) + p.part_bytes + p.tot_bytes;
+  void *frags = static_cast<char *>(ws) + p.part_bytes;
   void *wfr = static_cast<char *>(frags) + p.frag_bytes;
   float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
   hipError_t e;
   {
-    favor::LaunchTimer t(favor::kKerPrepW, st);
-    e = favor::launch_prep_w(sh, in, W, b, wfr, bq, st);
-  }
-  if (e != hipSuccess) return device_result(e, "favor_attn_bidir feature preparation");
-  {
     favor::LaunchTimer t(favor::kKerKside, st);
-    e = favor::launch_kside(sh, in, K, V, wfr, bq, part, p.rows_per_split, p.nsplit, st);
+    e = favor::launch_kside(sh, in, K, V, W, b, wfr, bq, part, p.rows_per_split, p.nsplit, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_bidir key pass");
   {
@@ -289,7 +281,8 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
       hipError_t e;
       {
         favor::LaunchTimer t(favor::kKerSegScan, st);
-        e = favor::launch_seg_scan(sh, nullptr, 0, state_in, state_out, nullptr, st);
+        e = favor::launch_seg_scan(sh, favor::Dt::F32, nullptr, 0, state_in, state_out, nullptr,
+                                   st);
       }
       return device_result(e, "favor_attn_causal state copy");
     }
@@ -305,18 +298,13 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
   float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
   hipError_t e;
   {
-    favor::LaunchTimer t(favor::kKerPrepW, st);
-    e = favor::launch_prep_w(sh, in, W, b, wfr, bq, st);
-  }
-  if (e != hipSuccess) return device_result(e, "favor_attn_causal feature preparation");
-  {
     favor::LaunchTimer t(favor::kKerKside, st);
-    e = favor::launch_kside(sh, in, K, V, wfr, bq, part, p.rows_per_split, p.nsplit, st);
+    e = favor::launch_kside(sh, in, K, V, W, b, wfr, bq, part, p.rows_per_split, p.nsplit, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal segment aggregates");
   {
     favor::LaunchTimer t(favor::kKerSegScan, st);
-    e = favor::launch_seg_scan(sh, part, p.nsplit, state_in, state_out, nullptr, st);
+    e = favor::launch_seg_scan(sh, in, part, p.nsplit, state_in, state_out, nullptr, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal segment scan");
   {
@@ -353,7 +341,8 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
       hipError_t e;
       {
         favor::LaunchTimer t(favor::kKerSegScan, st);
-        e = favor::launch_seg_scan(sh, nullptr, 0, state_in, state_out, nullptr, st);
+        e = favor::launch_seg_scan(sh, favor::Dt::F32, nullptr, 0, state_in, state_out, nullptr,
+                                   st);
       }
       return device_result(e, "favor_attn_both state copy");
     }
@@ -366,31 +355,21 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
   const favor::Dt in = dt_of(g->in_dtype);
   const favor::Dt out = dt_of(g->out_dtype);
   float *part = static_cast<float *>(ws);
-  float *tot = reinterpret_cast<float *>(static_cast<char *>(ws) + p.part_bytes);
-  void *frags = static_cast<char *>(ws) + p.part_bytes + p.tot_bytes;
+  void *frags = static_cast<char *>(ws) + p.part_bytes;
   void *wfr = static_cast<char *>(frags) + p.frag_bytes;
   float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
   hipError_t e;
   {
-    favor::LaunchTimer t(favor::kKerPrepW, st);
-    e = favor::launch_prep_w(sh, in, W, b, wfr, bq, st);
-  }
-  if (e != hipSuccess) return device_result(e, "favor_attn_both feature preparation");
-  {
     favor::LaunchTimer t(favor::kKerKside, st);
-    e = favor::launch_kside(sh, in, K, V, wfr, bq, part, p.rows_per_split, p.nsplit, st);
+    e = favor::launch_kside(sh, in, K, V, W, b, wfr, bq, part, p.rows_per_split, p.nsplit, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_both segment aggregates");
   {
+    // the segment scan also writes the total over the sequence (Buf1) as Q-side fragments
     favor::LaunchTimer t(favor::kKerSegScan, st);
-    e = favor::launch_seg_scan(sh, part, p.nsplit, state_in, state_out, tot, st);
+    e = favor::launch_seg_scan(sh, in, part, p.nsplit, state_in, state_out, frags, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_both segment scan");
-  {
-    favor::LaunchTimer t(favor::kKerFinalize, st);
-    e = favor::launch_finalize(sh, in, tot, 1, frags, st);
-  }
-  if (e != hipSuccess) return device_result(e, "favor_attn_both Buf1 fragments");
   {
     favor::LaunchTimer t(favor::kKerQside, st);
     e = favor::launch_qside(sh, in, out, Q, wfr, bq, frags, out_bidir, st);

@@ -28,15 +28,13 @@ hipError_t launch_orf_draw(uint64_t seed, int n_heads, int M, int kind, float *W
 hipError_t launch_feature_map(const Shape &sh, Dt in, Dt out, const void *X, const float *W,
                               const float *b, void *Xp, hipStream_t st);
 
-// W'' = (s / 2 pi) W as matrix-core fragments [H][M/16][2][64] (element type of
-// `in`) and b'' = b / 2 pi [H][M] fp32, once per call into the workspace.
-hipError_t launch_prep_w(const Shape &sh, Dt in, const float *W, const float *b, void *wfr,
-                         float *bq, hipStream_t st);
-
 // K side: per (head, row range) partial Buf1 = K'^T [V 1] -> part [BH][nsplit][M][65].
-hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const void *wfr,
-                        const float *bq, float *part, int rows_per_split, int nsplit,
-                        hipStream_t st);
+// Builds W'' = (s / 2 pi) W from W, b itself and stores the fragments
+// [H][M/16][2][64] (element type of `in`) and b'' = b / 2 pi [H][M] of every
+// head into wfr, bq for the launches that follow.
+hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const float *W,
+                        const float *b, void *wfr, float *bq, float *part, int rows_per_split,
+                        int nsplit, hipStream_t st);
 
 // Sum the partials of each head and write Buf1^T as Q-side operand fragments.
 hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit, void *frags,
@@ -47,9 +45,11 @@ hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const voi
                         const float *bq, const void *frags, void *o, hipStream_t st);
 
 // In-place exclusive scan of segment partials (plus state_in); writes state_out
-// (state_in + total) and, if non-null, the total of this call's tokens.
-hipError_t launch_seg_scan(const Shape &sh, float *part, int nseg, const float *state_in,
-                           float *state_out, float *total, hipStream_t st);
+// (state_in + total) and, if non-null, the total of this call's tokens as the
+// Q-side Buf1^T fragments (the layout launch_finalize writes; element type of
+// `in`).
+hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const float *state_in,
+                           float *state_out, void *total_frags, hipStream_t st);
 
 // Causal chunk scan of each segment starting from its prefix state.
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,
@@ -69,7 +69,6 @@ enum KernelId {
   kKerQside,
   kKerSegScan,
   kKerCausal,
-  kKerPrepW,
   kNumKernels
 };
 const char *kernel_name(int k);

@@ -217,49 +217,6 @@ __device__ __forceinline__ void key_features_lds(const KVTile<T> &tl,
   }
 }
 
-// W'' fragments of one head (precomputed, see k_prep_w): wfr[mb][ks][lane] holds
-// W''[16 mb + lane % 16][32 ks + 8 (lane / 16) .. + 8]. The same 16 bytes serve as
-// the A operand (lane row m) and as the B operand (lane col m).
-template <typename T, int MB>
-__device__ __forceinline__ void load_w_bfrags(const typename Mma<T>::frag *__restrict__ wfr,
-                                              const float *__restrict__ bq, int m0,
-                                              typename Mma<T>::frag (&Wf)[MB][2],
-                                              f32x4 (&bC)[MB]) {
-  const int l = lane_id();
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int mbg = m0 / 16 + mb;
-    Wf[mb][0] = wfr[(mbg * 2 + 0) * 64 + l];
-    Wf[mb][1] = wfr[(mbg * 2 + 1) * 64 + l];
-    const float bb = bq[m0 + mb * 16 + (l & 15)];
-    bC[mb] = f32x4{bb, bb, bb, bb};
-  }
-}
-
-// Fill W'' A-operand fragments (lane row m, loaded d order) for all M rows and
-// b'' into LDS, cooperatively (256 threads; compile-time trip counts so the
-// global loads of all iterations are in flight together).
-template <typename T, int M>
-__device__ __forceinline__ void fill_w_afrags(typename Mma<T>::frag (*WA)[2][64], float *bq,
-                                              const float *__restrict__ Wh,
-                                              const float *__restrict__ bh, float ws) {
-  constexpr int N = (M / 16) * 2 * 64;
-  static_assert(N % 256 == 0, "256 threads");
-  float v[N / 256][8];
-#pragma unroll
-  for (int it = 0; it < N / 256; ++it) {
-    const int idx = it * 256 + threadIdx.x;
-    const int m = (idx >> 7) * 16 + (idx & 15);
-    load8_f32(Wh + (size_t)m * kD + ((idx >> 6) & 1) * 32 + 8 * ((idx & 63) >> 4), v[it]);
-  }
-#pragma unroll
-  for (int it = 0; it < N / 256; ++it) {
-    const int idx = it * 256 + threadIdx.x;
-    WA[idx >> 7][(idx >> 6) & 1][idx & 63] = Mma<T>::from_f32(v[it], ws);
-  }
-  if (threadIdx.x < M) bq[threadIdx.x] = bh[threadIdx.x] * kInv2Pi;
-}
-
 // Copy n fragments global -> LDS with 256 threads, all loads issued first.
 template <typename F, int N>
 __device__ __forceinline__ void copy_frags(F *__restrict__ dst, const F *__restrict__ src) {

@@ -24,7 +24,7 @@ int64_t g_count[kNumKernels] = {};
 
 const char *const kNames[kNumKernels] = {"k_orf_draw", "k_feature_map", "k_kside",
                                          "k_finalize", "k_qside",       "k_seg_scan",
-                                         "k_causal",   "k_prep_w"};
+                                         "k_causal"};
 
 hipEvent_t take_event() {
   if (!g_pool.empty()) {
