@@ -11,13 +11,13 @@ nothing is skipped inside the timed region.
 
 value = B*H*L / (seconds per step): token-heads per second through the whole
 step (each token-head goes through the draw, both directions), from a timed
-region without per-launch instrumentation. In that region the features of step
-i + 1 are drawn on a second stream while step i attends with its own (two
-feature buffers, ordered by events), as a training loop that redraws features
-every step would run; the region holds exactly one draw and one attention pass
-per step. ms_per_step_serial times the same steps with the draw in line on one
-stream. A third region, serial, with every launch bracketed by HIP events on its
-stream, gives the per-kernel durations and the roofline entry for the dominant
+region without per-launch instrumentation, the draw in line before the
+attention pass on one stream. ms_per_step_pipelined times the same steps with
+the features of step i + 1 drawn on a second stream while step i attends with
+its own (two feature buffers, ordered by events); every attention kernel fills
+the chip, so there the draw delays them instead of hiding. A third region,
+serial, with every launch bracketed by HIP events on its stream, gives the
+per-kernel durations and the roofline entry for the dominant
 kernel. The line also carries the fp64 CPU oracle timed on this host
 (cpu_baseline).
 """
@@ -243,18 +243,19 @@ def main():
     for i in range(args.warmup):
         step_serial(i)
     first = args.warmup
+    # headline: the draw in line on one stream, no per-launch instrumentation (each
+    # event record adds a gap of a few microseconds between launches)
+    ms_step = timed_region(step_serial, first)
+    first += args.steps
+    # the same steps with the next step's draw on a second stream (every attention
+    # kernel fills the chip, so the draw's workgroups delay them rather than hide)
     prime(first)
     for i in range(args.warmup):
         step_pipelined(first + i)
     first += args.warmup
     torch.cuda.synchronize()
     prime(first)
-    # headline: the pipelined loop, no per-launch instrumentation (each event record
-    # adds a gap of a few microseconds between launches)
-    ms_step = timed_region(step_pipelined, first, last_draw=lambda k: ev_draw[k])
-    first += args.steps
-    # the same steps with the draw in line, on one stream
-    ms_step_serial = timed_region(step_serial, first)
+    ms_step_pipelined = timed_region(step_pipelined, first, last_draw=lambda k: ev_draw[k])
     first += args.steps
     # per-kernel durations: serial steps with every launch bracketed by events
     ms_step_instrumented = timed_region(step_serial, first, instrumented=True)
@@ -301,10 +302,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": M,
                    "direction": w.direction, "orf_draw_per_step": True,
-                   "orf_draw": "drawn one step ahead on a second stream",
+                   "orf_draw": "drawn in line before the attention pass, same stream",
                    "parallelism": "single GPU"},
         "kernels": kernels,
-        "ms_per_step_serial": ms_step_serial,
+        "ms_per_step_pipelined": ms_step_pipelined,
         "ms_per_step_instrumented": ms_step_instrumented,
         "roofline": roof,
     }

@@ -1,9 +1,9 @@
 // bidir.hip - bidirectional FAVOR (Sec. 2.5, Algorithm 1) on CDNA4 matrix cores.
 //
 // Three launches, none of which stores a feature matrix:
-//   k_kside     grid (splits * B*H). Each wave converts its slice of W to
-//               W'' = (s / 2 pi) W fragments (one workgroup per head also stores
-//               them for the Q side). Each workgroup streams 64-token tiles of
+//   k_kside     grid (splits * B*H). The workgroup converts the head's W to
+//               W'' = (s / 2 pi) W fragments in LDS (one workgroup per head also
+//               stores them for the Q side). Each workgroup streams 64-token tiles of
 //               one head's K and V, rebuilds the key features K-hat on the
 //               matrix cores (projection + fused cosine), and accumulates its
 //               share of Buf1 = K'^T [V 1] in fp32 accumulators. D_K and the
@@ -26,35 +26,58 @@
 
 namespace favor {
 
-// W'' = (s / 2 pi) W fragments of this wave's feature blocks (B operand of the
-// key projection, lane col m) and b'' = b / 2 pi as accumulator seeds, built
-// from the fp32 draw; the workgroup of (batch 0, split 0) of each head also
-// stores the head's fragments and b'' for the launches that follow.
-template <typename T, int MB>
-__device__ __forceinline__ void build_w_bfrags(const float *__restrict__ Wh,
-                                               const float *__restrict__ bh, int mb0, float ws,
-                                               typename Mma<T>::frag (&Wf)[MB][2], f32x4 (&bC)[MB],
-                                               typename Mma<T>::frag *__restrict__ wfr_out,
-                                               float *__restrict__ bq_out) {
-  const int l = lane_id();
+// The head's W'' = (s / 2 pi) W as B-operand fragments [M/16][2][64] (lane
+// col m) and b'' = b / 2 pi, built into LDS by all NT threads of the
+// workgroup: thread i converts the eight consecutive floats W[m][8 c .. 8 c + 7]
+// (m = i / 8, c = i % 8; row-contiguous, so the loads are fully coalesced) into
+// lane 16 (c % 4) + m % 16 of fragment (m / 16, c / 4). All loads are issued
+// before the first LDS store.
+template <typename T, int M, int NT>
+__device__ __forceinline__ void fill_w_bfrags_lds(typename Mma<T>::frag (*WB)[2][64], float *bq,
+                                                  const float *__restrict__ Wh,
+                                                  const float *__restrict__ bh, float ws) {
+  constexpr int N = M * 8;   // fragment lanes of the head
+  constexpr int IT = N / NT;
+  static_assert(N % NT == 0 && M <= NT, "thread count");
+  const int tid = threadIdx.x;
+  float v[IT][8];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const int m = 16 * (mb0 + mb) + (l & 15);
+  for (int it = 0; it < IT; ++it) load8_f32(Wh + (size_t)(it * NT + tid) * 8, v[it]);
+  const float bb = tid < M ? bh[tid] : 0.f;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      float v[8];
-      load8_f32(Wh + (size_t)m * kD + 32 * ks + 8 * (l >> 4), v);
-      Wf[mb][ks] = Mma<T>::from_f32(v, ws);
-      if (wfr_out) wfr_out[((mb0 + mb) * 2 + ks) * 64 + l] = Wf[mb][ks];
-    }
-    const float bb = bh[m] * kInv2Pi;
-    bC[mb] = f32x4{bb, bb, bb, bb};
-    if (bq_out && l < 16) bq_out[m] = bb;
+  for (int it = 0; it < IT; ++it) {
+    const int idx = it * NT + tid;
+    const int m = idx >> 3;
+    const int c = idx & 7;
+    WB[m >> 4][c >> 2][16 * (c & 3) + (m & 15)] = Mma<T>::from_f32(v[it], ws);
   }
+  if (tid < M) bq[tid] = bb * kInv2Pi;
 }
 
+// Workgroup = NG groups of four waves. Group G takes the 64-token tiles
+// r0 + 64 (NG i + G) of the split; wave q of every group owns features
+// [q M/4, (q+1) M/4). With NG = 2 two waves share each SIMD (one builds features
+// while the other contracts) and one W'' build and one partial store serve the
+// whole split: at the end the groups hand each other half of their
+// accumulators through LDS and each stores the summed half.
+template <typename T, int M, int NG>
+struct KsideSmem {
+  typename Mma<T>::frag WB[M / 16][2][64];   // the head's W'' fragments
+  float bq[M];                               // b''
+  union {
+    KVTile<T> tl[NG][2];
+    f32x4 red[NG][4][M / 128][5][64];   // [group][wave][half of the blocks][column block][lane]
+  };
+};
 template <typename T, int M>
-__global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_kside(
+struct KsideSmem<T, M, 1> {
+  typename Mma<T>::frag WB[M / 16][2][64];
+  float bq[M];
+  KVTile<T> tl[1][2];
+};
+
+template <typename T, int M, int NG>
+__global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k_kside(
     const T *__restrict__ K, const T *__restrict__ V, const float *__restrict__ W,
     const float *__restrict__ b, typename Mma<T>::frag *__restrict__ wfr,
     float *__restrict__ bqg, float *__restrict__ part, int H, int L, int rows_per_split,
@@ -64,26 +87,49 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_kside(
   const int split = item - bh * nsplit;
   constexpr int MW = M / 4;
   constexpr int MB = MW / 16;
+  static_assert(NG == 1 || MB % 2 == 0, "the groups split the feature blocks in halves");
   using P = Mma<T>;
   using frag = typename P::frag;
-  __shared__ KVTile<T> tl[2];
+  __shared__ KsideSmem<T, M, NG> sm;
 
   const int h = bh % H;
-  const int tid = threadIdx.x;
+  const int G = threadIdx.x >> 8;
+  const int tid = threadIdx.x & 255;   // thread within the group
   const int w = tid >> 6;
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
   const int r0 = split * rows_per_split;
   const int r1 = min(L, r0 + rows_per_split);
+  const int ntiles = (r1 - r0 + 63) / 64;
+  const int nit = (ntiles + NG - 1) / NG;   // every group runs nit iterations
 
+  const T *Kh = K + (size_t)bh * L * kD;
+  const T *Vh = V + (size_t)bh * L * kD;
+  const float s2half = 0.5f * s * s;
+  const float cM = sqrtf(2.0f / M);
+
+  // first tile's loads in flight while W'' is built
+  TileRegs<T> rg;
+  load_tile_regs<T>(rg, Kh, Vh, r0 + 64 * G, r1, tid);
+
+  fill_w_bfrags_lds<T, M, 256 * NG>(sm.WB, sm.bq, W + (size_t)h * M * kD, b + (size_t)h * M,
+                                    s * kInv2Pi);
+  __syncthreads();
+  if (bh < H && split == 0) {   // one workgroup per head stores W'' and b'' for later launches
+    constexpr int NF = (M / 16) * 2 * 64;
+    frag *dst = wfr + (size_t)h * NF;
+    for (int i = threadIdx.x; i < NF; i += 256 * NG) dst[i] = (&sm.WB[0][0][0])[i];
+    if (threadIdx.x < M) bqg[(size_t)h * M + threadIdx.x] = sm.bq[threadIdx.x];
+  }
   frag Wf[MB][2];
   f32x4 bC[MB];
-  {
-    const bool writer = bh < H && split == 0;   // one workgroup per head
-    build_w_bfrags<T, MB>(W + (size_t)h * M * kD, b + (size_t)h * M, w * MB, s * kInv2Pi, Wf, bC,
-                          writer ? wfr + (size_t)h * (M / 16) * 2 * 64 : nullptr,
-                          writer ? bqg + (size_t)h * M : nullptr);
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    Wf[mb][0] = sm.WB[w * MB + mb][0][l];
+    Wf[mb][1] = sm.WB[w * MB + mb][1][l];
+    const float bb = sm.bq[16 * (w * MB + mb) + c16];
+    bC[mb] = f32x4{bb, bb, bb, bb};
   }
   frag sel[2] = {select_frag<T>(0), select_frag<T>(1)};
 
@@ -93,27 +139,24 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_kside(
 #pragma unroll
     for (int nb = 0; nb < 5; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const T *Kh = K + (size_t)bh * L * kD;
-  const T *Vh = V + (size_t)bh * L * kD;
-  const float s2half = 0.5f * s * s;
-  const float cM = sqrtf(2.0f / M);
-
-  TileRegs<T> rg;
-  load_tile_regs<T>(rg, Kh, Vh, r0, r1);
-  stage_tile<T>(tl[0], rg, sel, r0, r1, s2half, cM);
+  stage_tile<T>(sm.tl[G][0], rg, sel, r0 + 64 * G, r1, s2half, cM, tid);
   __syncthreads();
   int buf = 0;
-  for (int t0 = r0; t0 < r1; t0 += 64, buf ^= 1) {
-    const bool next = t0 + 64 < r1;
-    if (next) load_tile_regs<T>(rg, Kh, Vh, t0 + 64, r1);
+  for (int it = 0; it < nit; ++it, buf ^= 1) {
+    // tiles past r1 (a group's last one when ntiles is not a multiple of NG)
+    // load nothing and stage zero value weights
+    const int tn = r0 + 64 * (NG * (it + 1) + G);
+    const bool next = it + 1 < nit;
+    if (next) load_tile_regs<T>(rg, Kh, Vh, tn, r1, tid);
+    const KVTile<T> &tc = sm.tl[G][buf];
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
       f32x4 kf[MB][2];
-      key_features<T, MB>(tl[buf], Wf, bC, sidx, kf);
+      key_features<T, MB>(tc, Wf, bC, sidx, kf);
       frag vb[4];
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) vb[nb] = tl[buf].VtF[nb][sidx][l];
-      const frag db = tl[buf].DF[sidx][g];
+      for (int nb = 0; nb < 4; ++nb) vb[nb] = tc.VtF[nb][sidx][l];
+      const frag db = tc.DF[sidx][g];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const frag a = P::pack(kf[mb][0], kf[mb][1]);
@@ -122,20 +165,46 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_kside(
         acc[mb][4] = P::mma(a, db, acc[mb][4]);
       }
     }
-    if (next) stage_tile<T>(tl[buf ^ 1], rg, sel, t0 + 64, r1, s2half, cM);
+    if (next) stage_tile<T>(sm.tl[G][buf ^ 1], rg, sel, tn, r1, s2half, cM, tid);
     __syncthreads();
   }
 
   float *dst = part + ((size_t)bh * nsplit + split) * M * 65;
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+  auto store_block = [&](int mb, const f32x4 (&a)[5]) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int m = w * MW + mb * 16 + 4 * g + j;
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) dst[m * 65 + nb * 16 + c16] = acc[mb][nb][j];
-      if (c16 == 0) dst[m * 65 + 64] = acc[mb][4][j];
+      for (int nb = 0; nb < 4; ++nb) dst[m * 65 + nb * 16 + c16] = a[nb][j];
+      if (c16 == 0) dst[m * 65 + 64] = a[4][j];
     }
+  };
+  if constexpr (NG == 1) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) store_block(mb, acc[mb]);
+  } else {
+    // group G stores feature blocks [G MB/2, (G+1) MB/2) of every wave and hands
+    // the other half to the group that stores it (the tile buffers are free)
+    constexpr int HB = MB / 2;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+      if ((mb / HB) != G)
+#pragma unroll
+        for (int nb = 0; nb < 5; ++nb) sm.red[G][w][mb % HB][nb][l] = acc[mb][nb];
+    __syncthreads();
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+      if ((mb / HB) == G) {
+        f32x4 a[5];
+#pragma unroll
+        for (int nb = 0; nb < 5; ++nb) {
+          const f32x4 o = sm.red[G ^ 1][w][mb % HB][nb][l];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) a[nb][j] = acc[mb][nb][j] + o[j];
+        }
+        store_block(mb, a);
+      }
+  }
 }
 
 // Four threads per (fragment block, lane): each sums every fourth split of the
@@ -334,12 +403,13 @@ hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, co
                         int nsplit, hipStream_t st) {
   dim3 grid(nsplit * sh.BH);
   if (in == Dt::BF16) {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<bf16, MM>), grid, dim3(256), 0, st,
+    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<bf16, MM, kside_groups(Dt::BF16, MM)>),
+                                               grid, dim3(256 * kside_groups(Dt::BF16, MM)), 0, st,
                                                (const bf16 *)K, (const bf16 *)V, W, b,
                                                (Mma<bf16>::frag *)wfr, bq, part, sh.H, sh.L,
                                                rows_per_split, nsplit, sh.s));
   } else {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM>), grid, dim3(256), 0, st,
+    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM, 1>), grid, dim3(256), 0, st,
                                                (const float *)K, (const float *)V, W, b,
                                                (Mma<float>::frag *)wfr, bq, part, sh.H, sh.L,
                                                rows_per_split, nsplit, sh.s));

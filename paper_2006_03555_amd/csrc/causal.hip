@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 
   __syncthreads();
   TileRegs<T> rg;
-  load_tile_regs<T>(rg, Kh, Vh, r0, r1);
+  load_tile_regs<T>(rg, Kh, Vh, r0, r1, tid);
   frag qn[2];
   load_query_frags<T>(qn, Qh, r0 + 16 * w + c16, r1);
   KVTile<T> &tl = sm.tl;
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
     // and values and publish S (the state before this chunk)
     {
       const frag sel[2] = {sm.SEL[0][l], sm.SEL[1][l]};
-      stage_tile<T>(tl, rg, sel, t0, r1, s2half, cM);
+      stage_tile<T>(tl, rg, sel, t0, r1, s2half, cM, tid);
     }
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
     const frag qf[2] = {qn[0], qn[1]};
     __syncthreads();
     if (next) {
-      load_tile_regs<T>(rg, Kh, Vh, t0 + 64, r1);
+      load_tile_regs<T>(rg, Kh, Vh, t0 + 64, r1, tid);
       load_query_frags<T>(qn, Qh, t0 + 64 + 16 * w + c16, r1);
     }
 
@@ -508,7 +508,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   // the first tile's loads go out first: staging waits for them alone
   TileRegs<bf16> rg;
   frag rq[2];
-  load_tile_regs<bf16>(rg, Kh, Vh, r0, r1);
+  load_tile_regs<bf16>(rg, Kh, Vh, r0, r1, tid);
   load_q_rows(rq, Qh, r0, r1);
 
   // W'' fragments of this wave's features: A operand of the query projection
@@ -546,7 +546,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 
   stage_causal_tile(sm.tile[0], rg, rq, r0, r1, s2half, cM, eps);
   if (r0 + 64 < r1) {
-    load_tile_regs<bf16>(rg, Kh, Vh, r0 + 64, r1);
+    load_tile_regs<bf16>(rg, Kh, Vh, r0 + 64, r1, tid);
     load_q_rows(rq, Qh, r0 + 64, r1);
   }
   __syncthreads();
@@ -591,7 +591,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
     if (t0 + 64 < r1) {
       stage_causal_tile(sm.tile[buf ^ 1], rg, rq, t0 + 64, r1, s2half, cM, eps);
       if (t0 + 128 < r1) {
-        load_tile_regs<bf16>(rg, Kh, Vh, t0 + 128, r1);
+        load_tile_regs<bf16>(rg, Kh, Vh, t0 + 128, r1, tid);
         load_q_rows(rq, Qh, t0 + 128, r1);
       }
     }

@@ -93,7 +93,10 @@ Plan make_plan(const favor_desc *g, int op) {
   if (causal && g->chunk > 0) {
     rows = g->chunk;
   } else {
-    const int target = causal ? kCausalWorkgroups : kTargetWorkgroups;
+    // a two-group k_kside workgroup fills a CU by itself
+    const favor::Dt in = g->in_dtype == FAVOR_BF16 ? favor::Dt::BF16 : favor::Dt::F32;
+    const int target =
+        causal ? kCausalWorkgroups : kTargetWorkgroups / favor::kside_groups(in, g->M);
     int want = (target + p.BH - 1) / p.BH;
     int max_split = tiles / (kMinRowsPerSplit / 64);
     if (max_split < 1) max_split = 1;

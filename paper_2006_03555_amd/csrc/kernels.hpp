@@ -28,6 +28,10 @@ hipError_t launch_orf_draw(uint64_t seed, int n_heads, int M, int kind, float *W
 hipError_t launch_feature_map(const Shape &sh, Dt in, Dt out, const void *X, const float *W,
                               const float *b, void *Xp, hipStream_t st);
 
+// Groups of four waves in one k_kside workgroup (two groups share each SIMD and
+// one partial per row range): bf16 inputs with M >= 128 use two.
+constexpr int kside_groups(Dt in, int M) { return in == Dt::BF16 && M >= 128 ? 2 : 1; }
+
 // K side: per (head, row range) partial Buf1 = K'^T [V 1] -> part [BH][nsplit][M][65].
 // Builds W'' = (s / 2 pi) W from W, b itself and stores the fragments
 // [H][M/16][2][64] (element type of `in`) and b'' = b / 2 pi [H][M] of every

@@ -6,19 +6,22 @@
 // half of each 64-bit output), u = (x + 0.5) 2^-32, and Gaussians by the
 // Box-Muller transform of consecutive uniform pairs.
 //
-// Four threads own one row of the block, 16 consecutive elements each, held in
-// fp64 registers from the Gaussian draw to the final store. The rows are
-// orthogonalised in order by modified Gram-Schmidt: when row j is final, its
-// owners publish it into its own LDS slot and raise a ready flag; every later
-// row then removes its component along row j (quad-local dot products; the
-// readers also form ||row j||^2 from the same loads). Waves wait on the flags of the rows they need
-// rather than on workgroup barriers, so the work of rows far from the next
-// pivot overlaps the chain of pivots. A wave waits only for rows owned by
-// itself (published earlier in its own program order) or by lower waves, so
-// every flag is raised and every wave finishes; a bounded spin makes that hold
-// even if it did not. Rows stay unnormalised during the sweep and are
-// normalised at the store. The triangular factor of row Gram-Schmidt has a
-// positive diagonal, so the result is the unique orthogonal factor. Rows are
+// Eight threads own one row of the block, 8 consecutive elements each (one
+// generator call), held in fp64 registers from the Gaussian draw to the final
+// store; wave w holds the panel of rows 8 w .. 8 w + 7. The rows are
+// orthogonalised in order by modified Gram-Schmidt. Inside a panel the pivot
+// chain stays in its wave: the owners of the final row j write it to its LDS
+// slot and the wave reads it back (no flag: a wavefront-scope fence orders the
+// stores before the loads and one wave's LDS accesses complete in order), then
+// removes its component from its later rows. Each row is also published
+// to the later waves by a ready flag; they remove the earlier panels' rows two
+// at a time as the flags come up. Removing two orthogonal rows at once is the
+// same projection as removing them one after the other. Dot products and norms
+// are 8-lane sums on the DPP network. A wave waits only for flags of lower
+// waves, so every flag is raised and every wave finishes; a bounded spin makes
+// that hold even if it did not. Rows stay unnormalised during the sweep and
+// are normalised at the store. The triangular factor of row Gram-Schmidt has
+// a positive diagonal, so the result is the unique orthogonal factor. Rows are
 // then scaled by chi_d norms (independent Gaussian vectors) or sqrt(d) and
 // rounded to fp32.
 #include <type_traits>
@@ -84,8 +87,9 @@ __device__ __forceinline__ void gaussians8(uint64_t seed, uint32_t head, uint32_
   }
 }
 
-// Sum over the four lanes of an aligned quad (DPP quad permutes, no LDS traffic).
-__device__ __forceinline__ double quad_sum(double v) {
+// Sum over the eight lanes of an aligned group (DPP: swap within pairs, within
+// quads, then mirror within the half-row; no LDS traffic).
+__device__ __forceinline__ double sum8(double v) {
   auto perm = [](double x, auto ctrl_tag) {
     constexpr int ctrl = decltype(ctrl_tag)::value;
     const long long b = __double_as_longlong(x);
@@ -93,137 +97,187 @@ __device__ __forceinline__ double quad_sum(double v) {
     const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), ctrl, 0xF, 0xF, false);
     return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
   };
-  v += perm(v, std::integral_constant<int, 0xB1>{});   // quad_perm(1,0,3,2): lane ^ 1
-  v += perm(v, std::integral_constant<int, 0x4E>{});   // quad_perm(2,3,0,1): lane ^ 2
+  v += perm(v, std::integral_constant<int, 0xB1>{});    // quad_perm(1,0,3,2): lane ^ 1
+  v += perm(v, std::integral_constant<int, 0x4E>{});    // quad_perm(2,3,0,1): lane ^ 2
+  v += perm(v, std::integral_constant<int, 0x141>{});   // row_half_mirror: lane 7 - i
   return v;
 }
 
-__global__ __launch_bounds__(256) void k_orf_draw(uint64_t seed, int M, int kind,
+// Row j's eight doubles of lane part p, from its LDS slot.
+__device__ __forceinline__ void read_row(const double *src, double (&q)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; i += 2) {
+    const double2 v = *(const double2 *)(src + i);
+    q[i] = v.x;
+    q[i + 1] = v.y;
+  }
+}
+
+// x . q and q . q over a row held by an aligned group of eight lanes.
+__device__ __forceinline__ void dot_and_norm(const double (&x)[8], const double (&q)[8],
+                                             double &dot, double &nq) {
+  double a0 = 0.0, a1 = 0.0, n0 = 0.0, n1 = 0.0;
+#pragma unroll
+  for (int i = 0; i < 8; i += 2) {
+    a0 = fma(x[i], q[i], a0);
+    a1 = fma(x[i + 1], q[i + 1], a1);
+    n0 = fma(q[i], q[i], n0);
+    n1 = fma(q[i + 1], q[i + 1], n1);
+  }
+  dot = sum8(a0 + a1);
+  nq = sum8(n0 + n1);
+}
+
+// 1 / v: hardware reciprocal refined by two Newton steps.
+__device__ __forceinline__ double recip(double v) {
+  double inv = __builtin_amdgcn_rcp(v);
+  inv = inv * fma(-v, inv, 2.0);
+  return inv * fma(-v, inv, 2.0);
+}
+
+// Orders this wave's LDS stores before its later LDS loads across lanes (a
+// wavefront-scope release/acquire pair around a wave barrier: no instructions,
+// but the compiler may not move another lane's load above the store).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ bool flag_set(const int *f) {
+  return __hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != 0;
+}
+__device__ __forceinline__ void wait_flag(const int *f) {
+  for (int spin = 0; spin < (1 << 22); ++spin)
+    if (flag_set(f)) break;
+}
+
+__global__ __launch_bounds__(512) void k_orf_draw(uint64_t seed, int M, int kind,
                                                   float *__restrict__ W, float *__restrict__ b) {
-  constexpr int D = kOrfD;             // 64 rows of 64; thread = (row, quarter)
+  constexpr int D = kOrfD;             // 64 rows of 64; thread = (row, eighth)
+  constexpr int RW = 8;                // rows per wave (one panel)
   __shared__ double pub[D][D];         // finished rows, one slot each
   __shared__ int ready[D];             // row j published
 
   const int blk = blockIdx.x;
   const int h = blockIdx.y;
   const int tid = threadIdx.x;
-  const int r = tid >> 2;              // row within the block
-  const int p = tid & 3;               // elements 16 p .. 16 p + 15 of the row
+  const int w = tid >> 6;              // wave = panel of rows 8 w .. 8 w + 7
+  const int r = tid >> 3;              // row within the block
+  const int p = tid & 7;               // elements 8 p .. 8 p + 7 of the row
   const uint64_t m = (uint64_t)blk * D + r;   // feature index of the row
+  constexpr int kLastWave = D / RW - 1;
   if (tid < D) ready[tid] = 0;
+  __syncthreads();                     // flags cleared before any wave publishes
 
-  // Gaussian block: element (blk D + r) D + c comes from call ((blk D + r) D + c) / 8
-  double x[16];
+  // Gaussian block: element (blk D + r) D + c comes from call ((blk D + r) D + c) / 8,
+  // so the eight elements of this lane are exactly call m D / 8 + p
+  double x[8];
   {
     float z[8];
-    gaussians8(seed, h, 0, m * (D / 8) + 2 * p, z);
+    gaussians8(seed, h, 0, m * (D / 8) + p, z);
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = (double)z[i];
-    gaussians8(seed, h, 0, m * (D / 8) + 2 * p + 1, z);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[8 + i] = (double)z[i];
   }
-  // chi_d norm of row m: elements m D .. m D + D - 1 (calls m D / 8 + q, q < 8)
+  // chi_d norm of row m (elements m D .. m D + D - 1, calls m D / 8 + p) and
+  // the phases (element m = blk D + i): work off the pivot chain, done by the
+  // last panel's wave while it waits for the earlier panels and by the others
+  // after their own panel.
   double rho = 8.0;                    // sqrt(64) for the fixed-norm kind
-  if (kind == 0) {
-    double ss = 0.0;
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
+  auto side_work = [&]() __attribute__((always_inline)) {
+    if (kind == 0) {
       float z[8];
-      gaussians8(seed, h, 1, m * (D / 8) + 2 * p + q, z);
+      gaussians8(seed, h, 1, m * (D / 8) + p, z);
+      double ss = 0.0;
 #pragma unroll
       for (int i = 0; i < 8; ++i) ss = fma((double)z[i], (double)z[i], ss);
+      rho = sqrt(sum8(ss));
     }
-    rho = sqrt(quad_sum(ss));
-  }
-  // phases: element m = blk D + i
-  if (tid < D / 8) {
-    float u[8];
-    uniforms8(seed, h, 2, (uint64_t)blk * (D / 8) + tid, u);
+    if (w == kLastWave && (tid & 63) < D / 8) {
+      const int k = tid & 63;
+      float u[8];
+      uniforms8(seed, h, 2, (uint64_t)blk * (D / 8) + k, u);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int mm = blk * D + tid * 8 + i;
-      if (mm < M) b[(size_t)h * M + mm] = 6.283185307179586f * u[i];
+      for (int i = 0; i < 8; ++i) {
+        const int mm = blk * D + k * 8 + i;
+        if (mm < M) b[(size_t)h * M + mm] = 6.283185307179586f * u[i];
+      }
     }
-  }
+  };
 
   double scale = 1.0;
-  __syncthreads();                     // flags cleared
-  if (kind != 2) {
-    // owners of row j publish it (data, then the flag); readers form its squared
-    // norm themselves from the same loads, which keeps the norm and its
-    // reciprocal off the owner's side of the chain
-    auto publish = [&](int j) {
-      double *dst = &pub[j][16 * p];
+  if (kind == 2) {
+    side_work();
+  } else {
+    if (w == kLastWave) side_work();
+    // Earlier panels' rows, two at a time as their owners publish them (each
+    // owner raises its flags in order, each after its row's data, so the second
+    // flag covers both rows). The two rows are orthogonal, so removing both
+    // components at once is the same projection (modified Gram-Schmidt in
+    // blocks of two).
+    for (int j0 = 0; j0 < RW * w; j0 += 2) {
+      wait_flag(&ready[j0 + 1]);
+      double q0[8], q1[8];
+      read_row(&pub[j0][8 * p], q0);
+      read_row(&pub[j0 + 1][8 * p], q1);
+      double d0, n0, d1, n1;
+      dot_and_norm(x, q0, d0, n0);
+      dot_and_norm(x, q1, d1, n1);
+      const double c0 = d0 * recip(n0);
+      const double c1 = d1 * recip(n1);
 #pragma unroll
-      for (int i = 0; i < 16; i += 2) *(double2 *)(dst + i) = make_double2(x[i], x[i + 1]);
-      if (p == 0)
-        __hip_atomic_store(&ready[j], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-    };
-    if (r == 0) publish(0);
-    // a wave holds rows 16 w .. 16 w + 15; the last step that changes one of them is
-    // j = 16 w + 14
-    const int last = (tid >> 6) * 16 + 15;
-    for (int j = 0; j < last; ++j) {
-      for (int spin = 0; spin < (1 << 22); ++spin)
-        if (__hip_atomic_load(&ready[j], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) break;
-      const double *src = &pub[j][16 * p];
-      double q[16];
-#pragma unroll
-      for (int i = 0; i < 16; i += 2) {
-        const double2 v = *(const double2 *)(src + i);
-        q[i] = v.x;
-        q[i + 1] = v.y;
-      }
-      double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
-      double n0 = 0.0, n1 = 0.0, n2 = 0.0, n3 = 0.0;
-#pragma unroll
-      for (int i = 0; i < 16; i += 4) {
-        a0 = fma(x[i], q[i], a0);
-        a1 = fma(x[i + 1], q[i + 1], a1);
-        a2 = fma(x[i + 2], q[i + 2], a2);
-        a3 = fma(x[i + 3], q[i + 3], a3);
-        n0 = fma(q[i], q[i], n0);
-        n1 = fma(q[i + 1], q[i + 1], n1);
-        n2 = fma(q[i + 2], q[i + 2], n2);
-        n3 = fma(q[i + 3], q[i + 3], n3);
-      }
-      const double dot = quad_sum((a0 + a1) + (a2 + a3));
-      const double nq = quad_sum((n0 + n1) + (n2 + n3));
-      // 1 / ||row j||^2: hardware reciprocal refined by two Newton steps
-      double inv = __builtin_amdgcn_rcp(nq);
-      inv = inv * fma(-nq, inv, 2.0);
-      inv = inv * fma(-nq, inv, 2.0);
-      const double c = (r > j) ? dot * inv : 0.0;   // rows up to j are final
-#pragma unroll
-      for (int i = 0; i < 16; ++i) x[i] = fma(-c, q[i], x[i]);
-      if (r == j + 1) publish(j + 1);
+      for (int i = 0; i < 8; ++i) x[i] = fma(-c1, q1[i], fma(-c0, q0[i], x[i]));
     }
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    // This wave's panel: row j is final once rows up to j - 1 are removed. Its
+    // owners write it to its slot and the whole wave reads it back (ordered by a
+    // wavefront-scope fence; no flag is needed inside the wave); the flag for
+    // the later panels is raised after the read is issued.
+    for (int jj = 0; jj < RW; ++jj) {
+      const int j = RW * w + jj;
+      double *slot = &pub[j][8 * p];
+      if (r == j) {
 #pragma unroll
-    for (int i = 0; i < 16; i += 4) {
+        for (int i = 0; i < 8; i += 2) *(double2 *)(slot + i) = make_double2(x[i], x[i + 1]);
+      }
+      if (jj == RW - 1) {
+        if (r == j && p == 0)
+          __hip_atomic_store(&ready[j], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        break;
+      }
+      wave_sync();   // the owners' stores before every lane's loads
+      double q[8];
+      read_row(slot, q);
+      if (r == j && p == 0)
+        __hip_atomic_store(&ready[j], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      double dot, nq;
+      dot_and_norm(x, q, dot, nq);
+      const double cj = (r > j) ? dot * recip(nq) : 0.0;   // rows up to j are final
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = fma(-cj, q[i], x[i]);
+    }
+    if (w != kLastWave) side_work();
+    double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) {
       s0 = fma(x[i], x[i], s0);
       s1 = fma(x[i + 1], x[i + 1], s1);
-      s2 = fma(x[i + 2], x[i + 2], s2);
-      s3 = fma(x[i + 3], x[i + 3], s3);
     }
-    const double nrm2 = quad_sum((s0 + s1) + (s2 + s3));
-    scale = rho / sqrt(nrm2);
+    scale = rho / sqrt(sum8(s0 + s1));
   }
 
   if ((int)m < M) {
-    float4* dst = (float4 *)(W + ((size_t)h * M + m) * D + 16 * p);
-#pragma unroll
-    for (int i = 0; i < 16; i += 4)
-      dst[i / 4] = make_float4((float)(x[i] * scale), (float)(x[i + 1] * scale),
-                               (float)(x[i + 2] * scale), (float)(x[i + 3] * scale));
+    float4 *dst = (float4 *)(W + ((size_t)h * M + m) * D + 8 * p);
+    dst[0] = make_float4((float)(x[0] * scale), (float)(x[1] * scale), (float)(x[2] * scale),
+                         (float)(x[3] * scale));
+    dst[1] = make_float4((float)(x[4] * scale), (float)(x[5] * scale), (float)(x[6] * scale),
+                         (float)(x[7] * scale));
   }
 }
 
 hipError_t launch_orf_draw(uint64_t seed, int n_heads, int M, int kind, float *W, float *b,
                            hipStream_t st) {
   dim3 grid((M + kOrfD - 1) / kOrfD, n_heads);
-  hipLaunchKernelGGL(k_orf_draw, grid, dim3(256), 0, st, seed, M, kind, W, b);
+  hipLaunchKernelGGL(k_orf_draw, grid, dim3(512), 0, st, seed, M, kind, W, b);
   return hipGetLastError();
 }
 

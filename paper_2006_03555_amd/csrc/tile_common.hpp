@@ -39,8 +39,8 @@ struct TileRegs {
 
 template <typename T>
 __device__ __forceinline__ void load_tile_regs(TileRegs<T> &r, const T *__restrict__ Kh,
-                                               const T *__restrict__ Vh, int t0, int r1) {
-  const int tid = threadIdx.x;
+                                               const T *__restrict__ Vh, int t0, int r1,
+                                               int tid) {
   const int l = tid & 63;
   const int rk = t0 + (tid >> 2);
   const int rv = t0 + 16 * (tid >> 6) + (l & 15);
@@ -110,9 +110,8 @@ __device__ __forceinline__ void load_query_frags(typename Mma<T>::frag (&qf)[2],
 template <typename T>
 __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
                                            const typename Mma<T>::frag (&sel)[2], int t0, int r1,
-                                           float s2half, float cM) {
+                                           float s2half, float cM, int tid) {
   using P = Mma<T>;
-  const int tid = threadIdx.x;
   const int w = tid >> 6;
   const int l = tid & 63;
   const int g = l >> 4;
