@@ -7,7 +7,9 @@ One step is one pass of the whole path over the protein-shaped workload
 8 heads (favor_orf_draw, a fresh seed per step), then bidirectional FAVOR and
 unidirectional FAVOR over the same Q, K, V (favor_attn_both: one pass over the
 keys serves both directions). Inputs are synthetic and already resident in HBM;
-nothing is skipped inside the timed region.
+nothing is skipped inside the timed region. Untimed warmup runs at least
+--warmup steps and at least --min-warmup-seconds (the clocks settle over a few
+hundred milliseconds; a short warmup reads about 7% slow).
 
 value = B*H*L / (seconds per step): token-heads per second through the whole
 step (each token-head goes through the draw, both directions), from a timed
@@ -142,6 +144,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--min-warmup-seconds", type=float, default=0.3,
+                    help="keep running untimed warmup steps until this long has passed "
+                         "(the GPU clocks settle over a few hundred milliseconds)")
     ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -240,9 +245,15 @@ def main():
             fv.timing_enable(False)
         return e0.elapsed_time(e1) / args.steps
 
-    for i in range(args.warmup):
-        step_serial(i)
-    first = args.warmup
+    t_warm = time.perf_counter()
+    n_warm = 0
+    while n_warm < args.warmup or time.perf_counter() - t_warm < args.min_warmup_seconds:
+        step_serial(n_warm)
+        n_warm += 1
+        if n_warm % 16 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    first = n_warm
     # headline: the draw in line on one stream, no per-launch instrumentation (each
     # event record adds a gap of a few microseconds between launches)
     ms_step = timed_region(step_serial, first)
@@ -305,6 +316,7 @@ def main():
                    "orf_draw": "drawn in line before the attention pass, same stream",
                    "parallelism": "single GPU"},
         "kernels": kernels,
+        "warmup_steps_run": n_warm,
         "ms_per_step_pipelined": ms_step_pipelined,
         "ms_per_step_instrumented": ms_step_instrumented,
         "roofline": roof,
