@@ -263,7 +263,7 @@ __device__ __forceinline__ void load_q_frags(typename Mma<T>::frag (&qf)[TBW][2]
   }
 }
 
-template <typename T, typename To, int M>
+template <typename T, typename To, int M, bool EPS>
 __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *__restrict__ Q,
                                                   const typename Mma<T>::frag *__restrict__ wfr,
                                                   const float *__restrict__ bqg,
@@ -323,8 +323,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
     float epsq[TBW];
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
-      float nrm = 0.f;
-      if (eps != 0.f) {
+      epsq[tb] = 0.f;
+      if constexpr (EPS) {
+        float nrm = 0.f;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
@@ -334,19 +335,15 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
           }
         nrm += __shfl_xor(nrm, 16);
         nrm += __shfl_xor(nrm, 32);
+        // features here omit D_Q sqrt(2/M); the stabiliser is divided by it instead
+        epsq[tb] = eps / (cM * expf(0.5f * s * s * nrm));
       }
-      // features here omit D_Q sqrt(2/M); the stabiliser is divided by it instead
-      epsq[tb] = (eps != 0.f) ? eps / (cM * expf(0.5f * s * s * nrm)) : 0.f;
     }
 
+    // 32 features per step: project and take the cosines, then contract with
+    // Buf1^T (the first step starts the accumulators from zero)
     f32x4 acc[5][TBW];
-#pragma unroll
-    for (int nb = 0; nb < 5; ++nb)
-#pragma unroll
-      for (int tb = 0; tb < TBW; ++tb) acc[nb][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll 2
-    for (int sidx = 0; sidx < NS; ++sidx) {
+    auto feature_step = [&](int sidx, bool first) __attribute__((always_inline)) {
       f32x4 pf[2][TBW];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
@@ -369,16 +366,20 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
       for (int nb = 0; nb < 5; ++nb) {
         const frag a = BF[nb][sidx][l];
 #pragma unroll
-        for (int tb = 0; tb < TBW; ++tb) acc[nb][tb] = P::mma(a, qb[tb], acc[nb][tb]);
+        for (int tb = 0; tb < TBW; ++tb)
+          acc[nb][tb] = P::mma(a, qb[tb], first ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[nb][tb]);
       }
-    }
+    };
+    feature_step(0, true);
+#pragma unroll 2
+    for (int sidx = 1; sidx < NS; ++sidx) feature_step(sidx, false);
 
     To *Oh = out + (size_t)bh * L * kD;
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
       const int t = rbase + tb * 16 + c16;
       if (t < L) {
-        const float inv = 1.0f / (acc[4][tb][0] + epsq[tb]);
+        const float inv = __builtin_amdgcn_rcpf(acc[4][tb][0] + epsq[tb]);
         // blocks 2 p, 2 p + 1 hold value columns 32 p + 8 g .. + 7 in this lane
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp)
@@ -441,10 +442,17 @@ static hipError_t qside_typed(const Shape &sh, const void *Q, const void *wfr, c
   const int ntiles = (sh.L + rows - 1) / rows;
   const int nitems = ntiles * sh.BH;
   dim3 grid(min(nitems, kQsideMaxWorkgroups));
-  FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM>), grid, dim3(256), 0, st,
-                                             (const T *)Q, (const typename Mma<T>::frag *)wfr, bq,
-                                             (const typename Mma<T>::frag *)frags, (To *)o, sh.H,
-                                             sh.L, sh.s, sh.eps, ntiles, nitems));
+  if (sh.eps != 0.f) {
+    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM, true>), grid, dim3(256), 0, st,
+                                               (const T *)Q, (const typename Mma<T>::frag *)wfr,
+                                               bq, (const typename Mma<T>::frag *)frags, (To *)o,
+                                               sh.H, sh.L, sh.s, sh.eps, ntiles, nitems));
+  } else {
+    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM, false>), grid, dim3(256), 0, st,
+                                               (const T *)Q, (const typename Mma<T>::frag *)wfr,
+                                               bq, (const typename Mma<T>::frag *)frags, (To *)o,
+                                               sh.H, sh.L, sh.s, sh.eps, ntiles, nitems));
+  }
   return hipGetLastError();
 }
 
