@@ -15,13 +15,12 @@
 
 namespace favor {
 
-// Rows per work item: 4 waves x TBW blocks of 16 rows.
-template <typename T> struct FmapCfg { static constexpr int TBW = 2; };
-template <> struct FmapCfg<float> { static constexpr int TBW = 2; };
-// workgroups launched (measured best on 256 CUs: one per CU when writing bf16,
-// two when writing fp32)
-template <typename To> struct FmapGrid { static constexpr int kWorkgroups = 256; };
-template <> struct FmapGrid<float> { static constexpr int kWorkgroups = 512; };
+// One workgroup of eight waves per CU (two per SIMD: one wave's cosines and
+// stores overlap the other's matrix work; the head's W'' is loaded once for
+// all eight). A work item is 8 waves x TBW blocks of 16 rows.
+constexpr int kFmapThreads = 512;
+constexpr int kFmapWorkgroups = 256;
+template <typename T> struct FmapCfg { static constexpr int TBW = 1; };
 
 template <typename To>
 __device__ __forceinline__ int fmap_row(int mb, int r) {
@@ -30,26 +29,26 @@ __device__ __forceinline__ int fmap_row(int mb, int r) {
 }
 
 // W'' A-operand fragments in the store order above and b'' (natural order)
-// into LDS, cooperatively (256 threads, all global loads in flight).
-template <typename T, typename To, int M>
+// into LDS, cooperatively (NT threads, loads in flight in batches).
+template <typename T, typename To, int M, int NT>
 __device__ __forceinline__ void fill_w_afrags_perm(typename Mma<T>::frag (*WA)[2][64], float *bq,
                                                    const float *__restrict__ Wh,
                                                    const float *__restrict__ bh, float ws) {
   constexpr int N = (M / 16) * 2 * 64;
-  constexpr int NB = (N / 256) < 4 ? (N / 256) : 4;   // loads in flight per batch
-  static_assert(N % (256 * NB) == 0, "256 threads");
+  constexpr int NB = (N / NT) < 4 ? (N / NT) : 4;   // loads in flight per batch
+  static_assert(N % (NT * NB) == 0, "thread count");
 #pragma unroll
-  for (int it0 = 0; it0 < N / 256; it0 += NB) {
+  for (int it0 = 0; it0 < N / NT; it0 += NB) {
     float v[NB][8];
 #pragma unroll
     for (int it = 0; it < NB; ++it) {
-      const int idx = (it0 + it) * 256 + threadIdx.x;
+      const int idx = (it0 + it) * NT + threadIdx.x;
       const int m = fmap_row<To>(idx >> 7, idx & 15);
       load8_f32(Wh + (size_t)m * kD + ((idx >> 6) & 1) * 32 + 8 * ((idx & 63) >> 4), v[it]);
     }
 #pragma unroll
     for (int it = 0; it < NB; ++it) {
-      const int idx = (it0 + it) * 256 + threadIdx.x;
+      const int idx = (it0 + it) * NT + threadIdx.x;
       WA[idx >> 7][(idx >> 6) & 1][idx & 63] = Mma<T>::from_f32(v[it], ws);
     }
   }
@@ -72,7 +71,7 @@ __device__ __forceinline__ void store_row64(float *p, int g, const f32x4 (&v)[4]
 // loads the head's W'' when the head changes, and prefetches the next tile's
 // rows while the current one is projected and written.
 template <typename T, typename To, int M>
-__global__ __launch_bounds__(256, sizeof(T) == 2 ? 4 : 2) void k_feature_map(const T *__restrict__ X,
+__global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__restrict__ X,
                                                      const float *__restrict__ W,
                                                      const float *__restrict__ bph,
                                                      To *__restrict__ Xp, int H, int L, float s,
@@ -98,7 +97,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 4 : 2) void k_feature_map(con
   // rows rbase + 16 tb + c16 of an item, columns 8 g .. and 32 + 8 g ..
   auto load_rows = [&](int item, frag (&xf)[TBW][2]) {
     const int bh = item / ntiles;
-    const int rbase = (item - bh * ntiles) * (64 * TBW) + w * (16 * TBW);
+    const int rbase = (item - bh * ntiles) * (kFmapThreads / 4 * TBW) + w * (16 * TBW);
     const T *Xh = X + (size_t)bh * L * kD;
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
@@ -121,7 +120,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 4 : 2) void k_feature_map(con
     if (bh != cur) {   // the head's W'' fragments and b''
       const int h = bh % H;
       __syncthreads();
-      fill_w_afrags_perm<T, To, M>(WA, bq, W + (size_t)h * M * kD, bph + (size_t)h * M,
+      fill_w_afrags_perm<T, To, M, kFmapThreads>(WA, bq, W + (size_t)h * M * kD, bph + (size_t)h * M,
                                    s * kInv2Pi);
       __syncthreads();
       cur = bh;
@@ -151,7 +150,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 4 : 2) void k_feature_map(con
       dfac[tb] = cM * expf(s2half * nrm);
     }
 
-    const int rbase = (item - bh * ntiles) * (64 * TBW) + w * (16 * TBW);
+    const int rbase = (item - bh * ntiles) * (kFmapThreads / 4 * TBW) + w * (16 * TBW);
     To *Oh = Xp + (size_t)bh * L * M;
     for (int q = 0; q < M / 64; ++q) {   // features 64 q .. 64 q + 63
       frag a[4][2];
@@ -183,22 +182,22 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 4 : 2) void k_feature_map(con
 template <typename T, typename To>
 static hipError_t fmap_typed(const Shape &sh, const void *X, const float *W, const float *b,
                              void *Xp, hipStream_t st) {
-  const int rows = 64 * FmapCfg<T>::TBW;
+  const int rows = kFmapThreads / 4 * FmapCfg<T>::TBW;
   const int ntiles = (sh.L + rows - 1) / rows;
   const int nitems = ntiles * sh.BH;
-  const int cap = FmapGrid<To>::kWorkgroups;
+  const int cap = kFmapWorkgroups;
   dim3 grid(nitems < cap ? nitems : cap);
   switch (sh.M) {
     case 64:
-      hipLaunchKernelGGL((k_feature_map<T, To, 64>), grid, dim3(256), 0, st, (const T *)X, W, b,
+      hipLaunchKernelGGL((k_feature_map<T, To, 64>), grid, dim3(kFmapThreads), 0, st, (const T *)X, W, b,
                          (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
       break;
     case 128:
-      hipLaunchKernelGGL((k_feature_map<T, To, 128>), grid, dim3(256), 0, st, (const T *)X, W, b,
+      hipLaunchKernelGGL((k_feature_map<T, To, 128>), grid, dim3(kFmapThreads), 0, st, (const T *)X, W, b,
                          (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
       break;
     case 256:
-      hipLaunchKernelGGL((k_feature_map<T, To, 256>), grid, dim3(256), 0, st, (const T *)X, W, b,
+      hipLaunchKernelGGL((k_feature_map<T, To, 256>), grid, dim3(kFmapThreads), 0, st, (const T *)X, W, b,
                          (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
       break;
     default:
