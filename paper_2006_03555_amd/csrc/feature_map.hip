@@ -20,7 +20,7 @@ namespace favor {
 // all eight). A work item is 8 waves x TBW blocks of 16 rows.
 constexpr int kFmapThreads = 512;
 constexpr int kFmapWorkgroups = 256;
-template <typename T> struct FmapCfg { static constexpr int TBW = 1; };
+template <typename T> struct FmapCfg { static constexpr int TBW = 2; };
 
 template <typename To>
 __device__ __forceinline__ int fmap_row(int mb, int r) {
