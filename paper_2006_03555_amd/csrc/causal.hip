@@ -33,58 +33,69 @@
 
 namespace favor {
 
-// Thread idx = m * 65 + n of head bh. With frags non-null the total of this
-// call's tokens is scattered into the Buf1^T fragments: value column n < 64 is
-// lane row c of block nb with pi(nb, c) = n; column 64 (the denominator) is
-// replicated over the 16 lane rows of block 4. Feature m is slot
-// 4 ((m % 32) / 16) + m % 4 of lane group (m % 16) / 4 in k-step m / 32.
+// Workgroup (feature block of 32 rows, head): the 32 x 65 aggregates of its
+// rows are 520 consecutive float4; thread u takes unit u (one thread per unit,
+// so every unit's loads are in flight together) and walks the segments eight
+// loads at a time, replacing every segment aggregate by the
+// exclusive prefix (plus state_in). The total of this call's tokens goes
+// through LDS into the Buf1^T fragments when frags is non-null: fragment lane
+// (nb, l) of this k-step holds, in slot i, feature 16 (i / 4) + 4 (l / 16) + i % 4
+// of value column pi(nb, l % 16) (block 4: the denominator column 64 in all
+// 16 lane rows), written as one vector store.
+constexpr int kSegScanThreads = 576;   // 520 float4 units of a 32-row block, nine waves
+
 template <typename E>
-__global__ __launch_bounds__(256) void k_seg_scan(float *__restrict__ part, int nseg, int M,
+__global__ __launch_bounds__(kSegScanThreads) void k_seg_scan(float *__restrict__ part, int nseg, int M,
                                                   const float *__restrict__ state_in,
                                                   float *__restrict__ state_out,
                                                   E *__restrict__ frags) {
-  const int n65 = M * 65;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  constexpr int kUnits = 32 * 65 / 4;   // float4 per 32-row block
+  __shared__ f32x4 tot[kUnits];
+  const int sidx = blockIdx.x;
   const int bh = blockIdx.y;
-  if (idx >= n65) return;
-  const float s0 = state_in ? state_in[(size_t)bh * n65 + idx] : 0.f;
-  float run = 0.f;   // aggregate of the segments before sg (tokens of this call only)
-  float *p = part + (size_t)bh * nseg * n65 + idx;
-  int sg = 0;
-  for (; sg + 8 <= nseg; sg += 8) {   // eight loads in flight
+  const int n65 = M * 65;
+  const size_t head = (size_t)bh * n65 / 4 + (size_t)sidx * kUnits;   // in float4
+  f32x4 *p = reinterpret_cast<f32x4 *>(part) + (size_t)bh * nseg * (n65 / 4) + sidx * kUnits;
+  const size_t stride = n65 / 4;   // one segment, in float4
+  static_assert(kUnits <= kSegScanThreads, "one thread per unit");
+  const int u = threadIdx.x;
+  if (u < kUnits) {
+    const f32x4 s0 = state_in ? reinterpret_cast<const f32x4 *>(state_in)[head + u]
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 run = {0.f, 0.f, 0.f, 0.f};   // aggregate of the segments before sg
+    int sg = 0;
+    for (; sg + 8 <= nseg; sg += 8) {   // eight loads in flight
+      f32x4 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = p[(sg + k) * stride + u];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        p[(sg + k) * stride + u] = s0 + run;
+        run += v[k];
+      }
+    }
+    for (; sg < nseg; ++sg) {
+      const f32x4 v = p[sg * stride + u];
+      p[sg * stride + u] = s0 + run;
+      run += v;
+    }
+    if (state_out) reinterpret_cast<f32x4 *>(state_out)[head + u] = s0 + run;
+    tot[u] = run;
+  }
+  if (!frags) return;
+  __syncthreads();
+  const float *t = reinterpret_cast<const float *>(tot);
+  const int ns = M / 32;
+  for (int f = threadIdx.x; f < 5 * 64; f += kSegScanThreads) {
+    const int nb = f >> 6;
+    const int l = f & 63;
+    const int gq = l >> 4;
+    const int n = nb < 4 ? perm_col(nb, l & 15) : 64;
     float v[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = p[(size_t)(sg + k) * n65];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      p[(size_t)(sg + k) * n65] = s0 + run;
-      run += v[k];
-    }
-  }
-  for (; sg < nseg; ++sg) {
-    const float v = p[(size_t)sg * n65];
-    p[(size_t)sg * n65] = s0 + run;
-    run += v;
-  }
-  if (state_out) state_out[(size_t)bh * n65 + idx] = s0 + run;
-  if (frags) {
-    const int m = idx / 65;
-    const int n = idx - m * 65;
-    const int ns = M / 32;
-    const int sidx = m >> 5;
-    const int q = m & 31;
-    const int gq = (q >> 2) & 3;
-    const int slot = 4 * (q >> 4) + (q & 3);
-    E *fb = frags + (size_t)bh * 5 * ns * 64 * 8;
-    const E v = (E)run;
-    if (n < 64) {
-      const int nb = 2 * (n >> 5) + ((n >> 2) & 1);
-      const int c = 4 * ((n & 31) >> 3) + (n & 3);        // lane row with pi(nb, c) = n
-      fb[((size_t)(nb * ns + sidx) * 64 + 16 * gq + c) * 8 + slot] = v;
-    } else {
-#pragma unroll 4
-      for (int c = 0; c < 16; ++c) fb[((size_t)(4 * ns + sidx) * 64 + 16 * gq + c) * 8 + slot] = v;
-    }
+    for (int i = 0; i < 8; ++i) v[i] = t[(16 * (i >> 2) + 4 * gq + (i & 3)) * 65 + n];
+    reinterpret_cast<typename Mma<E>::frag *>(frags)[((size_t)bh * 5 * ns + nb * ns + sidx) * 64 + l] =
+        Mma<E>::from_f32(v, 1.f);
   }
 }
 
@@ -767,13 +778,12 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 
 hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const float *state_in,
                            float *state_out, void *total_frags, hipStream_t st) {
-  const int n = sh.M * 65;
-  dim3 grid((n + 255) / 256, sh.BH);
+  dim3 grid(sh.M / 32, sh.BH);
   if (in == Dt::BF16)
-    hipLaunchKernelGGL(k_seg_scan<bf16>, grid, dim3(256), 0, st, part, nseg, sh.M, state_in,
+    hipLaunchKernelGGL(k_seg_scan<bf16>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M, state_in,
                        state_out, (bf16 *)total_frags);
   else
-    hipLaunchKernelGGL(k_seg_scan<float>, grid, dim3(256), 0, st, part, nseg, sh.M, state_in,
+    hipLaunchKernelGGL(k_seg_scan<float>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M, state_in,
                        state_out, (float *)total_frags);
   return hipGetLastError();
 }
