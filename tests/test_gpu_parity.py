@@ -250,8 +250,14 @@ def test_deterministic_bitwise():
     a2 = fv.attn_bidir(*args, S64)
     c1 = fv.attn_causal(*args, S64)
     c2 = fv.attn_causal(*args, S64)
+    ob1, oc1 = fv.attn_both(*args, S64)
+    ob2, oc2 = fv.attn_both(*args, S64)
+    w1, b1 = fv.orf_draw(61, 2, 256)
+    w2, b2 = fv.orf_draw(61, 2, 256)
     torch.cuda.synchronize()
     assert torch.equal(a1, a2) and torch.equal(c1, c2)
+    assert torch.equal(ob1, ob2) and torch.equal(oc1, oc2)
+    assert torch.equal(w1, w2) and torch.equal(b1, b2)
 
 
 def test_empty_batch_is_noop():
