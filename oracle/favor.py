@@ -17,6 +17,13 @@ Readings of points the paper leaves open:
   * The stabiliser is added to the denominator D-hat; 0 reproduces Algorithm 1.
   * Algorithm 1's "Result in R^{L x L}" is read as R^{L x d}; the prefix-sum
     row is (G^PS_i)^T Q'_i in R^{d+1}; the cumsum index runs over j.
+  * Generalized attention with f = ReLU (Sec. 2.2, Eq. interesting; the
+    "Performer-ReLU" default of App. B): g = h = 1 (no D_Q, D_K), c = 1, b = 0,
+    and the kernel stabiliser ("kernel_epsilon", App. B) added to every feature:
+    phi(x)_m = ReLU(omega_m . x~) / sqrt(M) + kernel_eps. The same R-ORF rows W
+    serve both kernels; the phases b are not used by ReLU features.
+  * "renormalize_attention" (App. B) switches the final D-hat^-1 of Algorithm 1:
+    off returns Buf3 = Q' K'^T V itself.
 """
 import numpy as np
 
@@ -25,6 +32,9 @@ from . import philox
 RF_ORTHO_CHI = 0     # R-ORF blocks, rows scaled by independent chi_d norms
 RF_ORTHO_FIXED = 1   # R-ORF blocks, rows scaled to sqrt(d)
 RF_IID = 2           # unstructured Gaussian rows
+
+KERNEL_SOFTMAX = 0   # Gaussian-kernel features (cos), softmax attention
+KERNEL_RELU = 1      # generalized attention with f = ReLU
 
 
 def gram_schmidt_rows(G):
@@ -105,6 +115,27 @@ def feature_map(X, W, b, input_scale):
     return D[..., None] * Xhat
 
 
+def feature_map_relu(X, W, input_scale, kernel_eps=1e-3):
+    """Generalized-attention features with f = ReLU (Sec. 2.2, Eqs. interesting and
+    qkprime with g = h = 1, c = 1, b = 0): X [..., L, d] -> [..., L, M],
+    phi(x)_m = ReLU(omega_m . x~) / sqrt(M) + kernel_eps, x~ = s x.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    if X.ndim < 3:
+        W = W[0]
+    M = W.shape[-2]
+    proj = np.matmul(input_scale * X, np.swapaxes(W, -1, -2))   # [..., L, M]
+    return np.maximum(proj, 0.0) / np.sqrt(M) + kernel_eps
+
+
+def features(X, W, b, input_scale, kernel=KERNEL_SOFTMAX, kernel_eps=1e-3):
+    """Q' or K' for the chosen kernel (softmax: feature_map; ReLU: feature_map_relu)."""
+    if kernel == KERNEL_RELU:
+        return feature_map_relu(X, W, input_scale, kernel_eps)
+    return feature_map(X, W, b, input_scale)
+
+
 def _with_ones(V):
     """C = [V 1_L] (Algorithm 1)."""
     V = np.asarray(V, dtype=np.float64)
@@ -112,27 +143,31 @@ def _with_ones(V):
     return np.concatenate([V, ones], axis=-1)
 
 
-def attn_bidir_features(Qp, Kp, V, denom_eps=0.0):
+def attn_bidir_features(Qp, Kp, V, denom_eps=0.0, renormalize=True):
     """Algorithm 1, bidirectional branch, given Q' and K'.
 
-    Buf1 = K'^T C, Buf2 = Q' Buf1, [Buf3 buf4] = Buf2, return diag(buf4)^-1 Buf3.
+    Buf1 = K'^T C, Buf2 = Q' Buf1, [Buf3 buf4] = Buf2, return diag(buf4)^-1 Buf3
+    (Buf3 itself when renormalize is off).
     """
     C = _with_ones(V)
     d = C.shape[-1] - 1
     Buf1 = np.matmul(np.swapaxes(Kp, -1, -2), C)                # [..., M, d+1]
     Buf2 = np.matmul(Qp, Buf1)                                  # [..., L, d+1]
     Buf3, buf4 = Buf2[..., :d], Buf2[..., d]
+    if not renormalize:
+        return Buf3
     return Buf3 / (buf4 + denom_eps)[..., None]
 
 
-def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0):
+def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, kernel=KERNEL_SOFTMAX,
+               kernel_eps=1e-3, renormalize=True):
     """Bidirectional FAVOR (Sec. 2.5, Algorithm 1)."""
-    Qp = feature_map(Q, W, b, input_scale)
-    Kp = feature_map(K, W, b, input_scale)
-    return attn_bidir_features(Qp, Kp, V, denom_eps)
+    Qp = features(Q, W, b, input_scale, kernel, kernel_eps)
+    Kp = features(K, W, b, input_scale, kernel, kernel_eps)
+    return attn_bidir_features(Qp, Kp, V, denom_eps, renormalize)
 
 
-def attn_causal_features(Qp, Kp, V, denom_eps=0.0, state_in=None):
+def attn_causal_features(Qp, Kp, V, denom_eps=0.0, state_in=None, renormalize=True):
     """Unidirectional FAVOR by sequential prefix aggregation (Sec. 2.5.1, Eq. cumsum;
     the O(Md + Ld + ML)-space variant of Sec. 2.6).
 
@@ -153,27 +188,34 @@ def attn_causal_features(Qp, Kp, V, denom_eps=0.0, state_in=None):
         S += Kp[..., i, :, None] * C[..., i, None, :]
         Buf2[..., i, :] = np.einsum("...m,...mp->...p", Qp[..., i, :], S)
     Buf3, buf4 = Buf2[..., :d], Buf2[..., d]
+    if not renormalize:
+        return Buf3, S
     return Buf3 / (buf4 + denom_eps)[..., None], S
 
 
-def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None):
+def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None,
+                kernel=KERNEL_SOFTMAX, kernel_eps=1e-3, renormalize=True):
     """Unidirectional FAVOR (Algorithm 1, prefix-sum branch). Returns (out, state)."""
-    Qp = feature_map(Q, W, b, input_scale)
-    Kp = feature_map(K, W, b, input_scale)
-    return attn_causal_features(Qp, Kp, V, denom_eps, state_in)
+    Qp = features(Q, W, b, input_scale, kernel, kernel_eps)
+    Kp = features(K, W, b, input_scale, kernel, kernel_eps)
+    return attn_causal_features(Qp, Kp, V, denom_eps, state_in, renormalize)
 
 
-def attn_explicit(Q, K, V, W, b, input_scale, causal, denom_eps=0.0):
+def attn_explicit(Q, K, V, W, b, input_scale, causal, denom_eps=0.0, kernel=KERNEL_SOFTMAX,
+                  kernel_eps=1e-3, renormalize=True):
     """The L x L estimator itself: A-hat = Q' K'^T (Eq. unbiased_attention_estimation),
     masked by tril (diagonal included) when causal, then D-hat^-1 A-hat V with
-    D-hat = diag(A-hat 1_L). Only for small L."""
-    Qp = feature_map(Q, W, b, input_scale)
-    Kp = feature_map(K, W, b, input_scale)
+    D-hat = diag(A-hat 1_L) (A-hat V itself when renormalize is off). Only for small L."""
+    Qp = features(Q, W, b, input_scale, kernel, kernel_eps)
+    Kp = features(K, W, b, input_scale, kernel, kernel_eps)
     Ahat = np.matmul(Qp, np.swapaxes(Kp, -1, -2))
     if causal:
         Ahat = np.tril(Ahat)
+    AV = np.matmul(Ahat, np.asarray(V, dtype=np.float64))
+    if not renormalize:
+        return AV
     Dhat = np.sum(Ahat, axis=-1)
-    return np.matmul(Ahat, np.asarray(V, dtype=np.float64)) / (Dhat + denom_eps)[..., None]
+    return AV / (Dhat + denom_eps)[..., None]
 
 
 def softmax_attn(Q, K, V, input_scale, causal):

@@ -275,3 +275,81 @@ def test_converges_to_softmax_as_m_grows():
     e1, e2, e3 = err(64), err(256), err(1024)
     assert e1 > e2 > e3
     assert 0.3 < e2 / e1 < 0.7 and 0.3 < e3 / e2 < 0.7
+
+
+# ---------------------------------------------------------------- generalized attention, f = ReLU
+def _arccos1(x, y):
+    """First-order arc-cosine kernel (Cho and Saul, NeurIPS 2009): for omega ~ N(0, I),
+    E[ReLU(omega . x) ReLU(omega . y)] = |x| |y| (sin t + (pi - t) cos t) / (2 pi)."""
+    nx, ny = np.linalg.norm(x, axis=-1), np.linalg.norm(y, axis=-1)
+    t = np.arccos(np.clip(np.sum(x * y, -1) / (nx * ny), -1.0, 1.0))
+    return nx * ny * (np.sin(t) + (np.pi - t) * np.cos(t)) / (2 * np.pi)
+
+
+def test_relu_features_reproduce_the_arccosine_kernel():
+    """Large-M IID ReLU features: phi(x)^T phi(y) -> the arc-cosine kernel of x~, y~
+    (pins f = ReLU, the 1/sqrt(M) scale, the input scale and the absence of D factors)."""
+    d, M, s = 8, 1 << 16, 0.7
+    W, b = favor.orf_draw(5, 1, M, d, favor.RF_IID)
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal((8, d))
+    y = rng.standard_normal((8, d))
+    y[0] = x[0]                      # theta = 0: E = |x~|^2 / 2
+    y[1] = -x[1]                     # theta = pi: E = 0
+    fx = favor.feature_map_relu(x, W, s, kernel_eps=0.0)
+    fy = favor.feature_map_relu(y, W, s, kernel_eps=0.0)
+    est = np.sum(fx * fy, -1)
+    want = _arccos1(s * x, s * y)
+    # per-feature products have sample sd sd_m; the mean of M of them has sd sd_m / sqrt(M)
+    prod = fx * fy * M
+    se = np.std(prod, -1) / np.sqrt(M)
+    assert np.all(np.abs(est - want) <= 5 * se + 1e-12)
+    assert abs(want[1]) < 1e-12 and abs(est[1]) == 0.0
+    np.testing.assert_allclose(want[0], 0.5 * s * s * np.sum(x[0] ** 2), rtol=1e-12)
+
+
+def test_relu_feature_stabiliser_placement():
+    """kernel_eps is added to every feature after the ReLU and the scaling: a zero
+    projection gives exactly eps, a negative one too, and features never go below it."""
+    d, M, eps = 16, 64, 1e-3
+    W, b = favor.orf_draw(7, 1, M, d, favor.RF_ORTHO_CHI)
+    X = np.random.default_rng(8).standard_normal((40, d))
+    f0 = favor.feature_map_relu(X, np.zeros_like(W), 1.0, eps)
+    assert np.all(f0 == eps)
+    f = favor.feature_map_relu(X, W, 0.5, eps)
+    proj = 0.5 * X @ W[0].T
+    assert np.all(f >= eps)
+    assert np.all(f[proj < 0] == eps)
+    np.testing.assert_allclose(f[proj > 0], proj[proj > 0] / np.sqrt(M) + eps, rtol=1e-14)
+
+
+@pytest.mark.parametrize("renormalize", [True, False])
+@pytest.mark.parametrize("L,M", [(1, 16), (37, 32), (128, 64)])
+def test_relu_attention_equals_explicit(L, M, renormalize):
+    """Algorithm 1 (bidirectional and prefix-sum) with ReLU features equals the explicit
+    L x L generalized-attention estimator, with and without the final renormalisation."""
+    Q, K, V = _inputs(9 + L, 2, 3, L, D)
+    W, b = favor.orf_draw(10 + L, 3, M, D)
+    kw = dict(kernel=favor.KERNEL_RELU, kernel_eps=1e-3, renormalize=renormalize)
+    ob = favor.attn_bidir(Q, K, V, W, b, 1.0, **kw)
+    oc, _ = favor.attn_causal(Q, K, V, W, b, 1.0, **kw)
+    np.testing.assert_allclose(ob, favor.attn_explicit(Q, K, V, W, b, 1.0, False, **kw),
+                               rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(oc, favor.attn_explicit(Q, K, V, W, b, 1.0, True, **kw),
+                               rtol=1e-11, atol=1e-11)
+
+
+def test_relu_denominator_positive_and_constant_values():
+    """Non-negative features plus eps make D-hat > 0; V = 1 returns 1 (renormalised)
+    and D-hat itself (not renormalised)."""
+    Q, K, V = _inputs(11, 1, 2, 200, D, scale_qk=False)
+    W, b = favor.orf_draw(12, 2, 64, D)
+    kw = dict(kernel=favor.KERNEL_RELU, kernel_eps=1e-3)
+    ones = np.ones_like(V)
+    np.testing.assert_allclose(favor.attn_bidir(Q, K, ones, W, b, 1.0, **kw), 1.0, rtol=1e-12)
+    Qp = favor.feature_map_relu(Q, W, 1.0)
+    Kp = favor.feature_map_relu(K, W, 1.0)
+    Dhat = Qp @ np.swapaxes(Kp, -1, -2).sum(-1, keepdims=True)
+    assert np.all(Dhat > 0)
+    off = favor.attn_bidir(Q, K, ones, W, b, 1.0, renormalize=False, **kw)
+    np.testing.assert_allclose(off, np.broadcast_to(Dhat, off.shape), rtol=1e-12)
