@@ -59,6 +59,14 @@ typedef enum {
   FAVOR_RF_IID = 2          /* unstructured i.i.d. N(0, I_d) rows                              */
 } favor_rf_kind;
 
+/* Feature kernel (Sec. 2.2, Eq. interesting):
+ *   SOFTMAX  Gaussian-kernel features for softmax attention (Sec. 2.3):
+ *            phi(x)_m = exp(||x~||^2 / 2) sqrt(2/M) cos(omega_m . x~ + b_m)
+ *   RELU     generalized attention with f = ReLU, g = h = 1 (the paper's
+ *            "Performer-ReLU", App. B): phi(x)_m = ReLU(omega_m . x~) / sqrt(M)
+ *            + kernel_eps; the phases b are not used. */
+typedef enum { FAVOR_KERNEL_SOFTMAX = 0, FAVOR_KERNEL_RELU = 1 } favor_kernel;
+
 typedef struct {
   int32_t B, H, L, d, M;
   favor_dtype in_dtype;     /* Q, K, V (and X for the feature map) */
@@ -68,6 +76,12 @@ typedef struct {
   float denom_eps;          /* added to D-hat before dividing; 0 = Algorithm 1      */
   int32_t chunk;            /* causal: tokens per segment handled by one workgroup
                                (multiple of 64); 0 = library default                */
+  int32_t kernel;           /* favor_kernel; 0 (zero-initialised) = SOFTMAX         */
+  int32_t no_renormalize;   /* 0 = out = Buf3 / (buf4 + denom_eps) (Algorithm 1);
+                               1 = out = Buf3 = Q' K'^T V ("renormalize_attention"
+                               off, App. B; denom_eps is then unused)             */
+  float kernel_eps;         /* RELU: added to every feature (App. B kernel_epsilon,
+                               default 1e-3); ignored for SOFTMAX                  */
 } favor_desc;
 
 /*
@@ -184,7 +198,7 @@ FAVOR_API favor_status favor_timing_read(int32_t k, double *ms, int64_t *count);
 /* ABI version of this header; bumped on any incompatible change. */
 FAVOR_API int32_t favor_abi_version(void);
 
-#define FAVOR_ABI_VERSION 1
+#define FAVOR_ABI_VERSION 2
 
 #ifdef __cplusplus
 }

@@ -11,6 +11,9 @@ entries that pass near zero. Two gates are used instead, both max over rows:
           (causal). sigma is the first-order forward-error scale of a ratio of
           two sums of products, so E_cond is the error in units of the working
           precision's unit roundoff times the problem's condition.
+
+Without renormalisation the output is Buf3 itself, a plain sum of products,
+and sigma_ik = S_ik (err_cond_numerator).
 """
 import numpy as np
 
@@ -56,3 +59,11 @@ def err_cond(out, ref, S, den_abs):
     d = ref.shape[-1]
     sigma = (S[..., :d] + np.abs(ref) * S[..., d:d + 1]) / den_abs[..., None]
     return float(np.max(np.abs(out - ref) / sigma)) if ref.size else 0.0
+
+
+def err_cond_numerator(out, ref, S):
+    """E_cond for the unnormalised result Buf3: max |out - ref| / S[..., :d]."""
+    out = np.asarray(out, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    d = ref.shape[-1]
+    return float(np.max(np.abs(out - ref) / S[..., :d])) if ref.size else 0.0

@@ -8,12 +8,18 @@ and streams. If ``libfavor.so`` has not been built the calls raise
 
 Tensors: Q, K, V [B, H, L, d] (bfloat16 or float32, contiguous, on the GPU);
 W [H, M, d] float32 and b [H, M] float32 from ``orf_draw``.
+
+Keyword options of the feature and attention calls: kernel (KERNEL_SOFTMAX, the
+Gaussian-kernel features of softmax attention, or KERNEL_RELU, generalized
+attention with ReLU features), renormalize (False returns Q' K'^T V without the
+division by D-hat) and kernel_eps (added to every ReLU feature).
 """
 import ctypes
 import os
 
 from ._lib import (  # noqa: F401
     BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, OP_BIDIR, OP_BOTH, OP_CAUSAL, OP_FEATURE_MAP,
+    KERNEL_RELU, KERNEL_SOFTMAX,
     FavorDesc, FavorError, FavorLibraryMissing, lib, lib_path, make_desc, status_string,
     validate_desc, workspace_size, last_error, timing_enable, timing_reset, timing_read,
 )
@@ -97,7 +103,7 @@ def _require_features(W, b, H, M, d):
     _require_like(b, (H, M), torch.float32, "b")
 
 
-def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0, others=()):
+def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0, others=(), opts=None):
     """Descriptor for inputs X [B, H, L, d] (and tensors `others` of the same shape
     and dtype) with features W [H, M, d], b [H, M]."""
     if X.dim() != 4:
@@ -110,7 +116,12 @@ def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0, others=()):
     M = W.shape[1]
     in_code = _dtype_code(X.dtype)
     out_code = in_code if out_dtype is None else _dtype_code(out_dtype)
-    return make_desc(B, H, L, d, M, in_code, out_code, input_scale, denom_eps, chunk)
+    return make_desc(B, H, L, d, M, in_code, out_code, input_scale, denom_eps, chunk,
+                     **(opts or {}))
+
+
+def _opts(kernel, renormalize, kernel_eps):
+    return dict(kernel=kernel, renormalize=renormalize, kernel_eps=kernel_eps)
 
 
 def _out_dtype(out_dtype, out, X):
@@ -120,10 +131,12 @@ def _out_dtype(out_dtype, out, X):
     return out.dtype if out is not None else X.dtype
 
 
-def feature_map(X, W, b, input_scale, out_dtype=None, out=None, stream=None):
-    """X' = D_X X-hat [B, H, L, M] (favor_feature_map)."""
+def feature_map(X, W, b, input_scale, out_dtype=None, out=None, stream=None,
+                kernel=KERNEL_SOFTMAX, kernel_eps=1e-3):
+    """X' [B, H, L, M] (favor_feature_map): D_X X-hat, or the ReLU features."""
     torch = _torch()
-    g = _desc_for(X, W, input_scale, _out_dtype(out_dtype, out, X))
+    g = _desc_for(X, W, input_scale, _out_dtype(out_dtype, out, X),
+                  opts=_opts(kernel, True, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     shape = (g.B, g.H, g.L, g.M)
     if out is None:
@@ -145,11 +158,12 @@ def _workspace(g, causal, workspace):
 
 
 def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=None,
-               workspace=None, stream=None):
+               workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
+               kernel_eps=1e-3):
     """Bidirectional FAVOR, Algorithm 1 (favor_attn_bidir). Returns out [B, H, L, d]."""
     torch = _torch()
     g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps,
-                  others=(("K", K), ("V", V)))
+                  others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     if out is None:
         out = torch.empty(Q.shape, dtype=_torch_dtype(g.out_dtype), device=Q.device)
@@ -162,14 +176,15 @@ def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=No
 
 
 def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
-                chunk=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None):
+                chunk=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None,
+                kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3):
     """Unidirectional FAVOR by prefix sums (favor_attn_causal).
 
     Returns out, or (out, state_out [B, H, M, d+1]) when return_state is true.
     """
     torch = _torch()
     g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps, chunk,
-                  others=(("K", K), ("V", V)))
+                  others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     sshape = (g.B, g.H, g.M, g.d + 1)
     if out is None:
@@ -189,14 +204,15 @@ def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return
 
 def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
               chunk=0, out_dtype=None, out_bidir=None, out_causal=None, state_out=None,
-              workspace=None, stream=None):
+              workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
+              kernel_eps=1e-3):
     """Both directions over the same inputs with one key pass (favor_attn_both).
 
     Returns (out_bidir, out_causal) or (out_bidir, out_causal, state_out).
     """
     torch = _torch()
     g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out_bidir, Q), denom_eps, chunk,
-                  others=(("K", K), ("V", V)))
+                  others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     odt = _torch_dtype(g.out_dtype)
     sshape = (g.B, g.H, g.M, g.d + 1)

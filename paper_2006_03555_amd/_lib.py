@@ -33,6 +33,8 @@ class FavorDesc(ctypes.Structure):
         ("in_dtype", ctypes.c_int), ("out_dtype", ctypes.c_int),
         ("input_scale", ctypes.c_float), ("denom_eps", ctypes.c_float),
         ("chunk", ctypes.c_int32),
+        ("kernel", ctypes.c_int32), ("no_renormalize", ctypes.c_int32),
+        ("kernel_eps", ctypes.c_float),
     ]
 
 
@@ -74,8 +76,8 @@ def lib():
         f = getattr(L, name)
         f.restype = res
         f.argtypes = args
-    if L.favor_abi_version() != 1:
-        raise FavorLibraryMissing(f"{path}: ABI version {L.favor_abi_version()} != 1")
+    if L.favor_abi_version() != ABI_VERSION:
+        raise FavorLibraryMissing(f"{path}: ABI version {L.favor_abi_version()} != {ABI_VERSION}")
     _LIB = L
     return L
 
@@ -88,9 +90,15 @@ def last_error():
     return lib().favor_last_error().decode()
 
 
-def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, chunk=0):
+KERNEL_SOFTMAX = 0
+KERNEL_RELU = 1
+ABI_VERSION = 2   # favor_desc with kernel, no_renormalize, kernel_eps
+
+
+def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, chunk=0,
+              kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3):
     return FavorDesc(B, H, L, d, M, in_dtype, out_dtype, float(input_scale), float(denom_eps),
-                     chunk)
+                     chunk, int(kernel), 0 if renormalize else 1, float(kernel_eps))
 
 
 def validate_desc(g, op):

@@ -2,8 +2,9 @@
 //
 // Three launches, none of which stores a feature matrix:
 //   k_kside     grid (splits * B*H). The workgroup converts the head's W to
-//               W'' = (s / 2 pi) W fragments in LDS (one workgroup per head also
-//               stores them for the Q side). Each workgroup streams 64-token tiles of
+//               W'' = (s / 2 pi) W fragments in LDS ((s / sqrt M) W for ReLU
+//               features; one workgroup per head also stores them for the
+//               Q side). Each workgroup streams 64-token tiles of
 //               one head's K and V, rebuilds the key features K-hat on the
 //               matrix cores (projection + fused cosine), and accumulates its
 //               share of Buf1 = K'^T [V 1] in fp32 accumulators. D_K and the
@@ -19,15 +20,17 @@
 //               product), multiplies by Buf1^T streaming over features in steps
 //               of 32, and divides by the denominator. D_Q and sqrt(2/M) cancel
 //               in the ratio and are never applied; a non-zero stabiliser is
-//               rescaled by them instead.
+//               rescaled by them instead, and without renormalisation they
+//               multiply the numerator. ReLU features (generalized attention,
+//               Sec. 2.2) replace the cosine by max(., 0) + keps with D = 1.
 #include "favor_common.hpp"
 #include "kernels.hpp"
 #include "tile_common.hpp"
 
 namespace favor {
 
-// The head's W'' = (s / 2 pi) W as B-operand fragments [M/16][2][64] (lane
-// col m) and b'' = b / 2 pi, built into LDS by all NT threads of the
+// The head's W'' = ws W as B-operand fragments [M/16][2][64] (lane col m) and
+// b'' = bs b, built into LDS by all NT threads of the
 // workgroup: thread i converts the eight consecutive floats W[m][8 c .. 8 c + 7]
 // (m = i / 8, c = i % 8; row-contiguous, so the loads are fully coalesced) into
 // lane 16 (c % 4) + m % 16 of fragment (m / 16, c / 4). All loads are issued
@@ -35,7 +38,8 @@ namespace favor {
 template <typename T, int M, int NT>
 __device__ __forceinline__ void fill_w_bfrags_lds(typename Mma<T>::frag (*WB)[2][64], float *bq,
                                                   const float *__restrict__ Wh,
-                                                  const float *__restrict__ bh, float ws) {
+                                                  const float *__restrict__ bh, float ws,
+                                                  float bs) {
   constexpr int N = M * 8;   // fragment lanes of the head
   constexpr int IT = N / NT;
   static_assert(N % NT == 0 && M <= NT, "thread count");
@@ -51,7 +55,7 @@ __device__ __forceinline__ void fill_w_bfrags_lds(typename Mma<T>::frag (*WB)[2]
     const int c = idx & 7;
     WB[m >> 4][c >> 2][16 * (c & 3) + (m & 15)] = Mma<T>::from_f32(v[it], ws);
   }
-  if (tid < M) bq[tid] = bb * kInv2Pi;
+  if (tid < M) bq[tid] = bb * bs;
 }
 
 // Workgroup = NG groups of four waves. Group G takes the 64-token tiles
@@ -76,12 +80,12 @@ struct KsideSmem<T, M, 1> {
   KVTile<T> tl[1][2];
 };
 
-template <typename T, int M, int NG>
+template <typename T, int M, int NG, int KN>
 __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k_kside(
     const T *__restrict__ K, const T *__restrict__ V, const float *__restrict__ W,
     const float *__restrict__ b, typename Mma<T>::frag *__restrict__ wfr,
     float *__restrict__ bqg, float *__restrict__ part, int H, int L, int rows_per_split,
-    int nsplit, float s) {
+    int nsplit, float s, float ws, float bs, float keps) {
   const int item = xcd_item(blockIdx.x, gridDim.x);
   const int bh = item / nsplit;
   const int split = item - bh * nsplit;
@@ -114,7 +118,7 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
   load_tile_regs<T>(rg, Kh, Vh, r0 + 64 * G, r1, tid);
 
   fill_w_bfrags_lds<T, M, 256 * NG>(sm.WB, sm.bq, W + (size_t)h * M * kD, b + (size_t)h * M,
-                                    s * kInv2Pi);
+                                    ws, bs);
   __syncthreads();
   if (bh < H && split == 0) {   // one workgroup per head stores W'' and b'' for later launches
     constexpr int NF = (M / 16) * 2 * 64;
@@ -139,7 +143,7 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
 #pragma unroll
     for (int nb = 0; nb < 5; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  stage_tile<T>(sm.tl[G][0], rg, sel, r0 + 64 * G, r1, s2half, cM, tid);
+  stage_tile<T, KN>(sm.tl[G][0], rg, sel, r0 + 64 * G, r1, s2half, cM, tid);
   __syncthreads();
   int buf = 0;
   for (int it = 0; it < nit; ++it, buf ^= 1) {
@@ -152,7 +156,7 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
       f32x4 kf[MB][2];
-      key_features<T, MB>(tc, Wf, bC, sidx, kf);
+      key_features<T, MB, KN>(tc, Wf, bC, sidx, keps, kf);
       frag vb[4];
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) vb[nb] = tc.VtF[nb][sidx][l];
@@ -165,7 +169,7 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
         acc[mb][4] = P::mma(a, db, acc[mb][4]);
       }
     }
-    if (next) stage_tile<T>(sm.tl[G][buf ^ 1], rg, sel, tn, r1, s2half, cM, tid);
+    if (next) stage_tile<T, KN>(sm.tl[G][buf ^ 1], rg, sel, tn, r1, s2half, cM, tid);
     __syncthreads();
   }
 
@@ -263,13 +267,19 @@ __device__ __forceinline__ void load_q_frags(typename Mma<T>::frag (&qf)[TBW][2]
   }
 }
 
-template <typename T, typename To, int M, bool EPS>
+// Finalisation of a query row: divide by D-hat, divide by D-hat + eps, or
+// (renormalisation off) scale the numerator by the query factor.
+constexpr int kFinDiv = 0;
+constexpr int kFinDivEps = 1;
+constexpr int kFinScale = 2;
+
+template <typename T, typename To, int M, int KN, int FIN>
 __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *__restrict__ Q,
                                                   const typename Mma<T>::frag *__restrict__ wfr,
                                                   const float *__restrict__ bqg,
                                                   const typename Mma<T>::frag *__restrict__ frags,
                                                   To *__restrict__ out, int H, int L, float s,
-                                                  float eps, int ntiles, int nitems) {
+                                                  float eps, float keps, int ntiles, int nitems) {
   constexpr int NS = M / 32;
   constexpr int TBW = QsideCfg<T>::TBW;
   using P = Mma<T>;
@@ -320,11 +330,14 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
       load_q_frags<T, TBW>(qn, Q + (size_t)bn * L * kD,
                            (item + 1 - bn * ntiles) * (64 * TBW) + w * (16 * TBW), L);
     }
+    // per row: the stabiliser in units of the unscaled features (kFinDivEps) or
+    // the factor D_Q sqrt(2/M) the features omit (kFinScale); ReLU features
+    // have D_Q = 1 and carry their own scale
     float epsq[TBW];
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
-      epsq[tb] = 0.f;
-      if constexpr (EPS) {
+      epsq[tb] = FIN == kFinDiv ? 0.f : FIN == kFinDivEps ? eps : 1.f;
+      if constexpr (KN == kCos && FIN != kFinDiv) {
         float nrm = 0.f;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
@@ -336,7 +349,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
         nrm += __shfl_xor(nrm, 16);
         nrm += __shfl_xor(nrm, 32);
         // features here omit D_Q sqrt(2/M); the stabiliser is divided by it instead
-        epsq[tb] = eps / (cM * expf(0.5f * s * s * nrm));
+        const float dq = cM * expf(0.5f * s * s * nrm);
+        epsq[tb] = FIN == kFinDivEps ? eps / dq : dq;
       }
     }
 
@@ -356,7 +370,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
           f32x4 p = P::mma(a0, qf[tb][0], bcv);
           p = P::mma(a1, qf[tb][1], p);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) pf[hh][tb][j] = P::cos_rev(p[j]);
+          for (int j = 0; j < 4; ++j) pf[hh][tb][j] = feature<KN, P>(p[j], keps);
         }
       }
       frag qb[TBW];
@@ -379,7 +393,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
     for (int tb = 0; tb < TBW; ++tb) {
       const int t = rbase + tb * 16 + c16;
       if (t < L) {
-        const float inv = __builtin_amdgcn_rcpf(acc[4][tb][0] + epsq[tb]);
+        const float inv =
+            FIN == kFinScale ? epsq[tb] : __builtin_amdgcn_rcpf(acc[4][tb][0] + epsq[tb]);
         // blocks 2 p, 2 p + 1 hold value columns 32 p + 8 g .. + 7 in this lane
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp)
@@ -399,23 +414,34 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
     default: return hipErrorInvalidValue;                           \
   }
 
-hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const float *W,
-                        const float *b, void *wfr, float *bq, float *part, int rows_per_split,
-                        int nsplit, hipStream_t st) {
+template <int KN>
+static hipError_t kside_kernel(const Shape &sh, Dt in, const void *K, const void *V,
+                               const float *W, const float *b, void *wfr, float *bq, float *part,
+                               int rows_per_split, int nsplit, hipStream_t st) {
   dim3 grid(nsplit * sh.BH);
+  float ws, bs;
+  feature_scales(sh, ws, bs);
   if (in == Dt::BF16) {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<bf16, MM, kside_groups(Dt::BF16, MM)>),
+    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<bf16, MM, kside_groups(Dt::BF16, MM), KN>),
                                                grid, dim3(256 * kside_groups(Dt::BF16, MM)), 0, st,
                                                (const bf16 *)K, (const bf16 *)V, W, b,
                                                (Mma<bf16>::frag *)wfr, bq, part, sh.H, sh.L,
-                                               rows_per_split, nsplit, sh.s));
+                                               rows_per_split, nsplit, sh.s, ws, bs, sh.keps));
   } else {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM, 1>), grid, dim3(256), 0, st,
+    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM, 1, KN>), grid, dim3(256), 0, st,
                                                (const float *)K, (const float *)V, W, b,
                                                (Mma<float>::frag *)wfr, bq, part, sh.H, sh.L,
-                                               rows_per_split, nsplit, sh.s));
+                                               rows_per_split, nsplit, sh.s, ws, bs, sh.keps));
   }
   return hipGetLastError();
+}
+
+hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const float *W,
+                        const float *b, void *wfr, float *bq, float *part, int rows_per_split,
+                        int nsplit, hipStream_t st) {
+  return sh.kernel == 1
+             ? kside_kernel<kRelu>(sh, in, K, V, W, b, wfr, bq, part, rows_per_split, nsplit, st)
+             : kside_kernel<kCos>(sh, in, K, V, W, b, wfr, bq, part, rows_per_split, nsplit, st);
 }
 
 hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit, void *frags,
@@ -435,25 +461,33 @@ hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit
 // XCD-local range of row tiles.
 constexpr int kQsideMaxWorkgroups = 512;
 
-template <typename T, typename To>
-static hipError_t qside_typed(const Shape &sh, const void *Q, const void *wfr, const float *bq,
-                              const void *frags, void *o, hipStream_t st) {
+template <typename T, typename To, int KN, int FIN>
+static hipError_t qside_launch(const Shape &sh, const void *Q, const void *wfr, const float *bq,
+                               const void *frags, void *o, hipStream_t st) {
   const int rows = 64 * QsideCfg<T>::TBW;
   const int ntiles = (sh.L + rows - 1) / rows;
   const int nitems = ntiles * sh.BH;
   dim3 grid(min(nitems, kQsideMaxWorkgroups));
-  if (sh.eps != 0.f) {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM, true>), grid, dim3(256), 0, st,
-                                               (const T *)Q, (const typename Mma<T>::frag *)wfr,
-                                               bq, (const typename Mma<T>::frag *)frags, (To *)o,
-                                               sh.H, sh.L, sh.s, sh.eps, ntiles, nitems));
-  } else {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM, false>), grid, dim3(256), 0, st,
-                                               (const T *)Q, (const typename Mma<T>::frag *)wfr,
-                                               bq, (const typename Mma<T>::frag *)frags, (To *)o,
-                                               sh.H, sh.L, sh.s, sh.eps, ntiles, nitems));
-  }
+  FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM, KN, FIN>), grid, dim3(256), 0, st,
+                                             (const T *)Q, (const typename Mma<T>::frag *)wfr,
+                                             bq, (const typename Mma<T>::frag *)frags, (To *)o,
+                                             sh.H, sh.L, sh.s, sh.eps, sh.keps, ntiles, nitems));
   return hipGetLastError();
+}
+
+template <typename T, typename To, int KN>
+static hipError_t qside_kernel(const Shape &sh, const void *Q, const void *wfr, const float *bq,
+                               const void *frags, void *o, hipStream_t st) {
+  if (!sh.renorm) return qside_launch<T, To, KN, kFinScale>(sh, Q, wfr, bq, frags, o, st);
+  if (sh.eps != 0.f) return qside_launch<T, To, KN, kFinDivEps>(sh, Q, wfr, bq, frags, o, st);
+  return qside_launch<T, To, KN, kFinDiv>(sh, Q, wfr, bq, frags, o, st);
+}
+
+template <typename T, typename To>
+static hipError_t qside_typed(const Shape &sh, const void *Q, const void *wfr, const float *bq,
+                              const void *frags, void *o, hipStream_t st) {
+  return sh.kernel == 1 ? qside_kernel<T, To, kRelu>(sh, Q, wfr, bq, frags, o, st)
+                        : qside_kernel<T, To, kCos>(sh, Q, wfr, bq, frags, o, st);
 }
 
 hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const void *wfr,

@@ -24,7 +24,9 @@
 //   16 x 64 block of Q-hat K-hat^T with its product with C~ (all waves do the
 //   same work, keys after the query are zeroed), and writes normalised rows.
 // Keys, values and queries of the next chunk are loaded while this one is
-// computed.
+// computed. ReLU features (generalized attention, Sec. 2.2) replace the cosine
+// by max(., 0) + keps with D = 1; without renormalisation the numerator is
+// scaled by the query factor D_Q sqrt(2/M) (1 for ReLU) instead of divided.
 #include <type_traits>
 
 #include "favor_common.hpp"
@@ -111,14 +113,14 @@ struct CausalSmem {
   float bq[M];
 };
 
-template <typename T, typename To, int M>
+template <typename T, typename To, int M, int KN, bool RN>
 __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T *__restrict__ K,
                                                 const T *__restrict__ V,
                                                 const typename Mma<T>::frag *__restrict__ wfr,
                                                 const float *__restrict__ bqg,
                                                 const float *__restrict__ prefix,
                                                 To *__restrict__ out, int H, int L, int seg_len,
-                                                int nseg, float s, float eps) {
+                                                int nseg, float s, float eps, float keps) {
   constexpr int MW = M / 4;
   constexpr int MB = MW / 16;
   constexpr int NS = M / 32;
@@ -183,7 +185,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
     // and values and publish S (the state before this chunk)
     {
       const frag sel[2] = {sm.SEL[0][l], sm.SEL[1][l]};
-      stage_tile<T>(tl, rg, sel, t0, r1, s2half, cM, tid);
+      stage_tile<T, KN>(tl, rg, sel, t0, r1, s2half, cM, tid);
     }
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -212,7 +214,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
       f32x4 kf[MB][2];
-      key_features_lds<T, MB>(tl, sm.WA, sm.bq, w * MB, sidx, kf);
+      key_features_lds<T, MB, KN>(tl, sm.WA, sm.bq, w * MB, sidx, keps, kf);
       frag vb[4];
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) vb[nb] = tl.VtF[nb][sidx][l];
@@ -238,8 +240,10 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 
     // queries 16 w .. 16 w + 15 of the chunk (every wave does the same work)
     const int qt = t0 + 16 * w + c16;
-    float epsq = 0.f;
-    if (eps != 0.f) {
+    // the stabiliser in units of the unscaled features, or (renormalisation
+    // off) the factor D_Q sqrt(2/M) they omit; ReLU features carry their scale
+    float epsq = RN ? (KN == kCos ? 0.f : eps) : 1.f;
+    if (KN == kCos && (!RN || eps != 0.f)) {
       float nrm = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
@@ -250,7 +254,8 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
         }
       nrm += __shfl_xor(nrm, 16);
       nrm += __shfl_xor(nrm, 32);
-      epsq = eps / (cM * expf(s2half * nrm));
+      const float dq = cM * expf(s2half * nrm);
+      epsq = RN ? eps / dq : dq;
     }
 
     f32x4 o[5];
@@ -306,7 +311,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) pf[hh][j] = P::cos_rev(pc[hh][j]);
+        for (int j = 0; j < 4; ++j) pf[hh][j] = feature<KN, P>(pc[hh][j], keps);
       const frag qb = P::pack(pf[0], pf[1]);
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) o[nb] = P::mma(cur.sa[nb], qb, o[nb]);
@@ -335,7 +340,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
       o[4] = P::mma(tl.DF[sp][g], pb, o[4]);
     }
     if (qt < r1) {
-      const float inv = 1.0f / (o[4][0] + epsq);
+      const float inv = RN ? 1.0f / (o[4][0] + epsq) : epsq;
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) store4(Oh + (size_t)qt * kD + nb * 16 + 4 * g, o[nb] * inv);
     }
@@ -374,7 +379,8 @@ __device__ __forceinline__ void static_for(F &&f) {
 struct CausalFsTile {
   KVTile<bf16> kv;               // keys row-major, C~ (permuted columns) and D_K fragments
   bf16 Qs[64][kD + kKsPad];      // queries row-major (B operand of the query projection)
-  float epsq[64];                // denominator stabiliser per query (eps / (sqrt(2/M) D_Q))
+  float epsq[64];                // per query: eps / (sqrt(2/M) D_Q), or sqrt(2/M) D_Q
+                                 // when the result is not renormalised
 };
 struct CausalFsSmem {
   CausalFsTile tile[2];
@@ -417,9 +423,11 @@ __device__ __forceinline__ void load_q_rows(bf16x8 (&q)[2], const bf16 *__restri
 }
 
 // Stage a prefetched tile: keys and queries row-major, D_K(t) = sqrt(2/M)
-// exp(||s k_t||^2 / 2) (0 past r1), C~ = D_K [V 1] as chained-order B fragments
-// in permuted column order (wave w transposes the values of tokens 16 w ..),
-// and the per-query stabiliser when eps != 0.
+// exp(||s k_t||^2 / 2) (1 for ReLU features; 0 past r1), C~ = D_K [V 1] as
+// chained-order B fragments in permuted column order (wave w transposes the
+// values of tokens 16 w ..), and the per-query stabiliser when eps != 0 (the
+// query factor when not renormalising).
+template <int KN, bool RN>
 __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRegs<bf16> &r,
                                                   const bf16x8 (&q)[2], int t0, int r1,
                                                   float s2half, float cM, float eps) {
@@ -435,16 +443,19 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
   store_frag<bf16>(&tl.kv.Ks[tr][cq + 8], r.k[1]);
   store_frag<bf16>(&tl.Qs[tr][cq], q[0]);
   store_frag<bf16>(&tl.Qs[tr][cq + 8], q[1]);
-  float nrm = 0.f;
+  float Dt = (t0 + tr < r1) ? 1.f : 0.f;
+  if constexpr (KN == kCos) {
+    float nrm = 0.f;
 #pragma unroll
-  for (int hh = 0; hh < 2; ++hh)
+    for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float x = to_f32(r.k[hh][i]);
-      nrm = fmaf(x, x, nrm);
-    }
-  nrm = quad_sum_f32(nrm);
-  const float Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
+      for (int i = 0; i < 8; ++i) {
+        const float x = to_f32(r.k[hh][i]);
+        nrm = fmaf(x, x, nrm);
+      }
+    nrm = quad_sum_f32(nrm);
+    Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
+  }
   float Dj[4];   // D of tokens 16 w + 4 g + j, held by the quad of lanes 16 g + 4 j
 #pragma unroll
   for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Dt, 16 * g + 4 * j);
@@ -466,7 +477,7 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
 #pragma unroll
     for (int j = 0; j < 4; ++j) p[j] = (bf16)Dj[j];
   }
-  if (eps != 0.f) {
+  if (KN == kCos && (!RN || eps != 0.f)) {
     float qn = 0.f;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh)
@@ -476,11 +487,12 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
         qn = fmaf(x, x, qn);
       }
     qn = quad_sum_f32(qn);
-    if ((tid & 3) == 0) tl.epsq[tr] = (t0 + tr < r1) ? eps / (cM * expf(s2half * qn)) : 0.f;
+    const float dq = cM * expf(s2half * qn);
+    if ((tid & 3) == 0) tl.epsq[tr] = (t0 + tr < r1) ? (RN ? eps / dq : dq) : 0.f;
   }
 }
 
-template <typename To, int M>
+template <typename To, int M, int KN, bool RN>
 __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
                                                    const bf16 *__restrict__ K,
                                                    const bf16 *__restrict__ V,
@@ -488,7 +500,8 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
                                                    const float *__restrict__ bqg,
                                                    const float *__restrict__ prefix,
                                                    To *__restrict__ out, int H, int L,
-                                                   int seg_len, int nseg, float s, float eps) {
+                                                   int seg_len, int nseg, float s, float eps,
+                                                   float keps) {
   constexpr int MW = M / 4;          // features per wave
   constexpr int MB = MW / 16;        // 16-feature blocks per wave
   constexpr int KS = (MB + 1) / 2;   // 32-feature k-steps per wave (a lone block is zero-padded)
@@ -555,7 +568,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       }
   }
 
-  stage_causal_tile(sm.tile[0], rg, rq, r0, r1, s2half, cM, eps);
+  stage_causal_tile<KN, RN>(sm.tile[0], rg, rq, r0, r1, s2half, cM, eps);
   if (r0 + 64 < r1) {
     load_tile_regs<bf16>(rg, Kh, Vh, r0 + 64, r1, tid);
     load_q_rows(rq, Qh, r0 + 64, r1);
@@ -583,7 +596,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
     const float den = own[4][0] + (pden[0] + pden[1] + pden[2]);
     const int qt = tp + 16 * w + c16;
     if (qt < r1) {
-      const float inv = 1.0f / (den + own_epsq);
+      const float inv = RN ? 1.0f / (den + own_epsq) : own_epsq;
 #pragma unroll
       for (int pp = 0; pp < 2; ++pp)
         store8(Oh + (size_t)qt * kD + 32 * pp + 8 * g, num[2 * pp] * inv, num[2 * pp + 1] * inv);
@@ -598,9 +611,13 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   int buf = 0;
   for (int t0 = r0; t0 < r1; t0 += 64, buf ^= 1) {
     const CausalFsTile &tl = sm.tile[buf];
-    const float my_epsq = (eps != 0.f) ? tl.epsq[16 * w + c16] : 0.f;
+    float my_epsq;
+    if constexpr (KN == kCos)
+      my_epsq = (!RN || eps != 0.f) ? tl.epsq[16 * w + c16] : 0.f;
+    else
+      my_epsq = RN ? eps : 1.f;
     if (t0 + 64 < r1) {
-      stage_causal_tile(sm.tile[buf ^ 1], rg, rq, t0 + 64, r1, s2half, cM, eps);
+      stage_causal_tile<KN, RN>(sm.tile[buf ^ 1], rg, rq, t0 + 64, r1, s2half, cM, eps);
       if (t0 + 128 < r1) {
         load_tile_regs<bf16>(rg, Kh, Vh, t0 + 128, r1, tid);
         load_q_rows(rq, Qh, t0 + 128, r1);
@@ -643,7 +660,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) pr[mb][j] = P::cos_rev(pr[mb][j]);
+          for (int j = 0; j < 4; ++j) pr[mb][j] = feature<KN, P>(pr[mb][j], keps);
         if constexpr (i < 4) {
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks)
@@ -788,48 +805,60 @@ hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const 
   return hipGetLastError();
 }
 
+// Calls f(integral_constant<int, KN>, bool_constant<RN>) for the shape's
+// feature kernel and renormalisation.
+template <typename F>
+static hipError_t with_variant(const Shape &sh, F &&f) {
+  using relu = std::integral_constant<int, kRelu>;
+  using cosk = std::integral_constant<int, kCos>;
+  if (sh.kernel == 1) return sh.renorm ? f(relu{}, std::true_type{}) : f(relu{}, std::false_type{});
+  return sh.renorm ? f(cosk{}, std::true_type{}) : f(cosk{}, std::false_type{});
+}
+
 template <typename To>
 static hipError_t causal_fs_typed(const Shape &sh, const void *Q, const void *K, const void *V,
                                   const void *wfr, const float *bq, const float *prefix, void *o,
                                   int seg_len, int nseg, hipStream_t st) {
   dim3 grid(nseg * sh.BH);
+  return with_variant(sh, [&](auto kn, auto rn) -> hipError_t {
+    constexpr int KN = decltype(kn)::value;
+    constexpr bool RN = decltype(rn)::value;
 #define FAVOR_CAUSAL_FS_LAUNCH(MM)                                                          \
-  hipLaunchKernelGGL((k_causal_fs<To, MM>), grid, dim3(256), 0, st, (const bf16 *)Q,          \
+  hipLaunchKernelGGL((k_causal_fs<To, MM, KN, RN>), grid, dim3(256), 0, st, (const bf16 *)Q,  \
                      (const bf16 *)K, (const bf16 *)V, (const bf16x8 *)wfr, bq, prefix,        \
-                     (To *)o, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps)
-  switch (sh.M) {
-    case 64: FAVOR_CAUSAL_FS_LAUNCH(64); break;
-    case 128: FAVOR_CAUSAL_FS_LAUNCH(128); break;
-    case 256: FAVOR_CAUSAL_FS_LAUNCH(256); break;
-    default: return hipErrorInvalidValue;
-  }
+                     (To *)o, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps, sh.keps)
+    switch (sh.M) {
+      case 64: FAVOR_CAUSAL_FS_LAUNCH(64); break;
+      case 128: FAVOR_CAUSAL_FS_LAUNCH(128); break;
+      case 256: FAVOR_CAUSAL_FS_LAUNCH(256); break;
+      default: return hipErrorInvalidValue;
+    }
 #undef FAVOR_CAUSAL_FS_LAUNCH
-  return hipGetLastError();
+    return hipGetLastError();
+  });
 }
 
+// fp32 inputs (M <= 128).
 template <typename T, typename To>
 static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, const void *V,
                                const void *wfr, const float *bq, const float *prefix, void *o,
                                int seg_len, int nseg, hipStream_t st) {
   dim3 grid(nseg * sh.BH);
+  return with_variant(sh, [&](auto kn, auto rn) -> hipError_t {
+    constexpr int KN = decltype(kn)::value;
+    constexpr bool RN = decltype(rn)::value;
 #define FAVOR_CAUSAL_LAUNCH(MM)                                                             \
-  hipLaunchKernelGGL((k_causal<T, To, MM>), grid, dim3(256), 0, st, (const T *)Q,             \
-                     (const T *)K, (const T *)V, (const typename Mma<T>::frag *)wfr, bq, prefix,  \
-                     (To *)o, sh.H, sh.L, seg_len,                                           \
-                     nseg, sh.s, sh.eps)
-  switch (sh.M) {
-    case 64: FAVOR_CAUSAL_LAUNCH(64); break;
-    case 128: FAVOR_CAUSAL_LAUNCH(128); break;
-    case 256:
-      if constexpr (sizeof(T) == 2) {
-        FAVOR_CAUSAL_LAUNCH(256);
-        break;
-      }
-      return hipErrorInvalidValue;
-    default: return hipErrorInvalidValue;
-  }
+  hipLaunchKernelGGL((k_causal<T, To, MM, KN, RN>), grid, dim3(256), 0, st, (const T *)Q,     \
+                     (const T *)K, (const T *)V, (const typename Mma<T>::frag *)wfr, bq,       \
+                     prefix, (To *)o, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps, sh.keps)
+    switch (sh.M) {
+      case 64: FAVOR_CAUSAL_LAUNCH(64); break;
+      case 128: FAVOR_CAUSAL_LAUNCH(128); break;
+      default: return hipErrorInvalidValue;
+    }
 #undef FAVOR_CAUSAL_LAUNCH
-  return hipGetLastError();
+    return hipGetLastError();
+  });
 }
 
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,

@@ -58,6 +58,12 @@ favor_status validate(const favor_desc *g, int op) {
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "input_scale must be finite");
   if (!std::isfinite(g->denom_eps) || g->denom_eps < 0.f)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "denom_eps must be finite and >= 0");
+  if (g->kernel != FAVOR_KERNEL_SOFTMAX && g->kernel != FAVOR_KERNEL_RELU)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown kernel %d", (int)g->kernel);
+  if (g->no_renormalize != 0 && g->no_renormalize != 1)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "no_renormalize must be 0 or 1");
+  if (g->kernel == FAVOR_KERNEL_RELU && (!std::isfinite(g->kernel_eps) || g->kernel_eps < 0.f))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "kernel_eps must be finite and >= 0");
   if (g->chunk < 0 || g->chunk % 64 != 0)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "chunk=%d must be a non-negative multiple of 64",
                 g->chunk);
@@ -123,6 +129,9 @@ favor::Shape shape_of(const favor_desc *g) {
   sh.M = g->M;
   sh.s = g->input_scale;
   sh.eps = g->denom_eps;
+  sh.kernel = g->kernel;
+  sh.renorm = g->no_renormalize ? 0 : 1;
+  sh.keps = g->kernel == FAVOR_KERNEL_RELU ? g->kernel_eps : 0.f;
   return sh;
 }
 

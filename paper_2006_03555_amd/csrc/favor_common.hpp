@@ -149,6 +149,21 @@ __device__ __forceinline__ void store8(float *p, f32x4 a, f32x4 b) {
   *reinterpret_cast<f32x4 *>(p + 4) = b;
 }
 
+// Feature kernels (Sec. 2.2, Eq. interesting): the epilogue applied to a
+// projection p = W'' x + b''. kCos: cos(2 pi p) (W'' and b'' carry 1/2 pi; the
+// D_X sqrt(2/M) factor is applied, or cancelled, outside); kRelu: ReLU(p) + keps
+// (W'' carries s / sqrt(M), b'' = 0, no D_X factor).
+constexpr int kCos = 0;
+constexpr int kRelu = 1;
+template <int KN, typename P>
+__device__ __forceinline__ float feature(float p, float keps) {
+  if constexpr (KN == kRelu) {
+    return fmaxf(p, 0.f) + keps;
+  } else {
+    return P::cos_rev(p);
+  }
+}
+
 // Value-column order of the output-side operands (Buf1^T fragments, the causal
 // value tiles and state): row r of 16-column block nb is value column
 //   pi(nb, r) = 32 (nb / 2) + 8 (r / 4) + 4 (nb % 2) + r % 4,

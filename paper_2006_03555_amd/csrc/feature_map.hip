@@ -1,5 +1,6 @@
 // feature_map.hip - the random-feature map X' = D_X X-hat (Sec. 2.3, Eqs. dqdk
-// and qkprime) materialised in HBM.
+// and qkprime), or the ReLU features of generalized attention (Sec. 2.2),
+// materialised in HBM.
 //
 // The projection W'' x is a matrix-core product in transposed orientation
 // (result lane = row), seeded with b'' so the epilogue is cos(2 pi acc) *
@@ -33,7 +34,8 @@ __device__ __forceinline__ int fmap_row(int mb, int r) {
 template <typename T, typename To, int M, int NT>
 __device__ __forceinline__ void fill_w_afrags_perm(typename Mma<T>::frag (*WA)[2][64], float *bq,
                                                    const float *__restrict__ Wh,
-                                                   const float *__restrict__ bh, float ws) {
+                                                   const float *__restrict__ bh, float ws,
+                                                   float bs) {
   constexpr int N = (M / 16) * 2 * 64;
   constexpr int NB = (N / NT) < 4 ? (N / NT) : 4;   // loads in flight per batch
   static_assert(N % (NT * NB) == 0, "thread count");
@@ -52,7 +54,7 @@ __device__ __forceinline__ void fill_w_afrags_perm(typename Mma<T>::frag (*WA)[2
       WA[idx >> 7][(idx >> 6) & 1][idx & 63] = Mma<T>::from_f32(v[it], ws);
     }
   }
-  if (threadIdx.x < M) bq[threadIdx.x] = bh[threadIdx.x] * kInv2Pi;
+  if (threadIdx.x < M) bq[threadIdx.x] = bh[threadIdx.x] * bs;
 }
 
 // The four result tiles of 64 features for one row: bf16 lanes hold features
@@ -70,12 +72,13 @@ __device__ __forceinline__ void store_row64(float *p, int g, const f32x4 (&v)[4]
 // Persistent: workgroup i takes an XCD-local range of (head, row tile) items,
 // loads the head's W'' when the head changes, and prefetches the next tile's
 // rows while the current one is projected and written.
-template <typename T, typename To, int M>
+template <typename T, typename To, int M, int KN>
 __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__restrict__ X,
                                                      const float *__restrict__ W,
                                                      const float *__restrict__ bph,
                                                      To *__restrict__ Xp, int H, int L, float s,
-                                                     int ntiles, int nitems) {
+                                                     int ntiles, int nitems, float ws, float bs,
+                                                     float keps) {
   constexpr int TBW = FmapCfg<T>::TBW;
   using P = Mma<T>;
   using frag = typename P::frag;
@@ -120,8 +123,8 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
     if (bh != cur) {   // the head's W'' fragments and b''
       const int h = bh % H;
       __syncthreads();
-      fill_w_afrags_perm<T, To, M, kFmapThreads>(WA, bq, W + (size_t)h * M * kD, bph + (size_t)h * M,
-                                   s * kInv2Pi);
+      fill_w_afrags_perm<T, To, M, kFmapThreads>(WA, bq, W + (size_t)h * M * kD,
+                                                 bph + (size_t)h * M, ws, bs);
       __syncthreads();
       cur = bh;
     }
@@ -133,10 +136,12 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
     }
     if (item + 1 < end) load_rows(item + 1, xn);
 
-    // D_X(row) sqrt(2/M) = sqrt(2/M) exp(||s x||^2 / 2)
+    // D_X(row) sqrt(2/M) = sqrt(2/M) exp(||s x||^2 / 2) (1 for ReLU features)
     float dfac[TBW];
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
+      dfac[tb] = 1.f;
+      if constexpr (KN == kRelu) continue;
       float nrm = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
@@ -170,7 +175,7 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
           f32x4 p = P::mma(a[k][0], xf[tb][0], bcv[k]);
           p = P::mma(a[k][1], xf[tb][1], p);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[k][j] = P::cos_rev(p[j]) * dfac[tb];
+          for (int j = 0; j < 4; ++j) v[k][j] = feature<KN, P>(p[j], keps) * dfac[tb];
         }
         const int t = rbase + tb * 16 + c16;
         if (t < L) store_row64(Oh + (size_t)t * M + 64 * q, g, v);
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
   }
 }
 
-template <typename T, typename To>
+template <typename T, typename To, int KN>
 static hipError_t fmap_typed(const Shape &sh, const void *X, const float *W, const float *b,
                              void *Xp, hipStream_t st) {
   const int rows = kFmapThreads / 4 * FmapCfg<T>::TBW;
@@ -187,32 +192,36 @@ static hipError_t fmap_typed(const Shape &sh, const void *X, const float *W, con
   const int nitems = ntiles * sh.BH;
   const int cap = kFmapWorkgroups;
   dim3 grid(nitems < cap ? nitems : cap);
+  float ws, bs;
+  feature_scales(sh, ws, bs);
+#define FAVOR_FMAP_LAUNCH(MM)                                                               \
+  hipLaunchKernelGGL((k_feature_map<T, To, MM, KN>), grid, dim3(kFmapThreads), 0, st,        \
+                     (const T *)X, W, b, (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems, ws, bs, \
+                     sh.keps)
   switch (sh.M) {
-    case 64:
-      hipLaunchKernelGGL((k_feature_map<T, To, 64>), grid, dim3(kFmapThreads), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
-      break;
-    case 128:
-      hipLaunchKernelGGL((k_feature_map<T, To, 128>), grid, dim3(kFmapThreads), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
-      break;
-    case 256:
-      hipLaunchKernelGGL((k_feature_map<T, To, 256>), grid, dim3(kFmapThreads), 0, st, (const T *)X, W, b,
-                         (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems);
-      break;
-    default:
-      return hipErrorInvalidValue;
+    case 64: FAVOR_FMAP_LAUNCH(64); break;
+    case 128: FAVOR_FMAP_LAUNCH(128); break;
+    case 256: FAVOR_FMAP_LAUNCH(256); break;
+    default: return hipErrorInvalidValue;
   }
+#undef FAVOR_FMAP_LAUNCH
   return hipGetLastError();
+}
+
+template <typename T, typename To>
+static hipError_t fmap_kernel(const Shape &sh, const void *X, const float *W, const float *b,
+                              void *Xp, hipStream_t st) {
+  return sh.kernel == 1 ? fmap_typed<T, To, kRelu>(sh, X, W, b, Xp, st)
+                        : fmap_typed<T, To, kCos>(sh, X, W, b, Xp, st);
 }
 
 hipError_t launch_feature_map(const Shape &sh, Dt in, Dt out, const void *X, const float *W,
                               const float *b, void *Xp, hipStream_t st) {
   if (in == Dt::BF16)
-    return out == Dt::BF16 ? fmap_typed<bf16, bf16>(sh, X, W, b, Xp, st)
-                           : fmap_typed<bf16, float>(sh, X, W, b, Xp, st);
-  return out == Dt::BF16 ? fmap_typed<float, bf16>(sh, X, W, b, Xp, st)
-                         : fmap_typed<float, float>(sh, X, W, b, Xp, st);
+    return out == Dt::BF16 ? fmap_kernel<bf16, bf16>(sh, X, W, b, Xp, st)
+                           : fmap_kernel<bf16, float>(sh, X, W, b, Xp, st);
+  return out == Dt::BF16 ? fmap_kernel<float, bf16>(sh, X, W, b, Xp, st)
+                         : fmap_kernel<float, float>(sh, X, W, b, Xp, st);
 }
 
 }  // namespace favor

@@ -1,6 +1,8 @@
 // kernels.hpp - host-side launchers of the FAVOR kernels (internal to libfavor).
 #pragma once
 
+#include <cmath>
+
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -20,7 +22,23 @@ struct Shape {
   int M;
   float s;       // input scale
   float eps;     // denominator stabiliser
+  int kernel;    // 0 Gaussian-kernel (cos) features, 1 ReLU features
+  int renorm;    // 1 divide by D-hat, 0 return the numerator Q' K'^T V
+  float keps;    // ReLU: added to every feature
 };
+
+// Scales of the projection W'' = ws W and of its seed b'' = bs b for the
+// shape's feature kernel: cos takes revolutions (s / 2 pi, 1 / 2 pi); ReLU
+// features carry 1 / sqrt(M) and no phase.
+inline void feature_scales(const Shape &sh, float &ws, float &bs) {
+  if (sh.kernel == 1) {
+    ws = sh.s / sqrtf((float)sh.M);
+    bs = 0.f;
+  } else {
+    ws = sh.s * 0.15915494309189535f;
+    bs = 0.15915494309189535f;
+  }
+}
 
 hipError_t launch_orf_draw(uint64_t seed, int n_heads, int M, int kind, float *W, float *b,
                            hipStream_t st);

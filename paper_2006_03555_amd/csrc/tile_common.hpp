@@ -105,9 +105,10 @@ __device__ __forceinline__ void load_query_frags(typename Mma<T>::frag (&qf)[2],
 }
 
 // Stage a prefetched tile into LDS: keys row-major, D_K(t) = sqrt(2/M)
-// exp(||s k_t||^2 / 2) (0 past r1), and C~ = D_K [V 1] as chained-order
-// B fragments. Wave w transposes the values of its 16 tokens 16 w .. 16 w + 15.
-template <typename T>
+// exp(||s k_t||^2 / 2) (1 for ReLU features; 0 past r1), and C~ = D_K [V 1] as
+// chained-order B fragments. Wave w transposes the values of its 16 tokens
+// 16 w .. 16 w + 15.
+template <typename T, int KN>
 __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
                                            const typename Mma<T>::frag (&sel)[2], int t0, int r1,
                                            float s2half, float cM, int tid) {
@@ -118,17 +119,20 @@ __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
   const int c16 = l & 15;
   const int tr = tid >> 2;
   const int cq = (tid & 3) * 16;
-  float nrm = 0.f;
+  float Dt = (t0 + tr < r1) ? 1.f : 0.f;
+  if constexpr (KN == kCos) {
+    float nrm = 0.f;
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float x = to_f32(r.k[h][i]);
-      nrm = fmaf(x, x, nrm);
-    }
-  nrm += __shfl_xor(nrm, 1);
-  nrm += __shfl_xor(nrm, 2);
-  const float Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
+      for (int i = 0; i < 8; ++i) {
+        const float x = to_f32(r.k[h][i]);
+        nrm = fmaf(x, x, nrm);
+      }
+    nrm += __shfl_xor(nrm, 1);
+    nrm += __shfl_xor(nrm, 2);
+    Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
+  }
   store_frag<T>(&tl.Ks[tr][cq], r.k[0]);
   store_frag<T>(&tl.Ks[tr][cq + 8], r.k[1]);
   // D of rows 16 w + 4 g + j, held by lanes 16 g + 4 j of this wave
@@ -154,12 +158,13 @@ __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
 }
 
 // Key projection + features for one wave's MB m-blocks over token half sidx of
-// the staged tile: kf[mb][tbl][j] = cos(2 pi (W'' k_t + b'')) for token
-// t = 32 sidx + 16 tbl + 4 g + j and feature m = m0 + 16 mb + (lane % 16).
-template <typename T, int MB>
+// the staged tile: kf[mb][tbl][j] = cos(2 pi (W'' k_t + b'')) (ReLU features:
+// max(W'' k_t, 0) + keps) for token t = 32 sidx + 16 tbl + 4 g + j and feature
+// m = m0 + 16 mb + (lane % 16).
+template <typename T, int MB, int KN>
 __device__ __forceinline__ void key_features(const KVTile<T> &tl,
                                              const typename Mma<T>::frag (&Wf)[MB][2],
-                                             const f32x4 (&bC)[MB], int sidx,
+                                             const f32x4 (&bC)[MB], int sidx, float keps,
                                              f32x4 (&kf)[MB][2]) {
   using P = Mma<T>;
   const int l = lane_id();
@@ -175,7 +180,7 @@ __device__ __forceinline__ void key_features(const KVTile<T> &tl,
       f32x4 p = P::mma(a0, Wf[mb][0], bC[mb]);
       p = P::mma(a1, Wf[mb][1], p);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = P::cos_rev(p[j]);
+      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = feature<KN, P>(p[j], keps);
     }
   }
 }
@@ -183,10 +188,10 @@ __device__ __forceinline__ void key_features(const KVTile<T> &tl,
 // Key projection + features as key_features, with the B operand (W'' for this
 // wave's feature blocks) read from the head's W'' fragments in LDS and the
 // accumulator seeds b'' from LDS.
-template <typename T, int MB>
+template <typename T, int MB, int KN>
 __device__ __forceinline__ void key_features_lds(const KVTile<T> &tl,
                                                  const typename Mma<T>::frag (*WA)[2][64],
-                                                 const float *bq, int mb0, int sidx,
+                                                 const float *bq, int mb0, int sidx, float keps,
                                                  f32x4 (&kf)[MB][2]) {
   using P = Mma<T>;
   const int l = lane_id();
@@ -211,7 +216,7 @@ __device__ __forceinline__ void key_features_lds(const KVTile<T> &tl,
       f32x4 p = P::mma(a0, wb[mb][0], bC[mb]);
       p = P::mma(a1, wb[mb][1], p);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = P::cos_rev(p[j]);
+      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = feature<KN, P>(p[j], keps);
     }
   }
 }

@@ -22,16 +22,18 @@ def to_host(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
-def oracle_features(Q, K, W, b, s):
-    return favor.feature_map(Q, W, b, s), favor.feature_map(K, W, b, s)
+def oracle_features(Q, K, W, b, s, kernel=favor.KERNEL_SOFTMAX, kernel_eps=1e-3):
+    return (favor.features(Q, W, b, s, kernel, kernel_eps),
+            favor.features(K, W, b, s, kernel, kernel_eps))
 
 
 def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=None,
-           heads=None):
+           heads=None, kernel=favor.KERNEL_SOFTMAX, kernel_eps=1e-3, renormalize=True):
     """Compare a GPU output with the oracle on the same inputs and features.
 
     heads: optional list of (batch, head) pairs to check (large inputs).
-    Returns (E_row, E_cond); asserts both are within the tolerance."""
+    kernel, kernel_eps, renormalize: the feature kernel and normalisation of the
+    call. Returns (E_row, E_cond); asserts both are within the tolerance."""
     tol = TOL[dtype] if tol is None else tol
     Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
     out = np.asarray(out, dtype=np.float64)
@@ -44,16 +46,19 @@ def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=Non
         b = np.stack([b[hi] for _, hi in heads])[:, None]
         if state_in is not None:
             state_in = sel(np.asarray(state_in, dtype=np.float64))
-    Qp, Kp = oracle_features(Q, K, W, b, s)
+    Qp, Kp = oracle_features(Q, K, W, b, s, kernel, kernel_eps)
     if causal:
-        ref, _ = favor.attn_causal_features(Qp, Kp, V, eps, state_in)
+        ref, _ = favor.attn_causal_features(Qp, Kp, V, eps, state_in, renormalize)
     else:
-        ref = favor.attn_bidir_features(Qp, Kp, V, eps)
+        ref = favor.attn_bidir_features(Qp, Kp, V, eps, renormalize)
     e_row = metrics.err_row(out, ref)
     S, den = metrics.error_scale(Qp, Kp, V, causal, state_in_abs=state_in)
-    if eps:
-        den = np.abs(den + eps)
-    e_cond = metrics.err_cond(out, ref, S, den)
+    if not renormalize:
+        e_cond = metrics.err_cond_numerator(out, ref, S)
+    else:
+        if eps:
+            den = np.abs(den + eps)
+        e_cond = metrics.err_cond(out, ref, S, den)
     assert e_row <= tol, f"E_row {e_row:.3e} > {tol}"
     assert e_cond <= tol, f"E_cond {e_cond:.3e} > {tol}"
     return e_row, e_cond

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_strings(L):
-    assert L.favor_abi_version() == 1
+    assert L.favor_abi_version() == 2
     assert fv.status_string(0) == "FAVOR_OK"
     assert fv.status_string(3) == "FAVOR_ERR_WORKSPACE_TOO_SMALL"
 
@@ -67,6 +67,14 @@ def _desc(**kw):
     (dict(denom_eps=-1.0), 1),
     (dict(chunk=100), 1),
     (dict(B=300, H=300), 2),
+    (dict(kernel=fv.KERNEL_RELU), 0),
+    (dict(kernel=fv.KERNEL_RELU, kernel_eps=0.0), 0),
+    (dict(renormalize=False), 0),
+    (dict(kernel=2), 1),
+    (dict(kernel=-1), 1),
+    (dict(kernel=fv.KERNEL_RELU, kernel_eps=-1e-3), 1),
+    (dict(kernel=fv.KERNEL_RELU, kernel_eps=float("inf")), 1),
+    (dict(kernel_eps=-1.0), 0),   # kernel_eps is not read for softmax features
 ])
 def test_validate_desc(kw, status):
     for op in (fv.OP_FEATURE_MAP, fv.OP_BIDIR, fv.OP_CAUSAL, fv.OP_BOTH):

@@ -1,0 +1,162 @@
+"""GPU parity of generalized attention with ReLU features (Sec. 2.2,
+"Performer-ReLU") and of the unnormalised result Buf3 = Q' K'^T V (the
+renormalisation switch of App. B), through the C ABI against the fp64 oracle.
+
+Tolerances as for the softmax path: 1e-4 for fp32 inputs, 2e-2 for bf16.
+E_cond of an unnormalised result is in units of |Q'| |K'|^T |V|.
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from helpers import TOL, parity, to_dev, to_host
+from oracle import favor
+
+pytestmark = pytest.mark.gpu
+
+S64 = 64 ** -0.25
+RELU = favor.KERNEL_RELU
+SOFTMAX = favor.KERNEL_SOFTMAX
+
+
+def _fv():
+    import paper_2006_03555_amd as fv
+    return fv
+
+
+def _features(seed, H, M):
+    W, b = favor.orf_draw(seed, H, M, 64, favor.RF_ORTHO_CHI)
+    return W.astype(np.float32), b.astype(np.float32)
+
+
+def _qkv(B, H, L, dtype, seed):
+    return wl.make_qkv(wl.Workload("t", "bidir", B, H, L, 64, 64, dtype, seed))
+
+
+def _dev(dtype, *arrs):
+    return [to_dev(a, dtype) for a in arrs]
+
+
+# ---------------------------------------------------------------- feature map
+@pytest.mark.parametrize("din,dout", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
+@pytest.mark.parametrize("M,L,keps", [(256, 300, 1e-3), (128, 64, 0.0), (64, 1, 1e-3)])
+def test_relu_feature_map_parity(din, dout, M, L, keps):
+    import torch
+    fv = _fv()
+    Q, _, _ = _qkv(2, 3, L, din, seed=L + M + 1)
+    W, b = _features(17, 3, M)
+    Xp = fv.feature_map(to_dev(Q, din), to_dev(W), to_dev(b), S64,
+                        out_dtype=torch.bfloat16 if dout == "bf16" else torch.float32,
+                        kernel=fv.KERNEL_RELU, kernel_eps=keps)
+    torch.cuda.synchronize()
+    ref = favor.feature_map_relu(Q.astype(np.float64), W.astype(np.float64), S64, keps)
+    got = to_host(Xp)
+    scale = np.max(np.abs(ref), axis=-1, keepdims=True)
+    err = np.max(np.abs(got - ref) / scale)
+    tol = TOL["f32"] if din == "f32" and dout == "f32" else TOL["bf16"]
+    assert err <= tol, err
+    # the floor of every feature is kernel_eps (ReLU output >= 0)
+    assert got.min() >= keps * (1 - 1e-2) - 1e-7
+
+
+# ---------------------------------------------------------------- bidirectional
+BIDIR_CASES = [
+    # B, H, L, M, dtype, kernel, renormalize, kernel_eps, denom_eps
+    (1, 1, 1024, 128, "f32", RELU, True, 1e-3, 0.0),
+    (2, 2, 1000, 256, "bf16", RELU, True, 1e-3, 0.0),
+    (1, 3, 65, 64, "bf16", RELU, True, 1e-3, 0.0),
+    (2, 1, 63, 256, "f32", RELU, True, 1e-3, 0.0),
+    (1, 2, 300, 128, "f32", RELU, True, 0.0, 0.0),     # plain ReLU features
+    (1, 2, 300, 128, "bf16", RELU, True, 1e-3, 0.5),   # with the denominator stabiliser
+    (1, 2, 300, 128, "f32", SOFTMAX, False, 1e-3, 0.0),
+    (2, 2, 1000, 256, "bf16", SOFTMAX, False, 1e-3, 0.0),
+    (1, 2, 777, 64, "bf16", RELU, False, 1e-3, 0.0),
+    (1, 1, 129, 128, "f32", RELU, False, 1e-3, 0.0),
+]
+
+
+@pytest.mark.parametrize("B,H,L,M,dtype,kernel,renorm,keps,eps", BIDIR_CASES)
+def test_bidir_generalized_parity(B, H, L, M, dtype, kernel, renorm, keps, eps):
+    import torch
+    fv = _fv()
+    Q, K, V = _qkv(B, H, L, dtype, seed=31 + L + M)
+    W, b = _features(13 + L, H, M)
+    out = fv.attn_bidir(*_dev(dtype, Q, K, V), to_dev(W), to_dev(b), S64, denom_eps=eps,
+                        kernel=kernel, renormalize=renorm, kernel_eps=keps)
+    torch.cuda.synchronize()
+    parity(to_host(out), Q, K, V, W, b, S64, False, dtype, eps=eps, kernel=kernel,
+           kernel_eps=keps, renormalize=renorm)
+
+
+# ---------------------------------------------------------------- causal
+CAUSAL_CASES = [
+    # B, H, L, M, dtype, chunk, kernel, renormalize, denom_eps
+    (1, 1, 1024, 128, "f32", 0, RELU, True, 0.0),
+    (2, 2, 1000, 256, "bf16", 0, RELU, True, 0.0),
+    (1, 2, 1000, 256, "bf16", 64, RELU, True, 0.0),
+    (1, 3, 65, 64, "bf16", 0, RELU, True, 0.0),
+    (2, 1, 200, 64, "f32", 128, RELU, True, 0.0),
+    (1, 2, 300, 128, "bf16", 0, RELU, True, 0.5),
+    (1, 2, 300, 128, "f32", 0, SOFTMAX, False, 0.0),
+    (1, 2, 1000, 256, "bf16", 64, SOFTMAX, False, 0.0),
+    (2, 1, 333, 64, "bf16", 0, SOFTMAX, False, 0.0),
+    (1, 2, 500, 128, "bf16", 0, RELU, False, 0.0),
+    (1, 1, 190, 64, "f32", 64, RELU, False, 0.0),
+]
+
+
+@pytest.mark.parametrize("B,H,L,M,dtype,chunk,kernel,renorm,eps", CAUSAL_CASES)
+def test_causal_generalized_parity(B, H, L, M, dtype, chunk, kernel, renorm, eps):
+    import torch
+    fv = _fv()
+    Q, K, V = _qkv(B, H, L, dtype, seed=41 + L + M)
+    W, b = _features(19 + L, H, M)
+    out = fv.attn_causal(*_dev(dtype, Q, K, V), to_dev(W), to_dev(b), S64, denom_eps=eps,
+                         chunk=chunk, kernel=kernel, renormalize=renorm)
+    torch.cuda.synchronize()
+    parity(to_host(out), Q, K, V, W, b, S64, True, dtype, eps=eps, kernel=kernel,
+           renormalize=renorm)
+
+
+def test_causal_relu_state_carry_over():
+    """ReLU features: two calls with the state handed on equal one call, and
+    state_out is K'^T [V 1] of the oracle's features."""
+    import torch
+    fv = _fv()
+    Q, K, V = _qkv(1, 2, 600, "bf16", seed=8)
+    W, b = _features(8, 2, 128)
+    args = dict(kernel=fv.KERNEL_RELU)
+    q, k, v = _dev("bf16", Q, K, V)
+    Wd, bd = to_dev(W), to_dev(b)
+    full, st = fv.attn_causal(q, k, v, Wd, bd, S64, return_state=True, **args)
+    a, s1 = fv.attn_causal(q[:, :, :250].contiguous(), k[:, :, :250].contiguous(),
+                           v[:, :, :250].contiguous(), Wd, bd, S64, return_state=True, **args)
+    c, s2 = fv.attn_causal(q[:, :, 250:].contiguous(), k[:, :, 250:].contiguous(),
+                           v[:, :, 250:].contiguous(), Wd, bd, S64, state_in=s1,
+                           return_state=True, **args)
+    torch.cuda.synchronize()
+    parity(to_host(torch.cat([a, c], dim=2)), Q, K, V, W, b, S64, True, "bf16", kernel=RELU)
+    Kp = favor.feature_map_relu(K.astype(np.float64), W.astype(np.float64), S64)
+    C = np.concatenate([V, np.ones(V.shape[:-1] + (1,))], axis=-1)
+    ref = np.matmul(np.swapaxes(Kp, -1, -2), C)
+    for s in (st, s2):
+        got = to_host(s)
+        assert np.max(np.abs(got - ref)) / np.max(np.abs(ref)) <= TOL["bf16"]
+
+
+# ---------------------------------------------------------------- both directions
+@pytest.mark.parametrize("dtype,kernel,renorm", [
+    ("bf16", RELU, True), ("bf16", SOFTMAX, False), ("f32", RELU, False),
+])
+def test_both_directions_generalized(dtype, kernel, renorm):
+    import torch
+    fv = _fv()
+    L, M = 700, 128
+    Q, K, V = _qkv(2, 2, L, dtype, seed=51)
+    W, b = _features(51, 2, M)
+    ob, oc = fv.attn_both(*_dev(dtype, Q, K, V), to_dev(W), to_dev(b), S64, kernel=kernel,
+                          renormalize=renorm)
+    torch.cuda.synchronize()
+    kw = dict(kernel=kernel, renormalize=renorm)
+    parity(to_host(ob), Q, K, V, W, b, S64, False, dtype, **kw)
+    parity(to_host(oc), Q, K, V, W, b, S64, True, dtype, **kw)
