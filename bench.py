@@ -21,7 +21,8 @@ the chip, so there the draw delays them instead of hiding. A third region,
 serial, with every launch bracketed by HIP events on its stream, gives the
 per-kernel durations and the roofline entry for the dominant
 kernel. The line also carries the fp64 CPU oracle timed on this host
-(cpu_baseline).
+(cpu_baseline), and under "variants" the same step with generalized attention
+(ReLU features) and with the renormalisation off, timed the same way.
 """
 import argparse
 import json
@@ -50,13 +51,17 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = os.path.join(ROOT, "paper_2006_03555_amd", "csrc")
 
 
+# Sources of the kernels the bench step launches and of their launch planning.
+STEP_SOURCES = ("bidir.hip", "causal.hip", "feature_map.hip", "orf_draw.hip", "favor_api.cpp",
+                "favor_common.hpp", "kernels.hpp", "tile_common.hpp")
+
+
 def kernel_source_hash():
     import hashlib
     h = hashlib.sha256()
-    for fn in sorted(os.listdir(KERNEL_SOURCES)):
-        if fn.endswith((".hip", ".hpp", ".cpp")):
-            with open(os.path.join(KERNEL_SOURCES, fn), "rb") as f:
-                h.update(fn.encode() + b"\0" + f.read())
+    for fn in STEP_SOURCES:
+        with open(os.path.join(KERNEL_SOURCES, fn), "rb") as f:
+            h.update(fn.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 
@@ -149,6 +154,9 @@ def main():
                          "(the GPU clocks settle over a few hundred milliseconds)")
     ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the ReLU and unnormalised variants (profiler runs that "
+                         "average counters over every launch of a kernel)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of the workload, time a plain device-to-device copy of this "
                          "many bytes (reference for HBM bandwidth and for scaling the "
@@ -190,20 +198,22 @@ def main():
     ev_draw = [torch.cuda.Event(), torch.cuda.Event()]   # slot k drawn
     ev_attn = [torch.cuda.Event(), torch.cuda.Event()]   # attention done reading slot k
 
-    def attention(slot):
+    def attention(slot, opts=None):
+        opts = opts or {}
         if op == 2:     # one key pass serves both directions
             fv.attn_both(Qd, Kd, Vd, Wd[slot], bd[slot], s, out_bidir=out_b, out_causal=out_c,
-                         workspace=ws, stream=s_main)
+                         workspace=ws, stream=s_main, **opts)
         elif op == 0:
-            fv.attn_bidir(Qd, Kd, Vd, Wd[slot], bd[slot], s, out=out_b, workspace=ws, stream=s_main)
+            fv.attn_bidir(Qd, Kd, Vd, Wd[slot], bd[slot], s, out=out_b, workspace=ws,
+                          stream=s_main, **opts)
         else:
             fv.attn_causal(Qd, Kd, Vd, Wd[slot], bd[slot], s, out=out_c, workspace=ws,
-                           stream=s_main)
+                           stream=s_main, **opts)
 
-    def step_serial(i):
+    def step_serial(i, opts=None):
         """Draw this step's features, then attend with them (one stream)."""
         fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
-        attention(0)
+        attention(0, opts)
 
     def prime(i):
         """Draw the features of step i ahead of the pipelined steps."""
@@ -273,6 +283,27 @@ def main():
     kt = fv.timing_read()
     kernels = {k: {"ms_per_launch": v[0] / v[1], "launches_per_step": v[1] / args.steps}
                for k, v in kt.items() if v[1] > 0}
+    first += args.steps
+
+    # the same step with generalized attention (ReLU features) and without the
+    # renormalisation: same draw, same launches, other feature epilogue / finalisation
+    variants = {}
+    for name, opts in () if args.no_variants else (
+            ("relu", dict(kernel=fv.KERNEL_RELU)),
+            ("softmax_no_renormalize", dict(renormalize=False))):
+        step_v = lambda i, o=opts: step_serial(i, o)
+        for i in range(args.warmup):
+            step_v(first + i)
+        first += args.warmup
+        ms_v = timed_region(step_v, first)
+        first += args.steps
+        ms_vi = timed_region(step_v, first, instrumented=True)
+        first += args.steps
+        kv = fv.timing_read()
+        variants[name] = {
+            "ms_per_step": ms_v, "value": w.B * w.H * w.L / (ms_v / 1e3),
+            "ms_per_step_instrumented": ms_vi,
+            "kernels": {k: {"ms_per_launch": v[0] / v[1]} for k, v in kv.items() if v[1] > 0}}
 
     token_heads = w.B * w.H * w.L
     value = token_heads / (ms_step / 1e3)
@@ -320,6 +351,7 @@ def main():
         "ms_per_step_pipelined": ms_step_pipelined,
         "ms_per_step_instrumented": ms_step_instrumented,
         "roofline": roof,
+        "variants": variants,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, Q, K, V)
