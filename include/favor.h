@@ -115,9 +115,11 @@ FAVOR_API favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M,
  * favor_feature_map - X' = D_X X-hat, the paper's Q' = D_Q Q-hat (Sec. 2.3,
  * Eqs. dqdk and qkprime) with Gaussian-kernel features (c = sqrt 2, f = cos):
  *   X'[l][m] = exp(||x~_l||^2 / 2) * sqrt(2/M) * cos(omega_m . x~_l + b_m),
- *   x~_l = input_scale * X[l].
+ *   x~_l = input_scale * X[l];
+ * with g->kernel = FAVOR_KERNEL_RELU the generalized-attention features
+ *   X'[l][m] = max(omega_m . x~_l, 0) / sqrt(M) + g->kernel_eps   (b unused).
  * X [B][H][L][d] in g->in_dtype -> Xprime [B][H][L][M] in g->out_dtype.
- * g->denom_eps and g->chunk are ignored.
+ * g->denom_eps, g->chunk and g->no_renormalize are ignored.
  */
 FAVOR_API favor_status favor_feature_map(const favor_desc *g, const void *X, const float *W,
                                const float *b, void *Xprime, void *stream);
@@ -134,8 +136,9 @@ FAVOR_API size_t favor_workspace_size(const favor_desc *g, int causal);
  * favor_attn_bidir - bidirectional FAVOR (Sec. 2.5, Algorithm 1):
  *   C = [V 1_L], Buf1 = K'^T C (M x (d+1)), Buf2 = Q' Buf1,
  *   out = diag(buf4 + denom_eps)^-1 Buf3 with [Buf3 buf4] = Buf2,
- * where Q', K' are the feature maps of favor_feature_map. The L x L matrix
- * Q' K'^T and the L x M features are never stored. Deterministic (no atomics).
+ * where Q', K' are the feature maps of favor_feature_map for g->kernel. With
+ * g->no_renormalize = 1 the result is Buf3 itself. The L x L matrix Q' K'^T and
+ * the L x M features are never stored. Deterministic (no atomics).
  */
 FAVOR_API favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
                               const void *V, const float *W, const float *b, void *out,
@@ -143,7 +146,8 @@ FAVOR_API favor_status favor_attn_bidir(const favor_desc *g, const void *Q, cons
 
 /*
  * favor_attn_causal - unidirectional FAVOR by prefix sums (Sec. 2.5.1, Eq.
- * cumsum): row i of the result is (G^PS_i)^T Q'_i normalised as in Algorithm 1,
+ * cumsum): row i of the result is (G^PS_i)^T Q'_i normalised as in Algorithm 1
+ * (not normalised with g->no_renormalize = 1; features as for favor_attn_bidir),
  * G^PS_i = S_0 + sum_{j <= i} K'_j C_j^T (keys up to and including i). The
  * prefix tensor is never stored: workgroups scan chunks of tokens carrying an
  * M x (d+1) fp32 state.
