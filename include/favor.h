@@ -175,8 +175,50 @@ FAVOR_API favor_status favor_attn_both(const favor_desc *g, const void *Q, const
                                        const float *state_in, float *state_out,
                                        void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * Backward pass (the paper trains through FAVOR and benchmarks its backward
+ * pass, Sec. 4.1): gradients of a loss with respect to Q, K, V given
+ * dout = dLoss/dout, for the same descriptor, inputs and features as the
+ * forward call. Algorithm 1 and Eq. cumsum are taken in reverse:
+ *   [dBuf3 dbuf4] from the normalisation (dBuf3 = dout / (buf4 + eps), dbuf4 =
+ *   -(dout . out) / (buf4 + eps); dout and 0 without renormalisation),
+ *   dQ' = dBuf2 Buf1^T, dBuf1 = Q'^T dBuf2, dK' = C dBuf1^T, dV = (K' dBuf1)[:, :d],
+ * then through the feature maps. The forward quantities are recomputed (nothing
+ * from the forward call is needed); W and b receive no gradient.
+ * dout, dQ, dK, dV: [B][H][L][d] in in_dtype; out_dtype must equal in_dtype
+ * (FAVOR_ERR_UNSUPPORTED otherwise). fp32 inputs: M <= 128. Deterministic (no
+ * atomics). dQ, dK, dV are written in full (ragged tails included).
+ * Workspace: favor_backward_workspace_size(g, causal) bytes, 256-byte aligned.
+ */
+FAVOR_API size_t favor_backward_workspace_size(const favor_desc *g, int causal);
+
+/* favor_attn_bidir_backward - gradients of favor_attn_bidir. */
+FAVOR_API favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q,
+                                                 const void *K, const void *V, const float *W,
+                                                 const float *b, const void *dout, void *dQ,
+                                                 void *dK, void *dV, void *ws, size_t ws_bytes,
+                                                 void *stream);
+
+/*
+ * favor_attn_causal_backward - gradients of favor_attn_causal (Eq. cumsum):
+ * dQ'_i = G^PS_i dBuf2_i with the prefix aggregate, and with the suffix
+ * R_j = dstate_out + sum_{i >= j} Q'_i dBuf2_i^T: dK'_j = R_j C_j,
+ * dV_j = (R_j^T K'_j)[:d]. state_in (nullable) as in the forward call;
+ * dstate_out (nullable) [B][H][M][d+1] fp32: the gradient reaching state_out;
+ * dstate_in (nullable) [B][H][M][d+1] fp32: receives the gradient of state_in
+ * (R_1), so a sequence processed in pieces is differentiated piece by piece
+ * from the last. L = 0 copies dstate_out (or zeros) to dstate_in.
+ */
+FAVOR_API favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q,
+                                                  const void *K, const void *V, const float *W,
+                                                  const float *b, const float *state_in,
+                                                  const void *dout, const float *dstate_out,
+                                                  void *dQ, void *dK, void *dV, float *dstate_in,
+                                                  void *ws, size_t ws_bytes, void *stream);
+
 /* Host-only validation of a descriptor for an operation (0 feature map,
- * 1 bidirectional, 2 causal, 3 both); launches nothing and touches no device. */
+ * 1 bidirectional, 2 causal, 3 both, 4 bidirectional backward, 5 causal
+ * backward); launches nothing and touches no device. */
 FAVOR_API favor_status favor_validate_desc(const favor_desc *g, int op);
 
 FAVOR_API const char *favor_status_string(favor_status s);
@@ -202,7 +244,7 @@ FAVOR_API favor_status favor_timing_read(int32_t k, double *ms, int64_t *count);
 /* ABI version of this header; bumped on any incompatible change. */
 FAVOR_API int32_t favor_abi_version(void);
 
-#define FAVOR_ABI_VERSION 2
+#define FAVOR_ABI_VERSION 3
 
 #ifdef __cplusplus
 }

@@ -125,16 +125,14 @@ def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_
     G = np.zeros(Kp.shape[:-2] + (M, d + 1))
     if state_in is not None:
         G = G + np.asarray(state_in, dtype=np.float64)
-    Buf2 = np.zeros(C.shape)
+    dBuf2 = np.zeros(C.shape)
     dQp = np.zeros(Qp.shape)
-    Gs = []
     for i in range(L):
         G = G + Kp[..., i, :, None] * C[..., i, None, :]
-        Buf2[..., i, :] = np.einsum("...m,...mp->...p", Qp[..., i, :], G)
-        Gs.append(G)
-    dBuf2 = _dbuf2(Buf2, dout, denom_eps, renormalize)
-    for i in range(L):
-        dQp[..., i, :] = np.einsum("...mp,...p->...m", Gs[i], dBuf2[..., i, :])
+        Buf2_i = np.einsum("...m,...mp->...p", Qp[..., i, :], G)
+        dBuf2[..., i, :] = _dbuf2(Buf2_i[..., None, :], dout[..., i, None, :], denom_eps,
+                                  renormalize)[..., 0, :]
+        dQp[..., i, :] = np.einsum("...mp,...p->...m", G, dBuf2[..., i, :])
     R = np.zeros(Kp.shape[:-2] + (M, d + 1))
     if dstate_out is not None:
         R = R + np.asarray(dstate_out, dtype=np.float64)

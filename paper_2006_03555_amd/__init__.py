@@ -19,14 +19,14 @@ import os
 
 from ._lib import (  # noqa: F401
     BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, OP_BIDIR, OP_BOTH, OP_CAUSAL, OP_FEATURE_MAP,
-    KERNEL_RELU, KERNEL_SOFTMAX,
+    OP_BIDIR_BACKWARD, OP_CAUSAL_BACKWARD, KERNEL_RELU, KERNEL_SOFTMAX, backward_workspace_size,
     FavorDesc, FavorError, FavorLibraryMissing, lib, lib_path, make_desc, status_string,
     validate_desc, workspace_size, last_error, timing_enable, timing_reset, timing_read,
 )
 
 __all__ = [
     "orf_draw", "feature_map", "attn_bidir", "attn_causal", "attn_both", "workspace_size",
-    "make_desc",
+    "attn_bidir_backward", "attn_causal_backward", "backward_workspace_size", "make_desc",
     "validate_desc", "FavorError", "FavorLibraryMissing", "lib", "lib_path",
 ]
 
@@ -235,6 +235,70 @@ def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_s
     if return_state:
         return out_bidir, out_causal, state_out
     return out_bidir, out_causal
+
+
+def _bwd_workspace(g, causal, workspace):
+    torch = _torch()
+    n = backward_workspace_size(g, causal)
+    if workspace is None:
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8,
+                                device=torch.device("cuda", torch.cuda.current_device()))
+    return workspace, workspace.numel() * workspace.element_size()
+
+
+def _bwd_grads(Q, dQ, dK, dV):
+    torch = _torch()
+    out = []
+    for name, t in (("dQ", dQ), ("dK", dK), ("dV", dV)):
+        if t is None:
+            t = torch.empty_like(Q)
+        _require_like(t, Q.shape, Q.dtype, name)
+        out.append(t)
+    return out
+
+
+def attn_bidir_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, dQ=None, dK=None,
+                        dV=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
+                        renormalize=True, kernel_eps=1e-3):
+    """Gradients (dQ, dK, dV) of attn_bidir for the upstream gradient dout
+    (favor_attn_bidir_backward; the forward pass is recomputed)."""
+    g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps,
+                  others=(("K", K), ("V", V), ("dout", dout)),
+                  opts=_opts(kernel, renormalize, kernel_eps))
+    _require_features(W, b, g.H, g.M, g.d)
+    dQ, dK, dV = _bwd_grads(Q, dQ, dK, dV)
+    _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV)
+    ws, nbytes = _bwd_workspace(g, False, workspace)
+    _check(lib().favor_attn_bidir_backward(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W),
+                                           _ptr(b), _ptr(dout), _ptr(dQ), _ptr(dK), _ptr(dV),
+                                           _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
+    return dQ, dK, dV
+
+
+def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_in=None,
+                         dstate_out=None, return_state_grad=False, dQ=None, dK=None, dV=None,
+                         dstate_in=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
+                         renormalize=True, kernel_eps=1e-3):
+    """Gradients of attn_causal (favor_attn_causal_backward). Returns (dQ, dK, dV), plus
+    dstate_in [B, H, M, d+1] when return_state_grad is true."""
+    torch = _torch()
+    g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps,
+                  others=(("K", K), ("V", V), ("dout", dout)),
+                  opts=_opts(kernel, renormalize, kernel_eps))
+    _require_features(W, b, g.H, g.M, g.d)
+    dQ, dK, dV = _bwd_grads(Q, dQ, dK, dV)
+    sshape = (g.B, g.H, g.M, g.d + 1)
+    if return_state_grad and dstate_in is None:
+        dstate_in = torch.empty(sshape, dtype=torch.float32, device=Q.device)
+    for name, t in (("state_in", state_in), ("dstate_out", dstate_out), ("dstate_in", dstate_in)):
+        _require_like(t, sshape, torch.float32, name)
+    _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV, state_in, dstate_out, dstate_in)
+    ws, nbytes = _bwd_workspace(g, True, workspace)
+    _check(lib().favor_attn_causal_backward(
+        ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b), _ptr(state_in), _ptr(dout),
+        _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(dstate_in), _ptr(ws),
+        ctypes.c_size_t(nbytes), _stream(stream)))
+    return (dQ, dK, dV, dstate_in) if return_state_grad else (dQ, dK, dV)
 
 
 def library_loaded_from():

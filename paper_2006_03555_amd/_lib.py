@@ -11,6 +11,8 @@ OP_FEATURE_MAP = 0
 OP_BIDIR = 1
 OP_CAUSAL = 2
 OP_BOTH = 3
+OP_BIDIR_BACKWARD = 4
+OP_CAUSAL_BACKWARD = 5
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
@@ -61,6 +63,11 @@ def lib():
         "favor_attn_bidir": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_attn_causal": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_attn_both": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_backward_workspace_size": (sz, [dp, ctypes.c_int]),
+        "favor_attn_bidir_backward": (ctypes.c_int,
+                                      [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_causal_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                      vp, vp, vp, vp, sz, vp]),
         "favor_validate_desc": (ctypes.c_int, [dp, ctypes.c_int]),
         "favor_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "favor_last_error": (ctypes.c_char_p, []),
@@ -92,7 +99,7 @@ def last_error():
 
 KERNEL_SOFTMAX = 0
 KERNEL_RELU = 1
-ABI_VERSION = 2   # favor_desc with kernel, no_renormalize, kernel_eps
+ABI_VERSION = 3   # favor_desc with kernel, no_renormalize, kernel_eps; backward entry points
 
 
 def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, chunk=0,
@@ -103,6 +110,10 @@ def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, ch
 
 def validate_desc(g, op):
     return lib().favor_validate_desc(ctypes.byref(g), op)
+
+
+def backward_workspace_size(g, causal):
+    return lib().favor_backward_workspace_size(ctypes.byref(g), 1 if causal else 0)
 
 
 def workspace_size(g, causal):

@@ -19,8 +19,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfavor.so")
 ARCH = "gfx950"
 
-SOURCES = ["orf_draw.hip", "feature_map.hip", "bidir.hip", "causal.hip", "favor_api.cpp",
-           "timing.cpp"]
+SOURCES = ["orf_draw.hip", "feature_map.hip", "bidir.hip", "causal.hip", "backward.hip",
+           "favor_api.cpp", "timing.cpp"]
 
 # Packed fp32 arithmetic is disabled for all device code (no v_pk_*_f32).
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -30,6 +30,7 @@ PER_SOURCE_FLAGS = {
     "feature_map.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "bidir.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "causal.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "backward.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
                 "-Wno-unused-function", "-I", os.path.join(ROOT, "include")]

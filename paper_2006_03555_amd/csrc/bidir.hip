@@ -80,12 +80,15 @@ struct KsideSmem<T, M, 1> {
   KVTile<T> tl[1][2];
 };
 
-template <typename T, int M, int NG, int KN>
+// AGG (backward pass): K holds the queries and V the output gradient; the value
+// rows are weighted by aux[t].x and aux[t].y takes the place of the ones column,
+// so the partials are sum_t Q-hat_t^T [a_t dout_t, e_t]. W'' is not stored.
+template <typename T, int M, int NG, int KN, bool AGG = false>
 __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k_kside(
     const T *__restrict__ K, const T *__restrict__ V, const float *__restrict__ W,
     const float *__restrict__ b, typename Mma<T>::frag *__restrict__ wfr,
     float *__restrict__ bqg, float *__restrict__ part, int H, int L, int rows_per_split,
-    int nsplit, float s, float ws, float bs, float keps) {
+    int nsplit, float s, float ws, float bs, float keps, const float2 *__restrict__ aux) {
   const int item = xcd_item(blockIdx.x, gridDim.x);
   const int bh = item / nsplit;
   const int split = item - bh * nsplit;
@@ -120,7 +123,7 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
   fill_w_bfrags_lds<T, M, 256 * NG>(sm.WB, sm.bq, W + (size_t)h * M * kD, b + (size_t)h * M,
                                     ws, bs);
   __syncthreads();
-  if (bh < H && split == 0) {   // one workgroup per head stores W'' and b'' for later launches
+  if (!AGG && bh < H && split == 0) {   // one workgroup per head stores W'' and b'' for later launches
     constexpr int NF = (M / 16) * 2 * 64;
     frag *dst = wfr + (size_t)h * NF;
     for (int i = threadIdx.x; i < NF; i += 256 * NG) dst[i] = (&sm.WB[0][0][0])[i];
@@ -143,7 +146,16 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
 #pragma unroll
     for (int nb = 0; nb < 5; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  stage_tile<T, KN>(sm.tl[G][0], rg, sel, r0 + 64 * G, r1, s2half, cM, tid);
+  // the row weights of the backward pass's aggregation (0 past r1)
+  auto stage_agg = [&](KVTile<T> &tl, int t0) __attribute__((always_inline)) {
+    const int t = t0 + (tid >> 2);
+    const float2 a = t < r1 ? aux[(size_t)bh * L + t] : float2{0.f, 0.f};
+    stage_tile_rows<T>(tl, rg, sel, a.x, a.y, tid);
+  };
+  if constexpr (AGG)
+    stage_agg(sm.tl[G][0], r0 + 64 * G);
+  else
+    stage_tile<T, KN>(sm.tl[G][0], rg, sel, r0 + 64 * G, r1, s2half, cM, tid);
   __syncthreads();
   int buf = 0;
   for (int it = 0; it < nit; ++it, buf ^= 1) {
@@ -169,7 +181,12 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
         acc[mb][4] = P::mma(a, db, acc[mb][4]);
       }
     }
-    if (next) stage_tile<T, KN>(sm.tl[G][buf ^ 1], rg, sel, tn, r1, s2half, cM, tid);
+    if (next) {
+      if constexpr (AGG)
+        stage_agg(sm.tl[G][buf ^ 1], tn);
+      else
+        stage_tile<T, KN>(sm.tl[G][buf ^ 1], rg, sel, tn, r1, s2half, cM, tid);
+    }
     __syncthreads();
   }
 
@@ -273,13 +290,16 @@ constexpr int kFinDiv = 0;
 constexpr int kFinDivEps = 1;
 constexpr int kFinScale = 2;
 
-template <typename T, typename To, int M, int KN, int FIN>
+// SAVE: also write the row's 1 / (D-hat + eps) in the units of the unscaled
+// features (rsave [B*H][L]), which the backward pass reads.
+template <typename T, typename To, int M, int KN, int FIN, bool SAVE>
 __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *__restrict__ Q,
                                                   const typename Mma<T>::frag *__restrict__ wfr,
                                                   const float *__restrict__ bqg,
                                                   const typename Mma<T>::frag *__restrict__ frags,
-                                                  To *__restrict__ out, int H, int L, float s,
-                                                  float eps, float keps, int ntiles, int nitems) {
+                                                  To *__restrict__ out, float *__restrict__ rsave,
+                                                  int H, int L, float s, float eps, float keps,
+                                                  int ntiles, int nitems) {
   constexpr int NS = M / 32;
   constexpr int TBW = QsideCfg<T>::TBW;
   using P = Mma<T>;
@@ -395,6 +415,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
       if (t < L) {
         const float inv =
             FIN == kFinScale ? epsq[tb] : __builtin_amdgcn_rcpf(acc[4][tb][0] + epsq[tb]);
+        if constexpr (SAVE) {
+          if (g == 0) rsave[(size_t)bh * L + t] = inv;
+        }
         // blocks 2 p, 2 p + 1 hold value columns 32 p + 8 g .. + 7 in this lane
 #pragma unroll
         for (int pp = 0; pp < 2; ++pp)
@@ -414,24 +437,27 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
     default: return hipErrorInvalidValue;                           \
   }
 
-template <int KN>
+template <int KN, bool AGG>
 static hipError_t kside_kernel(const Shape &sh, Dt in, const void *K, const void *V,
                                const float *W, const float *b, void *wfr, float *bq, float *part,
-                               int rows_per_split, int nsplit, hipStream_t st) {
+                               int rows_per_split, int nsplit, hipStream_t st,
+                               const float2 *aux) {
   dim3 grid(nsplit * sh.BH);
   float ws, bs;
   feature_scales(sh, ws, bs);
   if (in == Dt::BF16) {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<bf16, MM, kside_groups(Dt::BF16, MM), KN>),
-                                               grid, dim3(256 * kside_groups(Dt::BF16, MM)), 0, st,
-                                               (const bf16 *)K, (const bf16 *)V, W, b,
-                                               (Mma<bf16>::frag *)wfr, bq, part, sh.H, sh.L,
-                                               rows_per_split, nsplit, sh.s, ws, bs, sh.keps));
+    FAVOR_DISPATCH_M(sh.M,
+                     hipLaunchKernelGGL((k_kside<bf16, MM, kside_groups(Dt::BF16, MM), KN, AGG>),
+                                        grid, dim3(256 * kside_groups(Dt::BF16, MM)), 0, st,
+                                        (const bf16 *)K, (const bf16 *)V, W, b,
+                                        (Mma<bf16>::frag *)wfr, bq, part, sh.H, sh.L,
+                                        rows_per_split, nsplit, sh.s, ws, bs, sh.keps, aux));
   } else {
-    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM, 1, KN>), grid, dim3(256), 0, st,
-                                               (const float *)K, (const float *)V, W, b,
+    FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM, 1, KN, AGG>), grid, dim3(256),
+                                               0, st, (const float *)K, (const float *)V, W, b,
                                                (Mma<float>::frag *)wfr, bq, part, sh.H, sh.L,
-                                               rows_per_split, nsplit, sh.s, ws, bs, sh.keps));
+                                               rows_per_split, nsplit, sh.s, ws, bs, sh.keps,
+                                               aux));
   }
   return hipGetLastError();
 }
@@ -439,9 +465,19 @@ static hipError_t kside_kernel(const Shape &sh, Dt in, const void *K, const void
 hipError_t launch_kside(const Shape &sh, Dt in, const void *K, const void *V, const float *W,
                         const float *b, void *wfr, float *bq, float *part, int rows_per_split,
                         int nsplit, hipStream_t st) {
-  return sh.kernel == 1
-             ? kside_kernel<kRelu>(sh, in, K, V, W, b, wfr, bq, part, rows_per_split, nsplit, st)
-             : kside_kernel<kCos>(sh, in, K, V, W, b, wfr, bq, part, rows_per_split, nsplit, st);
+  return sh.kernel == 1 ? kside_kernel<kRelu, false>(sh, in, K, V, W, b, wfr, bq, part,
+                                                     rows_per_split, nsplit, st, nullptr)
+                        : kside_kernel<kCos, false>(sh, in, K, V, W, b, wfr, bq, part,
+                                                    rows_per_split, nsplit, st, nullptr);
+}
+
+hipError_t launch_kside_agg(const Shape &sh, Dt in, const void *Q, const void *dout,
+                            const float *W, const float *b, const float2 *aux, float *part,
+                            int rows_per_split, int nsplit, hipStream_t st) {
+  return sh.kernel == 1 ? kside_kernel<kRelu, true>(sh, in, Q, dout, W, b, nullptr, nullptr,
+                                                    part, rows_per_split, nsplit, st, aux)
+                        : kside_kernel<kCos, true>(sh, in, Q, dout, W, b, nullptr, nullptr, part,
+                                                   rows_per_split, nsplit, st, aux);
 }
 
 hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit, void *frags,
@@ -461,16 +497,18 @@ hipError_t launch_finalize(const Shape &sh, Dt in, const float *part, int nsplit
 // XCD-local range of row tiles.
 constexpr int kQsideMaxWorkgroups = 512;
 
-template <typename T, typename To, int KN, int FIN>
+template <typename T, typename To, int KN, int FIN, bool SAVE = false>
 static hipError_t qside_launch(const Shape &sh, const void *Q, const void *wfr, const float *bq,
-                               const void *frags, void *o, hipStream_t st) {
+                               const void *frags, void *o, hipStream_t st,
+                               float *rsave = nullptr) {
   const int rows = 64 * QsideCfg<T>::TBW;
   const int ntiles = (sh.L + rows - 1) / rows;
   const int nitems = ntiles * sh.BH;
   dim3 grid(min(nitems, kQsideMaxWorkgroups));
-  FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM, KN, FIN>), grid, dim3(256), 0, st,
-                                             (const T *)Q, (const typename Mma<T>::frag *)wfr,
-                                             bq, (const typename Mma<T>::frag *)frags, (To *)o,
+  FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_qside<T, To, MM, KN, FIN, SAVE>), grid, dim3(256),
+                                             0, st, (const T *)Q,
+                                             (const typename Mma<T>::frag *)wfr, bq,
+                                             (const typename Mma<T>::frag *)frags, (To *)o, rsave,
                                              sh.H, sh.L, sh.s, sh.eps, sh.keps, ntiles, nitems));
   return hipGetLastError();
 }
@@ -488,6 +526,25 @@ static hipError_t qside_typed(const Shape &sh, const void *Q, const void *wfr, c
                               const void *frags, void *o, hipStream_t st) {
   return sh.kernel == 1 ? qside_kernel<T, To, kRelu>(sh, Q, wfr, bq, frags, o, st)
                         : qside_kernel<T, To, kCos>(sh, Q, wfr, bq, frags, o, st);
+}
+
+template <typename T, int KN>
+static hipError_t qside_save(const Shape &sh, const void *Q, const void *wfr, const float *bq,
+                             const void *frags, void *o, float *rsave, hipStream_t st) {
+  if (sh.eps != 0.f)
+    return qside_launch<T, T, KN, kFinDivEps, true>(sh, Q, wfr, bq, frags, o, st, rsave);
+  return qside_launch<T, T, KN, kFinDiv, true>(sh, Q, wfr, bq, frags, o, st, rsave);
+}
+
+hipError_t launch_qside_save(const Shape &sh, Dt in, const void *Q, const void *wfr,
+                             const float *bq, const void *frags, void *o, float *rsave,
+                             hipStream_t st) {
+  if (!sh.renorm) return hipErrorInvalidValue;
+  if (in == Dt::BF16)
+    return sh.kernel == 1 ? qside_save<bf16, kRelu>(sh, Q, wfr, bq, frags, o, rsave, st)
+                          : qside_save<bf16, kCos>(sh, Q, wfr, bq, frags, o, rsave, st);
+  return sh.kernel == 1 ? qside_save<float, kRelu>(sh, Q, wfr, bq, frags, o, rsave, st)
+                        : qside_save<float, kCos>(sh, Q, wfr, bq, frags, o, rsave, st);
 }
 
 hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const void *wfr,

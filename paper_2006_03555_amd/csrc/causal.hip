@@ -113,14 +113,17 @@ struct CausalSmem {
   float bq[M];
 };
 
-template <typename T, typename To, int M, int KN, bool RN>
+// SAVE: also write each row's 1 / (D-hat + eps) in units of the unscaled
+// features (rsave [B*H][L]) for the backward pass.
+template <typename T, typename To, int M, int KN, bool RN, bool SAVE>
 __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T *__restrict__ K,
                                                 const T *__restrict__ V,
                                                 const typename Mma<T>::frag *__restrict__ wfr,
                                                 const float *__restrict__ bqg,
                                                 const float *__restrict__ prefix,
-                                                To *__restrict__ out, int H, int L, int seg_len,
-                                                int nseg, float s, float eps, float keps) {
+                                                To *__restrict__ out, float *__restrict__ rsave,
+                                                int H, int L, int seg_len, int nseg, float s,
+                                                float eps, float keps) {
   constexpr int MW = M / 4;
   constexpr int MB = MW / 16;
   constexpr int NS = M / 32;
@@ -343,6 +346,9 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
       const float inv = RN ? 1.0f / (o[4][0] + epsq) : epsq;
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) store4(Oh + (size_t)qt * kD + nb * 16 + 4 * g, o[nb] * inv);
+      if constexpr (SAVE) {
+        if (g == 0) rsave[(size_t)bh * L + qt] = inv;
+      }
     }
     __syncthreads();
   }
@@ -492,16 +498,16 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
   }
 }
 
-template <typename To, int M, int KN, bool RN>
+template <typename To, int M, int KN, bool RN, bool SAVE>
 __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
                                                    const bf16 *__restrict__ K,
                                                    const bf16 *__restrict__ V,
                                                    const bf16x8 *__restrict__ wfr,
                                                    const float *__restrict__ bqg,
                                                    const float *__restrict__ prefix,
-                                                   To *__restrict__ out, int H, int L,
-                                                   int seg_len, int nseg, float s, float eps,
-                                                   float keps) {
+                                                   To *__restrict__ out, float *__restrict__ rsave,
+                                                   int H, int L, int seg_len, int nseg, float s,
+                                                   float eps, float keps) {
   constexpr int MW = M / 4;          // features per wave
   constexpr int MB = MW / 16;        // 16-feature blocks per wave
   constexpr int KS = (MB + 1) / 2;   // 32-feature k-steps per wave (a lone block is zero-padded)
@@ -600,6 +606,9 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 #pragma unroll
       for (int pp = 0; pp < 2; ++pp)
         store8(Oh + (size_t)qt * kD + 32 * pp + 8 * g, num[2 * pp] * inv, num[2 * pp + 1] * inv);
+      if constexpr (SAVE) {
+        if (g == 0) rsave[(size_t)bh * L + qt] = inv;
+      }
     }
   };
 
@@ -815,50 +824,71 @@ static hipError_t with_variant(const Shape &sh, F &&f) {
   return sh.renorm ? f(cosk{}, std::true_type{}) : f(cosk{}, std::false_type{});
 }
 
-template <typename To>
+template <typename To, bool SAVE = false>
 static hipError_t causal_fs_typed(const Shape &sh, const void *Q, const void *K, const void *V,
                                   const void *wfr, const float *bq, const float *prefix, void *o,
-                                  int seg_len, int nseg, hipStream_t st) {
+                                  int seg_len, int nseg, hipStream_t st, float *rsave = nullptr) {
   dim3 grid(nseg * sh.BH);
   return with_variant(sh, [&](auto kn, auto rn) -> hipError_t {
     constexpr int KN = decltype(kn)::value;
     constexpr bool RN = decltype(rn)::value;
+    if constexpr (SAVE && !RN) {
+      return hipErrorInvalidValue;
+    } else {
 #define FAVOR_CAUSAL_FS_LAUNCH(MM)                                                          \
-  hipLaunchKernelGGL((k_causal_fs<To, MM, KN, RN>), grid, dim3(256), 0, st, (const bf16 *)Q,  \
-                     (const bf16 *)K, (const bf16 *)V, (const bf16x8 *)wfr, bq, prefix,        \
-                     (To *)o, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps, sh.keps)
-    switch (sh.M) {
-      case 64: FAVOR_CAUSAL_FS_LAUNCH(64); break;
-      case 128: FAVOR_CAUSAL_FS_LAUNCH(128); break;
-      case 256: FAVOR_CAUSAL_FS_LAUNCH(256); break;
-      default: return hipErrorInvalidValue;
-    }
+  hipLaunchKernelGGL((k_causal_fs<To, MM, KN, RN, SAVE>), grid, dim3(256), 0, st,             \
+                     (const bf16 *)Q, (const bf16 *)K, (const bf16 *)V, (const bf16x8 *)wfr,   \
+                     bq, prefix, (To *)o, rsave, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps,      \
+                     sh.keps)
+      switch (sh.M) {
+        case 64: FAVOR_CAUSAL_FS_LAUNCH(64); break;
+        case 128: FAVOR_CAUSAL_FS_LAUNCH(128); break;
+        case 256: FAVOR_CAUSAL_FS_LAUNCH(256); break;
+        default: return hipErrorInvalidValue;
+      }
 #undef FAVOR_CAUSAL_FS_LAUNCH
-    return hipGetLastError();
+      return hipGetLastError();
+    }
   });
 }
 
 // fp32 inputs (M <= 128).
-template <typename T, typename To>
+template <typename T, typename To, bool SAVE = false>
 static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, const void *V,
                                const void *wfr, const float *bq, const float *prefix, void *o,
-                               int seg_len, int nseg, hipStream_t st) {
+                               int seg_len, int nseg, hipStream_t st, float *rsave = nullptr) {
   dim3 grid(nseg * sh.BH);
   return with_variant(sh, [&](auto kn, auto rn) -> hipError_t {
     constexpr int KN = decltype(kn)::value;
     constexpr bool RN = decltype(rn)::value;
+    if constexpr (SAVE && !RN) {
+      return hipErrorInvalidValue;
+    } else {
 #define FAVOR_CAUSAL_LAUNCH(MM)                                                             \
-  hipLaunchKernelGGL((k_causal<T, To, MM, KN, RN>), grid, dim3(256), 0, st, (const T *)Q,     \
-                     (const T *)K, (const T *)V, (const typename Mma<T>::frag *)wfr, bq,       \
-                     prefix, (To *)o, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps, sh.keps)
-    switch (sh.M) {
-      case 64: FAVOR_CAUSAL_LAUNCH(64); break;
-      case 128: FAVOR_CAUSAL_LAUNCH(128); break;
-      default: return hipErrorInvalidValue;
-    }
+  hipLaunchKernelGGL((k_causal<T, To, MM, KN, RN, SAVE>), grid, dim3(256), 0, st,             \
+                     (const T *)Q, (const T *)K, (const T *)V,                                 \
+                     (const typename Mma<T>::frag *)wfr, bq, prefix, (To *)o, rsave, sh.H,     \
+                     sh.L, seg_len, nseg, sh.s, sh.eps, sh.keps)
+      switch (sh.M) {
+        case 64: FAVOR_CAUSAL_LAUNCH(64); break;
+        case 128: FAVOR_CAUSAL_LAUNCH(128); break;
+        default: return hipErrorInvalidValue;
+      }
 #undef FAVOR_CAUSAL_LAUNCH
-    return hipGetLastError();
+      return hipGetLastError();
+    }
   });
+}
+
+hipError_t launch_causal_save(const Shape &sh, Dt in, const void *Q, const void *K,
+                              const void *V, const void *wfr, const float *bq,
+                              const float *prefix, void *o, float *rsave, int seg_len, int nseg,
+                              hipStream_t st) {
+  if (!sh.renorm) return hipErrorInvalidValue;
+  if (in == Dt::BF16)
+    return causal_fs_typed<bf16, true>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st, rsave);
+  return causal_typed<float, float, true>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st,
+                                          rsave);
 }
 
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,

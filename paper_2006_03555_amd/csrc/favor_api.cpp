@@ -40,11 +40,18 @@ constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
 constexpr int kCausalWorkgroups = 256;
 constexpr int kMinRowsPerSplit = 256;
 
-enum Op { kOpFeatureMap = 0, kOpBidir = 1, kOpCausal = 2, kOpBoth = 3 };
+enum Op {
+  kOpFeatureMap = 0,
+  kOpBidir = 1,
+  kOpCausal = 2,
+  kOpBoth = 3,
+  kOpBidirBackward = 4,
+  kOpCausalBackward = 5
+};
 
 favor_status validate(const favor_desc *g, int op) {
   if (!g) return fail(FAVOR_ERR_INVALID_ARGUMENT, "descriptor is NULL");
-  if (op < kOpFeatureMap || op > kOpBoth)
+  if (op < kOpFeatureMap || op > kOpCausalBackward)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown operation %d", op);
   if (g->B < 0 || g->H < 0 || g->L < 0)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "negative size B=%d H=%d L=%d", g->B, g->H, g->L);
@@ -74,8 +81,27 @@ favor_status validate(const favor_desc *g, int op) {
   if (bh > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "B*H=%lld exceeds 65535", bh);
   if ((op == kOpCausal || op == kOpBoth) && g->in_dtype == FAVOR_F32 && g->M > 128)
     return fail(FAVOR_ERR_UNSUPPORTED, "causal with fp32 inputs supports M <= 128");
+  if (op == kOpBidirBackward || op == kOpCausalBackward) {
+    if (g->out_dtype != g->in_dtype)
+      return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass needs out_dtype == in_dtype");
+    if (g->in_dtype == FAVOR_F32 && g->M > 128)
+      return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass with fp32 inputs supports M <= 128");
+  }
   return FAVOR_OK;
 }
+
+// Backward workspace: the forward plan's buffers (split or 64-token chunk
+// partials, Buf1^T fragments, W'', b''), then the recomputed output and row
+// reciprocals, the per-row (alpha, alpha u_d), the aggregated q-hat (x) u~
+// partials and, bidirectional, Buf1 and dBuf1 as plain [M][65] arrays.
+struct BwdPlan {
+  int BH = 0;
+  int nsplit = 0;
+  int rows_per_split = 0;
+  size_t part = 0, frags = 0, wfr = 0, bq = 0, out = 0, rsave = 0, aux = 0, part2 = 0,
+         buf1 = 0, dbuf1 = 0;
+  size_t total = 0;
+};
 
 // Workspace: [ split partials | Buf1^T fragments (bidir, both) | W'' fragments | b'' ]
 struct Plan {
@@ -118,6 +144,37 @@ Plan make_plan(const favor_desc *g, int op) {
   p.wfr_bytes = round_up((size_t)g->H * (g->M / 16) * 2 * 64 * fb, 256);
   p.bq_bytes = round_up((size_t)g->H * g->M * sizeof(float), 256);
   p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
+  return p;
+}
+
+BwdPlan make_bwd_plan(const favor_desc *g, bool causal) {
+  BwdPlan p;
+  p.BH = g->B * g->H;
+  if (p.BH == 0 || g->L == 0) return p;
+  const size_t elt = g->in_dtype == FAVOR_BF16 ? 2 : 4;
+  const size_t agg = (size_t)g->M * 65 * sizeof(float);
+  if (causal) {
+    // one 64-token chunk per segment: the segment prefixes are the chunk states
+    p.rows_per_split = 64;
+    p.nsplit = (g->L + 63) / 64;
+  } else {
+    const Plan f = make_plan(g, kOpBidir);
+    p.rows_per_split = f.rows_per_split;
+    p.nsplit = f.nsplit;
+  }
+  const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
+  p.part = round_up((size_t)p.BH * p.nsplit * agg, 256);
+  p.frags = causal ? 0 : round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
+  p.wfr = round_up((size_t)g->H * (g->M / 16) * 2 * 64 * fb, 256);
+  p.bq = round_up((size_t)g->H * g->M * sizeof(float), 256);
+  p.out = round_up((size_t)p.BH * g->L * 64 * elt, 256);
+  p.rsave = round_up((size_t)p.BH * g->L * sizeof(float), 256);
+  p.aux = round_up((size_t)p.BH * g->L * 2 * sizeof(float), 256);
+  p.part2 = p.part;
+  p.buf1 = causal ? 0 : round_up((size_t)p.BH * agg, 256);
+  p.dbuf1 = p.buf1;
+  p.total = p.part + p.frags + p.wfr + p.bq + p.out + p.rsave + p.aux + p.part2 + p.buf1 +
+            p.dbuf1;
   return p;
 }
 
@@ -178,6 +235,12 @@ const char *favor_status_string(favor_status s) {
 favor_status favor_validate_desc(const favor_desc *g, int op) {
   FAVOR_TRY(validate(g, op));
   return ok();
+}
+
+size_t favor_backward_workspace_size(const favor_desc *g, int causal) {
+  const int op = causal ? kOpCausalBackward : kOpBidirBackward;
+  if (validate(g, op) != FAVOR_OK) return 0;
+  return make_bwd_plan(g, causal != 0).total;
 }
 
 size_t favor_workspace_size(const favor_desc *g, int causal) {
@@ -393,6 +456,200 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
                              p.nsplit, st);
   }
   return device_result(e, "favor_attn_both chunk scan");
+}
+
+}  // extern "C"
+
+namespace {
+
+// Carve the backward workspace.
+struct BwdBufs {
+  float *part, *bq, *rsave, *part2, *buf1, *dbuf1;
+  void *frags, *wfr, *out;
+  float2 *aux;
+};
+
+BwdBufs carve(const BwdPlan &p, void *ws) {
+  char *c = static_cast<char *>(ws);
+  BwdBufs b;
+  b.part = reinterpret_cast<float *>(c);
+  c += p.part;
+  b.frags = c;
+  c += p.frags;
+  b.wfr = c;
+  c += p.wfr;
+  b.bq = reinterpret_cast<float *>(c);
+  c += p.bq;
+  b.out = c;
+  c += p.out;
+  b.rsave = reinterpret_cast<float *>(c);
+  c += p.rsave;
+  b.aux = reinterpret_cast<float2 *>(c);
+  c += p.aux;
+  b.part2 = reinterpret_cast<float *>(c);
+  c += p.part2;
+  b.buf1 = reinterpret_cast<float *>(c);
+  c += p.buf1;
+  b.dbuf1 = reinterpret_cast<float *>(c);
+  return b;
+}
+
+favor_status check_workspace(const void *ws, size_t ws_bytes, size_t need) {
+  if (!ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is not 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, need);
+  return FAVOR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const void *K,
+                                       const void *V, const float *W, const float *b,
+                                       const void *dout, void *dQ, void *dK, void *dV, void *ws,
+                                       size_t ws_bytes, void *stream) {
+  FAVOR_TRY(validate(g, kOpBidirBackward));
+  const BwdPlan p = make_bwd_plan(g, false);
+  const bool work = p.total > 0;
+  const void *in_ptrs[] = {Q, K, V, W, b, dout, dQ, dK, dV};
+  const char *names[] = {"Q", "K", "V", "W", "b", "dout", "dQ", "dK", "dV"};
+  for (int i = 0; i < 9; ++i) FAVOR_TRY(check_ptr(in_ptrs[i], names[i], work));
+  if (!work) return ok();
+  FAVOR_TRY(check_workspace(ws, ws_bytes, p.total));
+  const favor::Shape sh = shape_of(g);
+  const favor::Dt in = dt_of(g->in_dtype);
+  hipStream_t st = (hipStream_t)stream;
+  const BwdBufs w = carve(p, ws);
+  hipError_t e;
+  // forward recomputation: Buf1 (and W'' fragments), and the normalised output
+  // with each row's reciprocal
+  {
+    favor::LaunchTimer t(favor::kKerKside, st);
+    e = favor::launch_kside(sh, in, K, V, W, b, w.wfr, w.bq, w.part, p.rows_per_split, p.nsplit,
+                            st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward key pass");
+  if (sh.renorm) {
+    {
+      favor::LaunchTimer t(favor::kKerFinalize, st);
+      e = favor::launch_finalize(sh, in, w.part, p.nsplit, w.frags, st);
+    }
+    if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward reduction");
+    {
+      favor::LaunchTimer t(favor::kKerQside, st);
+      e = favor::launch_qside_save(sh, in, Q, w.wfr, w.bq, w.frags, w.out, w.rsave, st);
+    }
+    if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward query pass");
+  }
+  {
+    favor::LaunchTimer t(favor::kKerSumSplits, st);
+    e = favor::launch_sum_splits(sh, w.part, p.nsplit, w.buf1, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward Buf1");
+  favor::BwdArgs a{Q, K, V, dout, w.out, w.rsave, w.wfr, w.bq, W, w.buf1, dQ, dK, dV, w.aux};
+  {
+    favor::LaunchTimer t(favor::kKerBwdDq, st);
+    e = favor::launch_bwd_dq(sh, in, false, a, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward query gradients");
+  {
+    favor::LaunchTimer t(favor::kKerBwdAgg, st);
+    e = favor::launch_kside_agg(sh, in, Q, dout, W, b, w.aux, w.part2, p.rows_per_split,
+                                p.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward dBuf1 partials");
+  {
+    favor::LaunchTimer t(favor::kKerSumSplits, st);
+    e = favor::launch_sum_splits(sh, w.part2, p.nsplit, w.dbuf1, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward dBuf1");
+  a.state = w.dbuf1;
+  {
+    favor::LaunchTimer t(favor::kKerBwdDkv, st);
+    e = favor::launch_bwd_dkv(sh, in, false, a, st);
+  }
+  return device_result(e, "favor_attn_bidir_backward key and value gradients");
+}
+
+favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, const void *K,
+                                        const void *V, const float *W, const float *b,
+                                        const float *state_in, const void *dout,
+                                        const float *dstate_out, void *dQ, void *dK, void *dV,
+                                        float *dstate_in, void *ws, size_t ws_bytes,
+                                        void *stream) {
+  FAVOR_TRY(validate(g, kOpCausalBackward));
+  const BwdPlan p = make_bwd_plan(g, true);
+  const bool work = p.total > 0;
+  const bool heads = (long long)g->B * g->H > 0;
+  const void *in_ptrs[] = {Q, K, V, W, b, dout, dQ, dK, dV};
+  const char *names[] = {"Q", "K", "V", "W", "b", "dout", "dQ", "dK", "dV"};
+  for (int i = 0; i < 9; ++i) FAVOR_TRY(check_ptr(in_ptrs[i], names[i], work));
+  const void *st_ptrs[] = {state_in, dstate_out, dstate_in};
+  const char *st_names[] = {"state_in", "dstate_out", "dstate_in"};
+  for (int i = 0; i < 3; ++i)
+    if (st_ptrs[i] && !aligned(st_ptrs[i], 16))
+      return fail(FAVOR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", st_names[i]);
+  const favor::Shape sh = shape_of(g);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  if (!work) {
+    // no tokens: the state gradient passes through unchanged
+    if (heads && dstate_in) {
+      {
+        favor::LaunchTimer t(favor::kKerSuffixScan, st);
+        e = favor::launch_suffix_scan(sh, nullptr, 0, dstate_out, dstate_in, st);
+      }
+      return device_result(e, "favor_attn_causal_backward state gradient copy");
+    }
+    return ok();
+  }
+  FAVOR_TRY(check_workspace(ws, ws_bytes, p.total));
+  const favor::Dt in = dt_of(g->in_dtype);
+  const BwdBufs w = carve(p, ws);
+  // forward recomputation with 64-token segments: the chunk states S_c (exclusive
+  // prefixes plus state_in), and the output with each row's reciprocal
+  {
+    favor::LaunchTimer t(favor::kKerKside, st);
+    e = favor::launch_kside(sh, in, K, V, W, b, w.wfr, w.bq, w.part, p.rows_per_split, p.nsplit,
+                            st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward chunk aggregates");
+  {
+    favor::LaunchTimer t(favor::kKerSegScan, st);
+    e = favor::launch_seg_scan(sh, in, w.part, p.nsplit, state_in, nullptr, nullptr, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward chunk states");
+  if (sh.renorm) {
+    favor::LaunchTimer t(favor::kKerCausal, st);
+    e = favor::launch_causal_save(sh, in, Q, K, V, w.wfr, w.bq, w.part, w.out, w.rsave,
+                                  p.rows_per_split, p.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward forward pass");
+  favor::BwdArgs a{Q, K, V, dout, w.out, w.rsave, w.wfr, w.bq, W, w.part, dQ, dK, dV, w.aux};
+  {
+    favor::LaunchTimer t(favor::kKerBwdDq, st);
+    e = favor::launch_bwd_dq(sh, in, true, a, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward query gradients");
+  {
+    favor::LaunchTimer t(favor::kKerBwdAgg, st);
+    e = favor::launch_kside_agg(sh, in, Q, dout, W, b, w.aux, w.part2, p.rows_per_split,
+                                p.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward chunk aggregates");
+  {
+    favor::LaunchTimer t(favor::kKerSuffixScan, st);
+    e = favor::launch_suffix_scan(sh, w.part2, p.nsplit, dstate_out, dstate_in, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward suffix states");
+  a.state = w.part2;
+  {
+    favor::LaunchTimer t(favor::kKerBwdDkv, st);
+    e = favor::launch_bwd_dkv(sh, in, true, a, st);
+  }
+  return device_result(e, "favor_attn_causal_backward key and value gradients");
 }
 
 }  // extern "C"

@@ -64,8 +64,9 @@ template <> struct Mma<bf16> {
     for (int i = 0; i < 8; ++i) r[i] = h;
     return r;
   }
-  // cos(2 pi x): v_cos_f32 takes its argument in revolutions.
+  // cos(2 pi x), sin(2 pi x): v_cos_f32 / v_sin_f32 take revolutions.
   __device__ __forceinline__ static float cos_rev(float x) { return __builtin_amdgcn_cosf(x); }
+  __device__ __forceinline__ static float sin_rev(float x) { return __builtin_amdgcn_sinf(x); }
 };
 
 // fp32 inputs: eight v_mfma_f32_16x16x4_f32 per k32 fragment (slot i = k-step i),
@@ -97,6 +98,7 @@ template <> struct Mma<float> {
     return r;
   }
   __device__ __forceinline__ static float cos_rev(float x) { return cospif(2.0f * x); }
+  __device__ __forceinline__ static float sin_rev(float x) { return sinpif(2.0f * x); }
 };
 
 // ---- element conversions ---------------------------------------------------
@@ -161,6 +163,18 @@ __device__ __forceinline__ float feature(float p, float keps) {
     return fmaxf(p, 0.f) + keps;
   } else {
     return P::cos_rev(p);
+  }
+}
+
+// Derivative factor of a feature with respect to its projection, up to the
+// constant the caller folds in: kCos: sin(2 pi p) (d cos / d theta = -sin);
+// kRelu: the step [p > 0] (0 at p = 0).
+template <int KN, typename P>
+__device__ __forceinline__ float feature_slope(float p) {
+  if constexpr (KN == kRelu) {
+    return p > 0.f ? 1.f : 0.f;
+  } else {
+    return P::sin_rev(p);
   }
 }
 

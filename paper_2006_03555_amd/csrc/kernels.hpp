@@ -73,6 +73,44 @@ hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const voi
 hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const float *state_in,
                            float *state_out, void *total_frags, hipStream_t st);
 
+// Forward passes that also write each row's 1 / (D-hat + eps) in units of the
+// unscaled features (rsave [BH][L]) for the backward pass; renormalised shapes
+// and out dtype = in dtype only.
+hipError_t launch_qside_save(const Shape &sh, Dt in, const void *Q, const void *wfr,
+                             const float *bq, const void *frags, void *o, float *rsave,
+                             hipStream_t st);
+hipError_t launch_causal_save(const Shape &sh, Dt in, const void *Q, const void *K,
+                              const void *V, const void *wfr, const float *bq,
+                              const float *prefix, void *o, float *rsave, int seg_len, int nseg,
+                              hipStream_t st);
+
+// Backward pass. k_kside's weighted mode: part [BH][nsplit][M][65] = sum over
+// each row range of Q-hat_t^T [aux_t.x dout_t, aux_t.y].
+hipError_t launch_kside_agg(const Shape &sh, Dt in, const void *Q, const void *dout,
+                            const float *W, const float *b, const float2 *aux, float *part,
+                            int rows_per_split, int nsplit, hipStream_t st);
+
+// Pointers of one backward launch (device; unused ones may be null).
+struct BwdArgs {
+  const void *Q, *K, *V, *dout, *out;
+  const float *rsave;    // [BH][L] 1 / (D-hat + eps) (renormalised)
+  const void *wfr;       // W'' fragments written by k_kside
+  const float *bq;       // b''
+  const float *W;        // [H][M][d]
+  const float *state;    // dQ: Buf1 [BH][M][65] or prefix states [BH][nch][M][65];
+                         // dK, dV: dBuf1 or suffix states, same layouts
+  void *dQ, *dK, *dV;
+  float2 *aux;           // [BH][L] (alpha, alpha u_d)
+};
+hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st);
+hipError_t launch_bwd_dkv(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st);
+// Fixed-order sum of split partials [BH][ns][M][65] -> [BH][M][65].
+hipError_t launch_sum_splits(const Shape &sh, const float *part, int ns, float *dst,
+                             hipStream_t st);
+// In-place exclusive suffix scan over chunks plus dsout; the total plus dsout to dsin.
+hipError_t launch_suffix_scan(const Shape &sh, float *part, int nch, const float *dsout,
+                              float *dsin, hipStream_t st);
+
 // Causal chunk scan of each segment starting from its prefix state.
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,
                          const void *V, const void *wfr, const float *bq, const float *prefix,
@@ -91,6 +129,11 @@ enum KernelId {
   kKerQside,
   kKerSegScan,
   kKerCausal,
+  kKerSumSplits,
+  kKerBwdDq,
+  kKerBwdAgg,
+  kKerSuffixScan,
+  kKerBwdDkv,
   kNumKernels
 };
 const char *kernel_name(int k);

@@ -104,14 +104,14 @@ __device__ __forceinline__ void load_query_frags(typename Mma<T>::frag (&qf)[2],
   }
 }
 
-// Stage a prefetched tile into LDS: keys row-major, D_K(t) = sqrt(2/M)
-// exp(||s k_t||^2 / 2) (1 for ReLU features; 0 past r1), and C~ = D_K [V 1] as
-// chained-order B fragments. Wave w transposes the values of its 16 tokens
-// 16 w .. 16 w + 15.
-template <typename T, int KN>
-__device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
-                                           const typename Mma<T>::frag (&sel)[2], int t0, int r1,
-                                           float s2half, float cM, int tid) {
+// Stage a prefetched tile into LDS: keys row-major, the value rows scaled by
+// this thread's row weight a (row tid / 4) as chained-order B fragments, and
+// the extra column e in place of the ones column. Wave w transposes the values
+// of its 16 tokens 16 w .. 16 w + 15.
+template <typename T>
+__device__ __forceinline__ void stage_tile_rows(KVTile<T> &tl, const TileRegs<T> &r,
+                                                const typename Mma<T>::frag (&sel)[2], float a,
+                                                float e, int tid) {
   using P = Mma<T>;
   const int w = tid >> 6;
   const int l = tid & 63;
@@ -119,6 +119,41 @@ __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
   const int c16 = l & 15;
   const int tr = tid >> 2;
   const int cq = (tid & 3) * 16;
+  store_frag<T>(&tl.Ks[tr][cq], r.k[0]);
+  store_frag<T>(&tl.Ks[tr][cq + 8], r.k[1]);
+  // weights of rows 16 w + 4 g + j, held by lanes 16 g + 4 j of this wave
+  float aj[4], ej[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    aj[j] = __shfl(a, 16 * g + 4 * j);
+    ej[j] = __shfl(e, 16 * g + 4 * j);
+  }
+  const int sidx = w >> 1;
+  const int h = w & 1;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const f32x4 c = P::mma(r.v[kh], sel[half], f32x4{0.f, 0.f, 0.f, 0.f});
+      T *p = reinterpret_cast<T *>(&tl.VtF[2 * kh + half][sidx][l]) + 4 * h;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(c[j] * aj[j]);
+    }
+  if (c16 == 0) {
+    T *p = reinterpret_cast<T *>(&tl.DF[sidx][g]) + 4 * h;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(ej[j]);
+  }
+}
+
+// Stage a prefetched tile into LDS: keys row-major, D_K(t) = sqrt(2/M)
+// exp(||s k_t||^2 / 2) (1 for ReLU features; 0 past r1), and C~ = D_K [V 1] as
+// chained-order B fragments.
+template <typename T, int KN>
+__device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
+                                           const typename Mma<T>::frag (&sel)[2], int t0, int r1,
+                                           float s2half, float cM, int tid) {
+  const int tr = tid >> 2;
   float Dt = (t0 + tr < r1) ? 1.f : 0.f;
   if constexpr (KN == kCos) {
     float nrm = 0.f;
@@ -133,28 +168,7 @@ __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
     nrm += __shfl_xor(nrm, 2);
     Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
   }
-  store_frag<T>(&tl.Ks[tr][cq], r.k[0]);
-  store_frag<T>(&tl.Ks[tr][cq + 8], r.k[1]);
-  // D of rows 16 w + 4 g + j, held by lanes 16 g + 4 j of this wave
-  float Dj[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Dt, 16 * g + 4 * j);
-  const int sidx = w >> 1;
-  const int h = w & 1;
-#pragma unroll
-  for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const f32x4 c = P::mma(r.v[kh], sel[half], f32x4{0.f, 0.f, 0.f, 0.f});
-      T *p = reinterpret_cast<T *>(&tl.VtF[2 * kh + half][sidx][l]) + 4 * h;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(c[j] * Dj[j]);
-    }
-  if (c16 == 0) {
-    T *p = reinterpret_cast<T *>(&tl.DF[sidx][g]) + 4 * h;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(Dj[j]);
-  }
+  stage_tile_rows<T>(tl, r, sel, Dt, Dt, tid);
 }
 
 // Key projection + features for one wave's MB m-blocks over token half sidx of

@@ -22,9 +22,10 @@ std::vector<Pending> g_pending;
 double g_ms[kNumKernels] = {};
 int64_t g_count[kNumKernels] = {};
 
-const char *const kNames[kNumKernels] = {"k_orf_draw", "k_feature_map", "k_kside",
-                                         "k_finalize", "k_qside",       "k_seg_scan",
-                                         "k_causal"};
+const char *const kNames[kNumKernels] = {"k_orf_draw",   "k_feature_map", "k_kside",
+                                         "k_finalize",   "k_qside",       "k_seg_scan",
+                                         "k_causal",     "k_sum_splits",  "k_bwd_dq",
+                                         "k_kside_agg",  "k_suffix_scan", "k_bwd_dkv"};
 
 hipEvent_t take_event() {
   if (!g_pool.empty()) {

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_strings(L):
-    assert L.favor_abi_version() == 2
+    assert L.favor_abi_version() == 3
     assert fv.status_string(0) == "FAVOR_OK"
     assert fv.status_string(3) == "FAVOR_ERR_WORKSPACE_TOO_SMALL"
 
@@ -88,8 +88,49 @@ def test_fp32_causal_limits_m():
     assert fv.validate_desc(g, fv.OP_CAUSAL) == 2
     assert fv.validate_desc(g, fv.OP_BOTH) == 2
     assert fv.validate_desc(g, fv.OP_BIDIR) == 0
-    assert fv.validate_desc(g, 4) == 1
+    assert fv.validate_desc(g, 6) == 1
     assert fv.validate_desc(_desc(in_dtype=fv.F32, M=128), fv.OP_CAUSAL) == 0
+
+
+def test_backward_validation():
+    for op in (fv.OP_BIDIR_BACKWARD, fv.OP_CAUSAL_BACKWARD):
+        assert fv.validate_desc(_desc(), op) == 0
+        assert fv.validate_desc(_desc(out_dtype=fv.F32), op) == 2   # out dtype = in dtype
+        assert fv.validate_desc(_desc(in_dtype=fv.F32, out_dtype=fv.F32), op) == 2   # M 256
+        assert fv.validate_desc(_desc(in_dtype=fv.F32, out_dtype=fv.F32, M=128), op) == 0
+        assert fv.validate_desc(_desc(kernel=fv.KERNEL_RELU, renormalize=False), op) == 0
+
+
+def test_backward_workspace_size():
+    g = _desc()
+    nb = fv.backward_workspace_size(g, False)
+    nc = fv.backward_workspace_size(g, True)
+    assert nb > fv.workspace_size(g, 0) and nb % 256 == 0
+    assert nc > fv.workspace_size(g, 1) and nc % 256 == 0
+    assert fv.backward_workspace_size(_desc(L=0), True) == 0
+    assert fv.backward_workspace_size(_desc(out_dtype=fv.F32), False) == 0
+
+
+def test_backward_calls_fail_before_launch(L):
+    g = _desc()
+    null = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    f9 = [fake] * 6
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f9, null, fake, fake, fake, 1 << 40, null)
+    assert st == 1 and "dQ" in fv.last_error()
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f9, fake, fake, fake, fake, 16, null)
+    assert st == 3
+    st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), null, fake, null, fake,
+                                      fake, fake, null, fake, 16, null)
+    assert st == 3
+    odd = ctypes.c_void_p((1 << 20) + 4)
+    st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), odd, fake, null, fake,
+                                      fake, fake, null, fake, 1 << 40, null)
+    assert st == 1 and "state_in" in fv.last_error()
+    bad = _desc(out_dtype=fv.F32)
+    st = L.favor_attn_bidir_backward(ctypes.byref(bad), *f9, fake, fake, fake, fake, 1 << 40,
+                                     null)
+    assert st == 2
 
 
 def test_workspace_size():

@@ -1,0 +1,170 @@
+"""GPU parity of the backward pass (favor_attn_bidir_backward,
+favor_attn_causal_backward) against the fp64 oracle's gradients on the same
+seeded inputs and random features.
+
+Gate: for each gradient tensor and each (batch, head), max |got - ref| divided
+by the head's gradient scale, the largest |ref| entry of dQ, dK and dV of that
+head; 1e-4 for fp32 inputs, 2e-2 for bf16 inputs. (A common scale, because one
+of the three can vanish exactly: with a single key the renormalised output is
+v_1 whatever Q is, so dQ = 0.)
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from helpers import TOL, to_dev, to_host
+from oracle import backward as bw
+from oracle import favor
+
+pytestmark = pytest.mark.gpu
+
+S64 = 64 ** -0.25
+RELU = favor.KERNEL_RELU
+SOFTMAX = favor.KERNEL_SOFTMAX
+
+
+def _fv():
+    import paper_2006_03555_amd as fv
+    return fv
+
+
+def _inputs(B, H, L, M, dtype, seed):
+    Q, K, V = wl.make_qkv(wl.Workload("t", "bidir", B, H, L, 64, M, dtype, seed))
+    dout = np.random.default_rng(seed + 7).standard_normal((B, H, L, 64)).astype(np.float32)
+    if dtype == "bf16":
+        import torch
+        dout = torch.from_numpy(dout).to(torch.bfloat16).float().numpy()
+    W, b = favor.orf_draw(seed + 3, H, M, 64)
+    return Q, K, V, dout, W.astype(np.float32), b.astype(np.float32)
+
+
+def _oracle_w(W, M, dtype, kernel):
+    """The random features the oracle differentiates with. ReLU features have a
+    step derivative [W'' q > 0], an integer decision: with bf16 operands the
+    kernel takes it on W'' = bf16((s / sqrt M) W) (fp32 product, round to
+    nearest even), so the oracle takes it on the same matrix, W'' / (s / sqrt M),
+    evaluated in fp64. Cos features and fp32 inputs use W itself."""
+    if kernel != RELU or dtype != "bf16":
+        return W
+    import torch
+    ws = np.float32(np.float32(S64) / np.sqrt(np.float32(M)))
+    Wpp = torch.from_numpy((W.astype(np.float32) * ws).astype(np.float32))
+    Wpp = Wpp.to(torch.bfloat16).double().numpy()
+    return Wpp / np.float64(ws)
+
+
+def _check_all(got, ref, dtype):
+    """got, ref: dicts name -> [B, H, L, d] arrays."""
+    tol = TOL[dtype]
+    scale = np.max([np.abs(np.asarray(r, dtype=np.float64)).max(axis=(-2, -1))
+                    for r in ref.values()], axis=0)
+    errs = {}
+    for name in ref:
+        g = np.asarray(got[name], dtype=np.float64)
+        assert np.all(np.isfinite(g)), name
+        err = np.abs(g - ref[name]).max(axis=(-2, -1)) / scale
+        errs[name] = float(err.max())
+    bad = {k: v for k, v in errs.items() if v > tol}
+    assert not bad, f"{bad} > {tol}"
+    return errs
+
+
+BIDIR_CASES = [
+    # B, H, L, M, dtype, kernel, renormalize, denom_eps
+    (1, 2, 300, 128, "f32", SOFTMAX, True, 0.0),
+    (2, 2, 1000, 256, "bf16", SOFTMAX, True, 0.0),
+    (1, 3, 65, 64, "bf16", SOFTMAX, True, 0.0),
+    (1, 1, 1, 128, "f32", SOFTMAX, True, 0.0),
+    (1, 2, 300, 128, "bf16", SOFTMAX, True, 0.5),
+    (1, 1, 129, 64, "f32", SOFTMAX, False, 0.0),
+    (1, 2, 500, 256, "bf16", SOFTMAX, False, 0.0),
+    (1, 2, 257, 128, "f32", RELU, True, 0.0),
+    (2, 2, 1000, 256, "bf16", RELU, True, 0.0),
+    (1, 2, 400, 128, "bf16", RELU, False, 0.0),
+]
+
+
+@pytest.mark.parametrize("B,H,L,M,dtype,kernel,renorm,eps", BIDIR_CASES)
+def test_bidir_backward_parity(B, H, L, M, dtype, kernel, renorm, eps):
+    import torch
+    fv = _fv()
+    Q, K, V, dout, W, b = _inputs(B, H, L, M, dtype, seed=61 + L + M)
+    kw = dict(kernel=kernel, renormalize=renorm)
+    dQ, dK, dV = fv.attn_bidir_backward(to_dev(Q, dtype), to_dev(K, dtype), to_dev(V, dtype),
+                                        to_dev(W), to_dev(b), S64, to_dev(dout, dtype),
+                                        denom_eps=eps, **kw)
+    torch.cuda.synchronize()
+    rQ, rK, rV = bw.attn_bidir_backward(Q, K, V, _oracle_w(W, M, dtype, kernel), b, S64, dout,
+                                        denom_eps=eps, **kw)
+    _check_all({"dQ": to_host(dQ), "dK": to_host(dK), "dV": to_host(dV)},
+               {"dQ": rQ, "dK": rK, "dV": rV}, dtype)
+
+
+CAUSAL_CASES = [
+    # B, H, L, M, dtype, kernel, renormalize, denom_eps, with states
+    (1, 2, 300, 128, "f32", SOFTMAX, True, 0.0, False),
+    (2, 2, 1000, 256, "bf16", SOFTMAX, True, 0.0, False),
+    (1, 3, 65, 64, "bf16", SOFTMAX, True, 0.0, True),
+    (1, 1, 1, 64, "f32", SOFTMAX, True, 0.0, False),
+    (1, 2, 300, 128, "bf16", SOFTMAX, True, 0.5, False),
+    (1, 1, 190, 64, "f32", SOFTMAX, False, 0.0, True),
+    (1, 2, 500, 256, "bf16", SOFTMAX, False, 0.0, False),
+    (1, 2, 257, 128, "f32", RELU, True, 0.0, True),
+    (2, 2, 777, 256, "bf16", RELU, True, 0.0, True),
+    (1, 2, 400, 128, "bf16", RELU, False, 0.0, False),
+]
+
+
+@pytest.mark.parametrize("B,H,L,M,dtype,kernel,renorm,eps,states", CAUSAL_CASES)
+def test_causal_backward_parity(B, H, L, M, dtype, kernel, renorm, eps, states):
+    import torch
+    fv = _fv()
+    Q, K, V, dout, W, b = _inputs(B, H, L, M, dtype, seed=71 + L + M)
+    kw = dict(kernel=kernel, renormalize=renorm)
+    S0 = dS = None
+    if states:
+        # a carried state from 200 earlier tokens, and a gradient reaching state_out
+        Qe, Ke, Ve, _, _, _ = _inputs(B, H, 200, M, dtype, seed=5)
+        _, S0 = favor.attn_causal(Qe, Ke, Ve, W, b, S64, **kw, kernel_eps=1e-3)
+        S0 = S0.astype(np.float32)
+        dS = np.random.default_rng(9).standard_normal(S0.shape).astype(np.float32) * 0.01
+    dev = lambda x: None if x is None else to_dev(x)
+    dQ, dK, dV, dS0 = fv.attn_causal_backward(
+        to_dev(Q, dtype), to_dev(K, dtype), to_dev(V, dtype), to_dev(W), to_dev(b), S64,
+        to_dev(dout, dtype), denom_eps=eps, state_in=dev(S0), dstate_out=dev(dS),
+        return_state_grad=True, **kw)
+    torch.cuda.synchronize()
+    rQ, rK, rV, rS = bw.attn_causal_backward(Q, K, V, _oracle_w(W, M, dtype, kernel), b, S64,
+                                             dout, denom_eps=eps, state_in=S0, dstate_out=dS,
+                                             **kw)
+    _check_all({"dQ": to_host(dQ), "dK": to_host(dK), "dV": to_host(dV)},
+               {"dQ": rQ, "dK": rK, "dV": rV}, dtype)
+    got = to_host(dS0)
+    assert np.max(np.abs(got - rS)) <= TOL[dtype] * np.max(np.abs(rS))
+
+
+def test_causal_backward_empty_sequence_passes_state_gradient():
+    import torch
+    fv = _fv()
+    Q = torch.zeros((1, 2, 0, 64), dtype=torch.bfloat16, device="cuda")
+    W, b = _inputs(1, 2, 1, 128, "bf16", 3)[4:]
+    dS = torch.randn((1, 2, 128, 65), device="cuda")
+    _, _, _, dS0 = fv.attn_causal_backward(Q, Q, Q, to_dev(W), to_dev(b), S64, Q,
+                                           dstate_out=dS, return_state_grad=True)
+    torch.cuda.synchronize()
+    assert torch.equal(dS0, dS)
+
+
+def test_backward_is_deterministic():
+    import torch
+    fv = _fv()
+    Q, K, V, dout, W, b = _inputs(1, 2, 700, 256, "bf16", 13)
+    args = [to_dev(x, "bf16") for x in (Q, K, V)] + [to_dev(W), to_dev(b), S64,
+                                                      to_dev(dout, "bf16")]
+    a = fv.attn_bidir_backward(*args)
+    c = fv.attn_causal_backward(*args)
+    a2 = fv.attn_bidir_backward(*args)
+    c2 = fv.attn_causal_backward(*args)
+    torch.cuda.synchronize()
+    for x, y in zip(a + c, a2 + c2):
+        assert torch.equal(x, y)
