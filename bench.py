@@ -22,7 +22,8 @@ serial, with every launch bracketed by HIP events on its stream, gives the
 per-kernel durations and the roofline entry for the dominant
 kernel. The line also carries the fp64 CPU oracle timed on this host
 (cpu_baseline), and under "variants" the same step with generalized attention
-(ReLU features) and with the renormalisation off, timed the same way.
+(ReLU features) and with the renormalisation off, and the backward pass of the
+step's attention, timed the same way.
 """
 import argparse
 import json
@@ -304,6 +305,45 @@ def main():
             "ms_per_step": ms_v, "value": w.B * w.H * w.L / (ms_v / 1e3),
             "ms_per_step_instrumented": ms_vi,
             "kernels": {k: {"ms_per_launch": v[0] / v[1]} for k, v in kv.items() if v[1] > 0}}
+
+    # the backward pass of the step's attention: gradients with respect to Q, K, V of
+    # each direction the step computes, for a fixed synthetic upstream gradient (each
+    # call recomputes its forward quantities); the draw stays in the step
+    if not args.no_variants:
+        rng = np.random.default_rng(7)
+        dO = torch.from_numpy(rng.standard_normal(Q.shape, dtype=np.float32)).to(
+            device=dev, dtype=tdt).contiguous()
+        grads = [torch.empty_like(Qd) for _ in range(3)]
+        nbw = max(fv.backward_workspace_size(g, False) if op != 1 else 0,
+                  fv.backward_workspace_size(g, True) if op != 0 else 0)
+        wsb = torch.empty(nbw, dtype=torch.uint8, device=dev)
+
+        def step_bwd(i):
+            fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
+            gq, gk, gv = grads
+            if op != 1:
+                fv.attn_bidir_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dQ=gq, dK=gk, dV=gv,
+                                       workspace=wsb, stream=s_main)
+            if op != 0:
+                fv.attn_causal_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dQ=gq, dK=gk, dV=gv,
+                                        workspace=wsb, stream=s_main)
+
+        for i in range(args.warmup):
+            step_bwd(first + i)
+        first += args.warmup
+        ms_b = timed_region(step_bwd, first)
+        first += args.steps
+        ms_bi = timed_region(step_bwd, first, instrumented=True)
+        first += args.steps
+        kb = fv.timing_read()
+        variants["backward"] = {
+            "ms_per_step": ms_b, "value": w.B * w.H * w.L / (ms_b / 1e3),
+            "ms_per_step_instrumented": ms_bi,
+            "what": "ORF draw + gradients of " + {0: "bidirectional", 1: "causal",
+                                                   2: "bidirectional and causal"}[op]
+                    + " attention with respect to Q, K, V (forward recomputed inside)",
+            "kernels": {k: {"ms_per_launch": v[0] / v[1], "launches_per_step": v[1] / args.steps}
+                        for k, v in kb.items() if v[1] > 0}}
 
     token_heads = w.B * w.H * w.L
     value = token_heads / (ms_step / 1e3)

@@ -82,3 +82,40 @@ def test_protein_b4h8_full_both_directions():
 def test_causal_long_full_with_gpu_draw():
     w = wl.WORKLOADS["causal_long"]
     _run(w, 5, heads=[(0, 11)], gpu_draw=True)
+
+
+def test_protein_b4h8_full_backward():
+    """Both backward passes at the protein workload's full size (B4 H8 L8192 M256
+    bf16), sampled heads against the oracle's gradients; the gate of
+    test_gpu_backward (errors relative to the head's largest gradient entry)."""
+    import torch
+    fv = _fv()
+    from oracle import backward as bw
+    w = wl.WORKLOADS["protein_b4h8"]
+    Q, K, V = wl.make_qkv(w)
+    dout = np.random.default_rng(123).standard_normal(Q.shape).astype(np.float32)
+    dout = torch.from_numpy(dout).to(torch.bfloat16).float().numpy()
+    Wr, br = favor.orf_draw(8, w.H, w.M, w.d)
+    Wr, br = Wr.astype(np.float32), br.astype(np.float32)
+    args = [to_dev(x, "bf16") for x in (Q, K, V)] + [to_dev(Wr), to_dev(br), w.input_scale,
+                                                      to_dev(dout, "bf16")]
+    gb = fv.attn_bidir_backward(*args)
+    gc = fv.attn_causal_backward(*args)
+    torch.cuda.synchronize()
+    gb = [to_host(t) for t in gb]
+    gc = [to_host(t) for t in gc]
+    for t in gb + gc:
+        assert np.all(np.isfinite(t))
+    for (bi, hi) in [(0, 0), (3, 6)]:
+        sl = lambda a: a[bi:bi + 1, hi:hi + 1]
+        Wh, bh = Wr[hi:hi + 1], br[hi:hi + 1]
+        refs = {"bidir": bw.attn_bidir_backward(sl(Q), sl(K), sl(V), Wh, bh, w.input_scale,
+                                                sl(dout)),
+                "causal": bw.attn_causal_backward(sl(Q), sl(K), sl(V), Wh, bh, w.input_scale,
+                                                  sl(dout))[:3]}
+        for kind, got in (("bidir", gb), ("causal", gc)):
+            ref = refs[kind]
+            scale = max(np.max(np.abs(r)) for r in ref)
+            for name, g, r in zip(("dQ", "dK", "dV"), got, ref):
+                err = np.max(np.abs(sl(g) - r)) / scale
+                assert err <= 2e-2, (kind, name, bi, hi, err)
