@@ -220,246 +220,209 @@ __device__ __forceinline__ void chunk_features_t(typename Mma<T>::frag (*dst)[2]
   }
 }
 
-// ------------------------------------------------------------ dQ
-template <typename T, int M, bool CAUSAL>
+// ------------------------------------------------------------ shared row work
+// Gradient of one 16-row block of queries (lane column = query i = row0 + lane % 16;
+// qf, df the query and dout fragments, alpha and u_d of the row), with the
+// aggregate S in LDS (SA rows over value columns, sz its column d), W'' (WA, bq)
+// and the input-gradient matrix WT. INTRA adds g~ += K-hat^T P2 with the chunk's
+// key features KT (row m, k = keys) and P2 packed as B operand (k = keys).
+template <typename T, int M, int KN, bool INTRA>
+__device__ __forceinline__ void query_grad(
+    const typename Mma<T>::frag (*WA)[2][64], const float *bq,
+    const typename Mma<T>::frag (*WT)[M / 32][64], const typename Mma<T>::frag (*SA)[2][64],
+    const float *sz, const typename Mma<T>::frag (*KT)[2][64],
+    const typename Mma<T>::frag (&pb2)[2], const typename Mma<T>::frag (&qf)[2],
+    const typename Mma<T>::frag (&df)[2], float alpha, float ud, float s, float keps,
+    f32x4 (&dacc)[4], float &dot2) {
+  using P = Mma<T>;
+  using frag = typename P::frag;
+  constexpr int NS = M / 32;
+  constexpr float sgn = KN == kCos ? -1.f : 1.f;
+  const int l = lane_id();
+  const int g = l >> 4;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) dacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  dot2 = 0.f;
+#pragma unroll 2
+  for (int sidx = 0; sidx < NS; ++sidx) {
+    f32x4 G[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int mb = 2 * sidx + hh;
+      const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&bq[16 * mb + 4 * g]);
+      const f32x4 szv = *reinterpret_cast<const f32x4 *>(&sz[16 * mb + 4 * g]);
+      f32x4 p = P::mma(WA[mb][0][l], qf[0], bcv);
+      p = P::mma(WA[mb][1][l], qf[1], p);
+      f32x4 gt = P::mma(SA[mb][0][l], df[0], f32x4{0.f, 0.f, 0.f, 0.f});
+      gt = P::mma(SA[mb][1][l], df[1], gt);
+      if constexpr (INTRA) {
+        gt = P::mma(KT[mb][0][l], pb2[0], gt);
+        gt = P::mma(KT[mb][1][l], pb2[1], gt);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float gj = fmaf(szv[j], ud, gt[j]);
+        dot2 = fmaf(gj, feature<KN, P>(p[j], keps), dot2);
+        G[hh][j] = sgn * alpha * gj * feature_slope<KN, P>(p[j]);
+      }
+    }
+    const frag gb = P::pack(G[0], G[1]);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) dacc[kb] = P::mma(WT[kb][sidx][l], gb, dacc[kb]);
+  }
+  dot2 += __shfl_xor(dot2, 16);
+  dot2 += __shfl_xor(dot2, 32);
+}
+
+// dQ row store: dQ = WT G + alpha s^2 (g~ . q-hat) q (cos features).
+template <typename T, int KN>
+__device__ __forceinline__ void store_qgrad(T *dst, const f32x4 (&dacc)[4],
+                                            const typename Mma<T>::frag (&qf)[2], float alpha,
+                                            float dot2, float s) {
+  const int g = lane_id() >> 4;
+  const float cx = KN == kCos ? alpha * s * s * dot2 : 0.f;
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    f32x4 lo, hi;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo[e] = fmaf(cx, to_f32(qf[pp][e]), dacc[2 * pp][e]);
+      hi[e] = fmaf(cx, to_f32(qf[pp][4 + e]), dacc[2 * pp + 1][e]);
+    }
+    store8(dst + 32 * pp + 8 * g, lo, hi);
+  }
+}
+
+// alpha and u_d of query row i (lane column) from its dout and output fragments.
+template <typename T, int KN, bool RN>
+__device__ __forceinline__ void row_weights(const typename Mma<T>::frag (&qf)[2],
+                                            const typename Mma<T>::frag (&df)[2],
+                                            const T *__restrict__ Oh,
+                                            const float *__restrict__ rsave_h, int i, int L,
+                                            float cM, float s2half, float &alpha, float &ud) {
+  if constexpr (RN) {
+    typename Mma<T>::frag of[2];
+    load_rows64<T>(of, Oh, i, L);
+    float dot = 0.f;
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dot = fmaf(to_f32(df[k][e]), to_f32(of[k][e]), dot);
+    dot += __shfl_xor(dot, 16);
+    dot += __shfl_xor(dot, 32);
+    alpha = i < L ? rsave_h[i] : 0.f;
+    ud = -dot;
+  } else {
+    float a = 1.f;
+    if constexpr (KN == kCos) a = cM * expf(s2half * sq_norm16<T>(qf));
+    alpha = i < L ? a : 0.f;
+    ud = 0.f;
+  }
+}
+
+// ------------------------------------------------------------ bidirectional dQ
+template <typename T, int M>
 struct DqSmem {
   using frag = typename Mma<T>::frag;
   frag WA[M / 16][2][64];    // W'' (projection, lane row m)
   frag WT[4][M / 32][64];    // the input-gradient matrix (see build_wt)
-  frag SA[M / 16][2][64];    // S rows over value columns
-  float sz[M];               // S column d
+  frag SA[M / 16][2][64];    // Buf1 rows over value columns
+  float sz[M];               // Buf1 column d
   float bq[M];               // b''
-  frag KT[CAUSAL ? M / 16 : 1][2][64];   // the chunk's key features (row m, k = keys)
-  frag VA[CAUSAL ? 4 : 1][2][64];        // the chunk's value rows (lane row = key)
-  float dk[CAUSAL ? 64 : 1];             // D~ of the chunk's keys (0 past L)
 };
 
-// Bidirectional: items are (head, tile of 64 TBW rows), walked persistently over
-// XCD-local ranges; the state is Buf1 [BH][M][65]. Causal: one item per
-// workgroup, a 64-token chunk (TBW = 1) with its prefix state [BH][nch][M][65].
-template <typename T, int M, int KN, bool RN, bool CAUSAL, int TBW>
+// Items are (head, tile of 64 TBW rows), walked persistently over XCD-local
+// ranges; Buf1 [BH][M][65] fp32.
+template <typename T, int M, int KN, bool RN, int TBW>
 __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq(
-    const T *__restrict__ Q, const T *__restrict__ K, const T *__restrict__ V,
-    const T *__restrict__ dout, const T *__restrict__ out, const float *__restrict__ rsave,
-    const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
-    const float *__restrict__ W, const float *__restrict__ state, T *__restrict__ dQ,
-    float2 *__restrict__ aux, int H, int L, float s, float keps, float wts, int ntiles,
-    int nitems) {
-  static_assert(!CAUSAL || TBW == 1, "a causal chunk is one 16-row block per wave");
-  constexpr int NS = M / 32;
-  constexpr int MB = M / 64;   // feature blocks per wave for the chunk's keys
-  using P = Mma<T>;
-  using frag = typename P::frag;
-  __shared__ DqSmem<T, M, CAUSAL> sm;
+    const T *__restrict__ Q, const T *__restrict__ dout, const T *__restrict__ out,
+    const float *__restrict__ rsave, const typename Mma<T>::frag *__restrict__ wfr,
+    const float *__restrict__ bqg, const float *__restrict__ W, const float *__restrict__ buf1,
+    T *__restrict__ dQ, float2 *__restrict__ aux, int H, int L, float s, float keps, float wts,
+    int ntiles, int nitems) {
+  using frag = typename Mma<T>::frag;
+  __shared__ DqSmem<T, M> sm;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
-  const int l = tid & 63;
-  const int g = l >> 4;
-  const int c16 = l & 15;
+  const int g = (tid & 63) >> 4;
+  const int c16 = tid & 15;
   const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
-  constexpr float sgn = KN == kCos ? -1.f : 1.f;
-
   int begin, end;
-  if constexpr (CAUSAL) {
-    begin = xcd_item(blockIdx.x, gridDim.x);
-    end = begin + 1;
-  } else {
-    xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
-  }
+  xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
   int cur = -1;
   for (int item = begin; item < end; ++item) {
     const int bh = item / ntiles;
     const int tile = item - bh * ntiles;
     const int h = bh % H;
-    const int t0 = tile * 64 * TBW;
     if (bh != cur) {
       __syncthreads();
       copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
       if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
       build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
-      if constexpr (!CAUSAL) build_state_rows<T, M>(sm.SA, sm.sz, state + (size_t)bh * M * 65);
+      build_state_rows<T, M>(sm.SA, sm.sz, buf1 + (size_t)bh * M * 65);
       cur = bh;
       __syncthreads();
     }
-    if constexpr (CAUSAL) {
-      build_state_rows<T, M>(sm.SA, sm.sz, state + ((size_t)bh * ntiles + tile) * M * 65);
-      const T *Kh = K + (size_t)bh * L * kD;
-      frag ka[4][2];
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb) load_rows64<T>(ka[tb], Kh, t0 + 16 * tb + c16, L);
-      chunk_features_t<T, MB, KN>(sm.KT, sm.WA, sm.bq, ka, w * MB, keps);
-      frag va[2];
-      load_rows64<T>(va, V + (size_t)bh * L * kD, t0 + 16 * w + c16, L);
-      sm.VA[w][0][l] = va[0];
-      sm.VA[w][1][l] = va[1];
-      const float nrm = sq_norm16<T>(ka[w]);
-      const bool in = t0 + 16 * w + c16 < L;
-      const float D = !in ? 0.f : (KN == kCos ? cM * expf(s2half * nrm) : 1.f);
-      if (g == 0) sm.dk[16 * w + c16] = D;
-      __syncthreads();
-    }
-
     const T *Qh = Q + (size_t)bh * L * kD;
     const T *dOh = dout + (size_t)bh * L * kD;
     const T *Oh = out + (size_t)bh * L * kD;
-    frag qf[TBW][2], df[TBW][2];
-    float alpha[TBW], ud[TBW];
+    const frag none[2] = {};
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
-      const int i = t0 + 16 * (w * TBW + tb) + c16;
-      load_rows64<T>(qf[tb], Qh, i, L);
-      load_rows64<T>(df[tb], dOh, i, L);
-      if constexpr (RN) {
-        frag of[2];
-        load_rows64<T>(of, Oh, i, L);
-        float dot = 0.f;
-#pragma unroll
-        for (int k = 0; k < 2; ++k)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) dot = fmaf(to_f32(df[tb][k][e]), to_f32(of[k][e]), dot);
-        dot += __shfl_xor(dot, 16);
-        dot += __shfl_xor(dot, 32);
-        alpha[tb] = i < L ? rsave[(size_t)bh * L + i] : 0.f;
-        ud[tb] = -dot;
-      } else {
-        float a = 1.f;
-        if constexpr (KN == kCos) a = cM * expf(s2half * sq_norm16<T>(qf[tb]));
-        alpha[tb] = i < L ? a : 0.f;
-        ud[tb] = 0.f;
-      }
-    }
-
-    // causal: P2[j][i] = D~_j (v_j . dout_i + u_d,i) for keys j <= i of the chunk,
-    // packed as B operand (k = keys in chained order, column = query)
-    frag pb2[2];
-    if constexpr (CAUSAL) {
-      f32x4 pt[4];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        f32x4 c = P::mma(sm.VA[kb][0][l], df[0][0], f32x4{0.f, 0.f, 0.f, 0.f});
-        c = P::mma(sm.VA[kb][1][l], df[0][1], c);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int jp = 16 * kb + 4 * g + j;
-          pt[kb][j] = jp <= 16 * w + c16 ? sm.dk[jp] * (c[j] + ud[0]) : 0.f;
-        }
-      }
-      pb2[0] = P::pack(pt[0], pt[1]);
-      pb2[1] = P::pack(pt[2], pt[3]);
-    }
-
-    f32x4 dacc[TBW][4];
-    float dot2[TBW];
-#pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-      dot2[tb] = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) dacc[tb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-#pragma unroll 2
-    for (int sidx = 0; sidx < NS; ++sidx) {
-      f32x4 G[TBW][2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int mb = 2 * sidx + hh;
-        const frag a0 = sm.WA[mb][0][l];
-        const frag a1 = sm.WA[mb][1][l];
-        const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&sm.bq[16 * mb + 4 * g]);
-        const frag s0 = sm.SA[mb][0][l];
-        const frag s1 = sm.SA[mb][1][l];
-        const f32x4 szv = *reinterpret_cast<const f32x4 *>(&sm.sz[16 * mb + 4 * g]);
-#pragma unroll
-        for (int tb = 0; tb < TBW; ++tb) {
-          f32x4 p = P::mma(a0, qf[tb][0], bcv);
-          p = P::mma(a1, qf[tb][1], p);
-          f32x4 gt = P::mma(s0, df[tb][0], f32x4{0.f, 0.f, 0.f, 0.f});
-          gt = P::mma(s1, df[tb][1], gt);
-          if constexpr (CAUSAL) {
-            gt = P::mma(sm.KT[mb][0][l], pb2[0], gt);
-            gt = P::mma(sm.KT[mb][1][l], pb2[1], gt);
-          }
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float gj = fmaf(szv[j], ud[tb], gt[j]);
-            dot2[tb] = fmaf(gj, feature<KN, P>(p[j], keps), dot2[tb]);
-            G[tb][hh][j] = sgn * alpha[tb] * gj * feature_slope<KN, P>(p[j]);
-          }
-        }
-      }
-#pragma unroll
-      for (int tb = 0; tb < TBW; ++tb) {
-        const frag gb = P::pack(G[tb][0], G[tb][1]);
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) dacc[tb][kb] = P::mma(sm.WT[kb][sidx][l], gb, dacc[tb][kb]);
-      }
-    }
-
-#pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-      const int i = t0 + 16 * (w * TBW + tb) + c16;
-      float d2 = dot2[tb];
-      d2 += __shfl_xor(d2, 16);
-      d2 += __shfl_xor(d2, 32);
-      const float cx = KN == kCos ? alpha[tb] * s * s * d2 : 0.f;
+      const int i = tile * 64 * TBW + 16 * (w * TBW + tb) + c16;
+      frag qf[2], df[2];
+      load_rows64<T>(qf, Qh, i, L);
+      load_rows64<T>(df, dOh, i, L);
+      float alpha, ud;
+      row_weights<T, KN, RN>(qf, df, Oh, rsave + (size_t)bh * L, i, L, cM, s2half, alpha, ud);
+      f32x4 dacc[4];
+      float dot2;
+      query_grad<T, M, KN, false>(sm.WA, sm.bq, sm.WT, sm.SA, sm.sz, nullptr, none, qf, df, alpha,
+                                  ud, s, keps, dacc, dot2);
       if (i < L) {
-        T *dst = dQ + ((size_t)bh * L + i) * kD;
-#pragma unroll
-        for (int pp = 0; pp < 2; ++pp) {
-          f32x4 lo, hi;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            lo[e] = fmaf(cx, to_f32(qf[tb][pp][e]), dacc[tb][2 * pp][e]);
-            hi[e] = fmaf(cx, to_f32(qf[tb][pp][4 + e]), dacc[tb][2 * pp + 1][e]);
-          }
-          store8(dst + 32 * pp + 8 * g, lo, hi);
-        }
-        if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha[tb], alpha[tb] * ud[tb]);
+        store_qgrad<T, KN>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
+        if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
       }
     }
   }
 }
 
-// ------------------------------------------------------------ dK, dV
-constexpr int kPartBoth = 0;   // dK and dV (bidirectional)
-constexpr int kPartDv = 1;     // dV only (causal)
-constexpr int kPartDk = 2;     // dK only (causal)
-
-template <typename T, int M, bool CAUSAL, int PART>
-struct DkvSmem {
+// ------------------------------------------------------------ causal dQ
+template <typename T, int M>
+struct DqScanSmem {
   using frag = typename Mma<T>::frag;
-  static constexpr bool kK = PART != kPartDv;
-  static constexpr bool kV = PART != kPartDk;
   frag WA[M / 16][2][64];
+  frag WT[4][M / 32][64];
+  frag SA[M / 16][2][64];    // S before the chunk, rows over value columns
+  float sz[M];
   float bq[M];
-  frag WT[kK ? 4 : 1][kK ? M / 32 : 1][64];
-  frag RA[kK ? M / 16 : 1][2][64];        // R rows over value columns
-  float rz[kK ? M : 1];                   // R column d
-  frag RB[kV ? 4 : 1][kV ? M / 32 : 1][64];   // R value columns over features
-  // causal dV: the chunk's query features (lane row = query, k = m) and u~^T
-  frag QA[CAUSAL && kV ? 4 : 1][CAUSAL && kV ? M / 32 : 1][64];
-  frag UF[CAUSAL && kV ? 4 : 1][2][64];
-  // causal dK: the chunk's query features (row m, k = queries), dout rows, weights
-  frag QT[CAUSAL && kK ? M / 16 : 1][2][64];
-  frag DA[CAUSAL && kK ? 4 : 1][2][64];
-  float2 au[CAUSAL && kK ? 64 : 1];
+  frag KT[M / 16][2][64];    // the chunk's key features (row m, k = keys)
+  frag VtF[4][2][64];        // C~ of the chunk: row = value column (permuted), k = keys
+  frag DF[2][4];             // its column d (D~ per key), one fragment per lane group
 };
 
-template <typename T, int M, int KN, bool CAUSAL, int PART, int TBW>
-__global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv(
+// One workgroup per (head, segment of the forward plan). Wave w keeps rows
+// [w M/4, (w+1) M/4) of S^T (value columns in permuted order, fp32) in
+// registers, publishes S before each 64-token chunk, and folds the chunk's
+// C~^T K-hat in after; the chunk's queries then take S u plus the masked
+// intra-chunk terms.
+template <typename T, int M, int KN, bool RN>
+__global__ __launch_bounds__(kBwdThreads) void k_bwd_dq_scan(
     const T *__restrict__ Q, const T *__restrict__ K, const T *__restrict__ V,
-    const T *__restrict__ dout, const float2 *__restrict__ aux,
+    const T *__restrict__ dout, const T *__restrict__ out, const float *__restrict__ rsave,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
-    const float *__restrict__ W, const float *__restrict__ rstate, T *__restrict__ dK,
-    T *__restrict__ dV, int H, int L, float s, float keps, float wts, int ntiles, int nitems) {
-  static_assert(!CAUSAL || TBW == 1, "a causal chunk is one 16-row block per wave");
-  constexpr bool kK = PART != kPartDv;
-  constexpr bool kV = PART != kPartDk;
-  constexpr int NS = M / 32;
+    const float *__restrict__ W, const float *__restrict__ prefix, T *__restrict__ dQ,
+    float2 *__restrict__ aux, int H, int L, int seg_len, int nseg, float s, float keps,
+    float wts) {
   constexpr int MB = M / 64;
   using P = Mma<T>;
   using frag = typename P::frag;
-  __shared__ DkvSmem<T, M, CAUSAL, PART> sm;
+  __shared__ DqScanSmem<T, M> sm;
+  const int item = xcd_item(blockIdx.x, gridDim.x);
+  const int bh = item / nseg;
+  const int seg = item - bh * nseg;
+  const int h = bh % H;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
   const int l = tid & 63;
@@ -467,236 +430,530 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv(
   const int c16 = l & 15;
   const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
-  constexpr float sgn = KN == kCos ? -1.f : 1.f;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  const int r0 = seg * seg_len;
+  const int r1 = min(L, r0 + seg_len);
 
-  int begin, end;
-  if constexpr (CAUSAL) {
-    begin = xcd_item(blockIdx.x, gridDim.x);
-    end = begin + 1;
-  } else {
-    xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
+  copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
+  if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
+  build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
+  // S^T slice: acc[nb][mb] rows = value column perm_col(nb, 4 g + j) (block 4: column
+  // d replicated), lane = feature m = 16 (w MB + mb) + lane % 16
+  f32x4 acc[5][MB];
+  {
+    const float *S = prefix + ((size_t)bh * nseg + seg) * M * 65;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const float *row = S + (size_t)(16 * (w * MB + mb) + c16) * 65;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) acc[nb][mb][j] = row[perm_col(nb, 4 * g + j)];
+        acc[4][mb][j] = row[64];
+      }
+    }
   }
+  const frag sel[2] = {select_perm<T>(0), select_perm<T>(1)};
+  const T *Qh = Q + (size_t)bh * L * kD;
+  const T *Kh = K + (size_t)bh * L * kD;
+  const T *Vh = V + (size_t)bh * L * kD;
+  const T *dOh = dout + (size_t)bh * L * kD;
+  const T *Oh = out + (size_t)bh * L * kD;
+  __syncthreads();
+
+  for (int t0 = r0; t0 < r1; t0 += 64) {
+    // the chunk's keys and values (all four blocks in every wave), D~ per key
+    frag ka[4][2], va[4][2];
+    float Dk[4];
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      const int t = t0 + 16 * tb + c16;
+      load_rows64<T>(ka[tb], Kh, t, r1);
+      load_rows64<T>(va[tb], Vh, t, r1);
+      float D = 1.f;
+      if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(ka[tb]));
+      Dk[tb] = t < r1 ? D : 0.f;
+    }
+    chunk_features_t<T, MB, KN>(sm.KT, sm.WA, sm.bq, ka, w * MB, keps);
+    {
+      float Dj[4];   // D~ of keys 16 w + 4 g + j
+#pragma unroll
+      for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Dk[w], 4 * g + j);
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const f32x4 c = P::mma(va[w][kh], sel[half], zero4);
+          T *p = reinterpret_cast<T *>(&sm.VtF[2 * kh + half][w >> 1][l]) + 4 * (w & 1);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(c[j] * Dj[j]);
+        }
+      if (c16 == 0) {
+        T *p = reinterpret_cast<T *>(&sm.DF[w >> 1][g]) + 4 * (w & 1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(Dj[j]);
+      }
+    }
+    // publish S (before the chunk)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int mbg = w * MB + mb;
+      sm.SA[mbg][0][l] = P::pack(acc[0][mb], acc[1][mb]);
+      sm.SA[mbg][1][l] = P::pack(acc[2][mb], acc[3][mb]);
+      if (g == 0) sm.sz[16 * mbg + c16] = acc[4][mb][0];
+    }
+    __syncthreads();
+
+    // fold the chunk into S^T: rows value columns, k = keys, columns m
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        const frag kb = sm.KT[w * MB + mb][sidx][l];
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) acc[nb][mb] = P::mma(sm.VtF[nb][sidx][l], kb, acc[nb][mb]);
+        acc[4][mb] = P::mma(sm.DF[sidx][g], kb, acc[4][mb]);
+      }
+
+    // queries 16 w .. 16 w + 15 of the chunk
+    const int i = t0 + 16 * w + c16;
+    frag qf[2], df[2];
+    load_rows64<T>(qf, Qh, i, r1);
+    load_rows64<T>(df, dOh, i, r1);
+    float alpha, ud;
+    row_weights<T, KN, RN>(qf, df, Oh, rsave + (size_t)bh * L, i, r1, cM, s2half, alpha, ud);
+    // P2[j][i] = D~_j (v_j . dout_i + u_d,i) for keys j <= i (B operand, k = keys)
+    frag pb2[2];
+    {
+      f32x4 pt[4];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        f32x4 c = P::mma(va[kb][0], df[0], zero4);
+        c = P::mma(va[kb][1], df[1], c);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float D = __shfl(Dk[kb], 4 * g + j);
+          pt[kb][j] = 16 * kb + 4 * g + j <= 16 * w + c16 ? D * (c[j] + ud) : 0.f;
+        }
+      }
+      pb2[0] = P::pack(pt[0], pt[1]);
+      pb2[1] = P::pack(pt[2], pt[3]);
+    }
+    f32x4 dacc[4];
+    float dot2;
+    query_grad<T, M, KN, true>(sm.WA, sm.bq, sm.WT, sm.SA, sm.sz, sm.KT, pb2, qf, df, alpha, ud,
+                               s, keps, dacc, dot2);
+    if (i < r1) {
+      store_qgrad<T, KN>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
+      if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------ key-side rows
+// Gradient of one 16-row block of keys (lane column = key j): h = R C_j (+ INTRA_K:
+// Q-hat^T P3 with the chunk's query features QT and P3 packed, k = queries), dK
+// from h; dV = R^T k-hat (+ INTRA_V: u~^T (P4 masked) with the chunk's query
+// features QA and u~^T in UF). KPART / VPART select what is computed.
+template <typename T, int M, int KN, bool KPART, bool VPART, bool INTRA>
+__device__ __forceinline__ void key_grad(
+    const typename Mma<T>::frag (*WA)[2][64], const float *bq,
+    const typename Mma<T>::frag (*WT)[M / 32][64], const typename Mma<T>::frag (*RA)[2][64],
+    const float *rz, const typename Mma<T>::frag (*RB)[M / 32][64],
+    const typename Mma<T>::frag (*QT)[2][64], const typename Mma<T>::frag (&pb3)[2],
+    const typename Mma<T>::frag (*QA)[M / 32][64], const typename Mma<T>::frag (*UF)[2][64],
+    const typename Mma<T>::frag (&kf)[2], const typename Mma<T>::frag (&vf)[2], int jpos,
+    float keps, f32x4 (&kacc)[4], float &doth, f32x4 (&vacc)[4]) {
+  using P = Mma<T>;
+  using frag = typename P::frag;
+  constexpr int NS = M / 32;
+  constexpr float sgn = KN == kCos ? -1.f : 1.f;
+  const int l = lane_id();
+  const int g = l >> 4;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  f32x4 p4[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    kacc[k] = zero4;
+    vacc[k] = zero4;
+    p4[k] = zero4;
+  }
+  doth = 0.f;
+#pragma unroll 2
+  for (int sidx = 0; sidx < NS; ++sidx) {
+    f32x4 kh[2], G[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int mb = 2 * sidx + hh;
+      const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&bq[16 * mb + 4 * g]);
+      f32x4 p = P::mma(WA[mb][0][l], kf[0], bcv);
+      p = P::mma(WA[mb][1][l], kf[1], p);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kh[hh][j] = feature<KN, P>(p[j], keps);
+      if constexpr (KPART) {
+        f32x4 hv = P::mma(RA[mb][0][l], vf[0], zero4);
+        hv = P::mma(RA[mb][1][l], vf[1], hv);
+        if constexpr (INTRA) {
+          hv = P::mma(QT[mb][0][l], pb3[0], hv);
+          hv = P::mma(QT[mb][1][l], pb3[1], hv);
+        }
+        const f32x4 rzv = *reinterpret_cast<const f32x4 *>(&rz[16 * mb + 4 * g]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float hj = hv[j] + rzv[j];
+          doth = fmaf(hj, kh[hh][j], doth);
+          G[hh][j] = sgn * hj * feature_slope<KN, P>(p[j]);
+        }
+      }
+    }
+    if constexpr (KPART) {
+      const frag gb = P::pack(G[0], G[1]);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) kacc[kb] = P::mma(WT[kb][sidx][l], gb, kacc[kb]);
+    }
+    if constexpr (VPART) {
+      const frag kb_ = P::pack(kh[0], kh[1]);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) vacc[nb] = P::mma(RB[nb][sidx][l], kb_, vacc[nb]);
+      if constexpr (INTRA) {
+#pragma unroll
+        for (int qb = 0; qb < 4; ++qb) p4[qb] = P::mma(QA[qb][sidx][l], kb_, p4[qb]);
+      }
+    }
+  }
+  if constexpr (KPART) {
+    doth += __shfl_xor(doth, 16);
+    doth += __shfl_xor(doth, 32);
+  }
+  if constexpr (VPART && INTRA) {
+    // keep queries i >= j, then u~^T (q-hat . k-hat)
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) p4[qb][j] = 16 * qb + 4 * g + j >= jpos ? p4[qb][j] : 0.f;
+#pragma unroll
+    for (int sidx = 0; sidx < 2; ++sidx) {
+      const frag pb = P::pack(p4[2 * sidx], p4[2 * sidx + 1]);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) vacc[nb] = P::mma(UF[nb][sidx][l], pb, vacc[nb]);
+    }
+  }
+}
+
+// dK = D~ (WT G + s^2 (h . k-hat) k) (cos features), D~ (WT G) (ReLU); dV = D~ vacc.
+template <typename T, int KN>
+__device__ __forceinline__ void store_kgrad(T *dst, const f32x4 (&kacc)[4],
+                                            const typename Mma<T>::frag (&kf)[2], float D,
+                                            float doth, float s) {
+  const int g = lane_id() >> 4;
+  const float cx = KN == kCos ? s * s * doth : 0.f;
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    f32x4 lo, hi;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo[e] = D * fmaf(cx, to_f32(kf[pp][e]), kacc[2 * pp][e]);
+      hi[e] = D * fmaf(cx, to_f32(kf[pp][4 + e]), kacc[2 * pp + 1][e]);
+    }
+    store8(dst + 32 * pp + 8 * g, lo, hi);
+  }
+}
+template <typename T>
+__device__ __forceinline__ void store_vgrad(T *dst, const f32x4 (&vacc)[4], float D) {
+  const int g = lane_id() >> 4;
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp)
+    store8(dst + 32 * pp + 8 * g, vacc[2 * pp] * D, vacc[2 * pp + 1] * D);
+}
+
+// ------------------------------------------------------------ bidirectional dK, dV
+template <typename T, int M>
+struct DkvSmem {
+  using frag = typename Mma<T>::frag;
+  frag WA[M / 16][2][64];
+  float bq[M];
+  frag WT[4][M / 32][64];
+  frag RA[M / 16][2][64];   // dBuf1 rows over value columns
+  float rz[M];              // dBuf1 column d
+  frag RB[4][M / 32][64];   // dBuf1 value columns over features
+};
+
+template <typename T, int M, int KN, int TBW>
+__global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv(
+    const T *__restrict__ K, const T *__restrict__ V,
+    const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
+    const float *__restrict__ W, const float *__restrict__ dbuf1, T *__restrict__ dK,
+    T *__restrict__ dV, int H, int L, float s, float keps, float wts, int ntiles, int nitems) {
+  using frag = typename Mma<T>::frag;
+  __shared__ DkvSmem<T, M> sm;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int c16 = tid & 15;
+  const float cM = sqrtf(2.0f / M);
+  const float s2half = 0.5f * s * s;
+  int begin, end;
+  xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
   int cur = -1;
   for (int item = begin; item < end; ++item) {
     const int bh = item / ntiles;
     const int tile = item - bh * ntiles;
     const int h = bh % H;
-    const int t0 = tile * 64 * TBW;
-    const float *Rs = CAUSAL ? rstate + ((size_t)bh * ntiles + tile) * M * 65
-                             : rstate + (size_t)bh * M * 65;
     if (bh != cur) {
       __syncthreads();
       copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
       if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-      if constexpr (kK) build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
-      if constexpr (!CAUSAL) {
-        if constexpr (kK) build_state_rows<T, M>(sm.RA, sm.rz, Rs);
-        if constexpr (kV) build_state_cols<T, M>(sm.RB, Rs);
-      }
+      build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
+      const float *Rs = dbuf1 + (size_t)bh * M * 65;
+      build_state_rows<T, M>(sm.RA, sm.rz, Rs);
+      build_state_cols<T, M>(sm.RB, Rs);
       cur = bh;
       __syncthreads();
     }
-    if constexpr (CAUSAL) {
-      if constexpr (kK) build_state_rows<T, M>(sm.RA, sm.rz, Rs);
-      if constexpr (kV) build_state_cols<T, M>(sm.RB, Rs);
-      const T *Qh = Q + (size_t)bh * L * kD;
-      const T *dOh = dout + (size_t)bh * L * kD;
-      const int iq = t0 + 16 * w + c16;   // this wave's queries
-      if constexpr (kV) {
-        // features of queries 16 w .. (lane row = query), and u~^T = alpha dout^T
-        frag qf[2];
-        load_rows64<T>(qf, Qh, iq, L);
-#pragma unroll
-        for (int sidx = 0; sidx < NS; ++sidx) {
-          f32x4 f[2];
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int mb = 2 * sidx + hh;
-            const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&sm.bq[16 * mb + 4 * g]);
-            f32x4 p = P::mma(sm.WA[mb][0][l], qf[0], bcv);
-            p = P::mma(sm.WA[mb][1][l], qf[1], p);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) f[hh][j] = feature<KN, P>(p[j], keps);
-          }
-          sm.QA[w][sidx][l] = P::pack(f[0], f[1]);
-        }
-        frag dfq[2];
-        load_rows64<T>(dfq, dOh, iq, L);
-        float aj[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int t = t0 + 16 * w + 4 * g + j;
-          aj[j] = t < L ? aux[(size_t)bh * L + t].x : 0.f;
-        }
-        const frag sel[2] = {select_perm<T>(0), select_perm<T>(1)};
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            const f32x4 c = P::mma(dfq[kh], sel[half], zero4);
-            T *p = reinterpret_cast<T *>(&sm.UF[2 * kh + half][w >> 1][l]) + 4 * (w & 1);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(c[j] * aj[j]);
-          }
-      }
-      if constexpr (kK) {
-        frag qa[4][2];
-#pragma unroll
-        for (int tb = 0; tb < 4; ++tb) load_rows64<T>(qa[tb], Qh, t0 + 16 * tb + c16, L);
-        chunk_features_t<T, MB, KN>(sm.QT, sm.WA, sm.bq, qa, w * MB, keps);
-        frag dfq[2];
-        load_rows64<T>(dfq, dOh, iq, L);
-        sm.DA[w][0][l] = dfq[0];
-        sm.DA[w][1][l] = dfq[1];
-        if (g == 0) sm.au[16 * w + c16] = iq < L ? aux[(size_t)bh * L + iq] : make_float2(0.f, 0.f);
-      }
-      __syncthreads();
-    }
-
     const T *Kh = K + (size_t)bh * L * kD;
     const T *Vh = V + (size_t)bh * L * kD;
-    frag kf[TBW][2], vf[TBW][2];
-    float Dk[TBW];
+    const frag none[2] = {};
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
-      const int j = t0 + 16 * (w * TBW + tb) + c16;
-      load_rows64<T>(kf[tb], Kh, j, L);
-      load_rows64<T>(vf[tb], Vh, j, L);
+      const int j = tile * 64 * TBW + 16 * (w * TBW + tb) + c16;
+      frag kf[2], vf[2];
+      load_rows64<T>(kf, Kh, j, L);
+      load_rows64<T>(vf, Vh, j, L);
       float D = 1.f;
-      if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(kf[tb]));
-      Dk[tb] = j < L ? D : 0.f;
+      if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(kf));
+      f32x4 kacc[4], vacc[4];
+      float doth;
+      key_grad<T, M, KN, true, true, false>(sm.WA, sm.bq, sm.WT, sm.RA, sm.rz, sm.RB, nullptr,
+                                            none, nullptr, nullptr, kf, vf, 0, keps, kacc, doth,
+                                            vacc);
+      if (j < L) {
+        store_kgrad<T, KN>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
+        store_vgrad<T>(dV + ((size_t)bh * L + j) * kD, vacc, D);
+      }
     }
-    // causal dK: P3[i][j] = alpha_i (dout_i . v_j + u_d,i) for queries i >= j
+  }
+}
+
+// ------------------------------------------------------------ causal dK / dV
+template <typename T, int M, bool KPART>
+struct DkvScanSmem {
+  using frag = typename Mma<T>::frag;
+  frag WA[M / 16][2][64];
+  float bq[M];
+  frag QT[M / 16][2][64];      // the chunk's query features (row m, k = queries)
+  frag UF[4][2][64];           // u~^T: row = value column (permuted), k = queries
+  frag UD[KPART ? 2 : 1][4];   // u~ column d, one fragment per lane group
+  // dK: R rows over value columns, its column d, the input-gradient matrix
+  frag WT[KPART ? 4 : 1][KPART ? M / 32 : 1][64];
+  frag RA[KPART ? M / 16 : 1][2][64];
+  float rz[KPART ? M : 1];
+  // dV: R value columns over features, query features with lane row = query
+  frag RB[KPART ? 1 : 4][KPART ? 1 : M / 32][64];
+  frag QA[KPART ? 1 : 4][KPART ? 1 : M / 32][64];
+};
+
+// One workgroup per (head, segment), chunks from the last to the first. Wave w
+// keeps its slice of R, the aggregate of q-hat (x) u~ over the rows after the
+// chunk plus dstate_out: as R^T (rows = value columns permuted, lane = m) for dK,
+// as R (rows m, lane = value column) for dV. Each chunk publishes R, then folds
+// its own rows in; its keys take R plus the masked intra-chunk terms.
+template <typename T, int M, int KN, bool KPART>
+__global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv_scan(
+    const T *__restrict__ Q, const T *__restrict__ K, const T *__restrict__ V,
+    const T *__restrict__ dout, const float2 *__restrict__ aux,
+    const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
+    const float *__restrict__ W, const float *__restrict__ suffix, T *__restrict__ dK,
+    T *__restrict__ dV, int H, int L, int seg_len, int nseg, float s, float keps, float wts) {
+  constexpr int MB = M / 64;
+  constexpr int NS = M / 32;
+  using P = Mma<T>;
+  using frag = typename P::frag;
+  __shared__ DkvScanSmem<T, M, KPART> sm;
+  const int item = xcd_item(blockIdx.x, gridDim.x);
+  const int bh = item / nseg;
+  const int seg = item - bh * nseg;
+  const int h = bh % H;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6;
+  const int l = tid & 63;
+  const int g = l >> 4;
+  const int c16 = l & 15;
+  const float cM = sqrtf(2.0f / M);
+  const float s2half = 0.5f * s * s;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  const int r0 = seg * seg_len;
+  const int r1 = min(L, r0 + seg_len);
+
+  copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
+  if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
+  if constexpr (KPART) build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
+  // dK: acc[nb][mb] rows value column perm_col(nb, 4 g + j) (block 4: column d),
+  // lane m = 16 (w MB + mb) + lane % 16. dV: acc[mb][nb] rows m = 16 (w MB + mb)
+  // + 4 g + j, lane value column perm_col(nb, lane % 16).
+  f32x4 acc[KPART ? 5 : MB][KPART ? MB : 4];
+  {
+    const float *R = suffix + ((size_t)bh * nseg + seg) * M * 65;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (KPART) {
+          const float *row = R + (size_t)(16 * (w * MB + mb) + c16) * 65;
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) acc[nb][mb][j] = row[perm_col(nb, 4 * g + j)];
+          acc[4][mb][j] = row[64];
+        } else {
+          const float *row = R + (size_t)(16 * (w * MB + mb) + 4 * g + j) * 65;
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) acc[mb][nb][j] = row[perm_col(nb, c16)];
+        }
+      }
+  }
+  const frag sel[2] = {select_perm<T>(0), select_perm<T>(1)};
+  const T *Qh = Q + (size_t)bh * L * kD;
+  const T *Kh = K + (size_t)bh * L * kD;
+  const T *Vh = V + (size_t)bh * L * kD;
+  const T *dOh = dout + (size_t)bh * L * kD;
+  const float2 *auh = aux + (size_t)bh * L;
+  __syncthreads();
+
+  const int nch = (r1 - r0 + 63) / 64;
+  for (int c = nch - 1; c >= 0; --c) {
+    const int t0 = r0 + 64 * c;
+    // the chunk's queries: features (row m) of this wave's blocks, u~^T of this
+    // wave's 16 queries; (alpha, alpha u_d) of the rows
+    frag qa[4][2];
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) load_rows64<T>(qa[tb], Qh, t0 + 16 * tb + c16, r1);
+    chunk_features_t<T, MB, KN>(sm.QT, sm.WA, sm.bq, qa, w * MB, keps);
+    frag da[4][2];
+    float2 au[4];
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      const int t = t0 + 16 * tb + c16;
+      load_rows64<T>(da[tb], dOh, t, r1);
+      au[tb] = t < r1 ? auh[t] : make_float2(0.f, 0.f);
+    }
+    {
+      float aj[4], ej[4];   // of queries 16 w + 4 g + j
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        aj[j] = __shfl(au[w].x, 4 * g + j);
+        ej[j] = __shfl(au[w].y, 4 * g + j);
+      }
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const f32x4 cc = P::mma(da[w][kh], sel[half], zero4);
+          T *p = reinterpret_cast<T *>(&sm.UF[2 * kh + half][w >> 1][l]) + 4 * (w & 1);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(cc[j] * aj[j]);
+        }
+      if constexpr (KPART) {
+        if (c16 == 0) {
+          T *p = reinterpret_cast<T *>(&sm.UD[w >> 1][g]) + 4 * (w & 1);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(ej[j]);
+        }
+      }
+    }
+    if constexpr (!KPART) {
+      // this wave's 16 queries' features with lane row = query (k = m)
+      frag qf[2];
+      load_rows64<T>(qf, Qh, t0 + 16 * w + c16, r1);
+#pragma unroll
+      for (int sidx = 0; sidx < NS; ++sidx) {
+        f32x4 f[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int mb = 2 * sidx + hh;
+          const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&sm.bq[16 * mb + 4 * g]);
+          f32x4 p = P::mma(sm.WA[mb][0][l], qf[0], bcv);
+          p = P::mma(sm.WA[mb][1][l], qf[1], p);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) f[hh][j] = feature<KN, P>(p[j], keps);
+        }
+        sm.QA[w][sidx][l] = P::pack(f[0], f[1]);
+      }
+    }
+    // publish R (after the chunk)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int mbg = w * MB + mb;
+      if constexpr (KPART) {
+        sm.RA[mbg][0][l] = P::pack(acc[0][mb], acc[1][mb]);
+        sm.RA[mbg][1][l] = P::pack(acc[2][mb], acc[3][mb]);
+        if (g == 0) sm.rz[16 * mbg + c16] = acc[4][mb][0];
+      } else {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+          T *p = reinterpret_cast<T *>(&sm.RB[nb][mbg >> 1][l]) + 4 * (mbg & 1);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(acc[mb][nb][j]);
+        }
+      }
+    }
+    __syncthreads();
+
+    // fold the chunk's rows into R
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        const frag qt = sm.QT[w * MB + mb][sidx][l];
+        if constexpr (KPART) {
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) acc[nb][mb] = P::mma(sm.UF[nb][sidx][l], qt, acc[nb][mb]);
+          acc[4][mb] = P::mma(sm.UD[sidx][g], qt, acc[4][mb]);
+        } else {
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = P::mma(qt, sm.UF[nb][sidx][l], acc[mb][nb]);
+        }
+      }
+
+    // keys 16 w .. 16 w + 15 of the chunk
+    const int j = t0 + 16 * w + c16;
+    frag kf[2], vf[2];
+    load_rows64<T>(kf, Kh, j, r1);
+    load_rows64<T>(vf, Vh, j, r1);
+    float D = 1.f;
+    if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(kf));
+    // P3[i][j] = alpha_i (dout_i . v_j + u_d,i) for queries i >= j (B operand, k = queries)
     frag pb3[2];
-    if constexpr (CAUSAL && kK) {
+    if constexpr (KPART) {
       f32x4 pt[4];
 #pragma unroll
       for (int qb = 0; qb < 4; ++qb) {
-        f32x4 c = P::mma(sm.DA[qb][0][l], vf[0][0], zero4);
-        c = P::mma(sm.DA[qb][1][l], vf[0][1], c);
+        f32x4 cc = P::mma(da[qb][0], vf[0], zero4);
+        cc = P::mma(da[qb][1], vf[1], cc);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int ip = 16 * qb + 4 * g + j;
-          const float2 a = sm.au[ip];
-          pt[qb][j] = ip >= 16 * w + c16 ? fmaf(a.x, c[j], a.y) : 0.f;
+        for (int jj = 0; jj < 4; ++jj) {
+          const float a = __shfl(au[qb].x, 4 * g + jj);
+          const float e = __shfl(au[qb].y, 4 * g + jj);
+          pt[qb][jj] = 16 * qb + 4 * g + jj >= 16 * w + c16 ? fmaf(a, cc[jj], e) : 0.f;
         }
       }
       pb3[0] = P::pack(pt[0], pt[1]);
       pb3[1] = P::pack(pt[2], pt[3]);
     }
-
-    f32x4 kacc[TBW][4], vacc[TBW][4], p4[4];
-    float doth[TBW];
-#pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-      doth[tb] = 0.f;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        kacc[tb][k] = zero4;
-        vacc[tb][k] = zero4;
-      }
+    f32x4 kacc[4], vacc[4];
+    float doth;
+    // the tables of the other part are one-element placeholders, never read
+    using T2 = const frag(*)[2][64];
+    using TS = const frag(*)[M / 32][64];
+    key_grad<T, M, KN, KPART, !KPART, true>(
+        sm.WA, sm.bq, reinterpret_cast<TS>(&sm.WT[0][0][0]), reinterpret_cast<T2>(&sm.RA[0][0][0]),
+        sm.rz, reinterpret_cast<TS>(&sm.RB[0][0][0]), sm.QT, pb3,
+        reinterpret_cast<TS>(&sm.QA[0][0][0]), sm.UF, kf, vf, 16 * w + c16, keps, kacc, doth,
+        vacc);
+    if (j < r1) {
+      if constexpr (KPART)
+        store_kgrad<T, KN>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
+      else
+        store_vgrad<T>(dV + ((size_t)bh * L + j) * kD, vacc, D);
     }
-#pragma unroll
-    for (int qb = 0; qb < 4; ++qb) p4[qb] = zero4;
-
-#pragma unroll 2
-    for (int sidx = 0; sidx < NS; ++sidx) {
-      f32x4 kh[TBW][2], G[TBW][2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int mb = 2 * sidx + hh;
-        const frag a0 = sm.WA[mb][0][l];
-        const frag a1 = sm.WA[mb][1][l];
-        const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&sm.bq[16 * mb + 4 * g]);
-#pragma unroll
-        for (int tb = 0; tb < TBW; ++tb) {
-          f32x4 p = P::mma(a0, kf[tb][0], bcv);
-          p = P::mma(a1, kf[tb][1], p);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) kh[tb][hh][j] = feature<KN, P>(p[j], keps);
-          if constexpr (kK) {
-            f32x4 hv = P::mma(sm.RA[mb][0][l], vf[tb][0], zero4);
-            hv = P::mma(sm.RA[mb][1][l], vf[tb][1], hv);
-            if constexpr (CAUSAL) {
-              hv = P::mma(sm.QT[mb][0][l], pb3[0], hv);
-              hv = P::mma(sm.QT[mb][1][l], pb3[1], hv);
-            }
-            const f32x4 rzv = *reinterpret_cast<const f32x4 *>(&sm.rz[16 * mb + 4 * g]);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const float hj = hv[j] + rzv[j];
-              doth[tb] = fmaf(hj, kh[tb][hh][j], doth[tb]);
-              G[tb][hh][j] = sgn * hj * feature_slope<KN, P>(p[j]);
-            }
-          }
-        }
-      }
-#pragma unroll
-      for (int tb = 0; tb < TBW; ++tb) {
-        if constexpr (kK) {
-          const frag gb = P::pack(G[tb][0], G[tb][1]);
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb) kacc[tb][kb] = P::mma(sm.WT[kb][sidx][l], gb, kacc[tb][kb]);
-        }
-        if constexpr (kV) {
-          const frag kb_ = P::pack(kh[tb][0], kh[tb][1]);
-#pragma unroll
-          for (int nb = 0; nb < 4; ++nb) vacc[tb][nb] = P::mma(sm.RB[nb][sidx][l], kb_, vacc[tb][nb]);
-          if constexpr (CAUSAL) {
-#pragma unroll
-            for (int qb = 0; qb < 4; ++qb) p4[qb] = P::mma(sm.QA[qb][sidx][l], kb_, p4[qb]);
-          }
-        }
-      }
-    }
-    if constexpr (CAUSAL && kV) {
-      // keep queries i >= j, then u~^T (q-hat . k-hat) into the value gradient
-#pragma unroll
-      for (int qb = 0; qb < 4; ++qb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          p4[qb][j] = 16 * qb + 4 * g + j >= 16 * w + c16 ? p4[qb][j] : 0.f;
-#pragma unroll
-      for (int sidx = 0; sidx < 2; ++sidx) {
-        const frag pb = P::pack(p4[2 * sidx], p4[2 * sidx + 1]);
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) vacc[0][nb] = P::mma(sm.UF[nb][sidx][l], pb, vacc[0][nb]);
-      }
-    }
-
-#pragma unroll
-    for (int tb = 0; tb < TBW; ++tb) {
-      const int j = t0 + 16 * (w * TBW + tb) + c16;
-      float dh = doth[tb];
-      if constexpr (kK) {
-        dh += __shfl_xor(dh, 16);
-        dh += __shfl_xor(dh, 32);
-      }
-      if (j < L) {
-        const float D = Dk[tb];
-        if constexpr (kK) {
-          const float cx = KN == kCos ? s * s * dh : 0.f;
-          T *dst = dK + ((size_t)bh * L + j) * kD;
-#pragma unroll
-          for (int pp = 0; pp < 2; ++pp) {
-            f32x4 lo, hi;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              lo[e] = D * fmaf(cx, to_f32(kf[tb][pp][e]), kacc[tb][2 * pp][e]);
-              hi[e] = D * fmaf(cx, to_f32(kf[tb][pp][4 + e]), kacc[tb][2 * pp + 1][e]);
-            }
-            store8(dst + 32 * pp + 8 * g, lo, hi);
-          }
-        }
-        if constexpr (kV) {
-          T *dst = dV + ((size_t)bh * L + j) * kD;
-#pragma unroll
-          for (int pp = 0; pp < 2; ++pp)
-            store8(dst + 32 * pp + 8 * g, vacc[tb][2 * pp] * D, vacc[tb][2 * pp + 1] * D);
-        }
-      }
-    }
+    __syncthreads();
   }
 }
 
@@ -723,7 +980,8 @@ static float wt_scale(const Shape &sh) {
   return sh.kernel == 1 ? sh.s / sqrtf((float)sh.M) : sh.s;
 }
 
-// Rows per persistent bidirectional tile: 4 waves x TBW blocks of 16.
+// Rows per persistent bidirectional tile: 4 waves x kBwdTbw blocks of 16 (one
+// block per call of the row functions).
 constexpr int kBwdTbw = 2;
 constexpr int kBwdMaxWorkgroups = 256;
 
@@ -745,72 +1003,87 @@ hipError_t launch_suffix_scan(const Shape &sh, float *part, int nch, const float
   return hipGetLastError();
 }
 
-template <typename T, bool CAUSAL>
-static hipError_t bwd_dq_typed(const Shape &sh, const BwdArgs &a, hipStream_t st) {
-  constexpr int TBW = CAUSAL ? 1 : kBwdTbw;
-  const int rows = 64 * TBW;
-  const int ntiles = (sh.L + rows - 1) / rows;
-  const int nitems = ntiles * sh.BH;
-  dim3 grid(CAUSAL ? nitems : min(nitems, kBwdMaxWorkgroups));
-  const float wts = wt_scale(sh);
-  auto go = [&](auto kn, auto rn) -> hipError_t {
-    constexpr int KN = decltype(kn)::value;
-    constexpr bool RN = decltype(rn)::value;
-    FAVOR_BWD_DISPATCH_M(T, sh.M,
-        hipLaunchKernelGGL((k_bwd_dq<T, MM, KN, RN, CAUSAL, TBW>), grid, dim3(kBwdThreads), 0, st,
-                           (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
-                           (const T *)a.out, a.rsave, (const typename Mma<T>::frag *)a.wfr, a.bq,
-                           a.W, a.state, (T *)a.dQ, (float2 *)a.aux, sh.H, sh.L, sh.s, sh.keps,
-                           wts, ntiles, nitems));
-    return hipGetLastError();
-  };
+// Calls f(integral_constant KN, bool_constant RN) for the shape's feature kernel
+// and renormalisation.
+template <typename F>
+static hipError_t bwd_variant(const Shape &sh, F &&f) {
   using relu = std::integral_constant<int, kRelu>;
   using cosk = std::integral_constant<int, kCos>;
-  if (sh.kernel == 1) return sh.renorm ? go(relu{}, std::true_type{}) : go(relu{}, std::false_type{});
-  return sh.renorm ? go(cosk{}, std::true_type{}) : go(cosk{}, std::false_type{});
+  if (sh.kernel == 1) return sh.renorm ? f(relu{}, std::true_type{}) : f(relu{}, std::false_type{});
+  return sh.renorm ? f(cosk{}, std::true_type{}) : f(cosk{}, std::false_type{});
+}
+
+template <typename T>
+static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, hipStream_t st) {
+  const float wts = wt_scale(sh);
+  return bwd_variant(sh, [&](auto kn, auto rn) -> hipError_t {
+    constexpr int KN = decltype(kn)::value;
+    constexpr bool RN = decltype(rn)::value;
+    if (causal) {
+      dim3 grid(a.nseg * sh.BH);
+      FAVOR_BWD_DISPATCH_M(T, sh.M,
+          hipLaunchKernelGGL((k_bwd_dq_scan<T, MM, KN, RN>), grid, dim3(kBwdThreads), 0, st,
+                             (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
+                             (const T *)a.out, a.rsave, (const typename Mma<T>::frag *)a.wfr,
+                             a.bq, a.W, a.state, (T *)a.dQ, a.aux, sh.H, sh.L, a.seg_len, a.nseg,
+                             sh.s, sh.keps, wts));
+    } else {
+      const int ntiles = (sh.L + 64 * kBwdTbw - 1) / (64 * kBwdTbw);
+      const int nitems = ntiles * sh.BH;
+      dim3 grid(min(nitems, kBwdMaxWorkgroups));
+      FAVOR_BWD_DISPATCH_M(T, sh.M,
+          hipLaunchKernelGGL((k_bwd_dq<T, MM, KN, RN, kBwdTbw>), grid, dim3(kBwdThreads), 0, st,
+                             (const T *)a.Q, (const T *)a.dout, (const T *)a.out, a.rsave,
+                             (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                             (T *)a.dQ, a.aux, sh.H, sh.L, sh.s, sh.keps, wts, ntiles, nitems));
+    }
+    return hipGetLastError();
+  });
 }
 
 hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st) {
-  if (in == Dt::BF16)
-    return causal ? bwd_dq_typed<bf16, true>(sh, a, st) : bwd_dq_typed<bf16, false>(sh, a, st);
+  if (in == Dt::BF16) return bwd_dq_typed<bf16>(sh, causal, a, st);
   if (sh.M > 128) return hipErrorInvalidValue;
-  return causal ? bwd_dq_typed<float, true>(sh, a, st) : bwd_dq_typed<float, false>(sh, a, st);
+  return bwd_dq_typed<float>(sh, causal, a, st);
 }
 
-template <typename T, bool CAUSAL, int PART>
-static hipError_t bwd_dkv_typed(const Shape &sh, const BwdArgs &a, hipStream_t st) {
-  constexpr int TBW = CAUSAL ? 1 : kBwdTbw;
-  const int rows = 64 * TBW;
-  const int ntiles = (sh.L + rows - 1) / rows;
-  const int nitems = ntiles * sh.BH;
-  dim3 grid(CAUSAL ? nitems : min(nitems, kBwdMaxWorkgroups));
+template <typename T>
+static hipError_t bwd_dkv_typed(const Shape &sh, bool causal, const BwdArgs &a, hipStream_t st) {
   const float wts = wt_scale(sh);
-  auto go = [&](auto kn) -> hipError_t {
+  return bwd_variant(sh, [&](auto kn, auto) -> hipError_t {
     constexpr int KN = decltype(kn)::value;
-    FAVOR_BWD_DISPATCH_M(T, sh.M,
-        hipLaunchKernelGGL((k_bwd_dkv<T, MM, KN, CAUSAL, PART, TBW>), grid, dim3(kBwdThreads), 0,
-                           st, (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
-                           (const float2 *)a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W,
-                           a.state, (T *)a.dK, (T *)a.dV, sh.H, sh.L, sh.s, sh.keps, wts, ntiles,
-                           nitems));
+    if (causal) {
+      dim3 grid(a.nseg * sh.BH);
+      FAVOR_BWD_DISPATCH_M(T, sh.M, {
+        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, false>), grid, dim3(kBwdThreads), 0, st,
+                           (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
+                           a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.keps,
+                           wts);
+        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, true>), grid, dim3(kBwdThreads), 0, st,
+                           (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
+                           a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.keps,
+                           wts);
+      });
+    } else {
+      const int ntiles = (sh.L + 64 * kBwdTbw - 1) / (64 * kBwdTbw);
+      const int nitems = ntiles * sh.BH;
+      dim3 grid(min(nitems, kBwdMaxWorkgroups));
+      FAVOR_BWD_DISPATCH_M(T, sh.M,
+          hipLaunchKernelGGL((k_bwd_dkv<T, MM, KN, kBwdTbw>), grid, dim3(kBwdThreads), 0, st,
+                             (const T *)a.K, (const T *)a.V, (const typename Mma<T>::frag *)a.wfr,
+                             a.bq, a.W, a.state, (T *)a.dK, (T *)a.dV, sh.H, sh.L, sh.s, sh.keps,
+                             wts, ntiles, nitems));
+    }
     return hipGetLastError();
-  };
-  if (sh.kernel == 1) return go(std::integral_constant<int, kRelu>{});
-  return go(std::integral_constant<int, kCos>{});
+  });
 }
 
 hipError_t launch_bwd_dkv(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st) {
-  if (in == Dt::BF16) {
-    if (!causal) return bwd_dkv_typed<bf16, false, kPartBoth>(sh, a, st);
-    hipError_t e = bwd_dkv_typed<bf16, true, kPartDv>(sh, a, st);
-    if (e != hipSuccess) return e;
-    return bwd_dkv_typed<bf16, true, kPartDk>(sh, a, st);
-  }
+  if (in == Dt::BF16) return bwd_dkv_typed<bf16>(sh, causal, a, st);
   if (sh.M > 128) return hipErrorInvalidValue;
-  if (!causal) return bwd_dkv_typed<float, false, kPartBoth>(sh, a, st);
-  hipError_t e = bwd_dkv_typed<float, true, kPartDv>(sh, a, st);
-  if (e != hipSuccess) return e;
-  return bwd_dkv_typed<float, true, kPartDk>(sh, a, st);
+  return bwd_dkv_typed<float>(sh, causal, a, st);
 }
 
 }  // namespace favor

@@ -90,7 +90,7 @@ favor_status validate(const favor_desc *g, int op) {
   return FAVOR_OK;
 }
 
-// Backward workspace: the forward plan's buffers (split or 64-token chunk
+// Backward workspace: the forward plan's buffers (split or segment
 // partials, Buf1^T fragments, W'', b''), then the recomputed output and row
 // reciprocals, the per-row (alpha, alpha u_d), the aggregated q-hat (x) u~
 // partials and, bidirectional, Buf1 and dBuf1 as plain [M][65] arrays.
@@ -153,15 +153,10 @@ BwdPlan make_bwd_plan(const favor_desc *g, bool causal) {
   if (p.BH == 0 || g->L == 0) return p;
   const size_t elt = g->in_dtype == FAVOR_BF16 ? 2 : 4;
   const size_t agg = (size_t)g->M * 65 * sizeof(float);
-  if (causal) {
-    // one 64-token chunk per segment: the segment prefixes are the chunk states
-    p.rows_per_split = 64;
-    p.nsplit = (g->L + 63) / 64;
-  } else {
-    const Plan f = make_plan(g, kOpBidir);
-    p.rows_per_split = f.rows_per_split;
-    p.nsplit = f.nsplit;
-  }
+  // the forward plan's splits (bidirectional) or segments (causal)
+  const Plan f = make_plan(g, causal ? kOpCausal : kOpBidir);
+  p.rows_per_split = f.rows_per_split;
+  p.nsplit = f.nsplit;
   const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
   p.part = round_up((size_t)p.BH * p.nsplit * agg, 256);
   p.frags = causal ? 0 : round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
@@ -548,7 +543,8 @@ favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const
     e = favor::launch_sum_splits(sh, w.part, p.nsplit, w.buf1, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward Buf1");
-  favor::BwdArgs a{Q, K, V, dout, w.out, w.rsave, w.wfr, w.bq, W, w.buf1, dQ, dK, dV, w.aux};
+  favor::BwdArgs a{Q,  K,  V,  dout, w.out, w.rsave, w.wfr, w.bq, W, w.buf1,
+                   dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
   {
     favor::LaunchTimer t(favor::kKerBwdDq, st);
     e = favor::launch_bwd_dq(sh, in, false, a, st);
@@ -608,26 +604,27 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
   FAVOR_TRY(check_workspace(ws, ws_bytes, p.total));
   const favor::Dt in = dt_of(g->in_dtype);
   const BwdBufs w = carve(p, ws);
-  // forward recomputation with 64-token segments: the chunk states S_c (exclusive
-  // prefixes plus state_in), and the output with each row's reciprocal
+  // forward recomputation as favor_attn_causal runs it: the segment prefixes
+  // (plus state_in), and the output with each row's reciprocal
   {
     favor::LaunchTimer t(favor::kKerKside, st);
     e = favor::launch_kside(sh, in, K, V, W, b, w.wfr, w.bq, w.part, p.rows_per_split, p.nsplit,
                             st);
   }
-  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward chunk aggregates");
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward segment aggregates");
   {
     favor::LaunchTimer t(favor::kKerSegScan, st);
     e = favor::launch_seg_scan(sh, in, w.part, p.nsplit, state_in, nullptr, nullptr, st);
   }
-  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward chunk states");
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward segment prefixes");
   if (sh.renorm) {
     favor::LaunchTimer t(favor::kKerCausal, st);
     e = favor::launch_causal_save(sh, in, Q, K, V, w.wfr, w.bq, w.part, w.out, w.rsave,
                                   p.rows_per_split, p.nsplit, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward forward pass");
-  favor::BwdArgs a{Q, K, V, dout, w.out, w.rsave, w.wfr, w.bq, W, w.part, dQ, dK, dV, w.aux};
+  favor::BwdArgs a{Q,  K,  V,  dout, w.out, w.rsave, w.wfr, w.bq, W, w.part,
+                   dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
   {
     favor::LaunchTimer t(favor::kKerBwdDq, st);
     e = favor::launch_bwd_dq(sh, in, true, a, st);
@@ -638,7 +635,7 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
     e = favor::launch_kside_agg(sh, in, Q, dout, W, b, w.aux, w.part2, p.rows_per_split,
                                 p.nsplit, st);
   }
-  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward chunk aggregates");
+  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward row aggregates");
   {
     favor::LaunchTimer t(favor::kKerSuffixScan, st);
     e = favor::launch_suffix_scan(sh, w.part2, p.nsplit, dstate_out, dstate_in, st);

@@ -97,10 +97,11 @@ struct BwdArgs {
   const void *wfr;       // W'' fragments written by k_kside
   const float *bq;       // b''
   const float *W;        // [H][M][d]
-  const float *state;    // dQ: Buf1 [BH][M][65] or prefix states [BH][nch][M][65];
-                         // dK, dV: dBuf1 or suffix states, same layouts
+  const float *state;    // dQ: Buf1 [BH][M][65] or segment prefixes [BH][nseg][M][65];
+                         // dK, dV: dBuf1 or segment suffixes, same layouts
   void *dQ, *dK, *dV;
   float2 *aux;           // [BH][L] (alpha, alpha u_d)
+  int seg_len, nseg;     // causal: the segments of the forward plan
 };
 hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st);
 hipError_t launch_bwd_dkv(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st);
