@@ -37,7 +37,13 @@
 
 namespace favor {
 
-constexpr int kBwdThreads = 256;
+constexpr int kBwdBidirThreads = 512;   // the bidirectional kernels: two waves per SIMD
+
+// Copy N fragments global -> LDS with the whole workgroup.
+template <typename F, int N>
+__device__ __forceinline__ void copy_frags_wg(F *__restrict__ dst, const F *__restrict__ src) {
+  for (int idx = threadIdx.x; idx < N; idx += blockDim.x) dst[idx] = src[idx];
+}
 
 // ------------------------------------------------------------ small kernels
 __global__ __launch_bounds__(256) void k_sum_splits(const f32x4 *__restrict__ part, int ns, int n4,
@@ -96,7 +102,7 @@ template <typename T, int M>
 __device__ __forceinline__ void build_wt(typename Mma<T>::frag (*WT)[M / 32][64],
                                          const float *__restrict__ Wh, float scale) {
   constexpr int NS = M / 32;
-  for (int idx = threadIdx.x; idx < 4 * NS * 64; idx += kBwdThreads) {
+  for (int idx = threadIdx.x; idx < 4 * NS * 64; idx += blockDim.x) {
     const int l = idx & 63;
     const int s = (idx >> 6) % NS;
     const int kb = idx / (64 * NS);
@@ -115,7 +121,7 @@ __device__ __forceinline__ void build_wt(typename Mma<T>::frag (*WT)[M / 32][64]
 template <typename T, int M>
 __device__ __forceinline__ void build_state_rows(typename Mma<T>::frag (*SA)[2][64], float *sz,
                                                  const float *__restrict__ S) {
-  for (int idx = threadIdx.x; idx < (M / 16) * 2 * 64; idx += kBwdThreads) {
+  for (int idx = threadIdx.x; idx < (M / 16) * 2 * 64; idx += blockDim.x) {
     const int l = idx & 63;
     const int ks = (idx >> 6) & 1;
     const int mb = idx >> 7;
@@ -125,7 +131,7 @@ __device__ __forceinline__ void build_state_rows(typename Mma<T>::frag (*SA)[2][
     for (int i = 0; i < 8; ++i) v[i] = row[i];
     SA[mb][ks][l] = Mma<T>::from_f32(v, 1.f);
   }
-  for (int m = threadIdx.x; m < M; m += kBwdThreads) sz[m] = S[(size_t)m * 65 + 64];
+  for (int m = threadIdx.x; m < M; m += blockDim.x) sz[m] = S[(size_t)m * 65 + 64];
 }
 
 // The value columns of S as A operand over features: row = column
@@ -134,7 +140,7 @@ template <typename T, int M>
 __device__ __forceinline__ void build_state_cols(typename Mma<T>::frag (*SB)[M / 32][64],
                                                  const float *__restrict__ S) {
   constexpr int NS = M / 32;
-  for (int idx = threadIdx.x; idx < 4 * NS * 64; idx += kBwdThreads) {
+  for (int idx = threadIdx.x; idx < 4 * NS * 64; idx += blockDim.x) {
     const int l = idx & 63;
     const int s = (idx >> 6) % NS;
     const int nb = idx / (64 * NS);
@@ -233,10 +239,9 @@ __device__ __forceinline__ void query_grad(
     const float *sz, const typename Mma<T>::frag (*KT)[2][64],
     const typename Mma<T>::frag (&pb2)[2], const typename Mma<T>::frag (&qf)[2],
     const typename Mma<T>::frag (&df)[2], float alpha, float ud, float s, float keps,
-    f32x4 (&dacc)[4], float &dot2) {
+    f32x4 (&dacc)[4], float &dot2, int s0 = 0, int s1 = M / 32) {
   using P = Mma<T>;
   using frag = typename P::frag;
-  constexpr int NS = M / 32;
   constexpr float sgn = KN == kCos ? -1.f : 1.f;
   const int l = lane_id();
   const int g = l >> 4;
@@ -244,7 +249,7 @@ __device__ __forceinline__ void query_grad(
   for (int kb = 0; kb < 4; ++kb) dacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
   dot2 = 0.f;
 #pragma unroll 2
-  for (int sidx = 0; sidx < NS; ++sidx) {
+  for (int sidx = s0; sidx < s1; ++sidx) {
     f32x4 G[2];
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
@@ -331,10 +336,10 @@ struct DqSmem {
   float bq[M];               // b''
 };
 
-// Items are (head, tile of 64 TBW rows), walked persistently over XCD-local
-// ranges; Buf1 [BH][M][65] fp32.
+// Items are (head, tile of 8 waves x TBW x 16 rows), walked persistently over
+// XCD-local ranges; Buf1 [BH][M][65] fp32.
 template <typename T, int M, int KN, bool RN, int TBW>
-__global__ __launch_bounds__(kBwdThreads) void k_bwd_dq(
+__global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
     const T *__restrict__ Q, const T *__restrict__ dout, const T *__restrict__ out,
     const float *__restrict__ rsave, const typename Mma<T>::frag *__restrict__ wfr,
     const float *__restrict__ bqg, const float *__restrict__ W, const float *__restrict__ buf1,
@@ -357,7 +362,7 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq(
     const int h = bh % H;
     if (bh != cur) {
       __syncthreads();
-      copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
+      copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
       if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
       build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
       build_state_rows<T, M>(sm.SA, sm.sz, buf1 + (size_t)bh * M * 65);
@@ -370,7 +375,7 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq(
     const frag none[2] = {};
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
-      const int i = tile * 64 * TBW + 16 * (w * TBW + tb) + c16;
+      const int i = tile * (kBwdBidirThreads / 4) * TBW + 16 * (w * TBW + tb) + c16;
       frag qf[2], df[2];
       load_rows64<T>(qf, Qh, i, L);
       load_rows64<T>(df, dOh, i, L);
@@ -389,6 +394,18 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq(
 }
 
 // ------------------------------------------------------------ causal dQ
+// The segment-scan kernels run eight waves: wave w works on row block w % 4 of
+// the chunk over half hf = w / 4 of the feature steps (the two halves' partial
+// sums meet in LDS), and on FB feature blocks of the carried state.
+constexpr int kScanThreads = 512;
+template <int M>
+struct ScanSplit {
+  static constexpr int NB = M / 16;                 // feature blocks
+  static constexpr int FB = NB >= 8 ? NB / 8 : 1;   // blocks per state wave
+  static constexpr int FW = NB / FB;                // waves holding state (4 or 8)
+  static constexpr int NS = M / 32;                 // feature steps
+};
+
 template <typename T, int M>
 struct DqScanSmem {
   using frag = typename Mma<T>::frag;
@@ -400,22 +417,24 @@ struct DqScanSmem {
   frag KT[M / 16][2][64];    // the chunk's key features (row m, k = keys)
   frag VtF[4][2][64];        // C~ of the chunk: row = value column (permuted), k = keys
   frag DF[2][4];             // its column d (D~ per key), one fragment per lane group
+  float red[4][17][64];      // the second half's partial dQ and g~ . q-hat per row block
 };
 
-// One workgroup per (head, segment of the forward plan). Wave w keeps rows
-// [w M/4, (w+1) M/4) of S^T (value columns in permuted order, fp32) in
-// registers, publishes S before each 64-token chunk, and folds the chunk's
-// C~^T K-hat in after; the chunk's queries then take S u plus the masked
-// intra-chunk terms.
+// One workgroup per (head, segment of the forward plan). The state waves keep
+// rows of S^T (value columns in permuted order, fp32; lanes = their features)
+// in registers, publish S before each 64-token chunk and fold the chunk's
+// C~^T K-hat in after; the chunk's queries take S u plus the masked intra-chunk
+// terms.
 template <typename T, int M, int KN, bool RN>
-__global__ __launch_bounds__(kBwdThreads) void k_bwd_dq_scan(
+__global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
     const T *__restrict__ Q, const T *__restrict__ K, const T *__restrict__ V,
     const T *__restrict__ dout, const T *__restrict__ out, const float *__restrict__ rsave,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ prefix, T *__restrict__ dQ,
     float2 *__restrict__ aux, int H, int L, int seg_len, int nseg, float s, float keps,
     float wts) {
-  constexpr int MB = M / 64;
+  using SP = ScanSplit<M>;
+  constexpr int FB = SP::FB;
   using P = Mma<T>;
   using frag = typename P::frag;
   __shared__ DqScanSmem<T, M> sm;
@@ -428,23 +447,26 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq_scan(
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
+  const int qb = w & 3;          // row block of the chunk
+  const int hf = w >> 2;         // half of the feature steps
+  const bool sw = w < SP::FW;    // holds a slice of the state
   const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
   const int r0 = seg * seg_len;
   const int r1 = min(L, r0 + seg_len);
 
-  copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
+  copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
   if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
   build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
   // S^T slice: acc[nb][mb] rows = value column perm_col(nb, 4 g + j) (block 4: column
-  // d replicated), lane = feature m = 16 (w MB + mb) + lane % 16
-  f32x4 acc[5][MB];
-  {
+  // d replicated), lane = feature m = 16 (w FB + mb) + lane % 16
+  f32x4 acc[5][FB];
+  if (sw) {
     const float *S = prefix + ((size_t)bh * nseg + seg) * M * 65;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const float *row = S + (size_t)(16 * (w * MB + mb) + c16) * 65;
+    for (int mb = 0; mb < FB; ++mb) {
+      const float *row = S + (size_t)(16 * (w * FB + mb) + c16) * 65;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
 #pragma unroll
@@ -459,6 +481,8 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq_scan(
   const T *Vh = V + (size_t)bh * L * kD;
   const T *dOh = dout + (size_t)bh * L * kD;
   const T *Oh = out + (size_t)bh * L * kD;
+  const int s0 = hf * (SP::NS / 2);
+  const int s1 = s0 + SP::NS / 2;
   __syncthreads();
 
   for (int t0 = r0; t0 < r1; t0 += 64) {
@@ -474,49 +498,58 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq_scan(
       if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(ka[tb]));
       Dk[tb] = t < r1 ? D : 0.f;
     }
-    chunk_features_t<T, MB, KN>(sm.KT, sm.WA, sm.bq, ka, w * MB, keps);
-    {
-      float Dj[4];   // D~ of keys 16 w + 4 g + j
+    if (sw) chunk_features_t<T, FB, KN>(sm.KT, sm.WA, sm.bq, ka, w * FB, keps);
+    if (hf == 0) {   // C~ of key block qb (its rows loaded again: no runtime register index)
+      const int t = t0 + 16 * qb + c16;
+      frag ko[2], vo[2];
+      load_rows64<T>(ko, Kh, t, r1);
+      load_rows64<T>(vo, Vh, t, r1);
+      float Do = 1.f;
+      if constexpr (KN == kCos) Do = cM * expf(s2half * sq_norm16<T>(ko));
+      Do = t < r1 ? Do : 0.f;
+      float Dj[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Dk[w], 4 * g + j);
+      for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Do, 4 * g + j);
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-          const f32x4 c = P::mma(va[w][kh], sel[half], zero4);
-          T *p = reinterpret_cast<T *>(&sm.VtF[2 * kh + half][w >> 1][l]) + 4 * (w & 1);
+          const f32x4 c = P::mma(vo[kh], sel[half], zero4);
+          T *p = reinterpret_cast<T *>(&sm.VtF[2 * kh + half][qb >> 1][l]) + 4 * (qb & 1);
 #pragma unroll
           for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(c[j] * Dj[j]);
         }
       if (c16 == 0) {
-        T *p = reinterpret_cast<T *>(&sm.DF[w >> 1][g]) + 4 * (w & 1);
+        T *p = reinterpret_cast<T *>(&sm.DF[qb >> 1][g]) + 4 * (qb & 1);
 #pragma unroll
         for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(Dj[j]);
       }
     }
-    // publish S (before the chunk)
+    if (sw) {   // publish S (before the chunk)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int mbg = w * MB + mb;
-      sm.SA[mbg][0][l] = P::pack(acc[0][mb], acc[1][mb]);
-      sm.SA[mbg][1][l] = P::pack(acc[2][mb], acc[3][mb]);
-      if (g == 0) sm.sz[16 * mbg + c16] = acc[4][mb][0];
+      for (int mb = 0; mb < FB; ++mb) {
+        const int mbg = w * FB + mb;
+        sm.SA[mbg][0][l] = P::pack(acc[0][mb], acc[1][mb]);
+        sm.SA[mbg][1][l] = P::pack(acc[2][mb], acc[3][mb]);
+        if (g == 0) sm.sz[16 * mbg + c16] = acc[4][mb][0];
+      }
     }
     __syncthreads();
 
-    // fold the chunk into S^T: rows value columns, k = keys, columns m
+    if (sw) {   // fold the chunk into S^T: rows value columns, k = keys, columns m
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+      for (int mb = 0; mb < FB; ++mb)
 #pragma unroll
-      for (int sidx = 0; sidx < 2; ++sidx) {
-        const frag kb = sm.KT[w * MB + mb][sidx][l];
+        for (int sidx = 0; sidx < 2; ++sidx) {
+          const frag kb = sm.KT[w * FB + mb][sidx][l];
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) acc[nb][mb] = P::mma(sm.VtF[nb][sidx][l], kb, acc[nb][mb]);
-        acc[4][mb] = P::mma(sm.DF[sidx][g], kb, acc[4][mb]);
-      }
+          for (int nb = 0; nb < 4; ++nb) acc[nb][mb] = P::mma(sm.VtF[nb][sidx][l], kb, acc[nb][mb]);
+          acc[4][mb] = P::mma(sm.DF[sidx][g], kb, acc[4][mb]);
+        }
+    }
 
-    // queries 16 w .. 16 w + 15 of the chunk
-    const int i = t0 + 16 * w + c16;
+    // queries of row block qb, feature steps [s0, s1)
+    const int i = t0 + 16 * qb + c16;
     frag qf[2], df[2];
     load_rows64<T>(qf, Qh, i, r1);
     load_rows64<T>(df, dOh, i, r1);
@@ -533,7 +566,7 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq_scan(
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const float D = __shfl(Dk[kb], 4 * g + j);
-          pt[kb][j] = 16 * kb + 4 * g + j <= 16 * w + c16 ? D * (c[j] + ud) : 0.f;
+          pt[kb][j] = 16 * kb + 4 * g + j <= 16 * qb + c16 ? D * (c[j] + ud) : 0.f;
         }
       }
       pb2[0] = P::pack(pt[0], pt[1]);
@@ -542,12 +575,26 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dq_scan(
     f32x4 dacc[4];
     float dot2;
     query_grad<T, M, KN, true>(sm.WA, sm.bq, sm.WT, sm.SA, sm.sz, sm.KT, pb2, qf, df, alpha, ud,
-                               s, keps, dacc, dot2);
-    if (i < r1) {
-      store_qgrad<T, KN>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
-      if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
+                               s, keps, dacc, dot2, s0, s1);
+    if (hf == 1) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sm.red[qb][4 * k + j][l] = dacc[k][j];
+      sm.red[qb][16][l] = dot2;
     }
     __syncthreads();
+    if (hf == 0) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dacc[k][j] += sm.red[qb][4 * k + j][l];
+      dot2 += sm.red[qb][16][l];
+      if (i < r1) {
+        store_qgrad<T, KN>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
+        if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
+      }
+    }
   }
 }
 
@@ -564,10 +611,9 @@ __device__ __forceinline__ void key_grad(
     const typename Mma<T>::frag (*QT)[2][64], const typename Mma<T>::frag (&pb3)[2],
     const typename Mma<T>::frag (*QA)[M / 32][64], const typename Mma<T>::frag (*UF)[2][64],
     const typename Mma<T>::frag (&kf)[2], const typename Mma<T>::frag (&vf)[2], int jpos,
-    float keps, f32x4 (&kacc)[4], float &doth, f32x4 (&vacc)[4]) {
+    float keps, f32x4 (&kacc)[4], float &doth, f32x4 (&vacc)[4], int s0 = 0, int s1 = M / 32) {
   using P = Mma<T>;
   using frag = typename P::frag;
-  constexpr int NS = M / 32;
   constexpr float sgn = KN == kCos ? -1.f : 1.f;
   const int l = lane_id();
   const int g = l >> 4;
@@ -581,7 +627,7 @@ __device__ __forceinline__ void key_grad(
   }
   doth = 0.f;
 #pragma unroll 2
-  for (int sidx = 0; sidx < NS; ++sidx) {
+  for (int sidx = s0; sidx < s1; ++sidx) {
     f32x4 kh[2], G[2];
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
@@ -680,7 +726,7 @@ struct DkvSmem {
 };
 
 template <typename T, int M, int KN, int TBW>
-__global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv(
+__global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dkv(
     const T *__restrict__ K, const T *__restrict__ V,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ dbuf1, T *__restrict__ dK,
@@ -701,7 +747,7 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv(
     const int h = bh % H;
     if (bh != cur) {
       __syncthreads();
-      copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
+      copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
       if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
       build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
       const float *Rs = dbuf1 + (size_t)bh * M * 65;
@@ -715,7 +761,7 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv(
     const frag none[2] = {};
 #pragma unroll
     for (int tb = 0; tb < TBW; ++tb) {
-      const int j = tile * 64 * TBW + 16 * (w * TBW + tb) + c16;
+      const int j = tile * (kBwdBidirThreads / 4) * TBW + 16 * (w * TBW + tb) + c16;
       frag kf[2], vf[2];
       load_rows64<T>(kf, Kh, j, L);
       load_rows64<T>(vf, Vh, j, L);
@@ -750,22 +796,24 @@ struct DkvScanSmem {
   // dV: R value columns over features, query features with lane row = query
   frag RB[KPART ? 1 : 4][KPART ? 1 : M / 32][64];
   frag QA[KPART ? 1 : 4][KPART ? 1 : M / 32][64];
+  float red[4][17][64];        // the second half's partial sums per row block
 };
 
-// One workgroup per (head, segment), chunks from the last to the first. Wave w
-// keeps its slice of R, the aggregate of q-hat (x) u~ over the rows after the
-// chunk plus dstate_out: as R^T (rows = value columns permuted, lane = m) for dK,
-// as R (rows m, lane = value column) for dV. Each chunk publishes R, then folds
-// its own rows in; its keys take R plus the masked intra-chunk terms.
+// One workgroup per (head, segment), chunks from the last to the first. The
+// state waves keep their slice of R, the aggregate of q-hat (x) u~ over the rows
+// after the chunk plus dstate_out: as R^T (rows = value columns permuted, lanes =
+// m) for dK, as R (rows m, lanes = value columns) for dV. Each chunk publishes
+// R, then folds its own rows in; its keys take R plus the masked intra-chunk
+// terms.
 template <typename T, int M, int KN, bool KPART>
-__global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv_scan(
+__global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     const T *__restrict__ Q, const T *__restrict__ K, const T *__restrict__ V,
     const T *__restrict__ dout, const float2 *__restrict__ aux,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ suffix, T *__restrict__ dK,
     T *__restrict__ dV, int H, int L, int seg_len, int nseg, float s, float keps, float wts) {
-  constexpr int MB = M / 64;
-  constexpr int NS = M / 32;
+  using SP = ScanSplit<M>;
+  constexpr int FB = SP::FB;
   using P = Mma<T>;
   using frag = typename P::frag;
   __shared__ DkvScanSmem<T, M, KPART> sm;
@@ -778,32 +826,37 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv_scan(
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
+  const int qb = w & 3;
+  const int hf = w >> 2;
+  const bool sw = w < SP::FW;
   const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
   const int r0 = seg * seg_len;
   const int r1 = min(L, r0 + seg_len);
+  const int s0 = hf * (SP::NS / 2);
+  const int s1 = s0 + SP::NS / 2;
 
-  copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
+  copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
   if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
   if constexpr (KPART) build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
   // dK: acc[nb][mb] rows value column perm_col(nb, 4 g + j) (block 4: column d),
-  // lane m = 16 (w MB + mb) + lane % 16. dV: acc[mb][nb] rows m = 16 (w MB + mb)
+  // lane m = 16 (w FB + mb) + lane % 16. dV: acc[mb][nb] rows m = 16 (w FB + mb)
   // + 4 g + j, lane value column perm_col(nb, lane % 16).
-  f32x4 acc[KPART ? 5 : MB][KPART ? MB : 4];
-  {
+  f32x4 acc[KPART ? 5 : FB][KPART ? FB : 4];
+  if (sw) {
     const float *R = suffix + ((size_t)bh * nseg + seg) * M * 65;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int mb = 0; mb < FB; ++mb)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if constexpr (KPART) {
-          const float *row = R + (size_t)(16 * (w * MB + mb) + c16) * 65;
+          const float *row = R + (size_t)(16 * (w * FB + mb) + c16) * 65;
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) acc[nb][mb][j] = row[perm_col(nb, 4 * g + j)];
           acc[4][mb][j] = row[64];
         } else {
-          const float *row = R + (size_t)(16 * (w * MB + mb) + 4 * g + j) * 65;
+          const float *row = R + (size_t)(16 * (w * FB + mb) + 4 * g + j) * 65;
 #pragma unroll
           for (int nb = 0; nb < 4; ++nb) acc[mb][nb][j] = row[perm_col(nb, c16)];
         }
@@ -820,12 +873,12 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv_scan(
   const int nch = (r1 - r0 + 63) / 64;
   for (int c = nch - 1; c >= 0; --c) {
     const int t0 = r0 + 64 * c;
-    // the chunk's queries: features (row m) of this wave's blocks, u~^T of this
-    // wave's 16 queries; (alpha, alpha u_d) of the rows
+    // the chunk's queries: features (row m) of the state waves' blocks, u~^T of
+    // row block qb; (alpha, alpha u_d) of every row
     frag qa[4][2];
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) load_rows64<T>(qa[tb], Qh, t0 + 16 * tb + c16, r1);
-    chunk_features_t<T, MB, KN>(sm.QT, sm.WA, sm.bq, qa, w * MB, keps);
+    if (sw) chunk_features_t<T, FB, KN>(sm.QT, sm.WA, sm.bq, qa, w * FB, keps);
     frag da[4][2];
     float2 au[4];
 #pragma unroll
@@ -834,104 +887,110 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv_scan(
       load_rows64<T>(da[tb], dOh, t, r1);
       au[tb] = t < r1 ? auh[t] : make_float2(0.f, 0.f);
     }
-    {
-      float aj[4], ej[4];   // of queries 16 w + 4 g + j
+    if (hf == 0) {   // row block qb loaded again: no runtime register index
+      const int t = t0 + 16 * qb + c16;
+      frag dob[2];
+      load_rows64<T>(dob, dOh, t, r1);
+      const float2 ao = t < r1 ? auh[t] : make_float2(0.f, 0.f);
+      float aj[4], ej[4];   // of queries 16 qb + 4 g + j
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        aj[j] = __shfl(au[w].x, 4 * g + j);
-        ej[j] = __shfl(au[w].y, 4 * g + j);
+        aj[j] = __shfl(ao.x, 4 * g + j);
+        ej[j] = __shfl(ao.y, 4 * g + j);
       }
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-          const f32x4 cc = P::mma(da[w][kh], sel[half], zero4);
-          T *p = reinterpret_cast<T *>(&sm.UF[2 * kh + half][w >> 1][l]) + 4 * (w & 1);
+          const f32x4 cc = P::mma(dob[kh], sel[half], zero4);
+          T *p = reinterpret_cast<T *>(&sm.UF[2 * kh + half][qb >> 1][l]) + 4 * (qb & 1);
 #pragma unroll
           for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(cc[j] * aj[j]);
         }
       if constexpr (KPART) {
         if (c16 == 0) {
-          T *p = reinterpret_cast<T *>(&sm.UD[w >> 1][g]) + 4 * (w & 1);
+          T *p = reinterpret_cast<T *>(&sm.UD[qb >> 1][g]) + 4 * (qb & 1);
 #pragma unroll
           for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(ej[j]);
         }
       }
     }
     if constexpr (!KPART) {
-      // this wave's 16 queries' features with lane row = query (k = m)
-      frag qf[2];
-      load_rows64<T>(qf, Qh, t0 + 16 * w + c16, r1);
-#pragma unroll
-      for (int sidx = 0; sidx < NS; ++sidx) {
+      // row block qb's features with lane row = query (k = m), steps [s0, s1)
+      frag qo[2];
+      load_rows64<T>(qo, Qh, t0 + 16 * qb + c16, r1);
+#pragma unroll 2
+      for (int sidx = s0; sidx < s1; ++sidx) {
         f32x4 f[2];
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           const int mb = 2 * sidx + hh;
           const f32x4 bcv = *reinterpret_cast<const f32x4 *>(&sm.bq[16 * mb + 4 * g]);
-          f32x4 p = P::mma(sm.WA[mb][0][l], qf[0], bcv);
-          p = P::mma(sm.WA[mb][1][l], qf[1], p);
+          f32x4 p = P::mma(sm.WA[mb][0][l], qo[0], bcv);
+          p = P::mma(sm.WA[mb][1][l], qo[1], p);
 #pragma unroll
           for (int j = 0; j < 4; ++j) f[hh][j] = feature<KN, P>(p[j], keps);
         }
-        sm.QA[w][sidx][l] = P::pack(f[0], f[1]);
+        sm.QA[qb][sidx][l] = P::pack(f[0], f[1]);
       }
     }
-    // publish R (after the chunk)
+    if (sw) {   // publish R (after the chunk)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int mbg = w * MB + mb;
-      if constexpr (KPART) {
-        sm.RA[mbg][0][l] = P::pack(acc[0][mb], acc[1][mb]);
-        sm.RA[mbg][1][l] = P::pack(acc[2][mb], acc[3][mb]);
-        if (g == 0) sm.rz[16 * mbg + c16] = acc[4][mb][0];
-      } else {
+      for (int mb = 0; mb < FB; ++mb) {
+        const int mbg = w * FB + mb;
+        if constexpr (KPART) {
+          sm.RA[mbg][0][l] = P::pack(acc[0][mb], acc[1][mb]);
+          sm.RA[mbg][1][l] = P::pack(acc[2][mb], acc[3][mb]);
+          if (g == 0) sm.rz[16 * mbg + c16] = acc[4][mb][0];
+        } else {
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) {
-          T *p = reinterpret_cast<T *>(&sm.RB[nb][mbg >> 1][l]) + 4 * (mbg & 1);
+          for (int nb = 0; nb < 4; ++nb) {
+            T *p = reinterpret_cast<T *>(&sm.RB[nb][mbg >> 1][l]) + 4 * (mbg & 1);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(acc[mb][nb][j]);
+            for (int j = 0; j < 4; ++j) p[j] = from_f32<T>(acc[mb][nb][j]);
+          }
         }
       }
     }
     __syncthreads();
 
-    // fold the chunk's rows into R
+    if (sw) {   // fold the chunk's rows into R
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+      for (int mb = 0; mb < FB; ++mb)
 #pragma unroll
-      for (int sidx = 0; sidx < 2; ++sidx) {
-        const frag qt = sm.QT[w * MB + mb][sidx][l];
-        if constexpr (KPART) {
+        for (int sidx = 0; sidx < 2; ++sidx) {
+          const frag qt = sm.QT[w * FB + mb][sidx][l];
+          if constexpr (KPART) {
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb) acc[nb][mb] = P::mma(sm.UF[nb][sidx][l], qt, acc[nb][mb]);
-          acc[4][mb] = P::mma(sm.UD[sidx][g], qt, acc[4][mb]);
-        } else {
+            for (int nb = 0; nb < 4; ++nb)
+              acc[nb][mb] = P::mma(sm.UF[nb][sidx][l], qt, acc[nb][mb]);
+            acc[4][mb] = P::mma(sm.UD[sidx][g], qt, acc[4][mb]);
+          } else {
 #pragma unroll
-          for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = P::mma(qt, sm.UF[nb][sidx][l], acc[mb][nb]);
+            for (int nb = 0; nb < 4; ++nb)
+              acc[mb][nb] = P::mma(qt, sm.UF[nb][sidx][l], acc[mb][nb]);
+          }
         }
-      }
+    }
 
-    // keys 16 w .. 16 w + 15 of the chunk
-    const int j = t0 + 16 * w + c16;
+    // keys of row block qb, feature steps [s0, s1)
+    const int j = t0 + 16 * qb + c16;
     frag kf[2], vf[2];
     load_rows64<T>(kf, Kh, j, r1);
     load_rows64<T>(vf, Vh, j, r1);
-    float D = 1.f;
-    if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(kf));
     // P3[i][j] = alpha_i (dout_i . v_j + u_d,i) for queries i >= j (B operand, k = queries)
     frag pb3[2];
     if constexpr (KPART) {
       f32x4 pt[4];
 #pragma unroll
-      for (int qb = 0; qb < 4; ++qb) {
-        f32x4 cc = P::mma(da[qb][0], vf[0], zero4);
-        cc = P::mma(da[qb][1], vf[1], cc);
+      for (int q = 0; q < 4; ++q) {
+        f32x4 cc = P::mma(da[q][0], vf[0], zero4);
+        cc = P::mma(da[q][1], vf[1], cc);
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-          const float a = __shfl(au[qb].x, 4 * g + jj);
-          const float e = __shfl(au[qb].y, 4 * g + jj);
-          pt[qb][jj] = 16 * qb + 4 * g + jj >= 16 * w + c16 ? fmaf(a, cc[jj], e) : 0.f;
+          const float a = __shfl(au[q].x, 4 * g + jj);
+          const float e = __shfl(au[q].y, 4 * g + jj);
+          pt[q][jj] = 16 * q + 4 * g + jj >= 16 * qb + c16 ? fmaf(a, cc[jj], e) : 0.f;
         }
       }
       pb3[0] = P::pack(pt[0], pt[1]);
@@ -945,26 +1004,51 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv_scan(
     key_grad<T, M, KN, KPART, !KPART, true>(
         sm.WA, sm.bq, reinterpret_cast<TS>(&sm.WT[0][0][0]), reinterpret_cast<T2>(&sm.RA[0][0][0]),
         sm.rz, reinterpret_cast<TS>(&sm.RB[0][0][0]), sm.QT, pb3,
-        reinterpret_cast<TS>(&sm.QA[0][0][0]), sm.UF, kf, vf, 16 * w + c16, keps, kacc, doth,
-        vacc);
-    if (j < r1) {
-      if constexpr (KPART)
-        store_kgrad<T, KN>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
-      else
-        store_vgrad<T>(dV + ((size_t)bh * L + j) * kD, vacc, D);
+        reinterpret_cast<TS>(&sm.QA[0][0][0]), sm.UF, kf, vf, 16 * qb + c16, keps, kacc, doth,
+        vacc, s0, s1);
+    f32x4 (&part)[4] = KPART ? kacc : vacc;
+    if (hf == 1) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) sm.red[qb][4 * k + jj][l] = part[k][jj];
+      sm.red[qb][16][l] = doth;
     }
     __syncthreads();
+    if (hf == 0) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) part[k][jj] += sm.red[qb][4 * k + jj][l];
+      doth += sm.red[qb][16][l];
+      float D = 1.f;
+      if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(kf));
+      if (j < r1) {
+        if constexpr (KPART)
+          store_kgrad<T, KN>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
+        else
+          store_vgrad<T>(dV + ((size_t)bh * L + j) * kD, vacc, D);
+      }
+    }
   }
 }
 
 // ------------------------------------------------------------ launchers
-// M dispatch; fp32 operands double the LDS tables, so fp32 stops at M = 128.
-#define FAVOR_BWD_DISPATCH_M(T_, M_, ...)                                  \
+// M dispatch up to MAX_ (fp32 operands double the LDS tables: the fp32
+// kernels stop at M = 128 bidirectional and M = 64 causal).
+#define FAVOR_BWD_DISPATCH_M(MAX_, M_, ...)                                \
   switch (M_) {                                                            \
     case 64: { constexpr int MM = 64; __VA_ARGS__; } break;                 \
-    case 128: { constexpr int MM = 128; __VA_ARGS__; } break;               \
+    case 128:                                                              \
+      if constexpr (MAX_ >= 128) {                                          \
+        constexpr int MM = 128;                                            \
+        __VA_ARGS__;                                                       \
+        break;                                                             \
+      } else {                                                             \
+        return hipErrorInvalidValue;                                       \
+      }                                                                    \
     case 256:                                                              \
-      if constexpr (sizeof(T_) == 2) {                                      \
+      if constexpr (MAX_ >= 256) {                                          \
         constexpr int MM = 256;                                            \
         __VA_ARGS__;                                                       \
         break;                                                             \
@@ -974,13 +1058,17 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_dkv_scan(
     default: return hipErrorInvalidValue;                                  \
   }
 
+template <typename T> constexpr int bwd_max_m(bool causal) {
+  return sizeof(T) == 2 ? 256 : (causal ? 64 : 128);
+}
+
 // Scale of W in the input-gradient products: s for cos features (2 pi W'' = s W),
 // s / sqrt(M) for ReLU features (W'' itself).
 static float wt_scale(const Shape &sh) {
   return sh.kernel == 1 ? sh.s / sqrtf((float)sh.M) : sh.s;
 }
 
-// Rows per persistent bidirectional tile: 4 waves x kBwdTbw blocks of 16 (one
+// Rows per persistent bidirectional tile: 8 waves x kBwdTbw blocks of 16 (one
 // block per call of the row functions).
 constexpr int kBwdTbw = 2;
 constexpr int kBwdMaxWorkgroups = 256;
@@ -1021,18 +1109,20 @@ static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, h
     constexpr bool RN = decltype(rn)::value;
     if (causal) {
       dim3 grid(a.nseg * sh.BH);
-      FAVOR_BWD_DISPATCH_M(T, sh.M,
-          hipLaunchKernelGGL((k_bwd_dq_scan<T, MM, KN, RN>), grid, dim3(kBwdThreads), 0, st,
+      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(true), sh.M,
+          hipLaunchKernelGGL((k_bwd_dq_scan<T, MM, KN, RN>), grid, dim3(kScanThreads), 0, st,
                              (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
                              (const T *)a.out, a.rsave, (const typename Mma<T>::frag *)a.wfr,
                              a.bq, a.W, a.state, (T *)a.dQ, a.aux, sh.H, sh.L, a.seg_len, a.nseg,
                              sh.s, sh.keps, wts));
     } else {
-      const int ntiles = (sh.L + 64 * kBwdTbw - 1) / (64 * kBwdTbw);
+      const int rows = kBwdBidirThreads / 4 * kBwdTbw;
+      const int ntiles = (sh.L + rows - 1) / rows;
       const int nitems = ntiles * sh.BH;
       dim3 grid(min(nitems, kBwdMaxWorkgroups));
-      FAVOR_BWD_DISPATCH_M(T, sh.M,
-          hipLaunchKernelGGL((k_bwd_dq<T, MM, KN, RN, kBwdTbw>), grid, dim3(kBwdThreads), 0, st,
+      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(false), sh.M,
+          hipLaunchKernelGGL((k_bwd_dq<T, MM, KN, RN, kBwdTbw>), grid, dim3(kBwdBidirThreads), 0,
+                             st,
                              (const T *)a.Q, (const T *)a.dout, (const T *)a.out, a.rsave,
                              (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
                              (T *)a.dQ, a.aux, sh.H, sh.L, sh.s, sh.keps, wts, ntiles, nitems));
@@ -1054,24 +1144,25 @@ static hipError_t bwd_dkv_typed(const Shape &sh, bool causal, const BwdArgs &a, 
     constexpr int KN = decltype(kn)::value;
     if (causal) {
       dim3 grid(a.nseg * sh.BH);
-      FAVOR_BWD_DISPATCH_M(T, sh.M, {
-        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, false>), grid, dim3(kBwdThreads), 0, st,
+      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(true), sh.M, {
+        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, false>), grid, dim3(kScanThreads), 0, st,
                            (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
                            a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
                            (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.keps,
                            wts);
-        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, true>), grid, dim3(kBwdThreads), 0, st,
+        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, true>), grid, dim3(kScanThreads), 0, st,
                            (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
                            a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
                            (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.keps,
                            wts);
       });
     } else {
-      const int ntiles = (sh.L + 64 * kBwdTbw - 1) / (64 * kBwdTbw);
+      const int rows = kBwdBidirThreads / 4 * kBwdTbw;
+      const int ntiles = (sh.L + rows - 1) / rows;
       const int nitems = ntiles * sh.BH;
       dim3 grid(min(nitems, kBwdMaxWorkgroups));
-      FAVOR_BWD_DISPATCH_M(T, sh.M,
-          hipLaunchKernelGGL((k_bwd_dkv<T, MM, KN, kBwdTbw>), grid, dim3(kBwdThreads), 0, st,
+      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(false), sh.M,
+          hipLaunchKernelGGL((k_bwd_dkv<T, MM, KN, kBwdTbw>), grid, dim3(kBwdBidirThreads), 0, st,
                              (const T *)a.K, (const T *)a.V, (const typename Mma<T>::frag *)a.wfr,
                              a.bq, a.W, a.state, (T *)a.dK, (T *)a.dV, sh.H, sh.L, sh.s, sh.keps,
                              wts, ntiles, nitems));

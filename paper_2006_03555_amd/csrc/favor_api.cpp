@@ -86,6 +86,9 @@ favor_status validate(const favor_desc *g, int op) {
       return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass needs out_dtype == in_dtype");
     if (g->in_dtype == FAVOR_F32 && g->M > 128)
       return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass with fp32 inputs supports M <= 128");
+    if (op == kOpCausalBackward && g->in_dtype == FAVOR_F32 && g->M > 64)
+      return fail(FAVOR_ERR_UNSUPPORTED,
+                  "the causal backward pass with fp32 inputs supports M <= 64");
   }
   return FAVOR_OK;
 }

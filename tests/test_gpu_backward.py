@@ -102,15 +102,16 @@ def test_bidir_backward_parity(B, H, L, M, dtype, kernel, renorm, eps):
 
 CAUSAL_CASES = [
     # B, H, L, M, dtype, kernel, renormalize, denom_eps, with states
-    (1, 2, 300, 128, "f32", SOFTMAX, True, 0.0, False),
+    (1, 2, 300, 64, "f32", SOFTMAX, True, 0.0, False),
     (2, 2, 1000, 256, "bf16", SOFTMAX, True, 0.0, False),
     (1, 3, 65, 64, "bf16", SOFTMAX, True, 0.0, True),
     (1, 1, 1, 64, "f32", SOFTMAX, True, 0.0, False),
     (1, 2, 300, 128, "bf16", SOFTMAX, True, 0.5, False),
     (1, 1, 190, 64, "f32", SOFTMAX, False, 0.0, True),
     (1, 2, 500, 256, "bf16", SOFTMAX, False, 0.0, False),
-    (1, 2, 257, 128, "f32", RELU, True, 0.0, True),
+    (1, 2, 257, 64, "f32", RELU, True, 0.0, True),
     (2, 2, 777, 256, "bf16", RELU, True, 0.0, True),
+    (1, 2, 1500, 128, "bf16", SOFTMAX, True, 0.0, True),
     (1, 2, 400, 128, "bf16", RELU, False, 0.0, False),
 ]
 
