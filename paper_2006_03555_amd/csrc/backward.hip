@@ -486,14 +486,25 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
   __syncthreads();
 
   for (int t0 = r0; t0 < r1; t0 += 64) {
-    // the chunk's keys and values (all four blocks in every wave), D~ per key
+    // every global load of the chunk first: the keys and values (all four blocks
+    // in every wave) and this row block's queries, output gradient and output
     frag ka[4][2], va[4][2];
-    float Dk[4];
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) {
       const int t = t0 + 16 * tb + c16;
       load_rows64<T>(ka[tb], Kh, t, r1);
       load_rows64<T>(va[tb], Vh, t, r1);
+    }
+    const int i = t0 + 16 * qb + c16;
+    frag qf[2], df[2];
+    load_rows64<T>(qf, Qh, i, r1);
+    load_rows64<T>(df, dOh, i, r1);
+    float alpha, ud;
+    row_weights<T, KN, RN>(qf, df, Oh, rsave + (size_t)bh * L, i, r1, cM, s2half, alpha, ud);
+    float Dk[4];   // D~ per key
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      const int t = t0 + 16 * tb + c16;
       float D = 1.f;
       if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(ka[tb]));
       Dk[tb] = t < r1 ? D : 0.f;
@@ -549,12 +560,6 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
     }
 
     // queries of row block qb, feature steps [s0, s1)
-    const int i = t0 + 16 * qb + c16;
-    frag qf[2], df[2];
-    load_rows64<T>(qf, Qh, i, r1);
-    load_rows64<T>(df, dOh, i, r1);
-    float alpha, ud;
-    row_weights<T, KN, RN>(qf, df, Oh, rsave + (size_t)bh * L, i, r1, cM, s2half, alpha, ud);
     // P2[j][i] = D~_j (v_j . dout_i + u_d,i) for keys j <= i (B operand, k = keys)
     frag pb2[2];
     {
@@ -873,6 +878,11 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
   const int nch = (r1 - r0 + 63) / 64;
   for (int c = nch - 1; c >= 0; --c) {
     const int t0 = r0 + 64 * c;
+    // this row block's keys and values, loaded with the chunk's other rows
+    const int j = t0 + 16 * qb + c16;
+    frag kf[2], vf[2];
+    load_rows64<T>(kf, Kh, j, r1);
+    load_rows64<T>(vf, Vh, j, r1);
     // the chunk's queries: features (row m) of the state waves' blocks, u~^T of
     // row block qb; (alpha, alpha u_d) of every row
     frag qa[4][2];
@@ -974,10 +984,6 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     }
 
     // keys of row block qb, feature steps [s0, s1)
-    const int j = t0 + 16 * qb + c16;
-    frag kf[2], vf[2];
-    load_rows64<T>(kf, Kh, j, r1);
-    load_rows64<T>(vf, Vh, j, r1);
     // P3[i][j] = alpha_i (dout_i . v_j + u_d,i) for queries i >= j (B operand, k = queries)
     frag pb3[2];
     if constexpr (KPART) {
