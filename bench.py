@@ -156,8 +156,10 @@ def main():
     ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
-                    help="skip the ReLU and unnormalised variants (profiler runs that "
-                         "average counters over every launch of a kernel)")
+                    help="skip the ReLU, unnormalised and backward variants (profiler runs "
+                         "that average counters over every launch of a kernel)")
+    ap.add_argument("--variants", default="relu,softmax_no_renormalize,backward",
+                    help="comma-separated variants to time after the headline step")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of the workload, time a plain device-to-device copy of this "
                          "many bytes (reference for HBM bandwidth and for scaling the "
@@ -289,9 +291,11 @@ def main():
     # the same step with generalized attention (ReLU features) and without the
     # renormalisation: same draw, same launches, other feature epilogue / finalisation
     variants = {}
-    for name, opts in () if args.no_variants else (
-            ("relu", dict(kernel=fv.KERNEL_RELU)),
-            ("softmax_no_renormalize", dict(renormalize=False))):
+    chosen = set() if args.no_variants else set(args.variants.split(","))
+    for name, opts in (("relu", dict(kernel=fv.KERNEL_RELU)),
+                       ("softmax_no_renormalize", dict(renormalize=False))):
+        if name not in chosen:
+            continue
         step_v = lambda i, o=opts: step_serial(i, o)
         for i in range(args.warmup):
             step_v(first + i)
@@ -309,7 +313,7 @@ def main():
     # the backward pass of the step's attention: gradients with respect to Q, K, V of
     # each direction the step computes, for a fixed synthetic upstream gradient (each
     # call recomputes its forward quantities); the draw stays in the step
-    if not args.no_variants:
+    if "backward" in chosen:
         rng = np.random.default_rng(7)
         dO = torch.from_numpy(rng.standard_normal(Q.shape, dtype=np.float32)).to(
             device=dev, dtype=tdt).contiguous()
