@@ -1,0 +1,125 @@
+"""Approximation error of FAVOR against exact softmax attention, on the GPU path
+(Sec. 4.2, Fig. "approx": attention-matrix and output error against the number of
+random features M, orthogonal against i.i.d. features; L = 4096, d = 16).
+
+The kernels take d = 64; d = 16 is run exactly by zero-padding: Q, K, V get 48
+zero columns and the random-feature rows (drawn in 16 dimensions, R-ORF blocks of
+16 x 16 or i.i.d. Gaussian) 48 zero columns, so every projection, norm and feature
+is the d = 16 one. input_scale = 16^-1/4 gives the paper's exp(Q K^T / sqrt d).
+The attention matrix D-hat^-1 A-hat, which the path never stores, is read 64
+columns at a time by passing one-hot value blocks (out = D-hat^-1 A-hat V).
+Inputs (the paper does not give them): Q, K entries i.i.d. N(0, 1/4), so that the
+scaled rows have ||x~||^2 = 1 on average, V entries N(0, 1) (seeded). Errors are
+mean squared errors against the exact softmax attention of the oracle (fp64),
+mean and standard deviation over feature samples.
+
+Checks: the GPU attention matrix equals the oracle's explicit estimator on the
+same features (fp32 tolerance); the errors fall as M grows; orthogonal features
+give lower error than i.i.d. ones (the paper's finding), on average over M.
+"""
+import os
+
+import numpy as np
+import pytest
+
+from helpers import to_dev, to_host
+from oracle import favor
+
+pytestmark = pytest.mark.gpu
+
+L, D, DP = 4096, 16, 64
+S = D ** -0.25
+MS = (64, 128, 256)
+SAMPLES = int(os.environ.get("FAVOR_APPROX_SAMPLES", "3"))
+
+
+def _pad(x):
+    out = np.zeros(x.shape[:-1] + (DP,), dtype=np.float32)
+    out[..., :x.shape[-1]] = x
+    return out
+
+
+def _inputs():
+    rng = np.random.default_rng(2024)
+    Q, K, V = (rng.standard_normal((1, 1, L, D)) for _ in range(3))
+    return 0.5 * Q, 0.5 * K, V
+
+
+def _gpu_attention(fv, Qd, Kd, Wd, bd):
+    """D-hat^-1 A-hat [L, L] from the GPU, 64 columns per call."""
+    import torch
+    A = torch.empty((L, L), dtype=torch.float32, device="cuda")
+    eye = torch.zeros((1, 1, L, DP), dtype=torch.float32, device="cuda")
+    idx = torch.arange(DP, device="cuda")
+    out = torch.empty_like(eye)
+    for c in range(0, L, DP):
+        eye.zero_()
+        eye[0, 0, c + idx, idx] = 1.0
+        fv.attn_bidir(Qd, Kd, eye, Wd, bd, S, out=out)
+        A[:, c:c + DP] = out[0, 0]
+    return A
+
+
+def _errors(kind, M, sample, Q, K, V, A_exact, out_exact):
+    import torch
+    fv = __import__("paper_2006_03555_amd")
+    W, b = favor.orf_draw(500 + 10 * sample + M, 1, M, D, kind)
+    Wd, bd = to_dev(_pad(W.astype(np.float32))), to_dev(b.astype(np.float32))
+    Qd, Kd, Vd = (to_dev(_pad(x.astype(np.float32))) for x in (Q, K, V))
+    out = fv.attn_bidir(Qd, Kd, Vd, Wd, bd, S)
+    A = _gpu_attention(fv, Qd, Kd, Wd, bd)
+    torch.cuda.synchronize()
+    out = to_host(out)[0, 0, :, :D]
+    A = A.double().cpu().numpy()
+    return (float(np.mean((A - A_exact) ** 2)), float(np.mean((out - out_exact) ** 2)), A, W, b)
+
+
+@pytest.fixture(scope="module")
+def exact():
+    Q, K, V = _inputs()
+    Qs, Ks = S * Q[0, 0], S * K[0, 0]
+    logits = Qs @ Ks.T
+    logits -= logits.max(axis=-1, keepdims=True)
+    A = np.exp(logits)
+    A /= A.sum(axis=-1, keepdims=True)
+    out = favor.softmax_attn(Q, K, V, S, causal=False)[0, 0]
+    np.testing.assert_allclose(A @ V[0, 0], out, atol=1e-12)
+    return Q, K, V, A, out
+
+
+def test_gpu_attention_matrix_equals_the_explicit_estimator(exact):
+    Q, K, V, A_exact, out_exact = exact
+    _, _, A, W, b = _errors(favor.RF_ORTHO_CHI, 128, 0, Q, K, V, A_exact, out_exact)
+    Qp = favor.feature_map(Q[0, 0], W, b, S)
+    Kp = favor.feature_map(K[0, 0], W, b, S)
+    Ahat = Qp @ Kp.T
+    ref = Ahat / Ahat.sum(axis=-1, keepdims=True)
+    # E_cond with one-hot values: sigma_ij = (|Q'_i| |K'_j| + |ref_ij| sum_k |Q'_i| |K'_k|)
+    # / |D-hat_i|, the first-order error scale of the ratio (as for every output)
+    S1 = np.abs(Qp) @ np.abs(Kp).T
+    sigma = (S1 + np.abs(ref) * S1.sum(axis=-1, keepdims=True)) / np.abs(
+        Ahat.sum(axis=-1, keepdims=True))
+    err = np.max(np.abs(A - ref) / sigma)
+    assert err <= 1e-4, err
+
+
+def test_error_falls_with_m_and_orthogonal_features_beat_iid(exact):
+    Q, K, V, A_exact, out_exact = exact
+    res = {}
+    for kind in (favor.RF_ORTHO_CHI, favor.RF_IID):
+        for M in MS:
+            e = np.array([_errors(kind, M, s, Q, K, V, A_exact, out_exact)[:2]
+                          for s in range(SAMPLES)])
+            res[(kind, M)] = (e.mean(axis=0), e.std(axis=0))
+    print("\nM, kind, attention-matrix MSE (mean, sd), output MSE (mean, sd) over "
+          f"{SAMPLES} samples")
+    for (kind, M), (mu, sd) in sorted(res.items(), key=lambda t: (t[0][1], t[0][0])):
+        name = "ORF" if kind == favor.RF_ORTHO_CHI else "iid"
+        print(f"{M:4d} {name}  {mu[0]:.3e} {sd[0]:.1e}   {mu[1]:.3e} {sd[1]:.1e}")
+    for kind in (favor.RF_ORTHO_CHI, favor.RF_IID):
+        for q in (0, 1):
+            assert res[(kind, MS[-1])][0][q] < res[(kind, MS[0])][0][q]
+    for q in (0, 1):
+        orf = np.mean([res[(favor.RF_ORTHO_CHI, M)][0][q] for M in MS])
+        iid = np.mean([res[(favor.RF_IID, M)][0][q] for M in MS])
+        assert orf < iid, (q, orf, iid)
