@@ -32,6 +32,8 @@ from . import philox
 RF_ORTHO_CHI = 0     # R-ORF blocks, rows scaled by independent chi_d norms
 RF_ORTHO_FIXED = 1   # R-ORF blocks, rows scaled to sqrt(d)
 RF_IID = 2           # unstructured Gaussian rows
+RF_HADAMARD = 3      # H-ORF blocks sqrt(d) H D3 H D2 H D1 (Sec. 2.4)
+RF_GIVENS = 4        # G-ORF blocks sqrt(d) G_1 ... G_K, K = 2 d log2 d rotations (Sec. 2.4)
 
 KERNEL_SOFTMAX = 0   # Gaussian-kernel features (cos), softmax attention
 KERNEL_RELU = 1      # generalized attention with f = ReLU
@@ -55,6 +57,69 @@ def gram_schmidt_rows(G):
     return Qr
 
 
+def hadamard(d):
+    """Normalised Sylvester-Hadamard matrix: H[i][j] = (-1)^popcount(i & j) / sqrt(d)."""
+    i = np.arange(d)
+    bits = np.bitwise_and.outer(i, i)
+    par = np.zeros_like(bits)
+    while np.any(bits):
+        par ^= bits & 1
+        bits >>= 1
+    return (1.0 - 2.0 * par) / np.sqrt(d)
+
+
+def hadamard_signs(seed, head, blk, d):
+    """The three Rademacher diagonals of block blk: element (3 blk + t) d + c of
+    stream SIGNS is +1 when its 32-bit word is below 2^31, else -1. Shape [3, d]."""
+    n = (3 * blk + 3) * d
+    w = philox.words32(seed, head, philox.PURPOSE_SIGNS, n)[3 * blk * d:].reshape(3, d)
+    return np.where(w < np.uint64(1 << 31), 1.0, -1.0)
+
+
+def hadamard_block(seed, head, blk, d):
+    """H-ORF block (Sec. 2.4 (2); the random Hadamard construction it cites):
+    sqrt(d) H D3 H D2 H D1 with Rademacher diagonals D_t. Orthogonal rows of norm sqrt(d)."""
+    H = hadamard(d)
+    D = hadamard_signs(seed, head, blk, d)
+    return np.sqrt(d) * (H * D[2]) @ (H * D[1]) @ (H * D[0])
+
+
+def givens_params(seed, head, blk, d, K):
+    """Rotation t of block blk from call blk K + t of stream GIVENS (words x0, x1, x2):
+    i = floor(x0 d / 2^32), j' = floor(x1 (d - 1) / 2^32), j = j' + [j' >= i],
+    theta = 2 pi (x2 + 0.5) 2^-32."""
+    n = (blk * K + K) * 8
+    w = philox.words32(seed, head, philox.PURPOSE_GIVENS, n)[blk * K * 8:].reshape(K, 8)
+    i = (w[:, 0] * np.uint64(d)) >> np.uint64(32)
+    jp = (w[:, 1] * np.uint64(d - 1)) >> np.uint64(32)
+    j = jp + (jp >= i)
+    theta = 2.0 * np.pi * (w[:, 2].astype(np.float64) + 0.5) * 2.0 ** -32
+    return i.astype(np.int64), j.astype(np.int64), theta
+
+
+def givens_count(d):
+    """Rotations per G-ORF block: 2 d log2 d."""
+    return 2 * d * int(round(np.log2(d)))
+
+
+def givens_block(seed, head, blk, d, K=None):
+    """G-ORF block (Sec. 2.4 (2); Kac's random walk of the Givens construction it
+    cites): sqrt(d) G_1 G_2 ... G_K, G_t the rotation by theta_t in the (i_t, j_t)
+    plane (G[i][i] = G[j][j] = cos, G[i][j] = -sin, G[j][i] = sin); K = 2 d log2 d
+    rotations, O(M log d) numbers for M rows as the paper counts (d log2 d leaves the
+    entries visibly non-Gaussian, fourth moment ~5.5; twice that mixes them, ~3.0)."""
+    if K is None:
+        K = givens_count(d)
+    i, j, theta = givens_params(seed, head, blk, d, K)
+    B = np.eye(d)
+    for t in range(K):
+        c, s = np.cos(theta[t]), np.sin(theta[t])
+        bi, bj = B[:, i[t]].copy(), B[:, j[t]].copy()
+        B[:, i[t]] = c * bi + s * bj       # row vector v <- v G_t
+        B[:, j[t]] = -s * bi + c * bj
+    return np.sqrt(d) * B
+
+
 def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI):
     """Random-feature matrix W [H, M, d] and phases b [H, M] (Secs. 2.3-2.4).
 
@@ -65,6 +130,8 @@ def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI):
     m d .. m d + d - 1). The blocks are stacked and the first M rows kept.
     b_m = 2 pi u_m with u_m uniform (purpose PHASE, element m).
     FIXED kind uses rho = sqrt(d); IID kind keeps the raw Gaussian rows.
+    HADAMARD and GIVENS kinds use the structured orthogonal blocks (rows of norm
+    sqrt(d)) in place of the Gram-Schmidt ones.
     """
     nblk = -(-M // d)
     W = np.zeros((n_heads, M, d), dtype=np.float64)
@@ -75,6 +142,10 @@ def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI):
         for k in range(nblk):
             if kind == RF_IID:
                 rows.append(g[k])
+            elif kind == RF_HADAMARD:
+                rows.append(hadamard_block(seed, h, k, d))
+            elif kind == RF_GIVENS:
+                rows.append(givens_block(seed, h, k, d))
             else:
                 rows.append(gram_schmidt_rows(g[k]))
         Wh = np.concatenate(rows, axis=0)[:M]

@@ -14,7 +14,9 @@ Stream definition (shared contract with the library, restated in its header):
   key      = (seed, 0)
   counter  = (index, head, purpose, 0)      purpose: 0 ORF Gaussian blocks,
                                                      1 chi row-norm Gaussians,
-                                                     2 phases b
+                                                     2 phases b,
+                                                     3 Hadamard-block signs,
+                                                     4 Givens rotations
   one call -> four 64-bit words w0..w3 -> eight 32-bit words
               x[2j] = low half of wj, x[2j+1] = high half of wj
   element n of a stream is word n % 8 of the call with index n // 8.
@@ -34,6 +36,8 @@ _ROUNDS = 10
 PURPOSE_ORF = 0
 PURPOSE_CHI = 1
 PURPOSE_PHASE = 2
+PURPOSE_SIGNS = 3       # Rademacher diagonals of Hadamard ORF blocks
+PURPOSE_GIVENS = 4      # coordinate pairs and angles of Givens ORF blocks
 
 _LO32 = np.uint64(0xFFFFFFFF)
 _S32 = np.uint64(32)

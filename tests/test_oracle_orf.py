@@ -90,3 +90,88 @@ def test_head_h_uses_its_own_stream():
     q0 = favor.gram_schmidt_rows(g[0])
     rho = np.linalg.norm(W_all[2, :16], axis=1)
     assert np.allclose(W_all[2, :16] / rho[:, None], q0, atol=1e-12)
+
+
+# ---------------------------------------------------------------- structured ORFs
+def test_hadamard_matrix_matches_scipy_sylvester_construction():
+    import scipy.linalg
+    for d in (2, 16, 64):
+        np.testing.assert_array_equal(favor.hadamard(d) * np.sqrt(d), scipy.linalg.hadamard(d))
+
+
+def test_hadamard_orf_block_is_the_hd_product_and_orthogonal():
+    import scipy.linalg
+    d = 64
+    for blk in (0, 3):
+        W = favor.hadamard_block(11, 2, blk, d)
+        np.testing.assert_allclose(W @ W.T, d * np.eye(d), atol=1e-10)
+        H = scipy.linalg.hadamard(d) / np.sqrt(d)
+        D = favor.hadamard_signs(11, 2, blk, d)
+        ref = np.sqrt(d) * H @ np.diag(D[2]) @ H @ np.diag(D[1]) @ H @ np.diag(D[0])
+        np.testing.assert_allclose(W, ref, atol=1e-12)
+
+
+def test_hadamard_signs_are_fair_and_block_local():
+    D = np.concatenate([favor.hadamard_signs(5, h, blk, 64).ravel()
+                        for h in range(4) for blk in range(8)])
+    assert set(np.unique(D)) == {-1.0, 1.0}
+    n = D.size
+    assert abs(np.sum(D > 0) - n / 2) < 4 * np.sqrt(n / 4)
+    # block 1 reads the stream after block 0: no overlap
+    assert not np.array_equal(favor.hadamard_signs(5, 0, 0, 64), favor.hadamard_signs(5, 0, 1, 64))
+
+
+def test_hadamard_orf_entries_are_nearly_gaussian():
+    """Three HD factors: entries of sqrt(d) H D3 H D2 H D1 have mean 0, variance 1
+    (rows of norm sqrt(d)) and a fourth moment near the Gaussian 3."""
+    x = np.concatenate([favor.hadamard_block(7, h, 0, 64).ravel() for h in range(40)])
+    assert abs(x.mean()) < 0.02
+    np.testing.assert_allclose(np.mean(x * x), 1.0, atol=1e-12)
+    assert 2.6 < np.mean(x ** 4) < 3.1
+
+
+def test_givens_parameters_are_valid():
+    i, j, th = favor.givens_params(3, 1, 2, 64, 5000)
+    assert i.min() >= 0 and i.max() < 64 and j.min() >= 0 and j.max() < 64
+    assert np.all(i != j)
+    assert th.min() > 0 and th.max() < 2 * np.pi
+    # pairs spread over all coordinates
+    assert len(np.unique(i)) == 64 and len(np.unique(j)) == 64
+
+
+def test_givens_block_is_the_rotation_product():
+    d = 8
+    for K in (1, 2, 3):
+        W = favor.givens_block(9, 0, 1, d, K)
+        i, j, th = favor.givens_params(9, 0, 1, d, K)
+        ref = np.eye(d)
+        for t in range(K):
+            G = np.eye(d)
+            c, s = np.cos(th[t]), np.sin(th[t])
+            G[i[t], i[t]] = c
+            G[j[t], j[t]] = c
+            G[i[t], j[t]] = -s
+            G[j[t], i[t]] = s
+            ref = ref @ G
+        np.testing.assert_allclose(W, np.sqrt(d) * ref, atol=1e-13)
+
+
+def test_givens_orf_is_orthogonal_and_mixes():
+    d = 64
+    W = favor.givens_block(4, 0, 0, d)
+    np.testing.assert_allclose(W @ W.T, d * np.eye(d), atol=1e-10)
+    # 2 d log2 d rotations spread the mass: entries close to the N(0, 1) marginals
+    # of a Haar-random orthogonal matrix (d log2 d alone leaves a fourth moment ~5.5)
+    x = np.concatenate([favor.givens_block(4, h, 0, d).ravel() for h in range(30)])
+    assert abs(x.mean()) < 0.03
+    assert 2.7 < np.mean(x ** 4) < 3.3
+    assert favor.givens_count(64) == 768
+
+
+def test_orf_draw_structured_kinds_stack_blocks():
+    W, b = favor.orf_draw(21, 2, 100, 64, favor.RF_HADAMARD)
+    assert W.shape == (2, 100, 64)
+    np.testing.assert_allclose(W[1, :64], favor.hadamard_block(21, 1, 0, 64), atol=0)
+    np.testing.assert_allclose(W[1, 64:], favor.hadamard_block(21, 1, 1, 64)[:36], atol=0)
+    W, _ = favor.orf_draw(21, 1, 64, 64, favor.RF_GIVENS)
+    np.testing.assert_allclose(W[0], favor.givens_block(21, 0, 0, 64), atol=0)
