@@ -22,8 +22,9 @@ serial, with every launch bracketed by HIP events on its stream, gives the
 per-kernel durations and the roofline entry for the dominant
 kernel. The line also carries the fp64 CPU oracle timed on this host
 (cpu_baseline), and under "variants" the same step with generalized attention
-(ReLU features) and with the renormalisation off, and the backward pass of the
-step's attention, timed the same way.
+(ReLU features) and with the renormalisation off, the draw alone for every kind
+of random features, and the backward pass of the step's attention, timed the
+same way.
 """
 import argparse
 import json
@@ -158,7 +159,7 @@ def main():
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the ReLU, unnormalised and backward variants (profiler runs "
                          "that average counters over every launch of a kernel)")
-    ap.add_argument("--variants", default="relu,softmax_no_renormalize,backward",
+    ap.add_argument("--variants", default="relu,softmax_no_renormalize,draws,backward",
                     help="comma-separated variants to time after the headline step")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of the workload, time a plain device-to-device copy of this "
@@ -309,6 +310,21 @@ def main():
             "ms_per_step": ms_v, "value": w.B * w.H * w.L / (ms_v / 1e3),
             "ms_per_step_instrumented": ms_vi,
             "kernels": {k: {"ms_per_launch": v[0] / v[1]} for k, v in kv.items() if v[1] > 0}}
+
+    # the random-feature draw of the step (8 heads x M rows) for every kind of features
+    if "draws" in chosen:
+        kinds = {"ortho_chi": fv.RF_ORTHO_CHI, "ortho_fixed": fv.RF_ORTHO_FIXED,
+                 "iid": fv.RF_IID, "hadamard": fv.RF_HADAMARD, "givens": fv.RF_GIVENS}
+        draws = {}
+        for name, kind in kinds.items():
+            step_d = lambda i, k=kind: fv.orf_draw(1000 + i, H, M, w.d, kind=k, W=Wd[0], b=bd[0],
+                                                   stream=s_main)
+            for i in range(args.warmup):
+                step_d(first + i)
+            first += args.warmup
+            draws[name] = {"ms_per_draw": timed_region(step_d, first)}
+            first += args.steps
+        variants["draws"] = draws
 
     # the backward pass of the step's attention: gradients with respect to Q, K, V of
     # each direction the step computes, for a fixed synthetic upstream gradient (each

@@ -56,7 +56,9 @@ typedef enum { FAVOR_F32 = 0, FAVOR_BF16 = 1 } favor_dtype;
 typedef enum {
   FAVOR_RF_ORTHO_CHI = 0,   /* R-ORF blocks, rows scaled by independent chi_d norms (default) */
   FAVOR_RF_ORTHO_FIXED = 1, /* R-ORF blocks, every row scaled to norm sqrt(d)                  */
-  FAVOR_RF_IID = 2          /* unstructured i.i.d. N(0, I_d) rows                              */
+  FAVOR_RF_IID = 2,         /* unstructured i.i.d. N(0, I_d) rows                              */
+  FAVOR_RF_HADAMARD = 3,    /* H-ORF blocks sqrt(d) H D3 H D2 H D1 (Sec. 2.4 (2))              */
+  FAVOR_RF_GIVENS = 4       /* G-ORF blocks sqrt(d) G_1 ... G_K, K = 2 d log2 d (Sec. 2.4 (2)) */
 } favor_rf_kind;
 
 /* Feature kernel (Sec. 2.2, Eq. interesting):
@@ -94,10 +96,18 @@ typedef struct {
  * with positive triangular diagonal); row m = k d + r is scaled by rho_m (kind
  * CHI: the norm of an independent N(0, I_d) vector; FIXED: sqrt(d)); the first
  * M stacked rows are kept. IID kind keeps the raw Gaussian rows. b_m = 2 pi u_m.
+ * HADAMARD: block k = sqrt(d) H D3 H D2 H D1 with the normalised Sylvester-
+ * Hadamard matrix H[i][j] = (-1)^popcount(i & j) / sqrt(d) and diagonals D_t of
+ * signs: element (3 k + t) d + c of purpose 3 is +1 when its 32-bit word is
+ * below 2^31, else -1. GIVENS: block k = sqrt(d) G_1 ... G_K, K = 2 d log2 d;
+ * G_t rotates the (i, j) plane by theta (row vectors: v_i <- cos v_i + sin v_j,
+ * v_j <- -sin v_i + cos v_j), from words x0, x1, x2 of call k K + t of purpose 4:
+ * i = (x0 d) >> 32, j' = (x1 (d - 1)) >> 32, j = j' + [j' >= i],
+ * theta = 2 pi (x2 + 0.5) 2^-32. Both are orthogonal with rows of norm sqrt(d).
  *
  * Random numbers: Philox4x64-10 (Salmon et al., SC'11), key (seed, 0), counter
  * (i, h, purpose, 0) with purpose 0 = Gaussian blocks, 1 = chi-norm Gaussians,
- * 2 = phases. Call i yields four 64-bit words w0..w3, i.e. eight 32-bit words
+ * 2 = phases, 3 = Hadamard signs, 4 = Givens rotations. Call i yields four 64-bit words w0..w3, i.e. eight 32-bit words
  * x[2j] = low(wj), x[2j+1] = high(wj); stream element n is word n % 8 of call
  * n / 8; u = (x + 0.5) 2^-32; Gaussians by Box-Muller from uniform pairs
  * (u[2p], u[2p+1]): sqrt(-2 ln u[2p]) * (cos, sin)(2 pi u[2p+1]). Gaussian

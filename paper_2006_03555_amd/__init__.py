@@ -18,7 +18,7 @@ import ctypes
 import os
 
 from ._lib import (  # noqa: F401
-    BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, OP_BIDIR, OP_BOTH, OP_CAUSAL, OP_FEATURE_MAP,
+    BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, RF_HADAMARD, RF_GIVENS, OP_BIDIR, OP_BOTH, OP_CAUSAL, OP_FEATURE_MAP,
     OP_BIDIR_BACKWARD, OP_CAUSAL_BACKWARD, KERNEL_RELU, KERNEL_SOFTMAX, backward_workspace_size,
     FavorDesc, FavorError, FavorLibraryMissing, lib, lib_path, make_desc, status_string,
     validate_desc, workspace_size, last_error, timing_enable, timing_reset, timing_read,

@@ -7,6 +7,8 @@ BF16 = 1
 RF_ORTHO_CHI = 0
 RF_ORTHO_FIXED = 1
 RF_IID = 2
+RF_HADAMARD = 3
+RF_GIVENS = 4
 OP_FEATURE_MAP = 0
 OP_BIDIR = 1
 OP_CAUSAL = 2

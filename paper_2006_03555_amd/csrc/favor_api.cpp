@@ -251,7 +251,8 @@ favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d
                             favor_rf_kind kind, float *W, float *b, void *stream) {
   if (n_heads < 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "n_heads=%d is negative", n_heads);
   if (M <= 0 || d <= 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "M=%d d=%d must be positive", M, d);
-  if (kind != FAVOR_RF_ORTHO_CHI && kind != FAVOR_RF_ORTHO_FIXED && kind != FAVOR_RF_IID)
+  if (kind != FAVOR_RF_ORTHO_CHI && kind != FAVOR_RF_ORTHO_FIXED && kind != FAVOR_RF_IID &&
+      kind != FAVOR_RF_HADAMARD && kind != FAVOR_RF_GIVENS)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown random-feature kind %d", (int)kind);
   if (d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", d);
   if (M > 4096) return fail(FAVOR_ERR_UNSUPPORTED, "M=%d exceeds 4096", M);

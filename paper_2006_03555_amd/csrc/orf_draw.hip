@@ -1,4 +1,5 @@
-// orf_draw.hip - orthogonal random features (Sec. 2.4, R-ORFs) drawn on the GPU.
+// orf_draw.hip - orthogonal random features (Sec. 2.4: R-ORFs, and the
+// Hadamard / Givens H/G-ORFs at the end of the file) drawn on the GPU.
 //
 // One workgroup per (d x d block, head). Random numbers come from Philox4x64-10
 // (Salmon, Moraes, Dror, Shaw, SC'11) with key (seed, 0) and counter
@@ -274,10 +275,165 @@ __global__ __launch_bounds__(512) void k_orf_draw(uint64_t seed, int M, int kind
   }
 }
 
+// ---------------------------------------------------------------------------
+// Structured orthogonal blocks (Sec. 2.4 (2)). Rows have norm sqrt(d); the
+// phases are drawn as for the other kinds.
+
+// The eight 32-bit words of call idx of stream (seed, head, purpose).
+__device__ __forceinline__ void words8(uint64_t seed, uint32_t head, uint32_t purpose,
+                                       uint64_t idx, uint32_t x[8]) {
+  uint64_t c[4] = {idx, head, purpose, 0};
+  philox4x64_10(c, seed, 0);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    x[2 * j] = (uint32_t)c[j];
+    x[2 * j + 1] = (uint32_t)(c[j] >> 32);
+  }
+}
+
+__device__ __forceinline__ void store_phases(uint64_t seed, int h, int blk, int M,
+                                             float *__restrict__ b) {
+  const int k = threadIdx.x;   // 8 threads, 8 phases each
+  float u[8];
+  uniforms8(seed, h, 2, (uint64_t)blk * (kOrfD / 8) + k, u);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int mm = blk * kOrfD + k * 8 + i;
+    if (mm < M) b[(size_t)h * M + mm] = 6.283185307179586f * u[i];
+  }
+}
+
+// Unnormalised Walsh-Hadamard transform of a 64-vector held by an aligned group
+// of eight lanes (lane p: elements 8 p .. 8 p + 7), natural (Sylvester) order.
+__device__ __forceinline__ void fwht64(double (&v)[8], int p) {
+#pragma unroll
+  for (int s = 1; s < 8; s <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if ((e & s) == 0) {
+        const double a = v[e], c = v[e + s];
+        v[e] = a + c;
+        v[e + s] = a - c;
+      }
+#pragma unroll
+  for (int m = 1; m < 8; m <<= 1) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const double o = __shfl_xor(v[e], m);
+      v[e] = (p & m) ? o - v[e] : v[e] + o;
+    }
+  }
+}
+
+// H-ORF: row r of block blk is sqrt(d) e_r^T H D3 H D2 H D1 (normalised
+// Sylvester-Hadamard H, Rademacher diagonals from stream 3: element
+// (3 blk + t) d + c is +1 when its word is below 2^31). 512 threads: eight per row.
+__global__ __launch_bounds__(512) void k_orf_hadamard(uint64_t seed, int M,
+                                                      float *__restrict__ W,
+                                                      float *__restrict__ b) {
+  constexpr int D = kOrfD;
+  const int blk = blockIdx.x;
+  const int h = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int r = tid >> 3;
+  const int p = tid & 7;
+  double sg[3][8];
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    uint32_t x[8];
+    words8(seed, h, 3, (uint64_t)(3 * blk + t) * (D / 8) + p, x);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sg[t][e] = x[e] < 0x80000000u ? 1.0 : -1.0;
+  }
+  double v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {   // (row r of H) o d3, H[r][c] = (-1)^popcount(r & c) / 8
+    const int c = 8 * p + e;
+    v[e] = ((__popc(r & c) & 1) ? -0.125 : 0.125) * sg[2][e];
+  }
+  fwht64(v, p);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] *= 0.125 * sg[1][e];
+  fwht64(v, p);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] *= 0.125 * sg[0][e] * 8.0;   // times sqrt(d)
+  const int m = blk * D + r;
+  if (m < M) {
+    float4 *dst = (float4 *)(W + ((size_t)h * M + m) * D + 8 * p);
+    dst[0] = make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+    dst[1] = make_float4((float)v[4], (float)v[5], (float)v[6], (float)v[7]);
+  }
+  if (tid < D / 8) store_phases(seed, h, blk, M, b);
+}
+
+// G-ORF: block blk is sqrt(d) G_1 ... G_K, K = 2 d log2 d rotations; rotation t
+// comes from call blk K + t of stream 4 (words x0, x1, x2): i = (x0 d) >> 32,
+// j' = (x1 (d - 1)) >> 32, j = j' + [j' >= i], theta = 2 pi (x2 + 0.5) 2^-32, and
+// acts on row vectors as v_i <- c v_i + s v_j, v_j <- -s v_i + c v_j. The
+// parameters go to LDS first (all threads); then thread r rotates row r of the
+// identity through the K rotations in order, in fp64 in LDS.
+constexpr int kGivensK = 2 * kOrfD * 6;
+__global__ __launch_bounds__(256) void k_orf_givens(uint64_t seed, int M, float *__restrict__ W,
+                                                    float *__restrict__ b) {
+  constexpr int D = kOrfD;
+  constexpr int K = kGivensK;
+  __shared__ double cs[K][2];
+  __shared__ unsigned char pi[K], pj[K];
+  __shared__ double rows[D][D + 1];
+  const int blk = blockIdx.x;
+  const int h = blockIdx.y;
+  const int tid = threadIdx.x;
+  for (int t = tid; t < K; t += blockDim.x) {
+    uint32_t x[8];
+    words8(seed, h, 4, (uint64_t)blk * K + t, x);
+    const int i = (int)(((uint64_t)x[0] * D) >> 32);
+    const int jp = (int)(((uint64_t)x[1] * (D - 1)) >> 32);
+    const double th = 6.283185307179586 * (((double)x[2] + 0.5) * 0x1p-32);
+    double sn, cn;
+    sincos(th, &sn, &cn);
+    pi[t] = (unsigned char)i;
+    pj[t] = (unsigned char)(jp + (jp >= i ? 1 : 0));
+    cs[t][0] = cn;
+    cs[t][1] = sn;
+  }
+  for (int e = tid; e < D * D; e += blockDim.x) rows[e / D][e % D] = (e / D == e % D) ? 1.0 : 0.0;
+  __syncthreads();
+  if (tid < D) {
+    double *v = rows[tid];
+    for (int t = 0; t < K; ++t) {
+      const int i = pi[t], j = pj[t];
+      const double c = cs[t][0], s = cs[t][1];
+      const double vi = v[i], vj = v[j];
+      v[i] = fma(c, vi, s * vj);
+      v[j] = fma(-s, vi, c * vj);
+    }
+  }
+  __syncthreads();
+  // rows * sqrt(d) -> W, 16-byte stores (thread = (row, eighth))
+  for (int e = tid; e < D * 8; e += blockDim.x) {
+    const int r = e >> 3, q = e & 7;
+    const int m = blk * D + r;
+    if (m < M) {
+      const double *v = &rows[r][8 * q];
+      float4 *dst = (float4 *)(W + ((size_t)h * M + m) * D + 8 * q);
+      dst[0] = make_float4((float)(8.0 * v[0]), (float)(8.0 * v[1]), (float)(8.0 * v[2]),
+                           (float)(8.0 * v[3]));
+      dst[1] = make_float4((float)(8.0 * v[4]), (float)(8.0 * v[5]), (float)(8.0 * v[6]),
+                           (float)(8.0 * v[7]));
+    }
+  }
+  if (tid < D / 8) store_phases(seed, h, blk, M, b);
+}
+
 hipError_t launch_orf_draw(uint64_t seed, int n_heads, int M, int kind, float *W, float *b,
                            hipStream_t st) {
   dim3 grid((M + kOrfD - 1) / kOrfD, n_heads);
-  hipLaunchKernelGGL(k_orf_draw, grid, dim3(512), 0, st, seed, M, kind, W, b);
+  if (kind == 3)
+    hipLaunchKernelGGL(k_orf_hadamard, grid, dim3(512), 0, st, seed, M, W, b);
+  else if (kind == 4)
+    hipLaunchKernelGGL(k_orf_givens, grid, dim3(256), 0, st, seed, M, W, b);
+  else
+    hipLaunchKernelGGL(k_orf_draw, grid, dim3(512), 0, st, seed, M, kind, W, b);
   return hipGetLastError();
 }
 

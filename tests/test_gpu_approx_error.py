@@ -15,7 +15,8 @@ mean and standard deviation over feature samples.
 
 Checks: the GPU attention matrix equals the oracle's explicit estimator on the
 same features (fp32 tolerance); the errors fall as M grows; orthogonal features
-give lower error than i.i.d. ones (the paper's finding), on average over M.
+give lower error than i.i.d. ones (the paper's finding), on average over M. The
+Hadamard and Givens features (Sec. 2.4 (2)) are measured beside them.
 """
 import os
 
@@ -106,15 +107,17 @@ def test_gpu_attention_matrix_equals_the_explicit_estimator(exact):
 def test_error_falls_with_m_and_orthogonal_features_beat_iid(exact):
     Q, K, V, A_exact, out_exact = exact
     res = {}
-    for kind in (favor.RF_ORTHO_CHI, favor.RF_IID):
+    for kind in (favor.RF_ORTHO_CHI, favor.RF_IID, favor.RF_HADAMARD, favor.RF_GIVENS):
         for M in MS:
             e = np.array([_errors(kind, M, s, Q, K, V, A_exact, out_exact)[:2]
                           for s in range(SAMPLES)])
             res[(kind, M)] = (e.mean(axis=0), e.std(axis=0))
     print("\nM, kind, attention-matrix MSE (mean, sd), output MSE (mean, sd) over "
           f"{SAMPLES} samples")
+    names = {favor.RF_ORTHO_CHI: "ORF", favor.RF_IID: "iid", favor.RF_HADAMARD: "H-ORF",
+             favor.RF_GIVENS: "G-ORF"}
     for (kind, M), (mu, sd) in sorted(res.items(), key=lambda t: (t[0][1], t[0][0])):
-        name = "ORF" if kind == favor.RF_ORTHO_CHI else "iid"
+        name = names[kind]
         print(f"{M:4d} {name}  {mu[0]:.3e} {sd[0]:.1e}   {mu[1]:.3e} {sd[1]:.1e}")
     for kind in (favor.RF_ORTHO_CHI, favor.RF_IID):
         for q in (0, 1):

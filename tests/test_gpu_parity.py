@@ -32,7 +32,8 @@ def _qkv(B, H, L, dtype, seed):
 
 
 # ---------------------------------------------------------------- ORF draw
-@pytest.mark.parametrize("kind", [favor.RF_ORTHO_CHI, favor.RF_ORTHO_FIXED, favor.RF_IID])
+@pytest.mark.parametrize("kind", [favor.RF_ORTHO_CHI, favor.RF_ORTHO_FIXED, favor.RF_IID,
+                                  favor.RF_HADAMARD, favor.RF_GIVENS])
 @pytest.mark.parametrize("M,H", [(256, 8), (128, 1), (64, 3), (100, 2)])
 def test_orf_draw_matches_oracle(kind, M, H):
     import torch
