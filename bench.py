@@ -23,7 +23,8 @@ per-kernel durations and the roofline entry for the dominant
 kernel. The line also carries the fp64 CPU oracle timed on this host
 (cpu_baseline), and under "variants" the same step with generalized attention
 (ReLU features) and with the renormalisation off, the draw alone for every kind
-of random features, and the backward pass of the step's attention, timed the
+of random features, the backward pass of the step's attention, and the training
+step (forward saving the row scales, then the backward reading them), timed the
 same way.
 """
 import argparse
@@ -159,7 +160,8 @@ def main():
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the ReLU, unnormalised and backward variants (profiler runs "
                          "that average counters over every launch of a kernel)")
-    ap.add_argument("--variants", default="relu,softmax_no_renormalize,draws,backward",
+    ap.add_argument("--variants",
+                    default="relu,softmax_no_renormalize,draws,backward,train_step",
                     help="comma-separated variants to time after the headline step")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of the workload, time a plain device-to-device copy of this "
@@ -327,9 +329,12 @@ def main():
         variants["draws"] = draws
 
     # the backward pass of the step's attention: gradients with respect to Q, K, V of
-    # each direction the step computes, for a fixed synthetic upstream gradient (each
-    # call recomputes its forward quantities); the draw stays in the step
-    if "backward" in chosen:
+    # each direction the step computes, for a fixed synthetic upstream gradient; the
+    # draw stays in the step. "backward": the gradient calls alone, each recomputing
+    # its forward quantities. "train_step": the forward pass saving each row's
+    # 1 / (D-hat + eps), then the gradient calls reading the saved outputs and scales.
+    directions = {0: "bidirectional", 1: "causal", 2: "bidirectional and causal"}[op]
+    if chosen & {"backward", "train_step"}:
         rng = np.random.default_rng(7)
         dO = torch.from_numpy(rng.standard_normal(Q.shape, dtype=np.float32)).to(
             device=dev, dtype=tdt).contiguous()
@@ -337,33 +342,61 @@ def main():
         nbw = max(fv.backward_workspace_size(g, False) if op != 1 else 0,
                   fv.backward_workspace_size(g, True) if op != 0 else 0)
         wsb = torch.empty(nbw, dtype=torch.uint8, device=dev)
+        rs_b = torch.empty((w.B, H, w.L), dtype=torch.float32, device=dev)
+        rs_c = torch.empty_like(rs_b)
 
-        def step_bwd(i):
-            fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
+        def gradients(saved):
             gq, gk, gv = grads
             if op != 1:
                 fv.attn_bidir_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dQ=gq, dK=gk, dV=gv,
-                                       workspace=wsb, stream=s_main)
+                                       workspace=wsb, stream=s_main,
+                                       out=out_b if saved else None,
+                                       row_scale=rs_b if saved else None)
             if op != 0:
                 fv.attn_causal_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dQ=gq, dK=gk, dV=gv,
-                                        workspace=wsb, stream=s_main)
+                                        workspace=wsb, stream=s_main,
+                                        out=out_c if saved else None,
+                                        row_scale=rs_c if saved else None)
 
-        for i in range(args.warmup):
-            step_bwd(first + i)
-        first += args.warmup
-        ms_b = timed_region(step_bwd, first)
-        first += args.steps
-        ms_bi = timed_region(step_bwd, first, instrumented=True)
-        first += args.steps
-        kb = fv.timing_read()
-        variants["backward"] = {
-            "ms_per_step": ms_b, "value": w.B * w.H * w.L / (ms_b / 1e3),
-            "ms_per_step_instrumented": ms_bi,
-            "what": "ORF draw + gradients of " + {0: "bidirectional", 1: "causal",
-                                                   2: "bidirectional and causal"}[op]
-                    + " attention with respect to Q, K, V (forward recomputed inside)",
-            "kernels": {k: {"ms_per_launch": v[0] / v[1], "launches_per_step": v[1] / args.steps}
-                        for k, v in kb.items() if v[1] > 0}}
+        def step_bwd(i):
+            fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
+            gradients(False)
+
+        def step_train(i):
+            fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
+            if op == 2:
+                fv.attn_both(Qd, Kd, Vd, Wd[0], bd[0], s, out_bidir=out_b, out_causal=out_c,
+                             workspace=ws, stream=s_main, row_scale_bidir=rs_b,
+                             row_scale_causal=rs_c)
+            elif op == 0:
+                fv.attn_bidir(Qd, Kd, Vd, Wd[0], bd[0], s, out=out_b, workspace=ws,
+                              stream=s_main, row_scale=rs_b)
+            else:
+                fv.attn_causal(Qd, Kd, Vd, Wd[0], bd[0], s, out=out_c, workspace=ws,
+                               stream=s_main, row_scale=rs_c)
+            gradients(True)
+
+        for name, step_v, what in (
+                ("backward", step_bwd, "ORF draw + gradients of " + directions
+                 + " attention with respect to Q, K, V (forward recomputed inside)"),
+                ("train_step", step_train, "ORF draw + " + directions + " attention saving "
+                 "the row scales + gradients with respect to Q, K, V from the saved outputs")):
+            if name not in chosen:
+                continue
+            for i in range(args.warmup):
+                step_v(first + i)
+            first += args.warmup
+            ms_b = timed_region(step_v, first)
+            first += args.steps
+            ms_bi = timed_region(step_v, first, instrumented=True)
+            first += args.steps
+            kb = fv.timing_read()
+            variants[name] = {
+                "ms_per_step": ms_b, "value": w.B * w.H * w.L / (ms_b / 1e3),
+                "ms_per_step_instrumented": ms_bi, "what": what,
+                "kernels": {k: {"ms_per_launch": v[0] / v[1],
+                                "launches_per_step": v[1] / args.steps}
+                            for k, v in kb.items() if v[1] > 0}}
 
     token_heads = w.B * w.H * w.L
     value = token_heads / (ms_step / 1e3)

@@ -149,10 +149,13 @@ FAVOR_API size_t favor_workspace_size(const favor_desc *g, int causal);
  * where Q', K' are the feature maps of favor_feature_map for g->kernel. With
  * g->no_renormalize = 1 the result is Buf3 itself. The L x L matrix Q' K'^T and
  * the L x M features are never stored. Deterministic (no atomics).
+ * row_scale (nullable) [B][H][L] fp32: receives each row's 1 / (buf4 + denom_eps)
+ * in units of the features without D_Q sqrt(2/M), for the backward pass; needs
+ * out_dtype == in_dtype; not written without renormalisation.
  */
 FAVOR_API favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
                               const void *V, const float *W, const float *b, void *out,
-                              void *ws, size_t ws_bytes, void *stream);
+                              float *row_scale, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * favor_attn_causal - unidirectional FAVOR by prefix sums (Sec. 2.5.1, Eq.
@@ -164,10 +167,11 @@ FAVOR_API favor_status favor_attn_bidir(const favor_desc *g, const void *Q, cons
  * state_in  (nullable) [B][H][M][d+1] fp32: S_0, the aggregate of earlier tokens.
  * state_out (nullable) [B][H][M][d+1] fp32: receives S_0 + sum over all L tokens,
  * so a long sequence can be processed in pieces. Deterministic (no atomics).
+ * row_scale (nullable): as for favor_attn_bidir.
  */
 FAVOR_API favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K,
                                const void *V, const float *W, const float *b, void *out,
-                               const float *state_in, float *state_out,
+                               const float *state_in, float *state_out, float *row_scale,
                                void *ws, size_t ws_bytes, void *stream);
 
 /*
@@ -178,11 +182,13 @@ FAVOR_API favor_status favor_attn_causal(const favor_desc *g, const void *Q, con
  * sequence (G^PS_L of Eq. cumsum), so one pass over the keys serves both:
  * the key features are built once per segment and the segment scan also
  * returns the total. Workspace: favor_workspace_size(g, 2). Deterministic.
+ * row_scale_bidir, row_scale_causal (nullable): as for favor_attn_bidir.
  */
 FAVOR_API favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K,
                                        const void *V, const float *W, const float *b,
                                        void *out_bidir, void *out_causal,
                                        const float *state_in, float *state_out,
+                                       float *row_scale_bidir, float *row_scale_causal,
                                        void *ws, size_t ws_bytes, void *stream);
 
 /*
@@ -200,15 +206,20 @@ FAVOR_API favor_status favor_attn_both(const favor_desc *g, const void *Q, const
  * M <= 64 (causal); bf16 inputs: every M. Deterministic (no
  * atomics). dQ, dK, dV are written in full (ragged tails included).
  * Workspace: favor_backward_workspace_size(g, causal) bytes, 256-byte aligned.
+ * out and row_scale (both nullable, both or neither): the forward call's output
+ * and row_scale for the same inputs, features and descriptor; given, the backward
+ * skips recomputing them (their recomputation otherwise runs inside the call).
+ * Not read without renormalisation.
  */
 FAVOR_API size_t favor_backward_workspace_size(const favor_desc *g, int causal);
 
 /* favor_attn_bidir_backward - gradients of favor_attn_bidir. */
 FAVOR_API favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q,
                                                  const void *K, const void *V, const float *W,
-                                                 const float *b, const void *dout, void *dQ,
-                                                 void *dK, void *dV, void *ws, size_t ws_bytes,
-                                                 void *stream);
+                                                 const float *b, const void *dout,
+                                                 const void *out, const float *row_scale,
+                                                 void *dQ, void *dK, void *dV, void *ws,
+                                                 size_t ws_bytes, void *stream);
 
 /*
  * favor_attn_causal_backward - gradients of favor_attn_causal (Eq. cumsum):
@@ -223,9 +234,11 @@ FAVOR_API favor_status favor_attn_bidir_backward(const favor_desc *g, const void
 FAVOR_API favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q,
                                                   const void *K, const void *V, const float *W,
                                                   const float *b, const float *state_in,
-                                                  const void *dout, const float *dstate_out,
-                                                  void *dQ, void *dK, void *dV, float *dstate_in,
-                                                  void *ws, size_t ws_bytes, void *stream);
+                                                  const void *dout, const void *out,
+                                                  const float *row_scale,
+                                                  const float *dstate_out, void *dQ, void *dK,
+                                                  void *dV, float *dstate_in, void *ws,
+                                                  size_t ws_bytes, void *stream);
 
 /* Host-only validation of a descriptor for an operation (0 feature map,
  * 1 bidirectional, 2 causal, 3 both, 4 bidirectional backward, 5 causal
@@ -255,7 +268,7 @@ FAVOR_API favor_status favor_timing_read(int32_t k, double *ms, int64_t *count);
 /* ABI version of this header; bumped on any incompatible change. */
 FAVOR_API int32_t favor_abi_version(void);
 
-#define FAVOR_ABI_VERSION 3
+#define FAVOR_ABI_VERSION 4
 
 #ifdef __cplusplus
 }

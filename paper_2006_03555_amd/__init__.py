@@ -12,7 +12,9 @@ W [H, M, d] float32 and b [H, M] float32 from ``orf_draw``.
 Keyword options of the feature and attention calls: kernel (KERNEL_SOFTMAX, the
 Gaussian-kernel features of softmax attention, or KERNEL_RELU, generalized
 attention with ReLU features), renormalize (False returns Q' K'^T V without the
-division by D-hat) and kernel_eps (added to every ReLU feature).
+division by D-hat) and kernel_eps (added to every ReLU feature). The attention
+calls take row_scale (a [B, H, L] float32 tensor) to save each row's
+1 / (D-hat + eps) for the backward calls, which then skip recomputing it.
 """
 import ctypes
 import os
@@ -157,9 +159,14 @@ def _workspace(g, causal, workspace):
     return workspace, workspace.numel() * workspace.element_size()
 
 
+def _require_row_scale(t, g, name):
+    torch = _torch()
+    _require_like(t, (g.B, g.H, g.L), torch.float32, name)
+
+
 def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=None,
                workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
-               kernel_eps=1e-3):
+               kernel_eps=1e-3, row_scale=None):
     """Bidirectional FAVOR, Algorithm 1 (favor_attn_bidir). Returns out [B, H, L, d]."""
     torch = _torch()
     g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps,
@@ -168,16 +175,18 @@ def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=No
     if out is None:
         out = torch.empty(Q.shape, dtype=_torch_dtype(g.out_dtype), device=Q.device)
     _require_like(out, Q.shape, _torch_dtype(g.out_dtype), "out")
-    _require_cuda(Q, K, V, W, b, out)
+    _require_row_scale(row_scale, g, "row_scale")
+    _require_cuda(Q, K, V, W, b, out, row_scale)
     ws, nbytes = _workspace(g, 0, workspace)
     _check(lib().favor_attn_bidir(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
-                                  _ptr(out), _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
+                                  _ptr(out), _ptr(row_scale), _ptr(ws), ctypes.c_size_t(nbytes),
+                                  _stream(stream)))
     return out
 
 
 def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
                 chunk=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None,
-                kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3):
+                kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3, row_scale=None):
     """Unidirectional FAVOR by prefix sums (favor_attn_causal).
 
     Returns out, or (out, state_out [B, H, M, d+1]) when return_state is true.
@@ -194,18 +203,19 @@ def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return
     _require_like(out, Q.shape, _torch_dtype(g.out_dtype), "out")
     _require_like(state_in, sshape, torch.float32, "state_in")
     _require_like(state_out, sshape, torch.float32, "state_out")
-    _require_cuda(Q, K, V, W, b, out, state_in, state_out)
+    _require_row_scale(row_scale, g, "row_scale")
+    _require_cuda(Q, K, V, W, b, out, state_in, state_out, row_scale)
     ws, nbytes = _workspace(g, 1, workspace)
     _check(lib().favor_attn_causal(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
-                                   _ptr(out), _ptr(state_in), _ptr(state_out), _ptr(ws),
-                                   ctypes.c_size_t(nbytes), _stream(stream)))
+                                   _ptr(out), _ptr(state_in), _ptr(state_out), _ptr(row_scale),
+                                   _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
     return (out, state_out) if return_state else out
 
 
 def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
               chunk=0, out_dtype=None, out_bidir=None, out_causal=None, state_out=None,
               workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
-              kernel_eps=1e-3):
+              kernel_eps=1e-3, row_scale_bidir=None, row_scale_causal=None):
     """Both directions over the same inputs with one key pass (favor_attn_both).
 
     Returns (out_bidir, out_causal) or (out_bidir, out_causal, state_out).
@@ -226,12 +236,15 @@ def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_s
     _require_like(out_causal, Q.shape, odt, "out_causal")
     _require_like(state_in, sshape, torch.float32, "state_in")
     _require_like(state_out, sshape, torch.float32, "state_out")
-    _require_cuda(Q, K, V, W, b, out_bidir, out_causal, state_in, state_out)
+    _require_row_scale(row_scale_bidir, g, "row_scale_bidir")
+    _require_row_scale(row_scale_causal, g, "row_scale_causal")
+    _require_cuda(Q, K, V, W, b, out_bidir, out_causal, state_in, state_out, row_scale_bidir,
+                  row_scale_causal)
     ws, nbytes = _workspace(g, 2, workspace)
     _check(lib().favor_attn_both(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
                                  _ptr(out_bidir), _ptr(out_causal), _ptr(state_in),
-                                 _ptr(state_out), _ptr(ws), ctypes.c_size_t(nbytes),
-                                 _stream(stream)))
+                                 _ptr(state_out), _ptr(row_scale_bidir), _ptr(row_scale_causal),
+                                 _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
     if return_state:
         return out_bidir, out_causal, state_out
     return out_bidir, out_causal
@@ -257,30 +270,42 @@ def _bwd_grads(Q, dQ, dK, dV):
     return out
 
 
+def _saved(out, row_scale, g, Q):
+    if (out is None) != (row_scale is None):
+        raise FavorError(1, "pass the forward call's out and row_scale together")
+    if out is not None:
+        _require_like(out, Q.shape, Q.dtype, "out")
+        _require_row_scale(row_scale, g, "row_scale")
+
+
 def attn_bidir_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, dQ=None, dK=None,
                         dV=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
-                        renormalize=True, kernel_eps=1e-3):
+                        renormalize=True, kernel_eps=1e-3, out=None, row_scale=None):
     """Gradients (dQ, dK, dV) of attn_bidir for the upstream gradient dout
-    (favor_attn_bidir_backward; the forward pass is recomputed)."""
+    (favor_attn_bidir_backward). out and row_scale, from the forward call with
+    row_scale, spare recomputing them."""
     g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps,
                   others=(("K", K), ("V", V), ("dout", dout)),
                   opts=_opts(kernel, renormalize, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     dQ, dK, dV = _bwd_grads(Q, dQ, dK, dV)
-    _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV)
+    _saved(out, row_scale, g, Q)
+    _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV, out, row_scale)
     ws, nbytes = _bwd_workspace(g, False, workspace)
     _check(lib().favor_attn_bidir_backward(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W),
-                                           _ptr(b), _ptr(dout), _ptr(dQ), _ptr(dK), _ptr(dV),
-                                           _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
+                                           _ptr(b), _ptr(dout), _ptr(out), _ptr(row_scale),
+                                           _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws),
+                                           ctypes.c_size_t(nbytes), _stream(stream)))
     return dQ, dK, dV
 
 
 def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_in=None,
                          dstate_out=None, return_state_grad=False, dQ=None, dK=None, dV=None,
                          dstate_in=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
-                         renormalize=True, kernel_eps=1e-3):
+                         renormalize=True, kernel_eps=1e-3, out=None, row_scale=None):
     """Gradients of attn_causal (favor_attn_causal_backward). Returns (dQ, dK, dV), plus
-    dstate_in [B, H, M, d+1] when return_state_grad is true."""
+    dstate_in [B, H, M, d+1] when return_state_grad is true. out and row_scale as for
+    attn_bidir_backward."""
     torch = _torch()
     g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps,
                   others=(("K", K), ("V", V), ("dout", dout)),
@@ -292,12 +317,14 @@ def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_
         dstate_in = torch.empty(sshape, dtype=torch.float32, device=Q.device)
     for name, t in (("state_in", state_in), ("dstate_out", dstate_out), ("dstate_in", dstate_in)):
         _require_like(t, sshape, torch.float32, name)
-    _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV, state_in, dstate_out, dstate_in)
+    _saved(out, row_scale, g, Q)
+    _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV, state_in, dstate_out, dstate_in, out,
+                  row_scale)
     ws, nbytes = _bwd_workspace(g, True, workspace)
     _check(lib().favor_attn_causal_backward(
         ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b), _ptr(state_in), _ptr(dout),
-        _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(dstate_in), _ptr(ws),
-        ctypes.c_size_t(nbytes), _stream(stream)))
+        _ptr(out), _ptr(row_scale), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
+        _ptr(dstate_in), _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
     return (dQ, dK, dV, dstate_in) if return_state_grad else (dQ, dK, dV)
 
 

@@ -62,14 +62,16 @@ def lib():
         "favor_orf_draw": (ctypes.c_int, [u64, i32, i32, i32, ctypes.c_int, vp, vp, vp]),
         "favor_feature_map": (ctypes.c_int, [dp, vp, vp, vp, vp, vp]),
         "favor_workspace_size": (sz, [dp, ctypes.c_int]),
-        "favor_attn_bidir": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
-        "favor_attn_causal": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
-        "favor_attn_both": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_bidir": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_causal": (ctypes.c_int,
+                              [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_both": (ctypes.c_int,
+                            [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_backward_workspace_size": (sz, [dp, ctypes.c_int]),
-        "favor_attn_bidir_backward": (ctypes.c_int,
-                                      [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
-        "favor_attn_causal_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                                      vp, vp, vp, vp, sz, vp]),
+        "favor_attn_bidir_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                     vp, vp, vp, vp, sz, vp]),
+        "favor_attn_causal_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                      vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_validate_desc": (ctypes.c_int, [dp, ctypes.c_int]),
         "favor_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "favor_last_error": (ctypes.c_char_p, []),
@@ -101,7 +103,7 @@ def last_error():
 
 KERNEL_SOFTMAX = 0
 KERNEL_RELU = 1
-ABI_VERSION = 3   # favor_desc with kernel, no_renormalize, kernel_eps; backward entry points
+ABI_VERSION = 4   # forward row scales saved for the backward pass
 
 
 def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, chunk=0,

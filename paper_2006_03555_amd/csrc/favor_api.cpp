@@ -199,6 +199,15 @@ favor_status check_ptr(const void *p, const char *name, bool needed) {
   return FAVOR_OK;
 }
 
+// A forward call's optional row_scale output.
+favor_status check_row_scale(const favor_desc *g, const void *rs, const char *name) {
+  if (!rs || g->no_renormalize) return FAVOR_OK;
+  if (!aligned(rs, 4)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "%s is not 4-byte aligned", name);
+  if (g->out_dtype != g->in_dtype)
+    return fail(FAVOR_ERR_UNSUPPORTED, "%s needs out_dtype == in_dtype", name);
+  return FAVOR_OK;
+}
+
 favor_status device_result(hipError_t e, const char *what) {
   if (e != hipSuccess)
     return fail(FAVOR_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
@@ -289,8 +298,9 @@ favor_status favor_feature_map(const favor_desc *g, const void *X, const float *
 
 favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
                               const void *V, const float *W, const float *b, void *out,
-                              void *ws, size_t ws_bytes, void *stream) {
+                              float *row_scale, void *ws, size_t ws_bytes, void *stream) {
   FAVOR_TRY(validate(g, kOpBidir));
+  FAVOR_TRY(check_row_scale(g, row_scale, "row_scale"));
   const Plan p = make_plan(g, kOpBidir);
   const bool work = p.total > 0;
   FAVOR_TRY(check_ptr(Q, "Q", work));
@@ -324,16 +334,20 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
   if (e != hipSuccess) return device_result(e, "favor_attn_bidir reduction");
   {
     favor::LaunchTimer t(favor::kKerQside, st);
-    e = favor::launch_qside(sh, in, dt_of(g->out_dtype), Q, wfr, bq, frags, out, st);
+    if (row_scale && sh.renorm)
+      e = favor::launch_qside_save(sh, in, Q, wfr, bq, frags, out, row_scale, st);
+    else
+      e = favor::launch_qside(sh, in, dt_of(g->out_dtype), Q, wfr, bq, frags, out, st);
   }
   return device_result(e, "favor_attn_bidir query pass");
 }
 
 favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K,
                                const void *V, const float *W, const float *b, void *out,
-                               const float *state_in, float *state_out, void *ws,
-                               size_t ws_bytes, void *stream) {
+                               const float *state_in, float *state_out, float *row_scale,
+                               void *ws, size_t ws_bytes, void *stream) {
   FAVOR_TRY(validate(g, kOpCausal));
+  FAVOR_TRY(check_row_scale(g, row_scale, "row_scale"));
   const Plan p = make_plan(g, kOpCausal);
   const bool work = p.total > 0;
   const bool heads = (long long)g->B * g->H > 0;
@@ -383,17 +397,24 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
   if (e != hipSuccess) return device_result(e, "favor_attn_causal segment scan");
   {
     favor::LaunchTimer t(favor::kKerCausal, st);
-    e = favor::launch_causal(sh, in, dt_of(g->out_dtype), Q, K, V, wfr, bq, part, out,
-                             p.rows_per_split, p.nsplit, st);
+    if (row_scale && sh.renorm)
+      e = favor::launch_causal_save(sh, in, Q, K, V, wfr, bq, part, out, row_scale,
+                                    p.rows_per_split, p.nsplit, st);
+    else
+      e = favor::launch_causal(sh, in, dt_of(g->out_dtype), Q, K, V, wfr, bq, part, out,
+                               p.rows_per_split, p.nsplit, st);
   }
   return device_result(e, "favor_attn_causal chunk scan");
 }
 
 favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, const void *V,
                              const float *W, const float *b, void *out_bidir, void *out_causal,
-                             const float *state_in, float *state_out, void *ws,
-                             size_t ws_bytes, void *stream) {
+                             const float *state_in, float *state_out, float *row_scale_bidir,
+                             float *row_scale_causal, void *ws, size_t ws_bytes,
+                             void *stream) {
   FAVOR_TRY(validate(g, kOpBoth));
+  FAVOR_TRY(check_row_scale(g, row_scale_bidir, "row_scale_bidir"));
+  FAVOR_TRY(check_row_scale(g, row_scale_causal, "row_scale_causal"));
   const Plan p = make_plan(g, kOpBoth);
   const bool work = p.total > 0;
   const bool heads = (long long)g->B * g->H > 0;
@@ -446,13 +467,20 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
   if (e != hipSuccess) return device_result(e, "favor_attn_both segment scan");
   {
     favor::LaunchTimer t(favor::kKerQside, st);
-    e = favor::launch_qside(sh, in, out, Q, wfr, bq, frags, out_bidir, st);
+    if (row_scale_bidir && sh.renorm)
+      e = favor::launch_qside_save(sh, in, Q, wfr, bq, frags, out_bidir, row_scale_bidir, st);
+    else
+      e = favor::launch_qside(sh, in, out, Q, wfr, bq, frags, out_bidir, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_both bidirectional query pass");
   {
     favor::LaunchTimer t(favor::kKerCausal, st);
-    e = favor::launch_causal(sh, in, out, Q, K, V, wfr, bq, part, out_causal, p.rows_per_split,
-                             p.nsplit, st);
+    if (row_scale_causal && sh.renorm)
+      e = favor::launch_causal_save(sh, in, Q, K, V, wfr, bq, part, out_causal,
+                                    row_scale_causal, p.rows_per_split, p.nsplit, st);
+    else
+      e = favor::launch_causal(sh, in, out, Q, K, V, wfr, bq, part, out_causal,
+                               p.rows_per_split, p.nsplit, st);
   }
   return device_result(e, "favor_attn_both chunk scan");
 }
@@ -493,6 +521,16 @@ BwdBufs carve(const BwdPlan &p, void *ws) {
   return b;
 }
 
+// The forward call's output and row scales, when the caller passes them.
+favor_status check_saved(const favor_desc *g, const void *out, const float *rs, bool &saved) {
+  if ((out == nullptr) != (rs == nullptr))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "out and row_scale are passed together or not at all");
+  saved = out != nullptr && !g->no_renormalize;
+  if (saved && (!aligned(out, 16) || !aligned(rs, 4)))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "out must be 16-byte, row_scale 4-byte aligned");
+  return FAVOR_OK;
+}
+
 favor_status check_workspace(const void *ws, size_t ws_bytes, size_t need) {
   if (!ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is NULL");
   if (!aligned(ws, 256)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is not 256-byte aligned");
@@ -507,9 +545,12 @@ extern "C" {
 
 favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const void *K,
                                        const void *V, const float *W, const float *b,
-                                       const void *dout, void *dQ, void *dK, void *dV, void *ws,
-                                       size_t ws_bytes, void *stream) {
+                                       const void *dout, const void *out_fwd,
+                                       const float *row_scale, void *dQ, void *dK, void *dV,
+                                       void *ws, size_t ws_bytes, void *stream) {
   FAVOR_TRY(validate(g, kOpBidirBackward));
+  bool saved = false;
+  FAVOR_TRY(check_saved(g, out_fwd, row_scale, saved));
   const BwdPlan p = make_bwd_plan(g, false);
   const bool work = p.total > 0;
   const void *in_ptrs[] = {Q, K, V, W, b, dout, dQ, dK, dV};
@@ -530,7 +571,7 @@ favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const
                             st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward key pass");
-  if (sh.renorm) {
+  if (sh.renorm && !saved) {
     {
       favor::LaunchTimer t(favor::kKerFinalize, st);
       e = favor::launch_finalize(sh, in, w.part, p.nsplit, w.frags, st);
@@ -547,8 +588,8 @@ favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const
     e = favor::launch_sum_splits(sh, w.part, p.nsplit, w.buf1, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward Buf1");
-  favor::BwdArgs a{Q,  K,  V,  dout, w.out, w.rsave, w.wfr, w.bq, W, w.buf1,
-                   dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
+  favor::BwdArgs a{Q,  K,  V,  dout, saved ? out_fwd : w.out, saved ? row_scale : w.rsave,
+                   w.wfr, w.bq, W, w.buf1, dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
   {
     favor::LaunchTimer t(favor::kKerBwdDq, st);
     e = favor::launch_bwd_dq(sh, in, false, a, st);
@@ -576,10 +617,13 @@ favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const
 favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, const void *K,
                                         const void *V, const float *W, const float *b,
                                         const float *state_in, const void *dout,
+                                        const void *out_fwd, const float *row_scale,
                                         const float *dstate_out, void *dQ, void *dK, void *dV,
                                         float *dstate_in, void *ws, size_t ws_bytes,
                                         void *stream) {
   FAVOR_TRY(validate(g, kOpCausalBackward));
+  bool saved = false;
+  FAVOR_TRY(check_saved(g, out_fwd, row_scale, saved));
   const BwdPlan p = make_bwd_plan(g, true);
   const bool work = p.total > 0;
   const bool heads = (long long)g->B * g->H > 0;
@@ -621,14 +665,14 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
     e = favor::launch_seg_scan(sh, in, w.part, p.nsplit, state_in, nullptr, nullptr, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward segment prefixes");
-  if (sh.renorm) {
+  if (sh.renorm && !saved) {
     favor::LaunchTimer t(favor::kKerCausal, st);
     e = favor::launch_causal_save(sh, in, Q, K, V, w.wfr, w.bq, w.part, w.out, w.rsave,
                                   p.rows_per_split, p.nsplit, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward forward pass");
-  favor::BwdArgs a{Q,  K,  V,  dout, w.out, w.rsave, w.wfr, w.bq, W, w.part,
-                   dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
+  favor::BwdArgs a{Q,  K,  V,  dout, saved ? out_fwd : w.out, saved ? row_scale : w.rsave,
+                   w.wfr, w.bq, W, w.part, dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
   {
     favor::LaunchTimer t(favor::kKerBwdDq, st);
     e = favor::launch_bwd_dq(sh, in, true, a, st);

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_strings(L):
-    assert L.favor_abi_version() == 3
+    assert L.favor_abi_version() == 4
     assert fv.status_string(0) == "FAVOR_OK"
     assert fv.status_string(3) == "FAVOR_ERR_WORKSPACE_TOO_SMALL"
 
@@ -120,22 +120,32 @@ def test_backward_calls_fail_before_launch(L):
     g = _desc()
     null = ctypes.c_void_p(0)
     fake = ctypes.c_void_p(1 << 20)
-    f9 = [fake] * 6
-    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f9, null, fake, fake, fake, 1 << 40, null)
+    f6 = [fake] * 6
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, null, null, null, fake, fake, fake,
+                                     1 << 40, null)
     assert st == 1 and "dQ" in fv.last_error()
-    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f9, fake, fake, fake, fake, 16, null)
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, null, null, fake, fake, fake, fake, 16,
+                                     null)
     assert st == 3
-    st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), null, fake, null, fake,
-                                      fake, fake, null, fake, 16, null)
+    # out and row_scale come together or not at all
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, fake, null, fake, fake, fake, fake,
+                                     1 << 40, null)
+    assert st == 1 and "together" in fv.last_error()
+    st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), null, fake, null, null,
+                                      null, fake, fake, fake, null, fake, 16, null)
     assert st == 3
     odd = ctypes.c_void_p((1 << 20) + 4)
-    st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), odd, fake, null, fake,
-                                      fake, fake, null, fake, 1 << 40, null)
+    st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), odd, fake, null, null,
+                                      null, fake, fake, fake, null, fake, 1 << 40, null)
     assert st == 1 and "state_in" in fv.last_error()
     bad = _desc(out_dtype=fv.F32)
-    st = L.favor_attn_bidir_backward(ctypes.byref(bad), *f9, fake, fake, fake, fake, 1 << 40,
-                                     null)
+    st = L.favor_attn_bidir_backward(ctypes.byref(bad), *f6, null, null, fake, fake, fake, fake,
+                                     1 << 40, null)
     assert st == 2
+    # a forward row_scale needs out dtype = in dtype
+    st = L.favor_attn_bidir(ctypes.byref(bad), fake, fake, fake, fake, fake, fake, fake, fake,
+                            1 << 40, null)
+    assert st == 2 and "row_scale" in fv.last_error()
 
 
 def test_workspace_size():
@@ -156,23 +166,26 @@ def test_calls_fail_before_launch(L):
     null = ctypes.c_void_p(0)
     fake = ctypes.c_void_p(1 << 20)
     # NULL tensors
-    st = L.favor_attn_bidir(ctypes.byref(g), null, null, null, null, null, null, null, 0, null)
+    st = L.favor_attn_bidir(ctypes.byref(g), null, null, null, null, null, null, null, null, 0,
+                            null)
     assert st == 1 and "NULL" in fv.last_error()
     # misaligned tensor
     odd = ctypes.c_void_p((1 << 20) + 2)
-    st = L.favor_attn_bidir(ctypes.byref(g), odd, fake, fake, fake, fake, fake, fake, 1 << 30, null)
+    st = L.favor_attn_bidir(ctypes.byref(g), odd, fake, fake, fake, fake, fake, null, fake,
+                            1 << 30, null)
     assert st == 1 and "aligned" in fv.last_error()
     # workspace too small
-    st = L.favor_attn_bidir(ctypes.byref(g), fake, fake, fake, fake, fake, fake, fake, 16, null)
+    st = L.favor_attn_bidir(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, fake, 16,
+                            null)
     assert st == 3
     st = L.favor_attn_causal(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, null,
-                             fake, 16, null)
+                             null, fake, 16, null)
     assert st == 3
     st = L.favor_attn_both(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, null, null,
-                           fake, 1 << 30, null)
+                           null, null, fake, 1 << 30, null)
     assert st == 1 and "out_causal" in fv.last_error()
     st = L.favor_attn_both(ctypes.byref(g), fake, fake, fake, fake, fake, fake, fake, null, null,
-                           fake, 16, null)
+                           null, null, fake, 16, null)
     assert st == 3
     # bad descriptor
     bad = _desc(M=100)

@@ -169,3 +169,68 @@ def test_backward_is_deterministic():
     torch.cuda.synchronize()
     for x, y in zip(a + c, a2 + c2):
         assert torch.equal(x, y)
+
+
+SAVED_CASES = [
+    # B, H, L, M, dtype, kernel, denom_eps (fp32 causal gradients take M <= 64)
+    (1, 2, 300, 64, "f32", SOFTMAX, 0.0),
+    (2, 2, 1000, 256, "bf16", SOFTMAX, 0.0),
+    (1, 2, 517, 128, "bf16", SOFTMAX, 0.5),
+    (1, 2, 257, 64, "f32", RELU, 0.1),
+    (1, 3, 777, 256, "bf16", RELU, 0.0),
+]
+
+
+def _expected_row_scale(Q, K, W, b, M, kernel, eps, causal):
+    """1 / (buf4 + eps) of Algorithm 1 (prefix sums of K' when causal), in units of
+    the features without the query factor D_Q sqrt(2/M): times that factor for
+    softmax features, as is for ReLU features (which have none)."""
+    Qp = favor.features(Q, W, b, S64, kernel, 1e-3)
+    Kp = favor.features(K, W, b, S64, kernel, 1e-3)
+    ksum = np.cumsum(Kp, axis=-2) if causal else Kp.sum(axis=-2, keepdims=True)
+    r = 1.0 / (np.sum(Qp * ksum, axis=-1) + eps)
+    if kernel == SOFTMAX:
+        qs = S64 * np.asarray(Q, dtype=np.float64)
+        r = r * np.sqrt(2.0 / M) * np.exp(0.5 * np.sum(qs * qs, axis=-1))
+    return r
+
+
+@pytest.mark.parametrize("B,H,L,M,dtype,kernel,eps", SAVED_CASES)
+def test_saved_row_scales_spare_the_recompute(B, H, L, M, dtype, kernel, eps):
+    """attn_both with row scales: outputs as without them, the scales equal the
+    oracle's 1 / (D-hat + eps), and the backward calls given (out, row_scale)
+    return the gradients of the calls that recompute them."""
+    import torch
+    fv = _fv()
+    Q, K, V, dout, W, b = _inputs(B, H, L, M, dtype, seed=91 + L + M)
+    q, k, v, do = (to_dev(x, dtype) for x in (Q, K, V, dout))
+    Wd, bd = to_dev(W), to_dev(b)
+    kw = dict(kernel=kernel, denom_eps=eps)
+    ob0, oc0 = fv.attn_both(q, k, v, Wd, bd, S64, **kw)
+    rb = torch.full((B, H, L), float("nan"), device="cuda")
+    rc = torch.full((B, H, L), float("nan"), device="cuda")
+    ob, oc = fv.attn_both(q, k, v, Wd, bd, S64, row_scale_bidir=rb, row_scale_causal=rc, **kw)
+    ob1 = fv.attn_bidir(q, k, v, Wd, bd, S64, row_scale=torch.empty_like(rb), **kw)
+    rc1 = torch.empty_like(rc)
+    oc1 = fv.attn_causal(q, k, v, Wd, bd, S64, row_scale=rc1, **kw)
+    grads = {}
+    for causal, o, r in ((False, ob, rb), (True, oc, rc)):
+        f = fv.attn_causal_backward if causal else fv.attn_bidir_backward
+        grads[causal] = (f(q, k, v, Wd, bd, S64, do, **kw)[:3],
+                         f(q, k, v, Wd, bd, S64, do, out=o, row_scale=r, **kw)[:3])
+    torch.cuda.synchronize()
+    tol = TOL[dtype]
+    for a, c in ((ob0, ob), (oc0, oc), (ob, ob1), (oc, oc1)):
+        a, c = to_host(a), to_host(c)
+        assert np.max(np.abs(a - c)) <= tol * np.max(np.abs(a))
+    for causal, r in ((False, rb), (True, rc)):
+        want = _expected_row_scale(Q, K, W, b, M, kernel, eps, causal)
+        got = to_host(r).astype(np.float64)
+        assert np.all(np.isfinite(got))
+        assert np.max(np.abs(got - want) / np.abs(want)) <= tol, causal
+    assert np.max(np.abs(to_host(rc1) - to_host(rc)) / np.abs(to_host(rc))) <= tol
+    for causal in (False, True):
+        recomputed, saved = grads[causal]
+        names = ("dQ", "dK", "dV")
+        _check_all(dict(zip(names, map(to_host, saved))),
+                   dict(zip(names, (to_host(x).astype(np.float64) for x in recomputed))), dtype)
