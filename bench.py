@@ -156,6 +156,9 @@ def main():
                     help="keep running untimed warmup steps until this long has passed "
                          "(the GPU clocks settle over a few hundred milliseconds)")
     ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="rows per segment of the causal scan (a multiple of 64; 0 = the "
+                         "library's choice, one workgroup per CU) for the forward steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the ReLU, unnormalised and backward variants (profiler runs "
@@ -196,7 +199,7 @@ def main():
     out_b = torch.empty_like(Qd)
     out_c = torch.empty_like(Qd)
     g = fv.make_desc(w.B, H, w.L, w.d, M, fv.BF16 if w.dtype == "bf16" else fv.F32,
-                     fv.BF16 if w.dtype == "bf16" else fv.F32, s)
+                     fv.BF16 if w.dtype == "bf16" else fv.F32, s, chunk=args.chunk)
     op = {"bidir": 0, "causal": 1, "both": 2}[w.direction]
     ws = torch.empty(fv.workspace_size(g, op), dtype=torch.uint8, device=dev)
     s_main = torch.cuda.current_stream()
@@ -205,7 +208,9 @@ def main():
     ev_attn = [torch.cuda.Event(), torch.cuda.Event()]   # attention done reading slot k
 
     def attention(slot, opts=None):
-        opts = opts or {}
+        opts = dict(opts or {})
+        if op != 0:
+            opts["chunk"] = args.chunk
         if op == 2:     # one key pass serves both directions
             fv.attn_both(Qd, Kd, Vd, Wd[slot], bd[slot], s, out_bidir=out_b, out_causal=out_c,
                          workspace=ws, stream=s_main, **opts)
@@ -295,6 +300,8 @@ def main():
     # renormalisation: same draw, same launches, other feature epilogue / finalisation
     variants = {}
     chosen = set() if args.no_variants else set(args.variants.split(","))
+    if args.chunk:   # the backward calls take the library's segments
+        chosen -= {"backward", "train_step"}
     for name, opts in (("relu", dict(kernel=fv.KERNEL_RELU)),
                        ("softmax_no_renormalize", dict(renormalize=False))):
         if name not in chosen:
@@ -437,6 +444,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": M,
                    "direction": w.direction, "orf_draw_per_step": True,
+                   "causal_segment_rows": args.chunk or "library default",
                    "orf_draw": "drawn in line before the attention pass, same stream",
                    "parallelism": "single GPU"},
         "kernels": kernels,
