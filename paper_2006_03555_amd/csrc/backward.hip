@@ -67,15 +67,18 @@ __global__ __launch_bounds__(256) void k_sum_splits(const f32x4 *__restrict__ pa
 }
 
 // part [BH][nch][n4]: chunk c becomes dsout + sum_{c' > c} part[c']; the total
-// (dsout + every chunk) goes to dsin. Either pointer may be null.
+// (dsout + every chunk) goes to dsin. Either pointer may be null. dsout and dsin
+// hold the M_r rows drawn (n4u = M_r 65 / 4 units per head; the rows past them
+// are padding, zero in part).
 __global__ __launch_bounds__(256) void k_suffix_scan(f32x4 *__restrict__ part, int nch, int n4,
-                                                     const f32x4 *__restrict__ dsout,
+                                                     int n4u, const f32x4 *__restrict__ dsout,
                                                      f32x4 *__restrict__ dsin) {
   const int bh = blockIdx.y;
   const int u = blockIdx.x * 256 + threadIdx.x;
   if (u >= n4) return;
+  const bool drawn = u < n4u;
   f32x4 *p = part + (size_t)bh * nch * n4 + u;
-  f32x4 run = dsout ? dsout[(size_t)bh * n4 + u] : f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 run = dsout && drawn ? dsout[(size_t)bh * n4u + u] : f32x4{0.f, 0.f, 0.f, 0.f};
   int c = nch - 1;
   for (; c >= 7; c -= 8) {   // eight loads in flight
     f32x4 v[8];
@@ -92,7 +95,7 @@ __global__ __launch_bounds__(256) void k_suffix_scan(f32x4 *__restrict__ part, i
     p[(size_t)c * n4] = run;
     run += v;
   }
-  if (dsin) dsin[(size_t)bh * n4 + u] = run;
+  if (dsin && drawn) dsin[(size_t)bh * n4u + u] = run;
 }
 
 // ------------------------------------------------------------ LDS builders
@@ -100,7 +103,7 @@ __global__ __launch_bounds__(256) void k_suffix_scan(f32x4 *__restrict__ part, i
 // perm_col(kb, lane % 16) (store order), k = feature m = 32 s + chained(g, i).
 template <typename T, int M>
 __device__ __forceinline__ void build_wt(typename Mma<T>::frag (*WT)[M / 32][64],
-                                         const float *__restrict__ Wh, float scale) {
+                                         const float *__restrict__ Wh, float scale, int Mr) {
   constexpr int NS = M / 32;
   for (int idx = threadIdx.x; idx < 4 * NS * 64; idx += blockDim.x) {
     const int l = idx & 63;
@@ -110,7 +113,10 @@ __device__ __forceinline__ void build_wt(typename Mma<T>::frag (*WT)[M / 32][64]
     const int k = perm_col(kb, l & 15);
     float v[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = Wh[(32 * s + 16 * (i >> 2) + 4 * g + (i & 3)) * kD + k];
+    for (int i = 0; i < 8; ++i) {
+      const int m = 32 * s + 16 * (i >> 2) + 4 * g + (i & 3);
+      v[i] = m < Mr ? Wh[m * kD + k] : 0.f;   // rows past the M_r drawn are zero
+    }
     WT[kb][s][l] = Mma<T>::from_f32(v, scale);
   }
 }
@@ -203,8 +209,8 @@ template <typename T, int MB, int KN>
 __device__ __forceinline__ void chunk_features_t(typename Mma<T>::frag (*dst)[2][64],
                                                  const typename Mma<T>::frag (*WA)[2][64],
                                                  const float *bq,
-                                                 const typename Mma<T>::frag (&rf)[4][2], int mb0,
-                                                 float keps) {
+                                                 const typename Mma<T>::frag (&rf)[4][2],
+                                                 int mb0) {
   using P = Mma<T>;
   const int l = lane_id();
 #pragma unroll
@@ -219,7 +225,7 @@ __device__ __forceinline__ void chunk_features_t(typename Mma<T>::frag (*dst)[2]
       f32x4 p = P::mma(rf[tb][0], b0, f32x4{bb, bb, bb, bb});
       p = P::mma(rf[tb][1], b1, p);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) f[tb][j] = feature<KN, P>(p[j], keps);
+      for (int j = 0; j < 4; ++j) f[tb][j] = feature<KN, P>(p[j], bb);
     }
     dst[mbg][0][l] = P::pack(f[0], f[1]);
     dst[mbg][1][l] = P::pack(f[2], f[3]);
@@ -238,7 +244,7 @@ __device__ __forceinline__ void query_grad(
     const typename Mma<T>::frag (*WT)[M / 32][64], const typename Mma<T>::frag (*SA)[2][64],
     const float *sz, const typename Mma<T>::frag (*KT)[2][64],
     const typename Mma<T>::frag (&pb2)[2], const typename Mma<T>::frag (&qf)[2],
-    const typename Mma<T>::frag (&df)[2], float alpha, float ud, float s, float keps,
+    const typename Mma<T>::frag (&df)[2], float alpha, float ud, float s,
     f32x4 (&dacc)[4], float &dot2, int s0 = 0, int s1 = M / 32) {
   using P = Mma<T>;
   using frag = typename P::frag;
@@ -267,8 +273,8 @@ __device__ __forceinline__ void query_grad(
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float gj = fmaf(szv[j], ud, gt[j]);
-        dot2 = fmaf(gj, feature<KN, P>(p[j], keps), dot2);
-        G[hh][j] = sgn * alpha * gj * feature_slope<KN, P>(p[j]);
+        dot2 = fmaf(gj, feature<KN, P>(p[j], bcv[j]), dot2);
+        G[hh][j] = sgn * alpha * gj * feature_slope<KN, P>(p[j], bcv[j]);
       }
     }
     const frag gb = P::pack(G[0], G[1]);
@@ -343,7 +349,8 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
     const T *__restrict__ Q, const T *__restrict__ dout, const T *__restrict__ out,
     const float *__restrict__ rsave, const typename Mma<T>::frag *__restrict__ wfr,
     const float *__restrict__ bqg, const float *__restrict__ W, const float *__restrict__ buf1,
-    T *__restrict__ dQ, float2 *__restrict__ aux, int H, int L, float s, float keps, float wts,
+    T *__restrict__ dQ, float2 *__restrict__ aux, int H, int L, float s, int Mr, float cM,
+    float wts,
     int ntiles, int nitems) {
   using frag = typename Mma<T>::frag;
   __shared__ DqSmem<T, M> sm;
@@ -351,7 +358,6 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
   const int w = tid >> 6;
   const int g = (tid & 63) >> 4;
   const int c16 = tid & 15;
-  const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
   int begin, end;
   xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
@@ -364,7 +370,7 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
       __syncthreads();
       copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
       if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-      build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
+      build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
       build_state_rows<T, M>(sm.SA, sm.sz, buf1 + (size_t)bh * M * 65);
       cur = bh;
       __syncthreads();
@@ -384,7 +390,7 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
       f32x4 dacc[4];
       float dot2;
       query_grad<T, M, KN, false>(sm.WA, sm.bq, sm.WT, sm.SA, sm.sz, nullptr, none, qf, df, alpha,
-                                  ud, s, keps, dacc, dot2);
+                                  ud, s, dacc, dot2);
       if (i < L) {
         store_qgrad<T, KN>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
         if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
@@ -431,7 +437,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
     const T *__restrict__ dout, const T *__restrict__ out, const float *__restrict__ rsave,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ prefix, T *__restrict__ dQ,
-    float2 *__restrict__ aux, int H, int L, int seg_len, int nseg, float s, float keps,
+    float2 *__restrict__ aux, int H, int L, int seg_len, int nseg, float s, int Mr, float cM,
     float wts) {
   using SP = ScanSplit<M>;
   constexpr int FB = SP::FB;
@@ -450,7 +456,6 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
   const int qb = w & 3;          // row block of the chunk
   const int hf = w >> 2;         // half of the feature steps
   const bool sw = w < SP::FW;    // holds a slice of the state
-  const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
   const int r0 = seg * seg_len;
@@ -458,7 +463,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
 
   copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
   if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-  build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
+  build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
   // S^T slice: acc[nb][mb] rows = value column perm_col(nb, 4 g + j) (block 4: column
   // d replicated), lane = feature m = 16 (w FB + mb) + lane % 16
   f32x4 acc[5][FB];
@@ -509,7 +514,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
       if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(ka[tb]));
       Dk[tb] = t < r1 ? D : 0.f;
     }
-    if (sw) chunk_features_t<T, FB, KN>(sm.KT, sm.WA, sm.bq, ka, w * FB, keps);
+    if (sw) chunk_features_t<T, FB, KN>(sm.KT, sm.WA, sm.bq, ka, w * FB);
     if (hf == 0) {   // C~ of key block qb (its rows loaded again: no runtime register index)
       const int t = t0 + 16 * qb + c16;
       frag ko[2], vo[2];
@@ -580,7 +585,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
     f32x4 dacc[4];
     float dot2;
     query_grad<T, M, KN, true>(sm.WA, sm.bq, sm.WT, sm.SA, sm.sz, sm.KT, pb2, qf, df, alpha, ud,
-                               s, keps, dacc, dot2, s0, s1);
+                               s, dacc, dot2, s0, s1);
     if (hf == 1) {
 #pragma unroll
       for (int k = 0; k < 4; ++k)
@@ -616,7 +621,7 @@ __device__ __forceinline__ void key_grad(
     const typename Mma<T>::frag (*QT)[2][64], const typename Mma<T>::frag (&pb3)[2],
     const typename Mma<T>::frag (*QA)[M / 32][64], const typename Mma<T>::frag (*UF)[2][64],
     const typename Mma<T>::frag (&kf)[2], const typename Mma<T>::frag (&vf)[2], int jpos,
-    float keps, f32x4 (&kacc)[4], float &doth, f32x4 (&vacc)[4], int s0 = 0, int s1 = M / 32) {
+    f32x4 (&kacc)[4], float &doth, f32x4 (&vacc)[4], int s0 = 0, int s1 = M / 32) {
   using P = Mma<T>;
   using frag = typename P::frag;
   constexpr float sgn = KN == kCos ? -1.f : 1.f;
@@ -641,7 +646,7 @@ __device__ __forceinline__ void key_grad(
       f32x4 p = P::mma(WA[mb][0][l], kf[0], bcv);
       p = P::mma(WA[mb][1][l], kf[1], p);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kh[hh][j] = feature<KN, P>(p[j], keps);
+      for (int j = 0; j < 4; ++j) kh[hh][j] = feature<KN, P>(p[j], bcv[j]);
       if constexpr (KPART) {
         f32x4 hv = P::mma(RA[mb][0][l], vf[0], zero4);
         hv = P::mma(RA[mb][1][l], vf[1], hv);
@@ -654,7 +659,7 @@ __device__ __forceinline__ void key_grad(
         for (int j = 0; j < 4; ++j) {
           const float hj = hv[j] + rzv[j];
           doth = fmaf(hj, kh[hh][j], doth);
-          G[hh][j] = sgn * hj * feature_slope<KN, P>(p[j]);
+          G[hh][j] = sgn * hj * feature_slope<KN, P>(p[j], bcv[j]);
         }
       }
     }
@@ -735,13 +740,13 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dkv(
     const T *__restrict__ K, const T *__restrict__ V,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ dbuf1, T *__restrict__ dK,
-    T *__restrict__ dV, int H, int L, float s, float keps, float wts, int ntiles, int nitems) {
+    T *__restrict__ dV, int H, int L, float s, int Mr, float cM, float wts, int ntiles,
+    int nitems) {
   using frag = typename Mma<T>::frag;
   __shared__ DkvSmem<T, M> sm;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
   const int c16 = tid & 15;
-  const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
   int begin, end;
   xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
@@ -754,7 +759,7 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dkv(
       __syncthreads();
       copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
       if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-      build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
+      build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
       const float *Rs = dbuf1 + (size_t)bh * M * 65;
       build_state_rows<T, M>(sm.RA, sm.rz, Rs);
       build_state_cols<T, M>(sm.RB, Rs);
@@ -775,7 +780,7 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dkv(
       f32x4 kacc[4], vacc[4];
       float doth;
       key_grad<T, M, KN, true, true, false>(sm.WA, sm.bq, sm.WT, sm.RA, sm.rz, sm.RB, nullptr,
-                                            none, nullptr, nullptr, kf, vf, 0, keps, kacc, doth,
+                                            none, nullptr, nullptr, kf, vf, 0, kacc, doth,
                                             vacc);
       if (j < L) {
         store_kgrad<T, KN>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
@@ -816,7 +821,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     const T *__restrict__ dout, const float2 *__restrict__ aux,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ suffix, T *__restrict__ dK,
-    T *__restrict__ dV, int H, int L, int seg_len, int nseg, float s, float keps, float wts) {
+    T *__restrict__ dV, int H, int L, int seg_len, int nseg, float s, int Mr, float cM, float wts) {
   using SP = ScanSplit<M>;
   constexpr int FB = SP::FB;
   using P = Mma<T>;
@@ -834,7 +839,6 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
   const int qb = w & 3;
   const int hf = w >> 2;
   const bool sw = w < SP::FW;
-  const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
   const int r0 = seg * seg_len;
@@ -844,7 +848,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
 
   copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
   if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-  if constexpr (KPART) build_wt<T, M>(sm.WT, W + (size_t)h * M * kD, wts);
+  if constexpr (KPART) build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
   // dK: acc[nb][mb] rows value column perm_col(nb, 4 g + j) (block 4: column d),
   // lane m = 16 (w FB + mb) + lane % 16. dV: acc[mb][nb] rows m = 16 (w FB + mb)
   // + 4 g + j, lane value column perm_col(nb, lane % 16).
@@ -888,7 +892,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     frag qa[4][2];
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) load_rows64<T>(qa[tb], Qh, t0 + 16 * tb + c16, r1);
-    if (sw) chunk_features_t<T, FB, KN>(sm.QT, sm.WA, sm.bq, qa, w * FB, keps);
+    if (sw) chunk_features_t<T, FB, KN>(sm.QT, sm.WA, sm.bq, qa, w * FB);
     frag da[4][2];
     float2 au[4];
 #pragma unroll
@@ -939,7 +943,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
           f32x4 p = P::mma(sm.WA[mb][0][l], qo[0], bcv);
           p = P::mma(sm.WA[mb][1][l], qo[1], p);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) f[hh][j] = feature<KN, P>(p[j], keps);
+          for (int j = 0; j < 4; ++j) f[hh][j] = feature<KN, P>(p[j], bcv[j]);
         }
         sm.QA[qb][sidx][l] = P::pack(f[0], f[1]);
       }
@@ -1010,7 +1014,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     key_grad<T, M, KN, KPART, !KPART, true>(
         sm.WA, sm.bq, reinterpret_cast<TS>(&sm.WT[0][0][0]), reinterpret_cast<T2>(&sm.RA[0][0][0]),
         sm.rz, reinterpret_cast<TS>(&sm.RB[0][0][0]), sm.QT, pb3,
-        reinterpret_cast<TS>(&sm.QA[0][0][0]), sm.UF, kf, vf, 16 * qb + c16, keps, kacc, doth,
+        reinterpret_cast<TS>(&sm.QA[0][0][0]), sm.UF, kf, vf, 16 * qb + c16, kacc, doth,
         vacc, s0, s1);
     f32x4 (&part)[4] = KPART ? kacc : vacc;
     if (hf == 1) {
@@ -1071,7 +1075,7 @@ template <typename T> constexpr int bwd_max_m(bool causal) {
 // Scale of W in the input-gradient products: s for cos features (2 pi W'' = s W),
 // s / sqrt(M) for ReLU features (W'' itself).
 static float wt_scale(const Shape &sh) {
-  return sh.kernel == 1 ? sh.s / sqrtf((float)sh.M) : sh.s;
+  return sh.kernel == 1 ? sh.s / sqrtf((float)sh.Mr) : sh.s;
 }
 
 // Rows per persistent bidirectional tile: 8 waves x kBwdTbw blocks of 16 (one
@@ -1093,7 +1097,7 @@ hipError_t launch_suffix_scan(const Shape &sh, float *part, int nch, const float
   const int n4 = sh.M * 65 / 4;
   dim3 grid((n4 + 255) / 256, sh.BH);
   hipLaunchKernelGGL(k_suffix_scan, grid, dim3(256), 0, st, (f32x4 *)part, nch, n4,
-                     (const f32x4 *)dsout, (f32x4 *)dsin);
+                     sh.Mr * 65 / 4, (const f32x4 *)dsout, (f32x4 *)dsin);
   return hipGetLastError();
 }
 
@@ -1120,7 +1124,7 @@ static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, h
                              (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
                              (const T *)a.out, a.rsave, (const typename Mma<T>::frag *)a.wfr,
                              a.bq, a.W, a.state, (T *)a.dQ, a.aux, sh.H, sh.L, a.seg_len, a.nseg,
-                             sh.s, sh.keps, wts));
+                             sh.s, sh.Mr, feature_norm(sh), wts));
     } else {
       const int rows = kBwdBidirThreads / 4 * kBwdTbw;
       const int ntiles = (sh.L + rows - 1) / rows;
@@ -1131,7 +1135,8 @@ static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, h
                              st,
                              (const T *)a.Q, (const T *)a.dout, (const T *)a.out, a.rsave,
                              (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
-                             (T *)a.dQ, a.aux, sh.H, sh.L, sh.s, sh.keps, wts, ntiles, nitems));
+                             (T *)a.dQ, a.aux, sh.H, sh.L, sh.s, sh.Mr, feature_norm(sh), wts,
+                             ntiles, nitems));
     }
     return hipGetLastError();
   });
@@ -1154,13 +1159,13 @@ static hipError_t bwd_dkv_typed(const Shape &sh, bool causal, const BwdArgs &a, 
         hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, false>), grid, dim3(kScanThreads), 0, st,
                            (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
                            a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
-                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.keps,
-                           wts);
+                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
+                           feature_norm(sh), wts);
         hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, true>), grid, dim3(kScanThreads), 0, st,
                            (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
                            a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
-                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.keps,
-                           wts);
+                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
+                           feature_norm(sh), wts);
       });
     } else {
       const int rows = kBwdBidirThreads / 4 * kBwdTbw;
@@ -1170,8 +1175,8 @@ static hipError_t bwd_dkv_typed(const Shape &sh, bool causal, const BwdArgs &a, 
       FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(false), sh.M,
           hipLaunchKernelGGL((k_bwd_dkv<T, MM, KN, kBwdTbw>), grid, dim3(kBwdBidirThreads), 0, st,
                              (const T *)a.K, (const T *)a.V, (const typename Mma<T>::frag *)a.wfr,
-                             a.bq, a.W, a.state, (T *)a.dK, (T *)a.dV, sh.H, sh.L, sh.s, sh.keps,
-                             wts, ntiles, nitems));
+                             a.bq, a.W, a.state, (T *)a.dK, (T *)a.dV, sh.H, sh.L, sh.s, sh.Mr,
+                             feature_norm(sh), wts, ntiles, nitems));
     }
     return hipGetLastError();
   });

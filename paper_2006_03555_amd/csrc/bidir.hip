@@ -35,19 +35,27 @@ namespace favor {
 // (m = i / 8, c = i % 8; row-contiguous, so the loads are fully coalesced) into
 // lane 16 (c % 4) + m % 16 of fragment (m / 16, c / 4). All loads are issued
 // before the first LDS store.
-template <typename T, int M, int NT>
+template <typename T, int M, int NT, int KN>
 __device__ __forceinline__ void fill_w_bfrags_lds(typename Mma<T>::frag (*WB)[2][64], float *bq,
                                                   const float *__restrict__ Wh,
                                                   const float *__restrict__ bh, float ws,
-                                                  float bs) {
+                                                  float bs, int Mr, float keps) {
   constexpr int N = M * 8;   // fragment lanes of the head
   constexpr int IT = N / NT;
   static_assert(N % NT == 0 && M <= NT, "thread count");
   const int tid = threadIdx.x;
   float v[IT][8];
 #pragma unroll
-  for (int it = 0; it < IT; ++it) load8_f32(Wh + (size_t)(it * NT + tid) * 8, v[it]);
-  const float bb = tid < M ? bh[tid] : 0.f;
+  for (int it = 0; it < IT; ++it) {
+    const int idx = it * NT + tid;
+    if ((idx >> 3) < Mr) {   // W'' rows past the M_r drawn are zero
+      load8_f32(Wh + (size_t)idx * 8, v[it]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[it][i] = 0.f;
+    }
+  }
+  const float bb = tid < M ? seed_row<KN>(tid, Mr, bh, bs, keps) : 0.f;
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const int idx = it * NT + tid;
@@ -55,7 +63,7 @@ __device__ __forceinline__ void fill_w_bfrags_lds(typename Mma<T>::frag (*WB)[2]
     const int c = idx & 7;
     WB[m >> 4][c >> 2][16 * (c & 3) + (m & 15)] = Mma<T>::from_f32(v[it], ws);
   }
-  if (tid < M) bq[tid] = bb * bs;
+  if (tid < M) bq[tid] = bb;
 }
 
 // Workgroup = NG groups of four waves. Group G takes the 64-token tiles
@@ -88,7 +96,8 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
     const T *__restrict__ K, const T *__restrict__ V, const float *__restrict__ W,
     const float *__restrict__ b, typename Mma<T>::frag *__restrict__ wfr,
     float *__restrict__ bqg, float *__restrict__ part, int H, int L, int rows_per_split,
-    int nsplit, float s, float ws, float bs, float keps, const float2 *__restrict__ aux) {
+    int nsplit, float s, float ws, float bs, float keps, int Mr, float cM,
+    const float2 *__restrict__ aux) {
   const int item = xcd_item(blockIdx.x, gridDim.x);
   const int bh = item / nsplit;
   const int split = item - bh * nsplit;
@@ -114,16 +123,16 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
   const T *Kh = K + (size_t)bh * L * kD;
   const T *Vh = V + (size_t)bh * L * kD;
   const float s2half = 0.5f * s * s;
-  const float cM = sqrtf(2.0f / M);
 
   // first tile's loads in flight while W'' is built
   TileRegs<T> rg;
   load_tile_regs<T>(rg, Kh, Vh, r0 + 64 * G, r1, tid);
 
-  fill_w_bfrags_lds<T, M, 256 * NG>(sm.WB, sm.bq, W + (size_t)h * M * kD, b + (size_t)h * M,
-                                    ws, bs);
+  fill_w_bfrags_lds<T, M, 256 * NG, KN>(sm.WB, sm.bq, W + (size_t)h * Mr * kD,
+                                        b + (size_t)h * Mr, ws, bs, Mr, keps);
   __syncthreads();
-  if (!AGG && bh < H && split == 0) {   // one workgroup per head stores W'' and b'' for later launches
+  // one workgroup per head stores W'' and b'' for later launches
+  if (!AGG && bh < H && split == 0) {
     constexpr int NF = (M / 16) * 2 * 64;
     frag *dst = wfr + (size_t)h * NF;
     for (int i = threadIdx.x; i < NF; i += 256 * NG) dst[i] = (&sm.WB[0][0][0])[i];
@@ -168,7 +177,7 @@ __global__ __launch_bounds__(256 * NG, sizeof(T) == 2 && NG == 1 ? 2 : 1) void k
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
       f32x4 kf[MB][2];
-      key_features<T, MB, KN>(tc, Wf, bC, sidx, keps, kf);
+      key_features<T, MB, KN>(tc, Wf, bC, sidx, kf);
       frag vb[4];
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) vb[nb] = tc.VtF[nb][sidx][l];
@@ -298,7 +307,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
                                                   const float *__restrict__ bqg,
                                                   const typename Mma<T>::frag *__restrict__ frags,
                                                   To *__restrict__ out, float *__restrict__ rsave,
-                                                  int H, int L, float s, float eps, float keps,
+                                                  int H, int L, float s, float eps, float cM,
                                                   int ntiles, int nitems) {
   constexpr int NS = M / 32;
   constexpr int TBW = QsideCfg<T>::TBW;
@@ -313,7 +322,6 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
-  const float cM = sqrtf(2.0f / M);
 
   int begin, end;
   xcd_range(blockIdx.x, gridDim.x, nitems, begin, end);
@@ -390,7 +398,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
           f32x4 p = P::mma(a0, qf[tb][0], bcv);
           p = P::mma(a1, qf[tb][1], p);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) pf[hh][tb][j] = feature<KN, P>(p[j], keps);
+          for (int j = 0; j < 4; ++j) pf[hh][tb][j] = feature<KN, P>(p[j], bcv[j]);
         }
       }
       frag qb[TBW];
@@ -451,12 +459,14 @@ static hipError_t kside_kernel(const Shape &sh, Dt in, const void *K, const void
                                         grid, dim3(256 * kside_groups(Dt::BF16, MM)), 0, st,
                                         (const bf16 *)K, (const bf16 *)V, W, b,
                                         (Mma<bf16>::frag *)wfr, bq, part, sh.H, sh.L,
-                                        rows_per_split, nsplit, sh.s, ws, bs, sh.keps, aux));
+                                        rows_per_split, nsplit, sh.s, ws, bs, sh.keps, sh.Mr,
+                                        feature_norm(sh), aux));
   } else {
     FAVOR_DISPATCH_M(sh.M, hipLaunchKernelGGL((k_kside<float, MM, 1, KN, AGG>), grid, dim3(256),
                                                0, st, (const float *)K, (const float *)V, W, b,
                                                (Mma<float>::frag *)wfr, bq, part, sh.H, sh.L,
                                                rows_per_split, nsplit, sh.s, ws, bs, sh.keps,
+                                               sh.Mr, feature_norm(sh),
                                                aux));
   }
   return hipGetLastError();
@@ -509,7 +519,8 @@ static hipError_t qside_launch(const Shape &sh, const void *Q, const void *wfr, 
                                              0, st, (const T *)Q,
                                              (const typename Mma<T>::frag *)wfr, bq,
                                              (const typename Mma<T>::frag *)frags, (To *)o, rsave,
-                                             sh.H, sh.L, sh.s, sh.eps, sh.keps, ntiles, nitems));
+                                             sh.H, sh.L, sh.s, sh.eps, feature_norm(sh), ntiles,
+                                             nitems));
   return hipGetLastError();
 }
 

@@ -48,7 +48,7 @@ constexpr int kSegScanThreads = 576;   // 520 float4 units of a 32-row block, ni
 
 template <typename E>
 __global__ __launch_bounds__(kSegScanThreads) void k_seg_scan(float *__restrict__ part, int nseg, int M,
-                                                  const float *__restrict__ state_in,
+                                                  int Mr, const float *__restrict__ state_in,
                                                   float *__restrict__ state_out,
                                                   E *__restrict__ frags) {
   constexpr int kUnits = 32 * 65 / 4;   // float4 per 32-row block
@@ -56,14 +56,18 @@ __global__ __launch_bounds__(kSegScanThreads) void k_seg_scan(float *__restrict_
   const int sidx = blockIdx.x;
   const int bh = blockIdx.y;
   const int n65 = M * 65;
-  const size_t head = (size_t)bh * n65 / 4 + (size_t)sidx * kUnits;   // in float4
+  // state_in / state_out hold the M_r rows drawn: the same row-major index, a
+  // head stride of M_r rows, and no padding rows (M_r 65 is a multiple of 4)
+  const int nuser = Mr * 65 / 4;
+  const size_t head = (size_t)bh * nuser + (size_t)sidx * kUnits;   // in float4
   f32x4 *p = reinterpret_cast<f32x4 *>(part) + (size_t)bh * nseg * (n65 / 4) + sidx * kUnits;
   const size_t stride = n65 / 4;   // one segment, in float4
   static_assert(kUnits <= kSegScanThreads, "one thread per unit");
   const int u = threadIdx.x;
   if (u < kUnits) {
-    const f32x4 s0 = state_in ? reinterpret_cast<const f32x4 *>(state_in)[head + u]
-                              : f32x4{0.f, 0.f, 0.f, 0.f};
+    const bool drawn = sidx * kUnits + u < nuser;
+    const f32x4 s0 = state_in && drawn ? reinterpret_cast<const f32x4 *>(state_in)[head + u]
+                                       : f32x4{0.f, 0.f, 0.f, 0.f};
     f32x4 run = {0.f, 0.f, 0.f, 0.f};   // aggregate of the segments before sg
     int sg = 0;
     for (; sg + 8 <= nseg; sg += 8) {   // eight loads in flight
@@ -81,7 +85,7 @@ __global__ __launch_bounds__(kSegScanThreads) void k_seg_scan(float *__restrict_
       p[sg * stride + u] = s0 + run;
       run += v;
     }
-    if (state_out) reinterpret_cast<f32x4 *>(state_out)[head + u] = s0 + run;
+    if (state_out && drawn) reinterpret_cast<f32x4 *>(state_out)[head + u] = s0 + run;
     tot[u] = run;
   }
   if (!frags) return;
@@ -123,7 +127,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
                                                 const float *__restrict__ prefix,
                                                 To *__restrict__ out, float *__restrict__ rsave,
                                                 int H, int L, int seg_len, int nseg, float s,
-                                                float eps, float keps) {
+                                                float eps, float cM) {
   constexpr int MW = M / 4;
   constexpr int MB = MW / 16;
   constexpr int NS = M / 32;
@@ -172,7 +176,6 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
   const T *Vh = V + (size_t)bh * L * kD;
   To *Oh = out + (size_t)bh * L * kD;
   const float s2half = 0.5f * s * s;
-  const float cM = sqrtf(2.0f / M);
   const int r0 = seg * seg_len;
   const int r1 = min(L, r0 + seg_len);
 
@@ -217,7 +220,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx) {
       f32x4 kf[MB][2];
-      key_features_lds<T, MB, KN>(tl, sm.WA, sm.bq, w * MB, sidx, keps, kf);
+      key_features_lds<T, MB, KN>(tl, sm.WA, sm.bq, w * MB, sidx, kf);
       frag vb[4];
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) vb[nb] = tl.VtF[nb][sidx][l];
@@ -314,7 +317,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) pf[hh][j] = feature<KN, P>(pc[hh][j], keps);
+        for (int j = 0; j < 4; ++j) pf[hh][j] = feature<KN, P>(pc[hh][j], cur.bc[hh][j]);
       const frag qb = P::pack(pf[0], pf[1]);
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) o[nb] = P::mma(cur.sa[nb], qb, o[nb]);
@@ -507,7 +510,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
                                                    const float *__restrict__ prefix,
                                                    To *__restrict__ out, float *__restrict__ rsave,
                                                    int H, int L, int seg_len, int nseg, float s,
-                                                   float eps, float keps) {
+                                                   float eps, float cM) {
   constexpr int MW = M / 4;          // features per wave
   constexpr int MB = MW / 16;        // 16-feature blocks per wave
   constexpr int KS = (MB + 1) / 2;   // 32-feature k-steps per wave (a lone block is zero-padded)
@@ -531,7 +534,6 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   const bf16 *Vh = V + (size_t)bh * L * kD;
   To *Oh = out + (size_t)bh * L * kD;
   const float s2half = 0.5f * s * s;
-  const float cM = sqrtf(2.0f / M);
   const int r0 = seg * seg_len;
   const int r1 = min(L, r0 + seg_len);
 
@@ -669,7 +671,8 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) pr[mb][j] = feature<KN, P>(pr[mb][j], keps);
+          for (int j = 0; j < 4; ++j)
+            pr[mb][j] = feature<KN, P>(pr[mb][j], i < 4 ? bqv[mb][j] : bk[mb]);
         if constexpr (i < 4) {
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks)
@@ -806,11 +809,11 @@ hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const 
                            float *state_out, void *total_frags, hipStream_t st) {
   dim3 grid(sh.M / 32, sh.BH);
   if (in == Dt::BF16)
-    hipLaunchKernelGGL(k_seg_scan<bf16>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M, state_in,
-                       state_out, (bf16 *)total_frags);
+    hipLaunchKernelGGL(k_seg_scan<bf16>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M,
+                       sh.Mr, state_in, state_out, (bf16 *)total_frags);
   else
-    hipLaunchKernelGGL(k_seg_scan<float>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M, state_in,
-                       state_out, (float *)total_frags);
+    hipLaunchKernelGGL(k_seg_scan<float>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M,
+                       sh.Mr, state_in, state_out, (float *)total_frags);
   return hipGetLastError();
 }
 
@@ -839,7 +842,7 @@ static hipError_t causal_fs_typed(const Shape &sh, const void *Q, const void *K,
   hipLaunchKernelGGL((k_causal_fs<To, MM, KN, RN, SAVE>), grid, dim3(256), 0, st,             \
                      (const bf16 *)Q, (const bf16 *)K, (const bf16 *)V, (const bf16x8 *)wfr,   \
                      bq, prefix, (To *)o, rsave, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps,      \
-                     sh.keps)
+                     feature_norm(sh))
       switch (sh.M) {
         case 64: FAVOR_CAUSAL_FS_LAUNCH(64); break;
         case 128: FAVOR_CAUSAL_FS_LAUNCH(128); break;
@@ -868,7 +871,7 @@ static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, co
   hipLaunchKernelGGL((k_causal<T, To, MM, KN, RN, SAVE>), grid, dim3(256), 0, st,             \
                      (const T *)Q, (const T *)K, (const T *)V,                                 \
                      (const typename Mma<T>::frag *)wfr, bq, prefix, (To *)o, rsave, sh.H,     \
-                     sh.L, seg_len, nseg, sh.s, sh.eps, sh.keps)
+                     sh.L, seg_len, nseg, sh.s, sh.eps, feature_norm(sh))
       switch (sh.M) {
         case 64: FAVOR_CAUSAL_LAUNCH(64); break;
         case 128: FAVOR_CAUSAL_LAUNCH(128); break;

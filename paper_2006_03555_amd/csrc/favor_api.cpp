@@ -34,6 +34,10 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Rows the kernels work on for M features: 64, 128 or 256 (the rows past M are
+// padding with zero features).
+int padded_m(int M) { return M <= 64 ? 64 : M <= 128 ? 128 : 256; }
+
 constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
 // the causal pass holds a whole compute unit per workgroup (LDS and registers),
 // so its segments are sized for one workgroup per CU
@@ -75,8 +79,9 @@ favor_status validate(const favor_desc *g, int op) {
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "chunk=%d must be a non-negative multiple of 64",
                 g->chunk);
   if (g->d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", g->d);
-  if (g->M != 64 && g->M != 128 && g->M != 256)
-    return fail(FAVOR_ERR_UNSUPPORTED, "M=%d not supported (64, 128, 256)", g->M);
+  if (g->M % 16 != 0 || g->M > 256)
+    return fail(FAVOR_ERR_UNSUPPORTED, "M=%d not supported (a multiple of 16, at most 256)",
+                g->M);
   const long long bh = (long long)g->B * g->H;
   if (bh > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "B*H=%lld exceeds 65535", bh);
   if ((op == kOpCausal || op == kOpBoth) && g->in_dtype == FAVOR_F32 && g->M > 128)
@@ -130,8 +135,8 @@ Plan make_plan(const favor_desc *g, int op) {
   } else {
     // a two-group k_kside workgroup fills a CU by itself
     const favor::Dt in = g->in_dtype == FAVOR_BF16 ? favor::Dt::BF16 : favor::Dt::F32;
-    const int target =
-        causal ? kCausalWorkgroups : kTargetWorkgroups / favor::kside_groups(in, g->M);
+    const int target = causal ? kCausalWorkgroups
+                              : kTargetWorkgroups / favor::kside_groups(in, padded_m(g->M));
     int want = (target + p.BH - 1) / p.BH;
     int max_split = tiles / (kMinRowsPerSplit / 64);
     if (max_split < 1) max_split = 1;
@@ -141,11 +146,12 @@ Plan make_plan(const favor_desc *g, int op) {
   }
   p.rows_per_split = rows;
   p.nsplit = (g->L + rows - 1) / rows;
-  p.part_bytes = round_up((size_t)p.BH * p.nsplit * g->M * 65 * sizeof(float), 256);
+  const int M = padded_m(g->M);
+  p.part_bytes = round_up((size_t)p.BH * p.nsplit * M * 65 * sizeof(float), 256);
   const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
-  if (op != kOpCausal) p.frag_bytes = round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
-  p.wfr_bytes = round_up((size_t)g->H * (g->M / 16) * 2 * 64 * fb, 256);
-  p.bq_bytes = round_up((size_t)g->H * g->M * sizeof(float), 256);
+  if (op != kOpCausal) p.frag_bytes = round_up((size_t)p.BH * 5 * (M / 32) * 64 * fb, 256);
+  p.wfr_bytes = round_up((size_t)g->H * (M / 16) * 2 * 64 * fb, 256);
+  p.bq_bytes = round_up((size_t)g->H * M * sizeof(float), 256);
   p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
   return p;
 }
@@ -155,16 +161,17 @@ BwdPlan make_bwd_plan(const favor_desc *g, bool causal) {
   p.BH = g->B * g->H;
   if (p.BH == 0 || g->L == 0) return p;
   const size_t elt = g->in_dtype == FAVOR_BF16 ? 2 : 4;
-  const size_t agg = (size_t)g->M * 65 * sizeof(float);
+  const int M = padded_m(g->M);
+  const size_t agg = (size_t)M * 65 * sizeof(float);
   // the forward plan's splits (bidirectional) or segments (causal)
   const Plan f = make_plan(g, causal ? kOpCausal : kOpBidir);
   p.rows_per_split = f.rows_per_split;
   p.nsplit = f.nsplit;
   const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
   p.part = round_up((size_t)p.BH * p.nsplit * agg, 256);
-  p.frags = causal ? 0 : round_up((size_t)p.BH * 5 * (g->M / 32) * 64 * fb, 256);
-  p.wfr = round_up((size_t)g->H * (g->M / 16) * 2 * 64 * fb, 256);
-  p.bq = round_up((size_t)g->H * g->M * sizeof(float), 256);
+  p.frags = causal ? 0 : round_up((size_t)p.BH * 5 * (M / 32) * 64 * fb, 256);
+  p.wfr = round_up((size_t)g->H * (M / 16) * 2 * 64 * fb, 256);
+  p.bq = round_up((size_t)g->H * M * sizeof(float), 256);
   p.out = round_up((size_t)p.BH * g->L * 64 * elt, 256);
   p.rsave = round_up((size_t)p.BH * g->L * sizeof(float), 256);
   p.aux = round_up((size_t)p.BH * g->L * 2 * sizeof(float), 256);
@@ -181,7 +188,8 @@ favor::Shape shape_of(const favor_desc *g) {
   sh.BH = g->B * g->H;
   sh.H = g->H;
   sh.L = g->L;
-  sh.M = g->M;
+  sh.M = padded_m(g->M);
+  sh.Mr = g->M;
   sh.s = g->input_scale;
   sh.eps = g->denom_eps;
   sh.kernel = g->kernel;

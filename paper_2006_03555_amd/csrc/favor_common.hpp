@@ -152,15 +152,22 @@ __device__ __forceinline__ void store8(float *p, f32x4 a, f32x4 b) {
 }
 
 // Feature kernels (Sec. 2.2, Eq. interesting): the epilogue applied to a
-// projection p = W'' x + b''. kCos: cos(2 pi p) (W'' and b'' carry 1/2 pi; the
-// D_X sqrt(2/M) factor is applied, or cancelled, outside); kRelu: ReLU(p) + keps
-// (W'' carries s / sqrt(M), b'' = 0, no D_X factor).
+// projection p = W'' x + b'' whose accumulator was seeded with the row's b''.
+// kCos: cos(2 pi p) (W'' and b'' carry 1/2 pi; the D_X sqrt(2/M) factor is
+// applied, or cancelled, outside). kRelu: ReLU(W'' x) + kernel_eps, computed as
+// max(p, b'') with b'' = kernel_eps (W'' carries s / sqrt(M), no D_X factor).
+//
+// Rows past the M features drawn (the kernels work on 64, 128 or 256 rows) have
+// W'' = 0 and the seed seed_row gives them: a quarter revolution for cos
+// features (cos(pi/2), zero up to the hardware cosine's error, which enters the
+// products only squared) and 0 for ReLU features (max(0, 0) = 0 exactly), so
+// they add nothing to any aggregate.
 constexpr int kCos = 0;
 constexpr int kRelu = 1;
 template <int KN, typename P>
-__device__ __forceinline__ float feature(float p, float keps) {
+__device__ __forceinline__ float feature(float p, float seed) {
   if constexpr (KN == kRelu) {
-    return fmaxf(p, 0.f) + keps;
+    return fmaxf(p, seed);
   } else {
     return P::cos_rev(p);
   }
@@ -168,14 +175,23 @@ __device__ __forceinline__ float feature(float p, float keps) {
 
 // Derivative factor of a feature with respect to its projection, up to the
 // constant the caller folds in: kCos: sin(2 pi p) (d cos / d theta = -sin);
-// kRelu: the step [p > 0] (0 at p = 0).
+// kRelu: the step [W'' x > 0] = [p > seed] (0 at W'' x = 0).
 template <int KN, typename P>
-__device__ __forceinline__ float feature_slope(float p) {
+__device__ __forceinline__ float feature_slope(float p, float seed) {
   if constexpr (KN == kRelu) {
-    return p > 0.f ? 1.f : 0.f;
+    return p > seed ? 1.f : 0.f;
   } else {
     return P::sin_rev(p);
   }
+}
+
+// b'' of feature row m of M_r drawn rows: the phase b_m bs (cos) or kernel_eps
+// (ReLU); rows m >= M_r are padding (see above).
+template <int KN>
+__device__ __forceinline__ float seed_row(int m, int Mr, const float *__restrict__ b, float bs,
+                                          float keps) {
+  if (m >= Mr) return KN == kRelu ? 0.f : 0.25f;
+  return KN == kRelu ? keps : b[m] * bs;
 }
 
 // Value-column order of the output-side operands (Buf1^T fragments, the causal

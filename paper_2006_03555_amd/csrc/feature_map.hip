@@ -31,11 +31,11 @@ __device__ __forceinline__ int fmap_row(int mb, int r) {
 
 // W'' A-operand fragments in the store order above and b'' (natural order)
 // into LDS, cooperatively (NT threads, loads in flight in batches).
-template <typename T, typename To, int M, int NT>
+template <typename T, typename To, int M, int NT, int KN>
 __device__ __forceinline__ void fill_w_afrags_perm(typename Mma<T>::frag (*WA)[2][64], float *bq,
                                                    const float *__restrict__ Wh,
                                                    const float *__restrict__ bh, float ws,
-                                                   float bs) {
+                                                   float bs, int Mr, float keps) {
   constexpr int N = (M / 16) * 2 * 64;
   constexpr int NB = (N / NT) < 4 ? (N / NT) : 4;   // loads in flight per batch
   static_assert(N % (NT * NB) == 0, "thread count");
@@ -46,7 +46,12 @@ __device__ __forceinline__ void fill_w_afrags_perm(typename Mma<T>::frag (*WA)[2
     for (int it = 0; it < NB; ++it) {
       const int idx = (it0 + it) * NT + threadIdx.x;
       const int m = fmap_row<To>(idx >> 7, idx & 15);
-      load8_f32(Wh + (size_t)m * kD + ((idx >> 6) & 1) * 32 + 8 * ((idx & 63) >> 4), v[it]);
+      if (m < Mr) {   // W'' rows past the M_r drawn are zero
+        load8_f32(Wh + (size_t)m * kD + ((idx >> 6) & 1) * 32 + 8 * ((idx & 63) >> 4), v[it]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[it][i] = 0.f;
+      }
     }
 #pragma unroll
     for (int it = 0; it < NB; ++it) {
@@ -54,19 +59,21 @@ __device__ __forceinline__ void fill_w_afrags_perm(typename Mma<T>::frag (*WA)[2
       WA[idx >> 7][(idx >> 6) & 1][idx & 63] = Mma<T>::from_f32(v[it], ws);
     }
   }
-  if (threadIdx.x < M) bq[threadIdx.x] = bh[threadIdx.x] * bs;
+  if (threadIdx.x < M) bq[threadIdx.x] = seed_row<KN>(threadIdx.x, Mr, bh, bs, keps);
 }
 
 // The four result tiles of 64 features for one row: bf16 lanes hold features
 // 8 g .. 8 g + 7 (tiles 0, 1) and 32 + 8 g .. (tiles 2, 3) of the 64; fp32 lanes
-// hold 16 k + 4 g .. 16 k + 4 g + 3 in tile k.
-__device__ __forceinline__ void store_row64(bf16 *p, int g, const f32x4 (&v)[4]) {
-  store8(p + 8 * g, v[0], v[1]);
-  store8(p + 32 + 8 * g, v[2], v[3]);
+// hold 16 k + 4 g .. 16 k + 4 g + 3 in tile k. Only the first nv features of the
+// 64 are stored (nv a multiple of 16: each store is all in or all out).
+__device__ __forceinline__ void store_row64(bf16 *p, int g, const f32x4 (&v)[4], int nv) {
+  if (nv >= 64 || 8 * g < nv) store8(p + 8 * g, v[0], v[1]);
+  if (nv >= 64 || 32 + 8 * g < nv) store8(p + 32 + 8 * g, v[2], v[3]);
 }
-__device__ __forceinline__ void store_row64(float *p, int g, const f32x4 (&v)[4]) {
+__device__ __forceinline__ void store_row64(float *p, int g, const f32x4 (&v)[4], int nv) {
 #pragma unroll
-  for (int k = 0; k < 4; ++k) *reinterpret_cast<f32x4 *>(p + 16 * k + 4 * g) = v[k];
+  for (int k = 0; k < 4; ++k)
+    if (nv >= 64 || 16 * k + 4 * g < nv) *reinterpret_cast<f32x4 *>(p + 16 * k + 4 * g) = v[k];
 }
 
 // Persistent: workgroup i takes an XCD-local range of (head, row tile) items,
@@ -78,7 +85,7 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
                                                      const float *__restrict__ bph,
                                                      To *__restrict__ Xp, int H, int L, float s,
                                                      int ntiles, int nitems, float ws, float bs,
-                                                     float keps) {
+                                                     float keps, int Mr, float cM) {
   constexpr int TBW = FmapCfg<T>::TBW;
   using P = Mma<T>;
   using frag = typename P::frag;
@@ -90,7 +97,6 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
-  const float cM = sqrtf(2.0f / M);
   const float s2half = 0.5f * s * s;
 
   int begin, end;
@@ -123,8 +129,8 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
     if (bh != cur) {   // the head's W'' fragments and b''
       const int h = bh % H;
       __syncthreads();
-      fill_w_afrags_perm<T, To, M, kFmapThreads>(WA, bq, W + (size_t)h * M * kD,
-                                                 bph + (size_t)h * M, ws, bs);
+      fill_w_afrags_perm<T, To, M, kFmapThreads, KN>(WA, bq, W + (size_t)h * Mr * kD,
+                                                     bph + (size_t)h * Mr, ws, bs, Mr, keps);
       __syncthreads();
       cur = bh;
     }
@@ -156,8 +162,8 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
     }
 
     const int rbase = (item - bh * ntiles) * (kFmapThreads / 4 * TBW) + w * (16 * TBW);
-    To *Oh = Xp + (size_t)bh * L * M;
-    for (int q = 0; q < M / 64; ++q) {   // features 64 q .. 64 q + 63
+    To *Oh = Xp + (size_t)bh * L * Mr;   // rows of M_r features
+    for (int q = 0; q < M / 64; ++q) {   // features 64 q .. 64 q + 63 (stored: < M_r)
       frag a[4][2];
       f32x4 bcv[4];   // b'' of result rows 4 g + j of tile k (in store order)
 #pragma unroll
@@ -175,10 +181,15 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
           f32x4 p = P::mma(a[k][0], xf[tb][0], bcv[k]);
           p = P::mma(a[k][1], xf[tb][1], p);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[k][j] = feature<KN, P>(p[j], keps) * dfac[tb];
+          for (int j = 0; j < 4; ++j) v[k][j] = feature<KN, P>(p[j], bcv[k][j]) * dfac[tb];
         }
         const int t = rbase + tb * 16 + c16;
-        if (t < L) store_row64(Oh + (size_t)t * M + 64 * q, g, v);
+        if (t < L) {
+          if (Mr == M)   // every tile whole: the stores need no feature mask
+            store_row64(Oh + (size_t)t * M + 64 * q, g, v, 64);
+          else
+            store_row64(Oh + (size_t)t * Mr + 64 * q, g, v, Mr - 64 * q);
+        }
       }
     }
   }
@@ -197,7 +208,7 @@ static hipError_t fmap_typed(const Shape &sh, const void *X, const float *W, con
 #define FAVOR_FMAP_LAUNCH(MM)                                                               \
   hipLaunchKernelGGL((k_feature_map<T, To, MM, KN>), grid, dim3(kFmapThreads), 0, st,        \
                      (const T *)X, W, b, (To *)Xp, sh.H, sh.L, sh.s, ntiles, nitems, ws, bs, \
-                     sh.keps)
+                     sh.keps, sh.Mr, feature_norm(sh))
   switch (sh.M) {
     case 64: FAVOR_FMAP_LAUNCH(64); break;
     case 128: FAVOR_FMAP_LAUNCH(128); break;

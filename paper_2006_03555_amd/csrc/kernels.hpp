@@ -19,7 +19,8 @@ struct Shape {
   int BH;        // B * H
   int H;         // heads (W and b are per head)
   int L;
-  int M;
+  int M;         // rows the kernels work on: 64, 128 or 256 (M_r rounded up)
+  int Mr;        // features drawn (a multiple of 16); rows M_r .. M - 1 are padding
   float s;       // input scale
   float eps;     // denominator stabiliser
   int kernel;    // 0 Gaussian-kernel (cos) features, 1 ReLU features
@@ -30,9 +31,13 @@ struct Shape {
 // Scales of the projection W'' = ws W and of its seed b'' = bs b for the
 // shape's feature kernel: cos takes revolutions (s / 2 pi, 1 / 2 pi); ReLU
 // features carry 1 / sqrt(M) and no phase.
+// sqrt(2 / M) of the cos features' D factor, for the M_r features drawn (a
+// kernel argument, so that it stays in a scalar register).
+inline float feature_norm(const Shape &sh) { return sqrtf(2.0f / (float)sh.Mr); }
+
 inline void feature_scales(const Shape &sh, float &ws, float &bs) {
   if (sh.kernel == 1) {
-    ws = sh.s / sqrtf((float)sh.M);
+    ws = sh.s / sqrtf((float)sh.Mr);
     bs = 0.f;
   } else {
     ws = sh.s * 0.15915494309189535f;

@@ -172,13 +172,13 @@ __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
 }
 
 // Key projection + features for one wave's MB m-blocks over token half sidx of
-// the staged tile: kf[mb][tbl][j] = cos(2 pi (W'' k_t + b'')) (ReLU features:
-// max(W'' k_t, 0) + keps) for token t = 32 sidx + 16 tbl + 4 g + j and feature
+// the staged tile: kf[mb][tbl][j] = feature(W'' k_t + b'') (bC: the seeds b'' of
+// the lane's feature) for token t = 32 sidx + 16 tbl + 4 g + j and feature
 // m = m0 + 16 mb + (lane % 16).
 template <typename T, int MB, int KN>
 __device__ __forceinline__ void key_features(const KVTile<T> &tl,
                                              const typename Mma<T>::frag (&Wf)[MB][2],
-                                             const f32x4 (&bC)[MB], int sidx, float keps,
+                                             const f32x4 (&bC)[MB], int sidx,
                                              f32x4 (&kf)[MB][2]) {
   using P = Mma<T>;
   const int l = lane_id();
@@ -194,7 +194,7 @@ __device__ __forceinline__ void key_features(const KVTile<T> &tl,
       f32x4 p = P::mma(a0, Wf[mb][0], bC[mb]);
       p = P::mma(a1, Wf[mb][1], p);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = feature<KN, P>(p[j], keps);
+      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = feature<KN, P>(p[j], bC[mb][j]);
     }
   }
 }
@@ -205,7 +205,7 @@ __device__ __forceinline__ void key_features(const KVTile<T> &tl,
 template <typename T, int MB, int KN>
 __device__ __forceinline__ void key_features_lds(const KVTile<T> &tl,
                                                  const typename Mma<T>::frag (*WA)[2][64],
-                                                 const float *bq, int mb0, int sidx, float keps,
+                                                 const float *bq, int mb0, int sidx,
                                                  f32x4 (&kf)[MB][2]) {
   using P = Mma<T>;
   const int l = lane_id();
@@ -230,7 +230,7 @@ __device__ __forceinline__ void key_features_lds(const KVTile<T> &tl,
       f32x4 p = P::mma(a0, wb[mb][0], bC[mb]);
       p = P::mma(a1, wb[mb][1], p);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = feature<KN, P>(p[j], keps);
+      for (int j = 0; j < 4; ++j) kf[mb][tbl][j] = feature<KN, P>(p[j], bC[mb][j]);
     }
   }
 }

@@ -60,6 +60,10 @@ def _desc(**kw):
     (dict(d=0), 1),
     (dict(d=32), 2),
     (dict(M=100), 2),
+    (dict(M=272), 2),
+    (dict(M=48), 0),
+    (dict(M=16), 0),
+    (dict(M=208), 0),
     (dict(M=0), 1),
     (dict(in_dtype=7), 1),
     (dict(out_dtype=-1), 1),
@@ -157,6 +161,10 @@ def test_workspace_size():
     assert nboth > nc and nboth % 256 == 0
     assert fv.workspace_size(_desc(L=0), 0) == 0
     assert fv.workspace_size(_desc(M=100), 0) == 0
+    # M is padded to the kernels' 64, 128 or 256 rows inside the workspace
+    for op in (0, 1, 2):
+        assert fv.workspace_size(_desc(M=48), op) == fv.workspace_size(_desc(M=64), op)
+        assert fv.workspace_size(_desc(M=144), op) == fv.workspace_size(_desc(M=256), op)
     # causal segment length is honoured: more segments need more workspace
     assert fv.workspace_size(_desc(chunk=128), 1) > fv.workspace_size(_desc(chunk=512), 1)
 

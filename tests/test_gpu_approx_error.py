@@ -30,7 +30,7 @@ pytestmark = pytest.mark.gpu
 
 L, D, DP = 4096, 16, 64
 S = D ** -0.25
-MS = (64, 128, 256)
+MS = (16, 32, 64, 128, 256)
 SAMPLES = int(os.environ.get("FAVOR_APPROX_SAMPLES", "3"))
 
 
