@@ -21,9 +21,10 @@
  *   state          [B][H][M][d+1] float, column d holds sum_j K'_j (the "1" column)
  * One draw (W, b) per head is shared by every batch entry.
  *
- * Supported: d = 64; M a multiple of 16 from 16 to 256 (causal with F32 inputs:
- * M <= 128; the kernels work on M rounded up to 64, 128 or 256 rows, the rows
- * past M being padding whose features are zero, so every array above keeps M);
+ * Supported: d = 64; M a multiple of 16 from 16 to 256 (the kernels work on M
+ * rounded up to 64, 128 or 256 rows, the rows past M being padding whose
+ * features are zero, so every array above keeps M; the causal scan with F32
+ * inputs and M > 128 runs as two passes over the feature halves);
  * L >= 0 (any length, ragged tails handled; L = 0 is a no-op); B, H >= 0,
  * B*H <= 65535; in_dtype F32 or BF16; out_dtype F32 or BF16. F32 inputs use
  * fp32 matrix cores and an accurately rounded cosine; BF16 inputs use bf16

@@ -119,15 +119,22 @@ struct CausalSmem {
 
 // SAVE: also write each row's 1 / (D-hat + eps) in units of the unscaled
 // features (rsave [B*H][L]) for the backward pass.
-template <typename T, typename To, int M, int KN, bool RN, bool SAVE>
+// PART: 0 all M features; 1 and 2 the features [m0, m0 + M) of Mall (the
+// head strides of W'', b'' and the prefix states): pass 1 stores each row's raw
+// numerators and denominator (halves [B*H][L][kHalfRow]), pass 2 adds its own
+// and finalises. Buf2 is a sum over features, so the two passes together give
+// the one-pass result; they let fp32 inputs take M = 256 on tables sized for 128.
+constexpr int kHalfRow = 68;   // 64 numerators, the denominator, padding to 16 bytes
+template <typename T, typename To, int M, int KN, bool RN, bool SAVE, int PART>
 __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T *__restrict__ K,
                                                 const T *__restrict__ V,
                                                 const typename Mma<T>::frag *__restrict__ wfr,
                                                 const float *__restrict__ bqg,
                                                 const float *__restrict__ prefix,
                                                 To *__restrict__ out, float *__restrict__ rsave,
-                                                int H, int L, int seg_len, int nseg, float s,
-                                                float eps, float cM) {
+                                                float *__restrict__ halves, int H, int L,
+                                                int seg_len, int nseg, float s, float eps,
+                                                float cM, int Mall, int m0) {
   constexpr int MW = M / 4;
   constexpr int MB = MW / 16;
   constexpr int NS = M / 32;
@@ -145,9 +152,9 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
   const int g = l >> 4;
   const int c16 = l & 15;
 
-  const frag *wh = wfr + (size_t)h * (M / 16) * 2 * 64;
+  const frag *wh = wfr + ((size_t)h * (Mall / 16) + m0 / 16) * 2 * 64;
   copy_frags<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wh);
-  if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
+  if (tid < M) sm.bq[tid] = bqg[(size_t)h * Mall + m0 + tid];
   if (w == 0) {
     sm.SEL[0][l] = select_frag<T>(0);
     sm.SEL[1][l] = select_frag<T>(1);
@@ -159,7 +166,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
   // holds the ones column replicated over its 16 columns)
   f32x4 accS[MB][5];
   {
-    const float *pre = prefix + ((size_t)bh * nseg + seg) * M * 65;
+    const float *pre = prefix + (((size_t)bh * nseg + seg) * Mall + m0) * 65;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -346,11 +353,26 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
       o[4] = P::mma(tl.DF[sp][g], pb, o[4]);
     }
     if (qt < r1) {
-      const float inv = RN ? 1.0f / (o[4][0] + epsq) : epsq;
+      float *hp = halves + ((size_t)bh * L + qt) * kHalfRow;
+      if constexpr (PART == 1) {   // raw partials of the first feature half
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) store4(Oh + (size_t)qt * kD + nb * 16 + 4 * g, o[nb] * inv);
-      if constexpr (SAVE) {
-        if (g == 0) rsave[(size_t)bh * L + qt] = inv;
+        for (int nb = 0; nb < 4; ++nb)
+          *reinterpret_cast<f32x4 *>(hp + nb * 16 + 4 * g) = o[nb];
+        if (g == 0) hp[64] = o[4][0];
+      } else {
+        if constexpr (PART == 2) {
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb)
+            o[nb] += *reinterpret_cast<const f32x4 *>(hp + nb * 16 + 4 * g);
+          o[4][0] += hp[64];
+        }
+        const float inv = RN ? 1.0f / (o[4][0] + epsq) : epsq;
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb)
+          store4(Oh + (size_t)qt * kD + nb * 16 + 4 * g, o[nb] * inv);
+        if constexpr (SAVE) {
+          if (g == 0) rsave[(size_t)bh * L + qt] = inv;
+        }
       }
     }
     __syncthreads();
@@ -855,11 +877,13 @@ static hipError_t causal_fs_typed(const Shape &sh, const void *Q, const void *K,
   });
 }
 
-// fp32 inputs (M <= 128).
+// fp32 inputs: M <= 128 in one pass, M = 256 in two passes over the feature
+// halves (the raw partials of the first in halves [BH][L][kHalfRow]).
 template <typename T, typename To, bool SAVE = false>
 static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, const void *V,
                                const void *wfr, const float *bq, const float *prefix, void *o,
-                               int seg_len, int nseg, hipStream_t st, float *rsave = nullptr) {
+                               int seg_len, int nseg, hipStream_t st, float *halves,
+                               float *rsave = nullptr) {
   dim3 grid(nseg * sh.BH);
   return with_variant(sh, [&](auto kn, auto rn) -> hipError_t {
     constexpr int KN = decltype(kn)::value;
@@ -867,14 +891,19 @@ static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, co
     if constexpr (SAVE && !RN) {
       return hipErrorInvalidValue;
     } else {
-#define FAVOR_CAUSAL_LAUNCH(MM)                                                             \
-  hipLaunchKernelGGL((k_causal<T, To, MM, KN, RN, SAVE>), grid, dim3(256), 0, st,             \
+#define FAVOR_CAUSAL_LAUNCH(MM, PART, M0)                                                   \
+  hipLaunchKernelGGL((k_causal<T, To, MM, KN, RN, SAVE, PART>), grid, dim3(256), 0, st,       \
                      (const T *)Q, (const T *)K, (const T *)V,                                 \
-                     (const typename Mma<T>::frag *)wfr, bq, prefix, (To *)o, rsave, sh.H,     \
-                     sh.L, seg_len, nseg, sh.s, sh.eps, feature_norm(sh))
+                     (const typename Mma<T>::frag *)wfr, bq, prefix, (To *)o, rsave, halves,   \
+                     sh.H, sh.L, seg_len, nseg, sh.s, sh.eps, feature_norm(sh), sh.M, M0)
       switch (sh.M) {
-        case 64: FAVOR_CAUSAL_LAUNCH(64); break;
-        case 128: FAVOR_CAUSAL_LAUNCH(128); break;
+        case 64: FAVOR_CAUSAL_LAUNCH(64, 0, 0); break;
+        case 128: FAVOR_CAUSAL_LAUNCH(128, 0, 0); break;
+        case 256:
+          if (!halves) return hipErrorInvalidValue;
+          FAVOR_CAUSAL_LAUNCH(128, 1, 0);
+          FAVOR_CAUSAL_LAUNCH(128, 2, 128);
+          break;
         default: return hipErrorInvalidValue;
       }
 #undef FAVOR_CAUSAL_LAUNCH
@@ -886,24 +915,25 @@ static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, co
 hipError_t launch_causal_save(const Shape &sh, Dt in, const void *Q, const void *K,
                               const void *V, const void *wfr, const float *bq,
                               const float *prefix, void *o, float *rsave, int seg_len, int nseg,
-                              hipStream_t st) {
+                              float *halves, hipStream_t st) {
   if (!sh.renorm) return hipErrorInvalidValue;
   if (in == Dt::BF16)
     return causal_fs_typed<bf16, true>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st, rsave);
   return causal_typed<float, float, true>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st,
-                                          rsave);
+                                          halves, rsave);
 }
 
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,
                          const void *V, const void *wfr, const float *bq, const float *prefix,
-                         void *o, int seg_len, int nseg, hipStream_t st) {
+                         void *o, int seg_len, int nseg, float *halves, hipStream_t st) {
   if (in == Dt::BF16)
     return out == Dt::BF16
                ? causal_fs_typed<bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st)
                : causal_fs_typed<float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st);
-  return out == Dt::BF16
-             ? causal_typed<float, bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st)
-             : causal_typed<float, float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len, nseg, st);
+  return out == Dt::BF16 ? causal_typed<float, bf16>(sh, Q, K, V, wfr, bq, prefix, o, seg_len,
+                                                     nseg, st, halves)
+                         : causal_typed<float, float>(sh, Q, K, V, wfr, bq, prefix, o, seg_len,
+                                                      nseg, st, halves);
 }
 
 }  // namespace favor

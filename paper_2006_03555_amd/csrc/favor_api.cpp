@@ -84,8 +84,6 @@ favor_status validate(const favor_desc *g, int op) {
                 g->M);
   const long long bh = (long long)g->B * g->H;
   if (bh > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "B*H=%lld exceeds 65535", bh);
-  if ((op == kOpCausal || op == kOpBoth) && g->in_dtype == FAVOR_F32 && g->M > 128)
-    return fail(FAVOR_ERR_UNSUPPORTED, "causal with fp32 inputs supports M <= 128");
   if (op == kOpBidirBackward || op == kOpCausalBackward) {
     if (g->out_dtype != g->in_dtype)
       return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass needs out_dtype == in_dtype");
@@ -111,7 +109,8 @@ struct BwdPlan {
   size_t total = 0;
 };
 
-// Workspace: [ split partials | Buf1^T fragments (bidir, both) | W'' fragments | b'' ]
+// Workspace: [ split partials | Buf1^T fragments (bidir, both) | W'' fragments | b'' |
+//              feature-half partials (causal and both, fp32 inputs at M > 128) ]
 struct Plan {
   int BH = 0;
   int nsplit = 0;         // bidir: K-side splits; causal and both: segments
@@ -120,6 +119,7 @@ struct Plan {
   size_t frag_bytes = 0;  // bidir and both
   size_t wfr_bytes = 0;
   size_t bq_bytes = 0;
+  size_t half_bytes = 0;  // [BH][L][68] fp32: the first feature half's raw row results
   size_t total = 0;
 };
 
@@ -152,7 +152,9 @@ Plan make_plan(const favor_desc *g, int op) {
   if (op != kOpCausal) p.frag_bytes = round_up((size_t)p.BH * 5 * (M / 32) * 64 * fb, 256);
   p.wfr_bytes = round_up((size_t)g->H * (M / 16) * 2 * 64 * fb, 256);
   p.bq_bytes = round_up((size_t)g->H * M * sizeof(float), 256);
-  p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes;
+  if (causal && g->in_dtype == FAVOR_F32 && M > 128)
+    p.half_bytes = round_up((size_t)p.BH * g->L * 68 * sizeof(float), 256);
+  p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes + p.half_bytes;
   return p;
 }
 
@@ -392,6 +394,9 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
   float *part = static_cast<float *>(ws);
   void *wfr = static_cast<char *>(ws) + p.part_bytes;
   float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
+  float *halves = p.half_bytes ? reinterpret_cast<float *>(reinterpret_cast<char *>(bq) +
+                                                           p.bq_bytes)
+                               : nullptr;
   hipError_t e;
   {
     favor::LaunchTimer t(favor::kKerKside, st);
@@ -407,10 +412,10 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
     favor::LaunchTimer t(favor::kKerCausal, st);
     if (row_scale && sh.renorm)
       e = favor::launch_causal_save(sh, in, Q, K, V, wfr, bq, part, out, row_scale,
-                                    p.rows_per_split, p.nsplit, st);
+                                    p.rows_per_split, p.nsplit, halves, st);
     else
       e = favor::launch_causal(sh, in, dt_of(g->out_dtype), Q, K, V, wfr, bq, part, out,
-                               p.rows_per_split, p.nsplit, st);
+                               p.rows_per_split, p.nsplit, halves, st);
   }
   return device_result(e, "favor_attn_causal chunk scan");
 }
@@ -461,6 +466,9 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
   void *frags = static_cast<char *>(ws) + p.part_bytes;
   void *wfr = static_cast<char *>(frags) + p.frag_bytes;
   float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
+  float *halves = p.half_bytes ? reinterpret_cast<float *>(reinterpret_cast<char *>(bq) +
+                                                           p.bq_bytes)
+                               : nullptr;
   hipError_t e;
   {
     favor::LaunchTimer t(favor::kKerKside, st);
@@ -485,10 +493,10 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
     favor::LaunchTimer t(favor::kKerCausal, st);
     if (row_scale_causal && sh.renorm)
       e = favor::launch_causal_save(sh, in, Q, K, V, wfr, bq, part, out_causal,
-                                    row_scale_causal, p.rows_per_split, p.nsplit, st);
+                                    row_scale_causal, p.rows_per_split, p.nsplit, halves, st);
     else
       e = favor::launch_causal(sh, in, out, Q, K, V, wfr, bq, part, out_causal,
-                               p.rows_per_split, p.nsplit, st);
+                               p.rows_per_split, p.nsplit, halves, st);
   }
   return device_result(e, "favor_attn_both chunk scan");
 }
@@ -676,7 +684,7 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
   if (sh.renorm && !saved) {
     favor::LaunchTimer t(favor::kKerCausal, st);
     e = favor::launch_causal_save(sh, in, Q, K, V, w.wfr, w.bq, w.part, w.out, w.rsave,
-                                  p.rows_per_split, p.nsplit, st);
+                                  p.rows_per_split, p.nsplit, nullptr, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward forward pass");
   favor::BwdArgs a{Q,  K,  V,  dout, saved ? out_fwd : w.out, saved ? row_scale : w.rsave,

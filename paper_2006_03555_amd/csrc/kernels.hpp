@@ -87,7 +87,7 @@ hipError_t launch_qside_save(const Shape &sh, Dt in, const void *Q, const void *
 hipError_t launch_causal_save(const Shape &sh, Dt in, const void *Q, const void *K,
                               const void *V, const void *wfr, const float *bq,
                               const float *prefix, void *o, float *rsave, int seg_len, int nseg,
-                              hipStream_t st);
+                              float *halves, hipStream_t st);
 
 // Backward pass. k_kside's weighted mode: part [BH][nsplit][M][65] = sum over
 // each row range of Q-hat_t^T [aux_t.x dout_t, aux_t.y].
@@ -117,10 +117,12 @@ hipError_t launch_sum_splits(const Shape &sh, const float *part, int ns, float *
 hipError_t launch_suffix_scan(const Shape &sh, float *part, int nch, const float *dsout,
                               float *dsin, hipStream_t st);
 
-// Causal chunk scan of each segment starting from its prefix state.
+// Causal chunk scan of each segment starting from its prefix state. halves:
+// [BH][L][68] fp32 scratch for fp32 inputs at M = 256 (two feature-half
+// passes), else unused (may be null).
 hipError_t launch_causal(const Shape &sh, Dt in, Dt out, const void *Q, const void *K,
                          const void *V, const void *wfr, const float *bq, const float *prefix,
-                         void *o, int seg_len, int nseg, hipStream_t st);
+                         void *o, int seg_len, int nseg, float *halves, hipStream_t st);
 
 }  // namespace favor
 

@@ -87,13 +87,20 @@ def test_validate_desc(kw, status):
             assert fv.last_error() != ""
 
 
-def test_fp32_causal_limits_m():
+def test_fp32_causal_takes_every_m():
+    """fp32 causal at M > 128 runs as two feature-half passes, which need a
+    [B*H][L][68] fp32 area of workspace more than M = 128."""
     g = _desc(in_dtype=fv.F32, out_dtype=fv.F32, M=256)
-    assert fv.validate_desc(g, fv.OP_CAUSAL) == 2
-    assert fv.validate_desc(g, fv.OP_BOTH) == 2
-    assert fv.validate_desc(g, fv.OP_BIDIR) == 0
+    for op in (fv.OP_CAUSAL, fv.OP_BOTH, fv.OP_BIDIR):
+        assert fv.validate_desc(g, op) == 0
     assert fv.validate_desc(g, 6) == 1
-    assert fv.validate_desc(_desc(in_dtype=fv.F32, M=128), fv.OP_CAUSAL) == 0
+    half = -(-2 * 4 * 1000 * 68 * 4 // 256) * 256
+    # bf16 at M = 256 runs in one pass; fp32 W'' fragments take 16 more bytes per lane
+    plain = fv.workspace_size(_desc(M=256), 1) + 4 * (256 // 16) * 2 * 64 * 16
+    for M in (144, 256):
+        n = fv.workspace_size(_desc(in_dtype=fv.F32, out_dtype=fv.F32, M=M), 1)
+        assert n == plain + half
+    assert fv.workspace_size(_desc(in_dtype=fv.F32, out_dtype=fv.F32, M=128), 1) < plain
 
 
 def test_backward_validation():

@@ -201,3 +201,54 @@ def test_backward_any_m(B, H, L, M, dtype, kernel, causal, seed):
     names = ("dQ", "dK", "dV")
     _check_all(dict(zip(names, (to_host(x) for x in got[:3]))), dict(zip(names, ref[:3])),
                dtype)
+
+
+# fp32 inputs at M > 128: the causal scan runs as two passes over the feature
+# halves (the first stores each row's raw numerators and denominator)
+FP32_CAUSAL_CASES = [
+    # B, H, L, M, kernel, renormalize, denom_eps, chunk
+    (1, 2, 700, 256, SOFTMAX, True, 0.0, 0),
+    (2, 1, 1100, 208, RELU, True, 0.0, 256),
+    (1, 2, 333, 256, SOFTMAX, False, 0.0, 0),
+    (1, 1, 513, 144, SOFTMAX, True, 0.4, 128),
+]
+
+
+@pytest.mark.parametrize("B,H,L,M,kernel,renorm,eps,chunk", FP32_CAUSAL_CASES)
+def test_fp32_causal_feature_halves(B, H, L, M, kernel, renorm, eps, chunk):
+    import torch
+    fv = _fv()
+    Q, K, V = _qkv(B, H, L, "f32", seed=L + M)
+    W, b = _features(M + 11, H, M)
+    Qe, Ke, Ve = _qkv(B, H, 90, "f32", seed=M + 3)
+    _, S0 = favor.attn_causal(Qe, Ke, Ve, W, b, S64, kernel=kernel)
+    S0 = S0.astype(np.float32)
+    kw = dict(denom_eps=eps, kernel=kernel, renormalize=renorm, chunk=chunk)
+    out, st = fv.attn_causal(to_dev(Q), to_dev(K), to_dev(V), to_dev(W), to_dev(b), S64,
+                             state_in=to_dev(S0), return_state=True, **kw)
+    torch.cuda.synchronize()
+    parity(to_host(out), Q, K, V, W, b, S64, True, "f32", eps=eps, state_in=S0, kernel=kernel,
+           renormalize=renorm)
+    _, ref_state = favor.attn_causal(Q, K, V, W, b, S64, state_in=S0, kernel=kernel)
+    assert np.max(np.abs(to_host(st) - ref_state)) <= 1e-4 * np.max(np.abs(ref_state))
+
+
+def test_fp32_both_directions_feature_halves_and_saved_scales():
+    """attn_both at fp32 M = 256: both outputs against the oracle, and the
+    causal row scales written by the second pass equal the oracle's."""
+    import torch
+    from test_gpu_backward import _expected_row_scale
+    fv = _fv()
+    B, H, L, M = 1, 2, 900, 256
+    Q, K, V = _qkv(B, H, L, "f32", seed=77)
+    W, b = _features(78, H, M)
+    rb = torch.empty((B, H, L), device="cuda")
+    rc = torch.empty((B, H, L), device="cuda")
+    ob, oc = fv.attn_both(to_dev(Q), to_dev(K), to_dev(V), to_dev(W), to_dev(b), S64,
+                          row_scale_bidir=rb, row_scale_causal=rc)
+    torch.cuda.synchronize()
+    parity(to_host(ob), Q, K, V, W, b, S64, False, "f32")
+    parity(to_host(oc), Q, K, V, W, b, S64, True, "f32")
+    for causal, r in ((False, rb), (True, rc)):
+        want = _expected_row_scale(Q, K, W, b, M, SOFTMAX, 0.0, causal)
+        assert np.max(np.abs(to_host(r) - want) / np.abs(want)) <= 1e-4
