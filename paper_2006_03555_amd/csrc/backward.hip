@@ -189,14 +189,7 @@ __device__ __forceinline__ void load_rows64(typename Mma<T>::frag (&f)[2], const
 
 template <typename T>
 __device__ __forceinline__ float sq_norm16(const typename Mma<T>::frag (&f)[2]) {
-  float n = 0.f;
-#pragma unroll
-  for (int k = 0; k < 2; ++k)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float x = to_f32(f[k][i]);
-      n = fmaf(x, x, n);
-    }
+  float n = sq_sum16(f);
   n += __shfl_xor(n, 16);
   n += __shfl_xor(n, 32);
   return n;

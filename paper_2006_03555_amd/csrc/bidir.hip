@@ -366,14 +366,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 2 : 1) void k_qside(const T *
     for (int tb = 0; tb < TBW; ++tb) {
       epsq[tb] = FIN == kFinDiv ? 0.f : FIN == kFinDivEps ? eps : 1.f;
       if constexpr (KN == kCos && FIN != kFinDiv) {
-        float nrm = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const float x = to_f32(qf[tb][ks][i]);
-            nrm = fmaf(x, x, nrm);
-          }
+        float nrm = sq_sum16(qf[tb]);
         nrm += __shfl_xor(nrm, 16);
         nrm += __shfl_xor(nrm, 32);
         // features here omit D_Q sqrt(2/M); the stabiliser is divided by it instead

@@ -257,14 +257,7 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
     // off) the factor D_Q sqrt(2/M) they omit; ReLU features carry their scale
     float epsq = RN ? (KN == kCos ? 0.f : eps) : 1.f;
     if (KN == kCos && (!RN || eps != 0.f)) {
-      float nrm = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float x = to_f32(qf[ks][i]);
-          nrm = fmaf(x, x, nrm);
-        }
+      float nrm = sq_sum16(qf);
       nrm += __shfl_xor(nrm, 16);
       nrm += __shfl_xor(nrm, 32);
       const float dq = cM * expf(s2half * nrm);
@@ -476,15 +469,7 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
   store_frag<bf16>(&tl.Qs[tr][cq + 8], q[1]);
   float Dt = (t0 + tr < r1) ? 1.f : 0.f;
   if constexpr (KN == kCos) {
-    float nrm = 0.f;
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float x = to_f32(r.k[hh][i]);
-        nrm = fmaf(x, x, nrm);
-      }
-    nrm = quad_sum_f32(nrm);
+    float nrm = quad_sum_f32(sq_sum16(r.k));
     Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
   }
   float Dj[4];   // D of tokens 16 w + 4 g + j, held by the quad of lanes 16 g + 4 j
@@ -509,15 +494,7 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
     for (int j = 0; j < 4; ++j) p[j] = (bf16)Dj[j];
   }
   if (KN == kCos && (!RN || eps != 0.f)) {
-    float qn = 0.f;
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float x = to_f32(q[hh][i]);
-        qn = fmaf(x, x, qn);
-      }
-    qn = quad_sum_f32(qn);
+    const float qn = quad_sum_f32(sq_sum16(q));
     const float dq = cM * expf(s2half * qn);
     if ((tid & 3) == 0) tl.epsq[tr] = (t0 + tr < r1) ? (RN ? eps / dq : dq) : 0.f;
   }

@@ -104,6 +104,30 @@ template <> struct Mma<float> {
 // ---- element conversions ---------------------------------------------------
 __device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
 __device__ __forceinline__ float to_f32(float v) { return v; }
+
+// Sum of squares of the 16 values of two fragments (a lane's share of a row):
+// bf16 pairs go through the dot2 instruction (two exact products and an fp32
+// sum per instruction, no conversions); fp32 values through fused multiply-adds.
+__device__ __forceinline__ float sq_sum16(const bf16x8 (&f)[2]) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  struct Pairs { bf16x2 p[4]; };
+  float n = 0.f;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const Pairs q = __builtin_bit_cast(Pairs, f[k]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) n = __builtin_amdgcn_fdot2_f32_bf16(q.p[i], q.p[i], n, false);
+  }
+  return n;
+}
+__device__ __forceinline__ float sq_sum16(const f32x8 (&f)[2]) {
+  float n = 0.f;
+#pragma unroll
+  for (int k = 0; k < 2; ++k)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) n = fmaf(f[k][i], f[k][i], n);
+  return n;
+}
 template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }

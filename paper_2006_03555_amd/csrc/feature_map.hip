@@ -148,14 +148,7 @@ __global__ __launch_bounds__(kFmapThreads, 1) void k_feature_map(const T *__rest
     for (int tb = 0; tb < TBW; ++tb) {
       dfac[tb] = 1.f;
       if constexpr (KN == kRelu) continue;
-      float nrm = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float x = to_f32(xf[tb][ks][i]);
-          nrm = fmaf(x, x, nrm);
-        }
+      float nrm = sq_sum16(xf[tb]);
       nrm += __shfl_xor(nrm, 16);
       nrm += __shfl_xor(nrm, 32);
       dfac[tb] = cM * expf(s2half * nrm);

@@ -156,14 +156,7 @@ __device__ __forceinline__ void stage_tile(KVTile<T> &tl, const TileRegs<T> &r,
   const int tr = tid >> 2;
   float Dt = (t0 + tr < r1) ? 1.f : 0.f;
   if constexpr (KN == kCos) {
-    float nrm = 0.f;
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float x = to_f32(r.k[h][i]);
-        nrm = fmaf(x, x, nrm);
-      }
+    float nrm = sq_sum16(r.k);
     nrm += __shfl_xor(nrm, 1);
     nrm += __shfl_xor(nrm, 2);
     Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
