@@ -23,9 +23,10 @@ per-kernel durations and the roofline entry for the dominant
 kernel. The line also carries the fp64 CPU oracle timed on this host
 (cpu_baseline), and under "variants" the same step with generalized attention
 (ReLU features) and with the renormalisation off, the draw alone for every kind
-of random features, the backward pass of the step's attention, and the training
-step (forward saving the row scales, then the backward reading them), timed the
-same way.
+of random features, one GPU's share of a causal pass sharded eight ways along
+the sequence (the last L/8 tokens from a carried state), the backward pass of
+the step's attention, and the training step (forward saving the row scales,
+then the backward reading them), timed the same way.
 """
 import argparse
 import json
@@ -164,7 +165,8 @@ def main():
                     help="skip the ReLU, unnormalised and backward variants (profiler runs "
                          "that average counters over every launch of a kernel)")
     ap.add_argument("--variants",
-                    default="relu,softmax_no_renormalize,draws,backward,train_step",
+                    default="relu,softmax_no_renormalize,draws,causal_shard,backward,"
+                            "train_step",
                     help="comma-separated variants to time after the headline step")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of the workload, time a plain device-to-device copy of this "
@@ -319,6 +321,44 @@ def main():
             "ms_per_step": ms_v, "value": w.B * w.H * w.L / (ms_v / 1e3),
             "ms_per_step_instrumented": ms_vi,
             "kernels": {k: {"ms_per_launch": v[0] / v[1]} for k, v in kv.items() if v[1] > 0}}
+
+    # one GPU's share of a causal pass sharded over 8 GPUs along the sequence: the
+    # last L/8 tokens, entered with the state the seven shards before it hand over
+    # (state_in non-zero; state_out is the hand-off to a next shard). The state is
+    # computed before the timed region; the step is the draw + the shard's pass.
+    if "causal_shard" in chosen and w.L % 8 == 0:
+        ls = w.L // 8
+        sl = slice(w.L - ls, w.L)
+        Qs, Ks, Vs = (x[:, :, sl].contiguous() for x in (Qd, Kd, Vd))
+        fv.orf_draw(999, H, M, w.d, W=Wd[1], b=bd[1], stream=s_main)
+        before = [x[:, :, :w.L - ls].contiguous() for x in (Qd, Kd, Vd)]
+        _, st_in = fv.attn_causal(*before, Wd[1], bd[1], s, return_state=True, stream=s_main)
+        del before
+        st_out = torch.empty_like(st_in)
+        out_s = torch.empty_like(Qs)
+        code = fv.BF16 if w.dtype == "bf16" else fv.F32
+        gs = fv.make_desc(w.B, H, ls, w.d, M, code, code, s)
+        ws_s = torch.empty(max(fv.workspace_size(gs, 1), 1), dtype=torch.uint8, device=dev)
+
+        def step_shard(i):
+            fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
+            fv.attn_causal(Qs, Ks, Vs, Wd[0], bd[0], s, state_in=st_in, state_out=st_out,
+                           out=out_s, workspace=ws_s, stream=s_main)
+
+        for i in range(args.warmup):
+            step_shard(first + i)
+        first += args.warmup
+        ms_sh = timed_region(step_shard, first)
+        first += args.steps
+        ms_shi = timed_region(step_shard, first, instrumented=True)
+        first += args.steps
+        ks = fv.timing_read()
+        variants["causal_shard"] = {
+            "ms_per_step": ms_sh, "value": w.B * w.H * ls / (ms_sh / 1e3),
+            "ms_per_step_instrumented": ms_shi,
+            "what": f"ORF draw + causal pass over tokens {w.L - ls}..{w.L - 1} (one GPU's share "
+                    "of 8 along the sequence) from the state of the tokens before them",
+            "kernels": {k: {"ms_per_launch": v[0] / v[1]} for k, v in ks.items() if v[1] > 0}}
 
     # the random-feature draw of the step (8 heads x M rows) for every kind of features
     if "draws" in chosen:
