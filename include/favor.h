@@ -205,9 +205,10 @@ FAVOR_API favor_status favor_attn_both(const favor_desc *g, const void *Q, const
  * then through the feature maps. The forward quantities are recomputed (nothing
  * from the forward call is needed); W and b receive no gradient.
  * dout, dQ, dK, dV: [B][H][L][d] in in_dtype; out_dtype must equal in_dtype
- * (FAVOR_ERR_UNSUPPORTED otherwise). fp32 inputs: M <= 128 (bidirectional),
- * M <= 64 (causal); bf16 inputs: every M. Deterministic (no
- * atomics). dQ, dK, dV are written in full (ragged tails included).
+ * (FAVOR_ERR_UNSUPPORTED otherwise). Every supported M; with fp32 inputs the
+ * gradient kernels take 128 (bidirectional) or 64 (causal) features at a time
+ * and add the slices' parts into dQ, dK, dV in a fixed order. Deterministic
+ * (no atomics). dQ, dK, dV are written in full (ragged tails included).
  * Workspace: favor_backward_workspace_size(g, causal) bytes, 256-byte aligned.
  * out and row_scale (both nullable, both or neither): the forward call's output
  * and row_scale for the same inputs, features and descriptor; given, the backward

@@ -279,7 +279,20 @@ __device__ __forceinline__ void query_grad(
 }
 
 // dQ row store: dQ = WT G + alpha s^2 (g~ . q-hat) q (cos features).
-template <typename T, int KN>
+// Store 8 consecutive values, or (ACC) add them to what dst holds: the fp32
+// gradients of a feature slice after the first (a gradient is a sum over
+// features, see the launchers).
+template <bool ACC, typename T>
+__device__ __forceinline__ void put8(T *p, f32x4 a, f32x4 b) {
+  if constexpr (ACC) {
+    static_assert(sizeof(T) == 4, "slices accumulate fp32 gradients");
+    a += *reinterpret_cast<const f32x4 *>(p);
+    b += *reinterpret_cast<const f32x4 *>(p + 4);
+  }
+  store8(p, a, b);
+}
+
+template <typename T, int KN, bool ACC = false>
 __device__ __forceinline__ void store_qgrad(T *dst, const f32x4 (&dacc)[4],
                                             const typename Mma<T>::frag (&qf)[2], float alpha,
                                             float dot2, float s) {
@@ -293,7 +306,7 @@ __device__ __forceinline__ void store_qgrad(T *dst, const f32x4 (&dacc)[4],
       lo[e] = fmaf(cx, to_f32(qf[pp][e]), dacc[2 * pp][e]);
       hi[e] = fmaf(cx, to_f32(qf[pp][4 + e]), dacc[2 * pp + 1][e]);
     }
-    store8(dst + 32 * pp + 8 * g, lo, hi);
+    put8<ACC>(dst + 32 * pp + 8 * g, lo, hi);
   }
 }
 
@@ -337,14 +350,13 @@ struct DqSmem {
 
 // Items are (head, tile of 8 waves x TBW x 16 rows), walked persistently over
 // XCD-local ranges; Buf1 [BH][M][65] fp32.
-template <typename T, int M, int KN, bool RN, int TBW>
+template <typename T, int M, int KN, bool RN, int TBW, bool ACC>
 __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
     const T *__restrict__ Q, const T *__restrict__ dout, const T *__restrict__ out,
     const float *__restrict__ rsave, const typename Mma<T>::frag *__restrict__ wfr,
     const float *__restrict__ bqg, const float *__restrict__ W, const float *__restrict__ buf1,
     T *__restrict__ dQ, float2 *__restrict__ aux, int H, int L, float s, int Mr, float cM,
-    float wts,
-    int ntiles, int nitems) {
+    int Mall, int m0, float wts, int ntiles, int nitems) {
   using frag = typename Mma<T>::frag;
   __shared__ DqSmem<T, M> sm;
   const int tid = threadIdx.x;
@@ -361,10 +373,10 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
     const int h = bh % H;
     if (bh != cur) {
       __syncthreads();
-      copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
-      if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-      build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
-      build_state_rows<T, M>(sm.SA, sm.sz, buf1 + (size_t)bh * M * 65);
+      copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + ((size_t)h * (Mall / 16) + m0 / 16) * 2 * 64);
+      if (tid < M) sm.bq[tid] = bqg[(size_t)h * Mall + m0 + tid];
+      build_wt<T, M>(sm.WT, W + ((size_t)h * Mr + m0) * kD, wts, Mr - m0);
+      build_state_rows<T, M>(sm.SA, sm.sz, buf1 + ((size_t)bh * Mall + m0) * 65);
       cur = bh;
       __syncthreads();
     }
@@ -385,7 +397,7 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dq(
       query_grad<T, M, KN, false>(sm.WA, sm.bq, sm.WT, sm.SA, sm.sz, nullptr, none, qf, df, alpha,
                                   ud, s, dacc, dot2);
       if (i < L) {
-        store_qgrad<T, KN>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
+        store_qgrad<T, KN, ACC>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
         if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
       }
     }
@@ -424,14 +436,14 @@ struct DqScanSmem {
 // in registers, publish S before each 64-token chunk and fold the chunk's
 // C~^T K-hat in after; the chunk's queries take S u plus the masked intra-chunk
 // terms.
-template <typename T, int M, int KN, bool RN>
+template <typename T, int M, int KN, bool RN, bool ACC>
 __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
     const T *__restrict__ Q, const T *__restrict__ K, const T *__restrict__ V,
     const T *__restrict__ dout, const T *__restrict__ out, const float *__restrict__ rsave,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ prefix, T *__restrict__ dQ,
     float2 *__restrict__ aux, int H, int L, int seg_len, int nseg, float s, int Mr, float cM,
-    float wts) {
+    int Mall, int m0, float wts) {
   using SP = ScanSplit<M>;
   constexpr int FB = SP::FB;
   using P = Mma<T>;
@@ -454,14 +466,14 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
   const int r0 = seg * seg_len;
   const int r1 = min(L, r0 + seg_len);
 
-  copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
-  if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-  build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
+  copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + ((size_t)h * (Mall / 16) + m0 / 16) * 2 * 64);
+  if (tid < M) sm.bq[tid] = bqg[(size_t)h * Mall + m0 + tid];
+  build_wt<T, M>(sm.WT, W + ((size_t)h * Mr + m0) * kD, wts, Mr - m0);
   // S^T slice: acc[nb][mb] rows = value column perm_col(nb, 4 g + j) (block 4: column
   // d replicated), lane = feature m = 16 (w FB + mb) + lane % 16
   f32x4 acc[5][FB];
   if (sw) {
-    const float *S = prefix + ((size_t)bh * nseg + seg) * M * 65;
+    const float *S = prefix + (((size_t)bh * nseg + seg) * Mall + m0) * 65;
 #pragma unroll
     for (int mb = 0; mb < FB; ++mb) {
       const float *row = S + (size_t)(16 * (w * FB + mb) + c16) * 65;
@@ -594,7 +606,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
         for (int j = 0; j < 4; ++j) dacc[k][j] += sm.red[qb][4 * k + j][l];
       dot2 += sm.red[qb][16][l];
       if (i < r1) {
-        store_qgrad<T, KN>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
+        store_qgrad<T, KN, ACC>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
         if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
       }
     }
@@ -691,7 +703,7 @@ __device__ __forceinline__ void key_grad(
 }
 
 // dK = D~ (WT G + s^2 (h . k-hat) k) (cos features), D~ (WT G) (ReLU); dV = D~ vacc.
-template <typename T, int KN>
+template <typename T, int KN, bool ACC = false>
 __device__ __forceinline__ void store_kgrad(T *dst, const f32x4 (&kacc)[4],
                                             const typename Mma<T>::frag (&kf)[2], float D,
                                             float doth, float s) {
@@ -705,15 +717,15 @@ __device__ __forceinline__ void store_kgrad(T *dst, const f32x4 (&kacc)[4],
       lo[e] = D * fmaf(cx, to_f32(kf[pp][e]), kacc[2 * pp][e]);
       hi[e] = D * fmaf(cx, to_f32(kf[pp][4 + e]), kacc[2 * pp + 1][e]);
     }
-    store8(dst + 32 * pp + 8 * g, lo, hi);
+    put8<ACC>(dst + 32 * pp + 8 * g, lo, hi);
   }
 }
-template <typename T>
+template <typename T, bool ACC = false>
 __device__ __forceinline__ void store_vgrad(T *dst, const f32x4 (&vacc)[4], float D) {
   const int g = lane_id() >> 4;
 #pragma unroll
   for (int pp = 0; pp < 2; ++pp)
-    store8(dst + 32 * pp + 8 * g, vacc[2 * pp] * D, vacc[2 * pp + 1] * D);
+    put8<ACC>(dst + 32 * pp + 8 * g, vacc[2 * pp] * D, vacc[2 * pp + 1] * D);
 }
 
 // ------------------------------------------------------------ bidirectional dK, dV
@@ -728,13 +740,13 @@ struct DkvSmem {
   frag RB[4][M / 32][64];   // dBuf1 value columns over features
 };
 
-template <typename T, int M, int KN, int TBW>
+template <typename T, int M, int KN, int TBW, bool ACC>
 __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dkv(
     const T *__restrict__ K, const T *__restrict__ V,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ dbuf1, T *__restrict__ dK,
-    T *__restrict__ dV, int H, int L, float s, int Mr, float cM, float wts, int ntiles,
-    int nitems) {
+    T *__restrict__ dV, int H, int L, float s, int Mr, float cM, int Mall, int m0, float wts,
+    int ntiles, int nitems) {
   using frag = typename Mma<T>::frag;
   __shared__ DkvSmem<T, M> sm;
   const int tid = threadIdx.x;
@@ -750,10 +762,10 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dkv(
     const int h = bh % H;
     if (bh != cur) {
       __syncthreads();
-      copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
-      if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-      build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
-      const float *Rs = dbuf1 + (size_t)bh * M * 65;
+      copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + ((size_t)h * (Mall / 16) + m0 / 16) * 2 * 64);
+      if (tid < M) sm.bq[tid] = bqg[(size_t)h * Mall + m0 + tid];
+      build_wt<T, M>(sm.WT, W + ((size_t)h * Mr + m0) * kD, wts, Mr - m0);
+      const float *Rs = dbuf1 + ((size_t)bh * Mall + m0) * 65;
       build_state_rows<T, M>(sm.RA, sm.rz, Rs);
       build_state_cols<T, M>(sm.RB, Rs);
       cur = bh;
@@ -776,8 +788,8 @@ __global__ __launch_bounds__(kBwdBidirThreads) void k_bwd_dkv(
                                             none, nullptr, nullptr, kf, vf, 0, kacc, doth,
                                             vacc);
       if (j < L) {
-        store_kgrad<T, KN>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
-        store_vgrad<T>(dV + ((size_t)bh * L + j) * kD, vacc, D);
+        store_kgrad<T, KN, ACC>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
+        store_vgrad<T, ACC>(dV + ((size_t)bh * L + j) * kD, vacc, D);
       }
     }
   }
@@ -808,13 +820,14 @@ struct DkvScanSmem {
 // m) for dK, as R (rows m, lanes = value columns) for dV. Each chunk publishes
 // R, then folds its own rows in; its keys take R plus the masked intra-chunk
 // terms.
-template <typename T, int M, int KN, bool KPART>
+template <typename T, int M, int KN, bool KPART, bool ACC>
 __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     const T *__restrict__ Q, const T *__restrict__ K, const T *__restrict__ V,
     const T *__restrict__ dout, const float2 *__restrict__ aux,
     const typename Mma<T>::frag *__restrict__ wfr, const float *__restrict__ bqg,
     const float *__restrict__ W, const float *__restrict__ suffix, T *__restrict__ dK,
-    T *__restrict__ dV, int H, int L, int seg_len, int nseg, float s, int Mr, float cM, float wts) {
+    T *__restrict__ dV, int H, int L, int seg_len, int nseg, float s, int Mr, float cM, int Mall, int m0,
+    float wts) {
   using SP = ScanSplit<M>;
   constexpr int FB = SP::FB;
   using P = Mma<T>;
@@ -839,15 +852,15 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
   const int s0 = hf * (SP::NS / 2);
   const int s1 = s0 + SP::NS / 2;
 
-  copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + (size_t)h * (M / 16) * 2 * 64);
-  if (tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
-  if constexpr (KPART) build_wt<T, M>(sm.WT, W + (size_t)h * Mr * kD, wts, Mr);
+  copy_frags_wg<frag, (M / 16) * 2 * 64>(&sm.WA[0][0][0], wfr + ((size_t)h * (Mall / 16) + m0 / 16) * 2 * 64);
+  if (tid < M) sm.bq[tid] = bqg[(size_t)h * Mall + m0 + tid];
+  if constexpr (KPART) build_wt<T, M>(sm.WT, W + ((size_t)h * Mr + m0) * kD, wts, Mr - m0);
   // dK: acc[nb][mb] rows value column perm_col(nb, 4 g + j) (block 4: column d),
   // lane m = 16 (w FB + mb) + lane % 16. dV: acc[mb][nb] rows m = 16 (w FB + mb)
   // + 4 g + j, lane value column perm_col(nb, lane % 16).
   f32x4 acc[KPART ? 5 : FB][KPART ? FB : 4];
   if (sw) {
-    const float *R = suffix + ((size_t)bh * nseg + seg) * M * 65;
+    const float *R = suffix + (((size_t)bh * nseg + seg) * Mall + m0) * 65;
 #pragma unroll
     for (int mb = 0; mb < FB; ++mb)
 #pragma unroll
@@ -1028,9 +1041,9 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
       if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(kf));
       if (j < r1) {
         if constexpr (KPART)
-          store_kgrad<T, KN>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
+          store_kgrad<T, KN, ACC>(dK + ((size_t)bh * L + j) * kD, kacc, kf, D, doth, s);
         else
-          store_vgrad<T>(dV + ((size_t)bh * L + j) * kD, vacc, D);
+          store_vgrad<T, ACC>(dV + ((size_t)bh * L + j) * kD, vacc, D);
       }
     }
   }
@@ -1104,40 +1117,70 @@ static hipError_t bwd_variant(const Shape &sh, F &&f) {
   return sh.renorm ? f(cosk{}, std::true_type{}) : f(cosk{}, std::false_type{});
 }
 
+// Feature slices of the gradient launches. A gradient is a sum over features
+// once the per-row weights (out, r, alpha) are fixed, so a shape wider than the
+// kernels' LDS tables (fp32 operands: bwd_max_m features) runs as slices
+// [m0, m0 + ms) of the M rows, the slices after the first adding into the fp32
+// gradients; slices wholly past the M_r features drawn add nothing and are
+// skipped. f(ms, m0, first) launches one slice.
+template <typename T, typename F>
+static hipError_t over_slices(const Shape &sh, bool causal, F &&f) {
+  const int ms = sh.M < bwd_max_m<T>(causal) ? sh.M : bwd_max_m<T>(causal);
+  for (int m0 = 0; m0 < sh.M && m0 < sh.Mr; m0 += ms) {
+    const hipError_t e = f(ms, m0, m0 == 0);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// Calls f(bool_constant ACC): false for the first slice, true after it (fp32 only).
+template <typename T, typename F>
+static hipError_t with_acc(bool first, F &&f) {
+  if constexpr (sizeof(T) == 4) {
+    if (!first) return f(std::true_type{});
+  }
+  return f(std::false_type{});
+}
+
 template <typename T>
 static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, hipStream_t st) {
   const float wts = wt_scale(sh);
   return bwd_variant(sh, [&](auto kn, auto rn) -> hipError_t {
     constexpr int KN = decltype(kn)::value;
     constexpr bool RN = decltype(rn)::value;
-    if (causal) {
-      dim3 grid(a.nseg * sh.BH);
-      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(true), sh.M,
-          hipLaunchKernelGGL((k_bwd_dq_scan<T, MM, KN, RN>), grid, dim3(kScanThreads), 0, st,
-                             (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
-                             (const T *)a.out, a.rsave, (const typename Mma<T>::frag *)a.wfr,
-                             a.bq, a.W, a.state, (T *)a.dQ, a.aux, sh.H, sh.L, a.seg_len, a.nseg,
-                             sh.s, sh.Mr, feature_norm(sh), wts));
-    } else {
-      const int rows = kBwdBidirThreads / 4 * kBwdTbw;
-      const int ntiles = (sh.L + rows - 1) / rows;
-      const int nitems = ntiles * sh.BH;
-      dim3 grid(min(nitems, kBwdMaxWorkgroups));
-      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(false), sh.M,
-          hipLaunchKernelGGL((k_bwd_dq<T, MM, KN, RN, kBwdTbw>), grid, dim3(kBwdBidirThreads), 0,
-                             st,
-                             (const T *)a.Q, (const T *)a.dout, (const T *)a.out, a.rsave,
-                             (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
-                             (T *)a.dQ, a.aux, sh.H, sh.L, sh.s, sh.Mr, feature_norm(sh), wts,
-                             ntiles, nitems));
-    }
-    return hipGetLastError();
+    return over_slices<T>(sh, causal, [&](int ms, int m0, bool first) -> hipError_t {
+      return with_acc<T>(first, [&](auto acc) -> hipError_t {
+        constexpr bool ACC = decltype(acc)::value;
+        if (causal) {
+          dim3 grid(a.nseg * sh.BH);
+          FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(true), ms,
+              hipLaunchKernelGGL((k_bwd_dq_scan<T, MM, KN, RN, ACC>), grid, dim3(kScanThreads),
+                                 0, st, (const T *)a.Q, (const T *)a.K, (const T *)a.V,
+                                 (const T *)a.dout, (const T *)a.out, a.rsave,
+                                 (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                                 (T *)a.dQ, a.aux, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
+                                 feature_norm(sh), sh.M, m0, wts));
+        } else {
+          const int rows = kBwdBidirThreads / 4 * kBwdTbw;
+          const int ntiles = (sh.L + rows - 1) / rows;
+          const int nitems = ntiles * sh.BH;
+          dim3 grid(min(nitems, kBwdMaxWorkgroups));
+          FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(false), ms,
+              hipLaunchKernelGGL((k_bwd_dq<T, MM, KN, RN, kBwdTbw, ACC>), grid,
+                                 dim3(kBwdBidirThreads), 0, st, (const T *)a.Q,
+                                 (const T *)a.dout, (const T *)a.out, a.rsave,
+                                 (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                                 (T *)a.dQ, a.aux, sh.H, sh.L, sh.s, sh.Mr, feature_norm(sh),
+                                 sh.M, m0, wts, ntiles, nitems));
+        }
+        return hipGetLastError();
+      });
+    });
   });
 }
 
 hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st) {
   if (in == Dt::BF16) return bwd_dq_typed<bf16>(sh, causal, a, st);
-  if (sh.M > 128) return hipErrorInvalidValue;
   return bwd_dq_typed<float>(sh, causal, a, st);
 }
 
@@ -1146,38 +1189,45 @@ static hipError_t bwd_dkv_typed(const Shape &sh, bool causal, const BwdArgs &a, 
   const float wts = wt_scale(sh);
   return bwd_variant(sh, [&](auto kn, auto) -> hipError_t {
     constexpr int KN = decltype(kn)::value;
-    if (causal) {
-      dim3 grid(a.nseg * sh.BH);
-      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(true), sh.M, {
-        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, false>), grid, dim3(kScanThreads), 0, st,
-                           (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
-                           a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
-                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
-                           feature_norm(sh), wts);
-        hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, true>), grid, dim3(kScanThreads), 0, st,
-                           (const T *)a.Q, (const T *)a.K, (const T *)a.V, (const T *)a.dout,
-                           a.aux, (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
-                           (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
-                           feature_norm(sh), wts);
+    return over_slices<T>(sh, causal, [&](int ms, int m0, bool first) -> hipError_t {
+      return with_acc<T>(first, [&](auto acc) -> hipError_t {
+        constexpr bool ACC = decltype(acc)::value;
+        if (causal) {
+          dim3 grid(a.nseg * sh.BH);
+          FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(true), ms, {
+            hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, false, ACC>), grid,
+                               dim3(kScanThreads), 0, st, (const T *)a.Q, (const T *)a.K,
+                               (const T *)a.V, (const T *)a.dout, a.aux,
+                               (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                               (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
+                               feature_norm(sh), sh.M, m0, wts);
+            hipLaunchKernelGGL((k_bwd_dkv_scan<T, MM, KN, true, ACC>), grid,
+                               dim3(kScanThreads), 0, st, (const T *)a.Q, (const T *)a.K,
+                               (const T *)a.V, (const T *)a.dout, a.aux,
+                               (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                               (T *)a.dK, (T *)a.dV, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
+                               feature_norm(sh), sh.M, m0, wts);
+          });
+        } else {
+          const int rows = kBwdBidirThreads / 4 * kBwdTbw;
+          const int ntiles = (sh.L + rows - 1) / rows;
+          const int nitems = ntiles * sh.BH;
+          dim3 grid(min(nitems, kBwdMaxWorkgroups));
+          FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(false), ms,
+              hipLaunchKernelGGL((k_bwd_dkv<T, MM, KN, kBwdTbw, ACC>), grid,
+                                 dim3(kBwdBidirThreads), 0, st, (const T *)a.K, (const T *)a.V,
+                                 (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                                 (T *)a.dK, (T *)a.dV, sh.H, sh.L, sh.s, sh.Mr,
+                                 feature_norm(sh), sh.M, m0, wts, ntiles, nitems));
+        }
+        return hipGetLastError();
       });
-    } else {
-      const int rows = kBwdBidirThreads / 4 * kBwdTbw;
-      const int ntiles = (sh.L + rows - 1) / rows;
-      const int nitems = ntiles * sh.BH;
-      dim3 grid(min(nitems, kBwdMaxWorkgroups));
-      FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(false), sh.M,
-          hipLaunchKernelGGL((k_bwd_dkv<T, MM, KN, kBwdTbw>), grid, dim3(kBwdBidirThreads), 0, st,
-                             (const T *)a.K, (const T *)a.V, (const typename Mma<T>::frag *)a.wfr,
-                             a.bq, a.W, a.state, (T *)a.dK, (T *)a.dV, sh.H, sh.L, sh.s, sh.Mr,
-                             feature_norm(sh), wts, ntiles, nitems));
-    }
-    return hipGetLastError();
+    });
   });
 }
 
 hipError_t launch_bwd_dkv(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st) {
   if (in == Dt::BF16) return bwd_dkv_typed<bf16>(sh, causal, a, st);
-  if (sh.M > 128) return hipErrorInvalidValue;
   return bwd_dkv_typed<float>(sh, causal, a, st);
 }
 

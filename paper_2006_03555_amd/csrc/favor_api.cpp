@@ -87,11 +87,6 @@ favor_status validate(const favor_desc *g, int op) {
   if (op == kOpBidirBackward || op == kOpCausalBackward) {
     if (g->out_dtype != g->in_dtype)
       return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass needs out_dtype == in_dtype");
-    if (g->in_dtype == FAVOR_F32 && g->M > 128)
-      return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass with fp32 inputs supports M <= 128");
-    if (op == kOpCausalBackward && g->in_dtype == FAVOR_F32 && g->M > 64)
-      return fail(FAVOR_ERR_UNSUPPORTED,
-                  "the causal backward pass with fp32 inputs supports M <= 64");
   }
   return FAVOR_OK;
 }
@@ -105,7 +100,7 @@ struct BwdPlan {
   int nsplit = 0;
   int rows_per_split = 0;
   size_t part = 0, frags = 0, wfr = 0, bq = 0, out = 0, rsave = 0, aux = 0, part2 = 0,
-         buf1 = 0, dbuf1 = 0;
+         buf1 = 0, dbuf1 = 0, halves = 0;
   size_t total = 0;
 };
 
@@ -180,8 +175,9 @@ BwdPlan make_bwd_plan(const favor_desc *g, bool causal) {
   p.part2 = p.part;
   p.buf1 = causal ? 0 : round_up((size_t)p.BH * agg, 256);
   p.dbuf1 = p.buf1;
+  p.halves = f.half_bytes;   // the recomputed causal pass of fp32 inputs at M > 128
   p.total = p.part + p.frags + p.wfr + p.bq + p.out + p.rsave + p.aux + p.part2 + p.buf1 +
-            p.dbuf1;
+            p.dbuf1 + p.halves;
   return p;
 }
 
@@ -507,7 +503,7 @@ namespace {
 
 // Carve the backward workspace.
 struct BwdBufs {
-  float *part, *bq, *rsave, *part2, *buf1, *dbuf1;
+  float *part, *bq, *rsave, *part2, *buf1, *dbuf1, *halves;
   void *frags, *wfr, *out;
   float2 *aux;
 };
@@ -534,6 +530,8 @@ BwdBufs carve(const BwdPlan &p, void *ws) {
   b.buf1 = reinterpret_cast<float *>(c);
   c += p.buf1;
   b.dbuf1 = reinterpret_cast<float *>(c);
+  c += p.dbuf1;
+  b.halves = p.halves ? reinterpret_cast<float *>(c) : nullptr;
   return b;
 }
 
@@ -684,7 +682,7 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
   if (sh.renorm && !saved) {
     favor::LaunchTimer t(favor::kKerCausal, st);
     e = favor::launch_causal_save(sh, in, Q, K, V, w.wfr, w.bq, w.part, w.out, w.rsave,
-                                  p.rows_per_split, p.nsplit, nullptr, st);
+                                  p.rows_per_split, p.nsplit, w.halves, st);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward forward pass");
   favor::BwdArgs a{Q,  K,  V,  dout, saved ? out_fwd : w.out, saved ? row_scale : w.rsave,

@@ -107,12 +107,9 @@ def test_backward_validation():
     for op in (fv.OP_BIDIR_BACKWARD, fv.OP_CAUSAL_BACKWARD):
         assert fv.validate_desc(_desc(), op) == 0
         assert fv.validate_desc(_desc(out_dtype=fv.F32), op) == 2   # out dtype = in dtype
-        assert fv.validate_desc(_desc(in_dtype=fv.F32, out_dtype=fv.F32), op) == 2   # M 256
-        assert fv.validate_desc(_desc(in_dtype=fv.F32, out_dtype=fv.F32, M=64), op) == 0
-    assert fv.validate_desc(_desc(in_dtype=fv.F32, out_dtype=fv.F32, M=128),
-                            fv.OP_BIDIR_BACKWARD) == 0
-    assert fv.validate_desc(_desc(in_dtype=fv.F32, out_dtype=fv.F32, M=128),
-                            fv.OP_CAUSAL_BACKWARD) == 2
+        # fp32 at every M (feature slices)
+        for M in (64, 128, 208, 256):
+            assert fv.validate_desc(_desc(in_dtype=fv.F32, out_dtype=fv.F32, M=M), op) == 0
     for op in (fv.OP_BIDIR_BACKWARD, fv.OP_CAUSAL_BACKWARD):
         assert fv.validate_desc(_desc(kernel=fv.KERNEL_RELU, renormalize=False), op) == 0
 

@@ -252,3 +252,63 @@ def test_fp32_both_directions_feature_halves_and_saved_scales():
     for causal, r in ((False, rb), (True, rc)):
         want = _expected_row_scale(Q, K, W, b, M, SOFTMAX, 0.0, causal)
         assert np.max(np.abs(to_host(r) - want) / np.abs(want)) <= 1e-4
+
+
+# fp32 gradients beyond the kernels' LDS tables (128 features bidirectional, 64
+# causal): feature slices whose parts add into dQ, dK, dV
+FP32_BWD_CASES = [
+    # B, H, L, M, kernel, causal, renormalize
+    (1, 2, 300, 256, SOFTMAX, False, True),
+    (1, 2, 333, 144, RELU, False, True),
+    (1, 2, 300, 128, SOFTMAX, True, True),
+    (1, 2, 400, 256, RELU, True, True),
+    (1, 1, 257, 208, SOFTMAX, True, False),
+]
+
+
+@pytest.mark.parametrize("B,H,L,M,kernel,causal,renorm", FP32_BWD_CASES)
+def test_fp32_backward_feature_slices(B, H, L, M, kernel, causal, renorm):
+    import torch
+    fv = _fv()
+    Q, K, V, dout, W, b = _bwd_inputs(B, H, L, M, "f32", seed=L + M + 1)
+    args = [to_dev(x) for x in (Q, K, V)] + [to_dev(W), to_dev(b), S64, to_dev(dout)]
+    kw = dict(kernel=kernel, renormalize=renorm)
+    names = ("dQ", "dK", "dV")
+    if not causal:
+        got = fv.attn_bidir_backward(*args, **kw)
+        torch.cuda.synchronize()
+        ref = bw.attn_bidir_backward(Q, K, V, W, b, S64, dout, **kw)
+    else:
+        Qe, Ke, Ve = _qkv(B, H, 120, "f32", seed=M + 4)
+        _, S0 = favor.attn_causal(Qe, Ke, Ve, W, b, S64, **kw)
+        S0 = S0.astype(np.float32)
+        dS = np.random.default_rng(5).standard_normal(S0.shape).astype(np.float32) * 0.01
+        got = fv.attn_causal_backward(*args, state_in=to_dev(S0), dstate_out=to_dev(dS),
+                                      return_state_grad=True, **kw)
+        torch.cuda.synchronize()
+        ref = bw.attn_causal_backward(Q, K, V, W, b, S64, dout, state_in=S0, dstate_out=dS,
+                                      **kw)
+        assert np.max(np.abs(to_host(got[3]) - ref[3])) <= 1e-4 * np.max(np.abs(ref[3]))
+    _check_all(dict(zip(names, (to_host(x) for x in got[:3]))), dict(zip(names, ref[:3])),
+               "f32")
+
+
+def test_fp32_backward_slices_with_saved_statistics():
+    """attn_both at fp32 M = 256 saving the row scales, then both backward calls
+    from the saved outputs: the gradients of the calls that recompute them."""
+    import torch
+    fv = _fv()
+    B, H, L, M = 1, 2, 500, 256
+    Q, K, V, dout, W, b = _bwd_inputs(B, H, L, M, "f32", seed=91)
+    q, k, v, do = (to_dev(x) for x in (Q, K, V, dout))
+    Wd, bd = to_dev(W), to_dev(b)
+    rb = torch.empty((B, H, L), device="cuda")
+    rc = torch.empty((B, H, L), device="cuda")
+    ob, oc = fv.attn_both(q, k, v, Wd, bd, S64, row_scale_bidir=rb, row_scale_causal=rc)
+    names = ("dQ", "dK", "dV")
+    for f, o, r in ((fv.attn_bidir_backward, ob, rb), (fv.attn_causal_backward, oc, rc)):
+        plain = f(q, k, v, Wd, bd, S64, do)[:3]
+        saved = f(q, k, v, Wd, bd, S64, do, out=o, row_scale=r)[:3]
+        torch.cuda.synchronize()
+        _check_all(dict(zip(names, map(to_host, saved))),
+                   dict(zip(names, (to_host(x) for x in plain))), "f32")
