@@ -1,0 +1,95 @@
+"""A seeded sweep of random call configurations through every forward entry
+point (favor_feature_map, favor_attn_bidir, favor_attn_causal, favor_attn_both),
+each against the fp64 oracle on the same inputs and features: B, H, ragged L,
+any M that is a multiple of 16, in/out dtypes, feature kind, renormalisation,
+stabiliser, causal segment length and a carried state (cos features from M 64,
+ReLU features from M 16). The configurations are drawn once from a fixed seed,
+so a failure names a reproducible case.
+
+Tolerances as everywhere: 1e-4 for fp32 inputs, 2e-2 for bf16 inputs.
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from helpers import TOL, parity, to_dev, to_host
+from oracle import favor
+
+pytestmark = pytest.mark.gpu
+
+S64 = 64 ** -0.25
+
+
+def _configs(n=24, seed=20261202):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        dtype = "f32" if rng.random() < 0.4 else "bf16"
+        kernel = favor.KERNEL_RELU if rng.random() < 0.4 else favor.KERNEL_SOFTMAX
+        out.append(dict(
+            case=i,
+            B=int(rng.integers(1, 3)), H=int(rng.integers(1, 4)),
+            L=int(rng.choice([1, 17, 63, 64, 65, 200, 511, 777, 1300])),
+            # cos features at M < 64 can leave a row's D-hat near 0 (E_row has no
+            # conditioning term): small M is swept with ReLU features
+            M=int(16 * rng.integers(1 if kernel == favor.KERNEL_RELU else 4, 17)),
+            dtype=dtype,
+            out_dtype="f32" if dtype == "bf16" and rng.random() < 0.3 else dtype,
+            kernel=kernel,
+            renorm=bool(rng.random() < 0.8),
+            eps=float(rng.choice([0.0, 0.0, 0.25])),
+            chunk=int(rng.choice([0, 0, 64, 192, 512])),
+            state=bool(rng.random() < 0.5),
+            kind=int(rng.choice([favor.RF_ORTHO_CHI, favor.RF_IID, favor.RF_HADAMARD])),
+        ))
+    return out
+
+
+CONFIGS = _configs()
+
+
+def _check(got, ref, tol):
+    scale = np.max(np.abs(ref), axis=-1, keepdims=True)
+    assert np.max(np.abs(got - ref) / np.maximum(scale, 1e-30)) <= tol
+
+
+@pytest.mark.parametrize("cfg", CONFIGS, ids=[f"case{c['case']}" for c in CONFIGS])
+def test_random_configuration(cfg):
+    import torch
+    fv = __import__("paper_2006_03555_amd")
+    B, H, L, M, dtype = cfg["B"], cfg["H"], cfg["L"], cfg["M"], cfg["dtype"]
+    print(f"\n{cfg}", flush=True)
+    Q, K, V = wl.make_qkv(wl.Workload("t", "bidir", B, H, L, 64, 64, dtype,
+                                      1000 + cfg["case"]))
+    W, b = favor.orf_draw(2000 + cfg["case"], H, M, 64, cfg["kind"])
+    W, b = W.astype(np.float32), b.astype(np.float32)
+    kw = dict(kernel=cfg["kernel"], renormalize=cfg["renorm"])
+    odt = torch.float32 if cfg["out_dtype"] == "f32" else torch.bfloat16
+    tol = TOL[dtype]
+    q, k, v, Wd, bd = to_dev(Q, dtype), to_dev(K, dtype), to_dev(V, dtype), to_dev(W), to_dev(b)
+    S0 = None
+    if cfg["state"]:
+        Qe, Ke, Ve = wl.make_qkv(wl.Workload("t", "bidir", B, H, 100, 64, 64, dtype, 7))
+        _, S0 = favor.attn_causal(Qe, Ke, Ve, W, b, S64, **kw)
+        S0 = S0.astype(np.float32)
+
+    Xp = fv.feature_map(q, Wd, bd, S64, out_dtype=odt, kernel=cfg["kernel"])
+    ob = fv.attn_bidir(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], out_dtype=odt, **kw)
+    oc, st = fv.attn_causal(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], chunk=cfg["chunk"],
+                            state_in=None if S0 is None else to_dev(S0), return_state=True,
+                            out_dtype=odt, **kw)
+    ob2, oc2 = fv.attn_both(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], chunk=cfg["chunk"],
+                            state_in=None if S0 is None else to_dev(S0), out_dtype=odt, **kw)
+    torch.cuda.synchronize()
+
+    ref_f = favor.features(Q.astype(np.float64), W, b, S64, cfg["kernel"], 1e-3)
+    _check(to_host(Xp), ref_f, tol if cfg["out_dtype"] == dtype else TOL["bf16"])
+    ptol = tol if cfg["out_dtype"] == dtype else TOL["bf16"]
+    for out in (ob, ob2):
+        parity(to_host(out), Q, K, V, W, b, S64, False, dtype, eps=cfg["eps"], tol=ptol,
+               kernel=cfg["kernel"], renormalize=cfg["renorm"])
+    for out in (oc, oc2):
+        parity(to_host(out), Q, K, V, W, b, S64, True, dtype, eps=cfg["eps"], tol=ptol,
+               state_in=S0, kernel=cfg["kernel"], renormalize=cfg["renorm"])
+    _, ref_state = favor.attn_causal(Q, K, V, W, b, S64, state_in=S0, **kw)
+    assert np.max(np.abs(to_host(st) - ref_state)) <= tol * np.max(np.abs(ref_state))
