@@ -698,9 +698,27 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
         if constexpr (i + 1 < 8) load_rows(std::integral_constant<int, i + 1>{}, rn);
         project(ic, rc, pc);
         finish(std::integral_constant<int, i - 1>{}, pp);
+        // the next group's rows first, then each projection MFMA followed by
+        // three vector instructions of the previous group's epilogue, so that
+        // the cosines issue while the matrix core works
+        if constexpr (i + 1 < 8) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        static_for<0, 2 * MB>([&](auto) __attribute__((always_inline)) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        });
         __builtin_amdgcn_sched_barrier(0);
       });
       finish(std::integral_constant<int, 7>{}, pr1);
+      // the features are complete here: keeps the compiler from sinking the
+      // cosines past the finalisation branch, away from the projection MFMAs
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(qB[tb][ks]));
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int sx = 0; sx < 2; ++sx) asm volatile("" : "+v"(kA[mb][sx]));
     }
 
     if (t0 > r0) finalize(t0 - 64, buf ^ 1);
