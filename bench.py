@@ -55,9 +55,10 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = os.path.join(ROOT, "paper_2006_03555_amd", "csrc")
 
 
-# Sources of the kernels the bench step launches and of their launch planning.
+# Sources of the kernels the bench step launches and of their launch planning, and
+# the build script (its per-source compiler flags change the kernels too).
 STEP_SOURCES = ("bidir.hip", "causal.hip", "feature_map.hip", "orf_draw.hip", "favor_api.cpp",
-                "favor_common.hpp", "kernels.hpp", "tile_common.hpp")
+                "favor_common.hpp", "kernels.hpp", "tile_common.hpp", "../build.py")
 
 
 def kernel_source_hash():
