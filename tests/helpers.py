@@ -52,13 +52,11 @@ def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=Non
     else:
         ref = favor.attn_bidir_features(Qp, Kp, V, eps, renormalize)
     e_row = metrics.err_row(out, ref)
-    S, den = metrics.error_scale(Qp, Kp, V, causal, state_in_abs=state_in)
+    S, den = metrics.error_scale(Qp, Kp, V, causal, state_in=state_in)
     if not renormalize:
         e_cond = metrics.err_cond_numerator(out, ref, S)
     else:
-        if eps:
-            den = np.abs(den + eps)
-        e_cond = metrics.err_cond(out, ref, S, den)
+        e_cond = metrics.err_cond(out, ref, S, den + eps)
     assert e_row <= tol, f"E_row {e_row:.3e} > {tol}"
     assert e_cond <= tol, f"E_cond {e_cond:.3e} > {tol}"
     return e_row, e_cond
