@@ -16,7 +16,9 @@ division by D-hat) and kernel_eps (added to every ReLU feature). The attention
 calls take row_scale (a [B, H, L] float32 tensor) to save each row's
 1 / (D-hat + eps) for the backward calls, which then skip recomputing it.
 """
+import contextlib
 import ctypes
+import functools
 import os
 
 from ._lib import (  # noqa: F401
@@ -58,6 +60,21 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _on_stream(fn):
+    """Run fn with the caller's stream (keyword `stream`) as torch's current
+    stream, so that the outputs and the temporary workspace fn allocates belong
+    to the stream the kernels run on: the caching allocator then hands a freed
+    workspace block only to later work on that same stream, never to another
+    stream while the kernels may still use it."""
+    @functools.wraps(fn)
+    def wrapper(*args, stream=None, **kw):
+        ctx = (contextlib.nullcontext() if stream is None
+               else _torch().cuda.stream(stream))
+        with ctx:
+            return fn(*args, stream=stream, **kw)
+    return wrapper
+
+
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
@@ -73,6 +90,7 @@ def _require_cuda(*ts):
             raise FavorError(1, "tensors must be contiguous GPU tensors")
 
 
+@_on_stream
 def orf_draw(seed, n_heads, M, d=64, kind=RF_ORTHO_CHI, W=None, b=None, stream=None):
     """Draw W [n_heads, M, d] and b [n_heads, M] on the GPU (favor_orf_draw)."""
     torch = _torch()
@@ -133,6 +151,7 @@ def _out_dtype(out_dtype, out, X):
     return out.dtype if out is not None else X.dtype
 
 
+@_on_stream
 def feature_map(X, W, b, input_scale, out_dtype=None, out=None, stream=None,
                 kernel=KERNEL_SOFTMAX, kernel_eps=1e-3):
     """X' [B, H, L, M] (favor_feature_map): D_X X-hat, or the ReLU features."""
@@ -164,6 +183,7 @@ def _require_row_scale(t, g, name):
     _require_like(t, (g.B, g.H, g.L), torch.float32, name)
 
 
+@_on_stream
 def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=None,
                workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
                kernel_eps=1e-3, row_scale=None):
@@ -184,6 +204,7 @@ def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=No
     return out
 
 
+@_on_stream
 def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
                 chunk=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None,
                 kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3, row_scale=None):
@@ -212,6 +233,7 @@ def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return
     return (out, state_out) if return_state else out
 
 
+@_on_stream
 def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
               chunk=0, out_dtype=None, out_bidir=None, out_causal=None, state_out=None,
               workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
@@ -278,6 +300,7 @@ def _saved(out, row_scale, g, Q):
         _require_row_scale(row_scale, g, "row_scale")
 
 
+@_on_stream
 def attn_bidir_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, dQ=None, dK=None,
                         dV=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
                         renormalize=True, kernel_eps=1e-3, out=None, row_scale=None):
@@ -299,6 +322,7 @@ def attn_bidir_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, dQ=None
     return dQ, dK, dV
 
 
+@_on_stream
 def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_in=None,
                          dstate_out=None, return_state_grad=False, dQ=None, dK=None, dV=None,
                          dstate_in=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,

@@ -148,9 +148,13 @@ __device__ __forceinline__ void wave_sync() {
 __device__ __forceinline__ bool flag_set(const int *f) {
   return __hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != 0;
 }
-__device__ __forceinline__ void wait_flag(const int *f) {
+// Bounded wait for a row's flag: true once it is set. The bound only keeps a
+// wave from spinning forever should a flag never come up; the caller then
+// poisons its row (NaN), so such a failure shows in W instead of passing.
+__device__ __forceinline__ bool wait_flag(const int *f) {
   for (int spin = 0; spin < (1 << 22); ++spin)
-    if (flag_set(f)) break;
+    if (flag_set(f)) return true;
+  return false;
 }
 
 __global__ __launch_bounds__(512) void k_orf_draw(uint64_t seed, int M, int kind,
@@ -216,8 +220,9 @@ __global__ __launch_bounds__(512) void k_orf_draw(uint64_t seed, int M, int kind
     // flag covers both rows). The two rows are orthogonal, so removing both
     // components at once is the same projection (modified Gram-Schmidt in
     // blocks of two).
+    bool published = true;
     for (int j0 = 0; j0 < RW * w; j0 += 2) {
-      wait_flag(&ready[j0 + 1]);
+      published = wait_flag(&ready[j0 + 1]) && published;
       double q0[8], q1[8];
       read_row(&pub[j0][8 * p], q0);
       read_row(&pub[j0 + 1][8 * p], q1);
@@ -264,6 +269,7 @@ __global__ __launch_bounds__(512) void k_orf_draw(uint64_t seed, int M, int kind
       s1 = fma(x[i + 1], x[i + 1], s1);
     }
     scale = rho / sqrt(sum8(s0 + s1));
+    if (!published) scale = __builtin_nan("");
   }
 
   if ((int)m < M) {

@@ -28,12 +28,16 @@ def oracle_features(Q, K, W, b, s, kernel=favor.KERNEL_SOFTMAX, kernel_eps=1e-3)
 
 
 def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=None,
-           heads=None, kernel=favor.KERNEL_SOFTMAX, kernel_eps=1e-3, renormalize=True):
+           heads=None, kernel=favor.KERNEL_SOFTMAX, kernel_eps=1e-3, renormalize=True,
+           gate="both", stats=None):
     """Compare a GPU output with the oracle on the same inputs and features.
 
     heads: optional list of (batch, head) pairs to check (large inputs).
     kernel, kernel_eps, renormalize: the feature kernel and normalisation of the
-    call. Returns (E_row, E_cond); asserts both are within the tolerance."""
+    call. gate: "both" asserts E_row and E_cond, "cond" only E_cond (regimes
+    where D-hat cancels, such as input_scale 1, or cos features at small M:
+    E_row has no conditioning term there). stats: optional dict that receives
+    the per-row condition numbers kappa. Returns (E_row, E_cond)."""
     tol = TOL[dtype] if tol is None else tol
     Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
     out = np.asarray(out, dtype=np.float64)
@@ -57,6 +61,9 @@ def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=Non
         e_cond = metrics.err_cond_numerator(out, ref, S)
     else:
         e_cond = metrics.err_cond(out, ref, S, den + eps)
-    assert e_row <= tol, f"E_row {e_row:.3e} > {tol}"
+    if stats is not None:
+        stats["kappa"] = metrics.kappa(S, den + eps)
+    if gate == "both":
+        assert e_row <= tol, f"E_row {e_row:.3e} > {tol}"
     assert e_cond <= tol, f"E_cond {e_cond:.3e} > {tol}"
     return e_row, e_cond

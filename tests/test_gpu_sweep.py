@@ -3,7 +3,8 @@ point (favor_feature_map, favor_attn_bidir, favor_attn_causal, favor_attn_both),
 each against the fp64 oracle on the same inputs and features: B, H, ragged L,
 any M that is a multiple of 16, in/out dtypes, feature kind, renormalisation,
 stabiliser, causal segment length and a carried state (cos features from M 64,
-ReLU features from M 16). The configurations are drawn once from a fixed seed,
+ReLU features from M 16; a second list takes cos features at M 16 to 48 and
+gates them by E_cond alone). The configurations are drawn once from a fixed seed,
 so a failure names a reproducible case.
 
 Tolerances as everywhere: 1e-4 for fp32 inputs, 2e-2 for bf16 inputs.
@@ -48,12 +49,39 @@ def _configs(n=24, seed=20261202):
 CONFIGS = _configs()
 
 
+def _small_m_configs(n=8, seed=777):
+    """Cosine features at M 16 to 48: D-hat can nearly cancel on some rows, so
+    these are gated by E_cond alone (E_row is printed)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        dtype = "f32" if rng.random() < 0.5 else "bf16"
+        out.append(dict(
+            case=100 + i,
+            B=int(rng.integers(1, 3)), H=int(rng.integers(1, 4)),
+            L=int(rng.choice([1, 63, 65, 200, 777, 1300])),
+            M=int(16 * rng.integers(1, 4)),
+            dtype=dtype, out_dtype=dtype, kernel=favor.KERNEL_SOFTMAX,
+            renorm=bool(rng.random() < 0.8),
+            eps=0.0,
+            chunk=int(rng.choice([0, 64, 192])),
+            state=bool(rng.random() < 0.5),
+            kind=int(rng.choice([favor.RF_ORTHO_CHI, favor.RF_IID, favor.RF_HADAMARD])),
+            gate="cond",
+        ))
+    return out
+
+
+CONFIGS_SMALL_M = _small_m_configs()
+
+
 def _check(got, ref, tol):
     scale = np.max(np.abs(ref), axis=-1, keepdims=True)
     assert np.max(np.abs(got - ref) / np.maximum(scale, 1e-30)) <= tol
 
 
-@pytest.mark.parametrize("cfg", CONFIGS, ids=[f"case{c['case']}" for c in CONFIGS])
+@pytest.mark.parametrize("cfg", CONFIGS + CONFIGS_SMALL_M,
+                         ids=[f"case{c['case']}" for c in CONFIGS + CONFIGS_SMALL_M])
 def test_random_configuration(cfg):
     import torch
     fv = __import__("paper_2006_03555_amd")
@@ -85,11 +113,14 @@ def test_random_configuration(cfg):
     ref_f = favor.features(Q.astype(np.float64), W, b, S64, cfg["kernel"], 1e-3)
     _check(to_host(Xp), ref_f, tol if cfg["out_dtype"] == dtype else TOL["bf16"])
     ptol = tol if cfg["out_dtype"] == dtype else TOL["bf16"]
+    gate = cfg.get("gate", "both")
     for out in (ob, ob2):
-        parity(to_host(out), Q, K, V, W, b, S64, False, dtype, eps=cfg["eps"], tol=ptol,
-               kernel=cfg["kernel"], renormalize=cfg["renorm"])
+        e = parity(to_host(out), Q, K, V, W, b, S64, False, dtype, eps=cfg["eps"], tol=ptol,
+                   kernel=cfg["kernel"], renormalize=cfg["renorm"], gate=gate)
+        print(f"bidir E_row {e[0]:.2e} E_cond {e[1]:.2e}", flush=True)
     for out in (oc, oc2):
-        parity(to_host(out), Q, K, V, W, b, S64, True, dtype, eps=cfg["eps"], tol=ptol,
-               state_in=S0, kernel=cfg["kernel"], renormalize=cfg["renorm"])
+        e = parity(to_host(out), Q, K, V, W, b, S64, True, dtype, eps=cfg["eps"], tol=ptol,
+                   state_in=S0, kernel=cfg["kernel"], renormalize=cfg["renorm"], gate=gate)
+        print(f"causal E_row {e[0]:.2e} E_cond {e[1]:.2e}", flush=True)
     _, ref_state = favor.attn_causal(Q, K, V, W, b, S64, state_in=S0, **kw)
     assert np.max(np.abs(to_host(st) - ref_state)) <= tol * np.max(np.abs(ref_state))

@@ -194,3 +194,112 @@ def test_carried_state_enters_the_denominator():
     _, den = metrics.error_scale(Qp, Kp, V, causal=True, state_in=st)
     want = [Qp[i] @ (st[:, d] + Kp[:i + 1].sum(0)) for i in range(L)]
     np.testing.assert_allclose(den, want, rtol=1e-13)
+
+
+# ---------------------------------------------------------------- gradients
+from oracle import backward as bw  # noqa: E402
+
+
+def _grad_case(seed, L=9, M=8, d=4, B=1, H=2):
+    rng = np.random.default_rng(seed)
+    Q = rng.normal(size=(B, H, L, d)) * 0.5
+    K = rng.normal(size=(B, H, L, d)) * 0.5
+    V = rng.normal(size=(B, H, L, d))
+    dout = rng.normal(size=(B, H, L, d))
+    W, b = favor.orf_draw(seed, H, M, d)
+    return Q, K, V, dout, W, b
+
+
+def _grads(Q, K, V, W, b, dout, causal, **kw):
+    if causal:
+        return bw.attn_causal_backward(Q, K, V, W, b, 1.0, dout, **kw)[:3]
+    return bw.attn_bidir_backward(Q, K, V, W, b, 1.0, dout, **kw)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("kernel,renorm,eps", [(favor.KERNEL_SOFTMAX, True, 0.0),
+                                               (favor.KERNEL_SOFTMAX, True, 0.3),
+                                               (favor.KERNEL_SOFTMAX, False, 0.0),
+                                               (favor.KERNEL_RELU, True, 0.0)])
+def test_grad_scale_bounds_relative_perturbations(causal, kernel, renorm, eps, monkeypatch):
+    """Perturb every factor the contractions multiply (the features Q', K', the
+    values V and the output gradient) by a relative amount of at most delta: each
+    gradient row moves by at most a small multiple of delta times its error scale,
+    in particular on the rows whose gradient cancels (the first causal row, whose
+    exact dQ is 0 with renormalisation)."""
+    delta = 1e-6
+    worst = 0.0
+    for seed in range(6):
+        Q, K, V, dout, W, b = _grad_case(seed)
+        kw = dict(kernel=kernel, renormalize=renorm, denom_eps=eps)
+        ref = _grads(Q, K, V, W, b, dout, causal, **kw)
+        scale = metrics.grad_error_scale(Q, K, V, W, b, 1.0, dout, causal, **kw)
+        for r, a in zip(ref, scale):
+            assert np.all(a >= np.abs(r) * (1 - 1e-12))
+        rng = np.random.default_rng(seed + 50)
+        real = favor.features
+        monkeypatch.setattr(favor, "features", lambda *a, **k: (
+            lambda f: f * (1 + delta * rng.uniform(-1, 1, size=f.shape)))(real(*a, **k)))
+        pert = lambda x: x * (1 + delta * rng.uniform(-1, 1, size=x.shape))
+        got = _grads(Q, K, pert(V), W, b, pert(dout), causal, **kw)
+        monkeypatch.setattr(favor, "features", real)
+        for g, r, a in zip(got, ref, scale):
+            e = metrics.err_grad_rows(g, r, a)
+            assert e <= 4 * delta, e
+            worst = max(worst, e)
+    assert worst >= 0.02 * delta
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_grad_scale_of_values_for_positive_terms(causal):
+    """Non-negative features (ReLU with kernel_eps > 0 on any input), values and
+    output gradient: dV_j = sum_i dout_i (Q'_i . K'_j) / D-hat_i has no
+    cancellation and kappa = 1, so its scale is exactly (1 + kappa) |dV| = 2 dV."""
+    rng = np.random.default_rng(2)
+    B, H, L, M, d = 1, 1, 7, 8, 3
+    Q = rng.normal(size=(B, H, L, d))
+    K = rng.normal(size=(B, H, L, d))
+    V = rng.uniform(0.5, 2.0, size=(B, H, L, d))
+    dout = rng.uniform(0.1, 1.0, size=(B, H, L, d))
+    W, b = favor.orf_draw(4, H, M, d)
+    kw = dict(kernel=favor.KERNEL_RELU, kernel_eps=0.05)
+    dV = _grads(Q, K, V, W, b, dout, causal, **kw)[2]
+    AdV = metrics.grad_error_scale(Q, K, V, W, b, 1.0, dout, causal, **kw)[2]
+    assert np.all(dV > 0)
+    np.testing.assert_allclose(AdV, 2 * dV, rtol=1e-12)
+
+
+def test_grad_scale_single_key_rows_keep_the_size_of_their_terms():
+    """With one key (L = 1) the renormalised output is v_1 whatever q and k are:
+    dQ and dK vanish in exact arithmetic, yet their error scale is the size of
+    the terms that cancel, comparable to that of dV."""
+    Q, K, V, dout, W, b = _grad_case(7, L=1)
+    dQ, dK, dV = _grads(Q, K, V, W, b, dout, False)
+    AdQ, AdK, AdV = metrics.grad_error_scale(Q, K, V, W, b, 1.0, dout, False)
+    assert np.max(np.abs(dQ)) <= 1e-12 * np.max(AdQ)
+    assert np.max(np.abs(dK)) <= 1e-12 * np.max(AdK)
+    assert np.min(AdQ.max(axis=-1)) > 1e-3 * np.max(AdV)
+
+
+def test_grad_scale_bounds_perturbations_with_carried_states(monkeypatch):
+    """The causal form with a carried state and a gradient reaching state_out:
+    both enter the prefix and suffix aggregates, and their magnitudes enter the
+    scale; perturbing them with the other factors stays within the bound."""
+    delta = 1e-6
+    for seed in range(4):
+        Q, K, V, dout, W, b = _grad_case(seed)
+        rng = np.random.default_rng(seed + 80)
+        S0 = rng.normal(size=(1, 2, 8, 5)) * 100.0
+        dS = rng.normal(size=(1, 2, 8, 5)) * 30.0
+        kw = dict(state_in=S0, dstate_out=dS)
+        ref = bw.attn_causal_backward(Q, K, V, W, b, 1.0, dout, **kw)[:3]
+        scale = metrics.grad_error_scale(Q, K, V, W, b, 1.0, dout, True, **kw)
+        real = favor.features
+        monkeypatch.setattr(favor, "features", lambda *a, **k: (
+            lambda f: f * (1 + delta * rng.uniform(-1, 1, size=f.shape)))(real(*a, **k)))
+        pert = lambda x: x * (1 + delta * rng.uniform(-1, 1, size=x.shape))
+        got = bw.attn_causal_backward(Q, K, pert(V), W, b, 1.0, pert(dout),
+                                      state_in=pert(S0), dstate_out=pert(dS))[:3]
+        monkeypatch.setattr(favor, "features", real)
+        for g, r, a in zip(got, ref, scale):
+            assert metrics.err_grad_rows(g, r, a) <= 4 * delta
