@@ -4,7 +4,8 @@
  *
  * Every tensor argument is a DEVICE pointer owned by the caller; the library
  * never allocates, frees or retains device memory (scratch is the caller's
- * workspace). Every call is asynchronous: work is enqueued on `stream` (a
+ * workspace; the one exception is the static scratch array each GPU holds for
+ * favor_attn_both_noalloc). Every call is asynchronous: work is enqueued on `stream` (a
  * hipStream_t passed as void*, NULL = the default stream) and nothing waits.
  *
  * Errors: arguments are validated completely before anything is launched. On
@@ -193,6 +194,30 @@ FAVOR_API favor_status favor_attn_both(const favor_desc *g, const void *Q, const
                                        const float *state_in, float *state_out,
                                        float *row_scale_bidir, float *row_scale_causal,
                                        void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * favor_attn_both_noalloc - favor_attn_both for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same arguments without ws / ws_bytes, and the same
+ * results. The workspace is a static array of favor_noalloc_scratch_bytes()
+ * bytes (32 MiB) that each GPU the library runs on holds from the first load of
+ * the library's code there until the process ends; nothing is allocated or
+ * freed by the call. A call whose favor_workspace_size(g, 2) exceeds it returns
+ * FAVOR_ERR_WORKSPACE_TOO_SMALL and launches nothing. Every call on one GPU uses
+ * that GPU's one array: calls that overlap on one GPU (concurrent streams,
+ * threads) race on it and must be serialised by the caller. The array needs no
+ * clearing (the kernels overwrite what they read). The current device is the
+ * one whose array is used (the stream must belong to it).
+ */
+FAVOR_API favor_status favor_attn_both_noalloc(const favor_desc *g, const void *Q,
+                                               const void *K, const void *V, const float *W,
+                                               const float *b, void *out_bidir,
+                                               void *out_causal, const float *state_in,
+                                               float *state_out, float *row_scale_bidir,
+                                               float *row_scale_causal, void *stream);
+
+/* Size in bytes of favor_attn_both_noalloc's static scratch array. */
+FAVOR_API size_t favor_noalloc_scratch_bytes(void);
 
 /*
  * Backward pass (the paper trains through FAVOR and benchmarks its backward

@@ -31,6 +31,7 @@ from ._lib import (  # noqa: F401
 __all__ = [
     "orf_draw", "feature_map", "attn_bidir", "attn_causal", "attn_both", "workspace_size",
     "attn_bidir_backward", "attn_causal_backward", "backward_workspace_size", "make_desc",
+    "attn_both_noalloc", "noalloc_scratch_bytes",
     "validate_desc", "FavorError", "FavorLibraryMissing", "lib", "lib_path",
 ]
 
@@ -270,6 +271,45 @@ def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_s
     if return_state:
         return out_bidir, out_causal, state_out
     return out_bidir, out_causal
+
+
+@_on_stream
+def attn_both_noalloc(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None,
+                      chunk=0, out_bidir=None, out_causal=None, state_out=None, stream=None,
+                      kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3,
+                      row_scale_bidir=None, row_scale_causal=None):
+    """attn_both with the library's static scratch as workspace
+    (favor_attn_both_noalloc): nothing is allocated when the outputs are given.
+    Returns (out_bidir, out_causal)."""
+    torch = _torch()
+    odt = out_bidir.dtype if out_bidir is not None else Q.dtype
+    g = _desc_for(Q, W, input_scale, odt, denom_eps, chunk,
+                  others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
+    _require_features(W, b, g.H, g.M, g.d)
+    tdt = _torch_dtype(g.out_dtype)
+    sshape = (g.B, g.H, g.M, g.d + 1)
+    if out_bidir is None:
+        out_bidir = torch.empty(Q.shape, dtype=tdt, device=Q.device)
+    if out_causal is None:
+        out_causal = torch.empty(Q.shape, dtype=tdt, device=Q.device)
+    _require_like(out_bidir, Q.shape, tdt, "out_bidir")
+    _require_like(out_causal, Q.shape, tdt, "out_causal")
+    _require_like(state_in, sshape, torch.float32, "state_in")
+    _require_like(state_out, sshape, torch.float32, "state_out")
+    _require_row_scale(row_scale_bidir, g, "row_scale_bidir")
+    _require_row_scale(row_scale_causal, g, "row_scale_causal")
+    _require_cuda(Q, K, V, W, b, out_bidir, out_causal, state_in, state_out, row_scale_bidir,
+                  row_scale_causal)
+    _check(lib().favor_attn_both_noalloc(
+        ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b), _ptr(out_bidir),
+        _ptr(out_causal), _ptr(state_in), _ptr(state_out), _ptr(row_scale_bidir),
+        _ptr(row_scale_causal), _stream(stream)))
+    return out_bidir, out_causal
+
+
+def noalloc_scratch_bytes():
+    """Size of the static scratch array attn_both_noalloc uses (per GPU)."""
+    return lib().favor_noalloc_scratch_bytes()
 
 
 def _bwd_workspace(g, causal, workspace):

@@ -67,6 +67,9 @@ def lib():
                               [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_attn_both": (ctypes.c_int,
                             [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_both_noalloc": (ctypes.c_int,
+                                    [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "favor_noalloc_scratch_bytes": (sz, []),
         "favor_backward_workspace_size": (sz, [dp, ctypes.c_int]),
         "favor_attn_bidir_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                      vp, vp, vp, vp, sz, vp]),

@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libfavor.so")
 ARCH = "gfx950"
 
 SOURCES = ["orf_draw.hip", "feature_map.hip", "bidir.hip", "causal.hip", "backward.hip",
-           "favor_api.cpp", "timing.cpp"]
+           "noalloc.hip", "favor_api.cpp", "timing.cpp"]
 
 # Packed fp32 arithmetic is disabled for all device code (no v_pk_*_f32).
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

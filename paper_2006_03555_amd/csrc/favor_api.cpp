@@ -228,6 +228,13 @@ favor_status device_result(hipError_t e, const char *what) {
 
 }  // namespace
 
+namespace favor {
+
+// Records msg as the calling thread's favor_last_error text and returns st.
+favor_status report(favor_status st, const char *msg) { return fail(st, "%s", msg); }
+
+}  // namespace favor
+
 extern "C" {
 
 int32_t favor_abi_version(void) { return FAVOR_ABI_VERSION; }

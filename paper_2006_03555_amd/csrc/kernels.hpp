@@ -4,6 +4,8 @@
 #include <cmath>
 
 #include <hip/hip_runtime.h>
+
+#include "../../include/favor.h"
 #include <stddef.h>
 #include <stdint.h>
 
@@ -145,6 +147,9 @@ enum KernelId {
   kNumKernels
 };
 const char *kernel_name(int k);
+
+// Records msg as the calling thread's favor_last_error text and returns st.
+favor_status report(favor_status st, const char *msg);
 
 // Brackets one launch with pooled HIP events on `st` while timing is enabled.
 class LaunchTimer {

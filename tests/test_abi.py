@@ -250,3 +250,20 @@ def test_binding_checks_tensor_shapes_and_dtypes():
         with pytest.raises(fv.FavorError) as e:
             call()
         assert name in str(e.value), (name, str(e.value))
+
+
+def test_noalloc_rejects_a_workspace_beyond_its_scratch(L):
+    """favor_attn_both_noalloc checks the workspace the call needs against its
+    static scratch before any device call (placeholder pointers: nothing runs)."""
+    assert L.favor_noalloc_scratch_bytes() == 32 << 20
+    # fp32 causal passes at M > 128 keep [B][H][L][68] fp32 rows in the workspace
+    g = _desc(B=8, H=8, L=8192, M=256, in_dtype=fv.F32, out_dtype=fv.F32)
+    assert fv.workspace_size(g, 2) > L.favor_noalloc_scratch_bytes()
+    p = ctypes.c_void_p(1 << 20)
+    st = L.favor_attn_both_noalloc(ctypes.byref(g), p, p, p, p, p, p, p, None, None, None,
+                                   None, None)
+    assert st == 3, fv.last_error()
+    assert "static scratch" in fv.last_error()
+    bad = _desc(d=32)
+    assert L.favor_attn_both_noalloc(ctypes.byref(bad), p, p, p, p, p, p, p, None, None, None,
+                                     None, None) == 2
