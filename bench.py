@@ -27,6 +27,17 @@ of random features, one GPU's share of a causal pass sharded eight ways along
 the sequence (the last L/8 tokens from a carried state), the backward pass of
 the step's attention, and the training step (forward saving the row scales,
 then the backward reading them), timed the same way.
+
+Beside the headline, the line carries "feature_map" (favor_feature_map on the
+workload's Q: the materialised feature-map phase) and "workloads": every
+other workload of the configuration list at its full size, each with its step
+time, per-kernel durations and the roofline of its dominant kernel
+(bidir_b8h8 and causal_b8h8 with the draw timed on its own beside the step,
+causal_b8h8 also over three causal segment lengths; causal_long with the
+redraw inside the timed step).
+
+python bench.py --summarize-counters DIR turns rocprofv3 FETCH_SIZE /
+WRITE_SIZE runs (see summarize_counters) into profiles/traffic.json.
 """
 import argparse
 import json
@@ -78,13 +89,13 @@ def measured_traffic(kernel, workload):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("source_sha256") != kernel_source_hash() or t.get("workload") != workload:
+    if t.get("source_sha256") != kernel_source_hash():
         return None
-    k = t.get("kernels", {}).get(kernel)
+    k = t.get("workloads", {}).get(workload, {}).get("kernels", {}).get(kernel)
     return None if k is None else k["bytes_per_launch"]
 
 
-def per_token_head(kernel, d, M, elt):
+def per_token_head(kernel, d, M, elt, out_elt=None):
     """Algorithmic (flops, bytes, cosines) per token-head of one launch of `kernel`.
 
     flops: the feature projections (2 d M each side computed) and the
@@ -94,12 +105,15 @@ def per_token_head(kernel, d, M, elt):
     proj = 2 * d * M
     contr = 2 * M * (d + 1)
     row = d * elt
+    out_elt = elt if out_elt is None else out_elt
     if kernel == "k_causal":      # Q and K features, Q S + intra, S update; reads Q K V, writes out
         return 2 * proj + 2 * contr, 4 * row, 2 * M
     if kernel == "k_qside":       # Q features, Q' Buf1; reads Q, writes out
         return proj + contr, 2 * row, M
     if kernel == "k_kside":       # K features, K'^T [V 1]; reads K, V
         return proj + contr, 2 * row, M
+    if kernel == "k_feature_map":  # X features; reads X, writes X' (M values per row)
+        return proj, row + M * out_elt, M
     return None
 
 
@@ -111,8 +125,18 @@ def cpu_baseline(w, Q, K, V):
         from threadpoolctl import threadpool_info
         blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
         cores = max((p["num_threads"] for p in blas), default=1)
+        vendor = ", ".join(sorted({f"{p.get('internal_api')} {p.get('version')}" for p in blas}))
     except Exception:
-        cores = 1
+        cores, vendor = 1, "unknown"
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     heads = w.B * w.H
     t0 = time.perf_counter()
     Wr, br = favor.orf_draw(12345, w.H, w.M, w.d)
@@ -122,9 +146,156 @@ def cpu_baseline(w, Q, K, V):
     favor.attn_causal_features(Qp, Kp, V)
     t = time.perf_counter() - t0
     return {"value": heads * w.L / t, "unit": "token-heads/s", "cores": int(cores),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": model, "blas": vendor,
+            "host_cpus_available": len(os.sched_getaffinity(0)),
             "sample": f"whole workload ({w.B}x{w.H} heads x L={w.L}): ORF draw + bidirectional "
                       f"+ causal in fp64 NumPy, {t:.2f} s wall"}
+
+
+def roofline(kernels, w, token_heads, out_elt=None):
+    """Roofline entry of the kernel with the largest share of the step: its
+    algorithmic FLOP, bytes and cosines per launch over its average launch
+    duration against the MI355X peaks; the reported bound is the resource with
+    the largest fraction."""
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_launch"] * kernels[k]["launches_per_step"])
+    elt = 2 if w.dtype == "bf16" else 4
+    costs = per_token_head(dom, w.d, w.M, elt, out_elt)
+    if costs is None:
+        return {"kernel": dom, "bound": None}
+    fl, by, cs = costs
+    t = kernels[dom]["ms_per_launch"] / 1e3
+    cand = {
+        "mfma": (fl * token_heads / t / 1e12, PEAK_MFMA_TFLOPS[w.dtype], "TFLOP/s"),
+        "hbm": (by * token_heads / t / 1e9, PEAK_HBM_GBS, "GB/s"),
+        "alu": (cs * token_heads / t / 1e12, PEAK_COS_PER_S / 1e12, "Tcos/s"),
+    }
+    bound = max(cand, key=lambda k: cand[k][0] / cand[k][1])
+    a, p, u = cand[bound]
+    return {"kernel": dom, "bound": bound, "achieved": a, "peak": p, "unit": u, "frac": a / p,
+            "traffic": measured_traffic(dom, w.name),
+            "algorithmic_bytes_per_launch": by * token_heads,
+            "algorithmic_flop_per_launch": fl * token_heads,
+            "others": {k: {"achieved": v[0], "peak": v[1], "unit": v[2], "frac": v[0] / v[1]}
+                       for k, v in cand.items() if k != bound}}
+
+
+def time_steps(torch, fv, stream, step, first, steps, instrumented=False):
+    """Milliseconds per step over `steps` calls of step(first + i), timed with
+    HIP events on `stream` (the library launches on the stream it is given);
+    instrumented also returns the library's per-kernel event times."""
+    torch.cuda.synchronize()
+    if instrumented:
+        fv.timing_reset()
+        fv.timing_enable(True)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(steps):
+        step(first + i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    if not instrumented:
+        return ms
+    fv.timing_enable(False)
+    kt = fv.timing_read()
+    return ms, {k: {"ms_per_launch": v[0] / v[1], "launches_per_step": v[1] / steps}
+                for k, v in kt.items() if v[1] > 0}
+
+
+def bench_workload(name, args, torch, fv, segment_rows=(0,)):
+    """One workload of the configuration list at its full size: the step is its
+    attention call(s) over inputs resident in HBM, with the random-feature draw
+    inside the step when the workload redraws on every call, else timed on its
+    own beside it. Returns its entry for the bench line."""
+    w = wl.WORKLOADS[name]
+    dev = torch.device("cuda", 0)
+    Q, K, V = wl.make_qkv(w)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    up = lambda x: torch.from_numpy(x).to(device=dev, dtype=tdt).contiguous()
+    Qd, Kd, Vd = up(Q), up(K), up(V)
+    del Q, K, V
+    s, H, M = w.input_scale, w.H, w.M
+    code = fv.BF16 if w.dtype == "bf16" else fv.F32
+    Wd = torch.empty((H, M, w.d), dtype=torch.float32, device=dev)
+    bd = torch.empty((H, M), dtype=torch.float32, device=dev)
+    out = torch.empty_like(Qd)
+    out2 = torch.empty_like(Qd)
+    st = torch.cuda.current_stream()
+    op = {"bidir": 0, "causal": 1, "both": 2}[w.direction]
+    th = w.B * w.H * w.L
+    first = 0
+    entry = {"config": {"B": w.B, "H": H, "L": w.L, "d": w.d, "M": M, "dtype": w.dtype,
+                        "direction": w.direction,
+                        "orf_draw": "inside the timed step (redrawn every call)" if w.redraw
+                        else "outside the timed step (timed on its own)"}}
+    fv.orf_draw(77, H, M, w.d, W=Wd, b=bd, stream=st)
+    sweep = {}
+    for rows in segment_rows:
+        g = fv.make_desc(w.B, H, w.L, w.d, M, code, code, s, chunk=rows)
+        ws = torch.empty(fv.workspace_size(g, op), dtype=torch.uint8, device=dev)
+
+        def step(i):
+            if w.redraw:
+                fv.orf_draw(1000 + i, H, M, w.d, W=Wd, b=bd, stream=st)
+            if op == 0:
+                fv.attn_bidir(Qd, Kd, Vd, Wd, bd, s, out=out, workspace=ws, stream=st)
+            elif op == 1:
+                fv.attn_causal(Qd, Kd, Vd, Wd, bd, s, out=out, workspace=ws, stream=st,
+                               chunk=rows)
+            else:
+                fv.attn_both(Qd, Kd, Vd, Wd, bd, s, out_bidir=out, out_causal=out2,
+                             workspace=ws, stream=st, chunk=rows)
+
+        t0 = time.perf_counter()
+        n = 0
+        while n < args.warmup or time.perf_counter() - t0 < args.min_warmup_seconds:
+            step(first + n)
+            n += 1
+            if n % 16 == 0:
+                torch.cuda.synchronize()
+        first += n
+        ms = time_steps(torch, fv, st, step, first, args.steps)
+        first += args.steps
+        ms_i, kernels = time_steps(torch, fv, st, step, first, args.steps, instrumented=True)
+        first += args.steps
+        sweep[rows] = {"ms_per_step": ms, "value": th / (ms / 1e3),
+                       "ms_per_step_instrumented": ms_i, "kernels": kernels,
+                       "roofline": roofline(kernels, w, th)}
+    best = sweep[segment_rows[0]]
+    entry.update(best)
+    if len(segment_rows) > 1:
+        entry["causal_segment_rows_sweep"] = {
+            ("library default" if r == 0 else str(r)): {"ms_per_step": v["ms_per_step"],
+                                                         "value": v["value"]}
+            for r, v in sweep.items()}
+    if not w.redraw:
+        draw = lambda i: fv.orf_draw(1000 + i, H, M, w.d, W=Wd, b=bd, stream=st)
+        for i in range(args.warmup):
+            draw(first + i)
+        first += args.warmup
+        entry["ms_orf_draw"] = time_steps(torch, fv, st, draw, first, args.steps)
+    return entry
+
+
+def bench_feature_map(w, Qd, Wd, bd, args, torch, fv):
+    """favor_feature_map on the workload's Q with bf16 (or the input dtype's) X'
+    of all M features: the materialised feature-map phase (Sec. 2.3)."""
+    st = torch.cuda.current_stream()
+    Xp = torch.empty((w.B, w.H, w.L, w.M), dtype=Qd.dtype, device=Qd.device)
+    step = lambda i: fv.feature_map(Qd, Wd, bd, w.input_scale, out=Xp, stream=st)
+    for i in range(max(args.warmup, 20)):
+        step(i)
+    ms = time_steps(torch, fv, st, step, 0, args.steps)
+    ms_i, kernels = time_steps(torch, fv, st, step, 0, args.steps, instrumented=True)
+    th = w.B * w.H * w.L
+    elt = Qd.element_size()
+    roof = roofline(kernels, w, th, out_elt=elt)
+    del Xp
+    return {"what": f"X' = phi(Q) of the {w.name} workload ({w.B}x{w.H} heads x L={w.L}, "
+                    f"M={w.M}), {w.dtype} in and out",
+            "ms_per_call": ms, "value": th / (ms / 1e3), "ms_per_call_instrumented": ms_i,
+            "kernels": kernels, "roofline": roof}
 
 
 def copy_reference(nbytes, steps, warmup):
@@ -149,6 +320,68 @@ def copy_reference(nbytes, steps, warmup):
                       "GB_per_s_read_plus_write": 2 * n * 4 / (ms / 1e3) / 1e9}), flush=True)
 
 
+COUNTERS = ("FETCH_SIZE", "WRITE_SIZE")
+COPY_KIB = 262144.0      # the calibration copy: 256 MiB read and 256 MiB written
+
+
+def _short_kernel(name):
+    for k in ("k_causal", "k_orf_draw", "k_kside", "k_qside", "k_seg_scan", "k_finalize",
+              "k_feature_map"):
+        if k in name:
+            return k
+    if "copyBuffer" in name or "rocclr" in name or "elementwise" in name.lower():
+        return "copy"
+    return name[:40]
+
+
+def _pmc_means(path):
+    import collections
+    import csv
+    agg = collections.defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            agg[_short_kernel(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in agg.items()}
+
+
+def summarize_counters(root):
+    """profiles/traffic.json from rocprofv3 --pmc runs, one counter per run:
+    <root>/pmc_<COUNTER>_<workload>/run_counter_collection.csv for each workload
+    and <root>/pmccopy_<COUNTER>/... for the calibration copy (bench.py
+    --copy-bytes 268435456). Each counter's KiB per dispatch is scaled by what it
+    reads for the copy, whose true traffic is 256 MiB each way."""
+    import glob
+    scale = {}
+    for c in COUNTERS:
+        copy = _pmc_means(os.path.join(root, f"pmccopy_{c}", "run_counter_collection.csv"))
+        scale[c] = COPY_KIB / copy["copy"]
+    out = {"source_sha256": kernel_source_hash(),
+           "fetch_scale": scale["FETCH_SIZE"], "write_scale": scale["WRITE_SIZE"],
+           "commands": {
+               "counter": "rocprofv3 --pmc <COUNTER> --output-format csv -d "
+                          "gpurun_out/pmc/pmc_<COUNTER>_<workload> -o run -- python3 bench.py "
+                          "--workload <workload> --steps 3 --warmup 1 --min-warmup-seconds 0 "
+                          "--no-cpu-baseline --no-variants --workloads ''",
+               "copy": "rocprofv3 --pmc <COUNTER> --output-format csv -d "
+                       "gpurun_out/pmc/pmccopy_<COUNTER> -o run -- python3 bench.py "
+                       "--copy-bytes 268435456 --steps 3 --warmup 1",
+               "summary": "python3 bench.py --summarize-counters gpurun_out/pmc"},
+           "workloads": {}}
+    for d in sorted(glob.glob(os.path.join(root, "pmc_FETCH_SIZE_*"))):
+        name = os.path.basename(d)[len("pmc_FETCH_SIZE_"):]
+        fetch = _pmc_means(os.path.join(d, "run_counter_collection.csv"))
+        write = _pmc_means(os.path.join(root, f"pmc_WRITE_SIZE_{name}",
+                                        "run_counter_collection.csv"))
+        out["workloads"][name] = {"kernels": {
+            k: {"fetch_kib_raw": v, "write_kib_raw": write.get(k, 0.0),
+                "bytes_per_launch": (v * scale["FETCH_SIZE"]
+                                     + write.get(k, 0.0) * scale["WRITE_SIZE"]) * 1024}
+            for k, v in fetch.items()}}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out, indent=1))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -169,11 +402,23 @@ def main():
                     default="relu,softmax_no_renormalize,draws,causal_shard,backward,"
                             "train_step",
                     help="comma-separated variants to time after the headline step")
+    ap.add_argument("--workloads", default="bidir_b8h8,causal_b8h8,causal_long",
+                    help="comma-separated further workloads of the configuration list, each "
+                         "timed at full size into the line's 'workloads' object ('' = none)")
+    ap.add_argument("--no-feature-map", action="store_true",
+                    help="skip the materialised feature-map phase (favor_feature_map)")
+    ap.add_argument("--summarize-counters", default="",
+                    help="instead of running, read the rocprofv3 FETCH_SIZE / WRITE_SIZE CSVs "
+                         "under this directory (pmc_<COUNTER>_<workload>/ and "
+                         "pmccopy_<COUNTER>/) and write profiles/traffic.json")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="instead of the workload, time a plain device-to-device copy of this "
                          "many bytes (reference for HBM bandwidth and for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FAVOR path "
               "shards over heads with no communication between GPUs", file=sys.stderr)
@@ -448,27 +693,19 @@ def main():
 
     token_heads = w.B * w.H * w.L
     value = token_heads / (ms_step / 1e3)
+    roof = roofline(kernels, w, token_heads)
 
-    # roofline of the kernel with the largest share of the step
-    dom = max(kernels, key=lambda k: kernels[k]["ms_per_launch"] * kernels[k]["launches_per_step"])
-    roof = None
-    elt = 2 if w.dtype == "bf16" else 4
-    costs = per_token_head(dom, w.d, M, elt)
-    if costs is not None:
-        fl, by, cs = costs
-        t = kernels[dom]["ms_per_launch"] / 1e3
-        cand = {
-            "mfma": (fl * token_heads / t / 1e12, PEAK_MFMA_TFLOPS[w.dtype], "TFLOP/s"),
-            "hbm": (by * token_heads / t / 1e9, PEAK_HBM_GBS, "GB/s"),
-            "alu": (cs * token_heads / t / 1e12, PEAK_COS_PER_S / 1e12, "Tcos/s"),
-        }
-        bound = max(cand, key=lambda k: cand[k][0] / cand[k][1])
-        a, p, u = cand[bound]
-        roof = {"kernel": dom, "bound": bound, "achieved": a, "peak": p, "unit": u,
-                "frac": a / p, "traffic": measured_traffic(dom, w.name),
-                "algorithmic_bytes_per_launch": by * token_heads,
-                "others": {k: {"achieved": v[0], "peak": v[1], "unit": v[2],
-                               "frac": v[0] / v[1]} for k, v in cand.items() if k != bound}}
+    feature_map = None
+    if not args.no_feature_map:
+        feature_map = bench_feature_map(w, Qd, Wd[0], bd[0], args, torch, fv)
+    # the other workloads of the configuration list, each at its full size
+    others = {}
+    names = [n for n in args.workloads.split(",") if n and n != w.name]
+    if names:
+        del Wd, bd, out_b, out_c, ws, Qd, Kd, Vd
+        for name in names:
+            rows = (0, 1024, 4096) if name == "causal_b8h8" else (0,)
+            others[name] = bench_workload(name, args, torch, fv, segment_rows=rows)
 
     res = {
         "metric": "FAVOR attention tokens/sec (B*H*L/s) + % of MFMA/HBM peak at L=8192, M=256",
@@ -493,6 +730,8 @@ def main():
         "ms_per_step_pipelined": ms_step_pipelined,
         "ms_per_step_instrumented": ms_step_instrumented,
         "roofline": roof,
+        "feature_map": feature_map,
+        "workloads": others,
         "variants": variants,
     }
     if not args.no_cpu_baseline:
