@@ -26,7 +26,7 @@
  * rounded up to 64, 128 or 256 rows, the rows past M being padding whose
  * features are zero, so every array above keeps M; the causal scan with F32
  * inputs and M > 128 runs as two passes over the feature halves);
- * L >= 0 (any length, ragged tails handled; L = 0 is a no-op); B, H >= 0,
+ * 0 <= L <= 2^30 (any length, ragged tails handled; L = 0 is a no-op); B, H >= 0,
  * B*H <= 65535; in_dtype F32 or BF16; out_dtype F32 or BF16. F32 inputs use
  * fp32 matrix cores and an accurately rounded cosine; BF16 inputs use bf16
  * matrix cores with fp32 accumulation, the hardware cosine and bf16 features.

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstring>
 #include <string>
 
 #include "../../include/favor.h"
@@ -32,6 +33,17 @@ favor_status ok() {
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// The integer a caller stored in an enum-typed field or argument. A C caller
+// may pass any int there, and in C++ reading an enum object that holds a value
+// outside its enumerators is undefined, so validation reads the bytes.
+static_assert(sizeof(favor_dtype) == sizeof(int) && sizeof(favor_rf_kind) == sizeof(int),
+              "the enums of the C ABI are int-sized");
+int raw_enum(const void *p) {
+  int v;
+  std::memcpy(&v, p, sizeof v);
+  return v;
+}
+
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Rows the kernels work on for M features: 64, 128 or 256 (the rows past M are
@@ -43,6 +55,9 @@ constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
 // so its segments are sized for one workgroup per CU
 constexpr int kCausalWorkgroups = 256;
 constexpr int kMinRowsPerSplit = 256;
+// Longest sequence per head (and longest causal segment): the kernels index
+// tokens with 32-bit integers and step past the end by up to two tiles.
+constexpr int kMaxL = 1 << 30;
 
 enum Op {
   kOpFeatureMap = 0,
@@ -61,10 +76,11 @@ favor_status validate(const favor_desc *g, int op) {
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "negative size B=%d H=%d L=%d", g->B, g->H, g->L);
   if (g->d <= 0 || g->M <= 0)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "d=%d and M=%d must be positive", g->d, g->M);
-  if (g->in_dtype != FAVOR_F32 && g->in_dtype != FAVOR_BF16)
-    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown in_dtype %d", (int)g->in_dtype);
-  if (g->out_dtype != FAVOR_F32 && g->out_dtype != FAVOR_BF16)
-    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown out_dtype %d", (int)g->out_dtype);
+  const int in_dt = raw_enum(&g->in_dtype), out_dt = raw_enum(&g->out_dtype);
+  if (in_dt != FAVOR_F32 && in_dt != FAVOR_BF16)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown in_dtype %d", in_dt);
+  if (out_dt != FAVOR_F32 && out_dt != FAVOR_BF16)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown out_dtype %d", out_dt);
   if (!std::isfinite(g->input_scale))
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "input_scale must be finite");
   if (!std::isfinite(g->denom_eps) || g->denom_eps < 0.f)
@@ -78,6 +94,8 @@ favor_status validate(const favor_desc *g, int op) {
   if (g->chunk < 0 || g->chunk % 64 != 0)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "chunk=%d must be a non-negative multiple of 64",
                 g->chunk);
+  if (g->L > kMaxL) return fail(FAVOR_ERR_UNSUPPORTED, "L=%d exceeds 2^30", g->L);
+  if (g->chunk > kMaxL) return fail(FAVOR_ERR_UNSUPPORTED, "chunk=%d exceeds 2^30", g->chunk);
   if (g->d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", g->d);
   if (g->M % 16 != 0 || g->M > 256)
     return fail(FAVOR_ERR_UNSUPPORTED, "M=%d not supported (a multiple of 16, at most 256)",
@@ -123,6 +141,7 @@ Plan make_plan(const favor_desc *g, int op) {
   Plan p;
   p.BH = g->B * g->H;
   if (p.BH == 0 || g->L == 0) return p;
+  // L and chunk are at most 2^30 (validated), so these stay within int
   const int tiles = (g->L + 63) / 64;
   int rows;
   if (causal && g->chunk > 0) {
@@ -140,7 +159,7 @@ Plan make_plan(const favor_desc *g, int op) {
     rows = 64 * ((tiles + want - 1) / want);
   }
   p.rows_per_split = rows;
-  p.nsplit = (g->L + rows - 1) / rows;
+  p.nsplit = (int)(((long long)g->L + rows - 1) / rows);
   const int M = padded_m(g->M);
   p.part_bytes = round_up((size_t)p.BH * p.nsplit * M * 65 * sizeof(float), 256);
   const int fb = g->in_dtype == FAVOR_BF16 ? 16 : 32;
@@ -273,9 +292,10 @@ favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d
                             favor_rf_kind kind, float *W, float *b, void *stream) {
   if (n_heads < 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "n_heads=%d is negative", n_heads);
   if (M <= 0 || d <= 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "M=%d d=%d must be positive", M, d);
-  if (kind != FAVOR_RF_ORTHO_CHI && kind != FAVOR_RF_ORTHO_FIXED && kind != FAVOR_RF_IID &&
-      kind != FAVOR_RF_HADAMARD && kind != FAVOR_RF_GIVENS)
-    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown random-feature kind %d", (int)kind);
+  const int k = raw_enum(&kind);
+  if (k != FAVOR_RF_ORTHO_CHI && k != FAVOR_RF_ORTHO_FIXED && k != FAVOR_RF_IID &&
+      k != FAVOR_RF_HADAMARD && k != FAVOR_RF_GIVENS)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown random-feature kind %d", k);
   if (d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", d);
   if (M > 4096) return fail(FAVOR_ERR_UNSUPPORTED, "M=%d exceeds 4096", M);
   if (n_heads > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "n_heads=%d exceeds 65535", n_heads);
@@ -286,7 +306,7 @@ favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d
   hipError_t e;
   {
     favor::LaunchTimer t(favor::kKerOrfDraw, (hipStream_t)stream);
-    e = favor::launch_orf_draw(seed, n_heads, M, (int)kind, W, b, (hipStream_t)stream);
+    e = favor::launch_orf_draw(seed, n_heads, M, k, W, b, (hipStream_t)stream);
   }
   return device_result(e, "favor_orf_draw launch");
 }

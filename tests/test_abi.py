@@ -79,6 +79,10 @@ def _desc(**kw):
     (dict(kernel=fv.KERNEL_RELU, kernel_eps=-1e-3), 1),
     (dict(kernel=fv.KERNEL_RELU, kernel_eps=float("inf")), 1),
     (dict(kernel_eps=-1.0), 0),   # kernel_eps is not read for softmax features
+    (dict(L=1 << 30), 0),         # the longest sequence per head
+    (dict(L=(1 << 30) + 1), 2),
+    (dict(chunk=1 << 30), 0),
+    (dict(chunk=(1 << 30) + 64), 2),
 ])
 def test_validate_desc(kw, status):
     for op in (fv.OP_FEATURE_MAP, fv.OP_BIDIR, fv.OP_CAUSAL, fv.OP_BOTH):
