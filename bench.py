@@ -203,6 +203,45 @@ def time_steps(torch, fv, stream, step, first, steps, instrumented=False):
                 for k, v in kt.items() if v[1] > 0}
 
 
+def measured_peaks(torch, fv):
+    """Rates this GPU reaches on the resources the roofline uses, beside the
+    published peaks: bf16 matrix-core FLOP/s and cosines/s from the library's
+    probes (favor_probe), HBM bytes/s from a 1 GiB device copy (read + write).
+    Best of five launches each."""
+    st = torch.cuda.current_stream()
+    sink = torch.zeros(512, dtype=torch.float32, device="cuda")
+    out = {}
+
+    def best(fn, n=5):
+        ts = []
+        for _ in range(n + 1):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            fn()
+            e1.record(st)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / 1e3)
+        return min(ts[1:])
+
+    for kind, iters, key, scale in ((0, 400, "mfma_bf16_tflops", 1e12),
+                                    (1, 20000, "cos_per_s", 1.0)):
+        import ctypes
+        run = lambda: fv.lib().favor_probe(kind, iters, ctypes.c_void_p(sink.data_ptr()),
+                                           ctypes.c_void_p(st.cuda_stream))
+        t = best(run)
+        out[key] = fv.lib().favor_probe_work(kind, iters) / t / scale
+    n = (1 << 30) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    t = best(lambda: dst.copy_(src))
+    out["hbm_copy_gbs"] = 2 * n * 4 / t / 1e9
+    out["published"] = {"mfma_bf16_tflops": PEAK_MFMA_TFLOPS["bf16"], "cos_per_s": PEAK_COS_PER_S,
+                        "hbm_gbs": PEAK_HBM_GBS}
+    del src, dst
+    return out
+
+
 def bench_workload(name, args, torch, fv, segment_rows=(0,)):
     """One workload of the configuration list at its full size: the step is its
     attention call(s) over inputs resident in HBM, with the random-feature draw
@@ -405,6 +444,8 @@ def main():
     ap.add_argument("--workloads", default="bidir_b8h8,causal_b8h8,causal_long",
                     help="comma-separated further workloads of the configuration list, each "
                          "timed at full size into the line's 'workloads' object ('' = none)")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the measured-peak probes (matrix cores, cosines, device copy)")
     ap.add_argument("--no-feature-map", action="store_true",
                     help="skip the materialised feature-map phase (favor_feature_map)")
     ap.add_argument("--summarize-counters", default="",
@@ -695,6 +736,7 @@ def main():
     value = token_heads / (ms_step / 1e3)
     roof = roofline(kernels, w, token_heads)
 
+    peaks = None if args.no_peaks else measured_peaks(torch, fv)
     feature_map = None
     if not args.no_feature_map:
         feature_map = bench_feature_map(w, Qd, Wd[0], bd[0], args, torch, fv)
@@ -730,6 +772,7 @@ def main():
         "ms_per_step_pipelined": ms_step_pipelined,
         "ms_per_step_instrumented": ms_step_instrumented,
         "roofline": roof,
+        "measured_peaks": peaks,
         "feature_map": feature_map,
         "workloads": others,
         "variants": variants,

@@ -70,6 +70,8 @@ def lib():
         "favor_attn_both_noalloc": (ctypes.c_int,
                                     [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "favor_noalloc_scratch_bytes": (sz, []),
+        "favor_probe": (ctypes.c_int, [i32, i32, vp, vp]),
+        "favor_probe_work": (ctypes.c_double, [i32, i32]),
         "favor_backward_workspace_size": (sz, [dp, ctypes.c_int]),
         "favor_attn_bidir_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                      vp, vp, vp, vp, sz, vp]),

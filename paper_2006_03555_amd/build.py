@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libfavor.so")
 ARCH = "gfx950"
 
 SOURCES = ["orf_draw.hip", "feature_map.hip", "bidir.hip", "causal.hip", "backward.hip",
-           "noalloc.hip", "favor_api.cpp", "timing.cpp"]
+           "noalloc.hip", "probe.hip", "favor_api.cpp", "timing.cpp"]
 
 # Packed fp32 arithmetic is disabled for all device code (no v_pk_*_f32).
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -34,6 +34,9 @@ PER_SOURCE_FLAGS = {
     "bidir.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "causal.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", *_TRACKERS],
     "backward.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", *_TRACKERS],
+    # without it the probe's independent accumulators end up in rotating AGPR
+    # ranges that chain every MFMA to the previous one
+    "probe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall",
                 "-Wno-unused-function", "-I", os.path.join(ROOT, "include")]
