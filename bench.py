@@ -271,7 +271,7 @@ def bench_workload(name, args, torch, fv, segment_rows=(0,)):
     fv.orf_draw(77, H, M, w.d, W=Wd, b=bd, stream=st)
     sweep = {}
     for rows in segment_rows:
-        g = fv.make_desc(w.B, H, w.L, w.d, M, code, code, s, chunk=rows)
+        g = fv.make_desc(w.B, H, w.L, w.d, M, code, code, s, segment=rows)
         ws = torch.empty(fv.workspace_size(g, op), dtype=torch.uint8, device=dev)
 
         def step(i):
@@ -281,10 +281,10 @@ def bench_workload(name, args, torch, fv, segment_rows=(0,)):
                 fv.attn_bidir(Qd, Kd, Vd, Wd, bd, s, out=out, workspace=ws, stream=st)
             elif op == 1:
                 fv.attn_causal(Qd, Kd, Vd, Wd, bd, s, out=out, workspace=ws, stream=st,
-                               chunk=rows)
+                               segment=rows)
             else:
                 fv.attn_both(Qd, Kd, Vd, Wd, bd, s, out_bidir=out, out_causal=out2,
-                             workspace=ws, stream=st, chunk=rows)
+                             workspace=ws, stream=st, segment=rows)
 
         t0 = time.perf_counter()
         n = 0
@@ -430,7 +430,7 @@ def main():
                     help="keep running untimed warmup steps until this long has passed "
                          "(the GPU clocks settle over a few hundred milliseconds)")
     ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
-    ap.add_argument("--chunk", type=int, default=0,
+    ap.add_argument("--segment", type=int, default=0,
                     help="rows per segment of the causal scan (a multiple of 64; 0 = the "
                          "library's choice, one workgroup per CU) for the forward steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -488,7 +488,7 @@ def main():
     out_b = torch.empty_like(Qd)
     out_c = torch.empty_like(Qd)
     g = fv.make_desc(w.B, H, w.L, w.d, M, fv.BF16 if w.dtype == "bf16" else fv.F32,
-                     fv.BF16 if w.dtype == "bf16" else fv.F32, s, chunk=args.chunk)
+                     fv.BF16 if w.dtype == "bf16" else fv.F32, s, segment=args.segment)
     op = {"bidir": 0, "causal": 1, "both": 2}[w.direction]
     ws = torch.empty(fv.workspace_size(g, op), dtype=torch.uint8, device=dev)
     s_main = torch.cuda.current_stream()
@@ -499,7 +499,7 @@ def main():
     def attention(slot, opts=None):
         opts = dict(opts or {})
         if op != 0:
-            opts["chunk"] = args.chunk
+            opts["segment"] = args.segment
         if op == 2:     # one key pass serves both directions
             fv.attn_both(Qd, Kd, Vd, Wd[slot], bd[slot], s, out_bidir=out_b, out_causal=out_c,
                          workspace=ws, stream=s_main, **opts)
@@ -589,7 +589,7 @@ def main():
     # renormalisation: same draw, same launches, other feature epilogue / finalisation
     variants = {}
     chosen = set() if args.no_variants else set(args.variants.split(","))
-    if args.chunk:   # the backward calls take the library's segments
+    if args.segment:   # the backward calls take the library's segments
         chosen -= {"backward", "train_step"}
     for name, opts in (("relu", dict(kernel=fv.KERNEL_RELU)),
                        ("softmax_no_renormalize", dict(renormalize=False))):
@@ -764,7 +764,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": M,
                    "direction": w.direction, "orf_draw_per_step": True,
-                   "causal_segment_rows": args.chunk or "library default",
+                   "causal_segment_rows": args.segment or "library default",
+                   "causal_chunk_tokens": 64,
                    "orf_draw": "drawn in line before the attention pass, same stream",
                    "parallelism": "single GPU"},
         "kernels": kernels,

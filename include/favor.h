@@ -5,8 +5,8 @@
  * Every tensor argument is a DEVICE pointer owned by the caller; the library
  * never allocates, frees or retains device memory (scratch is the caller's
  * workspace; the one exception is the static scratch array each GPU holds for
- * favor_attn_both_noalloc). Every call is asynchronous: work is enqueued on `stream` (a
- * hipStream_t passed as void*, NULL = the default stream) and nothing waits.
+ * favor_attn_both_noalloc). Every call is asynchronous: work is enqueued on `stream`
+ * (NULL = the default stream) and nothing waits.
  *
  * Errors: arguments are validated completely before anything is launched. On
  * failure a call returns a non-zero favor_status, writes no output and records
@@ -47,6 +47,12 @@
 extern "C" {
 #endif
 
+/* The HIP runtime's stream handle (the same declaration as in
+ * hip/hip_runtime_api.h, so either header may come first). NULL is the default
+ * stream. */
+struct ihipStream_t;
+typedef struct ihipStream_t *hipStream_t;
+
 typedef enum {
   FAVOR_OK = 0,
   FAVOR_ERR_INVALID_ARGUMENT = 1,  /* null/misaligned pointer, negative size, bad enum */
@@ -80,14 +86,22 @@ typedef struct {
   float input_scale;        /* x~ = input_scale * x. d^-1/4 evaluates the paper's
                                exp(Q K^T / sqrt d) (Sec. 2.1) on the given Q, K.  */
   float denom_eps;          /* added to D-hat before dividing; 0 = Algorithm 1      */
-  int32_t chunk;            /* causal: tokens per segment handled by one workgroup
-                               (multiple of 64); 0 = library default                */
+  int32_t chunk;            /* causal chunk length T: tokens per step of the
+                               prefix-sum scan (Sec. 2.5.1); 0 = library default.
+                               The kernels take T = 64, the matrix-core tile of
+                               the intra-chunk product; other values return
+                               FAVOR_ERR_UNSUPPORTED                               */
   int32_t kernel;           /* favor_kernel; 0 (zero-initialised) = SOFTMAX         */
   int32_t no_renormalize;   /* 0 = out = Buf3 / (buf4 + denom_eps) (Algorithm 1);
                                1 = out = Buf3 = Q' K'^T V ("renormalize_attention"
                                off, App. B; denom_eps is then unused)             */
   float kernel_eps;         /* RELU: added to every feature (App. B kernel_epsilon,
                                default 1e-3); ignored for SOFTMAX                  */
+  int32_t segment;          /* causal: tokens per segment, the stretch of the
+                               sequence one workgroup scans chunk by chunk from
+                               the aggregate of the segments before it (a multiple
+                               of 64, at most 2^30); 0 = library default (about one
+                               workgroup per compute unit)                         */
 } favor_desc;
 
 /*
@@ -123,7 +137,7 @@ typedef struct {
  * aligned, b 4-byte aligned.
  */
 FAVOR_API favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d,
-                            favor_rf_kind kind, float *W, float *b, void *stream);
+                            favor_rf_kind kind, float *W, float *b, hipStream_t stream);
 
 /*
  * favor_feature_map - X' = D_X X-hat, the paper's Q' = D_Q Q-hat (Sec. 2.3,
@@ -136,7 +150,7 @@ FAVOR_API favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M,
  * g->denom_eps, g->chunk and g->no_renormalize are ignored.
  */
 FAVOR_API favor_status favor_feature_map(const favor_desc *g, const void *X, const float *W,
-                               const float *b, void *Xprime, void *stream);
+                               const float *b, void *Xprime, hipStream_t stream);
 
 /*
  * favor_workspace_size - bytes of device workspace favor_attn_bidir (causal = 0),
@@ -153,13 +167,21 @@ FAVOR_API size_t favor_workspace_size(const favor_desc *g, int causal);
  * where Q', K' are the feature maps of favor_feature_map for g->kernel. With
  * g->no_renormalize = 1 the result is Buf3 itself. The L x L matrix Q' K'^T and
  * the L x M features are never stored. Deterministic (no atomics).
- * row_scale (nullable) [B][H][L] fp32: receives each row's 1 / (buf4 + denom_eps)
- * in units of the features without D_Q sqrt(2/M), for the backward pass; needs
- * out_dtype == in_dtype; not written without renormalisation.
  */
 FAVOR_API favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
                               const void *V, const float *W, const float *b, void *out,
-                              float *row_scale, void *ws, size_t ws_bytes, void *stream);
+                              void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * favor_attn_bidir_save - favor_attn_bidir that also writes, for the backward
+ * pass, row_scale [B][H][L] fp32 (nullable): each row's 1 / (buf4 + denom_eps)
+ * in units of the features without D_Q sqrt(2/M). Needs out_dtype == in_dtype;
+ * row_scale is not written without renormalisation.
+ */
+FAVOR_API favor_status favor_attn_bidir_save(const favor_desc *g, const void *Q, const void *K,
+                                             const void *V, const float *W, const float *b,
+                                             void *out, float *row_scale, void *ws,
+                                             size_t ws_bytes, hipStream_t stream);
 
 /*
  * favor_attn_causal - unidirectional FAVOR by prefix sums (Sec. 2.5.1, Eq.
@@ -171,12 +193,19 @@ FAVOR_API favor_status favor_attn_bidir(const favor_desc *g, const void *Q, cons
  * state_in  (nullable) [B][H][M][d+1] fp32: S_0, the aggregate of earlier tokens.
  * state_out (nullable) [B][H][M][d+1] fp32: receives S_0 + sum over all L tokens,
  * so a long sequence can be processed in pieces. Deterministic (no atomics).
- * row_scale (nullable): as for favor_attn_bidir.
  */
 FAVOR_API favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K,
                                const void *V, const float *W, const float *b, void *out,
-                               const float *state_in, float *state_out, float *row_scale,
-                               void *ws, size_t ws_bytes, void *stream);
+                               const float *state_in, float *state_out,
+                               void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* favor_attn_causal_save - favor_attn_causal that also writes row_scale, as
+ * favor_attn_bidir_save does. */
+FAVOR_API favor_status favor_attn_causal_save(const favor_desc *g, const void *Q,
+                                              const void *K, const void *V, const float *W,
+                                              const float *b, void *out, const float *state_in,
+                                              float *state_out, float *row_scale, void *ws,
+                                              size_t ws_bytes, hipStream_t stream);
 
 /*
  * favor_attn_both - both directions over the same Q, K, V in one call: the
@@ -186,14 +215,14 @@ FAVOR_API favor_status favor_attn_causal(const favor_desc *g, const void *Q, con
  * sequence (G^PS_L of Eq. cumsum), so one pass over the keys serves both:
  * the key features are built once per segment and the segment scan also
  * returns the total. Workspace: favor_workspace_size(g, 2). Deterministic.
- * row_scale_bidir, row_scale_causal (nullable): as for favor_attn_bidir.
+ * row_scale_bidir, row_scale_causal (nullable): as for favor_attn_bidir_save.
  */
 FAVOR_API favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K,
                                        const void *V, const float *W, const float *b,
                                        void *out_bidir, void *out_causal,
                                        const float *state_in, float *state_out,
                                        float *row_scale_bidir, float *row_scale_causal,
-                                       void *ws, size_t ws_bytes, void *stream);
+                                       void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * favor_attn_both_noalloc - favor_attn_both for callers that cannot allocate
@@ -214,7 +243,7 @@ FAVOR_API favor_status favor_attn_both_noalloc(const favor_desc *g, const void *
                                                const float *b, void *out_bidir,
                                                void *out_causal, const float *state_in,
                                                float *state_out, float *row_scale_bidir,
-                                               float *row_scale_causal, void *stream);
+                                               float *row_scale_causal, hipStream_t stream);
 
 /* Size in bytes of favor_attn_both_noalloc's static scratch array. */
 FAVOR_API size_t favor_noalloc_scratch_bytes(void);
@@ -248,7 +277,7 @@ FAVOR_API favor_status favor_attn_bidir_backward(const favor_desc *g, const void
                                                  const float *b, const void *dout,
                                                  const void *out, const float *row_scale,
                                                  void *dQ, void *dK, void *dV, void *ws,
-                                                 size_t ws_bytes, void *stream);
+                                                 size_t ws_bytes, hipStream_t stream);
 
 /*
  * favor_attn_causal_backward - gradients of favor_attn_causal (Eq. cumsum):
@@ -267,7 +296,7 @@ FAVOR_API favor_status favor_attn_causal_backward(const favor_desc *g, const voi
                                                   const float *row_scale,
                                                   const float *dstate_out, void *dQ, void *dK,
                                                   void *dV, float *dstate_in, void *ws,
-                                                  size_t ws_bytes, void *stream);
+                                                  size_t ws_bytes, hipStream_t stream);
 
 /* Host-only validation of a descriptor for an operation (0 feature map,
  * 1 bidirectional, 2 causal, 3 both, 4 bidirectional backward, 5 causal
@@ -303,13 +332,13 @@ FAVOR_API favor_status favor_timing_read(int32_t k, double *ms, int64_t *count);
  * 1) by its duration gives the rate this GPU reaches. sink: a device buffer of
  * at least 512 floats (never written for the probe's inputs).
  */
-FAVOR_API favor_status favor_probe(int32_t kind, int32_t iters, float *sink, void *stream);
+FAVOR_API favor_status favor_probe(int32_t kind, int32_t iters, float *sink, hipStream_t stream);
 FAVOR_API double favor_probe_work(int32_t kind, int32_t iters);
 
 /* ABI version of this header; bumped on any incompatible change. */
 FAVOR_API int32_t favor_abi_version(void);
 
-#define FAVOR_ABI_VERSION 4
+#define FAVOR_ABI_VERSION 5
 
 #ifdef __cplusplus
 }

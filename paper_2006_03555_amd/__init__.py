@@ -124,7 +124,7 @@ def _require_features(W, b, H, M, d):
     _require_like(b, (H, M), torch.float32, "b")
 
 
-def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0, others=(), opts=None):
+def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, segment=0, others=(), opts=None):
     """Descriptor for inputs X [B, H, L, d] (and tensors `others` of the same shape
     and dtype) with features W [H, M, d], b [H, M]."""
     if X.dim() != 4:
@@ -137,7 +137,7 @@ def _desc_for(X, W, input_scale, out_dtype, denom_eps=0.0, chunk=0, others=(), o
     M = W.shape[1]
     in_code = _dtype_code(X.dtype)
     out_code = in_code if out_dtype is None else _dtype_code(out_dtype)
-    return make_desc(B, H, L, d, M, in_code, out_code, input_scale, denom_eps, chunk,
+    return make_desc(B, H, L, d, M, in_code, out_code, input_scale, denom_eps, segment,
                      **(opts or {}))
 
 
@@ -199,22 +199,28 @@ def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=No
     _require_row_scale(row_scale, g, "row_scale")
     _require_cuda(Q, K, V, W, b, out, row_scale)
     ws, nbytes = _workspace(g, 0, workspace)
-    _check(lib().favor_attn_bidir(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
-                                  _ptr(out), _ptr(row_scale), _ptr(ws), ctypes.c_size_t(nbytes),
-                                  _stream(stream)))
+    if row_scale is None:
+        _check(lib().favor_attn_bidir(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W),
+                                      _ptr(b), _ptr(out), _ptr(ws), ctypes.c_size_t(nbytes),
+                                      _stream(stream)))
+    else:
+        _check(lib().favor_attn_bidir_save(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W),
+                                           _ptr(b), _ptr(out), _ptr(row_scale), _ptr(ws),
+                                           ctypes.c_size_t(nbytes), _stream(stream)))
     return out
 
 
 @_on_stream
 def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
-                chunk=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None,
+                segment=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None,
                 kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3, row_scale=None):
-    """Unidirectional FAVOR by prefix sums (favor_attn_causal).
+    """Unidirectional FAVOR by prefix sums (favor_attn_causal; favor_attn_causal_save
+    when row_scale is given). segment: rows per causal segment (0 = library default).
 
     Returns out, or (out, state_out [B, H, M, d+1]) when return_state is true.
     """
     torch = _torch()
-    g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps, chunk,
+    g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps, segment,
                   others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     sshape = (g.B, g.H, g.M, g.d + 1)
@@ -228,15 +234,21 @@ def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return
     _require_row_scale(row_scale, g, "row_scale")
     _require_cuda(Q, K, V, W, b, out, state_in, state_out, row_scale)
     ws, nbytes = _workspace(g, 1, workspace)
-    _check(lib().favor_attn_causal(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b),
-                                   _ptr(out), _ptr(state_in), _ptr(state_out), _ptr(row_scale),
-                                   _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
+    if row_scale is None:
+        _check(lib().favor_attn_causal(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W),
+                                       _ptr(b), _ptr(out), _ptr(state_in), _ptr(state_out),
+                                       _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
+    else:
+        _check(lib().favor_attn_causal_save(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W),
+                                            _ptr(b), _ptr(out), _ptr(state_in), _ptr(state_out),
+                                            _ptr(row_scale), _ptr(ws), ctypes.c_size_t(nbytes),
+                                            _stream(stream)))
     return (out, state_out) if return_state else out
 
 
 @_on_stream
 def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
-              chunk=0, out_dtype=None, out_bidir=None, out_causal=None, state_out=None,
+              segment=0, out_dtype=None, out_bidir=None, out_causal=None, state_out=None,
               workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
               kernel_eps=1e-3, row_scale_bidir=None, row_scale_causal=None):
     """Both directions over the same inputs with one key pass (favor_attn_both).
@@ -244,7 +256,7 @@ def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_s
     Returns (out_bidir, out_causal) or (out_bidir, out_causal, state_out).
     """
     torch = _torch()
-    g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out_bidir, Q), denom_eps, chunk,
+    g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out_bidir, Q), denom_eps, segment,
                   others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     odt = _torch_dtype(g.out_dtype)
@@ -275,7 +287,7 @@ def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_s
 
 @_on_stream
 def attn_both_noalloc(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None,
-                      chunk=0, out_bidir=None, out_causal=None, state_out=None, stream=None,
+                      segment=0, out_bidir=None, out_causal=None, state_out=None, stream=None,
                       kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3,
                       row_scale_bidir=None, row_scale_causal=None):
     """attn_both with the library's static scratch as workspace
@@ -283,7 +295,7 @@ def attn_both_noalloc(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None,
     Returns (out_bidir, out_causal)."""
     torch = _torch()
     odt = out_bidir.dtype if out_bidir is not None else Q.dtype
-    g = _desc_for(Q, W, input_scale, odt, denom_eps, chunk,
+    g = _desc_for(Q, W, input_scale, odt, denom_eps, segment,
                   others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
     _require_features(W, b, g.H, g.M, g.d)
     tdt = _torch_dtype(g.out_dtype)

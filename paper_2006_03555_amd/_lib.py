@@ -39,6 +39,7 @@ class FavorDesc(ctypes.Structure):
         ("chunk", ctypes.c_int32),
         ("kernel", ctypes.c_int32), ("no_renormalize", ctypes.c_int32),
         ("kernel_eps", ctypes.c_float),
+        ("segment", ctypes.c_int32),
     ]
 
 
@@ -62,9 +63,12 @@ def lib():
         "favor_orf_draw": (ctypes.c_int, [u64, i32, i32, i32, ctypes.c_int, vp, vp, vp]),
         "favor_feature_map": (ctypes.c_int, [dp, vp, vp, vp, vp, vp]),
         "favor_workspace_size": (sz, [dp, ctypes.c_int]),
-        "favor_attn_bidir": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_bidir": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_bidir_save": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_attn_causal": (ctypes.c_int,
-                              [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+                              [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "favor_attn_causal_save": (ctypes.c_int,
+                                   [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_attn_both": (ctypes.c_int,
                             [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "favor_attn_both_noalloc": (ctypes.c_int,
@@ -108,13 +112,15 @@ def last_error():
 
 KERNEL_SOFTMAX = 0
 KERNEL_RELU = 1
-ABI_VERSION = 4   # forward row scales saved for the backward pass
+ABI_VERSION = 5   # the contract's signatures; row scales through the *_save calls; segment
 
 
-def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, chunk=0,
-              kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3):
+def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, segment=0,
+              kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3, chunk=0):
+    """Descriptor; segment = causal rows per segment (0 = library default),
+    chunk = causal chunk length T (0 = library default, 64)."""
     return FavorDesc(B, H, L, d, M, in_dtype, out_dtype, float(input_scale), float(denom_eps),
-                     chunk, int(kernel), 0 if renormalize else 1, float(kernel_eps))
+                     chunk, int(kernel), 0 if renormalize else 1, float(kernel_eps), segment)
 
 
 def validate_desc(g, op):

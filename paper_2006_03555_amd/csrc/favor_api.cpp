@@ -58,6 +58,9 @@ constexpr int kMinRowsPerSplit = 256;
 // Longest sequence per head (and longest causal segment): the kernels index
 // tokens with 32-bit integers and step past the end by up to two tiles.
 constexpr int kMaxL = 1 << 30;
+// Tokens per step of the causal scan (the 64-token matrix-core tile of the
+// intra-chunk product).
+constexpr int kChunk = 64;
 
 enum Op {
   kOpFeatureMap = 0,
@@ -91,11 +94,16 @@ favor_status validate(const favor_desc *g, int op) {
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "no_renormalize must be 0 or 1");
   if (g->kernel == FAVOR_KERNEL_RELU && (!std::isfinite(g->kernel_eps) || g->kernel_eps < 0.f))
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "kernel_eps must be finite and >= 0");
-  if (g->chunk < 0 || g->chunk % 64 != 0)
-    return fail(FAVOR_ERR_INVALID_ARGUMENT, "chunk=%d must be a non-negative multiple of 64",
-                g->chunk);
+  if (g->chunk < 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "chunk=%d is negative", g->chunk);
+  if (g->segment < 0 || g->segment % 64 != 0)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "segment=%d must be a non-negative multiple of 64",
+                g->segment);
   if (g->L > kMaxL) return fail(FAVOR_ERR_UNSUPPORTED, "L=%d exceeds 2^30", g->L);
-  if (g->chunk > kMaxL) return fail(FAVOR_ERR_UNSUPPORTED, "chunk=%d exceeds 2^30", g->chunk);
+  if (g->chunk != 0 && g->chunk != kChunk)
+    return fail(FAVOR_ERR_UNSUPPORTED, "chunk=%d not supported (T = 64, the matrix-core tile)",
+                g->chunk);
+  if (g->segment > kMaxL)
+    return fail(FAVOR_ERR_UNSUPPORTED, "segment=%d exceeds 2^30", g->segment);
   if (g->d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", g->d);
   if (g->M % 16 != 0 || g->M > 256)
     return fail(FAVOR_ERR_UNSUPPORTED, "M=%d not supported (a multiple of 16, at most 256)",
@@ -141,11 +149,11 @@ Plan make_plan(const favor_desc *g, int op) {
   Plan p;
   p.BH = g->B * g->H;
   if (p.BH == 0 || g->L == 0) return p;
-  // L and chunk are at most 2^30 (validated), so these stay within int
+  // L and segment are at most 2^30 (validated), so these stay within int
   const int tiles = (g->L + 63) / 64;
   int rows;
-  if (causal && g->chunk > 0) {
-    rows = g->chunk;
+  if (causal && g->segment > 0) {
+    rows = g->segment;
   } else {
     // a two-group k_kside workgroup fills a CU by itself
     const favor::Dt in = g->in_dtype == FAVOR_BF16 ? favor::Dt::BF16 : favor::Dt::F32;
@@ -289,7 +297,7 @@ size_t favor_workspace_size(const favor_desc *g, int causal) {
 }
 
 favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d,
-                            favor_rf_kind kind, float *W, float *b, void *stream) {
+                            favor_rf_kind kind, float *W, float *b, hipStream_t stream) {
   if (n_heads < 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "n_heads=%d is negative", n_heads);
   if (M <= 0 || d <= 0) return fail(FAVOR_ERR_INVALID_ARGUMENT, "M=%d d=%d must be positive", M, d);
   const int k = raw_enum(&kind);
@@ -305,14 +313,14 @@ favor_status favor_orf_draw(uint64_t seed, int32_t n_heads, int32_t M, int32_t d
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "W must be 16-byte and b 4-byte aligned");
   hipError_t e;
   {
-    favor::LaunchTimer t(favor::kKerOrfDraw, (hipStream_t)stream);
-    e = favor::launch_orf_draw(seed, n_heads, M, k, W, b, (hipStream_t)stream);
+    favor::LaunchTimer t(favor::kKerOrfDraw, stream);
+    e = favor::launch_orf_draw(seed, n_heads, M, k, W, b, stream);
   }
   return device_result(e, "favor_orf_draw launch");
 }
 
 favor_status favor_feature_map(const favor_desc *g, const void *X, const float *W,
-                               const float *b, void *Xprime, void *stream) {
+                               const float *b, void *Xprime, hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpFeatureMap));
   const bool work = (long long)g->B * g->H * g->L > 0;
   FAVOR_TRY(check_ptr(X, "X", work));
@@ -322,16 +330,23 @@ favor_status favor_feature_map(const favor_desc *g, const void *X, const float *
   if (!work) return ok();
   hipError_t e;
   {
-    favor::LaunchTimer t(favor::kKerFeatureMap, (hipStream_t)stream);
+    favor::LaunchTimer t(favor::kKerFeatureMap, stream);
     e = favor::launch_feature_map(shape_of(g), dt_of(g->in_dtype), dt_of(g->out_dtype), X, W, b,
-                                  Xprime, (hipStream_t)stream);
+                                  Xprime, stream);
   }
   return device_result(e, "favor_feature_map launch");
 }
 
 favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
                               const void *V, const float *W, const float *b, void *out,
-                              float *row_scale, void *ws, size_t ws_bytes, void *stream) {
+                              void *ws, size_t ws_bytes, hipStream_t stream) {
+  return favor_attn_bidir_save(g, Q, K, V, W, b, out, nullptr, ws, ws_bytes, stream);
+}
+
+favor_status favor_attn_bidir_save(const favor_desc *g, const void *Q, const void *K,
+                                   const void *V, const float *W, const float *b, void *out,
+                                   float *row_scale, void *ws, size_t ws_bytes,
+                                   hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpBidir));
   FAVOR_TRY(check_row_scale(g, row_scale, "row_scale"));
   const Plan p = make_plan(g, kOpBidir);
@@ -349,7 +364,7 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
     return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, p.total);
   const favor::Shape sh = shape_of(g);
   const favor::Dt in = dt_of(g->in_dtype);
-  hipStream_t st = (hipStream_t)stream;
+  hipStream_t st = stream;
   float *part = static_cast<float *>(ws);
   void *frags = static_cast<char *>(ws) + p.part_bytes;
   void *wfr = static_cast<char *>(frags) + p.frag_bytes;
@@ -377,8 +392,16 @@ favor_status favor_attn_bidir(const favor_desc *g, const void *Q, const void *K,
 
 favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K,
                                const void *V, const float *W, const float *b, void *out,
-                               const float *state_in, float *state_out, float *row_scale,
-                               void *ws, size_t ws_bytes, void *stream) {
+                               const float *state_in, float *state_out, void *ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  return favor_attn_causal_save(g, Q, K, V, W, b, out, state_in, state_out, nullptr, ws,
+                                ws_bytes, stream);
+}
+
+favor_status favor_attn_causal_save(const favor_desc *g, const void *Q, const void *K,
+                                    const void *V, const float *W, const float *b, void *out,
+                                    const float *state_in, float *state_out, float *row_scale,
+                                    void *ws, size_t ws_bytes, hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpCausal));
   FAVOR_TRY(check_row_scale(g, row_scale, "row_scale"));
   const Plan p = make_plan(g, kOpCausal);
@@ -395,7 +418,7 @@ favor_status favor_attn_causal(const favor_desc *g, const void *Q, const void *K
   if (state_out && !aligned(state_out, 16))
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "state_out is not 16-byte aligned");
   const favor::Shape sh = shape_of(g);
-  hipStream_t st = (hipStream_t)stream;
+  hipStream_t st = stream;
   if (!work) {
     // no tokens: the carried state passes through unchanged
     if (heads && state_out) {
@@ -447,7 +470,7 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
                              const float *W, const float *b, void *out_bidir, void *out_causal,
                              const float *state_in, float *state_out, float *row_scale_bidir,
                              float *row_scale_causal, void *ws, size_t ws_bytes,
-                             void *stream) {
+                             hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpBoth));
   FAVOR_TRY(check_row_scale(g, row_scale_bidir, "row_scale_bidir"));
   FAVOR_TRY(check_row_scale(g, row_scale_causal, "row_scale_causal"));
@@ -466,7 +489,7 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
   if (state_out && !aligned(state_out, 16))
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "state_out is not 16-byte aligned");
   const favor::Shape sh = shape_of(g);
-  hipStream_t st = (hipStream_t)stream;
+  hipStream_t st = stream;
   if (!work) {
     if (heads && state_out) {
       hipError_t e;
@@ -588,7 +611,7 @@ favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const
                                        const void *V, const float *W, const float *b,
                                        const void *dout, const void *out_fwd,
                                        const float *row_scale, void *dQ, void *dK, void *dV,
-                                       void *ws, size_t ws_bytes, void *stream) {
+                                       void *ws, size_t ws_bytes, hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpBidirBackward));
   bool saved = false;
   FAVOR_TRY(check_saved(g, out_fwd, row_scale, saved));
@@ -601,7 +624,7 @@ favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const
   FAVOR_TRY(check_workspace(ws, ws_bytes, p.total));
   const favor::Shape sh = shape_of(g);
   const favor::Dt in = dt_of(g->in_dtype);
-  hipStream_t st = (hipStream_t)stream;
+  hipStream_t st = stream;
   const BwdBufs w = carve(p, ws);
   hipError_t e;
   // forward recomputation: Buf1 (and W'' fragments), and the normalised output
@@ -661,7 +684,7 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
                                         const void *out_fwd, const float *row_scale,
                                         const float *dstate_out, void *dQ, void *dK, void *dV,
                                         float *dstate_in, void *ws, size_t ws_bytes,
-                                        void *stream) {
+                                        hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpCausalBackward));
   bool saved = false;
   FAVOR_TRY(check_saved(g, out_fwd, row_scale, saved));
@@ -677,7 +700,7 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
     if (st_ptrs[i] && !aligned(st_ptrs[i], 16))
       return fail(FAVOR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", st_names[i]);
   const favor::Shape sh = shape_of(g);
-  hipStream_t st = (hipStream_t)stream;
+  hipStream_t st = stream;
   hipError_t e;
   if (!work) {
     // no tokens: the state gradient passes through unchanged

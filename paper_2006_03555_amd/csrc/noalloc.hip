@@ -60,7 +60,7 @@ FAVOR_API favor_status favor_attn_both_noalloc(const favor_desc *g, const void *
                                                const float *b, void *out_bidir,
                                                void *out_causal, const float *state_in,
                                                float *state_out, float *row_scale_bidir,
-                                               float *row_scale_causal, void *stream) {
+                                               float *row_scale_causal, hipStream_t stream) {
   // the descriptor is validated and the size checked before any device call
   favor_status st = favor_validate_desc(g, 3);
   if (st != FAVOR_OK) return st;

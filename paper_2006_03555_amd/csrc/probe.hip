@@ -68,16 +68,17 @@ FAVOR_API double favor_probe_work(int32_t kind, int32_t iters) {
   return 0.0;
 }
 
-FAVOR_API favor_status favor_probe(int32_t kind, int32_t iters, float *sink, void *stream) {
+FAVOR_API favor_status favor_probe(int32_t kind, int32_t iters, float *sink,
+                                   hipStream_t stream) {
   using namespace favor;
   if ((kind != 0 && kind != 1) || iters <= 0 || !sink)
     return report(FAVOR_ERR_INVALID_ARGUMENT, "favor_probe: kind 0 or 1, iters > 0, sink");
   const dim3 grid(kProbeCus * kProbeBlocksPerCu);
   if (kind == 0)
-    hipLaunchKernelGGL(k_probe_mfma, grid, dim3(kProbeThreads), 0, (hipStream_t)stream, iters,
+    hipLaunchKernelGGL(k_probe_mfma, grid, dim3(kProbeThreads), 0, stream, iters,
                        sink);
   else
-    hipLaunchKernelGGL(k_probe_cos, grid, dim3(kProbeThreads), 0, (hipStream_t)stream, iters,
+    hipLaunchKernelGGL(k_probe_cos, grid, dim3(kProbeThreads), 0, stream, iters,
                        sink);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? FAVOR_OK : report(FAVOR_ERR_DEVICE, hipGetErrorString(e));

@@ -61,6 +61,7 @@ favor_desc random_desc() {
   const float eps[] = {0.f, 0.f, 1e-6f, 0.5f, -1e-3f, std::numeric_limits<float>::quiet_NaN(),
                        std::numeric_limits<float>::infinity()};
   const int32_t chunks[] = {0, 0, 64, 128, 192, 1024, 100, -64, INT_MAX, INT_MAX - 63, 1 << 30};
+  const int32_t vT[] = {0, 64, 0, 64, 32, 128, -1};
   const int32_t kernels[] = {0, 1, 0, 2, -1};
   const int32_t rn[] = {0, 0, 1, 2, -1};
   if (coin(60)) {   // a valid descriptor, then at most one field mutated below
@@ -77,12 +78,13 @@ favor_desc random_desc() {
     g.out_dtype = coin(70) ? g.in_dtype : (favor_dtype)(next() % 2);
     g.input_scale = coin(80) ? 0.35355339f : 1.f;
     g.denom_eps = coin(70) ? 0.f : 0.25f;
-    g.chunk = pick(vc);
+    g.segment = pick(vc);
+    g.chunk = coin(80) ? 0 : 64;
     g.kernel = (int)(next() % 2);
     g.no_renormalize = coin(80) ? 0 : 1;
     g.kernel_eps = 1e-3f;
     if (coin(50)) return g;
-    switch (next() % 12) {
+    switch (next() % 14) {
       case 0: g.B = pick(Bs); break;
       case 1: g.H = pick(Bs); break;
       case 2: g.L = pick(Ls); break;
@@ -92,7 +94,8 @@ favor_desc random_desc() {
       case 6: g.out_dtype = (favor_dtype)pick(dts); break;
       case 7: g.input_scale = pick(fs); break;
       case 8: g.denom_eps = pick(eps); break;
-      case 9: g.chunk = pick(chunks); break;
+      case 9: g.segment = pick(chunks); break;
+      case 13: g.chunk = pick(vT); break;
       case 10: g.kernel = pick(kernels); break;
       default: g.no_renormalize = pick(rn); break;
     }
@@ -108,7 +111,8 @@ favor_desc random_desc() {
   g.out_dtype = (favor_dtype)pick(dts);
   g.input_scale = pick(fs);
   g.denom_eps = pick(eps);
-  g.chunk = pick(chunks);
+  g.segment = pick(chunks);
+  g.chunk = pick(vT);
   g.kernel = pick(kernels);
   g.no_renormalize = pick(rn);
   g.kernel_eps = pick(eps);
@@ -201,14 +205,28 @@ int main(int argc, char **argv) {
     call(it, "feature_map", b0, favor_feature_map(gp, ptr(), (float *)ptr(), (float *)ptr(),
                                                   ptr(), nullptr));
     b0 = g_launches;
-    call(it, "attn_bidir", b0,
-         favor_attn_bidir(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(), ptr(),
-                          coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nb), nullptr));
+    if (coin(50))
+      call(it, "attn_bidir", b0,
+           favor_attn_bidir(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(), ptr(),
+                            ws_ptr(), ws_for(nb), nullptr));
+    else
+      call(it, "attn_bidir_save", b0,
+           favor_attn_bidir_save(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(), ptr(),
+                                 coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nb),
+                                 nullptr));
     b0 = g_launches;
-    call(it, "attn_causal", b0,
-         favor_attn_causal(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(), ptr(),
-                           coin(30) ? (float *)ptr() : nullptr, coin(30) ? (float *)ptr() : nullptr,
-                           coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nc), nullptr));
+    if (coin(50))
+      call(it, "attn_causal", b0,
+           favor_attn_causal(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(), ptr(),
+                             coin(30) ? (float *)ptr() : nullptr,
+                             coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nc), nullptr));
+    else
+      call(it, "attn_causal_save", b0,
+           favor_attn_causal_save(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(), ptr(),
+                                  coin(30) ? (float *)ptr() : nullptr,
+                                  coin(30) ? (float *)ptr() : nullptr,
+                                  coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nc),
+                                  nullptr));
     b0 = g_launches;
     call(it, "attn_both", b0,
          favor_attn_both(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(), ptr(), ptr(),

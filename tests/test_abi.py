@@ -40,14 +40,14 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_strings(L):
-    assert L.favor_abi_version() == 4
+    assert L.favor_abi_version() == 5
     assert fv.status_string(0) == "FAVOR_OK"
     assert fv.status_string(3) == "FAVOR_ERR_WORKSPACE_TOO_SMALL"
 
 
 def _desc(**kw):
     base = dict(B=2, H=4, L=1000, d=64, M=256, in_dtype=fv.BF16, out_dtype=fv.BF16,
-                input_scale=64 ** -0.25, denom_eps=0.0, chunk=0)
+                input_scale=64 ** -0.25, denom_eps=0.0, segment=0)
     base.update(kw)
     return fv.make_desc(**base)
 
@@ -69,7 +69,12 @@ def _desc(**kw):
     (dict(out_dtype=-1), 1),
     (dict(input_scale=float("nan")), 1),
     (dict(denom_eps=-1.0), 1),
-    (dict(chunk=100), 1),
+    (dict(segment=100), 1),
+    (dict(segment=-64), 1),
+    (dict(chunk=-1), 1),
+    (dict(chunk=64), 0),         # the chunk length T of the scan: 64, the matrix-core tile
+    (dict(chunk=32), 2),
+    (dict(chunk=128), 2),
     (dict(B=300, H=300), 2),
     (dict(kernel=fv.KERNEL_RELU), 0),
     (dict(kernel=fv.KERNEL_RELU, kernel_eps=0.0), 0),
@@ -81,8 +86,8 @@ def _desc(**kw):
     (dict(kernel_eps=-1.0), 0),   # kernel_eps is not read for softmax features
     (dict(L=1 << 30), 0),         # the longest sequence per head
     (dict(L=(1 << 30) + 1), 2),
-    (dict(chunk=1 << 30), 0),
-    (dict(chunk=(1 << 30) + 64), 2),
+    (dict(segment=1 << 30), 0),
+    (dict(segment=(1 << 30) + 64), 2),
 ])
 def test_validate_desc(kw, status):
     for op in (fv.OP_FEATURE_MAP, fv.OP_BIDIR, fv.OP_CAUSAL, fv.OP_BOTH):
@@ -155,8 +160,11 @@ def test_backward_calls_fail_before_launch(L):
                                      1 << 40, null)
     assert st == 2
     # a forward row_scale needs out dtype = in dtype
-    st = L.favor_attn_bidir(ctypes.byref(bad), fake, fake, fake, fake, fake, fake, fake, fake,
-                            1 << 40, null)
+    st = L.favor_attn_bidir_save(ctypes.byref(bad), fake, fake, fake, fake, fake, fake, fake,
+                                 fake, 1 << 40, null)
+    assert st == 2 and "row_scale" in fv.last_error()
+    st = L.favor_attn_causal_save(ctypes.byref(bad), fake, fake, fake, fake, fake, fake, null,
+                                  null, fake, fake, 1 << 40, null)
     assert st == 2 and "row_scale" in fv.last_error()
 
 
@@ -174,7 +182,7 @@ def test_workspace_size():
         assert fv.workspace_size(_desc(M=48), op) == fv.workspace_size(_desc(M=64), op)
         assert fv.workspace_size(_desc(M=144), op) == fv.workspace_size(_desc(M=256), op)
     # causal segment length is honoured: more segments need more workspace
-    assert fv.workspace_size(_desc(chunk=128), 1) > fv.workspace_size(_desc(chunk=512), 1)
+    assert fv.workspace_size(_desc(segment=128), 1) > fv.workspace_size(_desc(segment=512), 1)
 
 
 def test_calls_fail_before_launch(L):
@@ -182,20 +190,18 @@ def test_calls_fail_before_launch(L):
     null = ctypes.c_void_p(0)
     fake = ctypes.c_void_p(1 << 20)
     # NULL tensors
-    st = L.favor_attn_bidir(ctypes.byref(g), null, null, null, null, null, null, null, null, 0,
-                            null)
+    st = L.favor_attn_bidir(ctypes.byref(g), null, null, null, null, null, null, null, 0, null)
     assert st == 1 and "NULL" in fv.last_error()
     # misaligned tensor
     odd = ctypes.c_void_p((1 << 20) + 2)
-    st = L.favor_attn_bidir(ctypes.byref(g), odd, fake, fake, fake, fake, fake, null, fake,
-                            1 << 30, null)
+    st = L.favor_attn_bidir(ctypes.byref(g), odd, fake, fake, fake, fake, fake, fake, 1 << 30,
+                            null)
     assert st == 1 and "aligned" in fv.last_error()
     # workspace too small
-    st = L.favor_attn_bidir(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, fake, 16,
-                            null)
+    st = L.favor_attn_bidir(ctypes.byref(g), fake, fake, fake, fake, fake, fake, fake, 16, null)
     assert st == 3
     st = L.favor_attn_causal(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, null,
-                             null, fake, 16, null)
+                             fake, 16, null)
     assert st == 3
     st = L.favor_attn_both(ctypes.byref(g), fake, fake, fake, fake, fake, fake, null, null, null,
                            null, null, fake, 1 << 30, null)
@@ -271,3 +277,28 @@ def test_noalloc_rejects_a_workspace_beyond_its_scratch(L):
     bad = _desc(d=32)
     assert L.favor_attn_both_noalloc(ctypes.byref(bad), p, p, p, p, p, p, p, None, None, None,
                                      None, None) == 2
+
+
+def test_header_compiles_as_c_and_after_the_hip_runtime(tmp_path):
+    """include/favor.h is a C header: it compiles as C11 on its own and as C++
+    after hip/hip_runtime_api.h (whose hipStream_t it declares identically)."""
+    import shutil
+    import subprocess
+    inc = os.path.join(ROOT, "include")
+    rocm = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
+    c = tmp_path / "a.c"
+    c.write_text('#include "favor.h"\nint main(void) { favor_desc g = {0}; hipStream_t s = 0;\n'
+                 '  (void)s; return (int)favor_workspace_size(&g, 0); }\n')
+    cxx = tmp_path / "b.cpp"
+    cxx.write_text('#include <hip/hip_runtime_api.h>\n#include "favor.h"\n'
+                   'int f(hipStream_t s) { return s == nullptr; }\n')
+    if shutil.which("gcc") is None:
+        pytest.skip("needs gcc")
+    r = subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-fsyntax-only", "-I", inc, str(c)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    if os.path.isdir(os.path.join(rocm, "hip")):
+        r = subprocess.run(["g++", "-std=c++17", "-Wall", "-Werror", "-fsyntax-only",
+                            "-D__HIP_PLATFORM_AMD__", "-I", rocm, "-I", inc, str(cxx)],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr

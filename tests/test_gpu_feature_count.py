@@ -204,7 +204,7 @@ def test_backward_any_m(B, H, L, M, dtype, kernel, causal, seed):
 # fp32 inputs at M > 128: the causal scan runs as two passes over the feature
 # halves (the first stores each row's raw numerators and denominator)
 FP32_CAUSAL_CASES = [
-    # B, H, L, M, kernel, renormalize, denom_eps, chunk
+    # B, H, L, M, kernel, renormalize, denom_eps, causal segment rows
     (1, 2, 700, 256, SOFTMAX, True, 0.0, 0),
     (2, 1, 1100, 208, RELU, True, 0.0, 256),
     (1, 2, 333, 256, SOFTMAX, False, 0.0, 0),
@@ -212,8 +212,8 @@ FP32_CAUSAL_CASES = [
 ]
 
 
-@pytest.mark.parametrize("B,H,L,M,kernel,renorm,eps,chunk", FP32_CAUSAL_CASES)
-def test_fp32_causal_feature_halves(B, H, L, M, kernel, renorm, eps, chunk):
+@pytest.mark.parametrize("B,H,L,M,kernel,renorm,eps,segment", FP32_CAUSAL_CASES)
+def test_fp32_causal_feature_halves(B, H, L, M, kernel, renorm, eps, segment):
     import torch
     fv = _fv()
     Q, K, V = _qkv(B, H, L, "f32", seed=L + M)
@@ -221,7 +221,7 @@ def test_fp32_causal_feature_halves(B, H, L, M, kernel, renorm, eps, chunk):
     Qe, Ke, Ve = _qkv(B, H, 90, "f32", seed=M + 3)
     _, S0 = favor.attn_causal(Qe, Ke, Ve, W, b, S64, kernel=kernel)
     S0 = S0.astype(np.float32)
-    kw = dict(denom_eps=eps, kernel=kernel, renormalize=renorm, chunk=chunk)
+    kw = dict(denom_eps=eps, kernel=kernel, renormalize=renorm, segment=segment)
     out, st = fv.attn_causal(to_dev(Q), to_dev(K), to_dev(V), to_dev(W), to_dev(b), S64,
                              state_in=to_dev(S0), return_state=True, **kw)
     torch.cuda.synchronize()

@@ -90,7 +90,7 @@ def test_bidir_generalized_parity(B, H, L, M, dtype, kernel, renorm, keps, eps):
 
 # ---------------------------------------------------------------- causal
 CAUSAL_CASES = [
-    # B, H, L, M, dtype, chunk, kernel, renormalize, denom_eps
+    # B, H, L, M, dtype, causal segment rows, kernel, renormalize, denom_eps
     (1, 1, 1024, 128, "f32", 0, RELU, True, 0.0),
     (2, 2, 1000, 256, "bf16", 0, RELU, True, 0.0),
     (1, 2, 1000, 256, "bf16", 64, RELU, True, 0.0),
@@ -105,14 +105,14 @@ CAUSAL_CASES = [
 ]
 
 
-@pytest.mark.parametrize("B,H,L,M,dtype,chunk,kernel,renorm,eps", CAUSAL_CASES)
-def test_causal_generalized_parity(B, H, L, M, dtype, chunk, kernel, renorm, eps):
+@pytest.mark.parametrize("B,H,L,M,dtype,segment,kernel,renorm,eps", CAUSAL_CASES)
+def test_causal_generalized_parity(B, H, L, M, dtype, segment, kernel, renorm, eps):
     import torch
     fv = _fv()
     Q, K, V = _qkv(B, H, L, dtype, seed=41 + L + M)
     W, b = _features(19 + L, H, M)
     out = fv.attn_causal(*_dev(dtype, Q, K, V), to_dev(W), to_dev(b), S64, denom_eps=eps,
-                         chunk=chunk, kernel=kernel, renormalize=renorm)
+                         segment=segment, kernel=kernel, renormalize=renorm)
     torch.cuda.synchronize()
     parity(to_host(out), Q, K, V, W, b, S64, True, dtype, eps=eps, kernel=kernel,
            renormalize=renorm)

@@ -190,13 +190,13 @@ def test_nan_key_reaches_only_its_head_and_later_chunks(dtype):
     Q, K, V = _qkv(B, H, L, dtype, seed=57)
     W, b = _features(58, H, M)
     q, k, v, Wd, bd = tuple(to_dev(x, dtype) for x in (Q, K, V)) + (to_dev(W), to_dev(b))
-    for chunk in (0, 128):
+    for segment in (0, 128):
         kb = k.clone()
         kb[1, 0, j, 5] = float("nan")
         cb = fv.attn_bidir(q, k, v, Wd, bd, S64)
-        cc = fv.attn_causal(q, k, v, Wd, bd, S64, chunk=chunk)
+        cc = fv.attn_causal(q, k, v, Wd, bd, S64, segment=segment)
         ob = fv.attn_bidir(q, kb, v, Wd, bd, S64)
-        oc = fv.attn_causal(q, kb, v, Wd, bd, S64, chunk=chunk)
+        oc = fv.attn_causal(q, kb, v, Wd, bd, S64, segment=segment)
         torch.cuda.synchronize()
         assert torch.isnan(ob[1, 0]).all()
         assert torch.isnan(oc[1, 0, j:]).all()

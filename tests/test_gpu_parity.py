@@ -130,10 +130,10 @@ def test_bidir_denominator_stabiliser():
 
 # ---------------------------------------------------------------- causal
 CAUSAL_CASES = [
-    # B, H, L, M, dtype, chunk
+    # B, H, L, M, dtype, causal segment rows
     (1, 1, 1024, 128, "f32", 0),
     (2, 2, 1000, 256, "bf16", 0),
-    (1, 2, 1000, 256, "bf16", 64),     # one chunk per segment: most hand-offs
+    (1, 2, 1000, 256, "bf16", 64),     # one 64-token chunk per segment: most hand-offs
     (1, 3, 65, 64, "bf16", 0),
     (1, 1, 1, 128, "f32", 0),
     (2, 1, 200, 64, "f32", 128),
@@ -143,14 +143,14 @@ CAUSAL_CASES = [
 ]
 
 
-@pytest.mark.parametrize("B,H,L,M,dtype,chunk", CAUSAL_CASES)
-def test_causal_parity(B, H, L, M, dtype, chunk):
+@pytest.mark.parametrize("B,H,L,M,dtype,segment", CAUSAL_CASES)
+def test_causal_parity(B, H, L, M, dtype, segment):
     import torch
     fv = _fv()
     Q, K, V = _qkv(B, H, L, dtype, seed=21 + L)
     W, b = _features(9 + L, H, M)
     out = fv.attn_causal(to_dev(Q, dtype), to_dev(K, dtype), to_dev(V, dtype), to_dev(W),
-                         to_dev(b), S64, chunk=chunk)
+                         to_dev(b), S64, segment=segment)
     torch.cuda.synchronize()
     parity(to_host(out), Q, K, V, W, b, S64, True, dtype)
 
@@ -287,23 +287,23 @@ def test_end_to_end_gpu_draw():
 
 
 # ---------------------------------------------------------------- both directions
-@pytest.mark.parametrize("B,H,L,M,dtype,chunk", [
+@pytest.mark.parametrize("B,H,L,M,dtype,segment", [
     (2, 2, 1000, 256, "bf16", 0),
     (1, 3, 65, 64, "bf16", 64),
     (1, 2, 300, 128, "f32", 0),
 ])
-def test_both_directions_one_pass(B, H, L, M, dtype, chunk):
+def test_both_directions_one_pass(B, H, L, M, dtype, segment):
     import torch
     fv = _fv()
     Q, K, V = _qkv(B, H, L, dtype, seed=81 + L)
     W, b = _features(81 + L, H, M)
     args = [to_dev(x, dtype) for x in (Q, K, V)] + [to_dev(W), to_dev(b)]
-    ob, oc = fv.attn_both(*args, S64, chunk=chunk)
+    ob, oc = fv.attn_both(*args, S64, segment=segment)
     torch.cuda.synchronize()
     parity(to_host(ob), Q, K, V, W, b, S64, False, dtype)
     parity(to_host(oc), Q, K, V, W, b, S64, True, dtype)
     # the causal output is the one favor_attn_causal gives (same kernels, same order)
-    oc2 = fv.attn_causal(*args, S64, chunk=chunk)
+    oc2 = fv.attn_causal(*args, S64, segment=segment)
     torch.cuda.synchronize()
     assert torch.equal(oc, oc2)
 

@@ -39,7 +39,7 @@ def _configs(n=24, seed=20261202):
             kernel=kernel,
             renorm=bool(rng.random() < 0.8),
             eps=float(rng.choice([0.0, 0.0, 0.25])),
-            chunk=int(rng.choice([0, 0, 64, 192, 512])),
+            segment=int(rng.choice([0, 0, 64, 192, 512])),
             state=bool(rng.random() < 0.5),
             kind=int(rng.choice([favor.RF_ORTHO_CHI, favor.RF_IID, favor.RF_HADAMARD])),
         ))
@@ -64,7 +64,7 @@ def _small_m_configs(n=8, seed=777):
             dtype=dtype, out_dtype=dtype, kernel=favor.KERNEL_SOFTMAX,
             renorm=bool(rng.random() < 0.8),
             eps=0.0,
-            chunk=int(rng.choice([0, 64, 192])),
+            segment=int(rng.choice([0, 64, 192])),
             state=bool(rng.random() < 0.5),
             kind=int(rng.choice([favor.RF_ORTHO_CHI, favor.RF_IID, favor.RF_HADAMARD])),
             gate="cond",
@@ -103,10 +103,10 @@ def test_random_configuration(cfg):
 
     Xp = fv.feature_map(q, Wd, bd, S64, out_dtype=odt, kernel=cfg["kernel"])
     ob = fv.attn_bidir(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], out_dtype=odt, **kw)
-    oc, st = fv.attn_causal(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], chunk=cfg["chunk"],
+    oc, st = fv.attn_causal(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], segment=cfg["segment"],
                             state_in=None if S0 is None else to_dev(S0), return_state=True,
                             out_dtype=odt, **kw)
-    ob2, oc2 = fv.attn_both(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], chunk=cfg["chunk"],
+    ob2, oc2 = fv.attn_both(q, k, v, Wd, bd, S64, denom_eps=cfg["eps"], segment=cfg["segment"],
                             state_in=None if S0 is None else to_dev(S0), out_dtype=odt, **kw)
     torch.cuda.synchronize()
 
