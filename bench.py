@@ -679,18 +679,23 @@ def main():
         rs_b = torch.empty((w.B, H, w.L), dtype=torch.float32, device=dev)
         rs_c = torch.empty_like(rs_b)
 
+        fwd_call = {0: "bidir", 1: "causal", 2: "both"}[op]
+
         def gradients(saved):
+            # saved: the forward call just ran with row scales; its outputs, row
+            # scales and workspace (Buf1, segment prefixes, W'') are read back
             gq, gk, gv = grads
+            fwd = dict(forward_workspace=ws, forward_call=fwd_call) if saved else {}
             if op != 1:
                 fv.attn_bidir_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dQ=gq, dK=gk, dV=gv,
                                        workspace=wsb, stream=s_main,
                                        out=out_b if saved else None,
-                                       row_scale=rs_b if saved else None)
+                                       row_scale=rs_b if saved else None, **fwd)
             if op != 0:
                 fv.attn_causal_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dQ=gq, dK=gk, dV=gv,
                                         workspace=wsb, stream=s_main,
                                         out=out_c if saved else None,
-                                        row_scale=rs_c if saved else None)
+                                        row_scale=rs_c if saved else None, **fwd)
 
         def step_bwd(i):
             fv.orf_draw(1000 + i, H, M, w.d, W=Wd[0], b=bd[0], stream=s_main)
@@ -714,7 +719,8 @@ def main():
                 ("backward", step_bwd, "ORF draw + gradients of " + directions
                  + " attention with respect to Q, K, V (forward recomputed inside)"),
                 ("train_step", step_train, "ORF draw + " + directions + " attention saving "
-                 "the row scales + gradients with respect to Q, K, V from the saved outputs")):
+                 "the row scales + gradients with respect to Q, K, V from the saved outputs, "
+                 "row scales and forward workspace")):
             if name not in chosen:
                 continue
             for i in range(args.warmup):

@@ -268,6 +268,15 @@ FAVOR_API size_t favor_noalloc_scratch_bytes(void);
  * and row_scale for the same inputs, features and descriptor; given, the backward
  * skips recomputing them (their recomputation otherwise runs inside the call).
  * Not read without renormalisation.
+ * fwd_ws, fwd_op: the workspace a forward call left behind and which call that
+ * was (1 favor_attn_bidir or favor_attn_bidir_save, 2 favor_attn_causal or
+ * favor_attn_causal_save, 3 favor_attn_both), or NULL and 0. The forward call must have had the same
+ * descriptor, K, V, W, b (and, causal, the same state_in), completed in stream
+ * order before, and its workspace must be unchanged since. Given, the backward
+ * reads Buf1 (bidirectional: 1 or 3) or the segment prefixes (causal: 2 or 3),
+ * the W'' fragments and b'' from it instead of recomputing them; fwd_ws is only
+ * read. Other fwd_op values, or fwd_ws without fwd_op, are
+ * FAVOR_ERR_INVALID_ARGUMENT.
  */
 FAVOR_API size_t favor_backward_workspace_size(const favor_desc *g, int causal);
 
@@ -276,6 +285,7 @@ FAVOR_API favor_status favor_attn_bidir_backward(const favor_desc *g, const void
                                                  const void *K, const void *V, const float *W,
                                                  const float *b, const void *dout,
                                                  const void *out, const float *row_scale,
+                                                 const void *fwd_ws, int32_t fwd_op,
                                                  void *dQ, void *dK, void *dV, void *ws,
                                                  size_t ws_bytes, hipStream_t stream);
 
@@ -293,8 +303,9 @@ FAVOR_API favor_status favor_attn_causal_backward(const favor_desc *g, const voi
                                                   const void *K, const void *V, const float *W,
                                                   const float *b, const float *state_in,
                                                   const void *dout, const void *out,
-                                                  const float *row_scale,
-                                                  const float *dstate_out, void *dQ, void *dK,
+                                                  const float *row_scale, const void *fwd_ws,
+                                                  int32_t fwd_op, const float *dstate_out,
+                                                  void *dQ, void *dK,
                                                   void *dV, float *dstate_in, void *ws,
                                                   size_t ws_bytes, hipStream_t stream);
 
@@ -338,7 +349,7 @@ FAVOR_API double favor_probe_work(int32_t kind, int32_t iters);
 /* ABI version of this header; bumped on any incompatible change. */
 FAVOR_API int32_t favor_abi_version(void);
 
-#define FAVOR_ABI_VERSION 5
+#define FAVOR_ABI_VERSION 6
 
 #ifdef __cplusplus
 }

@@ -344,6 +344,21 @@ def _bwd_grads(Q, dQ, dK, dV):
     return out
 
 
+_FWD_OPS = {"bidir": OP_BIDIR, "causal": OP_CAUSAL, "both": OP_BOTH}
+
+
+def _forward_ws(forward_workspace, forward_call, allowed):
+    """(pointer, op code) of a forward call's workspace offered to a backward call."""
+    if forward_workspace is None:
+        if forward_call is not None:
+            raise FavorError(1, "forward_call without forward_workspace")
+        return ctypes.c_void_p(0), 0
+    if forward_call not in allowed:
+        raise FavorError(1, f"forward_call must be one of {sorted(allowed)}, got {forward_call!r}")
+    _require_cuda(forward_workspace)
+    return _ptr(forward_workspace), _FWD_OPS[forward_call]
+
+
 def _saved(out, row_scale, g, Q):
     if (out is None) != (row_scale is None):
         raise FavorError(1, "pass the forward call's out and row_scale together")
@@ -355,10 +370,13 @@ def _saved(out, row_scale, g, Q):
 @_on_stream
 def attn_bidir_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, dQ=None, dK=None,
                         dV=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
-                        renormalize=True, kernel_eps=1e-3, out=None, row_scale=None):
+                        renormalize=True, kernel_eps=1e-3, out=None, row_scale=None,
+                        forward_workspace=None, forward_call=None):
     """Gradients (dQ, dK, dV) of attn_bidir for the upstream gradient dout
     (favor_attn_bidir_backward). out and row_scale, from the forward call with
-    row_scale, spare recomputing them."""
+    row_scale, spare recomputing them; forward_workspace, the workspace of the
+    forward call forward_call ("bidir" or "both") with the same descriptor and
+    inputs, spares recomputing Buf1."""
     g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps,
                   others=(("K", K), ("V", V), ("dout", dout)),
                   opts=_opts(kernel, renormalize, kernel_eps))
@@ -366,10 +384,11 @@ def attn_bidir_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, dQ=None
     dQ, dK, dV = _bwd_grads(Q, dQ, dK, dV)
     _saved(out, row_scale, g, Q)
     _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV, out, row_scale)
+    fptr, fop = _forward_ws(forward_workspace, forward_call, ("bidir", "both"))
     ws, nbytes = _bwd_workspace(g, False, workspace)
     _check(lib().favor_attn_bidir_backward(ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W),
                                            _ptr(b), _ptr(dout), _ptr(out), _ptr(row_scale),
-                                           _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws),
+                                           fptr, fop, _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws),
                                            ctypes.c_size_t(nbytes), _stream(stream)))
     return dQ, dK, dV
 
@@ -378,10 +397,13 @@ def attn_bidir_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, dQ=None
 def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_in=None,
                          dstate_out=None, return_state_grad=False, dQ=None, dK=None, dV=None,
                          dstate_in=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
-                         renormalize=True, kernel_eps=1e-3, out=None, row_scale=None):
+                         renormalize=True, kernel_eps=1e-3, out=None, row_scale=None,
+                         forward_workspace=None, forward_call=None):
     """Gradients of attn_causal (favor_attn_causal_backward). Returns (dQ, dK, dV), plus
     dstate_in [B, H, M, d+1] when return_state_grad is true. out and row_scale as for
-    attn_bidir_backward."""
+    attn_bidir_backward; forward_workspace of the forward call forward_call ("causal"
+    or "both", same descriptor, inputs and state_in) spares recomputing the segment
+    prefixes."""
     torch = _torch()
     g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps,
                   others=(("K", K), ("V", V), ("dout", dout)),
@@ -396,10 +418,11 @@ def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_
     _saved(out, row_scale, g, Q)
     _require_cuda(Q, K, V, W, b, dout, dQ, dK, dV, state_in, dstate_out, dstate_in, out,
                   row_scale)
+    fptr, fop = _forward_ws(forward_workspace, forward_call, ("causal", "both"))
     ws, nbytes = _bwd_workspace(g, True, workspace)
     _check(lib().favor_attn_causal_backward(
         ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b), _ptr(state_in), _ptr(dout),
-        _ptr(out), _ptr(row_scale), _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
+        _ptr(out), _ptr(row_scale), fptr, fop, _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
         _ptr(dstate_in), _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
     return (dQ, dK, dV, dstate_in) if return_state_grad else (dQ, dK, dV)
 

@@ -78,9 +78,10 @@ def lib():
         "favor_probe_work": (ctypes.c_double, [i32, i32]),
         "favor_backward_workspace_size": (sz, [dp, ctypes.c_int]),
         "favor_attn_bidir_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                                     vp, vp, vp, vp, sz, vp]),
+                                                     vp, i32, vp, vp, vp, vp, sz, vp]),
         "favor_attn_causal_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                                      vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+                                                      vp, vp, i32, vp, vp, vp, vp, vp, vp, sz,
+                                                      vp]),
         "favor_validate_desc": (ctypes.c_int, [dp, ctypes.c_int]),
         "favor_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "favor_last_error": (ctypes.c_char_p, []),
@@ -112,7 +113,7 @@ def last_error():
 
 KERNEL_SOFTMAX = 0
 KERNEL_RELU = 1
-ABI_VERSION = 5   # the contract's signatures; row scales through the *_save calls; segment
+ABI_VERSION = 6   # backward calls read the forward call's workspace
 
 
 def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, segment=0,

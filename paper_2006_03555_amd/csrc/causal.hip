@@ -43,14 +43,17 @@ namespace favor {
 // through LDS into the Buf1^T fragments when frags is non-null: fragment lane
 // (nb, l) of this k-step holds, in slot i, feature 16 (i / 4) + 4 (l / 16) + i % 4
 // of value column pi(nb, l % 16) (block 4: the denominator column 64 in all
-// 16 lane rows), written as one vector store.
+// 16 lane rows), written as one vector store. total (nullable) receives the
+// same total in the layout of an aggregate ([M][65] fp32 per head), for the
+// backward pass.
 constexpr int kSegScanThreads = 576;   // 520 float4 units of a 32-row block, nine waves
 
 template <typename E>
 __global__ __launch_bounds__(kSegScanThreads) void k_seg_scan(float *__restrict__ part, int nseg, int M,
                                                   int Mr, const float *__restrict__ state_in,
                                                   float *__restrict__ state_out,
-                                                  E *__restrict__ frags) {
+                                                  E *__restrict__ frags,
+                                                  float *__restrict__ total) {
   constexpr int kUnits = 32 * 65 / 4;   // float4 per 32-row block
   __shared__ f32x4 tot[kUnits];
   const int sidx = blockIdx.x;
@@ -86,6 +89,8 @@ __global__ __launch_bounds__(kSegScanThreads) void k_seg_scan(float *__restrict_
       run += v;
     }
     if (state_out && drawn) reinterpret_cast<f32x4 *>(state_out)[head + u] = s0 + run;
+    if (total)
+      reinterpret_cast<f32x4 *>(total)[(size_t)bh * (n65 / 4) + (size_t)sidx * kUnits + u] = run;
     tot[u] = run;
   }
   if (!frags) return;
@@ -823,14 +828,14 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 }
 
 hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const float *state_in,
-                           float *state_out, void *total_frags, hipStream_t st) {
+                           float *state_out, void *total_frags, hipStream_t st, float *total) {
   dim3 grid(sh.M / 32, sh.BH);
   if (in == Dt::BF16)
     hipLaunchKernelGGL(k_seg_scan<bf16>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M,
-                       sh.Mr, state_in, state_out, (bf16 *)total_frags);
+                       sh.Mr, state_in, state_out, (bf16 *)total_frags, total);
   else
     hipLaunchKernelGGL(k_seg_scan<float>, grid, dim3(kSegScanThreads), 0, st, part, nseg, sh.M,
-                       sh.Mr, state_in, state_out, (float *)total_frags);
+                       sh.Mr, state_in, state_out, (float *)total_frags, total);
   return hipGetLastError();
 }
 

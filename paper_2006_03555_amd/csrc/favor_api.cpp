@@ -131,7 +131,11 @@ struct BwdPlan {
 };
 
 // Workspace: [ split partials | Buf1^T fragments (bidir, both) | W'' fragments | b'' |
+//              Buf1 as an fp32 aggregate (both) |
 //              feature-half partials (causal and both, fp32 inputs at M > 128) ]
+// A backward call given the workspace of a forward call reads the partials
+// (split partials, or segment prefixes after the scan), W'', b'' and the
+// both-directions total from these offsets.
 struct Plan {
   int BH = 0;
   int nsplit = 0;         // bidir: K-side splits; causal and both: segments
@@ -140,9 +144,32 @@ struct Plan {
   size_t frag_bytes = 0;  // bidir and both
   size_t wfr_bytes = 0;
   size_t bq_bytes = 0;
+  size_t sum_bytes = 0;   // both: [BH][M][65] fp32, Buf1 = the scan's total
   size_t half_bytes = 0;  // [BH][L][68] fp32: the first feature half's raw row results
   size_t total = 0;
 };
+
+// Pointers into a forward call's workspace (plan p).
+struct FwdBufs {
+  float *part, *bq, *sum, *halves;
+  void *frags, *wfr;
+};
+FwdBufs carve_fwd(const Plan &p, void *ws) {
+  char *c = static_cast<char *>(ws);
+  FwdBufs f;
+  f.part = reinterpret_cast<float *>(c);
+  c += p.part_bytes;
+  f.frags = c;
+  c += p.frag_bytes;
+  f.wfr = c;
+  c += p.wfr_bytes;
+  f.bq = reinterpret_cast<float *>(c);
+  c += p.bq_bytes;
+  f.sum = p.sum_bytes ? reinterpret_cast<float *>(c) : nullptr;
+  c += p.sum_bytes;
+  f.halves = p.half_bytes ? reinterpret_cast<float *>(c) : nullptr;
+  return f;
+}
 
 Plan make_plan(const favor_desc *g, int op) {
   const bool causal = (op != kOpBidir);
@@ -174,9 +201,10 @@ Plan make_plan(const favor_desc *g, int op) {
   if (op != kOpCausal) p.frag_bytes = round_up((size_t)p.BH * 5 * (M / 32) * 64 * fb, 256);
   p.wfr_bytes = round_up((size_t)g->H * (M / 16) * 2 * 64 * fb, 256);
   p.bq_bytes = round_up((size_t)g->H * M * sizeof(float), 256);
+  if (op == kOpBoth) p.sum_bytes = round_up((size_t)p.BH * M * 65 * sizeof(float), 256);
   if (causal && g->in_dtype == FAVOR_F32 && M > 128)
     p.half_bytes = round_up((size_t)p.BH * g->L * 68 * sizeof(float), 256);
-  p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes + p.half_bytes;
+  p.total = p.part_bytes + p.frag_bytes + p.wfr_bytes + p.bq_bytes + p.sum_bytes + p.half_bytes;
   return p;
 }
 
@@ -365,10 +393,11 @@ favor_status favor_attn_bidir_save(const favor_desc *g, const void *Q, const voi
   const favor::Shape sh = shape_of(g);
   const favor::Dt in = dt_of(g->in_dtype);
   hipStream_t st = stream;
-  float *part = static_cast<float *>(ws);
-  void *frags = static_cast<char *>(ws) + p.part_bytes;
-  void *wfr = static_cast<char *>(frags) + p.frag_bytes;
-  float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
+  const FwdBufs f = carve_fwd(p, ws);
+  float *part = f.part;
+  void *frags = f.frags;
+  void *wfr = f.wfr;
+  float *bq = f.bq;
   hipError_t e;
   {
     favor::LaunchTimer t(favor::kKerKside, st);
@@ -437,12 +466,11 @@ favor_status favor_attn_causal_save(const favor_desc *g, const void *Q, const vo
   if (ws_bytes < p.total)
     return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, p.total);
   const favor::Dt in = dt_of(g->in_dtype);
-  float *part = static_cast<float *>(ws);
-  void *wfr = static_cast<char *>(ws) + p.part_bytes;
-  float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
-  float *halves = p.half_bytes ? reinterpret_cast<float *>(reinterpret_cast<char *>(bq) +
-                                                           p.bq_bytes)
-                               : nullptr;
+  const FwdBufs f = carve_fwd(p, ws);
+  float *part = f.part;
+  void *wfr = f.wfr;
+  float *bq = f.bq;
+  float *halves = f.halves;
   hipError_t e;
   {
     favor::LaunchTimer t(favor::kKerKside, st);
@@ -508,13 +536,12 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
     return fail(FAVOR_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", ws_bytes, p.total);
   const favor::Dt in = dt_of(g->in_dtype);
   const favor::Dt out = dt_of(g->out_dtype);
-  float *part = static_cast<float *>(ws);
-  void *frags = static_cast<char *>(ws) + p.part_bytes;
-  void *wfr = static_cast<char *>(frags) + p.frag_bytes;
-  float *bq = reinterpret_cast<float *>(static_cast<char *>(wfr) + p.wfr_bytes);
-  float *halves = p.half_bytes ? reinterpret_cast<float *>(reinterpret_cast<char *>(bq) +
-                                                           p.bq_bytes)
-                               : nullptr;
+  const FwdBufs f = carve_fwd(p, ws);
+  float *part = f.part;
+  void *frags = f.frags;
+  void *wfr = f.wfr;
+  float *bq = f.bq;
+  float *halves = f.halves;
   hipError_t e;
   {
     favor::LaunchTimer t(favor::kKerKside, st);
@@ -524,7 +551,7 @@ favor_status favor_attn_both(const favor_desc *g, const void *Q, const void *K, 
   {
     // the segment scan also writes the total over the sequence (Buf1) as Q-side fragments
     favor::LaunchTimer t(favor::kKerSegScan, st);
-    e = favor::launch_seg_scan(sh, in, part, p.nsplit, state_in, state_out, frags, st);
+    e = favor::launch_seg_scan(sh, in, part, p.nsplit, state_in, state_out, frags, st, f.sum);
   }
   if (e != hipSuccess) return device_result(e, "favor_attn_both segment scan");
   {
@@ -595,6 +622,23 @@ favor_status check_saved(const favor_desc *g, const void *out, const float *rs, 
   return FAVOR_OK;
 }
 
+// A forward call's workspace offered to a backward call: fwd_op names the call
+// that left it (0 none, kOpBidir, kOpCausal, kOpBoth); allowed lists the
+// forward calls whose workspace holds what this backward call reads.
+favor_status check_forward_ws(const void *fwd_ws, int fwd_op, int allowed_a, int allowed_b) {
+  if (fwd_op == 0) {
+    if (fwd_ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "fwd_ws given with fwd_op 0");
+    return FAVOR_OK;
+  }
+  if (fwd_op != allowed_a && fwd_op != allowed_b)
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "fwd_op %d does not name a forward call this "
+                                            "backward call can read", fwd_op);
+  if (!fwd_ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "fwd_op %d without fwd_ws", fwd_op);
+  if (!aligned(fwd_ws, 256))
+    return fail(FAVOR_ERR_INVALID_ARGUMENT, "fwd_ws is not 256-byte aligned");
+  return FAVOR_OK;
+}
+
 favor_status check_workspace(const void *ws, size_t ws_bytes, size_t need) {
   if (!ws) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is NULL");
   if (!aligned(ws, 256)) return fail(FAVOR_ERR_INVALID_ARGUMENT, "workspace is not 256-byte aligned");
@@ -610,11 +654,13 @@ extern "C" {
 favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const void *K,
                                        const void *V, const float *W, const float *b,
                                        const void *dout, const void *out_fwd,
-                                       const float *row_scale, void *dQ, void *dK, void *dV,
-                                       void *ws, size_t ws_bytes, hipStream_t stream) {
+                                       const float *row_scale, const void *fwd_ws, int32_t fwd_op,
+                                       void *dQ, void *dK, void *dV, void *ws, size_t ws_bytes,
+                                       hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpBidirBackward));
   bool saved = false;
   FAVOR_TRY(check_saved(g, out_fwd, row_scale, saved));
+  FAVOR_TRY(check_forward_ws(fwd_ws, fwd_op, kOpBidir, kOpBoth));
   const BwdPlan p = make_bwd_plan(g, false);
   const bool work = p.total > 0;
   const void *in_ptrs[] = {Q, K, V, W, b, dout, dQ, dK, dV};
@@ -627,33 +673,44 @@ favor_status favor_attn_bidir_backward(const favor_desc *g, const void *Q, const
   hipStream_t st = stream;
   const BwdBufs w = carve(p, ws);
   hipError_t e;
-  // forward recomputation: Buf1 (and W'' fragments), and the normalised output
-  // with each row's reciprocal
-  {
+  // the key side of the forward pass: Buf1 with the W'' fragments and b'', read
+  // from the forward call's workspace or recomputed; then the normalised output
+  // with each row's reciprocal unless saved
+  void *wfr = w.wfr, *frags = w.frags;
+  float *bq = w.bq, *part = w.part, *buf1 = w.buf1;
+  bool have_frags = false;
+  if (fwd_op != 0) {
+    const FwdBufs f = carve_fwd(make_plan(g, fwd_op), const_cast<void *>(fwd_ws));
+    wfr = f.wfr;
+    bq = f.bq;
+    frags = f.frags;
+    have_frags = true;
+    if (fwd_op == kOpBoth) buf1 = f.sum;
+    else part = f.part;
+  } else {
     favor::LaunchTimer t(favor::kKerKside, st);
-    e = favor::launch_kside(sh, in, K, V, W, b, w.wfr, w.bq, w.part, p.rows_per_split, p.nsplit,
-                            st);
+    e = favor::launch_kside(sh, in, K, V, W, b, wfr, bq, part, p.rows_per_split, p.nsplit, st);
+    if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward key pass");
   }
-  if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward key pass");
   if (sh.renorm && !saved) {
-    {
+    if (!have_frags) {
       favor::LaunchTimer t(favor::kKerFinalize, st);
-      e = favor::launch_finalize(sh, in, w.part, p.nsplit, w.frags, st);
+      e = favor::launch_finalize(sh, in, part, p.nsplit, frags, st);
+      if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward reduction");
     }
-    if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward reduction");
     {
       favor::LaunchTimer t(favor::kKerQside, st);
-      e = favor::launch_qside_save(sh, in, Q, w.wfr, w.bq, w.frags, w.out, w.rsave, st);
+      e = favor::launch_qside_save(sh, in, Q, wfr, bq, frags, w.out, w.rsave, st);
     }
     if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward query pass");
   }
-  {
+  if (buf1 == w.buf1) {
     favor::LaunchTimer t(favor::kKerSumSplits, st);
-    e = favor::launch_sum_splits(sh, w.part, p.nsplit, w.buf1, st);
+    e = favor::launch_sum_splits(sh, part, p.nsplit, w.buf1, st);
+    if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward Buf1");
   }
-  if (e != hipSuccess) return device_result(e, "favor_attn_bidir_backward Buf1");
   favor::BwdArgs a{Q,  K,  V,  dout, saved ? out_fwd : w.out, saved ? row_scale : w.rsave,
-                   w.wfr, w.bq, W, w.buf1, dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
+                   wfr, bq, W, buf1, dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
   {
     favor::LaunchTimer t(favor::kKerBwdDq, st);
     e = favor::launch_bwd_dq(sh, in, false, a, st);
@@ -682,12 +739,14 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
                                         const void *V, const float *W, const float *b,
                                         const float *state_in, const void *dout,
                                         const void *out_fwd, const float *row_scale,
+                                        const void *fwd_ws, int32_t fwd_op,
                                         const float *dstate_out, void *dQ, void *dK, void *dV,
                                         float *dstate_in, void *ws, size_t ws_bytes,
                                         hipStream_t stream) {
   FAVOR_TRY(validate(g, kOpCausalBackward));
   bool saved = false;
   FAVOR_TRY(check_saved(g, out_fwd, row_scale, saved));
+  FAVOR_TRY(check_forward_ws(fwd_ws, fwd_op, kOpCausal, kOpBoth));
   const BwdPlan p = make_bwd_plan(g, true);
   const bool work = p.total > 0;
   const bool heads = (long long)g->B * g->H > 0;
@@ -716,27 +775,38 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
   FAVOR_TRY(check_workspace(ws, ws_bytes, p.total));
   const favor::Dt in = dt_of(g->in_dtype);
   const BwdBufs w = carve(p, ws);
-  // forward recomputation as favor_attn_causal runs it: the segment prefixes
-  // (plus state_in), and the output with each row's reciprocal
-  {
-    favor::LaunchTimer t(favor::kKerKside, st);
-    e = favor::launch_kside(sh, in, K, V, W, b, w.wfr, w.bq, w.part, p.rows_per_split, p.nsplit,
-                            st);
+  // the forward pass as favor_attn_causal runs it: the segment prefixes (plus
+  // state_in) with the W'' fragments and b'', read from the forward call's
+  // workspace (where its scan left them) or recomputed; then the output with
+  // each row's reciprocal unless saved
+  void *wfr = w.wfr;
+  float *bq = w.bq, *prefix = w.part;
+  if (fwd_op != 0) {
+    const FwdBufs f = carve_fwd(make_plan(g, fwd_op), const_cast<void *>(fwd_ws));
+    wfr = f.wfr;
+    bq = f.bq;
+    prefix = f.part;
+  } else {
+    {
+      favor::LaunchTimer t(favor::kKerKside, st);
+      e = favor::launch_kside(sh, in, K, V, W, b, wfr, bq, prefix, p.rows_per_split, p.nsplit,
+                              st);
+    }
+    if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward segment aggregates");
+    {
+      favor::LaunchTimer t(favor::kKerSegScan, st);
+      e = favor::launch_seg_scan(sh, in, prefix, p.nsplit, state_in, nullptr, nullptr, st);
+    }
+    if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward segment prefixes");
   }
-  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward segment aggregates");
-  {
-    favor::LaunchTimer t(favor::kKerSegScan, st);
-    e = favor::launch_seg_scan(sh, in, w.part, p.nsplit, state_in, nullptr, nullptr, st);
-  }
-  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward segment prefixes");
   if (sh.renorm && !saved) {
     favor::LaunchTimer t(favor::kKerCausal, st);
-    e = favor::launch_causal_save(sh, in, Q, K, V, w.wfr, w.bq, w.part, w.out, w.rsave,
+    e = favor::launch_causal_save(sh, in, Q, K, V, wfr, bq, prefix, w.out, w.rsave,
                                   p.rows_per_split, p.nsplit, w.halves, st);
+    if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward forward pass");
   }
-  if (e != hipSuccess) return device_result(e, "favor_attn_causal_backward forward pass");
   favor::BwdArgs a{Q,  K,  V,  dout, saved ? out_fwd : w.out, saved ? row_scale : w.rsave,
-                   w.wfr, w.bq, W, w.part, dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
+                   wfr, bq, W, prefix, dQ, dK, dV, w.aux, p.rows_per_split, p.nsplit};
   {
     favor::LaunchTimer t(favor::kKerBwdDq, st);
     e = favor::launch_bwd_dq(sh, in, true, a, st);

@@ -76,9 +76,10 @@ hipError_t launch_qside(const Shape &sh, Dt in, Dt out, const void *Q, const voi
 // In-place exclusive scan of segment partials (plus state_in); writes state_out
 // (state_in + total) and, if non-null, the total of this call's tokens as the
 // Q-side Buf1^T fragments (the layout launch_finalize writes; element type of
-// `in`).
+// `in`) and as an aggregate total [BH][M][65] fp32.
 hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const float *state_in,
-                           float *state_out, void *total_frags, hipStream_t st);
+                           float *state_out, void *total_frags, hipStream_t st,
+                           float *total = nullptr);
 
 // Forward passes that also write each row's 1 / (D-hat + eps) in units of the
 // unscaled features (rsave [BH][L]) for the backward pass; renormalised shapes

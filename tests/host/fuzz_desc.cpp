@@ -238,13 +238,15 @@ int main(int argc, char **argv) {
     call(it, "attn_bidir_backward", b0,
          favor_attn_bidir_backward(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(),
                                    ptr(), saved ? ptr() : nullptr,
-                                   saved ? (float *)ptr() : nullptr, ptr(), ptr(), ptr(),
-                                   ws_ptr(), ws_for(nbb), nullptr));
+                                   saved ? (float *)ptr() : nullptr,
+                                   coin(30) ? ws_ptr() : nullptr, (int32_t)(next() % 5) - 1,
+                                   ptr(), ptr(), ptr(), ws_ptr(), ws_for(nbb), nullptr));
     b0 = g_launches;
     call(it, "attn_causal_backward", b0,
          favor_attn_causal_backward(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(),
                                     coin(30) ? (float *)ptr() : nullptr, ptr(),
                                     saved ? ptr() : nullptr, saved ? (float *)ptr() : nullptr,
+                                    coin(30) ? ws_ptr() : nullptr, (int32_t)(next() % 5) - 1,
                                     coin(30) ? (float *)ptr() : nullptr, ptr(), ptr(), ptr(),
                                     coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nbc),
                                     nullptr));

@@ -75,7 +75,7 @@ hipError_t launch_qside(const Shape &sh, Dt, Dt, const void *Q, const void *wfr,
   return ran();
 }
 hipError_t launch_seg_scan(const Shape &sh, Dt, float *part, int nseg, const float *, float *,
-                           void *, hipStream_t) {
+                           void *, hipStream_t, float *) {
   require(sh.BH > 0, "segment scan heads");
   require((part == nullptr) == (nseg == 0), "segment scan partials");
   return ran();

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_strings(L):
-    assert L.favor_abi_version() == 5
+    assert L.favor_abi_version() == 6
     assert fv.status_string(0) == "FAVOR_OK"
     assert fv.status_string(3) == "FAVOR_ERR_WORKSPACE_TOO_SMALL"
 
@@ -138,27 +138,39 @@ def test_backward_calls_fail_before_launch(L):
     null = ctypes.c_void_p(0)
     fake = ctypes.c_void_p(1 << 20)
     f6 = [fake] * 6
-    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, null, null, null, fake, fake, fake,
-                                     1 << 40, null)
+    nf = [null, 0]          # no forward workspace
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, null, null, *nf, null, fake, fake,
+                                     fake, 1 << 40, null)
     assert st == 1 and "dQ" in fv.last_error()
-    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, null, null, fake, fake, fake, fake, 16,
-                                     null)
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, null, null, *nf, fake, fake, fake,
+                                     fake, 16, null)
     assert st == 3
     # out and row_scale come together or not at all
-    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, fake, null, fake, fake, fake, fake,
-                                     1 << 40, null)
+    st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, fake, null, *nf, fake, fake, fake,
+                                     fake, 1 << 40, null)
     assert st == 1 and "together" in fv.last_error()
     st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), null, fake, null, null,
-                                      null, fake, fake, fake, null, fake, 16, null)
+                                      *nf, null, fake, fake, fake, null, fake, 16, null)
     assert st == 3
     odd = ctypes.c_void_p((1 << 20) + 4)
     st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), odd, fake, null, null,
-                                      null, fake, fake, fake, null, fake, 1 << 40, null)
+                                      *nf, null, fake, fake, fake, null, fake, 1 << 40, null)
     assert st == 1 and "state_in" in fv.last_error()
     bad = _desc(out_dtype=fv.F32)
-    st = L.favor_attn_bidir_backward(ctypes.byref(bad), *f6, null, null, fake, fake, fake, fake,
-                                     1 << 40, null)
+    st = L.favor_attn_bidir_backward(ctypes.byref(bad), *f6, null, null, *nf, fake, fake, fake,
+                                     fake, 1 << 40, null)
     assert st == 2
+    # a forward workspace names the forward call that left it, and only calls
+    # whose workspace holds what the backward reads are accepted
+    for fptr, fop, ok in ((fake, 1, True), (fake, 3, True), (fake, 2, False), (fake, 0, False),
+                          (null, 1, False), (odd, 1, False), (fake, 7, False)):
+        st = L.favor_attn_bidir_backward(ctypes.byref(g), *f6, null, null, fptr, fop, fake,
+                                         fake, fake, fake, 16, null)
+        assert st == (3 if ok else 1), (fop, fv.last_error())
+    for fptr, fop, ok in ((fake, 2, True), (fake, 3, True), (fake, 1, False), (null, 3, False)):
+        st = L.favor_attn_causal_backward(ctypes.byref(g), *([fake] * 5), null, fake, null, null,
+                                          fptr, fop, null, fake, fake, fake, null, fake, 16, null)
+        assert st == (3 if ok else 1), (fop, fv.last_error())
     # a forward row_scale needs out dtype = in dtype
     st = L.favor_attn_bidir_save(ctypes.byref(bad), fake, fake, fake, fake, fake, fake, fake,
                                  fake, 1 << 40, null)

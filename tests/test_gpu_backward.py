@@ -253,3 +253,72 @@ def test_saved_row_scales_spare_the_recompute(B, H, L, M, dtype, kernel, eps):
         _, scale, _ = _oracle_grads(Q, K, V, _oracle_w(W, M, dtype, kernel), b, dout, causal,
                                     **kw)
         _check_all(_host_grads(saved), _host_grads(recomputed), dtype, scale)
+
+
+@pytest.mark.parametrize("dtype,M,kernel", [("bf16", 256, SOFTMAX), ("f32", 64, SOFTMAX),
+                                            ("bf16", 128, RELU)])
+def test_backward_reads_the_forward_workspace(dtype, M, kernel):
+    """The backward calls given the workspace of the forward call (bidirectional,
+    causal or both directions) instead of recomputing Buf1 / the segment
+    prefixes: bit for bit the gradients of the recomputing calls where the
+    forward plan is the one the backward would rebuild (bidirectional splits for
+    the bidirectional call, the causal segments for the causal and both calls),
+    and within the gate of the oracle's gradients for the bidirectional gradients
+    from a both-directions workspace (its Buf1 sums segments, not splits); also
+    with the saved outputs and row scales, as a training step runs them."""
+    import torch
+    fv = _fv()
+    B, H, L = 2, 2, 1000
+    Q, K, V, dout, W, b = _inputs(B, H, L, M, dtype, seed=101 + M)
+    q, k, v, do = (to_dev(x, dtype) for x in (Q, K, V, dout))
+    Wd, bd = to_dev(W), to_dev(b)
+    Qe, Ke, Ve, _, _, _ = _inputs(B, H, 150, M, dtype, seed=7)
+    _, S0 = favor.attn_causal(Qe, Ke, Ve, W, b, S64, kernel=kernel)
+    S0 = S0.astype(np.float32)
+    s0 = to_dev(S0)
+    kw = dict(kernel=kernel)
+    g = fv.make_desc(B, H, L, 64, M, fv.BF16 if dtype == "bf16" else fv.F32,
+                     fv.BF16 if dtype == "bf16" else fv.F32, S64, kernel=kernel)
+    wsb = torch.empty(fv.workspace_size(g, 0), dtype=torch.uint8, device="cuda")
+    wsc = torch.empty(fv.workspace_size(g, 1), dtype=torch.uint8, device="cuda")
+    wsx = torch.empty(fv.workspace_size(g, 2), dtype=torch.uint8, device="cuda")
+    rb = torch.empty((B, H, L), device="cuda")
+    rc = torch.empty((B, H, L), device="cuda")
+    ob = fv.attn_bidir(q, k, v, Wd, bd, S64, workspace=wsb, row_scale=rb, **kw)
+    oc = fv.attn_causal(q, k, v, Wd, bd, S64, state_in=s0, workspace=wsc, row_scale=rc, **kw)
+    fv.attn_both(q, k, v, Wd, bd, S64, state_in=s0, workspace=wsx, **kw)
+    plain_b = fv.attn_bidir_backward(q, k, v, Wd, bd, S64, do, **kw)
+    plain_c = fv.attn_causal_backward(q, k, v, Wd, bd, S64, do, state_in=s0,
+                                      return_state_grad=True, **kw)
+    reuse_b = fv.attn_bidir_backward(q, k, v, Wd, bd, S64, do, forward_workspace=wsb,
+                                     forward_call="bidir", **kw)
+    reuse_bs = fv.attn_bidir_backward(q, k, v, Wd, bd, S64, do, forward_workspace=wsb,
+                                      forward_call="bidir", out=ob, row_scale=rb, **kw)
+    reuse_c = fv.attn_causal_backward(q, k, v, Wd, bd, S64, do, state_in=s0,
+                                      return_state_grad=True, forward_workspace=wsc,
+                                      forward_call="causal", **kw)
+    reuse_cs = fv.attn_causal_backward(q, k, v, Wd, bd, S64, do, state_in=s0,
+                                       return_state_grad=True, forward_workspace=wsc,
+                                       forward_call="causal", out=oc, row_scale=rc, **kw)
+    both_c = fv.attn_causal_backward(q, k, v, Wd, bd, S64, do, state_in=s0,
+                                     return_state_grad=True, forward_workspace=wsx,
+                                     forward_call="both", **kw)
+    both_b = fv.attn_bidir_backward(q, k, v, Wd, bd, S64, do, forward_workspace=wsx,
+                                    forward_call="both", **kw)
+    plain_bs = fv.attn_bidir_backward(q, k, v, Wd, bd, S64, do, out=ob, row_scale=rb, **kw)
+    plain_cs = fv.attn_causal_backward(q, k, v, Wd, bd, S64, do, state_in=s0,
+                                       return_state_grad=True, out=oc, row_scale=rc, **kw)
+    torch.cuda.synchronize()
+    for x, y in zip(reuse_b, plain_b):
+        assert torch.equal(x, y)
+    for x, y in zip(reuse_bs, plain_bs):
+        assert torch.equal(x, y)
+    for x, y in zip(reuse_c, plain_c):
+        assert torch.equal(x, y)
+    for x, y in zip(reuse_cs, plain_cs):
+        assert torch.equal(x, y)
+    for x, y in zip(both_c, plain_c):
+        assert torch.equal(x, y)
+    Wo = _oracle_w(W, M, dtype, kernel)
+    ref, scale, _ = _oracle_grads(Q, K, V, Wo, b, dout, False, **kw)
+    _check_all(_host_grads(both_b), ref, dtype, scale)
