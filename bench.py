@@ -368,7 +368,7 @@ def _short_kernel(name):
               "k_feature_map"):
         if k in name:
             return k
-    if "copyBuffer" in name or "rocclr" in name or "elementwise" in name.lower():
+    if "copyBuffer" in name:   # the runtime's device-to-device copy of the calibration run
         return "copy"
     return name[:40]
 
@@ -397,16 +397,18 @@ def summarize_counters(root):
     out = {"source_sha256": kernel_source_hash(),
            "fetch_scale": scale["FETCH_SIZE"], "write_scale": scale["WRITE_SIZE"],
            "commands": {
-               "counter": "rocprofv3 --pmc <COUNTER> --output-format csv -d "
+               "counter": "rocprofv3 --pmc <COUNTER> -f csv -d "
                           "gpurun_out/pmc/pmc_<COUNTER>_<workload> -o run -- python3 bench.py "
                           "--workload <workload> --steps 3 --warmup 1 --min-warmup-seconds 0 "
-                          "--no-cpu-baseline --no-variants --workloads ''",
-               "copy": "rocprofv3 --pmc <COUNTER> --output-format csv -d "
+                          "--no-cpu-baseline --no-variants --no-peaks --workloads ''",
+               "copy": "rocprofv3 --pmc <COUNTER> -f csv -d "
                        "gpurun_out/pmc/pmccopy_<COUNTER> -o run -- python3 bench.py "
                        "--copy-bytes 268435456 --steps 3 --warmup 1",
                "summary": "python3 bench.py --summarize-counters gpurun_out/pmc"},
            "workloads": {}}
     for d in sorted(glob.glob(os.path.join(root, "pmc_FETCH_SIZE_*"))):
+        if not os.path.isdir(d):
+            continue
         name = os.path.basename(d)[len("pmc_FETCH_SIZE_"):]
         fetch = _pmc_means(os.path.join(d, "run_counter_collection.csv"))
         write = _pmc_means(os.path.join(root, f"pmc_WRITE_SIZE_{name}",
