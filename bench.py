@@ -225,12 +225,16 @@ def measured_peaks(torch, fv):
         return min(ts[1:])
 
     for kind, iters, key, scale in ((0, 400, "mfma_bf16_tflops", 1e12),
-                                    (1, 20000, "cos_per_s", 1.0)):
+                                    (1, 20000, "cos_per_s", 1.0),
+                                    (2, 40, "hadamard_apply_tokens_per_s", 1.0)):
         import ctypes
         run = lambda: fv.lib().favor_probe(kind, iters, ctypes.c_void_p(sink.data_ptr()),
                                            ctypes.c_void_p(st.cuda_stream))
         t = best(run)
         out[key] = fv.lib().favor_probe_work(kind, iters) / t / scale
+    # the dense projection of one token onto M = 256 rows is 2 d M = 32768 FLOP on the
+    # matrix cores; the structured H-ORF apply does it in O(M log d) vector additions
+    out["dense_projection_tokens_per_s"] = out["mfma_bf16_tflops"] * 1e12 / (2 * 64 * 256)
     n = (1 << 30) // 4
     src = torch.ones(n, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)

@@ -337,11 +337,15 @@ FAVOR_API favor_status favor_timing_read(int32_t k, double *ms, int64_t *count);
 /*
  * Measurement probes for roofline reports (not part of the method): one launch
  * of 512 workgroups of 256 threads (two per CU) in which every wave issues
- * iters x 8 independent v_mfma_f32_16x16x32_bf16 (kind 0) or every lane
- * evaluates iters x 8 independent hardware cosines (kind 1). Timing a launch
- * and dividing favor_probe_work(kind, iters) (FLOP for kind 0, cosines for kind
- * 1) by its duration gives the rate this GPU reaches. sink: a device buffer of
- * at least 512 floats (never written for the probe's inputs).
+ * iters x 8 independent v_mfma_f32_16x16x32_bf16 (kind 0), every lane
+ * evaluates iters x 8 independent hardware cosines (kind 1), or every lane
+ * projects iters tokens onto M = 256 H-ORF rows the structured way, four blocks
+ * of three 64-point Walsh-Hadamard transforms with sign flips in registers
+ * (kind 2; the O(M log d) apply of Sec. 2.4, against which the dense matrix-core
+ * projection of kind 0 is compared). Timing a launch and dividing
+ * favor_probe_work(kind, iters) (FLOP for kind 0, cosines for kind 1, tokens
+ * for kind 2) by its duration gives the rate this GPU reaches. sink: a device
+ * buffer of at least 512 floats (never written for the probe's inputs).
  */
 FAVOR_API favor_status favor_probe(int32_t kind, int32_t iters, float *sink, hipStream_t stream);
 FAVOR_API double favor_probe_work(int32_t kind, int32_t iters);
