@@ -333,7 +333,12 @@ def bench_feature_map(w, Qd, Wd, bd, args, torch, fv):
     ms_i, kernels = time_steps(torch, fv, st, step, 0, args.steps, instrumented=True)
     th = w.B * w.H * w.L
     elt = Qd.element_size()
-    roof = roofline(kernels, w, th, out_elt=elt)
+    # every launch of the uninstrumented region is k_feature_map, so its time per
+    # call is the kernel's average duration; the events bracketing each launch in
+    # the instrumented region add a few microseconds to a kernel this short
+    kernels_region = {k: dict(v, ms_per_launch=ms / v["launches_per_step"])
+                      for k, v in kernels.items()}
+    roof = roofline(kernels_region, w, th, out_elt=elt)
     del Xp
     return {"what": f"X' = phi(Q) of the {w.name} workload ({w.B}x{w.H} heads x L={w.L}, "
                     f"M={w.M}), {w.dtype} in and out",
@@ -664,8 +669,16 @@ def main():
             for i in range(args.warmup):
                 step_d(first + i)
             first += args.warmup
+            # wall time per call (a short draw is bound by the host's launch rate)
+            # and the draw kernel's own duration from the events around its launch
             draws[name] = {"ms_per_draw": timed_region(step_d, first)}
             first += args.steps
+            timed_region(step_d, first, instrumented=True)
+            kd = fv.timing_read()
+            first += args.steps
+            tot, cnt = (sum(v[0] for v in kd.values()), sum(v[1] for v in kd.values()))
+            draws[name]["ms_per_launch"] = tot / cnt if cnt else None
+            draws[name]["kernel"] = ",".join(sorted(k for k, v in kd.items() if v[1] > 0))
         variants["draws"] = draws
 
     # the backward pass of the step's attention: gradients with respect to Q, K, V of

@@ -16,7 +16,6 @@ division by D-hat) and kernel_eps (added to every ReLU feature). The attention
 calls take row_scale (a [B, H, L] float32 tensor) to save each row's
 1 / (D-hat + eps) for the backward calls, which then skip recomputing it.
 """
-import contextlib
 import ctypes
 import functools
 import os
@@ -69,9 +68,11 @@ def _on_stream(fn):
     stream while the kernels may still use it."""
     @functools.wraps(fn)
     def wrapper(*args, stream=None, **kw):
-        ctx = (contextlib.nullcontext() if stream is None
-               else _torch().cuda.stream(stream))
-        with ctx:
+        # entering a stream context costs microseconds of host time per call:
+        # skip it when the caller's stream already is the current one
+        if stream is None or stream == _torch().cuda.current_stream():
+            return fn(*args, stream=stream, **kw)
+        with _torch().cuda.stream(stream):
             return fn(*args, stream=stream, **kw)
     return wrapper
 
