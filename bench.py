@@ -34,7 +34,8 @@ other workload of the configuration list at its full size, each with its step
 time, per-kernel durations and the roofline of its dominant kernel
 (bidir_b8h8 and causal_b8h8 with the draw timed on its own beside the step,
 causal_b8h8 also over three causal segment lengths; causal_long with the
-redraw inside the timed step).
+redraw inside the timed step); the causal workloads also over both chunk
+lengths of the scan (64 and 32 tokens).
 
 python bench.py --summarize-counters DIR turns rocprofv3 FETCH_SIZE /
 WRITE_SIZE runs (see summarize_counters) into profiles/traffic.json.
@@ -57,8 +58,8 @@ import workloads as wl  # noqa: E402
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 # v_cos_f32 issues at half the fp32 rate on CDNA4: 256 CUs x 4 SIMD x 16 lanes x
-# 2.4 GHz / 2 = 19.66e12 cosines per second (a microbenchmark of independent
-# v_cos_f32 chains reaches 18.1e12/s, 92 %).
+# 2.4 GHz / 2 = 19.66e12 cosines per second (the rate this GPU reaches is in the
+# line's measured_peaks, from the library's cosine probe).
 PEAK_COS_PER_S = 256 * 4 * 16 * 2.4e9 / 2
 # Measured HBM traffic per launch (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by a
 # plain copy of known size), valid only for the kernel sources it was taken on.
@@ -246,7 +247,7 @@ def measured_peaks(torch, fv):
     return out
 
 
-def bench_workload(name, args, torch, fv, segment_rows=(0,)):
+def bench_workload(name, args, torch, fv, segment_rows=(0,), chunks=(0,)):
     """One workload of the configuration list at its full size: the step is its
     attention call(s) over inputs resident in HBM, with the random-feature draw
     inside the step when the workload redraws on every call, else timed on its
@@ -274,8 +275,11 @@ def bench_workload(name, args, torch, fv, segment_rows=(0,)):
                         else "outside the timed step (timed on its own)"}}
     fv.orf_draw(77, H, M, w.d, W=Wd, b=bd, stream=st)
     sweep = {}
-    for rows in segment_rows:
-        g = fv.make_desc(w.B, H, w.L, w.d, M, code, code, s, segment=rows)
+    # (segment rows, chunk tokens): the first is the entry's own figure
+    configs = [(rows, chunks[0]) for rows in segment_rows] + [(segment_rows[0], c)
+                                                              for c in chunks[1:]]
+    for rows, chunk in configs:
+        g = fv.make_desc(w.B, H, w.L, w.d, M, code, code, s, segment=rows, chunk=chunk)
         ws = torch.empty(fv.workspace_size(g, op), dtype=torch.uint8, device=dev)
 
         def step(i):
@@ -285,10 +289,10 @@ def bench_workload(name, args, torch, fv, segment_rows=(0,)):
                 fv.attn_bidir(Qd, Kd, Vd, Wd, bd, s, out=out, workspace=ws, stream=st)
             elif op == 1:
                 fv.attn_causal(Qd, Kd, Vd, Wd, bd, s, out=out, workspace=ws, stream=st,
-                               segment=rows)
+                               segment=rows, chunk=chunk)
             else:
                 fv.attn_both(Qd, Kd, Vd, Wd, bd, s, out_bidir=out, out_causal=out2,
-                             workspace=ws, stream=st, segment=rows)
+                             workspace=ws, stream=st, segment=rows, chunk=chunk)
 
         t0 = time.perf_counter()
         n = 0
@@ -302,16 +306,19 @@ def bench_workload(name, args, torch, fv, segment_rows=(0,)):
         first += args.steps
         ms_i, kernels = time_steps(torch, fv, st, step, first, args.steps, instrumented=True)
         first += args.steps
-        sweep[rows] = {"ms_per_step": ms, "value": th / (ms / 1e3),
-                       "ms_per_step_instrumented": ms_i, "kernels": kernels,
-                       "roofline": roofline(kernels, w, th)}
-    best = sweep[segment_rows[0]]
-    entry.update(best)
+        sweep[(rows, chunk)] = {"ms_per_step": ms, "value": th / (ms / 1e3),
+                                "ms_per_step_instrumented": ms_i, "kernels": kernels,
+                                "roofline": roofline(kernels, w, th)}
+    entry.update(sweep[configs[0]])
+    brief = lambda v: {"ms_per_step": v["ms_per_step"], "value": v["value"],
+                       "kernels": {k: x["ms_per_launch"] for k, x in v["kernels"].items()}}
     if len(segment_rows) > 1:
         entry["causal_segment_rows_sweep"] = {
-            ("library default" if r == 0 else str(r)): {"ms_per_step": v["ms_per_step"],
-                                                         "value": v["value"]}
-            for r, v in sweep.items()}
+            ("library default" if r == 0 else str(r)): brief(sweep[(r, chunks[0])])
+            for r in segment_rows}
+    if len(chunks) > 1:
+        entry["causal_chunk_tokens_sweep"] = {
+            str(c or 64): brief(sweep[(segment_rows[0], c)]) for c in chunks}
     if not w.redraw:
         draw = lambda i: fv.orf_draw(1000 + i, H, M, w.d, W=Wd, b=bd, stream=st)
         for i in range(args.warmup):
@@ -444,6 +451,9 @@ def main():
     ap.add_argument("--segment", type=int, default=0,
                     help="rows per segment of the causal scan (a multiple of 64; 0 = the "
                          "library's choice, one workgroup per CU) for the forward steps")
+    ap.add_argument("--chunk", type=int, default=0, choices=(0, 32, 64),
+                    help="tokens per step of the causal scan for the forward steps (0 = the "
+                         "library's choice, 64); the causal workloads also time the other")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the ReLU, unnormalised and backward variants (profiler runs "
@@ -499,7 +509,8 @@ def main():
     out_b = torch.empty_like(Qd)
     out_c = torch.empty_like(Qd)
     g = fv.make_desc(w.B, H, w.L, w.d, M, fv.BF16 if w.dtype == "bf16" else fv.F32,
-                     fv.BF16 if w.dtype == "bf16" else fv.F32, s, segment=args.segment)
+                     fv.BF16 if w.dtype == "bf16" else fv.F32, s, segment=args.segment,
+                     chunk=args.chunk)
     op = {"bidir": 0, "causal": 1, "both": 2}[w.direction]
     ws = torch.empty(fv.workspace_size(g, op), dtype=torch.uint8, device=dev)
     s_main = torch.cuda.current_stream()
@@ -511,6 +522,7 @@ def main():
         opts = dict(opts or {})
         if op != 0:
             opts["segment"] = args.segment
+            opts["chunk"] = args.chunk
         if op == 2:     # one key pass serves both directions
             fv.attn_both(Qd, Kd, Vd, Wd[slot], bd[slot], s, out_bidir=out_b, out_causal=out_c,
                          workspace=ws, stream=s_main, **opts)
@@ -771,8 +783,11 @@ def main():
     if names:
         del Wd, bd, out_b, out_c, ws, Qd, Kd, Vd
         for name in names:
+            causal = wl.WORKLOADS[name].direction != "bidir"
             rows = (0, 1024, 4096) if name == "causal_b8h8" else (0,)
-            others[name] = bench_workload(name, args, torch, fv, segment_rows=rows)
+            chunks = (args.chunk, 32 if args.chunk != 32 else 64) if causal else (0,)
+            others[name] = bench_workload(name, args, torch, fv, segment_rows=rows,
+                                          chunks=chunks)
 
     res = {
         "metric": "FAVOR attention tokens/sec (B*H*L/s) + % of MFMA/HBM peak at L=8192, M=256",
@@ -790,7 +805,7 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": M,
                    "direction": w.direction, "orf_draw_per_step": True,
                    "causal_segment_rows": args.segment or "library default",
-                   "causal_chunk_tokens": 64,
+                   "causal_chunk_tokens": args.chunk or 64,
                    "orf_draw": "drawn in line before the attention pass, same stream",
                    "parallelism": "single GPU"},
         "kernels": kernels,

@@ -87,10 +87,12 @@ typedef struct {
                                exp(Q K^T / sqrt d) (Sec. 2.1) on the given Q, K.  */
   float denom_eps;          /* added to D-hat before dividing; 0 = Algorithm 1      */
   int32_t chunk;            /* causal chunk length T: tokens per step of the
-                               prefix-sum scan (Sec. 2.5.1); 0 = library default.
-                               The kernels take T = 64, the matrix-core tile of
-                               the intra-chunk product; other values return
-                               FAVOR_ERR_UNSUPPORTED                               */
+                               prefix-sum scan (Sec. 2.5.1); 0 = library default,
+                               64 (four 16-token matrix-core blocks in the
+                               intra-chunk product). bf16 inputs also take 32;
+                               other values, and 32 with fp32 inputs in a causal
+                               call, return FAVOR_ERR_UNSUPPORTED. The result is
+                               the same sum in another grouping                    */
   int32_t kernel;           /* favor_kernel; 0 (zero-initialised) = SOFTMAX         */
   int32_t no_renormalize;   /* 0 = out = Buf3 / (buf4 + denom_eps) (Algorithm 1);
                                1 = out = Buf3 = Q' K'^T V ("renormalize_attention"

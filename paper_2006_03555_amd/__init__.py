@@ -214,15 +214,18 @@ def attn_bidir(Q, K, V, W, b, input_scale, denom_eps=0.0, out_dtype=None, out=No
 @_on_stream
 def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
                 segment=0, out_dtype=None, out=None, state_out=None, workspace=None, stream=None,
-                kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3, row_scale=None):
+                kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3, row_scale=None,
+                chunk=0):
     """Unidirectional FAVOR by prefix sums (favor_attn_causal; favor_attn_causal_save
-    when row_scale is given). segment: rows per causal segment (0 = library default).
+    when row_scale is given). segment: rows per causal segment (0 = library default);
+    chunk: tokens per step of the scan (0 = 64; bf16 inputs also take 32).
 
     Returns out, or (out, state_out [B, H, M, d+1]) when return_state is true.
     """
     torch = _torch()
     g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out, Q), denom_eps, segment,
-                  others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
+                  others=(("K", K), ("V", V)),
+                  opts=dict(_opts(kernel, renormalize, kernel_eps), chunk=chunk))
     _require_features(W, b, g.H, g.M, g.d)
     sshape = (g.B, g.H, g.M, g.d + 1)
     if out is None:
@@ -251,14 +254,16 @@ def attn_causal(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return
 def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_state=False,
               segment=0, out_dtype=None, out_bidir=None, out_causal=None, state_out=None,
               workspace=None, stream=None, kernel=KERNEL_SOFTMAX, renormalize=True,
-              kernel_eps=1e-3, row_scale_bidir=None, row_scale_causal=None):
-    """Both directions over the same inputs with one key pass (favor_attn_both).
+              kernel_eps=1e-3, row_scale_bidir=None, row_scale_causal=None, chunk=0):
+    """Both directions over the same inputs with one key pass (favor_attn_both);
+    segment and chunk as for attn_causal.
 
     Returns (out_bidir, out_causal) or (out_bidir, out_causal, state_out).
     """
     torch = _torch()
     g = _desc_for(Q, W, input_scale, _out_dtype(out_dtype, out_bidir, Q), denom_eps, segment,
-                  others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
+                  others=(("K", K), ("V", V)),
+                  opts=dict(_opts(kernel, renormalize, kernel_eps), chunk=chunk))
     _require_features(W, b, g.H, g.M, g.d)
     odt = _torch_dtype(g.out_dtype)
     sshape = (g.B, g.H, g.M, g.d + 1)
@@ -290,14 +295,15 @@ def attn_both(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None, return_s
 def attn_both_noalloc(Q, K, V, W, b, input_scale, denom_eps=0.0, state_in=None,
                       segment=0, out_bidir=None, out_causal=None, state_out=None, stream=None,
                       kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3,
-                      row_scale_bidir=None, row_scale_causal=None):
+                      row_scale_bidir=None, row_scale_causal=None, chunk=0):
     """attn_both with the library's static scratch as workspace
     (favor_attn_both_noalloc): nothing is allocated when the outputs are given.
     Returns (out_bidir, out_causal)."""
     torch = _torch()
     odt = out_bidir.dtype if out_bidir is not None else Q.dtype
     g = _desc_for(Q, W, input_scale, odt, denom_eps, segment,
-                  others=(("K", K), ("V", V)), opts=_opts(kernel, renormalize, kernel_eps))
+                  others=(("K", K), ("V", V)),
+                  opts=dict(_opts(kernel, renormalize, kernel_eps), chunk=chunk))
     _require_features(W, b, g.H, g.M, g.d)
     tdt = _torch_dtype(g.out_dtype)
     sshape = (g.B, g.H, g.M, g.d + 1)

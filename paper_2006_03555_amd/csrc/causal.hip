@@ -378,17 +378,19 @@ __global__ __launch_bounds__(256) void k_causal(const T *__restrict__ Q, const T
 }
 
 // ---------------------------------------------------------------------------
-// Feature-split form for bf16 inputs. Wave w owns features [w MW, (w + 1) MW),
-// MW = M / 4, for the keys and for the queries of every 64-token chunk: its
-// slice of the state S (fp32 accumulators, rows m of its slice, 65 columns
-// padded to 80 with the ones column replicated over the last 16) never leaves
-// its registers, its W'' fragments are loaded once, and its key features are
-// transposed on the matrix cores without LDS. Since
+// Feature-split form for bf16 inputs, chunks of T = 64 or 32 tokens. Wave w
+// owns features [w MW, (w + 1) MW), MW = M / 4, for the keys and for the
+// queries of every chunk: its slice of the state S (fp32 accumulators, rows m
+// of its slice, 65 columns padded to 80 with the ones column replicated over
+// the last 16) never leaves its registers, its W'' fragments are loaded once,
+// and its key features are transposed on the matrix cores without LDS. Since
 //   Buf2 = Q-hat S + tril(Q-hat K-hat^T) C~ = sum over feature slices,
-// each wave forms partial numerators and denominators for all 64 tokens of
-// the chunk; wave w then finalises tokens 16 w .. 16 w + 15 from its own
-// partial and the three others, handed over through LDS. Tiles of K, Q and
-// C~ and the hand-over area are double-buffered, so one barrier per chunk
+// each wave forms partial numerators and denominators for all T tokens of
+// the chunk. The chunk's output is cut into four units, each finalised by one
+// wave from its own partial and the three others, handed over through LDS:
+// T = 64, unit w = tokens 16 w .. 16 w + 15; T = 32, unit w = tokens
+// 16 (w % 2) .. + 15, value columns 32 (w / 2) .. + 31. Tiles of K, Q and C~
+// and the hand-over area are double-buffered, so one barrier per chunk
 // separates producers from consumers.
 //
 // Value columns are held in a permuted order: row r of value block nb (the
@@ -405,16 +407,20 @@ __device__ __forceinline__ void static_for(F &&f) {
   }
 }
 
+template <int T>
 struct CausalFsTile {
-  KVTile<bf16> kv;               // keys row-major, C~ (permuted columns) and D_K fragments
-  bf16 Qs[64][kD + kKsPad];      // queries row-major (B operand of the query projection)
-  float epsq[64];                // per query: eps / (sqrt(2/M) D_Q), or sqrt(2/M) D_Q
+  bf16 Ks[T][kD + kKsPad];       // keys row-major (A operand of the key projection)
+  bf16x8 VtF[4][T / 32][64];     // C~ (permuted columns), chained token order per 32 keys
+  bf16x8 DF[T / 32][4];          // D_K (the ones column of C~), chained order
+  bf16 Qs[T][kD + kKsPad];       // queries row-major (B operand of the query projection)
+  float epsq[T];                 // per query: eps / (sqrt(2/M) D_Q), or sqrt(2/M) D_Q
                                  // when the result is not renormalised
 };
+template <int T>
 struct CausalFsSmem {
-  CausalFsTile tile[2];
-  f32x4 num[2][4][3][4][64];     // [buffer][source wave][slot][value block][lane]
-  float den[2][4][3][16];        // [buffer][source wave][slot][token]
+  CausalFsTile<T> tile[2];
+  f32x4 num[2][4][3][T / 16][64];   // [buffer][source wave][slot][value block of the unit][lane]
+  float den[2][4][3][16];           // [buffer][source wave][slot][token]
 };
 
 // Selection matrix in loaded k order with B[k][c] = (k == 8 (c / 4) + 4 half + c % 4):
@@ -436,12 +442,14 @@ __device__ __forceinline__ float quad_sum_f32(float v) {
   return v;
 }
 
-// Query rows of a 64-token tile, loaded like the keys (row tid / 4, 16 columns).
+// Query rows of a T-token tile, row (tid mod 4T) / 4, 16 columns (T = 32:
+// waves 0 and 1 load them, waves 2 and 3 take zeros).
+template <int T>
 __device__ __forceinline__ void load_q_rows(bf16x8 (&q)[2], const bf16 *__restrict__ Qh, int t0,
                                             int r1) {
   const int tid = threadIdx.x;
-  const int rq = t0 + (tid >> 2);
-  if (rq < r1) {
+  const int rq = t0 + (T == 64 ? tid >> 2 : (tid & 127) >> 2);
+  if (rq < r1 && (T == 64 || tid < 4 * T)) {
     const bf16 *qp = Qh + (size_t)rq * kD + (tid & 3) * 16;
     q[0] = load_frag<bf16>(qp);
     q[1] = load_frag<bf16>(qp + 8);
@@ -451,13 +459,43 @@ __device__ __forceinline__ void load_q_rows(bf16x8 (&q)[2], const bf16 *__restri
   }
 }
 
+// Keys and values of a T-token tile in registers. T = 64: load_tile_regs.
+// T = 32: every wave loads the keys of rows (tid mod 128) / 4 (waves 2 and 3
+// repeat those of waves 0 and 1, for the D_K of the tokens they transpose)
+// and the values of rows 16 (w % 2) + lane % 16, columns 32 (w / 2) + 8 g ..
+// into v[0].
+template <int T>
+__device__ __forceinline__ void load_causal_tile_regs(TileRegs<bf16> &r, const bf16 *__restrict__ Kh,
+                                                      const bf16 *__restrict__ Vh, int t0, int r1,
+                                                      int tid) {
+  if constexpr (T == 64) {
+    load_tile_regs<bf16>(r, Kh, Vh, t0, r1, tid);
+  } else {
+    const int l = tid & 63;
+    const int w = tid >> 6;
+    const int rk = t0 + ((tid & 127) >> 2);
+    const int rv = t0 + 16 * (w & 1) + (l & 15);
+    if (rk < r1) {
+      const bf16 *kp = Kh + (size_t)rk * kD + (tid & 3) * 16;
+      r.k[0] = load_frag<bf16>(kp);
+      r.k[1] = load_frag<bf16>(kp + 8);
+    } else {
+      r.k[0] = Mma<bf16>::splat(0.f);
+      r.k[1] = Mma<bf16>::splat(0.f);
+    }
+    r.v[0] = rv < r1 ? load_frag<bf16>(Vh + (size_t)rv * kD + 32 * (w >> 1) + 8 * (l >> 4))
+                     : Mma<bf16>::splat(0.f);
+  }
+}
+
 // Stage a prefetched tile: keys and queries row-major, D_K(t) = sqrt(2/M)
 // exp(||s k_t||^2 / 2) (1 for ReLU features; 0 past r1), C~ = D_K [V 1] as
-// chained-order B fragments in permuted column order (wave w transposes the
-// values of tokens 16 w ..), and the per-query stabiliser when eps != 0 (the
-// query factor when not renormalising).
-template <int KN, bool RN>
-__device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRegs<bf16> &r,
+// chained-order B fragments in permuted column order (T = 64: wave w
+// transposes the values of tokens 16 w ..; T = 32: of tokens 16 (w % 2) ..,
+// value columns 32 (w / 2) ..), and the per-query stabiliser when eps != 0
+// (the query factor when not renormalising).
+template <int T, int KN, bool RN>
+__device__ __forceinline__ void stage_causal_tile(CausalFsTile<T> &tl, const TileRegs<bf16> &r,
                                                   const bf16x8 (&q)[2], int t0, int r1,
                                                   float s2half, float cM, float eps) {
   using P = Mma<bf16>;
@@ -466,46 +504,56 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile &tl, const TileRe
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
-  const int tr = tid >> 2;
+  const int tr = T == 64 ? tid >> 2 : (tid & 127) >> 2;
   const int cq = (tid & 3) * 16;
-  store_frag<bf16>(&tl.kv.Ks[tr][cq], r.k[0]);
-  store_frag<bf16>(&tl.kv.Ks[tr][cq + 8], r.k[1]);
-  store_frag<bf16>(&tl.Qs[tr][cq], q[0]);
-  store_frag<bf16>(&tl.Qs[tr][cq + 8], q[1]);
+  const bool rows_owner = T == 64 || tid < 4 * T;   // T = 32: waves 0 and 1 store the rows
+  if (rows_owner) {
+    store_frag<bf16>(&tl.Ks[tr][cq], r.k[0]);
+    store_frag<bf16>(&tl.Ks[tr][cq + 8], r.k[1]);
+    store_frag<bf16>(&tl.Qs[tr][cq], q[0]);
+    store_frag<bf16>(&tl.Qs[tr][cq + 8], q[1]);
+  }
   float Dt = (t0 + tr < r1) ? 1.f : 0.f;
   if constexpr (KN == kCos) {
     float nrm = quad_sum_f32(sq_sum16(r.k));
     Dt = (t0 + tr < r1) ? cM * expf(s2half * nrm) : 0.f;
   }
-  float Dj[4];   // D of tokens 16 w + 4 g + j, held by the quad of lanes 16 g + 4 j
+  // D of tokens 16 (w mod T/16) + 4 g + j, held by the quad of lanes 16 g + 4 j
+  float Dj[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Dt, 16 * g + 4 * j);
   const bf16x8 sel[2] = {select_perm_frag(0), select_perm_frag(1)};
-  const int sidx = w >> 1;
+  const int sidx = T == 64 ? w >> 1 : 0;
   const int hw = w & 1;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int kh = 0; kh < 2; ++kh)
+  auto transpose = [&](const bf16x8 &v, int kh) __attribute__((always_inline)) {
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
-      const f32x4 c = P::mma(r.v[kh], sel[half], zero4);
-      bf16 *p = reinterpret_cast<bf16 *>(&tl.kv.VtF[2 * kh + half][sidx][l]) + 4 * hw;
+      const f32x4 c = P::mma(v, sel[half], zero4);
+      bf16 *p = reinterpret_cast<bf16 *>(&tl.VtF[2 * kh + half][sidx][l]) + 4 * hw;
 #pragma unroll
       for (int j = 0; j < 4; ++j) p[j] = (bf16)(c[j] * Dj[j]);
     }
-  if (c16 == 0) {
-    bf16 *p = reinterpret_cast<bf16 *>(&tl.kv.DF[sidx][g]) + 4 * hw;
+  };
+  if constexpr (T == 64) {
+    transpose(r.v[0], 0);
+    transpose(r.v[1], 1);
+  } else {
+    transpose(r.v[0], w >> 1);
+  }
+  if (c16 == 0 && (T == 64 || w < 2)) {
+    bf16 *p = reinterpret_cast<bf16 *>(&tl.DF[sidx][g]) + 4 * hw;
 #pragma unroll
     for (int j = 0; j < 4; ++j) p[j] = (bf16)Dj[j];
   }
   if (KN == kCos && (!RN || eps != 0.f)) {
     const float qn = quad_sum_f32(sq_sum16(q));
     const float dq = cM * expf(s2half * qn);
-    if ((tid & 3) == 0) tl.epsq[tr] = (t0 + tr < r1) ? (RN ? eps / dq : dq) : 0.f;
+    if ((tid & 3) == 0 && rows_owner) tl.epsq[tr] = (t0 + tr < r1) ? (RN ? eps / dq : dq) : 0.f;
   }
 }
 
-template <typename To, int M, int KN, bool RN, bool SAVE>
+template <typename To, int M, int KN, bool RN, bool SAVE, int T = 64>
 __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
                                                    const bf16 *__restrict__ K,
                                                    const bf16 *__restrict__ V,
@@ -518,9 +566,13 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   constexpr int MW = M / 4;          // features per wave
   constexpr int MB = MW / 16;        // 16-feature blocks per wave
   constexpr int KS = (MB + 1) / 2;   // 32-feature k-steps per wave (a lone block is zero-padded)
+  constexpr int NTB = T / 16;        // 16-token blocks of a chunk
+  constexpr int NKH = T / 32;        // 32-token key halves of a chunk
+  constexpr int NVB = NTB;           // 16-column value blocks of an output unit
+  static_assert(T == 32 || T == 64, "chunks of 32 or 64 tokens");
   using P = Mma<bf16>;
   using frag = bf16x8;
-  __shared__ CausalFsSmem sm;
+  __shared__ CausalFsSmem<T> sm;
 
   const int item = xcd_item(blockIdx.x, gridDim.x);
   const int bh = item / nseg;
@@ -531,6 +583,8 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   const int l = tid & 63;
   const int g = l >> 4;
   const int c16 = l & 15;
+  const int utb = T == 64 ? w : (w & 1);   // this wave's output unit: token block,
+  const int uvh = T == 64 ? 0 : (w >> 1);  // and value-column group (T = 32)
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
 
   const bf16 *Qh = Q + (size_t)bh * L * kD;
@@ -544,8 +598,8 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   // the first tile's loads go out first: staging waits for them alone
   TileRegs<bf16> rg;
   frag rq[2];
-  load_tile_regs<bf16>(rg, Kh, Vh, r0, r1, tid);
-  load_q_rows(rq, Qh, r0, r1);
+  load_causal_tile_regs<T>(rg, Kh, Vh, r0, r1, tid);
+  load_q_rows<T>(rq, Qh, r0, r1);
 
   // W'' fragments of this wave's features: A operand of the query projection
   // (lane row m), B operand of the key one (lane col m); b'' per row and column
@@ -580,40 +634,41 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       }
   }
 
-  stage_causal_tile<KN, RN>(sm.tile[0], rg, rq, r0, r1, s2half, cM, eps);
-  if (r0 + 64 < r1) {
-    load_tile_regs<bf16>(rg, Kh, Vh, r0 + 64, r1, tid);
-    load_q_rows(rq, Qh, r0 + 64, r1);
+  stage_causal_tile<T, KN, RN>(sm.tile[0], rg, rq, r0, r1, s2half, cM, eps);
+  if (r0 + T < r1) {
+    load_causal_tile_regs<T>(rg, Kh, Vh, r0 + T, r1, tid);
+    load_q_rows<T>(rq, Qh, r0 + T, r1);
   }
   __syncthreads();
 
-  // tokens 16 w .. 16 w + 15 of the previous chunk: sum the four partials (this
-  // wave's own and three handed over in buffer xb), normalise, store
-  f32x4 own[5];
+  // this wave's output unit of the previous chunk: sum the four partials (its
+  // own and three handed over in buffer xb), normalise, store
+  f32x4 own[5];   // value blocks 0 .. NVB - 1 of the unit; [4]: the denominator
   float own_epsq = 0.f;
   auto finalize = [&](int tp, int xb) __attribute__((always_inline)) {
-    f32x4 part[3][4];   // the other waves' partials, all loads issued together
+    f32x4 part[3][NVB];   // the other waves' partials, all loads issued together
     float pden[3];
 #pragma unroll
     for (int k = 1; k < 4; ++k) {
       const int src = (w + k) & 3;         // source wave
-      const int slot = (w - src - 1) & 3;  // its slot for this wave's tokens
+      const int slot = (w - src - 1) & 3;  // its slot for this wave's unit
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) part[k - 1][nb] = sm.num[xb][src][slot][nb][l];
+      for (int nb = 0; nb < NVB; ++nb) part[k - 1][nb] = sm.num[xb][src][slot][nb][l];
       pden[k - 1] = sm.den[xb][src][slot][c16];
     }
-    f32x4 num[4];
+    f32x4 num[NVB];
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) num[nb] = own[nb] + (part[0][nb] + part[1][nb] + part[2][nb]);
+    for (int nb = 0; nb < NVB; ++nb) num[nb] = own[nb] + (part[0][nb] + part[1][nb] + part[2][nb]);
     const float den = own[4][0] + (pden[0] + pden[1] + pden[2]);
-    const int qt = tp + 16 * w + c16;
+    const int qt = tp + 16 * utb + c16;
     if (qt < r1) {
       const float inv = RN ? 1.0f / (den + own_epsq) : own_epsq;
 #pragma unroll
-      for (int pp = 0; pp < 2; ++pp)
-        store8(Oh + (size_t)qt * kD + 32 * pp + 8 * g, num[2 * pp] * inv, num[2 * pp + 1] * inv);
+      for (int pp = 0; pp < NVB / 2; ++pp)
+        store8(Oh + (size_t)qt * kD + 32 * (uvh * (NVB / 2) + pp) + 8 * g, num[2 * pp] * inv,
+               num[2 * pp + 1] * inv);
       if constexpr (SAVE) {
-        if (g == 0) rsave[(size_t)bh * L + qt] = inv;
+        if (g == 0 && uvh == 0) rsave[(size_t)bh * L + qt] = inv;
       }
     }
   };
@@ -624,18 +679,18 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   // chunk c; hand its partials over; barrier. The vector and LDS work of
   // staging and finalising overlaps the matrix work of the chunk.
   int buf = 0;
-  for (int t0 = r0; t0 < r1; t0 += 64, buf ^= 1) {
-    const CausalFsTile &tl = sm.tile[buf];
+  for (int t0 = r0; t0 < r1; t0 += T, buf ^= 1) {
+    const CausalFsTile<T> &tl = sm.tile[buf];
     float my_epsq;
     if constexpr (KN == kCos)
-      my_epsq = (!RN || eps != 0.f) ? tl.epsq[16 * w + c16] : 0.f;
+      my_epsq = (!RN || eps != 0.f) ? tl.epsq[16 * utb + c16] : 0.f;
     else
       my_epsq = RN ? eps : 1.f;
-    if (t0 + 64 < r1) {
-      stage_causal_tile<KN, RN>(sm.tile[buf ^ 1], rg, rq, t0 + 64, r1, s2half, cM, eps);
-      if (t0 + 128 < r1) {
-        load_tile_regs<bf16>(rg, Kh, Vh, t0 + 128, r1, tid);
-        load_q_rows(rq, Qh, t0 + 128, r1);
+    if (t0 + T < r1) {
+      stage_causal_tile<T, KN, RN>(sm.tile[buf ^ 1], rg, rq, t0 + T, r1, s2half, cM, eps);
+      if (t0 + 2 * T < r1) {
+        load_causal_tile_regs<T>(rg, Kh, Vh, t0 + 2 * T, r1, tid);
+        load_q_rows<T>(rq, Qh, t0 + 2 * T, r1);
       }
     }
 
@@ -645,20 +700,20 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
     // cosines of group i.
     //   qB[tb][ks]  B operand: col = query 16 tb + c16, k = 32 features (chained)
     //   kA[mb][s]   A operand: lane row = feature 16 mb + c16, k = keys 32 s .. (chained)
-    frag qB[4][KS];
-    frag kA[MB][2];
+    frag qB[NTB][KS];
+    frag kA[MB][NKH];
     {
       auto load_rows = [&](auto ic, frag (&r)[2]) __attribute__((always_inline)) {
         constexpr int i = decltype(ic)::value;
-        const auto &src = (i < 4) ? tl.Qs : tl.kv.Ks;
-        r[0] = load_frag<bf16>(&src[16 * (i & 3) + c16][8 * g]);
-        r[1] = load_frag<bf16>(&src[16 * (i & 3) + c16][32 + 8 * g]);
+        const auto &src = (i < NTB) ? tl.Qs : tl.Ks;
+        r[0] = load_frag<bf16>(&src[16 * (i % NTB) + c16][8 * g]);
+        r[1] = load_frag<bf16>(&src[16 * (i % NTB) + c16][32 + 8 * g]);
       };
       auto project = [&](auto ic, const frag (&r)[2], f32x4 (&pr)[MB]) __attribute__((always_inline)) {
         constexpr int i = decltype(ic)::value;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-          if constexpr (i < 4) {   // C[m][t] = W'' q_t + b''
+          if constexpr (i < NTB) {   // C[m][t] = W'' q_t + b''
             pr[mb] = P::mma(wf[mb][0], r[0], bqv[mb]);
             pr[mb] = P::mma(wf[mb][1], r[1], pr[mb]);
           } else {                 // C[t][m] = W'' k_t + b''
@@ -671,13 +726,13 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       f32x4 kfh[MB];   // cosines of the first key block of a pair
       auto finish = [&](auto ic, f32x4 (&pr)[MB]) __attribute__((always_inline)) {
         constexpr int i = decltype(ic)::value;
-        constexpr int tb = i & 3;
+        constexpr int tb = i % NTB;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            pr[mb][j] = feature<KN, P>(pr[mb][j], i < 4 ? bqv[mb][j] : bk[mb]);
-        if constexpr (i < 4) {
+            pr[mb][j] = feature<KN, P>(pr[mb][j], i < NTB ? bqv[mb][j] : bk[mb]);
+        if constexpr (i < NTB) {
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks)
             qB[tb][ks] = P::pack(pr[2 * ks], (2 * ks + 1 < MB) ? pr[2 * ks + 1] : zero4);
@@ -694,44 +749,44 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       load_rows(std::integral_constant<int, 0>{}, rows0);
       load_rows(std::integral_constant<int, 1>{}, rows1);
       project(std::integral_constant<int, 0>{}, rows0, pr0);
-      static_for<1, 8>([&](auto ic) __attribute__((always_inline)) {
+      static_for<1, 2 * NTB>([&](auto ic) __attribute__((always_inline)) {
         constexpr int i = decltype(ic)::value;
         auto &rn = (i & 1) ? rows0 : rows1;   // the buffer of group i + 1
         auto &rc = (i & 1) ? rows1 : rows0;
         auto &pc = (i & 1) ? pr1 : pr0;
         auto &pp = (i & 1) ? pr0 : pr1;
-        if constexpr (i + 1 < 8) load_rows(std::integral_constant<int, i + 1>{}, rn);
+        if constexpr (i + 1 < 2 * NTB) load_rows(std::integral_constant<int, i + 1>{}, rn);
         project(ic, rc, pc);
         finish(std::integral_constant<int, i - 1>{}, pp);
         // the next group's rows first, then each projection MFMA followed by
         // three vector instructions of the previous group's epilogue, so that
         // the cosines issue while the matrix core works
-        if constexpr (i + 1 < 8) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        if constexpr (i + 1 < 2 * NTB) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
         static_for<0, 2 * MB>([&](auto) __attribute__((always_inline)) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
         });
         __builtin_amdgcn_sched_barrier(0);
       });
-      finish(std::integral_constant<int, 7>{}, pr1);
+      finish(std::integral_constant<int, 2 * NTB - 1>{}, pr1);
       // the features are complete here: keeps the compiler from sinking the
       // cosines past the finalisation branch, away from the projection MFMAs
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
+      for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(qB[tb][ks]));
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int sx = 0; sx < 2; ++sx) asm volatile("" : "+v"(kA[mb][sx]));
+        for (int sx = 0; sx < NKH; ++sx) asm volatile("" : "+v"(kA[mb][sx]));
     }
 
-    if (t0 > r0) finalize(t0 - 64, buf ^ 1);
+    if (t0 > r0) finalize(t0 - T, buf ^ 1);
 
     // partial Buf2 (value columns and the denominator) over this slice: o[nb][tb]
     // holds rows pi(nb, 4 g + j), column = token 16 tb + c16; first Q-hat S with
     // the state before the chunk
-    f32x4 o[5][4];
+    f32x4 o[5][NTB];
 #pragma unroll
     for (int nb = 0; nb < 5; ++nb) {
       frag sA[KS];   // lane row = value column, k = m
@@ -739,7 +794,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       for (int ks = 0; ks < KS; ++ks)
         sA[ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
+      for (int tb = 0; tb < NTB; ++tb) {
         o[nb][tb] = P::mma(sA[0], qB[tb][0], zero4);
 #pragma unroll
         for (int ks = 1; ks < KS; ++ks) o[nb][tb] = P::mma(sA[ks], qB[tb][ks], o[nb][tb]);
@@ -752,13 +807,13 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
     // slice for key blocks tb' <= tb (keys after the query zeroed) and C~^T P^T
     // into o
 #pragma unroll
-    for (int sidx = 0; sidx < 2; ++sidx) {
+    for (int sidx = 0; sidx < NKH; ++sidx) {
       // C~ of the half: B operand of the state update and A operand of the
       // intra-chunk product (lane = value column, k = token in chained order)
       frag vt[4];
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) vt[nb] = tl.kv.VtF[nb][sidx][l];
-      const frag df = tl.kv.DF[sidx][g];
+      for (int nb = 0; nb < 4; ++nb) vt[nb] = tl.VtF[nb][sidx][l];
+      const frag df = tl.DF[sidx][g];
       frag kT[2][KS];   // A operand: lane row = token 32 sidx + 16 tbl + c16, k = 32 features
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -783,7 +838,7 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
         for (int tbl = 0; tbl < 2; ++tbl) kT[tbl][ks] = P::pack(ct[tbl][0], ct[tbl][1]);
       }
 #pragma unroll
-      for (int tb = 2 * sidx; tb < 4; ++tb) {
+      for (int tb = 2 * sidx; tb < NTB; ++tb) {
         f32x4 pt[2];
 #pragma unroll
         for (int tbl = 0; tbl < 2; ++tbl) {
@@ -807,24 +862,32 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       }
     }
 
-    // hand the partials of the other waves' tokens over; keep this wave's own
+    // hand the partials of the other waves' units over; keep this wave's own
+    // (unit u: token block u % NTB, value blocks NVB (u / NTB) ..)
+    if constexpr (T == 64) {
 #pragma unroll
-    for (int nb = 0; nb < 5; ++nb)
-      own[nb] = (w == 0) ? o[nb][0] : (w == 1) ? o[nb][1] : (w == 2) ? o[nb][2] : o[nb][3];
+      for (int nb = 0; nb < 5; ++nb)
+        own[nb] = (w == 0) ? o[nb][0] : (w == 1) ? o[nb][1] : (w == 2) ? o[nb][2] : o[nb][3];
+    } else {
+#pragma unroll
+      for (int k = 0; k < NVB; ++k)
+        own[k] = (w == 0) ? o[k][0] : (w == 1) ? o[k][1] : (w == 2) ? o[NVB + k][0] : o[NVB + k][1];
+      own[4] = (w & 1) ? o[4][1] : o[4][0];
+    }
     own_epsq = my_epsq;
 #pragma unroll
-    for (int tb = 0; tb < 4; ++tb) {
-      if (tb != w) {
-        const int slot = (tb - w - 1) & 3;
+    for (int u = 0; u < 4; ++u) {
+      if (u != w) {
+        const int slot = (u - w - 1) & 3;
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) sm.num[buf][w][slot][nb][l] = o[nb][tb];
-        if (g == 0) sm.den[buf][w][slot][c16] = o[4][tb][0];
+        for (int k = 0; k < NVB; ++k) sm.num[buf][w][slot][k][l] = o[NVB * (u / NTB) + k][u % NTB];
+        if (g == 0) sm.den[buf][w][slot][c16] = o[4][u % NTB][0];
       }
     }
     __syncthreads();
   }
   // the last chunk
-  if (r1 > r0) finalize(r0 + 64 * ((r1 - r0 - 1) / 64), buf ^ 1);
+  if (r1 > r0) finalize(r0 + T * ((r1 - r0 - 1) / T), buf ^ 1);
 }
 
 hipError_t launch_seg_scan(const Shape &sh, Dt in, float *part, int nseg, const float *state_in,
@@ -860,17 +923,26 @@ static hipError_t causal_fs_typed(const Shape &sh, const void *Q, const void *K,
     if constexpr (SAVE && !RN) {
       return hipErrorInvalidValue;
     } else {
-#define FAVOR_CAUSAL_FS_LAUNCH(MM)                                                          \
-  hipLaunchKernelGGL((k_causal_fs<To, MM, KN, RN, SAVE>), grid, dim3(256), 0, st,             \
+#define FAVOR_CAUSAL_FS_LAUNCH(MM, TT)                                                      \
+  hipLaunchKernelGGL((k_causal_fs<To, MM, KN, RN, SAVE, TT>), grid, dim3(256), 0, st,         \
                      (const bf16 *)Q, (const bf16 *)K, (const bf16 *)V, (const bf16x8 *)wfr,   \
                      bq, prefix, (To *)o, rsave, sh.H, sh.L, seg_len, nseg, sh.s, sh.eps,      \
                      feature_norm(sh))
-      switch (sh.M) {
-        case 64: FAVOR_CAUSAL_FS_LAUNCH(64); break;
-        case 128: FAVOR_CAUSAL_FS_LAUNCH(128); break;
-        case 256: FAVOR_CAUSAL_FS_LAUNCH(256); break;
-        default: return hipErrorInvalidValue;
+#define FAVOR_CAUSAL_FS_M(TT)                                                                \
+  switch (sh.M) {                                                                           \
+    case 64: FAVOR_CAUSAL_FS_LAUNCH(64, TT); break;                                          \
+    case 128: FAVOR_CAUSAL_FS_LAUNCH(128, TT); break;                                        \
+    case 256: FAVOR_CAUSAL_FS_LAUNCH(256, TT); break;                                        \
+    default: return hipErrorInvalidValue;                                                   \
+  }
+      if (sh.chunk == 32) {
+        FAVOR_CAUSAL_FS_M(32)
+      } else if (sh.chunk == 64) {
+        FAVOR_CAUSAL_FS_M(64)
+      } else {
+        return hipErrorInvalidValue;
       }
+#undef FAVOR_CAUSAL_FS_M
 #undef FAVOR_CAUSAL_FS_LAUNCH
       return hipGetLastError();
     }
@@ -884,6 +956,7 @@ static hipError_t causal_typed(const Shape &sh, const void *Q, const void *K, co
                                const void *wfr, const float *bq, const float *prefix, void *o,
                                int seg_len, int nseg, hipStream_t st, float *halves,
                                float *rsave = nullptr) {
+  if (sh.chunk != 64) return hipErrorInvalidValue;   // 64-token chunks only
   dim3 grid(nseg * sh.BH);
   return with_variant(sh, [&](auto kn, auto rn) -> hipError_t {
     constexpr int KN = decltype(kn)::value;

@@ -58,9 +58,10 @@ constexpr int kMinRowsPerSplit = 256;
 // Longest sequence per head (and longest causal segment): the kernels index
 // tokens with 32-bit integers and step past the end by up to two tiles.
 constexpr int kMaxL = 1 << 30;
-// Tokens per step of the causal scan (the 64-token matrix-core tile of the
-// intra-chunk product).
+// Tokens per step of the causal scan: 64 by default (four 16-token matrix-core
+// blocks in the intra-chunk product); bf16 inputs also take 32.
 constexpr int kChunk = 64;
+constexpr int kChunkSmall = 32;
 
 enum Op {
   kOpFeatureMap = 0,
@@ -99,9 +100,11 @@ favor_status validate(const favor_desc *g, int op) {
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "segment=%d must be a non-negative multiple of 64",
                 g->segment);
   if (g->L > kMaxL) return fail(FAVOR_ERR_UNSUPPORTED, "L=%d exceeds 2^30", g->L);
-  if (g->chunk != 0 && g->chunk != kChunk)
-    return fail(FAVOR_ERR_UNSUPPORTED, "chunk=%d not supported (T = 64, the matrix-core tile)",
-                g->chunk);
+  if (g->chunk != 0 && g->chunk != kChunk && g->chunk != kChunkSmall)
+    return fail(FAVOR_ERR_UNSUPPORTED, "chunk=%d not supported (T = 64 or 32)", g->chunk);
+  if (g->chunk == kChunkSmall && in_dt != FAVOR_BF16 &&
+      (op == kOpCausal || op == kOpBoth || op == kOpCausalBackward))
+    return fail(FAVOR_ERR_UNSUPPORTED, "chunk=32 needs bf16 inputs (the fp32 scan takes T = 64)");
   if (g->segment > kMaxL)
     return fail(FAVOR_ERR_UNSUPPORTED, "segment=%d exceeds 2^30", g->segment);
   if (g->d != 64) return fail(FAVOR_ERR_UNSUPPORTED, "d=%d not supported (d = 64)", g->d);
@@ -248,6 +251,7 @@ favor::Shape shape_of(const favor_desc *g) {
   sh.kernel = g->kernel;
   sh.renorm = g->no_renormalize ? 0 : 1;
   sh.keps = g->kernel == FAVOR_KERNEL_RELU ? g->kernel_eps : 0.f;
+  sh.chunk = g->chunk == 0 ? kChunk : g->chunk;
   return sh;
 }
 

@@ -28,6 +28,7 @@ struct Shape {
   int kernel;    // 0 Gaussian-kernel (cos) features, 1 ReLU features
   int renorm;    // 1 divide by D-hat, 0 return the numerator Q' K'^T V
   float keps;    // ReLU: added to every feature
+  int chunk;     // tokens per step of the causal scan: 64, or 32 (bf16 inputs)
 };
 
 // Scales of the projection W'' = ws W and of its seed b'' = bs b for the

@@ -72,9 +72,10 @@ def _desc(**kw):
     (dict(segment=100), 1),
     (dict(segment=-64), 1),
     (dict(chunk=-1), 1),
-    (dict(chunk=64), 0),         # the chunk length T of the scan: 64, the matrix-core tile
-    (dict(chunk=32), 2),
+    (dict(chunk=64), 0),         # the chunk length T of the scan: 64 or 32 (bf16 inputs)
+    (dict(chunk=32), 0),
     (dict(chunk=128), 2),
+    (dict(chunk=48), 2),
     (dict(B=300, H=300), 2),
     (dict(kernel=fv.KERNEL_RELU), 0),
     (dict(kernel=fv.KERNEL_RELU, kernel_eps=0.0), 0),
@@ -94,6 +95,18 @@ def test_validate_desc(kw, status):
         assert fv.validate_desc(_desc(**kw), op) == status
         if status:
             assert fv.last_error() != ""
+
+
+def test_chunk_32_needs_bf16_inputs_for_the_scan():
+    """T = 32 is a variant of the bf16 chunked scan; fp32 inputs take T = 64, and
+    the calls without a scan ignore the field."""
+    g = _desc(in_dtype=fv.F32, out_dtype=fv.F32, chunk=32)
+    for op in (fv.OP_CAUSAL, fv.OP_BOTH, fv.OP_CAUSAL_BACKWARD):
+        assert fv.validate_desc(g, op) == 2
+        assert "bf16" in fv.last_error()
+    for op in (fv.OP_FEATURE_MAP, fv.OP_BIDIR, fv.OP_BIDIR_BACKWARD):
+        assert fv.validate_desc(g, op) == 0
+    assert fv.validate_desc(_desc(chunk=32), fv.OP_CAUSAL_BACKWARD) == 0
 
 
 def test_fp32_causal_takes_every_m():
