@@ -405,16 +405,17 @@ def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_
                          dstate_out=None, return_state_grad=False, dQ=None, dK=None, dV=None,
                          dstate_in=None, workspace=None, stream=None, kernel=KERNEL_SOFTMAX,
                          renormalize=True, kernel_eps=1e-3, out=None, row_scale=None,
-                         forward_workspace=None, forward_call=None):
+                         forward_workspace=None, forward_call=None, chunk=0):
     """Gradients of attn_causal (favor_attn_causal_backward). Returns (dQ, dK, dV), plus
     dstate_in [B, H, M, d+1] when return_state_grad is true. out and row_scale as for
     attn_bidir_backward; forward_workspace of the forward call forward_call ("causal"
     or "both", same descriptor, inputs and state_in) spares recomputing the segment
-    prefixes."""
+    prefixes. chunk: the scan's chunk length for the forward quantities the call
+    recomputes (as for attn_causal)."""
     torch = _torch()
     g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps,
                   others=(("K", K), ("V", V), ("dout", dout)),
-                  opts=_opts(kernel, renormalize, kernel_eps))
+                  opts=dict(_opts(kernel, renormalize, kernel_eps), chunk=chunk))
     _require_features(W, b, g.H, g.M, g.d)
     dQ, dK, dV = _bwd_grads(Q, dQ, dK, dV)
     sshape = (g.B, g.H, g.M, g.d + 1)

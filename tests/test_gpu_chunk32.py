@@ -145,3 +145,30 @@ def test_chunk32_full_size_causal_b8h8():
     e = parity(to_host(out), Q, K, V, W, b, w.input_scale, True, "bf16", heads=heads)
     print(f"\ncausal_b8h8, chunk 32, heads {heads}: E_row {e[0]:.2e} E_cond {e[1]:.2e}",
           flush=True)
+
+
+def test_chunk32_backward_recomputes_with_its_chunks():
+    """The causal backward call without saved statistics recomputes the forward
+    outputs and row scales with the descriptor's chunks: its gradients are those
+    of the 64-token call within the gradient gate of the backward tests, and,
+    given the outputs and row scales a 32-token forward call saved, the same
+    bits as recomputing them."""
+    import torch
+    fv = _fv()
+    from test_gpu_backward import _check_all, _host_grads, _oracle_grads
+    B, H, L, M = 1, 2, 700, 128
+    Q, K, V = _qkv(B, H, L, seed=441)
+    dout = np.random.default_rng(442).standard_normal(Q.shape).astype(np.float32)
+    W, b = _features(443, H, M)
+    q, k, v, do = (to_dev(x, "bf16") for x in (Q, K, V, dout))
+    Wd, bd = to_dev(W), to_dev(b)
+    g32 = fv.attn_causal_backward(q, k, v, Wd, bd, S64, do, chunk=32)[:3]
+    rs = torch.empty((B, H, L), dtype=torch.float32, device="cuda")
+    o32 = fv.attn_causal(q, k, v, Wd, bd, S64, chunk=32, row_scale=rs)
+    s32 = fv.attn_causal_backward(q, k, v, Wd, bd, S64, do, out=o32, row_scale=rs)[:3]
+    torch.cuda.synchronize()
+    for a, c in zip(g32, s32):
+        assert torch.equal(a, c)
+    Qb, Kb, Vb, dob = (np.asarray(to_host(x), dtype=np.float64) for x in (q, k, v, do))
+    ref, scale, _ = _oracle_grads(Qb, Kb, Vb, W, b, dob, True)
+    _check_all(_host_grads(g32), ref, "bf16", scale)
