@@ -310,16 +310,15 @@ __device__ __forceinline__ void store_qgrad(T *dst, const f32x4 (&dacc)[4],
   }
 }
 
-// alpha and u_d of query row i (lane column) from its dout and output fragments.
+// alpha and u_d of query row i (lane column) from its query, dout and output
+// fragments and its saved row scale rs (renormalised; 0 past the end).
 template <typename T, int KN, bool RN>
-__device__ __forceinline__ void row_weights(const typename Mma<T>::frag (&qf)[2],
-                                            const typename Mma<T>::frag (&df)[2],
-                                            const T *__restrict__ Oh,
-                                            const float *__restrict__ rsave_h, int i, int L,
-                                            float cM, float s2half, float &alpha, float &ud) {
+__device__ __forceinline__ void row_weights_loaded(const typename Mma<T>::frag (&qf)[2],
+                                                   const typename Mma<T>::frag (&df)[2],
+                                                   const typename Mma<T>::frag (&of)[2], float rs,
+                                                   int i, int L, float cM, float s2half,
+                                                   float &alpha, float &ud) {
   if constexpr (RN) {
-    typename Mma<T>::frag of[2];
-    load_rows64<T>(of, Oh, i, L);
     float dot = 0.f;
 #pragma unroll
     for (int k = 0; k < 2; ++k)
@@ -327,7 +326,7 @@ __device__ __forceinline__ void row_weights(const typename Mma<T>::frag (&qf)[2]
       for (int e = 0; e < 8; ++e) dot = fmaf(to_f32(df[k][e]), to_f32(of[k][e]), dot);
     dot += __shfl_xor(dot, 16);
     dot += __shfl_xor(dot, 32);
-    alpha = i < L ? rsave_h[i] : 0.f;
+    alpha = rs;
     ud = -dot;
   } else {
     float a = 1.f;
@@ -335,6 +334,31 @@ __device__ __forceinline__ void row_weights(const typename Mma<T>::frag (&qf)[2]
     alpha = i < L ? a : 0.f;
     ud = 0.f;
   }
+}
+
+// The output row and saved row scale of query row i (renormalised calls).
+template <typename T, bool RN>
+__device__ __forceinline__ void load_row_stats(typename Mma<T>::frag (&of)[2], float &rs,
+                                               const T *__restrict__ Oh,
+                                               const float *__restrict__ rsave_h, int i, int L) {
+  if constexpr (RN) {
+    load_rows64<T>(of, Oh, i, L);
+    rs = i < L ? rsave_h[i] : 0.f;
+  } else {
+    rs = 0.f;
+  }
+}
+
+template <typename T, int KN, bool RN>
+__device__ __forceinline__ void row_weights(const typename Mma<T>::frag (&qf)[2],
+                                            const typename Mma<T>::frag (&df)[2],
+                                            const T *__restrict__ Oh,
+                                            const float *__restrict__ rsave_h, int i, int L,
+                                            float cM, float s2half, float &alpha, float &ud) {
+  typename Mma<T>::frag of[2];
+  float rs;
+  load_row_stats<T, RN>(of, rs, Oh, rsave_h, i, L);
+  row_weights_loaded<T, KN, RN>(qf, df, of, rs, i, L, cM, s2half, alpha, ud);
 }
 
 // ------------------------------------------------------------ bidirectional dQ
@@ -428,7 +452,9 @@ struct DqScanSmem {
   frag KT[M / 16][2][64];    // the chunk's key features (row m, k = keys)
   frag VtF[4][2][64];        // C~ of the chunk: row = value column (permuted), k = keys
   frag DF[2][4];             // its column d (D~ per key), one fragment per lane group
-  float red[4][17][64];      // the second half's partial dQ and g~ . q-hat per row block
+  f32x4 dk[16];              // D~ of the chunk's 64 keys
+  f32x4 red[4][4][64];       // the second half's partial dQ per row block
+  float redd[4][64];         // and its g~ . q-hat
 };
 
 // One workgroup per (head, segment of the forward plan). The state waves keep
@@ -495,30 +521,33 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
   const int s1 = s0 + SP::NS / 2;
   __syncthreads();
 
-  for (int t0 = r0; t0 < r1; t0 += 64) {
-    // every global load of the chunk first: the keys and values (all four blocks
-    // in every wave) and this row block's queries, output gradient and output
-    frag ka[4][2], va[4][2];
+  // the keys and values of a chunk (all four blocks in every wave). bf16: loaded
+  // one chunk ahead, once the previous chunk's are no longer read, and the row
+  // statistics are loaded at the top of the chunk but used after its barrier;
+  // fp32 fragments are twice as wide and take the chunk's loads at its top (the
+  // registers would not hold both)
+  constexpr bool kAhead = sizeof(T) == 2;
+  frag ka[4][2], va[4][2];
+  auto load_kv = [&](int tc) __attribute__((always_inline)) {
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) {
-      const int t = t0 + 16 * tb + c16;
+      const int t = tc + 16 * tb + c16;
       load_rows64<T>(ka[tb], Kh, t, r1);
       load_rows64<T>(va[tb], Vh, t, r1);
     }
+  };
+  if (kAhead && r0 < r1) load_kv(r0);
+  for (int t0 = r0; t0 < r1; t0 += 64) {
+    if constexpr (!kAhead) load_kv(t0);
+    // this row block's queries, output gradient, output and row scale
     const int i = t0 + 16 * qb + c16;
-    frag qf[2], df[2];
+    frag qf[2], df[2], of[2];
+    float rs, alpha, ud;
     load_rows64<T>(qf, Qh, i, r1);
     load_rows64<T>(df, dOh, i, r1);
-    float alpha, ud;
-    row_weights<T, KN, RN>(qf, df, Oh, rsave + (size_t)bh * L, i, r1, cM, s2half, alpha, ud);
-    float Dk[4];   // D~ per key
-#pragma unroll
-    for (int tb = 0; tb < 4; ++tb) {
-      const int t = t0 + 16 * tb + c16;
-      float D = 1.f;
-      if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(ka[tb]));
-      Dk[tb] = t < r1 ? D : 0.f;
-    }
+    load_row_stats<T, RN>(of, rs, Oh, rsave + (size_t)bh * L, i, r1);
+    if constexpr (!kAhead)
+      row_weights_loaded<T, KN, RN>(qf, df, of, rs, i, r1, cM, s2half, alpha, ud);
     if (sw) chunk_features_t<T, FB, KN>(sm.KT, sm.WA, sm.bq, ka, w * FB);
     if (hf == 0) {   // C~ of key block qb (its rows loaded again: no runtime register index)
       const int t = t0 + 16 * qb + c16;
@@ -528,6 +557,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
       float Do = 1.f;
       if constexpr (KN == kCos) Do = cM * expf(s2half * sq_norm16<T>(ko));
       Do = t < r1 ? Do : 0.f;
+      if (g == 0) reinterpret_cast<float *>(sm.dk)[16 * qb + c16] = Do;   // for every wave's P2
       float Dj[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Do, 4 * g + j);
@@ -569,6 +599,8 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
         }
     }
 
+    if constexpr (kAhead)
+      row_weights_loaded<T, KN, RN>(qf, df, of, rs, i, r1, cM, s2half, alpha, ud);
     // queries of row block qb, feature steps [s0, s1)
     // P2[j][i] = D~_j (v_j . dout_i + u_d,i) for keys j <= i (B operand, k = keys)
     frag pb2[2];
@@ -578,33 +610,30 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
       for (int kb = 0; kb < 4; ++kb) {
         f32x4 c = P::mma(va[kb][0], df[0], zero4);
         c = P::mma(va[kb][1], df[1], c);
+        const f32x4 D = sm.dk[4 * kb + g];   // keys 16 kb + 4 g + j
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float D = __shfl(Dk[kb], 4 * g + j);
-          pt[kb][j] = 16 * kb + 4 * g + j <= 16 * qb + c16 ? D * (c[j] + ud) : 0.f;
-        }
+        for (int j = 0; j < 4; ++j)
+          pt[kb][j] = 16 * kb + 4 * g + j <= 16 * qb + c16 ? D[j] * (c[j] + ud) : 0.f;
       }
       pb2[0] = P::pack(pt[0], pt[1]);
       pb2[1] = P::pack(pt[2], pt[3]);
     }
+    // the chunk's keys and values are read for the last time above
+    if (kAhead && t0 + 64 < r1) load_kv(t0 + 64);
     f32x4 dacc[4];
     float dot2;
     query_grad<T, M, KN, true>(sm.WA, sm.bq, sm.WT, sm.SA, sm.sz, sm.KT, pb2, qf, df, alpha, ud,
                                s, dacc, dot2, s0, s1);
     if (hf == 1) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sm.red[qb][4 * k + j][l] = dacc[k][j];
-      sm.red[qb][16][l] = dot2;
+      for (int k = 0; k < 4; ++k) sm.red[qb][k][l] = dacc[k];
+      sm.redd[qb][l] = dot2;
     }
     __syncthreads();
     if (hf == 0) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dacc[k][j] += sm.red[qb][4 * k + j][l];
-      dot2 += sm.red[qb][16][l];
+      for (int k = 0; k < 4; ++k) dacc[k] += sm.red[qb][k][l];
+      dot2 += sm.redd[qb][l];
       if (i < r1) {
         store_qgrad<T, KN, ACC>(dQ + ((size_t)bh * L + i) * kD, dacc, qf, alpha, dot2, s);
         if (g == 0) aux[(size_t)bh * L + i] = make_float2(alpha, alpha * ud);
@@ -811,7 +840,8 @@ struct DkvScanSmem {
   // dV: R value columns over features, query features with lane row = query
   frag RB[KPART ? 1 : 4][KPART ? 1 : M / 32][64];
   frag QA[KPART ? 1 : 4][KPART ? 1 : M / 32][64];
-  float red[4][17][64];        // the second half's partial sums per row block
+  f32x4 red[4][4][64];         // the second half's partial sums per row block
+  float redd[4][64];           // and its h . k-hat
 };
 
 // One workgroup per (head, segment), chunks from the last to the first. The
@@ -1025,18 +1055,14 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     f32x4 (&part)[4] = KPART ? kacc : vacc;
     if (hf == 1) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) sm.red[qb][4 * k + jj][l] = part[k][jj];
-      sm.red[qb][16][l] = doth;
+      for (int k = 0; k < 4; ++k) sm.red[qb][k][l] = part[k];
+      sm.redd[qb][l] = doth;
     }
     __syncthreads();
     if (hf == 0) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) part[k][jj] += sm.red[qb][4 * k + jj][l];
-      doth += sm.red[qb][16][l];
+      for (int k = 0; k < 4; ++k) part[k] += sm.red[qb][k][l];
+      doth += sm.redd[qb][l];
       float D = 1.f;
       if constexpr (KN == kCos) D = cM * expf(s2half * sq_norm16<T>(kf));
       if (j < r1) {
