@@ -120,8 +120,12 @@ def givens_block(seed, head, blk, d, K=None):
     return np.sqrt(d) * B
 
 
-def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI):
+def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI, heads=None):
     """Random-feature matrix W [H, M, d] and phases b [H, M] (Secs. 2.3-2.4).
+
+    heads: optional list of head indices; W and b then hold only those heads, in
+    that order (each head is drawn from its own streams, so a head's rows do
+    not depend on the others).
 
     For each head and each d x d block k < ceil(M/d): a Gaussian block (Philox
     stream, purpose ORF, row-major element index (k d + r) d + c) has its rows
@@ -134,9 +138,10 @@ def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI):
     sqrt(d)) in place of the Gram-Schmidt ones.
     """
     nblk = -(-M // d)
-    W = np.zeros((n_heads, M, d), dtype=np.float64)
-    b = np.zeros((n_heads, M), dtype=np.float64)
-    for h in range(n_heads):
+    hs = list(range(n_heads)) if heads is None else list(heads)
+    W = np.zeros((len(hs), M, d), dtype=np.float64)
+    b = np.zeros((len(hs), M), dtype=np.float64)
+    for i, h in enumerate(hs):
         g = philox.gaussians(seed, h, philox.PURPOSE_ORF, nblk * d * d).reshape(nblk, d, d)
         rows = []
         for k in range(nblk):
@@ -155,8 +160,8 @@ def orf_draw(seed, n_heads, M, d, kind=RF_ORTHO_CHI):
             Wh = Wh * rho[:, None]
         elif kind == RF_ORTHO_FIXED:
             Wh = Wh * np.sqrt(d)
-        W[h] = Wh
-        b[h] = 2.0 * np.pi * philox.uniforms(seed, h, philox.PURPOSE_PHASE, M)
+        W[i] = Wh
+        b[i] = 2.0 * np.pi * philox.uniforms(seed, h, philox.PURPOSE_PHASE, M)
     return W, b
 
 

@@ -175,3 +175,10 @@ def test_orf_draw_structured_kinds_stack_blocks():
     np.testing.assert_allclose(W[1, 64:], favor.hadamard_block(21, 1, 1, 64)[:36], atol=0)
     W, _ = favor.orf_draw(21, 1, 64, 64, favor.RF_GIVENS)
     np.testing.assert_allclose(W[0], favor.givens_block(21, 0, 0, 64), atol=0)
+
+
+def test_orf_draw_head_subset_equals_the_full_draw():
+    """Drawing a subset of heads gives exactly those heads' rows of the full draw."""
+    W, b = favor.orf_draw(5, 6, 100, 64)
+    Ws, bs = favor.orf_draw(5, 6, 100, 64, heads=[4, 1])
+    assert np.array_equal(Ws, W[[4, 1]]) and np.array_equal(bs, b[[4, 1]])
