@@ -327,3 +327,27 @@ def test_header_compiles_as_c_and_after_the_hip_runtime(tmp_path):
                             "-D__HIP_PLATFORM_AMD__", "-I", rocm, "-I", inc, str(cxx)],
                            capture_output=True, text=True)
         assert r.returncode == 0, r.stderr
+
+
+def test_probe_arguments_and_work(L):
+    """favor_probe validates its arguments before any launch; favor_probe_work is
+    linear in the iteration count."""
+    sink = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+    for kind, iters, s in ((3, 1, sink), (-1, 1, sink), (0, 0, sink), (1, -5, sink),
+                           (2, 1, ctypes.c_void_p(0))):
+        assert L.favor_probe(kind, iters, s, None) == 1, (kind, iters)
+        assert "favor_probe" in fv.last_error()
+    for kind in (0, 1, 2):
+        w1, w3 = L.favor_probe_work(kind, 1), L.favor_probe_work(kind, 3)
+        assert w1 > 0 and w3 == 3 * w1, kind
+
+
+def test_timing_table(L):
+    """Kernel ids 0 .. n-1 carry distinct names; reads outside the table fail."""
+    n = L.favor_timing_num_kernels()
+    assert n >= 10
+    names = [L.favor_timing_kernel_name(k).decode() for k in range(n)]
+    assert len(set(names)) == n and all(x.startswith("k_") for x in names)
+    ms, cnt = ctypes.c_double(), ctypes.c_int64()
+    for k in (-1, n):
+        assert L.favor_timing_read(k, ctypes.byref(ms), ctypes.byref(cnt)) == 1
