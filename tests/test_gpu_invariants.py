@@ -235,3 +235,33 @@ def test_side_stream_without_workspace_is_not_raced():
     torch.cuda.synchronize()
     del junk
     assert torch.equal(ob, refb) and torch.equal(oc, refc) and torch.equal(oc1, refc1)
+
+
+# ------------------------------------------------------------ concurrent calls
+def test_concurrent_calls_on_two_streams_match_serial_calls():
+    """The library holds no state between calls (beyond the no-allocation
+    entry point's documented scratch): two calls running at the same time on
+    two streams, each with its own workspace, give bitwise the results of the
+    same calls made one after the other."""
+    import torch
+    fv = _fv()
+    B, H, L, M = 2, 4, 2000, 256
+    Q, K, V = _qkv(B, H, L, "bf16", seed=71)
+    W, b = _features(72, H, M)
+    a = tuple(to_dev(x, "bf16") for x in (Q, K, V)) + (to_dev(W), to_dev(b))
+    Q2, K2, V2 = _qkv(B, H, L, "bf16", seed=73)
+    a2 = tuple(to_dev(x, "bf16") for x in (Q2, K2, V2)) + (to_dev(W), to_dev(b))
+    refb, refc = fv.attn_both(*a, S64)
+    ref2 = fv.attn_causal(*a2, S64, chunk=32)
+    refx = fv.attn_bidir(*a2, S64)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for s in (s1, s2):
+        s.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        ob, oc = fv.attn_both(*a, S64, stream=s1)
+        o2 = fv.attn_causal(*a2, S64, chunk=32, stream=s2)
+        ox = fv.attn_bidir(*a2, S64, stream=s2)
+        torch.cuda.synchronize()
+        assert torch.equal(ob, refb) and torch.equal(oc, refc)
+        assert torch.equal(o2, ref2) and torch.equal(ox, refx)
