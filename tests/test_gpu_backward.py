@@ -322,3 +322,30 @@ def test_backward_reads_the_forward_workspace(dtype, M, kernel):
     Wo = _oracle_w(W, M, dtype, kernel)
     ref, scale, _ = _oracle_grads(Q, K, V, Wo, b, dout, False, **kw)
     _check_all(_host_grads(both_b), ref, dtype, scale)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_single_key_rows_have_vanishing_query_gradient(dtype):
+    """A renormalised row that sees one key returns that key's value whatever the
+    query is, so its dQ is exactly 0 (and with L = 1 so is dK): the rows of an
+    L = 1 call, bidirectional or causal, and the first row of every causal
+    pass without a carried state. The oracle gives 0 to fp64 rounding; the GPU
+    gives rounding noise of the terms that cancel, within the tolerance times
+    their size (the gradient error scale)."""
+    import torch
+    fv = _fv()
+    for L, causal in ((1, False), (1, True), (300, True)):
+        Q, K, V, dout, W, b = _inputs(2, 2, L, 128, dtype, seed=131 + L)
+        q, k, v, do = (to_dev(x, dtype) for x in (Q, K, V, dout))
+        f = fv.attn_causal_backward if causal else fv.attn_bidir_backward
+        dQ, dK = (to_host(x) for x in f(q, k, v, to_dev(W), to_dev(b), S64, do)[:2])
+        torch.cuda.synchronize()
+        ref, scale, _ = _oracle_grads(Q, K, V, W, b, dout, causal)
+        rows = slice(0, 1)   # the single-key row (all of them when L = 1)
+        a = np.max(np.abs(scale["dQ"][..., rows, :]))
+        assert np.max(np.abs(ref["dQ"][..., rows, :])) <= 1e-12 * a
+        assert np.max(np.abs(dQ[..., rows, :])) <= TOL[dtype] * a, (L, causal)
+        if L == 1:
+            ak = np.max(np.abs(scale["dK"]))
+            assert np.max(np.abs(ref["dK"])) <= 1e-12 * ak
+            assert np.max(np.abs(dK)) <= TOL[dtype] * ak, (L, causal)
