@@ -87,12 +87,13 @@ typedef struct {
                                exp(Q K^T / sqrt d) (Sec. 2.1) on the given Q, K.  */
   float denom_eps;          /* added to D-hat before dividing; 0 = Algorithm 1      */
   int32_t chunk;            /* causal chunk length T: tokens per step of the
-                               prefix-sum scan (Sec. 2.5.1); 0 = library default,
-                               64 (four 16-token matrix-core blocks in the
-                               intra-chunk product). bf16 inputs also take 32;
-                               other values, and 32 with fp32 inputs in a causal
-                               call, return FAVOR_ERR_UNSUPPORTED. The result is
-                               the same sum in another grouping                    */
+                               prefix-sum scan (Sec. 2.5.1): 64 (four 16-token
+                               matrix-core blocks in the intra-chunk product) or,
+                               for bf16 inputs, 32; 0 = library default: 32 for
+                               bf16 inputs with M <= 128, else 64. Other values,
+                               and 32 with fp32 inputs in a causal call, return
+                               FAVOR_ERR_UNSUPPORTED. The result is the same sum
+                               in another grouping                                 */
   int32_t kernel;           /* favor_kernel; 0 (zero-initialised) = SOFTMAX         */
   int32_t no_renormalize;   /* 0 = out = Buf3 / (buf4 + denom_eps) (Algorithm 1);
                                1 = out = Buf3 = Q' K'^T V ("renormalize_attention"
@@ -103,7 +104,8 @@ typedef struct {
                                sequence one workgroup scans chunk by chunk from
                                the aggregate of the segments before it (a multiple
                                of 64, at most 2^30); 0 = library default (about one
-                               workgroup per compute unit)                         */
+                               workgroup per compute unit with T = 64, two with
+                               T = 32)                                             */
 } favor_desc;
 
 /*

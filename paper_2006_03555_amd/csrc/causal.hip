@@ -421,6 +421,8 @@ struct CausalFsSmem {
   CausalFsTile<T> tile[2];
   f32x4 num[2][4][3][T / 16][64];   // [buffer][source wave][slot][value block of the unit][lane]
   float den[2][4][3][16];           // [buffer][source wave][slot][token]
+  float bq[256];                    // b'' of the head (T = 32: the query projections read it here)
+  bf16x8 sel[2][64];                // T = 32: the selection fragments of the value transposes
 };
 
 // Selection matrix in loaded k order with B[k][c] = (k == 8 (c / 4) + 4 half + c % 4):
@@ -442,17 +444,57 @@ __device__ __forceinline__ float quad_sum_f32(float v) {
   return v;
 }
 
+// A wave-uniform value the optimiser may not look through (it stays in scalar
+// registers): keeps loop invariant code motion from hoisting loads that are
+// meant to be repeated.
+__device__ __forceinline__ int opaque_uniform(int x) {
+  asm volatile("" : "+s"(x));
+  return x;
+}
+
+// Raw buffer access (T = 32 scan): the base is a scalar resource covering the
+// bytes a call may touch, the lane offset one 32-bit register, so the loop
+// holds no per-lane 64-bit address (with generic pointers the compiler hoists
+// base + lane offset out of the loop as a 64-bit pair per address).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+__device__ __forceinline__ bf16x8 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off, int soff = 0) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, 0));
+}
+__device__ __forceinline__ void buf_store8(__amdgpu_buffer_rsrc_t r, uint32_t off, bf16 *,
+                                           f32x4 a, f32x4 b) {
+  bf16x8 v;
+  v[0] = (bf16)a[0]; v[1] = (bf16)a[1]; v[2] = (bf16)a[2]; v[3] = (bf16)a[3];
+  v[4] = (bf16)b[0]; v[5] = (bf16)b[1]; v[6] = (bf16)b[2]; v[7] = (bf16)b[3];
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0);
+}
+__device__ __forceinline__ void buf_store8(__amdgpu_buffer_rsrc_t r, uint32_t off, float *,
+                                           f32x4 a, f32x4 b) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, a), r, off, 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, b), r, off + 16, 0, 0);
+}
+
 // Query rows of a T-token tile, row (tid mod 4T) / 4, 16 columns (T = 32:
 // waves 0 and 1 load them, waves 2 and 3 take zeros).
 template <int T>
 __device__ __forceinline__ void load_q_rows(bf16x8 (&q)[2], const bf16 *__restrict__ Qh, int t0,
                                             int r1) {
   const int tid = threadIdx.x;
-  const int rq = t0 + (T == 64 ? tid >> 2 : (tid & 127) >> 2);
-  if (rq < r1 && (T == 64 || tid < 4 * T)) {
-    const bf16 *qp = Qh + (size_t)rq * kD + (tid & 3) * 16;
-    q[0] = load_frag<bf16>(qp);
-    q[1] = load_frag<bf16>(qp + 8);
+  const int lr = T == 64 ? tid >> 2 : (tid & 127) >> 2;
+  if (t0 + lr < r1 && (T == 64 || tid < 4 * T)) {
+    if constexpr (T == 64) {
+      const bf16 *qp = Qh + (size_t)(t0 + lr) * kD + (tid & 3) * 16;
+      q[0] = load_frag<bf16>(qp);
+      q[1] = load_frag<bf16>(qp + 8);
+    } else {
+      const auto rs = buf_rsrc(Qh + (size_t)t0 * kD, T * kD * 2);
+      const uint32_t off = (lr * kD + (tid & 3) * 16) * 2;
+      q[0] = buf_load16(rs, off);
+      q[1] = buf_load16(rs, off + 16);
+    }
   } else {
     q[0] = Mma<bf16>::splat(0.f);
     q[1] = Mma<bf16>::splat(0.f);
@@ -473,18 +515,20 @@ __device__ __forceinline__ void load_causal_tile_regs(TileRegs<bf16> &r, const b
   } else {
     const int l = tid & 63;
     const int w = tid >> 6;
-    const int rk = t0 + ((tid & 127) >> 2);
-    const int rv = t0 + 16 * (w & 1) + (l & 15);
-    if (rk < r1) {
-      const bf16 *kp = Kh + (size_t)rk * kD + (tid & 3) * 16;
-      r.k[0] = load_frag<bf16>(kp);
-      r.k[1] = load_frag<bf16>(kp + 8);
+    const int lk = (tid & 127) >> 2;
+    const int lv = 16 * (w & 1) + (l & 15);
+    if (t0 + lk < r1) {
+      const auto rs = buf_rsrc(Kh + (size_t)t0 * kD, T * kD * 2);
+      const uint32_t off = (lk * kD + (tid & 3) * 16) * 2;
+      r.k[0] = buf_load16(rs, off);
+      r.k[1] = buf_load16(rs, off + 16);
     } else {
       r.k[0] = Mma<bf16>::splat(0.f);
       r.k[1] = Mma<bf16>::splat(0.f);
     }
-    r.v[0] = rv < r1 ? load_frag<bf16>(Vh + (size_t)rv * kD + 32 * (w >> 1) + 8 * (l >> 4))
-                     : Mma<bf16>::splat(0.f);
+    r.v[0] = t0 + lv < r1 ? buf_load16(buf_rsrc(Vh + (size_t)t0 * kD, T * kD * 2),
+                                       (lv * kD + 32 * (w >> 1) + 8 * (l >> 4)) * 2)
+                          : Mma<bf16>::splat(0.f);
   }
 }
 
@@ -496,8 +540,9 @@ __device__ __forceinline__ void load_causal_tile_regs(TileRegs<bf16> &r, const b
 // (the query factor when not renormalising).
 template <int T, int KN, bool RN>
 __device__ __forceinline__ void stage_causal_tile(CausalFsTile<T> &tl, const TileRegs<bf16> &r,
-                                                  const bf16x8 (&q)[2], int t0, int r1,
-                                                  float s2half, float cM, float eps) {
+                                                  const bf16x8 (&q)[2], const bf16x8 (&sel)[2],
+                                                  int t0, int r1, float s2half, float cM,
+                                                  float eps) {
   using P = Mma<bf16>;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
@@ -522,7 +567,6 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile<T> &tl, const Til
   float Dj[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) Dj[j] = __shfl(Dt, 16 * g + 4 * j);
-  const bf16x8 sel[2] = {select_perm_frag(0), select_perm_frag(1)};
   const int sidx = T == 64 ? w >> 1 : 0;
   const int hw = w & 1;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
@@ -554,7 +598,7 @@ __device__ __forceinline__ void stage_causal_tile(CausalFsTile<T> &tl, const Til
 }
 
 template <typename To, int M, int KN, bool RN, bool SAVE, int T = 64>
-__global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2 : 1))) void k_causal_fs(const bf16 *__restrict__ Q,
                                                    const bf16 *__restrict__ K,
                                                    const bf16 *__restrict__ V,
                                                    const bf16x8 *__restrict__ wfr,
@@ -585,6 +629,15 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   const int c16 = l & 15;
   const int utb = T == 64 ? w : (w & 1);   // this wave's output unit: token block,
   const int uvh = T == 64 ? 0 : (w >> 1);  // and value-column group (T = 32)
+  // T = 32 runs two workgroups per CU (two waves per SIMD, at most 256 registers
+  // each). M = 256 fits only in a reordered chunk: the seeds b'' stay in LDS
+  // and W'' is loaded again for every chunk, a chunk starts with the previous
+  // chunk's finalisation, the next tile is staged after the features, the
+  // loads of the one after it go out after the contractions, and the
+  // contractions run one value block at a time, each block handed over as
+  // soon as it is complete. Smaller M keeps the order of the 64-token chunk,
+  // which is faster where it fits.
+  constexpr bool kLate = T == 32 && M > 128;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
 
   const bf16 *Qh = Q + (size_t)bh * L * kD;
@@ -606,17 +659,50 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
   frag wf[MB][2];
   float bk[MB];
   f32x4 bqv[MB];
+  // T = 32: the fragments are loaded again for every chunk (after the previous
+  // chunk's contractions), from a base the compiler may not treat as loop
+  // invariant, so that they are not held across the contractions
+  const frag *whead = wfr + (size_t)h * (M / 16) * 2 * 64;
+  auto load_wf = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      if constexpr (kLate) {
+        const auto rs = buf_rsrc(whead, (M / 16) * 2 * 64 * 16);
+        const int again = opaque_uniform(0);
+        wf[mb][0] = buf_load16(rs, ((w * MB + mb) * 2 * 64 + l) * 16, again);
+        wf[mb][1] = buf_load16(rs, ((w * MB + mb) * 2 * 64 + 64 + l) * 16, again);
+      } else {
+        wf[mb][0] = whead[(w * MB + mb) * 2 * 64 + l];
+        wf[mb][1] = whead[(w * MB + mb) * 2 * 64 + 64 + l];
+      }
+    }
+  };
+  load_wf();
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int mbg = w * MB + mb;
-    const frag *wh = wfr + ((size_t)h * (M / 16) + mbg) * 2 * 64;
-    wf[mb][0] = wh[l];
-    wf[mb][1] = wh[64 + l];
     const float *bb = bqg + (size_t)h * M + 16 * mbg;
-    bk[mb] = bb[c16];
+    if constexpr (!kLate) {
+      bk[mb] = bb[c16];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bqv[mb][j] = bb[4 * g + j];
+      for (int j = 0; j < 4; ++j) bqv[mb][j] = bb[4 * g + j];
+    }
   }
+  if (kLate && tid < M) sm.bq[tid] = bqg[(size_t)h * M + tid];
+  // b'' of feature rows w MW + 16 mb + 4 g .. + 3 (the query projections'
+  // seeds) and of feature w MW + 16 mb + c16 (the key projections')
+  auto qseed = [&](int mb) __attribute__((always_inline)) {
+    if constexpr (kLate)
+      return *reinterpret_cast<const f32x4 *>(&sm.bq[w * MW + 16 * mb + 4 * g]);
+    else
+      return bqv[mb];
+  };
+  auto kseed = [&](int mb) __attribute__((always_inline)) {
+    if constexpr (kLate)
+      return sm.bq[w * MW + 16 * mb + c16];
+    else
+      return bk[mb];
+  };
 
   // state rows m = w MW + 16 mb + 4 g + j, lane column c16 of block nb holding
   // value column pi(nb, c16) (block 4: the ones column in all 16 columns)
@@ -634,7 +720,14 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       }
   }
 
-  stage_causal_tile<T, KN, RN>(sm.tile[0], rg, rq, r0, r1, s2half, cM, eps);
+  // selection fragments of the value transposes (T = 32: read from LDS at
+  // each staging after the first)
+  const bf16x8 sel0[2] = {select_perm_frag(0), select_perm_frag(1)};
+  if (kLate && w == 0) {
+    sm.sel[0][l] = sel0[0];
+    sm.sel[1][l] = sel0[1];
+  }
+  stage_causal_tile<T, KN, RN>(sm.tile[0], rg, rq, sel0, r0, r1, s2half, cM, eps);
   if (r0 + T < r1) {
     load_causal_tile_regs<T>(rg, Kh, Vh, r0 + T, r1, tid);
     load_q_rows<T>(rq, Qh, r0 + T, r1);
@@ -665,7 +758,12 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       const float inv = RN ? 1.0f / (den + own_epsq) : own_epsq;
 #pragma unroll
       for (int pp = 0; pp < NVB / 2; ++pp)
-        store8(Oh + (size_t)qt * kD + 32 * (uvh * (NVB / 2) + pp) + 8 * g, num[2 * pp] * inv,
+        if constexpr (kLate)
+          buf_store8(buf_rsrc(Oh + (size_t)tp * kD, T * kD * sizeof(To)),
+                     ((16 * utb + c16) * kD + 32 * (uvh * (NVB / 2) + pp) + 8 * g) * sizeof(To),
+                     Oh, num[2 * pp] * inv, num[2 * pp + 1] * inv);
+        else
+          store8(Oh + (size_t)qt * kD + 32 * (uvh * (NVB / 2) + pp) + 8 * g, num[2 * pp] * inv,
                num[2 * pp + 1] * inv);
       if constexpr (SAVE) {
         if (g == 0 && uvh == 0) rsave[(size_t)bh * L + qt] = inv;
@@ -686,8 +784,10 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
       my_epsq = (!RN || eps != 0.f) ? tl.epsq[16 * utb + c16] : 0.f;
     else
       my_epsq = RN ? eps : 1.f;
-    if (t0 + T < r1) {
-      stage_causal_tile<T, KN, RN>(sm.tile[buf ^ 1], rg, rq, t0 + T, r1, s2half, cM, eps);
+    if constexpr (kLate) {
+      if (t0 > r0) finalize(t0 - T, buf ^ 1);
+    } else if (t0 + T < r1) {
+      stage_causal_tile<T, KN, RN>(sm.tile[buf ^ 1], rg, rq, sel0, t0 + T, r1, s2half, cM, eps);
       if (t0 + 2 * T < r1) {
         load_causal_tile_regs<T>(rg, Kh, Vh, t0 + 2 * T, r1, tid);
         load_q_rows<T>(rq, Qh, t0 + 2 * T, r1);
@@ -714,10 +814,10 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           if constexpr (i < NTB) {   // C[m][t] = W'' q_t + b''
-            pr[mb] = P::mma(wf[mb][0], r[0], bqv[mb]);
+            pr[mb] = P::mma(wf[mb][0], r[0], qseed(mb));
             pr[mb] = P::mma(wf[mb][1], r[1], pr[mb]);
           } else {                 // C[t][m] = W'' k_t + b''
-            const float bb = bk[mb];
+            const float bb = kseed(mb);
             pr[mb] = P::mma(r[0], wf[mb][0], f32x4{bb, bb, bb, bb});
             pr[mb] = P::mma(r[1], wf[mb][1], pr[mb]);
           }
@@ -728,10 +828,15 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
         constexpr int i = decltype(ic)::value;
         constexpr int tb = i % NTB;
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+        for (int mb = 0; mb < MB; ++mb) {
+          f32x4 sd;
+          if constexpr (i < NTB)
+            sd = qseed(mb);
+          else
+            sd = f32x4{kseed(mb), kseed(mb), kseed(mb), kseed(mb)};
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            pr[mb][j] = feature<KN, P>(pr[mb][j], i < NTB ? bqv[mb][j] : bk[mb]);
+          for (int j = 0; j < 4; ++j) pr[mb][j] = feature<KN, P>(pr[mb][j], sd[j]);
+        }
         if constexpr (i < NTB) {
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks)
@@ -781,107 +886,200 @@ __global__ __launch_bounds__(256) void k_causal_fs(const bf16 *__restrict__ Q,
         for (int sx = 0; sx < NKH; ++sx) asm volatile("" : "+v"(kA[mb][sx]));
     }
 
-    if (t0 > r0) finalize(t0 - T, buf ^ 1);
-
-    // partial Buf2 (value columns and the denominator) over this slice: o[nb][tb]
-    // holds rows pi(nb, 4 g + j), column = token 16 tb + c16; first Q-hat S with
-    // the state before the chunk
-    f32x4 o[5][NTB];
-#pragma unroll
-    for (int nb = 0; nb < 5; ++nb) {
-      frag sA[KS];   // lane row = value column, k = m
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        sA[ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb) {
-        o[nb][tb] = P::mma(sA[0], qB[tb][0], zero4);
-#pragma unroll
-        for (int ks = 1; ks < KS; ++ks) o[nb][tb] = P::mma(sA[ks], qB[tb][ks], o[nb][tb]);
+    if constexpr (kLate) {
+      if (t0 + T < r1) {
+        const bf16x8 sel[2] = {sm.sel[0][l], sm.sel[1][l]};
+        stage_causal_tile<T, KN, RN>(sm.tile[buf ^ 1], rg, rq, sel, t0 + T, r1, s2half, cM, eps);
       }
+    } else if (t0 > r0) {
+      finalize(t0 - T, buf ^ 1);
     }
 
-    // keys, one 32-token half at a time: fold into S (after the queries above
-    // used it), transpose to token rows on the matrix cores, then the
-    // intra-chunk part of that half: P^T[t'][t] = K-hat_t' . Q-hat_t over the
-    // slice for key blocks tb' <= tb (keys after the query zeroed) and C~^T P^T
-    // into o
-#pragma unroll
-    for (int sidx = 0; sidx < NKH; ++sidx) {
-      // C~ of the half: B operand of the state update and A operand of the
-      // intra-chunk product (lane = value column, k = token in chained order)
-      frag vt[4];
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) vt[nb] = tl.VtF[nb][sidx][l];
-      const frag df = tl.DF[sidx][g];
-      frag kT[2][KS];   // A operand: lane row = token 32 sidx + 16 tbl + c16, k = 32 features
+    if constexpr (kLate) {
+      // one 32-token block of keys: its features transposed to token rows on
+      // the matrix cores, then the masked P^T[t'][t] = K-hat_t' . Q-hat_t over
+      // the slice for each query block (keys after the query zeroed)
+      frag kT[2][KS];   // A operand: lane row = token 16 tbl + c16, k = 32 features
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         f32x4 ct[2][2];
 #pragma unroll
-        for (int hm = 0; hm < 2; ++hm) {
-          const int mb = 2 * ks + hm;
-          if (mb >= MB) {
-            ct[0][hm] = zero4;
-            ct[1][hm] = zero4;
-            continue;
-          }
-          const frag a = kA[mb][sidx];
-#pragma unroll
-          for (int nb = 0; nb < 4; ++nb) accS[mb][nb] = P::mma(a, vt[nb], accS[mb][nb]);
-          accS[mb][4] = P::mma(a, df, accS[mb][4]);
+        for (int hm = 0; hm < 2; ++hm)
 #pragma unroll
           for (int tbl = 0; tbl < 2; ++tbl)
-            ct[tbl][hm] = P::mma(a, chained_select_frag<bf16>(tbl), zero4);
-        }
+            ct[tbl][hm] = (2 * ks + hm < MB)
+                              ? P::mma(kA[2 * ks + hm][0], chained_select_frag<bf16>(tbl), zero4)
+                              : zero4;
 #pragma unroll
         for (int tbl = 0; tbl < 2; ++tbl) kT[tbl][ks] = P::pack(ct[tbl][0], ct[tbl][1]);
       }
+      frag pb[NTB];
 #pragma unroll
-      for (int tb = 2 * sidx; tb < NTB; ++tb) {
+      for (int tb = 0; tb < NTB; ++tb) {
         f32x4 pt[2];
 #pragma unroll
         for (int tbl = 0; tbl < 2; ++tbl) {
-          const int tp = 2 * sidx + tbl;
-          if (tp > tb) {
+          if (tbl > tb) {
             pt[tbl] = zero4;
             continue;
           }
           pt[tbl] = P::mma(kT[tbl][0], qB[tb][0], zero4);
 #pragma unroll
           for (int ks = 1; ks < KS; ++ks) pt[tbl] = P::mma(kT[tbl][ks], qB[tb][ks], pt[tbl]);
-          if (tp == tb) {
+          if (tbl == tb) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) pt[tbl][j] = (4 * g + j <= c16) ? pt[tbl][j] : 0.f;
           }
         }
-        const frag pb = P::pack(pt[0], pt[1]);
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb) o[nb][tb] = P::mma(vt[nb], pb, o[nb][tb]);
-        o[4][tb] = P::mma(df, pb, o[4][tb]);
+        pb[tb] = P::pack(pt[0], pt[1]);
       }
-    }
+      // one value block at a time (the ones column last): Q-hat S with the
+      // state before the chunk, plus C~^T P^T, handed over (or kept when it is
+      // this wave's unit: token block u % 2, value blocks 2 (u / 2) ..); then
+      // the chunk's keys are folded into that block of S
+      const int wu = __builtin_amdgcn_readfirstlane(w);
+#pragma unroll
+      for (int nb = 0; nb < 5; ++nb) {
+        frag sA[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          sA[ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
+        const frag vt = nb < 4 ? tl.VtF[nb][0][l] : tl.DF[0][g];
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb) {
+          f32x4 on = P::mma(sA[0], qB[tb][0], zero4);
+#pragma unroll
+          for (int ks = 1; ks < KS; ++ks) on = P::mma(sA[ks], qB[tb][ks], on);
+          on = P::mma(vt, pb[tb], on);
+          if (nb < 4) {
+            const int u = 2 * (nb >> 1) + tb;
+            if (u == wu)
+              own[nb & 1] = on;
+            else
+              sm.num[buf][w][(u - w - 1) & 3][nb & 1][l] = on;
+          } else {
+#pragma unroll
+            for (int u = tb; u < 4; u += 2) {
+              if (u == wu)
+                own[4] = on;
+              else if (g == 0)
+                sm.den[buf][w][(u - w - 1) & 3][c16] = on[0];
+            }
+          }
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) accS[mb][nb] = P::mma(kA[mb][0], vt, accS[mb][nb]);
+      }
+      own_epsq = my_epsq;
+      if constexpr (kLate) {
+        if (t0 + 2 * T < r1) {
+          load_causal_tile_regs<T>(rg, Kh, Vh, t0 + 2 * T, r1, tid);
+          load_q_rows<T>(rq, Qh, t0 + 2 * T, r1);
+        }
+        if (t0 + T < r1) load_wf();
+      }
 
-    // hand the partials of the other waves' units over; keep this wave's own
-    // (unit u: token block u % NTB, value blocks NVB (u / NTB) ..)
-    if constexpr (T == 64) {
-#pragma unroll
-      for (int nb = 0; nb < 5; ++nb)
-        own[nb] = (w == 0) ? o[nb][0] : (w == 1) ? o[nb][1] : (w == 2) ? o[nb][2] : o[nb][3];
     } else {
-#pragma unroll
-      for (int k = 0; k < NVB; ++k)
-        own[k] = (w == 0) ? o[k][0] : (w == 1) ? o[k][1] : (w == 2) ? o[NVB + k][0] : o[NVB + k][1];
-      own[4] = (w & 1) ? o[4][1] : o[4][0];
-    }
-    own_epsq = my_epsq;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (u != w) {
-        const int slot = (u - w - 1) & 3;
-#pragma unroll
-        for (int k = 0; k < NVB; ++k) sm.num[buf][w][slot][k][l] = o[NVB * (u / NTB) + k][u % NTB];
-        if (g == 0) sm.den[buf][w][slot][c16] = o[4][u % NTB][0];
+      // partial Buf2 (value columns and the denominator) over this slice: o[nb][tb]
+      // holds rows pi(nb, 4 g + j), column = token 16 tb + c16; first Q-hat S with
+      // the state before the chunk
+      f32x4 o[5][NTB];
+  #pragma unroll
+      for (int nb = 0; nb < 5; ++nb) {
+        frag sA[KS];   // lane row = value column, k = m
+  #pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          sA[ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
+  #pragma unroll
+        for (int tb = 0; tb < NTB; ++tb) {
+          o[nb][tb] = P::mma(sA[0], qB[tb][0], zero4);
+  #pragma unroll
+          for (int ks = 1; ks < KS; ++ks) o[nb][tb] = P::mma(sA[ks], qB[tb][ks], o[nb][tb]);
+        }
+      }
+
+      // keys, one 32-token half at a time: fold into S (after the queries above
+      // used it), transpose to token rows on the matrix cores, then the
+      // intra-chunk part of that half: P^T[t'][t] = K-hat_t' . Q-hat_t over the
+      // slice for key blocks tb' <= tb (keys after the query zeroed) and C~^T P^T
+      // into o
+  #pragma unroll
+      for (int sidx = 0; sidx < NKH; ++sidx) {
+        // C~ of the half: B operand of the state update and A operand of the
+        // intra-chunk product (lane = value column, k = token in chained order)
+        frag vt[4];
+  #pragma unroll
+        for (int nb = 0; nb < 4; ++nb) vt[nb] = tl.VtF[nb][sidx][l];
+        const frag df = tl.DF[sidx][g];
+        frag kT[2][KS];   // A operand: lane row = token 32 sidx + 16 tbl + c16, k = 32 features
+  #pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          f32x4 ct[2][2];
+  #pragma unroll
+          for (int hm = 0; hm < 2; ++hm) {
+            const int mb = 2 * ks + hm;
+            if (mb >= MB) {
+              ct[0][hm] = zero4;
+              ct[1][hm] = zero4;
+              continue;
+            }
+            const frag a = kA[mb][sidx];
+  #pragma unroll
+            for (int nb = 0; nb < 4; ++nb) accS[mb][nb] = P::mma(a, vt[nb], accS[mb][nb]);
+            accS[mb][4] = P::mma(a, df, accS[mb][4]);
+  #pragma unroll
+            for (int tbl = 0; tbl < 2; ++tbl)
+              ct[tbl][hm] = P::mma(a, chained_select_frag<bf16>(tbl), zero4);
+          }
+  #pragma unroll
+          for (int tbl = 0; tbl < 2; ++tbl) kT[tbl][ks] = P::pack(ct[tbl][0], ct[tbl][1]);
+        }
+  #pragma unroll
+        for (int tb = 2 * sidx; tb < NTB; ++tb) {
+          f32x4 pt[2];
+  #pragma unroll
+          for (int tbl = 0; tbl < 2; ++tbl) {
+            const int tp = 2 * sidx + tbl;
+            if (tp > tb) {
+              pt[tbl] = zero4;
+              continue;
+            }
+            pt[tbl] = P::mma(kT[tbl][0], qB[tb][0], zero4);
+  #pragma unroll
+            for (int ks = 1; ks < KS; ++ks) pt[tbl] = P::mma(kT[tbl][ks], qB[tb][ks], pt[tbl]);
+            if (tp == tb) {
+  #pragma unroll
+              for (int j = 0; j < 4; ++j) pt[tbl][j] = (4 * g + j <= c16) ? pt[tbl][j] : 0.f;
+            }
+          }
+          const frag pb = P::pack(pt[0], pt[1]);
+  #pragma unroll
+          for (int nb = 0; nb < 4; ++nb) o[nb][tb] = P::mma(vt[nb], pb, o[nb][tb]);
+          o[4][tb] = P::mma(df, pb, o[4][tb]);
+        }
+      }
+
+      // hand the partials of the other waves' units over; keep this wave's own
+      // (unit u: token block u % NTB, value blocks NVB (u / NTB) ..)
+      if constexpr (T == 64) {
+  #pragma unroll
+        for (int nb = 0; nb < 5; ++nb)
+          own[nb] = (w == 0) ? o[nb][0] : (w == 1) ? o[nb][1] : (w == 2) ? o[nb][2] : o[nb][3];
+      } else {
+  #pragma unroll
+        for (int k = 0; k < NVB; ++k)
+          own[k] = (w == 0) ? o[k][0] : (w == 1) ? o[k][1] : (w == 2) ? o[NVB + k][0] : o[NVB + k][1];
+        own[4] = (w & 1) ? o[4][1] : o[4][0];
+      }
+      own_epsq = my_epsq;
+  #pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (u != w) {
+          const int slot = (u - w - 1) & 3;
+  #pragma unroll
+          for (int k = 0; k < NVB; ++k) sm.num[buf][w][slot][k][l] = o[NVB * (u / NTB) + k][u % NTB];
+          if (g == 0) sm.den[buf][w][slot][c16] = o[4][u % NTB][0];
+        }
       }
     }
     __syncthreads();

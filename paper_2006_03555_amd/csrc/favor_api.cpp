@@ -51,8 +51,9 @@ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 int padded_m(int M) { return M <= 64 ? 64 : M <= 128 ? 128 : 256; }
 
 constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
-// the causal pass holds a whole compute unit per workgroup (LDS and registers),
-// so its segments are sized for one workgroup per CU
+// the causal pass with 64-token chunks holds a whole compute unit per
+// workgroup (LDS and registers), so its segments are sized for one workgroup
+// per CU; with 32-token chunks two workgroups share a CU
 constexpr int kCausalWorkgroups = 256;
 constexpr int kMinRowsPerSplit = 256;
 // Longest sequence per head (and longest causal segment): the kernels index
@@ -62,6 +63,14 @@ constexpr int kMaxL = 1 << 30;
 // blocks in the intra-chunk product); bf16 inputs also take 32.
 constexpr int kChunk = 64;
 constexpr int kChunkSmall = 32;
+
+// The chunk length a call runs with: the descriptor's, or by default 32 for
+// bf16 inputs with at most 128 feature rows (two workgroups per CU scan those
+// faster) and 64 otherwise.
+int chunk_len(const favor_desc *g) {
+  if (g->chunk != 0) return g->chunk;
+  return g->in_dtype == FAVOR_BF16 && padded_m(g->M) <= 128 ? kChunkSmall : kChunk;
+}
 
 enum Op {
   kOpFeatureMap = 0,
@@ -187,8 +196,9 @@ Plan make_plan(const favor_desc *g, int op) {
   } else {
     // a two-group k_kside workgroup fills a CU by itself
     const favor::Dt in = g->in_dtype == FAVOR_BF16 ? favor::Dt::BF16 : favor::Dt::F32;
-    const int target = causal ? kCausalWorkgroups
-                              : kTargetWorkgroups / favor::kside_groups(in, padded_m(g->M));
+    const int target = !causal ? kTargetWorkgroups / favor::kside_groups(in, padded_m(g->M))
+                       : chunk_len(g) == kChunkSmall ? 2 * kCausalWorkgroups
+                                                     : kCausalWorkgroups;
     int want = (target + p.BH - 1) / p.BH;
     int max_split = tiles / (kMinRowsPerSplit / 64);
     if (max_split < 1) max_split = 1;
@@ -251,7 +261,7 @@ favor::Shape shape_of(const favor_desc *g) {
   sh.kernel = g->kernel;
   sh.renorm = g->no_renormalize ? 0 : 1;
   sh.keps = g->kernel == FAVOR_KERNEL_RELU ? g->kernel_eps : 0.f;
-  sh.chunk = g->chunk == 0 ? kChunk : g->chunk;
+  sh.chunk = chunk_len(g);
   return sh;
 }
 

@@ -109,6 +109,27 @@ def test_chunk_32_needs_bf16_inputs_for_the_scan():
     assert fv.validate_desc(_desc(chunk=32), fv.OP_CAUSAL_BACKWARD) == 0
 
 
+def test_default_chunk_and_segments():
+    """chunk = 0 scans bf16 inputs with M <= 128 in 32-token chunks, whose
+    workgroups share a compute unit two by two, so the default segments are
+    halved (twice the segment aggregates in the workspace); M = 256 and fp32
+    inputs default to 64-token chunks and one workgroup per compute unit."""
+    def ws(op=1, **kw):
+        return fv.workspace_size(_desc(B=1, H=2, L=65536, **kw), op)
+    for op in (1, 2):
+        for M in (64, 128):
+            assert ws(op, M=M) == ws(op, M=M, chunk=32)
+            assert ws(op, M=M) > ws(op, M=M, chunk=64)
+        assert ws(op, M=256) == ws(op, M=256, chunk=64)
+        assert ws(op, M=256) < ws(op, M=256, chunk=32)
+        f32 = dict(in_dtype=fv.F32, out_dtype=fv.F32, M=128)
+        assert ws(op, **f32) == ws(op, **f32, chunk=64)
+    # segment aggregates: M x 65 fp32 per segment; with an explicit segment
+    # length the chunk does not change the plan
+    assert ws(M=128, chunk=32) - ws(M=128, chunk=64) == 256 * 128 * 65 * 4
+    assert ws(M=128, segment=1024) == ws(M=128, segment=1024, chunk=64)
+
+
 def test_fp32_causal_takes_every_m():
     """fp32 causal at M > 128 runs as two feature-half passes, which need a
     [B*H][L][68] fp32 area of workspace more than M = 128."""

@@ -84,6 +84,9 @@ def test_chunk32_causal_parity(B, H, L, M, segment, kernel, renorm, eps, state, 
     e = parity(to_host(o32), Q, K, V, W, b, S64, True, "bf16", eps=eps, state_in=S0,
                kernel=kernel, renormalize=renorm, gate=gate)
     print(f"chunk 32: E_row {e[0]:.2e} E_cond {e[1]:.2e}", flush=True)
+    e = parity(to_host(o64), Q, K, V, W, b, S64, True, "bf16", eps=eps, state_in=S0,
+               kernel=kernel, renormalize=renorm, gate=gate)
+    print(f"chunk 64: E_row {e[0]:.2e} E_cond {e[1]:.2e}", flush=True)
     assert torch.equal(s32, s64)
     if gate == "both":
         a, c = to_host(o32), to_host(o64)

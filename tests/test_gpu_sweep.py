@@ -2,8 +2,8 @@
 point (favor_feature_map, favor_attn_bidir, favor_attn_causal, favor_attn_both),
 each against the fp64 oracle on the same inputs and features: B, H, ragged L,
 any M that is a multiple of 16, in/out dtypes, feature kind, renormalisation,
-stabiliser, causal segment length, the scan's chunk length (every third bf16
-case takes 32 tokens) and a carried state (cos features from M 64,
+stabiliser, causal segment length, the scan's chunk length (bf16 cases cycle
+through 32, 64 and the default) and a carried state (cos features from M 64,
 ReLU features from M 16; a second list takes cos features at M 16 to 48 and
 gates them by E_cond alone). The configurations are drawn once from a fixed seed,
 so a failure names a reproducible case.
@@ -87,9 +87,11 @@ def test_random_configuration(cfg):
     import torch
     fv = __import__("paper_2006_03555_amd")
     B, H, L, M, dtype = cfg["B"], cfg["H"], cfg["L"], cfg["M"], cfg["dtype"]
-    # every third bf16 case scans 32-token chunks (fp32 inputs take 64)
-    chunk = 32 if dtype == "bf16" and cfg["case"] % 3 == 1 else 0
-    print(f"\n{cfg} chunk {chunk or 64}", flush=True)
+    # bf16 cases cycle through 32-token chunks, 64-token chunks and the library
+    # default (32 for M <= 128, else 64); fp32 inputs take 64
+    chunk = (0, 32, 64)[cfg["case"] % 3] if dtype == "bf16" else 0
+    eff = chunk or (32 if dtype == "bf16" and M <= 128 else 64)
+    print(f"\n{cfg} chunk {eff}", flush=True)
     Q, K, V = wl.make_qkv(wl.Workload("t", "bidir", B, H, L, 64, 64, dtype,
                                       1000 + cfg["case"]))
     W, b = favor.orf_draw(2000 + cfg["case"], H, M, 64, cfg["kind"])
