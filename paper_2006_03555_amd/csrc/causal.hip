@@ -638,6 +638,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
   // soon as it is complete. Smaller M keeps the order of the 64-token chunk,
   // which is faster where it fits.
   constexpr bool kLate = T == 32 && M > 128;
+  // The contractions streamed one value block at a time (each block handed
+  // over as soon as it is complete) hold far fewer partial outputs; with
+  // 64-token chunks (one wave per SIMD either way) the form that first forms
+  // all partials and then hands them over is 2% faster.
+  constexpr bool kStream = kLate;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
 
   const bf16 *Qh = Q + (size_t)bh * L * kD;
@@ -895,48 +900,53 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
       finalize(t0 - T, buf ^ 1);
     }
 
-    if constexpr (kLate) {
-      // one 32-token block of keys: its features transposed to token rows on
-      // the matrix cores, then the masked P^T[t'][t] = K-hat_t' . Q-hat_t over
-      // the slice for each query block (keys after the query zeroed)
-      frag kT[2][KS];   // A operand: lane row = token 16 tbl + c16, k = 32 features
+    if constexpr (kStream) {
+      // the chunk's key features, one 32-token half at a time, transposed to
+      // token rows on the matrix cores; then the masked P^T[t'][t] = K-hat_t' .
+      // Q-hat_t over the slice for each (key half, query block) with keys up
+      // to the query (the keys after it zeroed)
+      frag pb[NKH][NTB];   // [half][query block]: used for tb >= 2 half
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        f32x4 ct[2][2];
+      for (int sidx = 0; sidx < NKH; ++sidx) {
+        frag kT[2][KS];   // A operand: lane row = token 32 sidx + 16 tbl + c16, k = 32 features
 #pragma unroll
-        for (int hm = 0; hm < 2; ++hm)
+        for (int ks = 0; ks < KS; ++ks) {
+          f32x4 ct[2][2];
 #pragma unroll
-          for (int tbl = 0; tbl < 2; ++tbl)
-            ct[tbl][hm] = (2 * ks + hm < MB)
-                              ? P::mma(kA[2 * ks + hm][0], chained_select_frag<bf16>(tbl), zero4)
-                              : zero4;
+          for (int hm = 0; hm < 2; ++hm)
 #pragma unroll
-        for (int tbl = 0; tbl < 2; ++tbl) kT[tbl][ks] = P::pack(ct[tbl][0], ct[tbl][1]);
-      }
-      frag pb[NTB];
+            for (int tbl = 0; tbl < 2; ++tbl)
+              ct[tbl][hm] = (2 * ks + hm < MB)
+                                ? P::mma(kA[2 * ks + hm][sidx], chained_select_frag<bf16>(tbl), zero4)
+                                : zero4;
 #pragma unroll
-      for (int tb = 0; tb < NTB; ++tb) {
-        f32x4 pt[2];
-#pragma unroll
-        for (int tbl = 0; tbl < 2; ++tbl) {
-          if (tbl > tb) {
-            pt[tbl] = zero4;
-            continue;
-          }
-          pt[tbl] = P::mma(kT[tbl][0], qB[tb][0], zero4);
-#pragma unroll
-          for (int ks = 1; ks < KS; ++ks) pt[tbl] = P::mma(kT[tbl][ks], qB[tb][ks], pt[tbl]);
-          if (tbl == tb) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) pt[tbl][j] = (4 * g + j <= c16) ? pt[tbl][j] : 0.f;
-          }
+          for (int tbl = 0; tbl < 2; ++tbl) kT[tbl][ks] = P::pack(ct[tbl][0], ct[tbl][1]);
         }
-        pb[tb] = P::pack(pt[0], pt[1]);
+#pragma unroll
+        for (int tb = 2 * sidx; tb < NTB; ++tb) {
+          f32x4 pt[2];
+#pragma unroll
+          for (int tbl = 0; tbl < 2; ++tbl) {
+            const int tp = 2 * sidx + tbl;
+            if (tp > tb) {
+              pt[tbl] = zero4;
+              continue;
+            }
+            pt[tbl] = P::mma(kT[tbl][0], qB[tb][0], zero4);
+#pragma unroll
+            for (int ks = 1; ks < KS; ++ks) pt[tbl] = P::mma(kT[tbl][ks], qB[tb][ks], pt[tbl]);
+            if (tp == tb) {
+#pragma unroll
+              for (int j = 0; j < 4; ++j) pt[tbl][j] = (4 * g + j <= c16) ? pt[tbl][j] : 0.f;
+            }
+          }
+          pb[sidx][tb] = P::pack(pt[0], pt[1]);
+        }
       }
       // one value block at a time (the ones column last): Q-hat S with the
-      // state before the chunk, plus C~^T P^T, handed over (or kept when it is
-      // this wave's unit: token block u % 2, value blocks 2 (u / 2) ..); then
-      // the chunk's keys are folded into that block of S
+      // state before the chunk, plus C~^T P^T of each key half, handed over (or
+      // kept when it is this wave's unit u: token block u % NTB, value blocks
+      // NVB (u / NTB) ..); then the chunk's keys are folded into that block of S
       const int wu = __builtin_amdgcn_readfirstlane(w);
 #pragma unroll
       for (int nb = 0; nb < 5; ++nb) {
@@ -944,22 +954,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
           sA[ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
-        const frag vt = nb < 4 ? tl.VtF[nb][0][l] : tl.DF[0][g];
+        frag vt[NKH];
+#pragma unroll
+        for (int sidx = 0; sidx < NKH; ++sidx) vt[sidx] = nb < 4 ? tl.VtF[nb][sidx][l] : tl.DF[sidx][g];
 #pragma unroll
         for (int tb = 0; tb < NTB; ++tb) {
           f32x4 on = P::mma(sA[0], qB[tb][0], zero4);
 #pragma unroll
           for (int ks = 1; ks < KS; ++ks) on = P::mma(sA[ks], qB[tb][ks], on);
-          on = P::mma(vt, pb[tb], on);
+#pragma unroll
+          for (int sidx = 0; sidx < NKH; ++sidx)
+            if (2 * sidx <= tb) on = P::mma(vt[sidx], pb[sidx][tb], on);
           if (nb < 4) {
-            const int u = 2 * (nb >> 1) + tb;
+            const int u = tb + NTB * (nb / NVB);
             if (u == wu)
-              own[nb & 1] = on;
+              own[nb % NVB] = on;
             else
-              sm.num[buf][w][(u - w - 1) & 3][nb & 1][l] = on;
+              sm.num[buf][w][(u - w - 1) & 3][nb % NVB][l] = on;
           } else {
 #pragma unroll
-            for (int u = tb; u < 4; u += 2) {
+            for (int u = tb; u < 4; u += NTB) {
               if (u == wu)
                 own[4] = on;
               else if (g == 0)
@@ -968,7 +982,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
           }
         }
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) accS[mb][nb] = P::mma(kA[mb][0], vt, accS[mb][nb]);
+        for (int sidx = 0; sidx < NKH; ++sidx)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) accS[mb][nb] = P::mma(kA[mb][sidx], vt[sidx], accS[mb][nb]);
       }
       own_epsq = my_epsq;
       if constexpr (kLate) {
@@ -984,16 +1000,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
       // holds rows pi(nb, 4 g + j), column = token 16 tb + c16; first Q-hat S with
       // the state before the chunk
       f32x4 o[5][NTB];
-  #pragma unroll
+#pragma unroll
       for (int nb = 0; nb < 5; ++nb) {
         frag sA[KS];   // lane row = value column, k = m
-  #pragma unroll
+#pragma unroll
         for (int ks = 0; ks < KS; ++ks)
           sA[ks] = P::pack(accS[2 * ks][nb], (2 * ks + 1 < MB) ? accS[2 * ks + 1][nb] : zero4);
-  #pragma unroll
+#pragma unroll
         for (int tb = 0; tb < NTB; ++tb) {
           o[nb][tb] = P::mma(sA[0], qB[tb][0], zero4);
-  #pragma unroll
+#pragma unroll
           for (int ks = 1; ks < KS; ++ks) o[nb][tb] = P::mma(sA[ks], qB[tb][ks], o[nb][tb]);
         }
       }
@@ -1003,19 +1019,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
       // intra-chunk part of that half: P^T[t'][t] = K-hat_t' . Q-hat_t over the
       // slice for key blocks tb' <= tb (keys after the query zeroed) and C~^T P^T
       // into o
-  #pragma unroll
+#pragma unroll
       for (int sidx = 0; sidx < NKH; ++sidx) {
         // C~ of the half: B operand of the state update and A operand of the
         // intra-chunk product (lane = value column, k = token in chained order)
         frag vt[4];
-  #pragma unroll
+#pragma unroll
         for (int nb = 0; nb < 4; ++nb) vt[nb] = tl.VtF[nb][sidx][l];
         const frag df = tl.DF[sidx][g];
         frag kT[2][KS];   // A operand: lane row = token 32 sidx + 16 tbl + c16, k = 32 features
-  #pragma unroll
+#pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           f32x4 ct[2][2];
-  #pragma unroll
+#pragma unroll
           for (int hm = 0; hm < 2; ++hm) {
             const int mb = 2 * ks + hm;
             if (mb >= MB) {
@@ -1024,20 +1040,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
               continue;
             }
             const frag a = kA[mb][sidx];
-  #pragma unroll
+#pragma unroll
             for (int nb = 0; nb < 4; ++nb) accS[mb][nb] = P::mma(a, vt[nb], accS[mb][nb]);
             accS[mb][4] = P::mma(a, df, accS[mb][4]);
-  #pragma unroll
+#pragma unroll
             for (int tbl = 0; tbl < 2; ++tbl)
               ct[tbl][hm] = P::mma(a, chained_select_frag<bf16>(tbl), zero4);
           }
-  #pragma unroll
+#pragma unroll
           for (int tbl = 0; tbl < 2; ++tbl) kT[tbl][ks] = P::pack(ct[tbl][0], ct[tbl][1]);
         }
-  #pragma unroll
+#pragma unroll
         for (int tb = 2 * sidx; tb < NTB; ++tb) {
           f32x4 pt[2];
-  #pragma unroll
+#pragma unroll
           for (int tbl = 0; tbl < 2; ++tbl) {
             const int tp = 2 * sidx + tbl;
             if (tp > tb) {
@@ -1045,15 +1061,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
               continue;
             }
             pt[tbl] = P::mma(kT[tbl][0], qB[tb][0], zero4);
-  #pragma unroll
+#pragma unroll
             for (int ks = 1; ks < KS; ++ks) pt[tbl] = P::mma(kT[tbl][ks], qB[tb][ks], pt[tbl]);
             if (tp == tb) {
-  #pragma unroll
+#pragma unroll
               for (int j = 0; j < 4; ++j) pt[tbl][j] = (4 * g + j <= c16) ? pt[tbl][j] : 0.f;
             }
           }
           const frag pb = P::pack(pt[0], pt[1]);
-  #pragma unroll
+#pragma unroll
           for (int nb = 0; nb < 4; ++nb) o[nb][tb] = P::mma(vt[nb], pb, o[nb][tb]);
           o[4][tb] = P::mma(df, pb, o[4][tb]);
         }
@@ -1062,21 +1078,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(T == 32 ? 2
       // hand the partials of the other waves' units over; keep this wave's own
       // (unit u: token block u % NTB, value blocks NVB (u / NTB) ..)
       if constexpr (T == 64) {
-  #pragma unroll
+#pragma unroll
         for (int nb = 0; nb < 5; ++nb)
           own[nb] = (w == 0) ? o[nb][0] : (w == 1) ? o[nb][1] : (w == 2) ? o[nb][2] : o[nb][3];
       } else {
-  #pragma unroll
+#pragma unroll
         for (int k = 0; k < NVB; ++k)
           own[k] = (w == 0) ? o[k][0] : (w == 1) ? o[k][1] : (w == 2) ? o[NVB + k][0] : o[NVB + k][1];
         own[4] = (w & 1) ? o[4][1] : o[4][0];
       }
       own_epsq = my_epsq;
-  #pragma unroll
+#pragma unroll
       for (int u = 0; u < 4; ++u) {
         if (u != w) {
           const int slot = (u - w - 1) & 3;
-  #pragma unroll
+#pragma unroll
           for (int k = 0; k < NVB; ++k) sm.num[buf][w][slot][k][l] = o[NVB * (u / NTB) + k][u % NTB];
           if (g == 0) sm.den[buf][w][slot][c16] = o[4][u % NTB][0];
         }
