@@ -334,8 +334,14 @@ def bench_feature_map(w, Qd, Wd, bd, args, torch, fv):
     st = torch.cuda.current_stream()
     Xp = torch.empty((w.B, w.H, w.L, w.M), dtype=Qd.dtype, device=Qd.device)
     step = lambda i: fv.feature_map(Qd, Wd, bd, w.input_scale, out=Xp, stream=st)
-    for i in range(max(args.warmup, 20)):
-        step(i)
+    # warm up like the other entries: at least the warmup steps and the minimum time
+    t0 = time.perf_counter()
+    n = 0
+    while n < max(args.warmup, 20) or time.perf_counter() - t0 < args.min_warmup_seconds:
+        step(n)
+        n += 1
+        if n % 64 == 0:
+            torch.cuda.synchronize()
     ms = time_steps(torch, fv, st, step, 0, args.steps)
     ms_i, kernels = time_steps(torch, fv, st, step, 0, args.steps, instrumented=True)
     th = w.B * w.H * w.L
