@@ -455,7 +455,8 @@ __device__ __forceinline__ int opaque_uniform(int x) {
 // Raw buffer access (T = 32 scan): the base is a scalar resource covering the
 // bytes a call may touch, the lane offset one 32-bit register, so the loop
 // holds no per-lane 64-bit address (with generic pointers the compiler hoists
-// base + lane offset out of the loop as a 64-bit pair per address).
+// base + lane offset out of the loop as a 64-bit pair per address). Word 3 of
+// the resource is the 32-bit data format of raw buffer access on this family.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
