@@ -247,6 +247,11 @@ def measured_peaks(torch, fv):
     return out
 
 
+def default_chunk(w):
+    """The chunk length the library picks for chunk = 0 (favor_desc.chunk)."""
+    return 32 if w.dtype == "bf16" and w.M <= 128 else 64
+
+
 def bench_workload(name, args, torch, fv, segment_rows=(0,), chunks=(0,)):
     """One workload of the configuration list at its full size: the step is its
     attention call(s) over inputs resident in HBM, with the random-feature draw
@@ -318,7 +323,7 @@ def bench_workload(name, args, torch, fv, segment_rows=(0,), chunks=(0,)):
             for r in segment_rows}
     if len(chunks) > 1:
         entry["causal_chunk_tokens_sweep"] = {
-            str(c or 64): brief(sweep[(segment_rows[0], c)]) for c in chunks}
+            str(c or default_chunk(w)): brief(sweep[(segment_rows[0], c)]) for c in chunks}
     if not w.redraw:
         draw = lambda i: fv.orf_draw(1000 + i, H, M, w.d, W=Wd, b=bd, stream=st)
         for i in range(args.warmup):
@@ -456,10 +461,12 @@ def main():
     ap.add_argument("--workload", default="protein_b4h8", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--segment", type=int, default=0,
                     help="rows per segment of the causal scan (a multiple of 64; 0 = the "
-                         "library's choice, one workgroup per CU) for the forward steps")
+                         "library's choice, one workgroup per CU with 64-token chunks, two "
+                         "with 32) for the forward steps")
     ap.add_argument("--chunk", type=int, default=0, choices=(0, 32, 64),
                     help="tokens per step of the causal scan for the forward steps (0 = the "
-                         "library's choice, 64); the causal workloads also time the other")
+                         "library's choice: 32 for bf16 inputs with M <= 128, else 64); the "
+                         "causal workloads also time the other")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the ReLU, unnormalised and backward variants (profiler runs "
@@ -791,7 +798,8 @@ def main():
         for name in names:
             causal = wl.WORKLOADS[name].direction != "bidir"
             rows = (0, 1024, 4096) if name == "causal_b8h8" else (0,)
-            chunks = (args.chunk, 32 if args.chunk != 32 else 64) if causal else (0,)
+            first = args.chunk or default_chunk(wl.WORKLOADS[name])
+            chunks = (args.chunk, 64 if first == 32 else 32) if causal else (0,)
             others[name] = bench_workload(name, args, torch, fv, segment_rows=rows,
                                           chunks=chunks)
 
@@ -811,7 +819,7 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d, "M": M,
                    "direction": w.direction, "orf_draw_per_step": True,
                    "causal_segment_rows": args.segment or "library default",
-                   "causal_chunk_tokens": args.chunk or 64,
+                   "causal_chunk_tokens": args.chunk or default_chunk(w),
                    "orf_draw": "drawn in line before the attention pass, same stream",
                    "parallelism": "single GPU"},
         "kernels": kernels,
