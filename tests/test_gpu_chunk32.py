@@ -5,12 +5,13 @@ The chunk length only changes how the scan groups the tokens of a segment
 (Eq. cumsum is the same sum, taken 32 instead of 64 tokens per step), so the
 outputs meet the bounds the 64-token scan meets: 2e-2 (E_row and E_cond) for
 bf16 inputs. The final state is formed from the segment aggregates, not by the
-scan, so it is bitwise the state of the 64-token scan. Cases: every M class
-the kernels take (64, 128, 256 rows, with padding), lengths around the chunk
-and segment boundaries, both feature kinds, renormalisation off, the
-stabiliser, a carried state, fp32 outputs, saved row scales, both directions
-in one call, the no-allocation entry point, and a full-size workload on
-sampled heads.
+scan, so with equal segments it is bitwise the state of the 64-token scan.
+Cases: every M class the kernels take (64, 128, 256 rows, with padding),
+lengths around the chunk and segment boundaries, both feature kinds,
+renormalisation off, the stabiliser, a carried state, fp32 outputs, saved row
+scales, both directions in one call, the no-allocation entry point, and
+full-size workloads on sampled heads (M = 256, and M = 128 where 32-token
+chunks are the default).
 """
 import numpy as np
 import pytest
@@ -148,6 +149,26 @@ def test_chunk32_full_size_causal_b8h8():
     e = parity(to_host(out), Q, K, V, W, b, w.input_scale, True, "bf16", heads=heads)
     print(f"\ncausal_b8h8, chunk 32, heads {heads}: E_row {e[0]:.2e} E_cond {e[1]:.2e}",
           flush=True)
+
+
+def test_default_chunk_full_size_m128():
+    """B8 H8 L8192 at M = 128, where chunk = 0 scans 32-token chunks at two
+    workgroups per CU (512 segments of 1024 tokens), checked on two heads; the
+    explicit 64-token call meets the same bound."""
+    import torch
+    fv = _fv()
+    w = wl.WORKLOADS["causal_b8h8"]
+    Q, K, V = wl.make_qkv(w)
+    W, b = _features(451, w.H, 128)
+    args = tuple(to_dev(x, "bf16") for x in (Q, K, V)) + (to_dev(W), to_dev(b), w.input_scale)
+    out = fv.attn_causal(*args)
+    o64 = fv.attn_causal(*args, chunk=64)
+    torch.cuda.synchronize()
+    heads = [(1, 2), (6, 7)]
+    for name, o in (("default (32)", out), ("64", o64)):
+        e = parity(to_host(o), Q, K, V, W, b, w.input_scale, True, "bf16", heads=heads)
+        print(f"\nM 128, chunk {name}, heads {heads}: E_row {e[0]:.2e} E_cond {e[1]:.2e}",
+              flush=True)
 
 
 def test_chunk32_backward_recomputes_with_its_chunks():
