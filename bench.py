@@ -711,14 +711,17 @@ def main():
     # draw stays in the step. "backward": the gradient calls alone, each recomputing
     # its forward quantities. "train_step": the forward pass saving each row's
     # 1 / (D-hat + eps), then the gradient calls reading the saved outputs and scales.
+    # Both directions take one favor_attn_both_backward call, with an upstream
+    # gradient of its own for each output.
     directions = {0: "bidirectional", 1: "causal", 2: "bidirectional and causal"}[op]
     if chosen & {"backward", "train_step"}:
         rng = np.random.default_rng(7)
         dO = torch.from_numpy(rng.standard_normal(Q.shape, dtype=np.float32)).to(
             device=dev, dtype=tdt).contiguous()
+        dO2 = torch.from_numpy(rng.standard_normal(Q.shape, dtype=np.float32)).to(
+            device=dev, dtype=tdt).contiguous()   # the causal output's gradient (both)
         grads = [torch.empty_like(Qd) for _ in range(3)]
-        nbw = max(fv.backward_workspace_size(g, False) if op != 1 else 0,
-                  fv.backward_workspace_size(g, True) if op != 0 else 0)
+        nbw = fv.backward_workspace_size(g, {0: False, 1: True, 2: 2}[op])
         wsb = torch.empty(nbw, dtype=torch.uint8, device=dev)
         rs_b = torch.empty((w.B, H, w.L), dtype=torch.float32, device=dev)
         rs_c = torch.empty_like(rs_b)
@@ -730,6 +733,14 @@ def main():
             # scales and workspace (Buf1, segment prefixes, W'') are read back
             gq, gk, gv = grads
             fwd = dict(forward_workspace=ws, forward_call=fwd_call) if saved else {}
+            if op == 2:
+                # one call for both directions: a single dK, dV pass over the
+                # bidirectional dBuf1 plus the causal suffix states
+                sv = dict(out_bidir=out_b, row_scale_bidir=rs_b, out_causal=out_c,
+                          row_scale_causal=rs_c) if saved else {}
+                fv.attn_both_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dO2, dQ=gq, dK=gk,
+                                      dV=gv, workspace=wsb, stream=s_main, **sv, **fwd)
+                return
             if op != 1:
                 fv.attn_bidir_backward(Qd, Kd, Vd, Wd[0], bd[0], s, dO, dQ=gq, dK=gk, dV=gv,
                                        workspace=wsb, stream=s_main,

@@ -267,7 +267,8 @@ FAVOR_API size_t favor_noalloc_scratch_bytes(void);
  * gradient kernels take 128 (bidirectional) or 64 (causal) features at a time
  * and add the slices' parts into dQ, dK, dV in a fixed order. Deterministic
  * (no atomics). dQ, dK, dV are written in full (ragged tails included).
- * Workspace: favor_backward_workspace_size(g, causal) bytes, 256-byte aligned.
+ * Workspace: favor_backward_workspace_size(g, causal) bytes, 256-byte aligned
+ * (causal: 0 bidirectional, 1 causal, 2 both directions in one call).
  * out and row_scale (both nullable, both or neither): the forward call's output
  * and row_scale for the same inputs, features and descriptor; given, the backward
  * skips recomputing them (their recomputation otherwise runs inside the call).
@@ -313,9 +314,40 @@ FAVOR_API favor_status favor_attn_causal_backward(const favor_desc *g, const voi
                                                   void *dV, float *dstate_in, void *ws,
                                                   size_t ws_bytes, hipStream_t stream);
 
+/*
+ * favor_attn_both_backward - gradients of favor_attn_both: of a loss that depends
+ * on both outputs, given dout_bidir and dout_causal (Algorithm 1 and Eq. cumsum
+ * in reverse, as the two calls above). dQ, dK, dV receive the sums of the two
+ * directions' gradients. The key side is one pass: the bidirectional dBuf1 is
+ * the aggregate every key of the sequence sees, so it is added to each key's
+ * causal suffix R_j before dK'_j = R_j C_j and dV_j = (R_j^T K'_j)[:d]; dQ of the
+ * causal direction is added onto the bidirectional one (bf16: one more
+ * rounding). out_bidir with row_scale_bidir, and out_causal with
+ * row_scale_causal: each pair nullable, both or neither, as the forward call
+ * saved them. fwd_ws, fwd_op: a favor_attn_both call's workspace and 3, or NULL
+ * and 0. state_in, dstate_out, dstate_in as for favor_attn_causal_backward
+ * (dstate_in receives the causal direction's state gradient only; the
+ * bidirectional output does not depend on state_in). Workspace:
+ * favor_backward_workspace_size(g, 2) bytes, 256-byte aligned. Other
+ * conditions and errors as for the two calls above.
+ */
+FAVOR_API favor_status favor_attn_both_backward(const favor_desc *g, const void *Q,
+                                                const void *K, const void *V, const float *W,
+                                                const float *b, const float *state_in,
+                                                const void *dout_bidir, const void *dout_causal,
+                                                const void *out_bidir,
+                                                const float *row_scale_bidir,
+                                                const void *out_causal,
+                                                const float *row_scale_causal,
+                                                const void *fwd_ws, int32_t fwd_op,
+                                                const float *dstate_out, void *dQ, void *dK,
+                                                void *dV, float *dstate_in, void *ws,
+                                                size_t ws_bytes, hipStream_t stream);
+
 /* Host-only validation of a descriptor for an operation (0 feature map,
  * 1 bidirectional, 2 causal, 3 both, 4 bidirectional backward, 5 causal
- * backward); launches nothing and touches no device. */
+ * backward, 6 backward of both directions); launches nothing and touches no
+ * device. */
 FAVOR_API favor_status favor_validate_desc(const favor_desc *g, int op);
 
 FAVOR_API const char *favor_status_string(favor_status s);
@@ -357,7 +389,7 @@ FAVOR_API double favor_probe_work(int32_t kind, int32_t iters);
 /* ABI version of this header; bumped on any incompatible change. */
 FAVOR_API int32_t favor_abi_version(void);
 
-#define FAVOR_ABI_VERSION 6
+#define FAVOR_ABI_VERSION 7
 
 #ifdef __cplusplus
 }

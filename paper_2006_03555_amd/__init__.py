@@ -22,14 +22,15 @@ import os
 
 from ._lib import (  # noqa: F401
     BF16, F32, RF_IID, RF_ORTHO_CHI, RF_ORTHO_FIXED, RF_HADAMARD, RF_GIVENS, OP_BIDIR, OP_BOTH, OP_CAUSAL, OP_FEATURE_MAP,
-    OP_BIDIR_BACKWARD, OP_CAUSAL_BACKWARD, KERNEL_RELU, KERNEL_SOFTMAX, backward_workspace_size,
+    OP_BIDIR_BACKWARD, OP_CAUSAL_BACKWARD, OP_BOTH_BACKWARD, KERNEL_RELU, KERNEL_SOFTMAX, backward_workspace_size,
     FavorDesc, FavorError, FavorLibraryMissing, lib, lib_path, make_desc, status_string,
     validate_desc, workspace_size, last_error, timing_enable, timing_reset, timing_read,
 )
 
 __all__ = [
     "orf_draw", "feature_map", "attn_bidir", "attn_causal", "attn_both", "workspace_size",
-    "attn_bidir_backward", "attn_causal_backward", "backward_workspace_size", "make_desc",
+    "attn_bidir_backward", "attn_causal_backward", "attn_both_backward",
+    "backward_workspace_size", "make_desc",
     "attn_both_noalloc", "noalloc_scratch_bytes",
     "validate_desc", "FavorError", "FavorLibraryMissing", "lib", "lib_path",
 ]
@@ -432,6 +433,47 @@ def attn_causal_backward(Q, K, V, W, b, input_scale, dout, denom_eps=0.0, state_
         ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b), _ptr(state_in), _ptr(dout),
         _ptr(out), _ptr(row_scale), fptr, fop, _ptr(dstate_out), _ptr(dQ), _ptr(dK), _ptr(dV),
         _ptr(dstate_in), _ptr(ws), ctypes.c_size_t(nbytes), _stream(stream)))
+    return (dQ, dK, dV, dstate_in) if return_state_grad else (dQ, dK, dV)
+
+
+def attn_both_backward(Q, K, V, W, b, input_scale, dout_bidir, dout_causal, denom_eps=0.0,
+                       state_in=None, dstate_out=None, return_state_grad=False, dQ=None,
+                       dK=None, dV=None, dstate_in=None, workspace=None, stream=None,
+                       kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3,
+                       out_bidir=None, row_scale_bidir=None, out_causal=None,
+                       row_scale_causal=None, forward_workspace=None, forward_call=None,
+                       chunk=0, segment=0):
+    """Gradients of attn_both (favor_attn_both_backward): of a loss of both outputs,
+    given dout_bidir and dout_causal. Returns (dQ, dK, dV), the sums over the two
+    directions, plus the causal state gradient dstate_in when return_state_grad is
+    true. out_* and row_scale_* as the forward call saved them (each pair or
+    neither); forward_workspace of an attn_both call (forward_call "both", same
+    descriptor, inputs and state_in) spares recomputing Buf1 and the segment
+    prefixes."""
+    torch = _torch()
+    g = _desc_for(Q, W, input_scale, Q.dtype, denom_eps, segment,
+                  others=(("K", K), ("V", V), ("dout_bidir", dout_bidir),
+                          ("dout_causal", dout_causal)),
+                  opts=dict(_opts(kernel, renormalize, kernel_eps), chunk=chunk))
+    _require_features(W, b, g.H, g.M, g.d)
+    dQ, dK, dV = _bwd_grads(Q, dQ, dK, dV)
+    sshape = (g.B, g.H, g.M, g.d + 1)
+    if return_state_grad and dstate_in is None:
+        dstate_in = torch.empty(sshape, dtype=torch.float32, device=Q.device)
+    for name, t in (("state_in", state_in), ("dstate_out", dstate_out), ("dstate_in", dstate_in)):
+        _require_like(t, sshape, torch.float32, name)
+    _saved(out_bidir, row_scale_bidir, g, Q)
+    _saved(out_causal, row_scale_causal, g, Q)
+    _require_cuda(Q, K, V, W, b, dout_bidir, dout_causal, dQ, dK, dV, state_in, dstate_out,
+                  dstate_in, out_bidir, row_scale_bidir, out_causal, row_scale_causal)
+    fptr, fop = _forward_ws(forward_workspace, forward_call, ("both",))
+    ws, nbytes = _bwd_workspace(g, 2, workspace)
+    _check(lib().favor_attn_both_backward(
+        ctypes.byref(g), _ptr(Q), _ptr(K), _ptr(V), _ptr(W), _ptr(b), _ptr(state_in),
+        _ptr(dout_bidir), _ptr(dout_causal), _ptr(out_bidir), _ptr(row_scale_bidir),
+        _ptr(out_causal), _ptr(row_scale_causal), fptr, fop, _ptr(dstate_out), _ptr(dQ),
+        _ptr(dK), _ptr(dV), _ptr(dstate_in), _ptr(ws), ctypes.c_size_t(nbytes),
+        _stream(stream)))
     return (dQ, dK, dV, dstate_in) if return_state_grad else (dQ, dK, dV)
 
 

@@ -15,6 +15,7 @@ OP_CAUSAL = 2
 OP_BOTH = 3
 OP_BIDIR_BACKWARD = 4
 OP_CAUSAL_BACKWARD = 5
+OP_BOTH_BACKWARD = 6
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
@@ -82,6 +83,9 @@ def lib():
         "favor_attn_causal_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                       vp, vp, i32, vp, vp, vp, vp, vp, vp, sz,
                                                       vp]),
+        "favor_attn_both_backward": (ctypes.c_int, [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                    vp, vp, vp, vp, i32, vp, vp, vp, vp, vp,
+                                                    vp, sz, vp]),
         "favor_validate_desc": (ctypes.c_int, [dp, ctypes.c_int]),
         "favor_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "favor_last_error": (ctypes.c_char_p, []),
@@ -113,7 +117,7 @@ def last_error():
 
 KERNEL_SOFTMAX = 0
 KERNEL_RELU = 1
-ABI_VERSION = 6   # backward calls read the forward call's workspace
+ABI_VERSION = 7   # the backward of both directions in one call
 
 
 def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, segment=0,
@@ -129,7 +133,9 @@ def validate_desc(g, op):
 
 
 def backward_workspace_size(g, causal):
-    return lib().favor_backward_workspace_size(ctypes.byref(g), 1 if causal else 0)
+    """causal: False/0 bidirectional, True/1 causal, 2 both directions in one call."""
+    return lib().favor_backward_workspace_size(ctypes.byref(g),
+                                               2 if causal == 2 else (1 if causal else 0))
 
 
 def workspace_size(g, causal):

@@ -69,16 +69,21 @@ __global__ __launch_bounds__(256) void k_sum_splits(const f32x4 *__restrict__ pa
 // part [BH][nch][n4]: chunk c becomes dsout + sum_{c' > c} part[c']; the total
 // (dsout + every chunk) goes to dsin. Either pointer may be null. dsout and dsin
 // hold the M_r rows drawn (n4u = M_r 65 / 4 units per head; the rows past them
-// are padding, zero in part).
+// are padding, zero in part). bias (nullable, [BH][n4] like part): added to
+// every chunk's suffix but not to dsin: the bidirectional aggregate dBuf1 that
+// every key of the sequence sees, when both directions are differentiated in
+// one pass.
 __global__ __launch_bounds__(256) void k_suffix_scan(f32x4 *__restrict__ part, int nch, int n4,
                                                      int n4u, const f32x4 *__restrict__ dsout,
-                                                     f32x4 *__restrict__ dsin) {
+                                                     f32x4 *__restrict__ dsin,
+                                                     const f32x4 *__restrict__ bias) {
   const int bh = blockIdx.y;
   const int u = blockIdx.x * 256 + threadIdx.x;
   if (u >= n4) return;
   const bool drawn = u < n4u;
   f32x4 *p = part + (size_t)bh * nch * n4 + u;
   f32x4 run = dsout && drawn ? dsout[(size_t)bh * n4u + u] : f32x4{0.f, 0.f, 0.f, 0.f};
+  const f32x4 bv = bias ? bias[(size_t)bh * n4 + u] : f32x4{0.f, 0.f, 0.f, 0.f};
   int c = nch - 1;
   for (; c >= 7; c -= 8) {   // eight loads in flight
     f32x4 v[8];
@@ -86,13 +91,13 @@ __global__ __launch_bounds__(256) void k_suffix_scan(f32x4 *__restrict__ part, i
     for (int k = 0; k < 8; ++k) v[k] = p[(size_t)(c - k) * n4];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      p[(size_t)(c - k) * n4] = run;
+      p[(size_t)(c - k) * n4] = run + bv;
       run += v[k];
     }
   }
   for (; c >= 0; --c) {
     const f32x4 v = p[(size_t)c * n4];
-    p[(size_t)c * n4] = run;
+    p[(size_t)c * n4] = run + bv;
     run += v;
   }
   if (dsin && drawn) dsin[(size_t)bh * n4u + u] = run;
@@ -281,13 +286,19 @@ __device__ __forceinline__ void query_grad(
 // dQ row store: dQ = WT G + alpha s^2 (g~ . q-hat) q (cos features).
 // Store 8 consecutive values, or (ACC) add them to what dst holds: the fp32
 // gradients of a feature slice after the first (a gradient is a sum over
-// features, see the launchers).
+// features, see the launchers), or the gradient of one direction onto the
+// other's when both are differentiated in one call (bf16 too: one more
+// rounding of the sum).
 template <bool ACC, typename T>
 __device__ __forceinline__ void put8(T *p, f32x4 a, f32x4 b) {
   if constexpr (ACC) {
-    static_assert(sizeof(T) == 4, "slices accumulate fp32 gradients");
-    a += *reinterpret_cast<const f32x4 *>(p);
-    b += *reinterpret_cast<const f32x4 *>(p + 4);
+    float v[8];
+    load8_f32(p, v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a[i] += v[i];
+      b[i] += v[4 + i];
+    }
   }
   store8(p, a, b);
 }
@@ -1125,11 +1136,11 @@ hipError_t launch_sum_splits(const Shape &sh, const float *part, int ns, float *
 }
 
 hipError_t launch_suffix_scan(const Shape &sh, float *part, int nch, const float *dsout,
-                              float *dsin, hipStream_t st) {
+                              float *dsin, hipStream_t st, const float *bias) {
   const int n4 = sh.M * 65 / 4;
   dim3 grid((n4 + 255) / 256, sh.BH);
   hipLaunchKernelGGL(k_suffix_scan, grid, dim3(256), 0, st, (f32x4 *)part, nch, n4,
-                     sh.Mr * 65 / 4, (const f32x4 *)dsout, (f32x4 *)dsin);
+                     sh.Mr * 65 / 4, (const f32x4 *)dsout, (f32x4 *)dsin, (const f32x4 *)bias);
   return hipGetLastError();
 }
 
@@ -1168,13 +1179,27 @@ static hipError_t with_acc(bool first, F &&f) {
   return f(std::false_type{});
 }
 
+// accumulate (causal only): every slice adds onto what dQ holds (the other
+// direction's gradient, when both are differentiated in one call).
 template <typename T>
-static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, hipStream_t st) {
+static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, hipStream_t st,
+                               bool accumulate) {
   const float wts = wt_scale(sh);
   return bwd_variant(sh, [&](auto kn, auto rn) -> hipError_t {
     constexpr int KN = decltype(kn)::value;
     constexpr bool RN = decltype(rn)::value;
     return over_slices<T>(sh, causal, [&](int ms, int m0, bool first) -> hipError_t {
+      if (causal && accumulate) {
+        dim3 grid(a.nseg * sh.BH);
+        FAVOR_BWD_DISPATCH_M(bwd_max_m<T>(true), ms,
+            hipLaunchKernelGGL((k_bwd_dq_scan<T, MM, KN, RN, true>), grid, dim3(kScanThreads),
+                               0, st, (const T *)a.Q, (const T *)a.K, (const T *)a.V,
+                               (const T *)a.dout, (const T *)a.out, a.rsave,
+                               (const typename Mma<T>::frag *)a.wfr, a.bq, a.W, a.state,
+                               (T *)a.dQ, a.aux, sh.H, sh.L, a.seg_len, a.nseg, sh.s, sh.Mr,
+                               feature_norm(sh), sh.M, m0, wts));
+        return hipGetLastError();
+      }
       return with_acc<T>(first, [&](auto acc) -> hipError_t {
         constexpr bool ACC = decltype(acc)::value;
         if (causal) {
@@ -1205,9 +1230,10 @@ static hipError_t bwd_dq_typed(const Shape &sh, bool causal, const BwdArgs &a, h
   });
 }
 
-hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st) {
-  if (in == Dt::BF16) return bwd_dq_typed<bf16>(sh, causal, a, st);
-  return bwd_dq_typed<float>(sh, causal, a, st);
+hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st,
+                         bool accumulate) {
+  if (in == Dt::BF16) return bwd_dq_typed<bf16>(sh, causal, a, st, accumulate);
+  return bwd_dq_typed<float>(sh, causal, a, st, accumulate);
 }
 
 template <typename T>

@@ -78,12 +78,13 @@ enum Op {
   kOpCausal = 2,
   kOpBoth = 3,
   kOpBidirBackward = 4,
-  kOpCausalBackward = 5
+  kOpCausalBackward = 5,
+  kOpBothBackward = 6
 };
 
 favor_status validate(const favor_desc *g, int op) {
   if (!g) return fail(FAVOR_ERR_INVALID_ARGUMENT, "descriptor is NULL");
-  if (op < kOpFeatureMap || op > kOpCausalBackward)
+  if (op < kOpFeatureMap || op > kOpBothBackward)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "unknown operation %d", op);
   if (g->B < 0 || g->H < 0 || g->L < 0)
     return fail(FAVOR_ERR_INVALID_ARGUMENT, "negative size B=%d H=%d L=%d", g->B, g->H, g->L);
@@ -112,7 +113,7 @@ favor_status validate(const favor_desc *g, int op) {
   if (g->chunk != 0 && g->chunk != kChunk && g->chunk != kChunkSmall)
     return fail(FAVOR_ERR_UNSUPPORTED, "chunk=%d not supported (T = 64 or 32)", g->chunk);
   if (g->chunk == kChunkSmall && in_dt != FAVOR_BF16 &&
-      (op == kOpCausal || op == kOpBoth || op == kOpCausalBackward))
+      (op == kOpCausal || op == kOpBoth || op == kOpCausalBackward || op == kOpBothBackward))
     return fail(FAVOR_ERR_UNSUPPORTED, "chunk=32 needs bf16 inputs (the fp32 scan takes T = 64)");
   if (g->segment > kMaxL)
     return fail(FAVOR_ERR_UNSUPPORTED, "segment=%d exceeds 2^30", g->segment);
@@ -122,7 +123,7 @@ favor_status validate(const favor_desc *g, int op) {
                 g->M);
   const long long bh = (long long)g->B * g->H;
   if (bh > 65535) return fail(FAVOR_ERR_UNSUPPORTED, "B*H=%lld exceeds 65535", bh);
-  if (op == kOpBidirBackward || op == kOpCausalBackward) {
+  if (op == kOpBidirBackward || op == kOpCausalBackward || op == kOpBothBackward) {
     if (g->out_dtype != g->in_dtype)
       return fail(FAVOR_ERR_UNSUPPORTED, "the backward pass needs out_dtype == in_dtype");
   }
@@ -327,8 +328,9 @@ favor_status favor_validate_desc(const favor_desc *g, int op) {
 }
 
 size_t favor_backward_workspace_size(const favor_desc *g, int causal) {
-  const int op = causal ? kOpCausalBackward : kOpBidirBackward;
+  const int op = causal == 2 ? kOpBothBackward : (causal ? kOpCausalBackward : kOpBidirBackward);
   if (validate(g, op) != FAVOR_OK) return 0;
+  if (op == kOpBothBackward) return make_bwd_plan(g, false).total + make_bwd_plan(g, true).total;
   return make_bwd_plan(g, causal != 0).total;
 }
 
@@ -843,6 +845,136 @@ favor_status favor_attn_causal_backward(const favor_desc *g, const void *Q, cons
     e = favor::launch_bwd_dkv(sh, in, true, a, st);
   }
   return device_result(e, "favor_attn_causal_backward key and value gradients");
+}
+
+favor_status favor_attn_both_backward(const favor_desc *g, const void *Q, const void *K,
+                                      const void *V, const float *W, const float *b,
+                                      const float *state_in, const void *dout_bidir,
+                                      const void *dout_causal, const void *out_bidir,
+                                      const float *row_scale_bidir, const void *out_causal,
+                                      const float *row_scale_causal, const void *fwd_ws,
+                                      int32_t fwd_op, const float *dstate_out, void *dQ,
+                                      void *dK, void *dV, float *dstate_in, void *ws,
+                                      size_t ws_bytes, hipStream_t stream) {
+  FAVOR_TRY(validate(g, kOpBothBackward));
+  bool saved_b = false, saved_c = false;
+  FAVOR_TRY(check_saved(g, out_bidir, row_scale_bidir, saved_b));
+  FAVOR_TRY(check_saved(g, out_causal, row_scale_causal, saved_c));
+  FAVOR_TRY(check_forward_ws(fwd_ws, fwd_op, kOpBoth, kOpBoth));
+  const BwdPlan pb = make_bwd_plan(g, false), pc = make_bwd_plan(g, true);
+  const bool work = pb.total > 0;
+  const bool heads = (long long)g->B * g->H > 0;
+  const void *in_ptrs[] = {Q, K, V, W, b, dout_bidir, dout_causal, dQ, dK, dV};
+  const char *names[] = {"Q", "K", "V", "W", "b", "dout_bidir", "dout_causal", "dQ", "dK", "dV"};
+  for (int i = 0; i < 10; ++i) FAVOR_TRY(check_ptr(in_ptrs[i], names[i], work));
+  const void *st_ptrs[] = {state_in, dstate_out, dstate_in};
+  const char *st_names[] = {"state_in", "dstate_out", "dstate_in"};
+  for (int i = 0; i < 3; ++i)
+    if (st_ptrs[i] && !aligned(st_ptrs[i], 16))
+      return fail(FAVOR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", st_names[i]);
+  const favor::Shape sh = shape_of(g);
+  hipStream_t st = stream;
+  hipError_t e;
+  if (!work) {
+    // no tokens: the state gradient passes through unchanged
+    if (heads && dstate_in) {
+      {
+        favor::LaunchTimer t(favor::kKerSuffixScan, st);
+        e = favor::launch_suffix_scan(sh, nullptr, 0, dstate_out, dstate_in, st);
+      }
+      return device_result(e, "favor_attn_both_backward state gradient copy");
+    }
+    return ok();
+  }
+  FAVOR_TRY(check_workspace(ws, ws_bytes, pb.total + pc.total));
+  const favor::Dt in = dt_of(g->in_dtype);
+  const BwdBufs wb = carve(pb, ws);
+  const BwdBufs wc = carve(pc, static_cast<char *>(ws) + pb.total);
+  // the forward quantities of favor_attn_both: the segment prefixes (plus
+  // state_in), Buf1 as a plain aggregate and as Q-side fragments, W'' and b'',
+  // read from the forward call's workspace or recomputed as that call computes
+  // them; then each direction's output and row reciprocals unless saved
+  void *wfr = wc.wfr, *frags = wb.frags;
+  float *bq = wc.bq, *prefix = wc.part, *buf1 = wb.buf1;
+  if (fwd_op != 0) {
+    const FwdBufs f = carve_fwd(make_plan(g, kOpBoth), const_cast<void *>(fwd_ws));
+    wfr = f.wfr;
+    bq = f.bq;
+    prefix = f.part;
+    frags = f.frags;
+    buf1 = f.sum;
+  } else {
+    {
+      favor::LaunchTimer t(favor::kKerKside, st);
+      e = favor::launch_kside(sh, in, K, V, W, b, wfr, bq, prefix, pc.rows_per_split, pc.nsplit,
+                              st);
+    }
+    if (e != hipSuccess) return device_result(e, "favor_attn_both_backward segment aggregates");
+    {
+      favor::LaunchTimer t(favor::kKerSegScan, st);
+      e = favor::launch_seg_scan(sh, in, prefix, pc.nsplit, state_in, nullptr, frags, st, buf1);
+    }
+    if (e != hipSuccess) return device_result(e, "favor_attn_both_backward segment prefixes");
+  }
+  if (sh.renorm && !saved_b) {
+    favor::LaunchTimer t(favor::kKerQside, st);
+    e = favor::launch_qside_save(sh, in, Q, wfr, bq, frags, wb.out, wb.rsave, st);
+    if (e != hipSuccess) return device_result(e, "favor_attn_both_backward bidirectional pass");
+  }
+  if (sh.renorm && !saved_c) {
+    favor::LaunchTimer t(favor::kKerCausal, st);
+    e = favor::launch_causal_save(sh, in, Q, K, V, wfr, bq, prefix, wc.out, wc.rsave,
+                                  pc.rows_per_split, pc.nsplit, wc.halves, st);
+    if (e != hipSuccess) return device_result(e, "favor_attn_both_backward causal pass");
+  }
+  // bidirectional: dQ of its rows, then dBuf1 = sum of q-hat (x) u~ over every row
+  favor::BwdArgs ab{Q,   K,   V,   dout_bidir, saved_b ? out_bidir : wb.out,
+                    saved_b ? row_scale_bidir : wb.rsave, wfr, bq, W, buf1, dQ, dK, dV,
+                    wb.aux, pb.rows_per_split, pb.nsplit};
+  {
+    favor::LaunchTimer t(favor::kKerBwdDq, st);
+    e = favor::launch_bwd_dq(sh, in, false, ab, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both_backward bidirectional dQ");
+  {
+    favor::LaunchTimer t(favor::kKerBwdAgg, st);
+    e = favor::launch_kside_agg(sh, in, Q, dout_bidir, W, b, wb.aux, wb.part2, pb.rows_per_split,
+                                pb.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both_backward dBuf1 partials");
+  {
+    favor::LaunchTimer t(favor::kKerSumSplits, st);
+    e = favor::launch_sum_splits(sh, wb.part2, pb.nsplit, wb.dbuf1, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both_backward dBuf1");
+  // causal: its dQ added onto the bidirectional one; the suffix aggregates with
+  // dBuf1 added (every key sees every row in the bidirectional direction), so
+  // one key pass gives dK and dV of both directions
+  favor::BwdArgs ac{Q,   K,   V,   dout_causal, saved_c ? out_causal : wc.out,
+                    saved_c ? row_scale_causal : wc.rsave, wfr, bq, W, prefix, dQ, dK, dV,
+                    wc.aux, pc.rows_per_split, pc.nsplit};
+  {
+    favor::LaunchTimer t(favor::kKerBwdDq, st);
+    e = favor::launch_bwd_dq(sh, in, true, ac, st, /*accumulate=*/true);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both_backward causal dQ");
+  {
+    favor::LaunchTimer t(favor::kKerBwdAgg, st);
+    e = favor::launch_kside_agg(sh, in, Q, dout_causal, W, b, wc.aux, wc.part2,
+                                pc.rows_per_split, pc.nsplit, st);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both_backward row aggregates");
+  {
+    favor::LaunchTimer t(favor::kKerSuffixScan, st);
+    e = favor::launch_suffix_scan(sh, wc.part2, pc.nsplit, dstate_out, dstate_in, st, wb.dbuf1);
+  }
+  if (e != hipSuccess) return device_result(e, "favor_attn_both_backward suffix states");
+  ac.state = wc.part2;
+  {
+    favor::LaunchTimer t(favor::kKerBwdDkv, st);
+    e = favor::launch_bwd_dkv(sh, in, true, ac, st);
+  }
+  return device_result(e, "favor_attn_both_backward key and value gradients");
 }
 
 }  // extern "C"

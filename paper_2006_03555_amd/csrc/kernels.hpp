@@ -112,14 +112,17 @@ struct BwdArgs {
   float2 *aux;           // [BH][L] (alpha, alpha u_d)
   int seg_len, nseg;     // causal: the segments of the forward plan
 };
-hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st);
+// accumulate (causal only): add onto dQ instead of overwriting it.
+hipError_t launch_bwd_dq(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st,
+                         bool accumulate = false);
 hipError_t launch_bwd_dkv(const Shape &sh, Dt in, bool causal, const BwdArgs &a, hipStream_t st);
 // Fixed-order sum of split partials [BH][ns][M][65] -> [BH][M][65].
 hipError_t launch_sum_splits(const Shape &sh, const float *part, int ns, float *dst,
                              hipStream_t st);
 // In-place exclusive suffix scan over chunks plus dsout; the total plus dsout to dsin.
+// bias (nullable, [BH][M][65]): added to every suffix but not to dsin.
 hipError_t launch_suffix_scan(const Shape &sh, float *part, int nch, const float *dsout,
-                              float *dsin, hipStream_t st);
+                              float *dsin, hipStream_t st, const float *bias = nullptr);
 
 // Causal chunk scan of each segment starting from its prefix state. halves:
 // [BH][L][68] fp32 scratch for fp32 inputs at M = 256 (two feature-half

@@ -178,7 +178,7 @@ int main(int argc, char **argv) {
   for (long it = 0; it < iters; ++it) {
     const favor_desc g = random_desc();
     // validation and sizes agree
-    for (int op = -1; op <= 6; ++op) (void)favor_validate_desc(&g, op);
+    for (int op = -1; op <= 7; ++op) (void)favor_validate_desc(&g, op);
     const int size_ops[] = {0, 1, 2};
     const int val_ops[] = {1, 2, 3};
     for (int k = 0; k < 3; ++k) {
@@ -187,7 +187,7 @@ int main(int argc, char **argv) {
       check(n == 0 || ok, "workspace size for an invalid descriptor", it);
       valid += ok;
     }
-    for (int c = 0; c < 2; ++c) {
+    for (int c = 0; c < 3; ++c) {
       const size_t n = favor_backward_workspace_size(&g, c);
       check(n == 0 || favor_validate_desc(&g, 4 + c) == FAVOR_OK,
             "backward workspace size for an invalid descriptor", it);
@@ -199,7 +199,8 @@ int main(int argc, char **argv) {
     const size_t nb = favor_workspace_size(&g, 0), nc = favor_workspace_size(&g, 1),
                  nboth = favor_workspace_size(&g, 2);
     const size_t nbb = favor_backward_workspace_size(&g, 0),
-                 nbc = favor_backward_workspace_size(&g, 1);
+                 nbc = favor_backward_workspace_size(&g, 1),
+                 nbboth = favor_backward_workspace_size(&g, 2);
     const favor_desc *gp = coin(97) ? &g : nullptr;
     int b0 = g_launches;
     call(it, "feature_map", b0, favor_feature_map(gp, ptr(), (float *)ptr(), (float *)ptr(),
@@ -250,6 +251,17 @@ int main(int argc, char **argv) {
                                     coin(30) ? (float *)ptr() : nullptr, ptr(), ptr(), ptr(),
                                     coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nbc),
                                     nullptr));
+    b0 = g_launches;
+    const bool saved_c = coin(40);
+    call(it, "attn_both_backward", b0,
+         favor_attn_both_backward(gp, ptr(), ptr(), ptr(), (float *)ptr(), (float *)ptr(),
+                                  coin(30) ? (float *)ptr() : nullptr, ptr(), ptr(),
+                                  saved ? ptr() : nullptr, saved ? (float *)ptr() : nullptr,
+                                  saved_c ? ptr() : nullptr, saved_c ? (float *)ptr() : nullptr,
+                                  coin(30) ? ws_ptr() : nullptr, (int32_t)(next() % 5) - 1,
+                                  coin(30) ? (float *)ptr() : nullptr, ptr(), ptr(), ptr(),
+                                  coin(30) ? (float *)ptr() : nullptr, ws_ptr(), ws_for(nbboth),
+                                  nullptr));
     b0 = g_launches;
     const int32_t heads[] = {0, 1, 8, -1, 65535, 65536};
     const int32_t Ms[] = {64, 256, 100, 0, -1, 4096, 4097};

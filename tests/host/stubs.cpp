@@ -110,9 +110,11 @@ hipError_t launch_kside_agg(const Shape &sh, Dt, const void *Q, const void *dout
   require(Q && dout && W && b && aux && part, "weighted key pass pointers");
   return ran();
 }
-hipError_t launch_bwd_dq(const Shape &sh, Dt, bool causal, const BwdArgs &a, hipStream_t) {
+hipError_t launch_bwd_dq(const Shape &sh, Dt, bool causal, const BwdArgs &a, hipStream_t,
+                         bool accumulate) {
   shape_ok(sh);
   require(a.Q && a.dout && a.out && a.rsave && a.W && a.state && a.dQ && a.aux, "dQ pass");
+  require(causal || !accumulate, "only the causal dQ pass adds onto dQ");
   if (causal) plan_ok(sh, a.seg_len, a.nseg);
   return ran();
 }
@@ -127,9 +129,10 @@ hipError_t launch_sum_splits(const Shape &sh, const float *part, int ns, float *
   require(part && dst && ns > 0, "sum of splits");
   return ran();
 }
-hipError_t launch_suffix_scan(const Shape &sh, float *, int nch, const float *, float *dsin,
-                              hipStream_t) {
+hipError_t launch_suffix_scan(const Shape &sh, float *part, int nch, const float *, float *dsin,
+                              hipStream_t, const float *bias) {
   require(sh.BH > 0 && nch >= 0 && (nch > 0 || dsin), "suffix scan");
+  require(!bias || (part && nch > 0), "suffix bias without suffixes");
   return ran();
 }
 

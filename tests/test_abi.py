@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_strings(L):
-    assert L.favor_abi_version() == 6
+    assert L.favor_abi_version() == 7
     assert fv.status_string(0) == "FAVOR_OK"
     assert fv.status_string(3) == "FAVOR_ERR_WORKSPACE_TOO_SMALL"
 
@@ -134,9 +134,9 @@ def test_fp32_causal_takes_every_m():
     """fp32 causal at M > 128 runs as two feature-half passes, which need a
     [B*H][L][68] fp32 area of workspace more than M = 128."""
     g = _desc(in_dtype=fv.F32, out_dtype=fv.F32, M=256)
-    for op in (fv.OP_CAUSAL, fv.OP_BOTH, fv.OP_BIDIR):
+    for op in (fv.OP_CAUSAL, fv.OP_BOTH, fv.OP_BIDIR, fv.OP_BOTH_BACKWARD):
         assert fv.validate_desc(g, op) == 0
-    assert fv.validate_desc(g, 6) == 1
+    assert fv.validate_desc(g, 7) == 1
     half = -(-2 * 4 * 1000 * 68 * 4 // 256) * 256
     # bf16 at M = 256 runs in one pass; fp32 W'' fragments take 16 more bytes per lane
     plain = fv.workspace_size(_desc(M=256), 1) + 4 * (256 // 16) * 2 * 64 * 16
