@@ -78,10 +78,11 @@ def test_both_backward_parity(B, H, L, M, dtype, kernel, renorm, eps, states):
     assert np.max(np.abs(got - rS)) <= TOL[dtype] * np.max(np.abs(rS))
 
 
-@pytest.mark.parametrize("dtype,M", [("bf16", 256), ("f32", 64)])
+@pytest.mark.parametrize("dtype,M", [("bf16", 256), ("bf16", 128), ("bf16", 64), ("f32", 64)])
 def test_both_backward_reads_saved_forward_quantities(dtype, M):
     """Given the workspace of the attn_both call (W'', b'', Buf1 and the segment
-    prefixes), the gradients are bitwise those of recomputing them; given also
+    prefixes; 32-token chunks at M <= 128 in bf16, the segment plan of two
+    workgroups per CU), the gradients are bitwise those of recomputing them; given also
     its outputs and row scales, within the gate of recomputing them. The causal
     state gradient is bitwise that of attn_causal_backward."""
     import torch
