@@ -24,9 +24,11 @@ kernel. The line also carries the fp64 CPU oracle timed on this host
 (cpu_baseline), and under "variants" the same step with generalized attention
 (ReLU features) and with the renormalisation off, the draw alone for every kind
 of random features, one GPU's share of a causal pass sharded eight ways along
-the sequence (the last L/8 tokens from a carried state), the backward pass of
-the step's attention, and the training step (forward saving the row scales,
-then the backward reading them), timed the same way.
+the sequence (the last L/8 tokens from a carried state), the step captured once
+as a HIP graph and replayed (and the launch-bound B1 H1 L1024 configuration
+eager against replayed), the backward pass of the step's attention, and the
+training step (forward saving the row scales, then the backward reading them),
+timed the same way.
 
 Beside the headline, the line carries "feature_map" (favor_feature_map on the
 workload's Q: the materialised feature-map phase) and "workloads": every
@@ -472,7 +474,7 @@ def main():
                     help="skip the ReLU, unnormalised and backward variants (profiler runs "
                          "that average counters over every launch of a kernel)")
     ap.add_argument("--variants",
-                    default="relu,softmax_no_renormalize,draws,causal_shard,backward,"
+                    default="relu,softmax_no_renormalize,draws,causal_shard,graph,backward,"
                             "train_step",
                     help="comma-separated variants to time after the headline step")
     ap.add_argument("--workloads", default="bidir_b8h8,causal_b8h8,causal_long",
@@ -531,20 +533,20 @@ def main():
     ev_draw = [torch.cuda.Event(), torch.cuda.Event()]   # slot k drawn
     ev_attn = [torch.cuda.Event(), torch.cuda.Event()]   # attention done reading slot k
 
-    def attention(slot, opts=None):
+    def attention(slot, opts=None, stream=s_main):
         opts = dict(opts or {})
         if op != 0:
             opts["segment"] = args.segment
             opts["chunk"] = args.chunk
         if op == 2:     # one key pass serves both directions
             fv.attn_both(Qd, Kd, Vd, Wd[slot], bd[slot], s, out_bidir=out_b, out_causal=out_c,
-                         workspace=ws, stream=s_main, **opts)
+                         workspace=ws, stream=stream, **opts)
         elif op == 0:
             fv.attn_bidir(Qd, Kd, Vd, Wd[slot], bd[slot], s, out=out_b, workspace=ws,
-                          stream=s_main, **opts)
+                          stream=stream, **opts)
         else:
             fv.attn_causal(Qd, Kd, Vd, Wd[slot], bd[slot], s, out=out_c, workspace=ws,
-                           stream=s_main, **opts)
+                           stream=stream, **opts)
 
     def step_serial(i, opts=None):
         """Draw this step's features, then attend with them (one stream)."""
@@ -705,6 +707,61 @@ def main():
             draws[name]["ms_per_launch"] = tot / cnt if cnt else None
             draws[name]["kernel"] = ",".join(sorted(k for k, v in kd.items() if v[1] > 0))
         variants["draws"] = draws
+
+    # the step captured once as a HIP graph and replayed (the library launches only
+    # kernels, so a whole step is capturable); each replay redoes the draw, with the
+    # seed captured. The launch-bound smallest configuration (B1 H1 L1024, fp32)
+    # shows what the capture saves in host launch time.
+    if "graph" in chosen:
+        def capture(step):
+            side = torch.cuda.Stream()   # default priority
+            side.wait_stream(s_main)
+            with torch.cuda.stream(side):
+                step()
+            s_main.wait_stream(side)
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                step()
+            torch.cuda.synchronize()
+            return gr
+
+        def replays(gr):
+            for _ in range(args.warmup):
+                gr.replay()
+            return time_steps(torch, fv, s_main, lambda i: gr.replay(), 0, args.steps)
+
+        def captured_step():
+            fv.orf_draw(1000 + first, H, M, w.d, W=Wd[0], b=bd[0])
+            attention(0, stream=torch.cuda.current_stream())
+
+        gr = capture(captured_step)
+        ms_g = replays(gr)
+        del gr
+        ws_small = wl.WORKLOADS["bidir_small"]
+        q1, k1, v1 = (torch.from_numpy(x).to(dev) for x in wl.make_qkv(ws_small))
+        W1 = torch.empty((ws_small.H, ws_small.M, ws_small.d), dtype=torch.float32, device=dev)
+        b1 = torch.empty((ws_small.H, ws_small.M), dtype=torch.float32, device=dev)
+        o1 = torch.empty_like(q1)
+        g1 = fv.make_desc(ws_small.B, ws_small.H, ws_small.L, ws_small.d, ws_small.M, fv.F32,
+                          fv.F32, ws_small.input_scale)
+        wk1 = torch.empty(fv.workspace_size(g1, 0), dtype=torch.uint8, device=dev)
+
+        def small_step(i=0):
+            fv.orf_draw(77, ws_small.H, ws_small.M, ws_small.d, W=W1, b=b1)
+            fv.attn_bidir(q1, k1, v1, W1, b1, ws_small.input_scale, out=o1, workspace=wk1)
+
+        for i in range(args.warmup):
+            small_step()
+        ms_small = time_steps(torch, fv, s_main, small_step, 0, args.steps)
+        gr = capture(small_step)
+        ms_small_g = replays(gr)
+        del gr
+        variants["graph"] = {
+            "ms_per_step": ms_g, "value": w.B * w.H * w.L / (ms_g / 1e3),
+            "what": "the step (ORF draw + " + w.direction + " attention) captured once as a "
+                    "HIP graph and replayed; each replay redoes the draw with the seed captured",
+            "small": {"workload": "bidir_small (B1 H1 L1024 M128 fp32, draw + bidirectional)",
+                      "ms_per_step_eager": ms_small, "ms_per_step_graph": ms_small_g}}
 
     # the backward pass of the step's attention: gradients with respect to Q, K, V of
     # each direction the step computes, for a fixed synthetic upstream gradient; the
