@@ -86,8 +86,10 @@ def test_causal_long_full_with_gpu_draw():
 
 def test_protein_b4h8_full_backward():
     """Both backward passes at the protein workload's full size (B4 H8 L8192 M256
-    bf16), sampled heads against the oracle's gradients; the gate of
-    test_gpu_backward (per row, in units of the oracle's error scale)."""
+    bf16), and the backward of both directions in one call (the same upstream
+    gradient for each output), sampled heads against the oracle's gradients; the
+    gate of test_gpu_backward (per row, in units of the oracle's error scale;
+    for the sum of the two directions, the sum of their scales)."""
     import torch
     fv = _fv()
     from test_gpu_backward import _check_all, _host_grads, _oracle_grads
@@ -101,14 +103,21 @@ def test_protein_b4h8_full_backward():
                                                       to_dev(dout, "bf16")]
     gb = fv.attn_bidir_backward(*args)
     gc = fv.attn_causal_backward(*args)
+    gx = fv.attn_both_backward(*args, args[-1])
     torch.cuda.synchronize()
     gb = [to_host(t) for t in gb]
     gc = [to_host(t) for t in gc]
-    for t in gb + gc:
+    gx = [to_host(t) for t in gx]
+    for t in gb + gc + gx:
         assert np.all(np.isfinite(t))
     for (bi, hi) in [(0, 0), (3, 6)]:
         sl = lambda a: a[bi:bi + 1, hi:hi + 1]
         Wh, bh = Wr[hi:hi + 1], br[hi:hi + 1]
+        refs = []
         for causal, got in ((False, gb), (True, gc)):
             ref, scale, _ = _oracle_grads(sl(Q), sl(K), sl(V), Wh, bh, sl(dout), causal)
             _check_all(_host_grads([sl(g) for g in got]), ref, "bf16", scale)
+            refs.append((ref, scale))
+        (rb, sb), (rc, sc) = refs
+        _check_all(_host_grads([sl(g) for g in gx]), {n: rb[n] + rc[n] for n in rb}, "bf16",
+                   {n: sb[n] + sc[n] for n in sb})
