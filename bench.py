@@ -737,18 +737,18 @@ def main():
         gr = capture(captured_step)
         ms_g = replays(gr)
         del gr
-        ws_small = wl.WORKLOADS["bidir_small"]
-        q1, k1, v1 = (torch.from_numpy(x).to(dev) for x in wl.make_qkv(ws_small))
-        W1 = torch.empty((ws_small.H, ws_small.M, ws_small.d), dtype=torch.float32, device=dev)
-        b1 = torch.empty((ws_small.H, ws_small.M), dtype=torch.float32, device=dev)
+        w_small = wl.WORKLOADS["bidir_small"]
+        q1, k1, v1 = (torch.from_numpy(x).to(dev) for x in wl.make_qkv(w_small))
+        W1 = torch.empty((w_small.H, w_small.M, w_small.d), dtype=torch.float32, device=dev)
+        b1 = torch.empty((w_small.H, w_small.M), dtype=torch.float32, device=dev)
         o1 = torch.empty_like(q1)
-        g1 = fv.make_desc(ws_small.B, ws_small.H, ws_small.L, ws_small.d, ws_small.M, fv.F32,
-                          fv.F32, ws_small.input_scale)
+        g1 = fv.make_desc(w_small.B, w_small.H, w_small.L, w_small.d, w_small.M, fv.F32,
+                          fv.F32, w_small.input_scale)
         wk1 = torch.empty(fv.workspace_size(g1, 0), dtype=torch.uint8, device=dev)
 
         def small_step(i=0):
-            fv.orf_draw(77, ws_small.H, ws_small.M, ws_small.d, W=W1, b=b1)
-            fv.attn_bidir(q1, k1, v1, W1, b1, ws_small.input_scale, out=o1, workspace=wk1)
+            fv.orf_draw(77, w_small.H, w_small.M, w_small.d, W=W1, b=b1)
+            fv.attn_bidir(q1, k1, v1, W1, b1, w_small.input_scale, out=o1, workspace=wk1)
 
         for i in range(args.warmup):
             small_step()
