@@ -926,19 +926,39 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
   const float2 *auh = aux + (size_t)bh * L;
   __syncthreads();
 
+  // The dV pass with bf16 operands has registers to spare: the rows the next
+  // chunk in scan order reads (its keys, queries, output gradients and row
+  // weights) are loaded once this chunk has consumed its own, right after its
+  // first barrier, so that their latency hides behind this chunk's products;
+  // the key rows, read until the end of the chunk, go to a second buffer.
+  constexpr bool kAhead = !KPART && sizeof(T) == 2;
+  frag kf[2], vf[2], kfn[2], qa[4][2], dob[2], qo[2];
+  float2 ao = make_float2(0.f, 0.f);
+  auto load_ahead = [&](int tc, frag (&kdst)[2]) __attribute__((always_inline)) {
+    const int t = tc + 16 * qb + c16;
+    load_rows64<T>(kdst, Kh, t, r1);
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) load_rows64<T>(qa[tb], Qh, tc + 16 * tb + c16, r1);
+    if (hf == 0) {
+      load_rows64<T>(dob, dOh, t, r1);
+      ao = t < r1 ? auh[t] : make_float2(0.f, 0.f);
+    }
+    load_rows64<T>(qo, Qh, t, r1);
+  };
   const int nch = (r1 - r0 + 63) / 64;
+  if (kAhead && nch > 0) load_ahead(r0 + 64 * (nch - 1), kf);
   for (int c = nch - 1; c >= 0; --c) {
     const int t0 = r0 + 64 * c;
     // this row block's keys and values, loaded with the chunk's other rows
     const int j = t0 + 16 * qb + c16;
-    frag kf[2], vf[2];
-    load_rows64<T>(kf, Kh, j, r1);
-    load_rows64<T>(vf, Vh, j, r1);
-    // the chunk's queries: features (row m) of the state waves' blocks, u~^T of
-    // row block qb; (alpha, alpha u_d) of every row
-    frag qa[4][2];
+    if constexpr (!kAhead) {
+      load_rows64<T>(kf, Kh, j, r1);
+      load_rows64<T>(vf, Vh, j, r1);
+      // the chunk's queries: features (row m) of the state waves' blocks, u~^T
+      // of row block qb; (alpha, alpha u_d) of every row
 #pragma unroll
-    for (int tb = 0; tb < 4; ++tb) load_rows64<T>(qa[tb], Qh, t0 + 16 * tb + c16, r1);
+      for (int tb = 0; tb < 4; ++tb) load_rows64<T>(qa[tb], Qh, t0 + 16 * tb + c16, r1);
+    }
     if (sw) chunk_features_t<T, FB, KN>(sm.QT, sm.WA, sm.bq, qa, w * FB);
     frag da[4][2];
     float2 au[4];
@@ -949,10 +969,11 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
       au[tb] = t < r1 ? auh[t] : make_float2(0.f, 0.f);
     }
     if (hf == 0) {   // row block qb loaded again: no runtime register index
-      const int t = t0 + 16 * qb + c16;
-      frag dob[2];
-      load_rows64<T>(dob, dOh, t, r1);
-      const float2 ao = t < r1 ? auh[t] : make_float2(0.f, 0.f);
+      if constexpr (!kAhead) {
+        const int t = t0 + 16 * qb + c16;
+        load_rows64<T>(dob, dOh, t, r1);
+        ao = t < r1 ? auh[t] : make_float2(0.f, 0.f);
+      }
       float aj[4], ej[4];   // of queries 16 qb + 4 g + j
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -978,8 +999,7 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
     }
     if constexpr (!KPART) {
       // row block qb's features with lane row = query (k = m), steps [s0, s1)
-      frag qo[2];
-      load_rows64<T>(qo, Qh, t0 + 16 * qb + c16, r1);
+      if constexpr (!kAhead) load_rows64<T>(qo, Qh, t0 + 16 * qb + c16, r1);
 #pragma unroll 2
       for (int sidx = s0; sidx < s1; ++sidx) {
         f32x4 f[2];
@@ -1014,6 +1034,9 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
       }
     }
     __syncthreads();
+    if constexpr (kAhead) {
+      if (c > 0) load_ahead(t0 - 64, kfn);
+    }
 
     if (sw) {   // fold the chunk's rows into R
 #pragma unroll
@@ -1082,6 +1105,10 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
         else
           store_vgrad<T, ACC>(dV + ((size_t)bh * L + j) * kD, vacc, D);
       }
+    }
+    if constexpr (kAhead) {
+      kf[0] = kfn[0];
+      kf[1] = kfn[1];
     }
   }
 }
