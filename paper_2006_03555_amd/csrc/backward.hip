@@ -560,11 +560,30 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dq_scan(
     if constexpr (!kAhead)
       row_weights_loaded<T, KN, RN>(qf, df, of, rs, i, r1, cM, s2half, alpha, ud);
     if (sw) chunk_features_t<T, FB, KN>(sm.KT, sm.WA, sm.bq, ka, w * FB);
-    if (hf == 0) {   // C~ of key block qb (its rows loaded again: no runtime register index)
+    if (hf == 0) {   // C~ of key block qb
       const int t = t0 + 16 * qb + c16;
       frag ko[2], vo[2];
-      load_rows64<T>(ko, Kh, t, r1);
-      load_rows64<T>(vo, Vh, t, r1);
+      if constexpr (kAhead) {
+        // the chunk's rows are held (loaded a chunk ahead); qb is uniform over
+        // the wave, so taking block qb is a scalar choice, not a runtime
+        // register index
+        const int qbu = __builtin_amdgcn_readfirstlane(qb);
+        ko[0] = ka[0][0];
+        ko[1] = ka[0][1];
+        vo[0] = va[0][0];
+        vo[1] = va[0][1];
+#pragma unroll
+        for (int tb = 1; tb < 4; ++tb)
+          if (tb == qbu) {
+            ko[0] = ka[tb][0];
+            ko[1] = ka[tb][1];
+            vo[0] = va[tb][0];
+            vo[1] = va[tb][1];
+          }
+      } else {   // fp32: loaded again (a runtime register index would go to scratch)
+        load_rows64<T>(ko, Kh, t, r1);
+        load_rows64<T>(vo, Vh, t, r1);
+      }
       float Do = 1.f;
       if constexpr (KN == kCos) Do = cM * expf(s2half * sq_norm16<T>(ko));
       Do = t < r1 ? Do : 0.f;
@@ -968,8 +987,22 @@ __global__ __launch_bounds__(kScanThreads) void k_bwd_dkv_scan(
       load_rows64<T>(da[tb], dOh, t, r1);
       au[tb] = t < r1 ? auh[t] : make_float2(0.f, 0.f);
     }
-    if (hf == 0) {   // row block qb loaded again: no runtime register index
-      if constexpr (!kAhead) {
+    if (hf == 0) {   // row block qb of the output gradients and row weights
+      if constexpr (KPART) {
+        // held in da, au; qb is uniform over the wave, so taking block qb is a
+        // scalar choice, not a runtime register index
+        const int qbu = __builtin_amdgcn_readfirstlane(qb);
+        dob[0] = da[0][0];
+        dob[1] = da[0][1];
+        ao = au[0];
+#pragma unroll
+        for (int tb = 1; tb < 4; ++tb)
+          if (tb == qbu) {
+            dob[0] = da[tb][0];
+            dob[1] = da[tb][1];
+            ao = au[tb];
+          }
+      } else if constexpr (!kAhead) {   // fp32 dV pass: loaded again
         const int t = t0 + 16 * qb + c16;
         load_rows64<T>(dob, dOh, t, r1);
         ao = t < r1 ? auh[t] : make_float2(0.f, 0.f);
