@@ -192,6 +192,30 @@ __device__ __forceinline__ void load_rows64(typename Mma<T>::frag (&f)[2], const
   }
 }
 
+// Dot product of the 16 values of two fragment pairs (a lane's share of two
+// rows): dot2 on bf16 pairs (two exact products and an fp32 sum per
+// instruction, no conversions), fused multiply-adds on fp32 values.
+__device__ __forceinline__ float dot16(const bf16x8 (&a)[2], const bf16x8 (&b)[2]) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  struct Pairs { bf16x2 p[4]; };
+  float n = 0.f;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const Pairs x = __builtin_bit_cast(Pairs, a[k]);
+    const Pairs y = __builtin_bit_cast(Pairs, b[k]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) n = __builtin_amdgcn_fdot2_f32_bf16(x.p[i], y.p[i], n, false);
+  }
+  return n;
+}
+__device__ __forceinline__ float dot16(const f32x8 (&a)[2], const f32x8 (&b)[2]) {
+  float n = 0.f;
+#pragma unroll
+  for (int k = 0; k < 2; ++k)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) n = fmaf(a[k][i], b[k][i], n);
+  return n;
+}
 template <typename T>
 __device__ __forceinline__ float sq_norm16(const typename Mma<T>::frag (&f)[2]) {
   float n = sq_sum16(f);
@@ -330,11 +354,7 @@ __device__ __forceinline__ void row_weights_loaded(const typename Mma<T>::frag (
                                                    int i, int L, float cM, float s2half,
                                                    float &alpha, float &ud) {
   if constexpr (RN) {
-    float dot = 0.f;
-#pragma unroll
-    for (int k = 0; k < 2; ++k)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) dot = fmaf(to_f32(df[k][e]), to_f32(of[k][e]), dot);
+    float dot = dot16(df, of);
     dot += __shfl_xor(dot, 16);
     dot += __shfl_xor(dot, 32);
     alpha = rs;
