@@ -123,7 +123,8 @@ ABI_VERSION = 7   # the backward of both directions in one call
 def make_desc(B, H, L, d, M, in_dtype, out_dtype, input_scale, denom_eps=0.0, segment=0,
               kernel=KERNEL_SOFTMAX, renormalize=True, kernel_eps=1e-3, chunk=0):
     """Descriptor; segment = causal rows per segment (0 = library default),
-    chunk = causal chunk length T (0 = library default, 64)."""
+    chunk = causal chunk length T (0 = the library's choice: 32 for bf16 inputs
+    with M <= 128, else 64)."""
     return FavorDesc(B, H, L, d, M, in_dtype, out_dtype, float(input_scale), float(denom_eps),
                      chunk, int(kernel), 0 if renormalize else 1, float(kernel_eps), segment)
 

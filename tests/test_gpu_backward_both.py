@@ -78,11 +78,13 @@ def test_both_backward_parity(B, H, L, M, dtype, kernel, renorm, eps, states):
     assert np.max(np.abs(got - rS)) <= TOL[dtype] * np.max(np.abs(rS))
 
 
-@pytest.mark.parametrize("dtype,M", [("bf16", 256), ("bf16", 128), ("bf16", 64), ("f32", 64)])
-def test_both_backward_reads_saved_forward_quantities(dtype, M):
+@pytest.mark.parametrize("dtype,M,chunk", [("bf16", 256, 0), ("bf16", 256, 32), ("bf16", 128, 0),
+                                           ("bf16", 64, 0), ("f32", 64, 0)])
+def test_both_backward_reads_saved_forward_quantities(dtype, M, chunk):
     """Given the workspace of the attn_both call (W'', b'', Buf1 and the segment
-    prefixes; 32-token chunks at M <= 128 in bf16, the segment plan of two
-    workgroups per CU), the gradients are bitwise those of recomputing them; given also
+    prefixes; 32-token chunks at M <= 128 in bf16, and when asked for at
+    M = 256, the segment plan of two workgroups per CU), the gradients are
+    bitwise those of recomputing them; given also
     its outputs and row scales, within the gate of recomputing them. The causal
     state gradient is bitwise that of attn_causal_backward."""
     import torch
@@ -94,13 +96,13 @@ def test_both_backward_reads_saved_forward_quantities(dtype, M):
     Wd, bd = to_dev(W), to_dev(b)
     dS = torch.randn((B, H, M, 65), device="cuda") * 0.01
     g = fv.make_desc(B, H, L, 64, M, fv.BF16 if dtype == "bf16" else fv.F32,
-                     fv.BF16 if dtype == "bf16" else fv.F32, S64)
+                     fv.BF16 if dtype == "bf16" else fv.F32, S64, chunk=chunk)
     ws = torch.empty(fv.workspace_size(g, 2), dtype=torch.uint8, device="cuda")
     rb = torch.empty((B, H, L), dtype=torch.float32, device="cuda")
     rc = torch.empty_like(rb)
     ob, oc = fv.attn_both(q, k, v, Wd, bd, S64, workspace=ws, row_scale_bidir=rb,
-                          row_scale_causal=rc)
-    kw = dict(dstate_out=dS, return_state_grad=True)
+                          row_scale_causal=rc, chunk=chunk)
+    kw = dict(dstate_out=dS, return_state_grad=True, chunk=chunk)
     fresh = fv.attn_both_backward(q, k, v, Wd, bd, S64, db, dc, **kw)
     reuse = fv.attn_both_backward(q, k, v, Wd, bd, S64, db, dc, forward_workspace=ws,
                                   forward_call="both", **kw)
