@@ -271,12 +271,15 @@ __device__ __forceinline__ void query_grad(
   using P = Mma<T>;
   using frag = typename P::frag;
   constexpr float sgn = KN == kCos ? -1.f : 1.f;
+  // two feature steps per unrolled iteration; at M = 64 (two steps in all) a
+  // full unroll would spill, so the loop stays rolled
+  constexpr int kFeatureUnroll = M > 64 ? 2 : 1;
   const int l = lane_id();
   const int g = l >> 4;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) dacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
   dot2 = 0.f;
-#pragma unroll 2
+#pragma unroll kFeatureUnroll
   for (int sidx = s0; sidx < s1; ++sidx) {
     f32x4 G[2];
 #pragma unroll
@@ -709,6 +712,9 @@ __device__ __forceinline__ void key_grad(
   using P = Mma<T>;
   using frag = typename P::frag;
   constexpr float sgn = KN == kCos ? -1.f : 1.f;
+  // two feature steps per unrolled iteration; at M = 64 (two steps in all) a
+  // full unroll would spill, so the loop stays rolled
+  constexpr int kFeatureUnroll = M > 64 ? 2 : 1;
   const int l = lane_id();
   const int g = l >> 4;
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
@@ -720,7 +726,7 @@ __device__ __forceinline__ void key_grad(
     p4[k] = zero4;
   }
   doth = 0.f;
-#pragma unroll 2
+#pragma unroll kFeatureUnroll
   for (int sidx = s0; sidx < s1; ++sidx) {
     f32x4 kh[2], G[2];
 #pragma unroll

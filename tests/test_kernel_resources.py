@@ -3,7 +3,8 @@ the kernel descriptors hipcc writes for gfx950 (the library's own compile
 flags): every 32-token instantiation of k_causal_fs fits two workgroups per CU
 (at most 256 vector registers per wave, VGPRs and AGPRs together, and at most
 half of the CU's 160 KB of LDS), the plan's segment choice for T = 32 assumes
-it; the 64-token ones fit one. No GPU is needed.
+it; the 64-token ones fit one. The gradient kernels use no scratch. No GPU is
+needed.
 """
 import os
 import re
@@ -17,15 +18,14 @@ LDS_PER_CU = 160 * 1024
 REGS_PER_LANE = 512   # vector registers per SIMD lane (VGPRs and AGPRs)
 
 
-@pytest.fixture(scope="module")
-def descriptors(tmp_path_factory):
+def _kernel_descriptors(tmp_path_factory, source):
     hipcc = B.hipcc()
     if not hipcc or not os.path.exists(hipcc):
         pytest.skip("hipcc not available")
-    out = tmp_path_factory.mktemp("asm") / "causal.s"
+    out = tmp_path_factory.mktemp("asm") / (source + ".s")
     cmd = [hipcc, f"--offload-arch={B.ARCH}", *B.COMMON_FLAGS, *B.DEVICE_FLAGS,
-           *B.PER_SOURCE_FLAGS.get("causal.hip", []), "--cuda-device-only", "-S", "-x", "hip",
-           os.path.join(B.CSRC, "causal.hip"), "-o", str(out)]
+           *B.PER_SOURCE_FLAGS.get(source, []), "--cuda-device-only", "-S", "-x", "hip",
+           os.path.join(B.CSRC, source), "-o", str(out)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     text = out.read_text()
@@ -34,6 +34,11 @@ def descriptors(tmp_path_factory):
         fields = dict(re.findall(r"\.amdhsa_(\w+) (\d+)", m.group(2)))
         kernels[m.group(1)] = {k: int(v) for k, v in fields.items()}
     return kernels
+
+
+@pytest.fixture(scope="module")
+def descriptors(tmp_path_factory):
+    return _kernel_descriptors(tmp_path_factory, "causal.hip")
 
 
 def _scan_kernels(kernels, chunk):
@@ -60,3 +65,14 @@ def test_64_token_scan_fits_one_workgroup_per_cu(descriptors):
     for name, f in _scan_kernels(descriptors, 64).items():
         assert f["next_free_vgpr"] <= REGS_PER_LANE, name
         assert LDS_PER_CU // 2 < f["group_segment_fixed_size"] <= LDS_PER_CU, name
+
+
+def test_gradient_kernels_keep_off_scratch(tmp_path_factory):
+    """Every instantiation of the gradient kernels (both feature kinds, bf16 and
+    fp32, every M) holds its registers without scratch: at M = 64 the feature
+    loop stays rolled, which a full unroll would spill."""
+    kernels = _kernel_descriptors(tmp_path_factory, "backward.hip")
+    assert kernels
+    spilled = {n: f["private_segment_fixed_size"] for n, f in kernels.items()
+               if f["private_segment_fixed_size"] > 0}
+    assert not spilled, spilled
