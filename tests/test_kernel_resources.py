@@ -54,11 +54,14 @@ def test_32_token_scan_fits_two_workgroups_per_cu(descriptors):
         assert f["group_segment_fixed_size"] <= LDS_PER_CU // 2, (name, f["group_segment_fixed_size"])
 
 
-def test_32_token_scan_at_256_features_keeps_the_loop_off_scratch(descriptors):
-    """The cosine instantiations at M = 256, the reordered chunk, need no scratch."""
-    for name, f in _scan_kernels(descriptors, 32).items():
-        if "Li256ELi0E" in name:
-            assert f["private_segment_fixed_size"] == 0, name
+def test_cosine_scan_keeps_off_scratch(descriptors):
+    """Every cosine-feature instantiation of the scan (each M and output type,
+    both chunk lengths, M = 256 at 32 tokens being the reordered chunk) needs no
+    scratch. (ReLU features at 32 tokens spill 8-16 bytes per lane at M = 128.)"""
+    for chunk in (32, 64):
+        for name, f in _scan_kernels(descriptors, chunk).items():
+            if re.search(r"Li(64|128|256)ELi0E", name):
+                assert f["private_segment_fixed_size"] == 0, name
 
 
 def test_64_token_scan_fits_one_workgroup_per_cu(descriptors):
