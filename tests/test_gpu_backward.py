@@ -11,6 +11,13 @@ of the terms that cancel rather than to its own rounding noise. That covers the
 single-key rows, whose exact dQ (and, for L = 1, dK) is 0 because the
 renormalised output is v_1 whatever the query and key are: every row with
 L = 1 and the first row of a causal pass without a carried state.
+
+ReLU features decide [W'' x > 0] per feature, an integer decision the kernel
+takes on an fp32 sum. Where |W'' x| lies within that sum's rounding bound
+either decision is right, and the step derivative makes the row's input
+gradient differ by a finite amount; such rows of dQ (queries) and dK (keys)
+are left out of the gate, must be finite, and may be at most 5% of the rows
+(or 4 rows).
 """
 import numpy as np
 import pytest
@@ -57,15 +64,40 @@ def _oracle_w(W, M, dtype, kernel):
     return Wpp / np.float64(ws)
 
 
+def _relu_ties(X, W):
+    """Rows of X [B, H, L, d] holding a ReLU decision [W x > 0] (W [H, M, d], any
+    positive scale) that an fp32 projection cannot take reliably: |W x| within
+    the first-order rounding bound of a d-term fp32 sum of rounded products on
+    rounded weights, (d + 2) 2^-24 sum_i |W_mi x_i|. The
+    step derivative is discontinuous there, so the kernel (fp32 sums) and the
+    oracle (fp64) may both be right with different input gradients for the row."""
+    X = np.asarray(X, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    proj = np.einsum("hmd,bhld->bhlm", W, X)
+    bound = (X.shape[-1] + 2) * 2.0 ** -24 * np.einsum("hmd,bhld->bhlm", np.abs(W), np.abs(X))
+    return np.any(np.abs(proj) <= bound, axis=-1)
+
+
 def _check_all(got, ref, dtype, scale):
     """got, ref, scale: dicts name -> [B, H, L, d] arrays (scale from
-    oracle.metrics.grad_error_scale). Per-row gate (module docstring)."""
+    oracle.metrics.grad_error_scale). Per-row gate (module docstring). Rows the
+    oracle marks undetermined (NaN: a ReLU decision at the fp32 rounding level,
+    see _relu_ties) must be finite and at most 5% of the rows, or 4 rows (the
+    bound is a worst case: it flags about 0.7% of the rows at M = 256); the gate
+    takes the others."""
     tol = TOL[dtype]
     errs = {}
     for name in ref:
         g = np.asarray(got[name], dtype=np.float64)
         assert np.all(np.isfinite(g)), name
-        errs[name] = metrics.err_grad_rows(g, ref[name], scale[name])
+        r = ref[name]
+        open_rows = np.isnan(r).any(axis=-1, keepdims=True)
+        if open_rows.any():
+            print(f"{name}: {int(open_rows.sum())} rows with a ReLU decision at the rounding "
+                  "level left out", flush=True)
+            assert open_rows.sum() <= max(4, 0.05 * open_rows.size), name
+            r = np.where(open_rows, g, r)
+        errs[name] = metrics.err_grad_rows(g, r, scale[name])
     print(f"\nper-row gradient errors (units of the error scale) {errs}", flush=True)
     bad = {k: v for k, v in errs.items() if v > tol}
     assert not bad, f"{bad} > {tol}"
@@ -82,7 +114,13 @@ def _oracle_grads(Q, K, V, W, b, dout, causal, **kw):
         ref = bw.attn_bidir_backward(Q, K, V, W, b, S64, dout, **kw)
         rS = None
     scale = metrics.grad_error_scale(Q, K, V, W, b, S64, dout, causal, **kw)
-    return dict(zip(names, ref[:3])), dict(zip(names, scale)), rS
+    ref = dict(zip(names, (np.array(r, dtype=np.float64) for r in ref[:3])))
+    if kw.get("kernel", SOFTMAX) == RELU:
+        # the input gradients of rows with a decision at the rounding level are
+        # not determined (see _relu_ties); dV involves no derivative
+        ref["dQ"][_relu_ties(Q, W)] = np.nan
+        ref["dK"][_relu_ties(K, W)] = np.nan
+    return ref, dict(zip(names, scale)), rS
 
 
 def _host_grads(got):

@@ -5,8 +5,9 @@ any M that is a multiple of 16, in/out dtypes, feature kind, renormalisation,
 stabiliser, causal segment length, the scan's chunk length (bf16 cases cycle
 through 32, 64 and the default) and a carried state (cos features from M 64,
 ReLU features from M 16; a second list takes cos features at M 16 to 48 and
-gates them by E_cond alone). The configurations are drawn once from a fixed seed,
-so a failure names a reproducible case.
+gates them by E_cond alone, as are the unnormalised cos outputs, whose rows
+cancel). The configurations are drawn once from a fixed seed, so a failure
+names a reproducible case.
 
 Tolerances as everywhere: 1e-4 for fp32 inputs, 2e-2 for bf16 inputs.
 """
@@ -119,7 +120,11 @@ def test_random_configuration(cfg):
     ref_f = favor.features(Q.astype(np.float64), W, b, S64, cfg["kernel"], 1e-3)
     _check(to_host(Xp), ref_f, tol if cfg["out_dtype"] == dtype else TOL["bf16"])
     ptol = tol if cfg["out_dtype"] == dtype else TOL["bf16"]
-    gate = cfg.get("gate", "both")
+    # the unnormalised numerator with cos features has weights of both signs:
+    # its rows cancel and E_row (no conditioning term) bounds nothing there, so
+    # E_cond, scaled by the absolute-value sums, is the gate
+    unnormalised_cos = cfg["kernel"] == favor.KERNEL_SOFTMAX and not cfg["renorm"]
+    gate = cfg.get("gate", "cond" if unnormalised_cos else "both")
     for out in (ob, ob2):
         e = parity(to_host(out), Q, K, V, W, b, S64, False, dtype, eps=cfg["eps"], tol=ptol,
                    kernel=cfg["kernel"], renormalize=cfg["renorm"], gate=gate)
