@@ -56,6 +56,11 @@ constexpr int kTargetWorkgroups = 512;  // two waves of workgroups over 256 CUs
 // per CU; with 32-token chunks two workgroups share a CU
 constexpr int kCausalWorkgroups = 256;
 constexpr int kMinRowsPerSplit = 256;
+// Causal segments may be shorter: on short sequences more segments keep more
+// CUs busy, and a segment of two 64-token chunks still amortises the scan's
+// prologue (measured: the causal call 10-23% and its gradients 25-32% faster at
+// L <= 1024 for 32 heads; longer sequences keep the workgroup target's segments)
+constexpr int kMinRowsPerSegment = 128;
 // Longest sequence per head (and longest causal segment): the kernels index
 // tokens with 32-bit integers and step past the end by up to two tiles.
 constexpr int kMaxL = 1 << 30;
@@ -201,7 +206,7 @@ Plan make_plan(const favor_desc *g, int op) {
                        : chunk_len(g) == kChunkSmall ? 2 * kCausalWorkgroups
                                                      : kCausalWorkgroups;
     int want = (target + p.BH - 1) / p.BH;
-    int max_split = tiles / (kMinRowsPerSplit / 64);
+    int max_split = tiles / ((causal ? kMinRowsPerSegment : kMinRowsPerSplit) / 64);
     if (max_split < 1) max_split = 1;
     if (want > max_split) want = max_split;
     if (want < 1) want = 1;
