@@ -5,7 +5,7 @@ any M that is a multiple of 16, in/out dtypes, feature kind, renormalisation,
 stabiliser, causal segment length, the scan's chunk length (bf16 cases cycle
 through 32, 64 and the default) and a carried state (cos features from M 64,
 ReLU features from M 16; a second list takes cos features at M 16 to 48 and
-gates them by E_cond alone, as are the unnormalised cos outputs, whose rows
+gates them by E_cond alone, as are the unnormalised outputs, whose rows
 cancel). The configurations are drawn once from a fixed seed, so a failure
 names a reproducible case.
 
@@ -120,11 +120,12 @@ def test_random_configuration(cfg):
     ref_f = favor.features(Q.astype(np.float64), W, b, S64, cfg["kernel"], 1e-3)
     _check(to_host(Xp), ref_f, tol if cfg["out_dtype"] == dtype else TOL["bf16"])
     ptol = tol if cfg["out_dtype"] == dtype else TOL["bf16"]
-    # the unnormalised numerator with cos features has weights of both signs:
-    # its rows cancel and E_row (no conditioning term) bounds nothing there, so
-    # E_cond, scaled by the absolute-value sums, is the gate
-    unnormalised_cos = cfg["kernel"] == favor.KERNEL_SOFTMAX and not cfg["renorm"]
-    gate = cfg.get("gate", "cond" if unnormalised_cos else "both")
+    # an unnormalised output is the numerator Q'(S + K'^T V) itself: its rows
+    # cancel (cos weights of both signs; any weights against values of both
+    # signs, with no denominator whose rounding follows the numerator's), and
+    # E_row, with no conditioning term, bounds nothing there; E_cond, scaled by
+    # the absolute-value sums, is the gate
+    gate = cfg.get("gate", "both" if cfg["renorm"] else "cond")
     for out in (ob, ob2):
         e = parity(to_host(out), Q, K, V, W, b, S64, False, dtype, eps=cfg["eps"], tol=ptol,
                    kernel=cfg["kernel"], renormalize=cfg["renorm"], gate=gate)
