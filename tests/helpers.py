@@ -36,8 +36,10 @@ def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=Non
     kernel, kernel_eps, renormalize: the feature kernel and normalisation of the
     call. gate: "both" asserts E_row and E_cond, "cond" only E_cond (regimes
     where D-hat cancels, such as input_scale 1, or cos features at small M:
-    E_row has no conditioning term there). stats: optional dict that receives
-    the per-row condition numbers kappa. Returns (E_row, E_cond)."""
+    E_row has no conditioning term there). Renormalised rows whose denominator
+    has no correct bit at the input precision (kappa u >= 1) may be non-finite;
+    they are left out. stats: optional dict that receives the per-row condition
+    numbers kappa. Returns (E_row, E_cond)."""
     tol = TOL[dtype] if tol is None else tol
     Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
     out = np.asarray(out, dtype=np.float64)
@@ -55,8 +57,17 @@ def parity(out, Q, K, V, W, b, s, causal, dtype, eps=0.0, state_in=None, tol=Non
         ref, _ = favor.attn_causal_features(Qp, Kp, V, eps, state_in, renormalize)
     else:
         ref = favor.attn_bidir_features(Qp, Kp, V, eps, renormalize)
-    e_row = metrics.err_row(out, ref)
     S, den = metrics.error_scale(Qp, Kp, V, causal, state_in=state_in)
+    if renormalize:
+        # a row whose denominator cancels below the rounding level of its terms
+        # (kappa u >= 1, u the unit roundoff of the input dtype) has no correct
+        # bit in D-hat: the kernel divides by whatever its sum gave, 0 included,
+        # so a non-finite result there is no fault; such rows are left out
+        u = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -24
+        open_rows = (metrics.kappa(S, den + eps) * u >= 1.0) & ~np.all(np.isfinite(out), axis=-1)
+        if open_rows.any():
+            out = np.where(open_rows[..., None], ref, out)
+    e_row = metrics.err_row(out, ref)
     if not renormalize:
         e_cond = metrics.err_cond_numerator(out, ref, S)
     else:
